@@ -1,0 +1,203 @@
+#!/usr/bin/env python3
+"""Benchmark of the TCL Mamba cost model on one MI355X.
+
+Default workload: one tuning round of B = 4096 candidate programs, L = 25,
+F = 164, d_model = 256, 4 blocks, fp32 -- scored by tcl_score with the
+features already resident in HBM. A step is one tcl_score call (every
+kernel of the scoring pass over the whole batch). Prints one JSON line:
+programs scored per second, the roofline position of the dominant kernel
+(algorithmic flops or bytes per launch over its event-timed duration on
+the launch stream) and the fp64 oracle timed on this host's cores.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--kernels]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
+BF16_MFMA_PEAK_TFS = 2516.6    # MI355X dense bf16 matrix, TFLOP/s
+METRIC = "candidate programs scored/sec (B=4096,L=25) + % of HBM / MFMA peak"
+
+
+def kernel_work(shape, M_v: int, B: int, dtype: str) -> dict:
+    """Algorithmic work per launch of each kernel of the scoring pass.
+
+    Counts use the valid tokens M_v only (padding is never computed) and each
+    kernel's minimal inputs and outputs read or written once.
+    Returns {name: (kind, amount)} with kind "flop" (MFMA-bound) or "byte".
+    """
+    d, E, N, R, F = shape.d_model, shape.d_inner, shape.d_state, shape.dt_rank, shape.F
+    XW = R + 2 * N
+    a = 4 if dtype == "f32" else 2  # bytes per activation element
+    return {
+        "gemm_input": ("flop", 2 * M_v * F * d),
+        "gemm_in_proj": ("flop", 2 * M_v * d * 2 * E),
+        "gemm_x_proj": ("byte", M_v * (E * a + XW * 4)),
+        "gemm_out_proj": ("flop", 2 * M_v * E * d),
+        "conv_silu": ("byte", M_v * 2 * E * a),
+        "scan": ("byte", M_v * (3 * E * a + XW * 4)),
+        "tail": ("byte", M_v * d * 4 + B * 8),
+        "offsets": ("byte", B * 8),
+    }
+
+
+def roofline_entry(kind, amount, ms_per_launch, dtype):
+    if kind == "flop":
+        achieved = amount / (ms_per_launch * 1e-3) / 1e12
+        peak = FP32_MFMA_PEAK_TFS if dtype == "f32" else BF16_MFMA_PEAK_TFS
+        return {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak}
+    achieved = amount / (ms_per_launch * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS}
+
+
+def cpu_baseline(w, blob, X, lengths, target_s: float) -> dict:
+    """The fp64 oracle, as it stands, on a bounded sample of the same batch."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import model as om
+
+    cfg = dict(F=w.model.F, d_model=w.model.d_model, d_inner=w.model.d_inner, d_state=w.model.d_state,
+               d_conv=w.model.d_conv, dt_rank=w.model.dt_rank, n_layers=w.model.n_layers,
+               head_hidden=w.model.head_hidden, final_norm=w.model.final_norm, norm_eps=w.model.norm_eps)
+    n0 = 8
+    t = time.perf_counter()
+    om.score(blob, X[:n0], lengths[:n0], cfg)
+    dt0 = time.perf_counter() - t
+    n = int(min(len(lengths), max(n0, target_s / max(dt0, 1e-6) * n0)))
+    idx = np.linspace(0, len(lengths) - 1, n).astype(np.int64)
+    t = time.perf_counter()
+    om.score(blob, X[idx], lengths[idx], cfg)
+    dt = time.perf_counter() - t
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    return {"value": n / dt, "unit": "programs/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} of {len(lengths)} programs (evenly strided) of the same batch, numpy fp64, "
+                      f"{dt:.1f} s; host has {os.cpu_count()} CPUs, affinity {len(os.sched_getaffinity(0))}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="score_B4096_L25_d256_f32")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernels", action="store_true", help="print the per-kernel table to stderr")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the scoring and distillation paths are single-GPU "
+              "(batches shard across GPUs by program with no exchange but the scores); run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2604_12891_amd import binding as tb
+    from paper_2604_12891_amd import workload as wl
+
+    w = wl.WORKLOADS[args.workload]
+    if w.student is not None:
+        print("distillation benchmark is not built yet", file=sys.stderr)
+        sys.exit(2)
+    blob, X, lengths = wl.make_workload(w.name)
+    dev = torch.device("cuda:0")
+    Xd = torch.from_numpy(X).to(dev)
+    Ld = torch.from_numpy(lengths).to(dev)
+    model = tb.CostModel(tb.config_from_shape(w.model, w.dtype), blob)
+    ws = model.workspace(w.B, w.L)
+    out = torch.empty(w.B, dtype=torch.float32, device=dev)
+    M_v = int(lengths.sum())
+
+    for _ in range(args.warmup):
+        model.score(Xd, Ld, out=out, workspace=ws)
+    torch.cuda.synchronize()
+
+    # timed region: K steps, synchronised on both sides
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        model.score(Xd, Ld, out=out, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    assert torch.isfinite(out).all().item(), "non-finite scores"
+
+    # the same K steps again with every kernel bracketed by events on its stream
+    model.timing(True)
+    model.timing_reset()
+    for _ in range(args.steps):
+        model.score(Xd, Ld, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    rep = model.timing_report()
+    model.timing(False)
+
+    work = kernel_work(w.model, M_v, w.B, w.dtype)
+    kernels = {}
+    for name, (tot, n) in rep.items():
+        per = tot / n
+        kind, amount = work[name]
+        # launches of one kernel per step (e.g. one per block) all do the same work
+        e = roofline_entry(kind, amount, per, w.dtype)
+        e.update({"ms_per_launch": per, "launches_per_step": n // args.steps,
+                  "ms_per_step": tot / args.steps, "work_per_launch": amount, "work_unit": kind})
+        kernels[name] = e
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    roof = {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 3), "peak": d["peak"],
+            "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None,
+            "ms_per_launch": round(d["ms_per_launch"], 5)}
+    if args.kernels:
+        print(f"{'kernel':16s} {'ms/step':>9s} {'ms/launch':>10s} {'achieved':>10s} {'unit':8s} {'frac':>6s}",
+              file=sys.stderr)
+        for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+            print(f"{k:16s} {e['ms_per_step']:9.4f} {e['ms_per_launch']:10.5f} {e['achieved']:10.2f} "
+                  f"{e['unit']:8s} {e['frac']:6.3f}", file=sys.stderr)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, blob, X, lengths, args.cpu_seconds)
+
+    rec = {
+        "metric": METRIC,
+        "value": w.B / (ms * 1e-3),
+        "unit": "programs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "F": w.model.F, "d_model": w.model.d_model,
+                   "d_inner": w.model.d_inner, "d_state": w.model.d_state, "n_layers": w.model.n_layers,
+                   "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v},
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
+                    for k, e in kernels.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,187 @@
+/*
+ * tcl.h - C ABI of libtcl, an MI355X (gfx950) implementation of the
+ * Mamba-based cost model of TCL (arXiv 2604.12891), section 5.2.
+ *
+ * The library scores batches of candidate tensor programs (each a
+ * zero-padded sequence of per-statement feature vectors, section 5.1) and
+ * runs the teacher -> student distillation step that the knowledge
+ * distillation phase of section 6 is built from.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers named d_* are device pointers on the model's device; h_*
+ *    are host pointers. The caller owns every buffer it passes; the
+ *    library owns only its handles and the weights it uploads at create.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Every device-side effect is enqueued on it, asynchronously; outputs
+ *    are valid once the stream has been synchronised. A handle must not be
+ *    used on two streams at the same time.
+ *  - Functions return a tcl_status; no C++ exception crosses the ABI.
+ *    On failure tcl_last_error() describes the cause (thread-local,
+ *    overwritten by the next failing call on the same thread).
+ *  - Launch errors are reported at the call (TCL_ERR_HIP); errors inside a
+ *    kernel surface at the caller's synchronisation.
+ *  - Feature tensors are fp32, row-major [B, L, F]; rows t >= length[b]
+ *    are ignored (the model is causal and the pool is masked, so they
+ *    cannot change a score) and never read.
+ *  - A program whose length is outside [1, L] is not scored: its score is
+ *    set to NaN and it contributes no tokens; the call itself succeeds.
+ *
+ * Parameter blob
+ * --------------
+ * Models are described by one flat fp32 array in this canonical order
+ * (every matrix row-major in [out, in] layout):
+ *   W0[d,F], b0[d],
+ *   per block l = 0..n_layers-1:
+ *     g[d], W_in[2E,d], conv_w[E,K], conv_b[E], W_x[R+2N,E],
+ *     W_dt[E,R], b_dt[E], A_log[E,N], D[E], W_out[d,E],
+ *   g_f[d], W1[h,d], b1[h], W2[1,h], b2[1]
+ * with d = d_model, E = d_inner, N = d_state, K = d_conv, R = dt_rank,
+ * h = head_hidden. The model it defines:
+ *   h0   = X W0^T + b0                                   (encoder)
+ *   per block: n = RMSNorm(h; g), [x|z] = n W_in^T,
+ *     u = SiLU(conv_b + causal depthwise conv_K(x; conv_w)),
+ *     [dt_r|B|C] = u W_x^T, dt = softplus(dt_r W_dt^T + b_dt),
+ *     A = -exp(A_log), selective scan (Eq. (4)-(5) discretised):
+ *       s_t = exp(dt_t A) s_{t-1} + dt_t u_t B_t,  y_t = C_t.s_t + D u_t,
+ *     h = h + (y * SiLU(z)) W_out^T
+ *   score = W2 ReLU(W1 pool(RMSNorm(h; g_f)) + b1) + b2
+ * where pool is the mean over each program's valid tokens. RMSNorm uses
+ * norm_eps; the conv has K-1 zeros on the left of each program and its last
+ * tap multiplies the current token.
+ */
+#ifndef TCL_H
+#define TCL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+#define TCL_EXTERN extern "C"
+#else
+#define TCL_EXTERN extern
+#endif
+#define TCL_API TCL_EXTERN __attribute__((visibility("default")))
+
+typedef enum tcl_status {
+  TCL_OK = 0,
+  TCL_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, mismatch */
+  TCL_ERR_UNSUPPORTED = -2, /* shape outside what the kernels implement  */
+  TCL_ERR_WORKSPACE = -3,   /* workspace smaller than *_workspace_bytes   */
+  TCL_ERR_OOM = -4,         /* device allocation failed                   */
+  TCL_ERR_HIP = -5          /* a HIP runtime call or launch failed        */
+} tcl_status;
+
+typedef enum tcl_dtype {
+  TCL_F32 = 0,  /* fp32 weights, activations and arithmetic                 */
+  TCL_BF16 = 1  /* bf16 weights and activations; fp32 accumulation and fp32
+                   scan state. Weights are rounded to bf16 (nearest-even) at
+                   create; pass bf16-representable values to avoid that.    */
+} tcl_dtype;
+
+/* Model hyper-parameters (section 5.2; the hyper-parameter study of
+ * section 7.2.1 names d_state, d_conv, expand and n_layers).
+ * Supported: F % 4 == 0, d_model in {64, 128, 256}, d_inner % 64 == 0 and
+ * <= 2048, d_state == 16, d_conv in [1, 4], dt_rank % 4 == 0 and <= 32,
+ * head_hidden % 64 == 0 and <= 256, n_layers in [1, 16]. */
+typedef struct tcl_config {
+  int32_t F;           /* features per token                        */
+  int32_t d_model;     /* residual width d                          */
+  int32_t d_inner;     /* expanded width E = expand * d_model       */
+  int32_t d_state;     /* SSM state size N per channel              */
+  int32_t d_conv;      /* depthwise conv width K                    */
+  int32_t dt_rank;     /* rank R of the dt projection               */
+  int32_t n_layers;    /* Mamba blocks                              */
+  int32_t head_hidden; /* hidden width h of the score head          */
+  int32_t final_norm;  /* 1: RMSNorm before the pool (section 5.2)  */
+  float norm_eps;      /* RMSNorm epsilon                           */
+  int32_t dtype;       /* tcl_dtype                                 */
+} tcl_config;
+
+typedef struct tcl_model tcl_model;     /* opaque, library-owned */
+typedef struct tcl_trainer tcl_trainer; /* opaque, library-owned */
+
+/* Number of fp32 values in the canonical parameter blob for `cfg`
+ * (0 if cfg is NULL). */
+TCL_API size_t tcl_param_count(const tcl_config* cfg);
+
+/* Create a cost model on the current HIP device from a host parameter blob
+ * of exactly tcl_param_count(cfg) values (copied; the caller keeps it).
+ * Allocates the device weights (once) and derives kernel layouts. Not
+ * stream-ordered: returns after the upload has completed. */
+TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_params,
+                                         size_t n_params, tcl_model** out);
+
+/* Free the model's device memory. Pending work that uses it must have
+ * finished. NULL is accepted. */
+TCL_API tcl_status tcl_cost_model_destroy(tcl_model* model);
+
+/* Bytes of device workspace tcl_score needs for a batch of B programs padded
+ * to L tokens (0 on invalid arguments). */
+TCL_API size_t tcl_score_workspace_bytes(const tcl_model* model, int32_t B, int32_t L);
+
+/* Score B candidate programs (section 3 / Fig. 2: the cost model ranks the
+ * candidates of a tuning round; higher score ranks first).
+ *   d_feats   [B, L, F] fp32 row-major (F = cfg.F); rows t >= len ignored
+ *   d_lengths [B] int32, valid programs have 1 <= len <= L
+ *   d_scores  [B] fp32 output
+ *   d_workspace, ws_bytes: >= tcl_score_workspace_bytes(model, B, L) bytes,
+ *   256-byte aligned; its contents on entry are ignored.
+ * Only the valid tokens are computed: tokens are packed program by program
+ * on the device and every kernel works on the packed rows. */
+TCL_API tcl_status tcl_score(tcl_model* model, int32_t B, int32_t L, const float* d_feats,
+                             const int32_t* d_lengths, float* d_scores, void* d_workspace,
+                             size_t ws_bytes, void* stream);
+
+/* Copy the fp32 master parameters (canonical blob) back to the host. */
+TCL_API tcl_status tcl_get_params(const tcl_model* model, float* h_out, size_t n_params);
+
+/* Replace the parameters from a host blob (synchronous, like create). */
+TCL_API tcl_status tcl_set_params(tcl_model* model, const float* h_params, size_t n_params);
+
+/* Per-kernel timing, for measurement. While enabled, every kernel launch of
+ * tcl_score is bracketed by a pair of hipEvents recorded on the caller's
+ * stream (the stream the kernel runs on), grouped by kernel name.
+ * tcl_timing_get waits for the recorded events and returns, for entry
+ * `idx` in [0, tcl_timing_count(model)), the kernel name (library-owned
+ * string), the summed duration in milliseconds and the number of launches.
+ * tcl_timing_reset clears the totals. */
+TCL_API tcl_status tcl_timing_enable(tcl_model* model, int32_t enable);
+TCL_API int32_t tcl_timing_count(const tcl_model* model);
+TCL_API tcl_status tcl_timing_get(tcl_model* model, int32_t idx, const char** name, double* total_ms,
+                                  int64_t* launches);
+TCL_API tcl_status tcl_timing_reset(tcl_model* model);
+
+/* Message describing the last failure on this thread ("" if none). */
+TCL_API const char* tcl_last_error(void);
+
+/* ---------------------------------------------------------------------
+ * Kernel-level entry points, used to test each kernel on its own. They
+ * run on packed tokens: program b owns rows offs[b] .. offs[b+1]-1 of
+ * every [rows, C] activation (row-major, leading dimension C unless given).
+ * ------------------------------------------------------------------- */
+
+/* C[M,N] = A[M,K] W[N,K]^T (+ bias[N] if d_bias) in fp32 via the fp32 MFMA
+ * GEMM used by the model's projections. K % 4 == 0. */
+TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const float* d_A,
+                                     const float* d_W, const float* d_bias, float* d_C,
+                                     void* stream);
+
+/* u = SiLU(conv_b + causal depthwise conv(x; conv_w)) per program, fp32.
+ * d_x rows have leading dimension ldx >= E; d_offs [B+1] int32 prefix sums
+ * of the lengths; d_w [E,K], d_b [E]; d_u [rows, E]. */
+TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const int32_t* d_offs,
+                                          const float* d_x, int32_t ldx, const float* d_w,
+                                          const float* d_b, float* d_u, void* stream);
+
+/* Selective scan with its dt_proj + softplus prologue and gate epilogue,
+ * fp32: out = (scan(u, softplus(dt_r W_dt^T + b_dt), -exp(A_log), B, C) +
+ * D u) * SiLU(z), with [dt_r|B|C] = d_xdbl rows of R + 2N values and z read
+ * from d_z with leading dimension ldz. N must be 16. */
+TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R,
+                                     const int32_t* d_offs, const float* d_u, const float* d_xdbl,
+                                     const float* d_z, int32_t ldz, const float* d_W_dt,
+                                     const float* d_b_dt, const float* d_A_log, const float* d_D,
+                                     float* d_out, void* stream);
+
+#endif /* TCL_H */

@@ -1,0 +1,204 @@
+"""Thin ctypes binding of libtcl (include/tcl.h): argument marshalling only.
+
+Every step of the cost model runs in libtcl's HIP kernels; this module only
+converts torch tensors to device pointers and the caller's current HIP
+stream, and raises on a non-OK status. Loading fails loudly if the library
+has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtcl.so")
+_lib = None
+
+TCL_F32, TCL_BF16 = 0, 1
+STATUS = {0: "TCL_OK", -1: "TCL_ERR_INVALID_ARG", -2: "TCL_ERR_UNSUPPORTED", -3: "TCL_ERR_WORKSPACE",
+          -4: "TCL_ERR_OOM", -5: "TCL_ERR_HIP"}
+
+
+class TclError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("F", "d_model", "d_inner", "d_state", "d_conv", "dt_rank", "n_layers", "head_hidden",
+                 "final_norm")] + [("norm_eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+_vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+_SIGS = {
+    "tcl_param_count": (_sz, [ctypes.POINTER(Config)]),
+    "tcl_cost_model_create": (_i32, [ctypes.POINTER(Config), _vp, _sz, ctypes.POINTER(_vp)]),
+    "tcl_cost_model_destroy": (_i32, [_vp]),
+    "tcl_score_workspace_bytes": (_sz, [_vp, _i32, _i32]),
+    "tcl_score": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "tcl_get_params": (_i32, [_vp, _vp, _sz]),
+    "tcl_set_params": (_i32, [_vp, _vp, _sz]),
+    "tcl_last_error": (ctypes.c_char_p, []),
+    "tcl_timing_enable": (_i32, [_vp, _i32]),
+    "tcl_timing_count": (_i32, [_vp]),
+    "tcl_timing_get": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
+                              ctypes.POINTER(ctypes.c_int64)]),
+    "tcl_timing_reset": (_i32, [_vp]),
+    "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
+    "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
+                                 _vp, _vp, _vp]),
+}
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """Load libtcl.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with `python -m paper_2604_12891_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def check(status: int):
+    if status != 0:
+        raise TclError(status, lib().tcl_last_error().decode())
+
+
+def make_config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden,
+                final_norm=1, norm_eps=1e-5, dtype="f32") -> Config:
+    return Config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden, final_norm,
+                  norm_eps, TCL_BF16 if dtype == "bf16" else TCL_F32)
+
+
+def config_from_shape(shape, dtype="f32") -> Config:
+    return make_config(shape.F, shape.d_model, shape.d_inner, shape.d_state, shape.d_conv, shape.dt_rank,
+                       shape.n_layers, shape.head_hidden, shape.final_norm, shape.norm_eps, dtype)
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+class CostModel:
+    """A device-resident cost model (tcl_cost_model_create / tcl_score)."""
+
+    def __init__(self, cfg: Config, params: np.ndarray):
+        L = lib()
+        self.cfg = cfg
+        self._n = L.tcl_param_count(ctypes.byref(cfg))
+        blob = np.ascontiguousarray(params, dtype=np.float32)
+        h = _vp()
+        check(L.tcl_cost_model_create(ctypes.byref(cfg), blob.ctypes.data, blob.size, ctypes.byref(h)))
+        self._h = h
+        self._ws = None
+
+    def close(self):
+        if getattr(self, "_h", None):
+            check(lib().tcl_cost_model_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self):
+        return self._h
+
+    def workspace_bytes(self, B: int, L: int) -> int:
+        return lib().tcl_score_workspace_bytes(self._h, B, L)
+
+    def workspace(self, B: int, L: int):
+        import torch
+        need = self.workspace_bytes(B, L)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        return self._ws
+
+    def score(self, feats, lengths, out=None, workspace=None, stream=None):
+        """feats [B,L,F] fp32 cuda, lengths [B] int32 cuda -> scores [B] fp32 cuda."""
+        import torch
+        B, L, _ = feats.shape
+        if out is None:
+            out = torch.empty(B, dtype=torch.float32, device=feats.device)
+        ws = self.workspace(B, L) if workspace is None else workspace
+        check(lib().tcl_score(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), out.data_ptr(),
+                              ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)))
+        return out
+
+    def timing(self, enable: bool):
+        check(lib().tcl_timing_enable(self._h, int(enable)))
+
+    def timing_reset(self):
+        check(lib().tcl_timing_reset(self._h))
+
+    def timing_report(self) -> dict:
+        """{kernel name: (total_ms, launches)} of the launches timed so far."""
+        L = lib()
+        out = {}
+        for i in range(L.tcl_timing_count(self._h)):
+            name, ms, n = ctypes.c_char_p(), ctypes.c_double(), ctypes.c_int64()
+            check(L.tcl_timing_get(self._h, i, ctypes.byref(name), ctypes.byref(ms), ctypes.byref(n)))
+            out[name.value.decode()] = (ms.value, n.value)
+        return out
+
+    def get_params(self) -> np.ndarray:
+        out = np.empty(self._n, dtype=np.float32)
+        check(lib().tcl_get_params(self._h, out.ctypes.data, out.size))
+        return out
+
+    def set_params(self, params: np.ndarray):
+        blob = np.ascontiguousarray(params, dtype=np.float32)
+        check(lib().tcl_set_params(self._h, blob.ctypes.data, blob.size))
+
+
+def gemm_f32(A, W, bias=None, out=None, stream=None):
+    import torch
+    M, K = A.shape
+    N = W.shape[0]
+    if out is None:
+        out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(),
+                                  _stream(stream)))
+    return out
+
+
+def conv_silu_f32(offs, x, w, b, E, out, ldx=None, stream=None):
+    B = offs.numel() - 1
+    check(lib().tcl_test_conv_silu_f32(B, E, w.shape[1], offs.data_ptr(), x.data_ptr(),
+                                       x.shape[1] if ldx is None else ldx, w.data_ptr(), b.data_ptr(),
+                                       out.data_ptr(), _stream(stream)))
+    return out
+
+
+def scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, out, ldz=None, stream=None):
+    B = offs.numel() - 1
+    E = u.shape[1]
+    N = A_log.shape[1]
+    R = W_dt.shape[1]
+    check(lib().tcl_test_scan_f32(B, E, N, R, offs.data_ptr(), u.data_ptr(), xdbl.data_ptr(), z.data_ptr(),
+                                  z.shape[1] if ldz is None else ldz, W_dt.data_ptr(), b_dt.data_ptr(),
+                                  A_log.data_ptr(), D.data_ptr(), out.data_ptr(), _stream(stream)))
+    return out

@@ -1,0 +1,238 @@
+// fp32 projections on the gfx950 matrix cores (v_mfma_f32_32x32x2_f32).
+//
+// C = A W^T with both operands K-contiguous (activations are row-major
+// [tokens, K]; weights keep the [out, in] layout). A workgroup computes a
+// BM x BN tile; each wavefront owns a (TM*32) x (TN*32) sub-tile made of
+// 32x32 MFMA blocks with their accumulators in registers. K is consumed in
+// chunks of 32 staged through LDS; the next chunk's global loads are issued
+// before the current chunk's MFMAs so that their latency overlaps compute.
+//
+// Operand k-order: v_mfma_f32_32x32x2_f32 multiplies A[32x2] by B[2x32];
+// lane l supplies row (l % 32) of A and column (l % 32) of B at the k
+// index (l / 32). The sum over k does not depend on which k each step
+// uses, so lane half g = l/32 walks k = 16g .. 16g+15 of the chunk while
+// lane half 0 walks k = 0..15: each lane then reads 16 contiguous floats
+// of its row with four 128-bit LDS loads instead of 16 scalar loads.
+//
+// Tile order is XCD-aware: workgroup i runs on XCD i % 8, and the mapping
+// below gives each XCD a stripe of M-tiles whose N-tiles it walks in
+// order, so the A rows of a tile are fetched into that XCD's L2 once.
+#include "common.h"
+#include "kernels.h"
+
+namespace tcl {
+namespace {
+
+constexpr int BK = 32;
+constexpr int PITCH = BK + 4;  // floats; 144-byte rows keep 8 lanes of b128 reads conflict-free
+constexpr int Q = BK / 4;      // float4 per row chunk
+
+template <int WM, int WN, int TM, int TN, int FL>
+__global__ __launch_bounds__(WM* WN * 64) void gemm_f32_kernel(GemmArgs p, int ntm, int ntn) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int BM = WM * TM * 32;
+  constexpr int BN = WN * TN * 32;
+  constexpr int NA = BM * Q / NT;
+  constexpr int NB = BN * Q / NT;
+  static_assert((BM * Q) % NT == 0 && (BN * Q) % NT == 0, "tile/thread mismatch");
+  static_assert(NT % Q == 0, "k offset must be thread-invariant");
+  constexpr bool kNorm = (FL & kRowNorm) != 0;
+
+  __shared__ __attribute__((aligned(16))) float sA[BM * PITCH];
+  __shared__ __attribute__((aligned(16))) float sB[BN * PITCH];
+  __shared__ float sR[kNorm ? BM : 1];
+
+  const int tid = threadIdx.x;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+
+  const int bid = blockIdx.x;
+  const int xcd = bid & 7, j = bid >> 3;
+  const int mt = xcd + 8 * (j / ntn), nt = j % ntn;
+  if (mt >= ntm) return;
+  const int row0 = mt * BM;
+  if (row0 >= M) return;
+  const int col0 = nt * BN;
+
+  const int q4 = (tid % Q) * 4;  // k offset of this thread's float4 within a chunk
+
+  const float* aptr[NA];
+  bool aval[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    const int r = (tid + i * NT) / Q;
+    const int grow = row0 + r;
+    aval[i] = grow < M;
+    int64_t src = grow;
+    if constexpr ((FL & kGather) != 0) {
+      if (aval[i]) {
+        int lo = 0, hi = p.B;  // largest b with offs[b] <= grow
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (p.offs[mid] <= grow) lo = mid; else hi = mid;
+        }
+        src = (int64_t)lo * p.L + (grow - p.offs[lo]);
+      }
+    }
+    aptr[i] = p.A + (aval[i] ? src : 0) * p.lda + q4;
+  }
+  const float* bptr[NB];
+  bool bval[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const int n = col0 + (tid + i * NT) / Q;
+    bval[i] = n < p.N;
+    bptr[i] = p.W + (bval[i] ? (int64_t)n : 0) * p.ldw + q4;
+  }
+
+  floatx4 ra[NA], rb[NB];
+  float ss[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) ss[i] = 0.f;
+
+  auto gload = [&](int k0) {
+    const bool kin = k0 + q4 < p.K;  // K % 4 == 0: a float4 is all in or all out
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      if (aval[i] && kin) {
+        ra[i] = *reinterpret_cast<const floatx4*>(aptr[i] + k0);
+      } else {
+        ra[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+      if constexpr (kNorm) {
+        ss[i] += ra[i].x * ra[i].x + ra[i].y * ra[i].y + ra[i].z * ra[i].z + ra[i].w * ra[i].w;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if (bval[i] && kin) {
+        rb[i] = *reinterpret_cast<const floatx4*>(bptr[i] + k0);
+      } else {
+        rb[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  };
+
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave / WN, wn = wave % WN;
+  const int li = lane & 31, lg = lane >> 5;
+
+  floatx16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  gload(0);
+  for (int k0 = 0; k0 < p.K; k0 += BK) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int r = (tid + i * NT) / Q;
+      *reinterpret_cast<floatx4*>(&sA[r * PITCH + q4]) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int r = (tid + i * NT) / Q;
+      *reinterpret_cast<floatx4*>(&sB[r * PITCH + q4]) = rb[i];
+    }
+    __syncthreads();
+    if (k0 + BK < p.K) gload(k0 + BK);
+
+    floatx4 a4[TM][4], b4[TN][4];
+#pragma unroll
+    for (int a = 0; a < TM; ++a) {
+      const float* src = &sA[(wm * TM * 32 + a * 32 + li) * PITCH + lg * 16];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) a4[a][c] = *reinterpret_cast<const floatx4*>(src + 4 * c);
+    }
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+      const float* src = &sB[(wn * TN * 32 + b * 32 + li) * PITCH + lg * 16];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) b4[b][c] = *reinterpret_cast<const floatx4*>(src + 4 * c);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int a = 0; a < TM; ++a)
+#pragma unroll
+          for (int b = 0; b < TN; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[a][c][e], b4[b][c][e], acc[a][b], 0, 0, 0);
+  }
+
+  if constexpr (kNorm) {
+    // the Q threads that loaded a row's k-slices are adjacent lanes
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      float v = ss[i];
+#pragma unroll
+      for (int o = 1; o < Q; o <<= 1) v += __shfl_xor(v, o, 64);
+      if ((tid % Q) == 0) {
+        const int r = (tid + i * NT) / Q;
+        sR[r] = 1.0f / sqrtf(v / (float)p.K + p.eps);
+      }
+    }
+    __syncthreads();
+  }
+
+  // Accumulator layout of a 32x32 block: lane l holds column l % 32 and rows
+  // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15.
+#pragma unroll
+  for (int a = 0; a < TM; ++a) {
+#pragma unroll
+    for (int b = 0; b < TN; ++b) {
+      const int col = col0 + wn * TN * 32 + b * 32 + li;
+      if (col >= p.N) continue;
+      const float bias = (FL & kBias) ? p.bias[col] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = wm * TM * 32 + a * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+        const int row = row0 + rl;
+        if (row >= M) continue;
+        float v = acc[a][b][r];
+        if constexpr (kNorm) v *= sR[rl];
+        v += bias;
+        float* dst = p.C + (int64_t)row * p.ldc + col;
+        if constexpr ((FL & kResid) != 0) v += *dst;
+        *dst = v;
+      }
+    }
+  }
+}
+
+template <int WM, int WN, int TM, int TN, int FL>
+hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
+  constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
+  const int ntm = (a.Mmax + BM - 1) / BM;
+  const int ntn = (a.N + BN - 1) / BN;
+  const int grid = 8 * ntn * ((ntm + 7) / 8);
+  if (grid <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_f32_kernel<WM, WN, TM, TN, FL>), dim3(grid), dim3(WM * WN * 64), 0, s,
+                     a, ntm, ntn);
+  return hipGetLastError();
+}
+
+template <int WM, int WN, int TM, int TN>
+hipError_t dispatch_flags(const GemmArgs& a, int flags, hipStream_t s) {
+  switch (flags) {
+    case 0: return launch_t<WM, WN, TM, TN, 0>(a, s);
+    case kBias: return launch_t<WM, WN, TM, TN, kBias>(a, s);
+    case kResid: return launch_t<WM, WN, TM, TN, kResid>(a, s);
+    case kRowNorm: return launch_t<WM, WN, TM, TN, kRowNorm>(a, s);
+    case kBias | kGather: return launch_t<WM, WN, TM, TN, kBias | kGather>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm_f32(const GemmArgs& a, int flags, GemmTile tile, hipStream_t s) {
+  if (tile == kWide) return dispatch_flags<2, 2, 2, 2>(a, flags, s);
+  return dispatch_flags<2, 2, 1, 1>(a, flags, s);
+}
+
+}  // namespace tcl

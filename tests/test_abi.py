@@ -1,0 +1,83 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/tcl.h declares, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import model as om
+from paper_2604_12891_amd import binding as tb
+from paper_2604_12891_amd import workload as wl
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "tcl.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return re.findall(r"TCL_API\s+[\w\s\*]+?\b(tcl_\w+)\s*\(", text)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(tb.lib_path()):
+        pytest.fail("libtcl.so is not built (run __graft_entry__.build())")
+    return tb.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_symbols()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    # and the binding declares a signature for each of them
+    assert set(names) <= set(tb._SIGS)
+
+
+@pytest.mark.parametrize("shape", [wl.TINY, wl.D256, wl.STUDENT])
+def test_param_count_matches_oracle_layout(lib, shape):
+    cfg = tb.config_from_shape(shape)
+    n = lib.tcl_param_count(ctypes.byref(cfg))
+    ocfg = dict(F=shape.F, d_model=shape.d_model, d_inner=shape.d_inner, d_state=shape.d_state,
+                d_conv=shape.d_conv, dt_rank=shape.dt_rank, n_layers=shape.n_layers,
+                head_hidden=shape.head_hidden)
+    assert n == sum(int(np.prod(s)) for _, s in om.layout(ocfg)) == wl.param_count(shape)
+
+
+def _create(lib, cfg, blob, n=None):
+    h = ctypes.c_void_p()
+    st = lib.tcl_cost_model_create(ctypes.byref(cfg) if cfg is not None else None,
+                                   blob.ctypes.data if blob is not None else None,
+                                   (0 if blob is None else blob.size) if n is None else n, ctypes.byref(h))
+    return st, h
+
+
+def test_create_rejects_bad_arguments(lib):
+    cfg = tb.config_from_shape(wl.TINY)
+    blob = np.zeros(wl.param_count(wl.TINY), np.float32)
+    st, h = _create(lib, None, blob)
+    assert st == -1 and h.value is None
+    st, _ = _create(lib, cfg, None)
+    assert st == -1
+    st, _ = _create(lib, cfg, blob, n=blob.size - 1)
+    assert st == -1 and b"needs" in lib.tcl_last_error()
+    for field, value in [("d_state", 8), ("d_model", 96), ("dt_rank", 6), ("head_hidden", 300), ("F", 163),
+                         ("d_conv", 5)]:
+        bad = tb.config_from_shape(wl.TINY)
+        setattr(bad, field, value)
+        st, _ = _create(lib, bad, np.zeros(lib.tcl_param_count(ctypes.byref(bad)), np.float32))
+        assert st == -2, field
+    bad = tb.config_from_shape(wl.TINY)
+    bad.norm_eps = 0.0
+    st, _ = _create(lib, bad, blob)
+    assert st == -1
+
+
+def test_calls_on_null_handles(lib):
+    assert lib.tcl_cost_model_destroy(None) == 0
+    assert lib.tcl_score(None, 1, 1, None, None, None, None, 0, None) == -1
+    assert lib.tcl_score_workspace_bytes(None, 4, 4) == 0
+    assert lib.tcl_get_params(None, None, 0) == -1
+    assert lib.tcl_test_gemm_f32(0, 4, 4, None, None, None, None, None) == -1
+    assert lib.tcl_test_scan_f32(1, 16, 8, 4, *([None] * 4), 16, *([None] * 6)) in (-1, -2)

@@ -1,0 +1,139 @@
+"""Kernel-level parity on the GPU: each kernel through its own C-ABI entry
+point against the oracle's matching piece on the same seeded inputs.
+
+Tolerances are derived from the fp32 arithmetic each kernel performs:
+  GEMM:  |c - c*| <= (K + 2) 2^-24 sum_k |a_k w_k|  (worst-case bound of an
+         fp32 dot product of length K; inputs are exact in fp64)
+  conv:  rtol 1e-5 on a scale of |b| + sum |w x| (4 FMAs, expf, one divide)
+  scan:  rtol 1e-4 on the output scale (16-term state sums over <= L steps,
+         exp2 of v_exp_f32, log1pf/expf in softplus)
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import model as om
+from paper_2604_12891_amd import binding as tb
+from paper_2604_12891_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+U = 2.0 ** -24
+
+
+def _dev(a, dtype=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda", dtype=dtype)
+
+
+def _offs(lengths):
+    return np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+
+
+def _pack(padded, lengths):
+    return np.concatenate([padded[b, :lengths[b]] for b in range(len(lengths))], axis=0)
+
+
+def _unpack(packed, lengths, L):
+    B = len(lengths)
+    out = np.zeros((B, L) + packed.shape[1:], dtype=packed.dtype)
+    o = _offs(lengths)
+    for b in range(B):
+        out[b, :lengths[b]] = packed[o[b]:o[b + 1]]
+    return out
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 4), (31, 48, 512), (129, 256, 164), (1000, 1024, 256),
+                                   (257, 256, 512), (77, 100, 36)])
+@pytest.mark.parametrize("bias", [False, True])
+def test_gemm_f32(M, N, K, bias):
+    print(f"gemm M={M} N={N} K={K} bias={bias}", flush=True)
+    rng = np.random.default_rng(M * 7 + N + K)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if bias else None
+    C = tb.gemm_f32(_dev(A), _dev(W), _dev(bv) if bias else None)
+    torch.cuda.synchronize()
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    bound = (K + 2) * U * (np.abs(A).astype(np.float64) @ np.abs(W).astype(np.float64).T)
+    if bias:
+        ref += bv
+        bound += U * np.abs(ref)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+@pytest.mark.parametrize("K", [1, 3, 4])
+def test_conv_silu_f32(K):
+    rng = np.random.default_rng(K)
+    lengths = np.array([1, 2, 3, 4, 25, 0, 17, 5, 9], dtype=np.int32)
+    B, L, E, ldx = len(lengths), 25, 192, 448
+    print(f"conv K={K} B={B} E={E}", flush=True)
+    x = rng.standard_normal((B, L, E))
+    w = rng.uniform(-0.5, 0.5, (E, K))
+    b = rng.uniform(-0.5, 0.5, E)
+    xp = np.zeros((int(lengths.sum()), ldx), np.float32)
+    xp[:, :E] = _pack(x, lengths)
+    out = torch.full((int(lengths.sum()), E), float("nan"), device="cuda")
+    tb.conv_silu_f32(_dev(_offs(lengths), torch.int32), _dev(xp), _dev(w.astype(np.float32)),
+                     _dev(b.astype(np.float32)), E, out, ldx=ldx)
+    torch.cuda.synchronize()
+    xr = _unpack(xp[:, :E].astype(np.float64), lengths, L)
+    wf, bf = w.astype(np.float32).astype(np.float64), b.astype(np.float32).astype(np.float64)
+    expect = _pack(om.silu(om.causal_conv1d(xr, wf, bf)), lengths)
+    scale = np.abs(bf) + _pack(om.causal_conv1d(np.abs(xr), np.abs(wf), 0 * bf), lengths)
+    np.testing.assert_array_less(np.abs(out.cpu().numpy() - expect), 1e-5 * scale + 1e-7)
+
+
+@pytest.mark.parametrize("R", [4, 16])
+@pytest.mark.parametrize("L", [1, 25, 70])
+def test_scan_f32(R, L):
+    N, E = 16, 320
+    rng = np.random.default_rng(R * 100 + L)
+    lengths = rng.integers(1, L + 1, size=11).astype(np.int32)
+    lengths[0] = L
+    lengths[1] = 1
+    B = len(lengths)
+    print(f"scan R={R} L={L} B={B} E={E}", flush=True)
+    rows = int(lengths.sum())
+    u = rng.standard_normal((rows, E)).astype(np.float32)
+    z = rng.standard_normal((rows, E)).astype(np.float32)
+    xdbl = (0.5 * rng.standard_normal((rows, R + 2 * N))).astype(np.float32)
+    W_dt = rng.uniform(-0.5, 0.5, (E, R)).astype(np.float32)
+    b_dt = np.log(np.expm1(np.exp(rng.uniform(np.log(1e-3), np.log(1e-1), E)))).astype(np.float32)
+    A_log = (np.log(np.arange(1, N + 1))[None, :] + 0.3 * rng.standard_normal((E, N))).astype(np.float32)
+    D = rng.standard_normal(E).astype(np.float32)
+    out = torch.full((rows, E), float("nan"), device="cuda")
+    tb.scan_f32(_dev(_offs(lengths), torch.int32), _dev(u), _dev(xdbl), _dev(z), _dev(W_dt), _dev(b_dt),
+                _dev(A_log), _dev(D), out)
+    torch.cuda.synchronize()
+    f = lambda a: a.astype(np.float64)
+    up, zp, xd = (_unpack(f(a), lengths, L) for a in (u, z, xdbl))
+    dt = om.softplus(xd[..., :R] @ f(W_dt).T + f(b_dt))
+    y = om.selective_scan(up, dt, -np.exp(f(A_log)), xd[..., R:R + N], xd[..., R + N:], f(D))
+    expect = _pack(y * om.silu(zp), lengths)
+    got = out.cpu().numpy()
+    scale = np.sqrt(np.mean(expect ** 2))
+    err = np.abs(got - expect)
+    assert np.all(err <= 1e-4 * (np.abs(expect) + scale)), float(np.max(err / (np.abs(expect) + scale)))
+
+
+def test_scan_in_place_matches_out_of_place():
+    """The model runs the scan with out aliasing u; results must not change."""
+    N, E, R = 16, 128, 4
+    rng = np.random.default_rng(3)
+    lengths = np.array([25, 3, 14], np.int32)
+    rows = int(lengths.sum())
+    args = [rng.standard_normal((rows, E)).astype(np.float32),
+            (0.5 * rng.standard_normal((rows, R + 2 * N))).astype(np.float32),
+            rng.standard_normal((rows, E)).astype(np.float32),
+            rng.uniform(-0.5, 0.5, (E, R)).astype(np.float32),
+            np.full(E, -3.0, np.float32),
+            np.tile(np.log(np.arange(1, N + 1)), (E, 1)).astype(np.float32),
+            np.ones(E, np.float32)]
+    d = [_dev(a) for a in args]
+    offs = _dev(_offs(lengths), torch.int32)
+    out = torch.empty_like(d[0])
+    tb.scan_f32(offs, *d, out)
+    u_copy = d[0].clone()
+    tb.scan_f32(offs, u_copy, *d[1:], u_copy)
+    torch.cuda.synchronize()
+    assert torch.equal(out, u_copy)
