@@ -167,8 +167,15 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
                                      const float* d_W, const float* d_bias, float* d_C,
                                      void* stream);
 
+/* Same with bf16 operands (row-major bf16 bit patterns, K % 8 == 0) on the
+ * bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16), fp32 accumulation and output. */
+TCL_API tcl_status tcl_test_gemm_bf16(int32_t M, int32_t N, int32_t K, const uint16_t* d_A,
+                                      const uint16_t* d_W, const float* d_bias, float* d_C,
+                                      void* stream);
+
 /* u = SiLU(conv_b + causal depthwise conv(x; conv_w)) per program, fp32.
- * d_x rows have leading dimension ldx >= E; d_offs [B+1] int32 prefix sums
+ * d_x rows have leading dimension ldx >= E (E and ldx multiples of 4, every
+ * pointer 16-byte aligned); d_offs [B+1] int32 prefix sums
  * of the lengths; d_w [E,K], d_b [E]; d_u [rows, E]. */
 TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const int32_t* d_offs,
                                           const float* d_x, int32_t ldx, const float* d_w,

@@ -49,6 +49,7 @@ _SIGS = {
                               ctypes.POINTER(ctypes.c_int64)]),
     "tcl_timing_reset": (_i32, [_vp]),
     "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                  _vp, _vp, _vp]),
@@ -182,6 +183,18 @@ def gemm_f32(A, W, bias=None, out=None, stream=None):
         out = torch.empty(M, N, dtype=torch.float32, device=A.device)
     check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(),
                                   _stream(stream)))
+    return out
+
+
+def gemm_bf16(A, W, bias=None, out=None, stream=None):
+    """A [M,K], W [N,K] torch.bfloat16 (cuda) -> fp32 [M,N]."""
+    import torch
+    M, K = A.shape
+    N = W.shape[0]
+    if out is None:
+        out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    check(lib().tcl_test_gemm_bf16(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(),
+                                   _stream(stream)))
     return out
 
 

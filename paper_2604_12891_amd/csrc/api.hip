@@ -114,7 +114,6 @@ tcl_status check_config(const tcl_config* c) {
     return fail(TCL_ERR_UNSUPPORTED, "head_hidden must be a multiple of 64, <= 256 (got %d)",
                 c->head_hidden);
   if (c->n_layers > 16) return fail(TCL_ERR_UNSUPPORTED, "n_layers must be <= 16");
-  if (c->dtype == TCL_BF16) return fail(TCL_ERR_UNSUPPORTED, "bf16 scoring is not built yet");
   return TCL_OK;
 }
 
@@ -129,9 +128,13 @@ struct tcl_model {
   size_t dev_bytes = 0;
   struct Layer {
     float *W_in, *conv_w, *conv_b, *W_x, *W_dt, *b_dt, *A_log, *D, *W_out;
+    float* g;                                    // RMSNorm gain (bf16 path applies it to A)
+    uint16_t *W_in_h, *W_x_h, *W_out_h;          // bf16 copies (bf16 models only)
   };
   float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1T = nullptr, *b1 = nullptr,
         *W2 = nullptr, *b2 = nullptr;
+  uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
+  int ldw0_h = 0;
   std::vector<Layer> layers;
 
   // Per-kernel event timing (tcl_timing_*).
@@ -187,62 +190,94 @@ struct tcl_model {
 
 namespace {
 
+uint16_t host_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+float round_bf16(float f) {
+  const uint32_t u = (uint32_t)host_bf16(f) << 16;
+  float r;
+  std::memcpy(&r, &u, 4);
+  return r;
+}
+
 // Derive the kernel layouts from the master blob and upload them:
-//  - W_in gets the pre-norm gain folded in: RMSNorm(h; g) W_in^T =
-//    rstd(h) * h (W_in diag(g))^T, so the in_proj GEMM only needs rstd.
+//  - fp32 models: W_in gets the pre-norm gain folded in, RMSNorm(h; g) W_in^T
+//    = rstd(h) * h (W_in diag(g))^T, so the in_proj GEMM only needs rstd.
+//  - bf16 models: every weight is rounded to bf16 (nearest-even) first; the
+//    projections are stored as bf16 (W0 zero-padded in K to a multiple of 8)
+//    and the gain is applied to the activations, not folded into W_in.
 //  - W1 is stored transposed for coalesced reads in the head.
 tcl_status upload(tcl_model* m) {
   const tcl_config& c = m->cfg;
+  const bool bf = c.dtype == TCL_BF16;
   const BlobLayout bl = blob_layout(c);
-  const float* P = m->master.data();
+  std::vector<float> work(m->master);
+  if (bf)
+    for (auto& v : work) v = round_bf16(v);
+  const float* P = work.data();
   const size_t d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank;
   const size_t F = c.F, h = c.head_hidden;
+  const size_t ldw0h = (F + 7) & ~size_t(7);
 
-  std::vector<float> host;
-  auto put = [&](size_t n) {
+  std::vector<uint8_t> host;
+  auto put = [&](size_t bytes) {
     const size_t off = host.size();
-    host.resize(align256((off + n) * 4) / 4, 0.f);
+    host.resize(align256(off + bytes), 0);
     return off;
   };
-  const size_t oW0 = put(d * F), ob0 = put(d);
-  std::memcpy(&host[oW0], P + bl.W0, d * F * 4);
-  std::memcpy(&host[ob0], P + bl.b0, d * 4);
-  struct LO { size_t W_in, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out; };
+  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(host.data() + off); };
+  auto b16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(host.data() + off); };
+  auto copy = [&](size_t src, size_t n) {
+    const size_t o = put(n * 4);
+    std::memcpy(host.data() + o, P + src, n * 4);
+    return o;
+  };
+  auto copy_h = [&](size_t src, size_t rows, size_t cols, size_t ld) {
+    const size_t o = put(rows * ld * 2);
+    for (size_t r = 0; r < rows; ++r)
+      for (size_t k = 0; k < cols; ++k) b16(o)[r * ld + k] = host_bf16(P[src + r * cols + k]);
+    return o;
+  };
+
+  const size_t oW0 = copy(bl.W0, d * F), ob0 = copy(bl.b0, d);
+  const size_t oW0h = bf ? copy_h(bl.W0, d, F, ldw0h) : 0;
+  struct LO { size_t W_in, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out, g, W_in_h, W_x_h, W_out_h; };
   std::vector<LO> lo;
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& L = bl.layers[l];
-    LO o;
-    o.W_in = put(2 * E * d);
+    LO o{};
+    o.W_in = put(2 * E * d * 4);
     for (size_t j = 0; j < 2 * E; ++j)
       for (size_t k = 0; k < d; ++k)
-        host[o.W_in + j * d + k] = (float)((double)P[L.W_in + j * d + k] * (double)P[L.g + k]);
-    o.conv_w = put(E * K);
-    std::memcpy(&host[o.conv_w], P + L.conv_w, E * K * 4);
-    o.conv_b = put(E);
-    std::memcpy(&host[o.conv_b], P + L.conv_b, E * 4);
-    o.W_x = put((R + 2 * N) * E);
-    std::memcpy(&host[o.W_x], P + L.W_x, (R + 2 * N) * E * 4);
-    o.W_dt = put(E * R);
-    std::memcpy(&host[o.W_dt], P + L.W_dt, E * R * 4);
-    o.b_dt = put(E);
-    std::memcpy(&host[o.b_dt], P + L.b_dt, E * 4);
-    o.A_log = put(E * N);
-    std::memcpy(&host[o.A_log], P + L.A_log, E * N * 4);
-    o.D = put(E);
-    std::memcpy(&host[o.D], P + L.D, E * 4);
-    o.W_out = put(d * E);
-    std::memcpy(&host[o.W_out], P + L.W_out, d * E * 4);
+        f32(o.W_in)[j * d + k] = (float)((double)P[L.W_in + j * d + k] * (double)P[L.g + k]);
+    o.conv_w = copy(L.conv_w, E * K);
+    o.conv_b = copy(L.conv_b, E);
+    o.W_x = copy(L.W_x, (R + 2 * N) * E);
+    o.W_dt = copy(L.W_dt, E * R);
+    o.b_dt = copy(L.b_dt, E);
+    o.A_log = copy(L.A_log, E * N);
+    o.D = copy(L.D, E);
+    o.W_out = copy(L.W_out, d * E);
+    o.g = copy(L.g, d);
+    if (bf) {
+      o.W_in_h = copy_h(L.W_in, 2 * E, d, d);
+      o.W_x_h = copy_h(L.W_x, R + 2 * N, E, E);
+      o.W_out_h = copy_h(L.W_out, d, E, E);
+    }
     lo.push_back(o);
   }
-  const size_t og = put(d), oW1T = put(d * h), ob1 = put(h), oW2 = put(h), ob2 = put(1);
-  std::memcpy(&host[og], P + bl.g_f, d * 4);
+  const size_t og = copy(bl.g_f, d);
+  const size_t oW1T = put(d * h * 4);
   for (size_t j = 0; j < h; ++j)
-    for (size_t k = 0; k < d; ++k) host[oW1T + k * h + j] = P[bl.W1 + j * d + k];
-  std::memcpy(&host[ob1], P + bl.b1, h * 4);
-  std::memcpy(&host[oW2], P + bl.W2, h * 4);
-  host[ob2] = P[bl.b2];
+    for (size_t k = 0; k < d; ++k) f32(oW1T)[k * h + j] = P[bl.W1 + j * d + k];
+  const size_t ob1 = copy(bl.b1, h), oW2 = copy(bl.W2, h), ob2 = copy(bl.b2, 1);
 
-  const size_t bytes = host.size() * 4;
+  const size_t bytes = host.size();
   if (m->dev && m->dev_bytes != bytes) {
     (void)hipFree(m->dev);
     m->dev = nullptr;
@@ -255,28 +290,38 @@ tcl_status upload(tcl_model* m) {
     m->dev_bytes = bytes;
   }
   TCL_HIP(hipMemcpy(m->dev, host.data(), bytes, hipMemcpyHostToDevice));
-  float* base = static_cast<float*>(m->dev);
-  m->W0 = base + oW0;
-  m->b0 = base + ob0;
+  uint8_t* base = static_cast<uint8_t*>(m->dev);
+  auto F32 = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
+  auto B16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
+  m->W0 = F32(oW0);
+  m->b0 = F32(ob0);
+  m->W0_h = bf ? B16(oW0h) : nullptr;
+  m->ldw0_h = (int)ldw0h;
   m->layers.clear();
   for (int l = 0; l < c.n_layers; ++l) {
-    tcl_model::Layer L;
-    L.W_in = base + lo[l].W_in;
-    L.conv_w = base + lo[l].conv_w;
-    L.conv_b = base + lo[l].conv_b;
-    L.W_x = base + lo[l].W_x;
-    L.W_dt = base + lo[l].W_dt;
-    L.b_dt = base + lo[l].b_dt;
-    L.A_log = base + lo[l].A_log;
-    L.D = base + lo[l].D;
-    L.W_out = base + lo[l].W_out;
+    tcl_model::Layer L{};
+    L.W_in = F32(lo[l].W_in);
+    L.conv_w = F32(lo[l].conv_w);
+    L.conv_b = F32(lo[l].conv_b);
+    L.W_x = F32(lo[l].W_x);
+    L.W_dt = F32(lo[l].W_dt);
+    L.b_dt = F32(lo[l].b_dt);
+    L.A_log = F32(lo[l].A_log);
+    L.D = F32(lo[l].D);
+    L.W_out = F32(lo[l].W_out);
+    L.g = F32(lo[l].g);
+    if (bf) {
+      L.W_in_h = B16(lo[l].W_in_h);
+      L.W_x_h = B16(lo[l].W_x_h);
+      L.W_out_h = B16(lo[l].W_out_h);
+    }
     m->layers.push_back(L);
   }
-  m->g_f = base + og;
-  m->W1T = base + oW1T;
-  m->b1 = base + ob1;
-  m->W2 = base + oW2;
-  m->b2 = base + ob2;
+  m->g_f = F32(og);
+  m->W1T = F32(oW1T);
+  m->b1 = F32(ob1);
+  m->W2 = F32(oW2);
+  m->b2 = F32(ob2);
   return TCL_OK;
 }
 
@@ -289,11 +334,12 @@ ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L) {
   ScorePlan p;
   const int64_t rows = B * L;
   const int64_t XW = c.dt_rank + 2 * c.d_state;
+  const size_t act = c.dtype == TCL_BF16 ? 2 : 4;  // bytes per stored activation
   size_t o = 0;
   p.offs = o; o = align256(o + (size_t)(B + 1) * 4);
   p.H = o; o = align256(o + (size_t)rows * c.d_model * 4);
-  p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * 4);
-  p.u = o; o = align256(o + (size_t)rows * c.d_inner * 4);
+  p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * act);
+  p.u = o; o = align256(o + (size_t)rows * c.d_inner * act);
   p.xdbl = o; o = align256(o + (size_t)rows * XW * 4);
   p.total = o;
   return p;
@@ -383,41 +429,71 @@ TCL_API tcl_status tcl_score(tcl_model* m, int32_t B, int32_t L, const float* d_
   char* ws = static_cast<char*>(d_ws);
   int* offs = reinterpret_cast<int*>(ws + p.offs);
   float* H = reinterpret_cast<float*>(ws + p.H);
-  float* xz = reinterpret_cast<float*>(ws + p.xz);
-  float* u = reinterpret_cast<float*>(ws + p.u);
   float* xdbl = reinterpret_cast<float*>(ws + p.xdbl);
   const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
   const int Mmax = B * L;
 
   TCL_LAUNCH(m, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  if (c.dtype == TCL_F32) {
+    float* xz = reinterpret_cast<float*>(ws + p.xz);
+    float* u = reinterpret_cast<float*>(ws + p.u);
+    GemmArgs g;
+    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
+    g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
+    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
+    TCL_LAUNCH(m, "gemm_input", launch_gemm_f32(g, kBias | kGather, kWide, s));
 
-  GemmArgs g;
-  g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
-  g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
-  g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
-  TCL_LAUNCH(m, "gemm_input", launch_gemm_f32(g, kBias | kGather, kWide, s));
+    for (int l = 0; l < c.n_layers; ++l) {
+      const auto& W = m->layers[l];
+      GemmArgs gi;
+      gi.A = H; gi.lda = d; gi.W = W.W_in; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
+      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
+      TCL_LAUNCH(m, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, kWide, s));
 
-  for (int l = 0; l < c.n_layers; ++l) {
-    const auto& W = m->layers[l];
-    GemmArgs gi;
-    gi.A = H; gi.lda = d; gi.W = W.W_in; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
-    gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-    TCL_LAUNCH(m, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, kWide, s));
+      TCL_LAUNCH(m, "conv_silu", launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w,
+                                                         W.conv_b, u, s));
+      GemmArgs gx;
+      gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
+      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
+      TCL_LAUNCH(m, "gemm_x_proj", launch_gemm_f32(gx, 0, kNarrow, s));
 
-    TCL_LAUNCH(m, "conv_silu", launch_conv_silu_f32(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w, W.conv_b, u, s));
+      TCL_LAUNCH(m, "scan", launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                               W.b_dt, W.A_log, W.D, u, s));
+      GemmArgs go;
+      go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
+      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
+      TCL_LAUNCH(m, "gemm_out_proj", launch_gemm_f32(go, kResid, kWide, s));
+    }
+  } else {
+    uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
+    uint16_t* u = reinterpret_cast<uint16_t*>(ws + p.u);
+    GemmArgsBF16 g;
+    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
+    g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
+    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
+    TCL_LAUNCH(m, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, s));
 
-    GemmArgs gx;
-    gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
-    gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-    TCL_LAUNCH(m, "gemm_x_proj", launch_gemm_f32(gx, 0, kNarrow, s));
+    for (int l = 0; l < c.n_layers; ++l) {
+      const auto& W = m->layers[l];
+      GemmArgsBF16 gi;
+      gi.A = H; gi.lda = d; gi.W = W.W_in_h; gi.ldw = d; gi.gain = W.g; gi.C = xz; gi.ldc = 2 * E;
+      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
+      TCL_LAUNCH(m, "gemm_in_proj", launch_gemm_bf16(gi, kNormF32toBF16, s));
 
-    TCL_LAUNCH(m, "scan", launch_scan_f32(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt, W.b_dt,
-                                          W.A_log, W.D, u, s));
+      TCL_LAUNCH(m, "conv_silu", launch_conv_silu<uint16_t>(B, E, c.d_conv, offs, xz, 2 * E,
+                                                            W.conv_w, W.conv_b, u, s));
+      GemmArgsBF16 gx;
+      gx.A = u; gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
+      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
+      TCL_LAUNCH(m, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32Narrow, s));
 
-    GemmArgs go;
-    go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
-    go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-    TCL_LAUNCH(m, "gemm_out_proj", launch_gemm_f32(go, kResid, kWide, s));
+      TCL_LAUNCH(m, "scan", launch_scan<uint16_t>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                                  W.b_dt, W.A_log, W.D, u, s));
+      GemmArgsBF16 go;
+      go.A = u; go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = H; go.ldc = d;
+      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
+      TCL_LAUNCH(m, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, s));
+    }
   }
 
   TCL_LAUNCH(m, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
@@ -479,9 +555,10 @@ TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const
                                           const float* d_x, int32_t ldx, const float* d_w,
                                           const float* d_b, float* d_u, void* stream) {
   if (B <= 0 || E <= 0 || K < 1 || K > 4 || ldx < E) return fail(TCL_ERR_INVALID_ARG, "bad sizes");
+  if (E % 4 || ldx % 4) return fail(TCL_ERR_INVALID_ARG, "E and ldx must be multiples of 4");
   if (!d_offs || !d_x || !d_w || !d_b || !d_u) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
-  TCL_HIP(launch_conv_silu_f32(B, E, K, d_offs, d_x, ldx, d_w, d_b, d_u,
-                               static_cast<hipStream_t>(stream)));
+  TCL_HIP(launch_conv_silu<float>(B, E, K, d_offs, d_x, ldx, d_w, d_b, d_u,
+                                  static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }
 
@@ -495,7 +572,21 @@ TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R,
   if (R % 4 || R <= 0 || R > 32) return fail(TCL_ERR_UNSUPPORTED, "dt_rank must be 4..32, step 4");
   if (!d_offs || !d_u || !d_xdbl || !d_z || !d_W_dt || !d_b_dt || !d_A_log || !d_D || !d_out)
     return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
-  TCL_HIP(launch_scan_f32(B, E, N, R, d_offs, d_u, d_xdbl, d_z, ldz, d_W_dt, d_b_dt, d_A_log, d_D,
-                          d_out, static_cast<hipStream_t>(stream)));
+  TCL_HIP(launch_scan<float>(B, E, N, R, d_offs, d_u, d_xdbl, d_z, ldz, d_W_dt, d_b_dt, d_A_log,
+                             d_D, d_out, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
+TCL_API tcl_status tcl_test_gemm_bf16(int32_t M, int32_t N, int32_t K, const uint16_t* d_A,
+                                      const uint16_t* d_W, const float* d_bias, float* d_C,
+                                      void* stream) {
+  if (M <= 0 || N <= 0 || K <= 0 || K % 8) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
+  if (!d_A || !d_W || !d_C) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_A) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
+    return fail(TCL_ERR_INVALID_ARG, "A and W must be 16-byte aligned");
+  GemmArgsBF16 g;
+  g.A = d_A; g.lda = K; g.W = d_W; g.ldw = K; g.bias = d_bias; g.C = d_C; g.ldc = N;
+  g.Mmax = M; g.N = N; g.K = K;
+  TCL_HIP(launch_gemm_bf16(g, d_bias ? kBF16toF32Bias : kBF16toF32, static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }

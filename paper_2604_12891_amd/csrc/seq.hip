@@ -1,4 +1,4 @@
-// Per-program kernels of the fp32 forward: token packing, causal conv +
+// Per-program kernels of the forward pass: token packing, causal conv +
 // SiLU, the selective scan, and the pool + score head.
 //
 // Tokens are packed program by program: program b owns rows
@@ -48,34 +48,102 @@ __global__ __launch_bounds__(1024) void offsets_kernel(const int* __restrict__ l
   if (tid == 1023) offs[B] = before + inc;
 }
 
+// ---------------------------------------------------------------- element access
+// Activations are fp32 or bf16 in memory; every kernel computes in fp32.
+__device__ __forceinline__ float ld1(const float* p) { return *p; }
+__device__ __forceinline__ float ld1(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ void st1(float* p, float v) { *p = v; }
+__device__ __forceinline__ void st1(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// CH adjacent channels per thread: one 16-byte access (4 fp32 or 8 bf16).
+template <typename T> struct Vec;
+template <> struct Vec<float> {
+  static constexpr int CH = 4;
+  static __device__ __forceinline__ void load(const float* p, float* v) {
+    const floatx4 x = *reinterpret_cast<const floatx4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float* v) {
+    *reinterpret_cast<floatx4*>(p) = floatx4{v[0], v[1], v[2], v[3]};
+  }
+};
+template <> struct Vec<uint16_t> {
+  static constexpr int CH = 8;
+  static __device__ __forceinline__ void load(const uint16_t* p, float* v) {
+    const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(x[i] << 16);
+      v[2 * i + 1] = __uint_as_float(x[i] & 0xFFFF0000u);
+    }
+  }
+  static __device__ __forceinline__ void store(uint16_t* p, const float* v) {
+    u32x4 x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      x[i] = (uint32_t)f32_to_bf16(v[2 * i]) | ((uint32_t)f32_to_bf16(v[2 * i + 1]) << 16);
+    *reinterpret_cast<u32x4*>(p) = x;
+  }
+};
+
 // ---------------------------------------------------------------- conv + SiLU
-// x_{t-K+1..t} of one channel live in a K-register window.
-template <int K>
+// One thread per (program, CH adjacent channels): 16-byte loads and stores,
+// x_{t-K+1..t} of its channels in a K-deep register window. The loop is
+// unrolled by 4 tokens with the loads issued ahead of the arithmetic.
+template <typename T, int K>
 __global__ __launch_bounds__(256) void conv_silu_kernel(const int* __restrict__ offs, int E,
-                                                        const float* __restrict__ x, int ldx,
+                                                        const T* __restrict__ x, int ldx,
                                                         const float* __restrict__ w,
                                                         const float* __restrict__ bias,
-                                                        float* __restrict__ u) {
+                                                        T* __restrict__ u) {
+  constexpr int CH = Vec<T>::CH;
   const int b = blockIdx.x;
-  const int e = blockIdx.y * blockDim.x + threadIdx.x;
-  if (e >= E) return;
+  const int e0 = (blockIdx.y * blockDim.x + threadIdx.x) * CH;
+  if (e0 >= E) return;
   const int base = offs[b], len = offs[b + 1] - base;
-  float wk[K], win[K];
+  float wk[K][CH], win[K][CH], be[CH];
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    wk[k] = w[e * K + k];
-    win[k] = 0.f;
+  for (int c = 0; c < CH; ++c) {
+    be[c] = bias[e0 + c];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      wk[k][c] = w[(e0 + c) * K + k];
+      win[k][c] = 0.f;
+    }
   }
-  const float be = bias[e];
-  for (int t = 0; t < len; ++t) {
-    const int64_t row = base + t;
+  const T* xp = x + (int64_t)base * ldx + e0;
+  T* up = u + (int64_t)base * E + e0;
+  auto step = [&](const float* xin, T* dst) {
 #pragma unroll
-    for (int k = 0; k < K - 1; ++k) win[k] = win[k + 1];
-    win[K - 1] = x[row * ldx + e];
-    float acc = be;
+    for (int k = 0; k < K - 1; ++k)
 #pragma unroll
-    for (int k = 0; k < K; ++k) acc = fmaf(wk[k], win[k], acc);
-    u[row * E + e] = silu(acc);
+      for (int c = 0; c < CH; ++c) win[k][c] = win[k + 1][c];
+    float acc[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      win[K - 1][c] = xin[c];
+      acc[c] = be[c];
+#pragma unroll
+      for (int k = 0; k < K; ++k) acc[c] = fmaf(wk[k][c], win[k][c], acc[c]);
+      acc[c] = silu(acc[c]);
+    }
+    Vec<T>::store(dst, acc);
+  };
+  constexpr int U = 4;
+  int t = 0;
+  for (; t + U <= len; t += U) {
+    float xin[U][CH];
+#pragma unroll
+    for (int j = 0; j < U; ++j) Vec<T>::load(xp + (int64_t)(t + j) * ldx, xin[j]);
+#pragma unroll
+    for (int j = 0; j < U; ++j) step(xin[j], up + (int64_t)(t + j) * E);
+  }
+  for (; t < len; ++t) {
+    float xin[CH];
+    Vec<T>::load(xp + (int64_t)t * ldx, xin);
+    step(xin, up + (int64_t)t * E);
   }
 }
 
@@ -88,12 +156,12 @@ __global__ __launch_bounds__(256) void conv_silu_kernel(const int* __restrict__ 
 constexpr int kScanThreads = 128;
 constexpr int kScanTC = 32;
 
-template <int N, int R>
+template <typename T, int N, int R>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(
-    const int* __restrict__ offs, int E, const float* u, const float* __restrict__ xdbl,
-    const float* __restrict__ z, int ldz, const float* __restrict__ W_dt,
+    const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
+    const T* __restrict__ z, int ldz, const float* __restrict__ W_dt,
     const float* __restrict__ b_dt, const float* __restrict__ A_log,
-    const float* __restrict__ Dp, float* out) {
+    const float* __restrict__ Dp, T* out) {
   constexpr int XW = R + 2 * N;
   __shared__ __attribute__((aligned(16))) float sX[kScanTC * XW];
   const int b = blockIdx.x;
@@ -119,11 +187,17 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
     for (int i = threadIdx.x; i < nt * XW; i += kScanThreads) sX[i] = src[i];
     __syncthreads();
     if (!active) continue;
+    // u and z of the next token are loaded while this token is computed
+    float un = ld1(u + (int64_t)(base + t0) * E + e);
+    float zn = ld1(z + (int64_t)(base + t0) * ldz + e);
     for (int tt = 0; tt < nt; ++tt) {
       const int64_t row = base + t0 + tt;
       const float* xr = &sX[tt * XW];
-      const float uv = u[row * E + e];
-      const float zv = z[row * ldz + e];
+      const float uv = un, zv = zn;
+      if (tt + 1 < nt) {
+        un = ld1(u + (row + 1) * E + e);
+        zn = ld1(z + (row + 1) * ldz + e);
+      }
       float v = bdt;
 #pragma unroll
       for (int r = 0; r < R; ++r) v = fmaf(wdt[r], xr[r], v);
@@ -137,7 +211,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
         y = fmaf(s[n], xr[R + N + n], y);
       }
       y = fmaf(Dv, uv, y);
-      out[row * E + e] = y * silu(zv);
+      st1(out + row * E + e, y * silu(zv));
     }
   }
 }
@@ -243,29 +317,32 @@ hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream
   return hipGetLastError();
 }
 
-hipError_t launch_conv_silu_f32(int B, int E, int K, const int* offs, const float* x, int ldx,
-                                const float* w, const float* b, float* u, hipStream_t s) {
+template <typename T>
+hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, int ldx,
+                            const float* w, const float* b, T* u, hipStream_t s) {
+  constexpr int CH = Vec<T>::CH;
   if (B <= 0) return hipSuccess;
-  dim3 grid(B, (E + 255) / 256);
+  if (E % CH || ldx % CH) return hipErrorInvalidValue;
+  dim3 grid(B, (E / CH + 255) / 256);
   switch (K) {
-    case 1: hipLaunchKernelGGL(conv_silu_kernel<1>, grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
-    case 2: hipLaunchKernelGGL(conv_silu_kernel<2>, grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
-    case 3: hipLaunchKernelGGL(conv_silu_kernel<3>, grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
-    case 4: hipLaunchKernelGGL(conv_silu_kernel<4>, grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
+    case 1: hipLaunchKernelGGL((conv_silu_kernel<T, 1>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
+    case 2: hipLaunchKernelGGL((conv_silu_kernel<T, 2>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
+    case 3: hipLaunchKernelGGL((conv_silu_kernel<T, 3>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
+    case 4: hipLaunchKernelGGL((conv_silu_kernel<T, 4>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, u); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_scan_f32(int B, int E, int N, int R, const int* offs, const float* u,
-                           const float* xdbl, const float* z, int ldz, const float* W_dt,
-                           const float* b_dt, const float* A_log, const float* D, float* out,
-                           hipStream_t s) {
+template <typename T>
+hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
+                       const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
+                       const float* D, T* out, hipStream_t s) {
   if (B <= 0) return hipSuccess;
   if (N != 16) return hipErrorInvalidValue;
   dim3 grid(B, (E + kScanThreads - 1) / kScanThreads);
-#define TCL_SCAN(RR)                                                                              \
-  hipLaunchKernelGGL((scan_kernel<16, RR>), grid, dim3(kScanThreads), 0, s, offs, E, u, xdbl, z, \
+#define TCL_SCAN(RR)                                                                                 \
+  hipLaunchKernelGGL((scan_kernel<T, 16, RR>), grid, dim3(kScanThreads), 0, s, offs, E, u, xdbl, z, \
                      ldz, W_dt, b_dt, A_log, D, out)
   switch (R) {
     case 4: TCL_SCAN(4); break;
@@ -281,6 +358,18 @@ hipError_t launch_scan_f32(int B, int E, int N, int R, const int* offs, const fl
 #undef TCL_SCAN
   return hipGetLastError();
 }
+
+template hipError_t launch_conv_silu<float>(int, int, int, const int*, const float*, int, const float*,
+                                            const float*, float*, hipStream_t);
+template hipError_t launch_conv_silu<uint16_t>(int, int, int, const int*, const uint16_t*, int,
+                                               const float*, const float*, uint16_t*, hipStream_t);
+template hipError_t launch_scan<float>(int, int, int, int, const int*, const float*, const float*,
+                                       const float*, int, const float*, const float*, const float*,
+                                       const float*, float*, hipStream_t);
+template hipError_t launch_scan<uint16_t>(int, int, int, int, const int*, const uint16_t*,
+                                          const float*, const uint16_t*, int, const float*,
+                                          const float*, const float*, const float*, uint16_t*,
+                                          hipStream_t);
 
 hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const int* lengths,
                            const float* H, const float* g_f, int final_norm, float eps,

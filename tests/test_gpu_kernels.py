@@ -61,6 +61,27 @@ def test_gemm_f32(M, N, K, bias):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+@pytest.mark.parametrize("M,N,K", [(1, 64, 8), (31, 48, 512), (129, 256, 168), (1000, 1024, 256),
+                                   (257, 256, 512), (77, 100, 40)])
+@pytest.mark.parametrize("bias", [False, True])
+def test_gemm_bf16(M, N, K, bias):
+    """bf16 x bf16 products are exact in fp32; only the fp32 accumulation rounds."""
+    print(f"gemm_bf16 M={M} N={N} K={K} bias={bias}", flush=True)
+    rng = np.random.default_rng(M * 5 + N + K)
+    A = wl.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+    W = wl.round_to_bf16(rng.standard_normal((N, K)).astype(np.float32))
+    bv = rng.standard_normal(N).astype(np.float32) if bias else None
+    C = tb.gemm_bf16(_dev(A, torch.bfloat16), _dev(W, torch.bfloat16), _dev(bv) if bias else None)
+    torch.cuda.synchronize()
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    bound = (K + 2) * U * (np.abs(A).astype(np.float64) @ np.abs(W).astype(np.float64).T)
+    if bias:
+        ref += bv
+        bound += U * np.abs(ref)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
 @pytest.mark.parametrize("K", [1, 3, 4])
 def test_conv_silu_f32(K):
     rng = np.random.default_rng(K)

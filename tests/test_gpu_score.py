@@ -72,6 +72,36 @@ def test_long_sequences_sampled():
     assert_scores_match(g[idx], oracle_scores(blob, X[idx], lengths[idx], w.model), "f32", w.name)
 
 
+@pytest.mark.parametrize("perturb", [False, True])
+def test_tiny_bf16(perturb):
+    """The bf16 path (bf16 weights and activations, fp32 accumulation and scan
+    state) on the small model; weights are bf16-representable on both sides."""
+    shape = wl.TINY
+    blob = wl.round_to_bf16(wl.init_params(shape, np.random.default_rng(21), perturb=perturb))
+    X, lengths = wl.make_inputs(64, 25, shape.F, 5, 25, np.random.default_rng(22))
+    print(f"tcl_score tiny bf16 perturb={perturb}", flush=True)
+    g = _score(_model(shape, blob, "bf16"), X, lengths)
+    assert_scores_match(g, oracle_scores(blob, X, lengths, shape), "bf16", "tiny bf16")
+
+
+def test_bf16_pool_full_size_sampled():
+    w = wl.WORKLOADS["score_B65536_L25_d256_bf16"]
+    print(f"tcl_score {w.name} full batch", flush=True)
+    blob, X, lengths = wl.make_workload(w.name)
+    g = _score(_model(w.model, blob, "bf16"), X, lengths)
+    assert np.all(np.isfinite(g))
+    idx = _sample(lengths, 96, seed=2)
+    assert_scores_match(g[idx], oracle_scores(blob, X[idx], lengths[idx], w.model), "bf16", w.name)
+
+
+def test_bf16_perturbed_weights():
+    w = wl.WORKLOADS["score_B65536_L25_d256_bf16"]
+    blob, X, lengths = wl.make_workload(w.name, B=128, perturb=True)
+    print(f"tcl_score {w.name} B=128 perturbed", flush=True)
+    g = _score(_model(w.model, blob, "bf16"), X, lengths)
+    assert_scores_match(g, oracle_scores(blob, X, lengths, w.model), "bf16", w.name + " perturbed")
+
+
 @pytest.mark.parametrize("case", ["B1", "L1", "all_full", "odd_B", "len_1_and_L"])
 def test_edge_shapes(case):
     shape = wl.TINY
