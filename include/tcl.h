@@ -152,6 +152,60 @@ TCL_API tcl_status tcl_timing_get(tcl_model* model, int32_t idx, const char** na
                                   int64_t* launches);
 TCL_API tcl_status tcl_timing_reset(tcl_model* model);
 
+/* ---------------------------------------------------------------------
+ * Distillation (section 6: the knowledge-distillation phase trains a
+ * student to match a frozen teacher; section 5.3 / the experimental setup
+ * use Adam). One step with B programs:
+ *   t = teacher(X) (frozen), s = student(X),
+ *   L = mean_b (s_b - t_b)^2 + mean_b (s_b - y_b)^2   (y = labels),
+ *   full backward of the student (including the selective scan), then one
+ *   bias-corrected Adam update (beta1, beta2, eps, no weight decay) of the
+ *   student's fp32 master weights, and the student's compute copies are
+ *   re-derived from the updated master.
+ * The student must be a bf16 model (bf16 weights and activations in the
+ * forward, fp32 master weights, fp32 scan state, fp32 gradients); d_inner
+ * <= 256 and dt_rank in {4, 8, 16}. The teacher may be fp32 or bf16. The
+ * trainer keeps pointers to both models; they must outlive it. While a
+ * trainer exists, the student's parameters change with every step
+ * (tcl_get_params returns the current master weights).
+ * ------------------------------------------------------------------- */
+
+/* Create a trainer (allocates the gradient blob and the Adam moments, zeroed;
+ * the step count starts at 0). max_B, max_L bound every later step; max_L is
+ * also limited by LDS staging in the scan backward (about 300 tokens). */
+TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, float lr, float beta1,
+                                      float beta2, float eps, int32_t max_B, int32_t max_L,
+                                      tcl_trainer** out);
+TCL_API tcl_status tcl_trainer_destroy(tcl_trainer* trainer);
+
+/* Device workspace for one step with B programs padded to L tokens (0 if the
+ * shape exceeds the trainer's bounds). */
+TCL_API size_t tcl_distill_workspace_bytes(const tcl_trainer* trainer, int32_t B, int32_t L);
+
+/* One distillation step (stream-ordered; see above).
+ *   d_feats [B, L, F] fp32, d_lengths [B] int32, d_labels [B] fp32 (device);
+ *   d_loss [3] fp32 output: total, mse(student, teacher), mse(student, label);
+ *   d_workspace >= tcl_distill_workspace_bytes, 256-byte aligned.
+ * The first step with a new (B, L) uploads a small reduction table and
+ * synchronises the device once. Programs with invalid lengths must not be
+ * passed (their NaN scores would poison the loss). */
+TCL_API tcl_status tcl_distill_step(tcl_trainer* trainer, int32_t B, int32_t L, const float* d_feats,
+                                    const int32_t* d_lengths, const float* d_labels, float* d_loss,
+                                    void* d_workspace, size_t ws_bytes, void* stream);
+
+/* Copy the gradient blob of the last step (canonical layout, fp32) to the
+ * host. Synchronous. */
+TCL_API tcl_status tcl_trainer_get_grads(const tcl_trainer* trainer, float* h_out, size_t n_params);
+
+/* Per-kernel timing of the step's own kernels, as for tcl_timing_* (the
+ * teacher's scoring kernels are timed on the teacher's handle with
+ * tcl_timing_enable). */
+TCL_API tcl_status tcl_trainer_timing_enable(tcl_trainer* trainer, int32_t enable);
+TCL_API int32_t tcl_trainer_timing_count(const tcl_trainer* trainer);
+TCL_API tcl_status tcl_trainer_timing_get(tcl_trainer* trainer, int32_t idx, const char** name,
+                                          double* total_ms, int64_t* launches);
+TCL_API tcl_status tcl_trainer_timing_reset(tcl_trainer* trainer);
+
 /* Message describing the last failure on this thread ("" if none). */
 TCL_API const char* tcl_last_error(void);
 

@@ -358,16 +358,20 @@ def adam_update(p, g, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-8):
 
 def distill_step(teacher_blob, tcfg, student_blob, scfg, X, lengths, labels,
                  m=None, v=None, step=1, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
-                 compute_blob=None):
+                 compute_blob=None, teacher_scores=None):
     """One teacher->student step.
 
     `student_blob` holds the master weights that Adam updates; the forward and
     backward use `compute_blob` when given (the bf16-rounded copy of the
-    master), else the master itself.
+    master), else the master itself. `teacher_scores`, when given, are the
+    teacher's scores of this batch (saves recomputing them).
     Returns dict(loss=(total, mt, ml), teacher=t, student=s, grad=flat,
     params=new master, m=, v=).
     """
-    t = score(teacher_blob, X, lengths, tcfg)
+    if teacher_scores is None:
+        t = score(teacher_blob, X, lengths, tcfg)
+    else:
+        t = np.asarray(teacher_scores, dtype=f64)
     P = unpack(student_blob if compute_blob is None else compute_blob, scfg)
     s, caches, top = forward(P, X, lengths, scfg, keep=True)
     loss, ds = distill_loss(s, t, np.asarray(labels, dtype=f64))

@@ -48,6 +48,17 @@ _SIGS = {
     "tcl_timing_get": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                               ctypes.POINTER(ctypes.c_int64)]),
     "tcl_timing_reset": (_i32, [_vp]),
+    "tcl_trainer_create": (_i32, [_vp, _vp, ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                  _i32, _i32, ctypes.POINTER(_vp)]),
+    "tcl_trainer_destroy": (_i32, [_vp]),
+    "tcl_distill_workspace_bytes": (_sz, [_vp, _i32, _i32]),
+    "tcl_distill_step": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "tcl_trainer_get_grads": (_i32, [_vp, _vp, _sz]),
+    "tcl_trainer_timing_enable": (_i32, [_vp, _i32]),
+    "tcl_trainer_timing_count": (_i32, [_vp]),
+    "tcl_trainer_timing_get": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
+                                      ctypes.POINTER(ctypes.c_int64)]),
+    "tcl_trainer_timing_reset": (_i32, [_vp]),
     "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
@@ -173,6 +184,75 @@ class CostModel:
     def set_params(self, params: np.ndarray):
         blob = np.ascontiguousarray(params, dtype=np.float32)
         check(lib().tcl_set_params(self._h, blob.ctypes.data, blob.size))
+
+
+class Trainer:
+    """Teacher -> student distillation (tcl_trainer_create / tcl_distill_step)."""
+
+    def __init__(self, teacher: CostModel, student: CostModel, lr=1e-3, betas=(0.9, 0.999), eps=1e-8,
+                 max_B=1024, max_L=25):
+        h = _vp()
+        check(lib().tcl_trainer_create(teacher.handle, student.handle, lr, betas[0], betas[1], eps, max_B,
+                                       max_L, ctypes.byref(h)))
+        self._h = h
+        self._n = student._n
+        self._keep = (teacher, student)  # the trainer must not outlive its models
+        self._ws = None
+
+    def close(self):
+        if getattr(self, "_h", None):
+            check(lib().tcl_trainer_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace_bytes(self, B: int, L: int) -> int:
+        return lib().tcl_distill_workspace_bytes(self._h, B, L)
+
+    def workspace(self, B: int, L: int):
+        import torch
+        need = self.workspace_bytes(B, L)
+        if need == 0:
+            raise ValueError(f"B={B}, L={L} exceed the trainer's bounds")
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        return self._ws
+
+    def step(self, feats, lengths, labels, loss=None, workspace=None, stream=None):
+        """One step; returns the device tensor [total, mse_teacher, mse_label]."""
+        import torch
+        B, L, _ = feats.shape
+        if loss is None:
+            loss = torch.empty(3, dtype=torch.float32, device=feats.device)
+        ws = self.workspace(B, L) if workspace is None else workspace
+        check(lib().tcl_distill_step(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), labels.data_ptr(),
+                                     loss.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
+                                     _stream(stream)))
+        return loss
+
+    def grads(self) -> np.ndarray:
+        out = np.empty(self._n, dtype=np.float32)
+        check(lib().tcl_trainer_get_grads(self._h, out.ctypes.data, out.size))
+        return out
+
+    def timing(self, enable: bool):
+        check(lib().tcl_trainer_timing_enable(self._h, int(enable)))
+
+    def timing_reset(self):
+        check(lib().tcl_trainer_timing_reset(self._h))
+
+    def timing_report(self) -> dict:
+        L = lib()
+        out = {}
+        for i in range(L.tcl_trainer_timing_count(self._h)):
+            name, ms, n = ctypes.c_char_p(), ctypes.c_double(), ctypes.c_int64()
+            check(L.tcl_trainer_timing_get(self._h, i, ctypes.byref(name), ctypes.byref(ms), ctypes.byref(n)))
+            out[name.value.decode()] = (ms.value, n.value)
+        return out
 
 
 def gemm_f32(A, W, bias=None, out=None, stream=None):

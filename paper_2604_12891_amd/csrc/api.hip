@@ -1,24 +1,21 @@
-// Host runtime of libtcl: argument checking, model state, workspace
-// planning and the launch sequence of the scoring pass. Every launch is
-// stream-ordered on the caller's stream; nothing here synchronises except
-// create / set / get, which move parameters between host and device.
+// Host runtime of libtcl: argument checking, model state, weight layouts,
+// workspace planning and the launch sequence of the scoring pass. Every
+// launch is stream-ordered on the caller's stream; nothing here synchronises
+// except create / set / get, which move parameters between host and device.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
-#include <cstdarg>
-#include <cstdio>
 #include <cstring>
-#include <string>
-#include <vector>
 
-#include "../../include/tcl.h"
-#include "kernels.h"
+#include "model.h"
 
 using namespace tcl;
 
-namespace {
+namespace tcl {
 
+namespace {
 thread_local std::string g_err;
+}
 
 tcl_status fail(tcl_status st, const char* fmt, ...) {
   char buf[512];
@@ -30,39 +27,47 @@ tcl_status fail(tcl_status st, const char* fmt, ...) {
   return st;
 }
 
-#define TCL_HIP(call)                                                                     \
-  do {                                                                                     \
-    hipError_t e_ = (call);                                                                \
-    if (e_ != hipSuccess) return fail(TCL_ERR_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
-  } while (0)
+const char* last_error() { return g_err.c_str(); }
 
-size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+int Timing::category(const char* n) {
+  for (size_t i = 0; i < names.size(); ++i)
+    if (names[i] == n) return (int)i;
+  names.emplace_back(n);
+  total_ms.push_back(0.0);
+  count.push_back(0);
+  return (int)names.size() - 1;
+}
 
-// Launch CALL (a hipError_t expression); with timing enabled, bracket it by
-// events on stream `s` under category NAME.
-#define TCL_LAUNCH(M, NAME, CALL)                                                 \
-  do {                                                                           \
-    hipEvent_t ea_ = nullptr, eb_ = nullptr;                                     \
-    if ((M)->timing.on) {                                                        \
-      TCL_HIP((M)->timing.event(&ea_));                                          \
-      TCL_HIP(hipEventRecord(ea_, s));                                           \
-    }                                                                            \
-    TCL_HIP(CALL);                                                               \
-    if ((M)->timing.on) {                                                        \
-      TCL_HIP((M)->timing.event(&eb_));                                          \
-      TCL_HIP(hipEventRecord(eb_, s));                                           \
-      (M)->timing.pending.push_back({(M)->timing.category(NAME), ea_, eb_});     \
-    }                                                                            \
-  } while (0)
+hipError_t Timing::event(hipEvent_t* e) {
+  if (!pool.empty()) {
+    *e = pool.back();
+    pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
 
-// Offsets of each tensor in the canonical blob.
-struct BlobLayout {
-  size_t W0, b0, g_f, W1, b1, W2, b2, total;
-  struct L {
-    size_t g, W_in, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
-  };
-  std::vector<L> layers;
-};
+hipError_t Timing::flush() {
+  for (auto& p : pending) {
+    hipError_t err = hipEventSynchronize(p.b);
+    if (err != hipSuccess) return err;
+    float ms = 0.f;
+    err = hipEventElapsedTime(&ms, p.a, p.b);
+    if (err != hipSuccess) return err;
+    total_ms[p.cat] += ms;
+    count[p.cat] += 1;
+    pool.push_back(p.a);
+    pool.push_back(p.b);
+  }
+  pending.clear();
+  return hipSuccess;
+}
+
+void Timing::release() {
+  (void)flush();
+  for (auto e : pool) (void)hipEventDestroy(e);
+  pool.clear();
+}
 
 BlobLayout blob_layout(const tcl_config& c) {
   BlobLayout bl;
@@ -94,6 +99,106 @@ BlobLayout blob_layout(const tcl_config& c) {
   return bl;
 }
 
+ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L) {
+  ScorePlan p;
+  const int64_t rows = B * L;
+  const int64_t XW = c.dt_rank + 2 * c.d_state;
+  const size_t act = c.dtype == TCL_BF16 ? 2 : 4;  // bytes per stored activation
+  size_t o = 0;
+  p.offs = o; o = align256(o + (size_t)(B + 1) * 4);
+  p.H = o; o = align256(o + (size_t)rows * c.d_model * 4);
+  p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * act);
+  p.u = o; o = align256(o + (size_t)rows * c.d_inner * act);
+  p.xdbl = o; o = align256(o + (size_t)rows * XW * 4);
+  p.total = o;
+  return p;
+}
+
+tcl_status derive_weights(tcl_model* m, hipStream_t s) {
+  TCL_HIP(launch_derive(m->master, m->jobs, m->njobs, m->derive_total, m->dev,
+                        m->cfg.dtype == TCL_BF16 ? 1 : 0, s));
+  return TCL_OK;
+}
+
+tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
+                     float* d_scores, char* ws, hipStream_t s) {
+  const tcl_config& c = m->cfg;
+  const ScorePlan p = score_plan(c, B, L);
+  int* offs = reinterpret_cast<int*>(ws + p.offs);
+  float* H = reinterpret_cast<float*>(ws + p.H);
+  float* xdbl = reinterpret_cast<float*>(ws + p.xdbl);
+  const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
+  const int Mmax = B * L;
+  Timing& T = m->timing;
+
+  TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  if (c.dtype == TCL_F32) {
+    float* xz = reinterpret_cast<float*>(ws + p.xz);
+    float* u = reinterpret_cast<float*>(ws + p.u);
+    GemmArgs g;
+    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
+    g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
+    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
+    TCL_LAUNCH(T, "gemm_input", launch_gemm_f32(g, kBias | kGather, kWide, s));
+
+    for (int l = 0; l < c.n_layers; ++l) {
+      const auto& W = m->layers[l];
+      GemmArgs gi;
+      gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
+      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
+      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, kWide, s));
+
+      TCL_LAUNCH(T, "conv_silu", launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w,
+                                                         W.conv_b, u, s));
+      GemmArgs gx;
+      gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
+      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
+      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_f32(gx, 0, kNarrow, s));
+
+      TCL_LAUNCH(T, "scan", launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                               W.b_dt, W.A_log, W.D, u, s));
+      GemmArgs go;
+      go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
+      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
+      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_f32(go, kResid, kWide, s));
+    }
+  } else {
+    uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
+    uint16_t* u = reinterpret_cast<uint16_t*>(ws + p.u);
+    GemmArgsBF16 g;
+    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
+    g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
+    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
+    TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, s));
+
+    for (int l = 0; l < c.n_layers; ++l) {
+      const auto& W = m->layers[l];
+      GemmArgsBF16 gi;
+      gi.A = H; gi.lda = d; gi.W = W.W_in_h; gi.ldw = d; gi.gain = W.g; gi.C = xz; gi.ldc = 2 * E;
+      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
+      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_bf16(gi, kNormF32toBF16, s));
+
+      TCL_LAUNCH(T, "conv_silu", launch_conv_silu<uint16_t>(B, E, c.d_conv, offs, xz, 2 * E,
+                                                            W.conv_w, W.conv_b, u, s));
+      GemmArgsBF16 gx;
+      gx.A = u; gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
+      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
+      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32Narrow, s));
+
+      TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                                  W.b_dt, W.A_log, W.D, u, s));
+      GemmArgsBF16 go;
+      go.A = u; go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = H; go.ldc = d;
+      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
+      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, s));
+    }
+  }
+  TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
+                                        c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2, m->b2,
+                                        d_scores, s));
+  return TCL_OK;
+}
+
 tcl_status check_config(const tcl_config* c) {
   if (!c) return fail(TCL_ERR_INVALID_ARG, "config is NULL");
   if (c->F <= 0 || c->d_model <= 0 || c->d_inner <= 0 || c->d_state <= 0 || c->d_conv <= 0 ||
@@ -117,232 +222,110 @@ tcl_status check_config(const tcl_config* c) {
   return TCL_OK;
 }
 
-}  // namespace
-
-// Device-side state of a model. All derived weights live in one allocation.
-struct tcl_model {
-  tcl_config cfg{};
-  int device = 0;
-  std::vector<float> master;  // canonical fp32 blob
-  void* dev = nullptr;
-  size_t dev_bytes = 0;
-  struct Layer {
-    float *W_in, *conv_w, *conv_b, *W_x, *W_dt, *b_dt, *A_log, *D, *W_out;
-    float* g;                                    // RMSNorm gain (bf16 path applies it to A)
-    uint16_t *W_in_h, *W_x_h, *W_out_h;          // bf16 copies (bf16 models only)
-  };
-  float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1T = nullptr, *b1 = nullptr,
-        *W2 = nullptr, *b2 = nullptr;
-  uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
-  int ldw0_h = 0;
-  std::vector<Layer> layers;
-
-  // Per-kernel event timing (tcl_timing_*).
-  struct Timing {
-    bool on = false;
-    std::vector<std::string> names;
-    std::vector<double> total_ms;
-    std::vector<int64_t> count;
-    struct Pending {
-      int cat;
-      hipEvent_t a, b;
-    };
-    std::vector<Pending> pending;
-    std::vector<hipEvent_t> pool;
-    int category(const char* n) {
-      for (size_t i = 0; i < names.size(); ++i)
-        if (names[i] == n) return (int)i;
-      names.emplace_back(n);
-      total_ms.push_back(0.0);
-      count.push_back(0);
-      return (int)names.size() - 1;
-    }
-    hipError_t event(hipEvent_t* e) {
-      if (!pool.empty()) {
-        *e = pool.back();
-        pool.pop_back();
-        return hipSuccess;
-      }
-      return hipEventCreate(e);
-    }
-    hipError_t flush() {
-      for (auto& p : pending) {
-        hipError_t err = hipEventSynchronize(p.b);
-        if (err != hipSuccess) return err;
-        float ms = 0.f;
-        err = hipEventElapsedTime(&ms, p.a, p.b);
-        if (err != hipSuccess) return err;
-        total_ms[p.cat] += ms;
-        count[p.cat] += 1;
-        pool.push_back(p.a);
-        pool.push_back(p.b);
-      }
-      pending.clear();
-      return hipSuccess;
-    }
-    void release() {
-      (void)flush();
-      for (auto e : pool) (void)hipEventDestroy(e);
-      pool.clear();
-    }
-  } timing;
-};
+}  // namespace tcl
 
 namespace {
 
-uint16_t host_bf16(float f) {
-  uint32_t u;
-  std::memcpy(&u, &f, 4);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-float round_bf16(float f) {
-  const uint32_t u = (uint32_t)host_bf16(f) << 16;
-  float r;
-  std::memcpy(&r, &u, 4);
-  return r;
-}
-
-// Derive the kernel layouts from the master blob and upload them:
-//  - fp32 models: W_in gets the pre-norm gain folded in, RMSNorm(h; g) W_in^T
-//    = rstd(h) * h (W_in diag(g))^T, so the in_proj GEMM only needs rstd.
-//  - bf16 models: every weight is rounded to bf16 (nearest-even) first; the
-//    projections are stored as bf16 (W0 zero-padded in K to a multiple of 8)
-//    and the gain is applied to the activations, not folded into W_in.
-//  - W1 is stored transposed for coalesced reads in the head.
-tcl_status upload(tcl_model* m) {
-  const tcl_config& c = m->cfg;
-  const bool bf = c.dtype == TCL_BF16;
-  const BlobLayout bl = blob_layout(c);
-  std::vector<float> work(m->master);
-  if (bf)
-    for (auto& v : work) v = round_bf16(v);
-  const float* P = work.data();
-  const size_t d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank;
-  const size_t F = c.F, h = c.head_hidden;
-  const size_t ldw0h = (F + 7) & ~size_t(7);
-
-  std::vector<uint8_t> host;
-  auto put = [&](size_t bytes) {
-    const size_t off = host.size();
-    host.resize(align256(off + bytes), 0);
-    return off;
+// Plan of the model's device block: every derived layout, then the master
+// blob, then the job table that derives the former from the latter.
+struct ModelPlan {
+  std::vector<DeriveJob> jobs;
+  int64_t total = 0;
+  size_t bytes = 0, master = 0, jobtab = 0;
+  size_t W0 = 0, b0 = 0, W0_h = 0, g_f = 0, W1 = 0, W1T = 0, b1 = 0, W2 = 0, b2 = 0;
+  struct L {
+    size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
+    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h;
   };
-  auto f32 = [&](size_t off) { return reinterpret_cast<float*>(host.data() + off); };
-  auto b16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(host.data() + off); };
-  auto copy = [&](size_t src, size_t n) {
-    const size_t o = put(n * 4);
-    std::memcpy(host.data() + o, P + src, n * 4);
-    return o;
-  };
-  auto copy_h = [&](size_t src, size_t rows, size_t cols, size_t ld) {
-    const size_t o = put(rows * ld * 2);
-    for (size_t r = 0; r < rows; ++r)
-      for (size_t k = 0; k < cols; ++k) b16(o)[r * ld + k] = host_bf16(P[src + r * cols + k]);
-    return o;
-  };
-
-  const size_t oW0 = copy(bl.W0, d * F), ob0 = copy(bl.b0, d);
-  const size_t oW0h = bf ? copy_h(bl.W0, d, F, ldw0h) : 0;
-  struct LO { size_t W_in, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out, g, W_in_h, W_x_h, W_out_h; };
-  std::vector<LO> lo;
-  for (int l = 0; l < c.n_layers; ++l) {
-    const auto& L = bl.layers[l];
-    LO o{};
-    o.W_in = put(2 * E * d * 4);
-    for (size_t j = 0; j < 2 * E; ++j)
-      for (size_t k = 0; k < d; ++k)
-        f32(o.W_in)[j * d + k] = (float)((double)P[L.W_in + j * d + k] * (double)P[L.g + k]);
-    o.conv_w = copy(L.conv_w, E * K);
-    o.conv_b = copy(L.conv_b, E);
-    o.W_x = copy(L.W_x, (R + 2 * N) * E);
-    o.W_dt = copy(L.W_dt, E * R);
-    o.b_dt = copy(L.b_dt, E);
-    o.A_log = copy(L.A_log, E * N);
-    o.D = copy(L.D, E);
-    o.W_out = copy(L.W_out, d * E);
-    o.g = copy(L.g, d);
-    if (bf) {
-      o.W_in_h = copy_h(L.W_in, 2 * E, d, d);
-      o.W_x_h = copy_h(L.W_x, R + 2 * N, E, E);
-      o.W_out_h = copy_h(L.W_out, d, E, E);
-    }
-    lo.push_back(o);
-  }
-  const size_t og = copy(bl.g_f, d);
-  const size_t oW1T = put(d * h * 4);
-  for (size_t j = 0; j < h; ++j)
-    for (size_t k = 0; k < d; ++k) f32(oW1T)[k * h + j] = P[bl.W1 + j * d + k];
-  const size_t ob1 = copy(bl.b1, h), oW2 = copy(bl.W2, h), ob2 = copy(bl.b2, 1);
-
-  const size_t bytes = host.size();
-  if (m->dev && m->dev_bytes != bytes) {
-    (void)hipFree(m->dev);
-    m->dev = nullptr;
-  }
-  if (!m->dev) {
-    if (hipMalloc(&m->dev, bytes) != hipSuccess) {
-      m->dev = nullptr;
-      return fail(TCL_ERR_OOM, "hipMalloc of %zu bytes for the weights failed", bytes);
-    }
-    m->dev_bytes = bytes;
-  }
-  TCL_HIP(hipMemcpy(m->dev, host.data(), bytes, hipMemcpyHostToDevice));
-  uint8_t* base = static_cast<uint8_t*>(m->dev);
-  auto F32 = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
-  auto B16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
-  m->W0 = F32(oW0);
-  m->b0 = F32(ob0);
-  m->W0_h = bf ? B16(oW0h) : nullptr;
-  m->ldw0_h = (int)ldw0h;
-  m->layers.clear();
-  for (int l = 0; l < c.n_layers; ++l) {
-    tcl_model::Layer L{};
-    L.W_in = F32(lo[l].W_in);
-    L.conv_w = F32(lo[l].conv_w);
-    L.conv_b = F32(lo[l].conv_b);
-    L.W_x = F32(lo[l].W_x);
-    L.W_dt = F32(lo[l].W_dt);
-    L.b_dt = F32(lo[l].b_dt);
-    L.A_log = F32(lo[l].A_log);
-    L.D = F32(lo[l].D);
-    L.W_out = F32(lo[l].W_out);
-    L.g = F32(lo[l].g);
-    if (bf) {
-      L.W_in_h = B16(lo[l].W_in_h);
-      L.W_x_h = B16(lo[l].W_x_h);
-      L.W_out_h = B16(lo[l].W_out_h);
-    }
-    m->layers.push_back(L);
-  }
-  m->g_f = F32(og);
-  m->W1T = F32(oW1T);
-  m->b1 = F32(ob1);
-  m->W2 = F32(oW2);
-  m->b2 = F32(ob2);
-  return TCL_OK;
-}
-
-// Workspace plan of one scoring call (byte offsets, 256-aligned).
-struct ScorePlan {
-  size_t offs, H, xz, u, xdbl, total;
+  std::vector<L> layers;
+  int ldw0_h = 0;
 };
 
-ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L) {
-  ScorePlan p;
-  const int64_t rows = B * L;
-  const int64_t XW = c.dt_rank + 2 * c.d_state;
-  const size_t act = c.dtype == TCL_BF16 ? 2 : 4;  // bytes per stored activation
+// Derived layouts:
+//  - fp32 copies of every tensor (bf16-rounded for bf16 models);
+//  - W_in with the pre-norm gain folded in, RMSNorm(h; g) W_in^T =
+//    rstd(h) * h (W_in diag(g))^T, for the fp32 in_proj (rstd only);
+//  - transposed fp32 copies of W_out, W_x, W_in, W_dt (backward GEMMs) and W1
+//    (coalesced head reads);
+//  - bf16 copies of the projections for bf16 models, W0 zero-padded in K to
+//    a multiple of 8 (the padding is zeroed once at create).
+ModelPlan plan_model(const tcl_config& c) {
+  ModelPlan P;
+  const BlobLayout bl = blob_layout(c);
+  const bool bf = c.dtype == TCL_BF16;
+  const int d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank, XW = R + 2 * N;
+  const int F = c.F, h = c.head_hidden;
+  P.ldw0_h = (F + 7) & ~7;
   size_t o = 0;
-  p.offs = o; o = align256(o + (size_t)(B + 1) * 4);
-  p.H = o; o = align256(o + (size_t)rows * c.d_model * 4);
-  p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * act);
-  p.u = o; o = align256(o + (size_t)rows * c.d_inner * act);
-  p.xdbl = o; o = align256(o + (size_t)rows * XW * 4);
-  p.total = o;
-  return p;
+  auto job = [&](size_t src, int rows, int cols, int kind, int transpose, int elem_bytes, int ld = -1,
+                 size_t src2 = 0) {
+    const size_t dst = o;
+    const int ldd = ld > 0 ? ld : (transpose ? rows : cols);
+    const size_t n_out = transpose ? (size_t)cols * ldd : (size_t)rows * ldd;
+    o = align256(o + n_out * elem_bytes);
+    DeriveJob J{};
+    J.start = P.total;
+    J.src = (int64_t)src;
+    J.src2 = (int64_t)src2;
+    J.dst = (int64_t)dst;
+    J.rows = rows;
+    J.cols = cols;
+    J.ld = ldd;
+    J.transpose = transpose;
+    J.kind = kind;
+    P.jobs.push_back(J);
+    P.total += (int64_t)rows * cols;
+    return dst;
+  };
+  P.W0 = job(bl.W0, d, F, kDeriveF32, 0, 4);
+  P.b0 = job(bl.b0, 1, d, kDeriveF32, 0, 4);
+  if (bf) P.W0_h = job(bl.W0, d, F, kDeriveBF16, 0, 2, P.ldw0_h);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const auto& B = bl.layers[l];
+    ModelPlan::L L{};
+    L.W_in_fold = job(B.W_in, 2 * E, d, kDeriveFold, 0, 4, -1, B.g);
+    L.g = job(B.g, 1, d, kDeriveF32, 0, 4);
+    L.conv_w = job(B.conv_w, E, K, kDeriveF32, 0, 4);
+    L.conv_b = job(B.conv_b, 1, E, kDeriveF32, 0, 4);
+    L.W_x = job(B.W_x, XW, E, kDeriveF32, 0, 4);
+    L.W_dt = job(B.W_dt, E, R, kDeriveF32, 0, 4);
+    L.b_dt = job(B.b_dt, 1, E, kDeriveF32, 0, 4);
+    L.A_log = job(B.A_log, E, N, kDeriveF32, 0, 4);
+    L.D = job(B.D, 1, E, kDeriveF32, 0, 4);
+    L.W_out = job(B.W_out, d, E, kDeriveF32, 0, 4);
+    L.W_outT = job(B.W_out, d, E, kDeriveF32, 1, 4);
+    L.W_xT = job(B.W_x, XW, E, kDeriveF32, 1, 4);
+    L.W_inT = job(B.W_in, 2 * E, d, kDeriveF32, 1, 4);
+    L.W_dtT = job(B.W_dt, E, R, kDeriveF32, 1, 4);
+    if (bf) {
+      L.W_in_h = job(B.W_in, 2 * E, d, kDeriveBF16, 0, 2);
+      L.W_x_h = job(B.W_x, XW, E, kDeriveBF16, 0, 2);
+      L.W_out_h = job(B.W_out, d, E, kDeriveBF16, 0, 2);
+    }
+    P.layers.push_back(L);
+  }
+  P.g_f = job(bl.g_f, 1, d, kDeriveF32, 0, 4);
+  P.W1 = job(bl.W1, h, d, kDeriveF32, 0, 4);
+  P.W1T = job(bl.W1, h, d, kDeriveF32, 1, 4);
+  P.b1 = job(bl.b1, 1, h, kDeriveF32, 0, 4);
+  P.W2 = job(bl.W2, 1, h, kDeriveF32, 0, 4);
+  P.b2 = job(bl.b2, 1, 1, kDeriveF32, 0, 4);
+  P.master = o;
+  o = align256(o + bl.total * 4);
+  P.jobtab = o;
+  o = align256(o + P.jobs.size() * sizeof(DeriveJob));
+  P.bytes = o;
+  return P;
+}
+
+// Upload a host blob into the model's master and derive every layout.
+// Synchronous.
+tcl_status load_params(tcl_model* m, const float* h_params) {
+  TCL_HIP(hipMemcpy(m->master, h_params, m->n_params * 4, hipMemcpyHostToDevice));
+  tcl_status st = derive_weights(m, nullptr);
+  if (st != TCL_OK) return st;
+  TCL_HIP(hipStreamSynchronize(nullptr));
+  return TCL_OK;
 }
 
 }  // namespace
@@ -352,7 +335,7 @@ TCL_API size_t tcl_param_count(const tcl_config* cfg) {
   return blob_layout(*cfg).total;
 }
 
-TCL_API const char* tcl_last_error(void) { return g_err.c_str(); }
+TCL_API const char* tcl_last_error(void) { return last_error(); }
 
 TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_params,
                                          size_t n_params, tcl_model** out) {
@@ -366,17 +349,70 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
     return fail(TCL_ERR_INVALID_ARG, "parameter blob has %zu values, config needs %zu", n_params, need);
   tcl_model* m = new tcl_model();
   m->cfg = *cfg;
+  m->n_params = n_params;
   if (hipGetDevice(&m->device) != hipSuccess) {
     delete m;
     return fail(TCL_ERR_HIP, "hipGetDevice failed");
   }
-  m->master.assign(h_params, h_params + n_params);
-  st = upload(m);
-  if (st != TCL_OK) {
-    if (m->dev) (void)hipFree(m->dev);
+  const ModelPlan P = plan_model(*cfg);
+  if (hipMalloc(&m->dev, P.bytes) != hipSuccess) {
     delete m;
-    return st;
+    return fail(TCL_ERR_OOM, "hipMalloc of %zu bytes for the weights failed", P.bytes);
   }
+  m->dev_bytes = P.bytes;
+  uint8_t* base = static_cast<uint8_t*>(m->dev);
+  auto F32 = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
+  auto B16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(base + off); };
+  const bool bf = cfg->dtype == TCL_BF16;
+  m->master = F32(P.master);
+  m->jobs = reinterpret_cast<DeriveJob*>(base + P.jobtab);
+  m->njobs = (int)P.jobs.size();
+  m->derive_total = P.total;
+  m->W0 = F32(P.W0);
+  m->b0 = F32(P.b0);
+  m->W0_h = bf ? B16(P.W0_h) : nullptr;
+  m->ldw0_h = P.ldw0_h;
+  for (const auto& L : P.layers) {
+    tcl_model::Layer W{};
+    W.W_in_fold = F32(L.W_in_fold);
+    W.g = F32(L.g);
+    W.conv_w = F32(L.conv_w);
+    W.conv_b = F32(L.conv_b);
+    W.W_x = F32(L.W_x);
+    W.W_dt = F32(L.W_dt);
+    W.b_dt = F32(L.b_dt);
+    W.A_log = F32(L.A_log);
+    W.D = F32(L.D);
+    W.W_out = F32(L.W_out);
+    W.W_outT = F32(L.W_outT);
+    W.W_xT = F32(L.W_xT);
+    W.W_inT = F32(L.W_inT);
+    W.W_dtT = F32(L.W_dtT);
+    if (bf) {
+      W.W_in_h = B16(L.W_in_h);
+      W.W_x_h = B16(L.W_x_h);
+      W.W_out_h = B16(L.W_out_h);
+    }
+    m->layers.push_back(W);
+  }
+  m->g_f = F32(P.g_f);
+  m->W1 = F32(P.W1);
+  m->W1T = F32(P.W1T);
+  m->b1 = F32(P.b1);
+  m->W2 = F32(P.W2);
+  m->b2 = F32(P.b2);
+  auto cleanup = [&](tcl_status s2) {
+    (void)hipFree(m->dev);
+    delete m;
+    return s2;
+  };
+  // zero the block once: padding (W0's bf16 K tail) is never written again
+  if (hipMemset(m->dev, 0, P.bytes) != hipSuccess) return cleanup(fail(TCL_ERR_HIP, "hipMemset failed"));
+  if (hipMemcpy(m->jobs, P.jobs.data(), P.jobs.size() * sizeof(DeriveJob), hipMemcpyHostToDevice) !=
+      hipSuccess)
+    return cleanup(fail(TCL_ERR_HIP, "upload of the derivation table failed"));
+  st = load_params(m, h_params);
+  if (st != TCL_OK) return cleanup(st);
   *out = m;
   return TCL_OK;
 }
@@ -391,18 +427,19 @@ TCL_API tcl_status tcl_cost_model_destroy(tcl_model* m) {
 
 TCL_API tcl_status tcl_get_params(const tcl_model* m, float* h_out, size_t n) {
   if (!m || !h_out) return fail(TCL_ERR_INVALID_ARG, "NULL argument");
-  if (n != m->master.size())
-    return fail(TCL_ERR_INVALID_ARG, "buffer has %zu values, model has %zu", n, m->master.size());
-  std::memcpy(h_out, m->master.data(), n * 4);
+  if (n != m->n_params)
+    return fail(TCL_ERR_INVALID_ARG, "buffer has %zu values, model has %zu", n, m->n_params);
+  TCL_HIP(hipDeviceSynchronize());
+  TCL_HIP(hipMemcpy(h_out, m->master, n * 4, hipMemcpyDeviceToHost));
   return TCL_OK;
 }
 
 TCL_API tcl_status tcl_set_params(tcl_model* m, const float* h_params, size_t n) {
   if (!m || !h_params) return fail(TCL_ERR_INVALID_ARG, "NULL argument");
-  if (n != m->master.size())
-    return fail(TCL_ERR_INVALID_ARG, "blob has %zu values, model has %zu", n, m->master.size());
-  m->master.assign(h_params, h_params + n);
-  return upload(m);
+  if (n != m->n_params)
+    return fail(TCL_ERR_INVALID_ARG, "blob has %zu values, model has %zu", n, m->n_params);
+  TCL_HIP(hipDeviceSynchronize());
+  return load_params(m, h_params);
 }
 
 TCL_API size_t tcl_score_workspace_bytes(const tcl_model* m, int32_t B, int32_t L) {
@@ -421,85 +458,11 @@ TCL_API tcl_status tcl_score(tcl_model* m, int32_t B, int32_t L, const float* d_
     return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
   if (reinterpret_cast<uintptr_t>(d_feats) % 16 || reinterpret_cast<uintptr_t>(d_ws) % 256)
     return fail(TCL_ERR_INVALID_ARG, "d_feats must be 16-byte and d_workspace 256-byte aligned");
-  const tcl_config& c = m->cfg;
-  const ScorePlan p = score_plan(c, B, L);
+  const ScorePlan p = score_plan(m->cfg, B, L);
   if (ws_bytes < p.total)
     return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, p.total);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(d_ws);
-  int* offs = reinterpret_cast<int*>(ws + p.offs);
-  float* H = reinterpret_cast<float*>(ws + p.H);
-  float* xdbl = reinterpret_cast<float*>(ws + p.xdbl);
-  const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
-  const int Mmax = B * L;
-
-  TCL_LAUNCH(m, "offsets", launch_offsets(d_lengths, B, L, offs, s));
-  if (c.dtype == TCL_F32) {
-    float* xz = reinterpret_cast<float*>(ws + p.xz);
-    float* u = reinterpret_cast<float*>(ws + p.u);
-    GemmArgs g;
-    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
-    g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
-    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
-    TCL_LAUNCH(m, "gemm_input", launch_gemm_f32(g, kBias | kGather, kWide, s));
-
-    for (int l = 0; l < c.n_layers; ++l) {
-      const auto& W = m->layers[l];
-      GemmArgs gi;
-      gi.A = H; gi.lda = d; gi.W = W.W_in; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
-      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-      TCL_LAUNCH(m, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, kWide, s));
-
-      TCL_LAUNCH(m, "conv_silu", launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w,
-                                                         W.conv_b, u, s));
-      GemmArgs gx;
-      gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
-      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-      TCL_LAUNCH(m, "gemm_x_proj", launch_gemm_f32(gx, 0, kNarrow, s));
-
-      TCL_LAUNCH(m, "scan", launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                               W.b_dt, W.A_log, W.D, u, s));
-      GemmArgs go;
-      go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
-      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-      TCL_LAUNCH(m, "gemm_out_proj", launch_gemm_f32(go, kResid, kWide, s));
-    }
-  } else {
-    uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
-    uint16_t* u = reinterpret_cast<uint16_t*>(ws + p.u);
-    GemmArgsBF16 g;
-    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
-    g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
-    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
-    TCL_LAUNCH(m, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, s));
-
-    for (int l = 0; l < c.n_layers; ++l) {
-      const auto& W = m->layers[l];
-      GemmArgsBF16 gi;
-      gi.A = H; gi.lda = d; gi.W = W.W_in_h; gi.ldw = d; gi.gain = W.g; gi.C = xz; gi.ldc = 2 * E;
-      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-      TCL_LAUNCH(m, "gemm_in_proj", launch_gemm_bf16(gi, kNormF32toBF16, s));
-
-      TCL_LAUNCH(m, "conv_silu", launch_conv_silu<uint16_t>(B, E, c.d_conv, offs, xz, 2 * E,
-                                                            W.conv_w, W.conv_b, u, s));
-      GemmArgsBF16 gx;
-      gx.A = u; gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
-      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-      TCL_LAUNCH(m, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32Narrow, s));
-
-      TCL_LAUNCH(m, "scan", launch_scan<uint16_t>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                                  W.b_dt, W.A_log, W.D, u, s));
-      GemmArgsBF16 go;
-      go.A = u; go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = H; go.ldc = d;
-      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-      TCL_LAUNCH(m, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, s));
-    }
-  }
-
-  TCL_LAUNCH(m, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
-                                        c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2, m->b2,
-                                        d_scores, s));
-  return TCL_OK;
+  return run_score(m, B, L, d_feats, d_lengths, d_scores, static_cast<char*>(d_ws),
+                   static_cast<hipStream_t>(stream));
 }
 
 // ------------------------------------------------------------------ timing
@@ -551,6 +514,20 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
   return TCL_OK;
 }
 
+TCL_API tcl_status tcl_test_gemm_bf16(int32_t M, int32_t N, int32_t K, const uint16_t* d_A,
+                                      const uint16_t* d_W, const float* d_bias, float* d_C,
+                                      void* stream) {
+  if (M <= 0 || N <= 0 || K <= 0 || K % 8) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
+  if (!d_A || !d_W || !d_C) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_A) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
+    return fail(TCL_ERR_INVALID_ARG, "A and W must be 16-byte aligned");
+  GemmArgsBF16 g;
+  g.A = d_A; g.lda = K; g.W = d_W; g.ldw = K; g.bias = d_bias; g.C = d_C; g.ldc = N;
+  g.Mmax = M; g.N = N; g.K = K;
+  TCL_HIP(launch_gemm_bf16(g, d_bias ? kBF16toF32Bias : kBF16toF32, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
 TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const int32_t* d_offs,
                                           const float* d_x, int32_t ldx, const float* d_w,
                                           const float* d_b, float* d_u, void* stream) {
@@ -574,19 +551,5 @@ TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R,
     return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
   TCL_HIP(launch_scan<float>(B, E, N, R, d_offs, d_u, d_xdbl, d_z, ldz, d_W_dt, d_b_dt, d_A_log,
                              d_D, d_out, static_cast<hipStream_t>(stream)));
-  return TCL_OK;
-}
-
-TCL_API tcl_status tcl_test_gemm_bf16(int32_t M, int32_t N, int32_t K, const uint16_t* d_A,
-                                      const uint16_t* d_W, const float* d_bias, float* d_C,
-                                      void* stream) {
-  if (M <= 0 || N <= 0 || K <= 0 || K % 8) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
-  if (!d_A || !d_W || !d_C) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
-  if (reinterpret_cast<uintptr_t>(d_A) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
-    return fail(TCL_ERR_INVALID_ARG, "A and W must be 16-byte aligned");
-  GemmArgsBF16 g;
-  g.A = d_A; g.lda = K; g.W = d_W; g.ldw = K; g.bias = d_bias; g.C = d_C; g.ldc = N;
-  g.Mmax = M; g.N = N; g.K = K;
-  TCL_HIP(launch_gemm_bf16(g, d_bias ? kBF16toF32Bias : kBF16toF32, static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }

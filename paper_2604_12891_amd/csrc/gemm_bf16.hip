@@ -212,7 +212,8 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_bf16_kernel(GemmArgsBF16 p, 
         v += bias;
         TC* dst = reinterpret_cast<TC*>(p.C) + (int64_t)row * p.ldc + col;
         if constexpr (sizeof(TC) == 4) {
-          if constexpr ((FL & kResid) != 0) v += *reinterpret_cast<float*>(dst);
+          if constexpr ((FL & kResid) != 0)
+            v += p.R ? p.R[(int64_t)row * p.ldc + col] : *reinterpret_cast<float*>(dst);
           *reinterpret_cast<float*>(dst) = v;
         } else {
           *reinterpret_cast<uint16_t*>(dst) = f32_to_bf16(v);
@@ -250,6 +251,8 @@ hipError_t launch_gemm_bf16(const GemmArgsBF16& a, GemmBF16Kind kind, hipStream_
       return launch_t<uint16_t, float, 2, 2, 2, 2, 0>(a, s);
     case kBF16toF32Bias:
       return launch_t<uint16_t, float, 2, 2, 2, 2, kBias>(a, s);
+    case kBF16toBF16:
+      return launch_t<uint16_t, uint16_t, 2, 2, 2, 2, 0>(a, s);
   }
   return hipErrorInvalidValue;
 }

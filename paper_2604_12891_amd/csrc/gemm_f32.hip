@@ -197,7 +197,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_f32_kernel(GemmArgs p, int n
         if constexpr (kNorm) v *= sR[rl];
         v += bias;
         float* dst = p.C + (int64_t)row * p.ldc + col;
-        if constexpr ((FL & kResid) != 0) v += *dst;
+        if constexpr ((FL & kResid) != 0) v += p.R ? p.R[(int64_t)row * p.ldc + col] : *dst;
         *dst = v;
       }
     }

@@ -27,6 +27,7 @@ struct GemmArgs {
   const float* bias = nullptr;
   float* C = nullptr;
   int64_t ldc = 0;
+  const float* R = nullptr;   // residual source for kResid (null: C itself), leading dim ldc
   const int* Mdev = nullptr;  // device row count (null: use Mmax)
   int Mmax = 0;               // upper bound on the row count (grid size)
   int N = 0, K = 0;
@@ -54,6 +55,7 @@ struct GemmArgsBF16 {
   const float* gain = nullptr;
   void* C = nullptr;
   int64_t ldc = 0;
+  const float* R = nullptr;   // residual source for kResid (null: C itself), leading dim ldc
   const int* Mdev = nullptr;
   int Mmax = 0;
   int N = 0, K = 0;
@@ -67,9 +69,31 @@ enum GemmBF16Kind {
   kBF16ResidF32,     // bf16 -> fp32 C += result
   kBF16toF32,        // bf16 -> fp32
   kBF16toF32Bias,    // bf16 -> fp32, + bias
+  kBF16toBF16,       // bf16 -> bf16
 };
 
 hipError_t launch_gemm_bf16(const GemmArgsBF16& a, GemmBF16Kind kind, hipStream_t s);
+
+// ---------------------------------------------------------------- weight-gradient GEMM
+// P[s][i][j] = sum over tokens m of split s of A[m, i] * B[m, j]
+// (A: [M, NI] fp32 with leading dimension lda; B: [M, NJ] fp32 or bf16, or
+// fp32 gathered from a padded [B, L, ldb] tensor by token offsets).
+// P holds `splits` partial [NI, NJ] tiles; sum them with launch_reduce.
+struct GemmTNArgs {
+  const float* A = nullptr;
+  int64_t lda = 0;
+  const void* Bm = nullptr;
+  int64_t ldb = 0;
+  const int* offs = nullptr;  // gather: token offsets of B's programs
+  int B = 0, L = 0;
+  float* P = nullptr;
+  const int* Mdev = nullptr;
+  int Mmax = 0;
+  int NI = 0, NJ = 0;
+};
+enum TNKind { kTN_F32_F32, kTN_F32_BF16, kTN_F32_GatherF32 };
+int gemm_tn_splits(int Mmax, int NI, int NJ);
+hipError_t launch_gemm_tn(const GemmTNArgs& a, TNKind kind, int splits, hipStream_t s);
 
 // ---------------------------------------------------------------- per-program kernels
 // offs[b] = sum of valid lengths before b; offs[B] = total packed rows.
@@ -88,16 +112,80 @@ hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, in
 // Selective scan with dt_proj+softplus prologue, D skip and SiLU(z) gate.
 // xdbl rows ([dt_r | B | C], R + 2N values) are fp32. out may alias u (each
 // element is read then written by the same thread).
+// ysave (optional): the pre-gate output y, for the backward pass.
 template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
-                       const float* D, T* out, hipStream_t s);
+                       const float* D, T* out, hipStream_t s, T* ysave = nullptr);
 
 // Final RMSNorm (optional) + masked mean-pool + Linear-ReLU-Linear head.
 // W1T is W1 transposed ([d, h]). Programs with invalid lengths get NaN.
+// pooled_out [B, d] and a1_out [B, h] (optional) keep the pooled vector and
+// the head's pre-ReLU activation for the backward pass.
 hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const int* lengths,
                            const float* H, const float* g_f, int final_norm, float eps,
                            const float* W1T, const float* b1, const float* W2, const float* b2,
-                           float* scores, hipStream_t s);
+                           float* scores, hipStream_t s, float* pooled_out = nullptr,
+                           float* a1_out = nullptr);
+
+// ---------------------------------------------------------------- distillation step
+// Reductions of per-block partials: dst[i * dst_stride] =
+// sum_s src[s * split_stride + i * src_stride], i < n. Offsets are in floats,
+// relative to the workspace (src) and to the gradient blob or the loss
+// vector (dst), so a job table depends only on the batch shape.
+struct ReduceJob {
+  int64_t src, split_stride, src_stride;
+  int64_t dst, dst_stride;
+  int64_t n;
+  int32_t nsplit;
+  int32_t dst_buf;  // 0: gradient blob, 1: loss vector
+};
+hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, const float* ws,
+                         float* grad, float* loss, hipStream_t s);
+
+// Weight layouts derived from the fp32 master blob: one flat index space over
+// all jobs (job j covers [start_j, start_j + rows*cols)); the destination is a
+// byte offset in the model's device block. kDeriveFold multiplies column c by
+// master[src2 + c]. With round_bf16 every master value is first rounded to
+// bf16 (bf16 models compute with the rounded weights).
+enum DeriveKind { kDeriveF32 = 0, kDeriveBF16 = 1, kDeriveFold = 2 };
+struct DeriveJob {
+  int64_t start, src, src2, dst;
+  int32_t rows, cols, ld, transpose, kind, pad_;
+};
+hipError_t launch_derive(const float* master, const DeriveJob* d_jobs, int njobs, int64_t total,
+                         void* base, int round_bf16, hipStream_t s);
+
+hipError_t launch_rmsnorm_fwd(int d, int Mmax, const int* Mdev, const float* H, const float* g,
+                              float eps, uint16_t* n, float* rstd, hipStream_t s);
+int rmsnorm_bwd_blocks(int Mmax);
+hipError_t launch_rmsnorm_bwd(int d, int Mmax, const int* Mdev, const float* dN, const float* H,
+                              const float* rstd, const float* g, float* dH, float* dg_part,
+                              hipStream_t s);
+int loss_head_blocks(int B);
+// part: [blocks][2h + 4] = dW2 (h) | db1 (h) | db2 | mse_t | mse_l | total
+hipError_t launch_loss_head_bwd(int B, int d, int h, const float* s, const float* t, const float* y,
+                                const float* a1, const float* W1, const float* W2, float* da1,
+                                float* dpooled, float* part, hipStream_t st);
+// dg_part: [B][d]
+hipError_t launch_normf_pool_bwd(int B, int d, const int* offs, const float* H, const float* g_f,
+                                 int final_norm, float eps, const float* dpooled, float* dH,
+                                 float* dg_part, hipStream_t s);
+size_t scan_bwd_ckpt_floats(int B, int E, int L, int N);
+// dA_part: [B][E][N] (already d/dA_log), dD_part: [B][E]
+hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, const uint16_t* u,
+                           const float* xdbl, const uint16_t* xz, const uint16_t* ysave,
+                           const float* dyg, const float* W_dt, const float* b_dt,
+                           const float* A_log, const float* D, float* ckpt, float* dv, float* du,
+                           float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s);
+// part: [B][K+1][E] = dw (K rows) | db
+hipError_t launch_conv_bwd(int B, int E, int K, const int* offs, const uint16_t* x, int ldx,
+                           const float* w, const float* b, const float* du, float* dx, int lddx,
+                           float* part, hipStream_t s);
+int colsum_splits(int Mmax);
+hipError_t launch_colsum(const int* Mdev, int Mmax, const float* A, int64_t lda, int C, int splits,
+                         float* part, hipStream_t s);
+hipError_t launch_adam(int64_t n, float* p, float* m, float* v, const float* g, float lr, float b1,
+                       float b2, float eps, float bc1, float bc2, hipStream_t s);
 
 }  // namespace tcl

@@ -1,0 +1,120 @@
+// Host-side model state shared by the scoring and training entry points
+// (internal to libtcl).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "tcl.h"
+
+namespace tcl {
+
+tcl_status fail(tcl_status st, const char* fmt, ...);
+const char* last_error();
+
+#define TCL_HIP(call)                                                                          \
+  do {                                                                                         \
+    hipError_t e_ = (call);                                                                    \
+    if (e_ != hipSuccess) return ::tcl::fail(TCL_ERR_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
+  } while (0)
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Offsets (in floats) of every tensor of the canonical parameter blob.
+struct BlobLayout {
+  size_t W0, b0, g_f, W1, b1, W2, b2, total;
+  struct L {
+    size_t g, W_in, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
+  };
+  std::vector<L> layers;
+};
+BlobLayout blob_layout(const tcl_config& c);
+
+// Per-kernel event timing (tcl_timing_*).
+struct Timing {
+  bool on = false;
+  std::vector<std::string> names;
+  std::vector<double> total_ms;
+  std::vector<int64_t> count;
+  struct Pending {
+    int cat;
+    hipEvent_t a, b;
+  };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+  int category(const char* n);
+  hipError_t event(hipEvent_t* e);
+  hipError_t flush();
+  void release();
+};
+
+// Launch CALL (a hipError_t expression) on stream `s`; with timing enabled,
+// bracket it by events on that stream under category NAME.
+#define TCL_LAUNCH(TIMING, NAME, CALL)                                                \
+  do {                                                                                \
+    hipEvent_t ea_ = nullptr, eb_ = nullptr;                                          \
+    if ((TIMING).on) {                                                                \
+      TCL_HIP((TIMING).event(&ea_));                                                  \
+      TCL_HIP(hipEventRecord(ea_, s));                                                \
+    }                                                                                 \
+    TCL_HIP(CALL);                                                                    \
+    if ((TIMING).on) {                                                                \
+      TCL_HIP((TIMING).event(&eb_));                                                  \
+      TCL_HIP(hipEventRecord(eb_, s));                                                \
+      (TIMING).pending.push_back({(TIMING).category(NAME), ea_, eb_});                \
+    }                                                                                 \
+  } while (0)
+
+}  // namespace tcl
+
+// Device-side state of a model: one allocation holding every derived weight
+// layout, the fp32 master blob, and the table of derivation jobs.
+struct tcl_model {
+  tcl_config cfg{};
+  int device = 0;
+  size_t n_params = 0;
+  void* dev = nullptr;
+  size_t dev_bytes = 0;
+  float* master = nullptr;                 // canonical fp32 blob (device)
+  tcl::DeriveJob* jobs = nullptr;          // derivation table (device)
+  int njobs = 0;
+  int64_t derive_total = 0;
+  struct Layer {
+    // fp32 (bf16-rounded for bf16 models)
+    float *W_in_fold, *g, *conv_w, *conv_b, *W_x, *W_dt, *b_dt, *A_log, *D, *W_out;
+    // transposed fp32 copies for the backward pass
+    float *W_outT, *W_xT, *W_inT, *W_dtT;
+    // bf16 copies (bf16 models)
+    uint16_t *W_in_h, *W_x_h, *W_out_h;
+  };
+  float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1 = nullptr, *W1T = nullptr,
+        *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;
+  uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
+  int ldw0_h = 0;
+  std::vector<Layer> layers;
+  tcl::Timing timing;
+};
+
+namespace tcl {
+
+// Workspace plan of one scoring call (byte offsets, 256-aligned).
+struct ScorePlan {
+  size_t offs, H, xz, u, xdbl, total;
+};
+ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L);
+
+// Enqueue the scoring pass (no argument checks).
+tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
+                     float* d_scores, char* ws, hipStream_t s);
+
+// Re-derive every weight layout from the device master blob (stream-ordered).
+tcl_status derive_weights(tcl_model* m, hipStream_t s);
+
+tcl_status check_config(const tcl_config* c);
+
+}  // namespace tcl

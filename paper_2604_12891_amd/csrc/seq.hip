@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
     const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
     const T* __restrict__ z, int ldz, const float* __restrict__ W_dt,
     const float* __restrict__ b_dt, const float* __restrict__ A_log,
-    const float* __restrict__ Dp, T* out) {
+    const float* __restrict__ Dp, T* out, T* __restrict__ ysave) {
   constexpr int XW = R + 2 * N;
   __shared__ __attribute__((aligned(16))) float sX[kScanTC * XW];
   const int b = blockIdx.x;
@@ -211,6 +211,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
         y = fmaf(s[n], xr[R + N + n], y);
       }
       y = fmaf(Dv, uv, y);
+      if (ysave) st1(ysave + row * E + e, y);
       st1(out + row * E + e, y * silu(zv));
     }
   }
@@ -234,7 +235,9 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
                                                    const float* __restrict__ b1,
                                                    const float* __restrict__ W2,
                                                    const float* __restrict__ b2,
-                                                   float* __restrict__ scores) {
+                                                   float* __restrict__ scores,
+                                                   float* __restrict__ pooled_out,
+                                                   float* __restrict__ a1_out) {
   constexpr int PL = DM / 64;  // values per lane
   __shared__ float sP[DM][kTailPB];
   __shared__ float sRed[4][kTailPB];
@@ -273,6 +276,7 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
       const int k = lane * PL + i;
       const float g = final_norm ? g_f[k] : 1.f;
       sP[k][p] = acc[i] * g * inv;
+      if (pooled_out && b < B) pooled_out[(int64_t)b * DM + k] = acc[i] * g * inv;
     }
   }
   __syncthreads();
@@ -293,6 +297,11 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
     const float w2 = W2[tid];
 #pragma unroll
     for (int p = 0; p < kTailPB; ++p) part[p] = w2 * fmaxf(a[p], 0.f);
+    if (a1_out) {
+#pragma unroll
+      for (int p = 0; p < kTailPB; ++p)
+        if (b0 + p < B) a1_out[(int64_t)(b0 + p) * h + tid] = a[p];
+    }
   }
 #pragma unroll
   for (int p = 0; p < kTailPB; ++p) {
@@ -337,13 +346,13 @@ hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, in
 template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
-                       const float* D, T* out, hipStream_t s) {
+                       const float* D, T* out, hipStream_t s, T* ysave) {
   if (B <= 0) return hipSuccess;
   if (N != 16) return hipErrorInvalidValue;
   dim3 grid(B, (E + kScanThreads - 1) / kScanThreads);
 #define TCL_SCAN(RR)                                                                                 \
   hipLaunchKernelGGL((scan_kernel<T, 16, RR>), grid, dim3(kScanThreads), 0, s, offs, E, u, xdbl, z, \
-                     ldz, W_dt, b_dt, A_log, D, out)
+                     ldz, W_dt, b_dt, A_log, D, out, ysave)
   switch (R) {
     case 4: TCL_SCAN(4); break;
     case 8: TCL_SCAN(8); break;
@@ -365,22 +374,22 @@ template hipError_t launch_conv_silu<uint16_t>(int, int, int, const int*, const 
                                                const float*, const float*, uint16_t*, hipStream_t);
 template hipError_t launch_scan<float>(int, int, int, int, const int*, const float*, const float*,
                                        const float*, int, const float*, const float*, const float*,
-                                       const float*, float*, hipStream_t);
+                                       const float*, float*, hipStream_t, float*);
 template hipError_t launch_scan<uint16_t>(int, int, int, int, const int*, const uint16_t*,
                                           const float*, const uint16_t*, int, const float*,
                                           const float*, const float*, const float*, uint16_t*,
-                                          hipStream_t);
+                                          hipStream_t, uint16_t*);
 
 hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const int* lengths,
                            const float* H, const float* g_f, int final_norm, float eps,
                            const float* W1T, const float* b1, const float* W2, const float* b2,
-                           float* scores, hipStream_t s) {
+                           float* scores, hipStream_t s, float* pooled_out, float* a1_out) {
   if (B <= 0) return hipSuccess;
   if (h > 256) return hipErrorInvalidValue;
   dim3 grid((B + kTailPB - 1) / kTailPB);
 #define TCL_TAIL(DD)                                                                          \
   hipLaunchKernelGGL((tail_kernel<DD>), grid, dim3(256), 0, s, B, L, h, offs, lengths, H, g_f, \
-                     final_norm, eps, W1T, b1, W2, b2, scores)
+                     final_norm, eps, W1T, b1, W2, b2, scores, pooled_out, a1_out)
   switch (d) {
     case 64: TCL_TAIL(64); break;
     case 128: TCL_TAIL(128); break;

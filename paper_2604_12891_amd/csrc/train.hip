@@ -1,0 +1,667 @@
+// Kernels of the teacher -> student distillation step (forward with saved
+// activations, backward, Adam, weight refresh). Reverse-mode derivatives of
+// the model that the scoring kernels compute; tokens are packed program by
+// program as everywhere else, and every reduction over tokens or programs
+// goes through per-block partials summed in a fixed order (deterministic).
+#include "common.h"
+#include "kernels.h"
+
+namespace tcl {
+namespace {
+
+__device__ __forceinline__ float sigmoid_fast(float x) { return rcp_fast(1.0f + exp_fast(-x)); }
+
+// d/dx SiLU(x) = s (1 + x (1 - s)), s = sigmoid(x)
+__device__ __forceinline__ float silu_grad(float x) {
+  const float s = sigmoid_fast(x);
+  return s * (1.0f + x * (1.0f - s));
+}
+
+__device__ __forceinline__ float ld_act(const float* p) { return *p; }
+__device__ __forceinline__ float ld_act(const uint16_t* p) { return bf16_to_f32(*p); }
+
+// ---------------------------------------------------------------- RMSNorm forward
+// One wavefront per token row: n = bf16(h * r * g), r = (mean h^2 + eps)^-1/2.
+template <int DM>
+__global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const int* __restrict__ Mdev,
+                                                          const float* __restrict__ H,
+                                                          const float* __restrict__ g, float eps,
+                                                          uint16_t* __restrict__ n,
+                                                          float* __restrict__ rstd) {
+  constexpr int PL = DM / 64;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= *Mdev) return;
+  const float* hr = H + (int64_t)row * DM + lane * PL;
+  float v[PL], ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < PL; ++i) {
+    v[i] = hr[i];
+    ss = fmaf(v[i], v[i], ss);
+  }
+  ss = wave_sum(ss);
+  const float r = 1.0f / sqrtf(ss / (float)DM + eps);
+#pragma unroll
+  for (int i = 0; i < PL; ++i) n[(int64_t)row * DM + lane * PL + i] = f32_to_bf16(v[i] * r * g[lane * PL + i]);
+  if (lane == 0) rstd[row] = r;
+}
+
+// ---------------------------------------------------------------- RMSNorm backward
+// dH[row] += r (g dN) - (r^3 / d) h sum(g dN h); per-block partial of
+// dg = sum over rows of dN h r.
+template <int DM>
+__global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict__ Mdev,
+                                                          const float* __restrict__ dN,
+                                                          const float* __restrict__ H,
+                                                          const float* __restrict__ rstd,
+                                                          const float* __restrict__ g,
+                                                          float* __restrict__ dH,
+                                                          float* __restrict__ dg_part,
+                                                          int rows_per_block) {
+  constexpr int PL = DM / 64;
+  __shared__ float sdg[4][DM];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int M = *Mdev;
+  float dg[PL];
+#pragma unroll
+  for (int i = 0; i < PL; ++i) dg[i] = 0.f;
+  const int r0 = blockIdx.x * rows_per_block;
+  const int r1 = min(r0 + rows_per_block, M);
+  for (int row = r0 + wave; row < r1; row += 4) {
+    const int64_t o = (int64_t)row * DM + lane * PL;
+    const float r = rstd[row];
+    float h[PL], gd[PL], dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      h[i] = H[o + i];
+      const float dn = dN[o + i];
+      gd[i] = dn * g[lane * PL + i];
+      dot = fmaf(gd[i], h[i], dot);
+      dg[i] = fmaf(dn, h[i] * r, dg[i]);
+    }
+    dot = wave_sum(dot);
+    const float c = r * r * r / (float)DM * dot;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) dH[o + i] += r * gd[i] - c * h[i];
+  }
+#pragma unroll
+  for (int i = 0; i < PL; ++i) sdg[wave][lane * PL + i] = dg[i];
+  __syncthreads();
+  for (int k = threadIdx.x; k < DM; k += 256)
+    dg_part[(int64_t)blockIdx.x * DM + k] = sdg[0][k] + sdg[1][k] + sdg[2][k] + sdg[3][k];
+}
+
+// ---------------------------------------------------------------- loss + head backward
+// 16 programs per block. For program b: ds = (2/B)(2 s - t - y),
+// da1 = ds W2 (a1 > 0), dpooled = da1 W1. Per-block partials of
+// [dW2 (h) | db1 (h) | db2 | sum (s-t)^2 | sum (s-y)^2].
+constexpr int kHB = 16;
+__global__ __launch_bounds__(256) void loss_head_bwd_kernel(
+    int B, int d, int h, const float* __restrict__ s, const float* __restrict__ t,
+    const float* __restrict__ y, const float* __restrict__ a1, const float* __restrict__ W1,
+    const float* __restrict__ W2, float* __restrict__ da1, float* __restrict__ dpooled,
+    float* __restrict__ part) {
+  __shared__ float sda[kHB][256];
+  __shared__ float sds[kHB];
+  const int tid = threadIdx.x;
+  const int b0 = blockIdx.x * kHB;
+  const float inv = 2.0f / (float)B;
+  if (tid < kHB) {
+    const int b = b0 + tid;
+    sds[tid] = b < B ? inv * (2.0f * s[b] - t[b] - y[b]) : 0.f;
+  }
+  __syncthreads();
+  float pw2 = 0.f, pb1 = 0.f;
+  if (tid < h) {
+    const float w2 = W2[tid];
+    for (int p = 0; p < kHB; ++p) {
+      const int b = b0 + p;
+      float g = 0.f;
+      if (b < B) {
+        const float a = a1[(int64_t)b * h + tid];
+        g = a > 0.f ? sds[p] * w2 : 0.f;
+        pw2 = fmaf(sds[p], fmaxf(a, 0.f), pw2);
+        da1[(int64_t)b * h + tid] = g;
+      }
+      sda[p][tid] = g;
+      pb1 += g;
+    }
+  }
+  __syncthreads();
+  if (tid < d) {
+    float acc[kHB];
+#pragma unroll
+    for (int p = 0; p < kHB; ++p) acc[p] = 0.f;
+    for (int j = 0; j < h; ++j) {
+      const float w = W1[(int64_t)j * d + tid];
+#pragma unroll
+      for (int p = 0; p < kHB; ++p) acc[p] = fmaf(sda[p][j], w, acc[p]);
+    }
+#pragma unroll
+    for (int p = 0; p < kHB; ++p)
+      if (b0 + p < B) dpooled[(int64_t)(b0 + p) * d + tid] = acc[p];
+  }
+  const int W = 2 * h + 4;
+  float* out = part + (int64_t)blockIdx.x * W;
+  if (tid < h) {
+    out[tid] = pw2;
+    out[h + tid] = pb1;
+  }
+  if (tid == 0) {
+    float db2 = 0.f, lt = 0.f, ly = 0.f;
+    for (int p = 0; p < kHB; ++p) {
+      const int b = b0 + p;
+      if (b >= B) break;
+      db2 += sds[p];
+      lt += (s[b] - t[b]) * (s[b] - t[b]);
+      ly += (s[b] - y[b]) * (s[b] - y[b]);
+    }
+    const float invB = 1.0f / (float)B;
+    out[2 * h] = db2;
+    out[2 * h + 1] = lt * invB;
+    out[2 * h + 2] = ly * invB;
+    out[2 * h + 3] = (lt + ly) * invB;
+  }
+}
+
+// ---------------------------------------------------------------- final norm + pool backward
+// Block per program; wavefronts take its tokens. dhf = dpooled[b] / len for
+// every valid token; dH = RMSNorm_f backward of dhf (or dhf itself without
+// the final norm). Per-program partial of dg_f.
+template <int DM>
+__global__ __launch_bounds__(256) void normf_pool_bwd_kernel(const int* __restrict__ offs,
+                                                             const float* __restrict__ H,
+                                                             const float* __restrict__ g_f,
+                                                             int final_norm, float eps,
+                                                             const float* __restrict__ dpooled,
+                                                             float* __restrict__ dH,
+                                                             float* __restrict__ dg_part) {
+  constexpr int PL = DM / 64;
+  __shared__ float sdg[4][DM];
+  const int b = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int base = offs[b], len = offs[b + 1] - base;
+  const float inv = len > 0 ? 1.0f / (float)len : 0.f;
+  float dhf[PL], gg[PL], dg[PL];
+#pragma unroll
+  for (int i = 0; i < PL; ++i) {
+    dhf[i] = dpooled[(int64_t)b * DM + lane * PL + i] * inv;
+    gg[i] = final_norm ? g_f[lane * PL + i] : 1.f;
+    dg[i] = 0.f;
+  }
+  for (int t = wave; t < len; t += 4) {
+    const int64_t o = (int64_t)(base + t) * DM + lane * PL;
+    if (!final_norm) {
+#pragma unroll
+      for (int i = 0; i < PL; ++i) dH[o + i] = dhf[i];
+      continue;
+    }
+    float hv[PL], ss = 0.f, dot = 0.f;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      hv[i] = H[o + i];
+      ss = fmaf(hv[i], hv[i], ss);
+      dot = fmaf(gg[i] * dhf[i], hv[i], dot);
+    }
+    ss = wave_sum(ss);
+    dot = wave_sum(dot);
+    const float r = 1.0f / sqrtf(ss / (float)DM + eps);
+    const float c = r * r * r / (float)DM * dot;
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      dH[o + i] = r * gg[i] * dhf[i] - c * hv[i];
+      dg[i] = fmaf(dhf[i], hv[i] * r, dg[i]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < PL; ++i) sdg[wave][lane * PL + i] = dg[i];
+  __syncthreads();
+  for (int k = threadIdx.x; k < DM; k += 256)
+    dg_part[(int64_t)b * DM + k] = sdg[0][k] + sdg[1][k] + sdg[2][k] + sdg[3][k];
+}
+
+// ---------------------------------------------------------------- selective-scan backward
+// Block per program, one thread per channel e (E threads). Per channel:
+//   forward recompute over the program, storing the state every TC tokens
+//   (checkpoints in a global scratch, one [N] vector per chunk boundary);
+//   reverse sweep chunk by chunk: the chunk's states are recomputed into
+//   registers from its checkpoint, then tokens are walked backwards with the
+//   state adjoint g_t = C_t dy_t + a_{t+1} g_{t+1}, a_t = exp(dt_t A).
+// Per token it writes dz (gate), du (scan part), dv = ddt * softplus'(v);
+// dB_t and dC_t are sums over channels, formed by a butterfly
+// reduce-scatter inside each wavefront plus an LDS sum across wavefronts.
+// dA_log and dD are accumulated per thread and written as per-program partials.
+constexpr int kTC = 8;
+
+// Reduce 32 values across the 64 lanes of a wavefront: afterwards lane l
+// holds the wavefront total of value ((l >> 1) & 31).
+__device__ __forceinline__ float butterfly32(float* v, int lane) {
+#pragma unroll
+  for (int step = 0; step < 5; ++step) {
+    const int half = 16 >> step;      // values kept after this step
+    const int mask = 32 >> step;      // partner lane distance
+    const bool up = (lane & mask) != 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const float mine = up ? v[half + i] : v[i];
+      const float other = up ? v[i] : v[half + i];
+      v[i] = mine + __shfl_xor(other, mask, 64);
+    }
+  }
+  return v[0] + __shfl_xor(v[0], 1, 64);
+}
+
+template <int N, int R, typename T>
+__global__ __launch_bounds__(256) void scan_bwd_kernel(
+    const int* __restrict__ offs, int E, int L, const T* __restrict__ u,
+    const float* __restrict__ xdbl, const T* __restrict__ xz, const T* __restrict__ ysave,
+    const float* __restrict__ dyg, const float* __restrict__ W_dt,
+    const float* __restrict__ b_dt, const float* __restrict__ A_log, const float* __restrict__ Dp,
+    float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
+    float* __restrict__ dxz, float* __restrict__ dxdbl, float* __restrict__ dA_part,
+    float* __restrict__ dD_part) {
+  constexpr int XW = R + 2 * N;
+  extern __shared__ float smem[];
+  float* sX = smem;                       // [L][XW] rows of this program
+  float* sRed = smem + L * XW;            // [4 waves][2N]
+  const int b = blockIdx.x;
+  const int e = threadIdx.x;              // blockDim == E
+  const int wave = e >> 6, lane = e & 63;
+  const int base = offs[b], len = offs[b + 1] - base;
+  const int nck = (len + kTC - 1) / kTC;
+  const int ldz = 2 * E;
+
+  for (int i = threadIdx.x; i < len * XW; i += blockDim.x) sX[i] = xdbl[(int64_t)base * XW + i];
+  __syncthreads();
+
+  float a2[N], An[N], wdt[R];
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    An[n] = -expf(A_log[e * N + n]);
+    a2[n] = An[n] * kLog2e;
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) wdt[r] = W_dt[e * R + r];
+  const float bdt = b_dt[e], Dv = Dp[e];
+  float* ck = ckpt + ((int64_t)b * E + e) * (int64_t)((L + kTC - 1) / kTC) * N;
+
+  auto dt_of = [&](int t, float& sig) {
+    const float* xr = &sX[t * XW];
+    float v = bdt;
+#pragma unroll
+    for (int r = 0; r < R; ++r) v = fmaf(wdt[r], xr[r], v);
+    sig = sigmoid_fast(v);
+    return softplus(v);
+  };
+
+  // forward recompute, checkpoint the state at the end of every chunk but the last
+  {
+    float s[N];
+#pragma unroll
+    for (int n = 0; n < N; ++n) s[n] = 0.f;
+    for (int t = 0; t < len; ++t) {
+      float sig;
+      const float dt = dt_of(t, sig);
+      const float dtu = dt * ld_act(u + (int64_t)(base + t) * E + e);
+      const float* xr = &sX[t * XW];
+#pragma unroll
+      for (int n = 0; n < N; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
+      if ((t % kTC) == kTC - 1 && t + 1 < len) {
+        float* dst = ck + (t / kTC) * N;
+#pragma unroll
+        for (int n = 0; n < N; ++n) dst[n] = s[n];
+      }
+    }
+  }
+
+  float g[N], anext[N], dA[N];
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    g[n] = 0.f;
+    anext[n] = 0.f;
+    dA[n] = 0.f;
+  }
+  float dD = 0.f;
+
+  for (int c = nck - 1; c >= 0; --c) {
+    const int t0 = c * kTC;
+    float sp[N];  // state before the chunk
+#pragma unroll
+    for (int n = 0; n < N; ++n) sp[n] = c > 0 ? ck[(c - 1) * N + n] : 0.f;
+    float hist[kTC][N];
+    {
+      float s[N];
+#pragma unroll
+      for (int n = 0; n < N; ++n) s[n] = sp[n];
+#pragma unroll
+      for (int tt = 0; tt < kTC; ++tt) {
+        const int t = t0 + tt;
+        if (t < len) {
+          float sig;
+          const float dt = dt_of(t, sig);
+          const float dtu = dt * ld_act(u + (int64_t)(base + t) * E + e);
+          const float* xr = &sX[t * XW];
+#pragma unroll
+          for (int n = 0; n < N; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
+        }
+#pragma unroll
+        for (int n = 0; n < N; ++n) hist[tt][n] = s[n];
+      }
+    }
+#pragma unroll
+    for (int tt = kTC - 1; tt >= 0; --tt) {
+      const int t = t0 + tt;
+      if (t < len) {  // uniform across the block: len is per program
+        const int64_t row = base + t;
+        const float* xr = &sX[t * XW];
+        float sig;
+        const float dt = dt_of(t, sig);
+        const float uv = ld_act(u + row * E + e);
+        const float zv = ld_act(xz + row * ldz + E + e);
+        const float yv = ld_act(ysave + row * E + e);
+        const float dgo = dyg[row * E + e];
+        const float dy = dgo * silu(zv);
+        dxz[row * ldz + E + e] = dgo * yv * silu_grad(zv);
+        float red[2 * N];
+        float gB = 0.f, ddt_a = 0.f;
+#pragma unroll
+        for (int n = 0; n < N; ++n) {
+          const float a = __builtin_amdgcn_exp2f(dt * a2[n]);
+          g[n] = fmaf(xr[R + N + n], dy, anext[n] * g[n]);
+          anext[n] = a;
+          const float sprev = tt > 0 ? hist[tt - 1][n] : sp[n];
+          const float gsa = g[n] * sprev * a;
+          gB = fmaf(g[n], xr[R + n], gB);
+          ddt_a = fmaf(gsa, An[n], ddt_a);
+          dA[n] = fmaf(gsa, dt, dA[n]);
+          red[n] = g[n] * dt * uv;         // dB_t[n] contribution
+          red[N + n] = dy * hist[tt][n];   // dC_t[n] contribution
+        }
+        dD = fmaf(dy, uv, dD);
+        du_out[row * E + e] = fmaf(Dv, dy, dt * gB);
+        dv_out[row * E + e] = (uv * gB + ddt_a) * sig;
+        const float tot = butterfly32(red, lane);
+        if ((lane & 1) == 0) sRed[wave * 2 * N + (lane >> 1)] = tot;
+        __syncthreads();
+        if (threadIdx.x < 2 * N) {
+          float acc = 0.f;
+          for (int w = 0; w < (int)(blockDim.x >> 6); ++w) acc += sRed[w * 2 * N + threadIdx.x];
+          dxdbl[row * XW + R + threadIdx.x] = acc;
+        }
+        __syncthreads();
+      }
+    }
+  }
+#pragma unroll
+  for (int n = 0; n < N; ++n) dA_part[((int64_t)b * E + e) * N + n] = dA[n] * An[n];  // d/dA_log
+  dD_part[(int64_t)b * E + e] = dD;
+}
+
+// ---------------------------------------------------------------- conv + SiLU backward
+// Thread per (program, channel), tokens walked backwards. xc is recomputed
+// from the x window; dx_t = sum_k w_k dxc_{t+K-1-k} uses a window of future
+// dxc. Per-program partials of dw (K values) and db.
+template <int K, typename T>
+__global__ __launch_bounds__(256) void conv_bwd_kernel(const int* __restrict__ offs, int E,
+                                                       const T* __restrict__ x, int ldx,
+                                                       const float* __restrict__ w,
+                                                       const float* __restrict__ bias,
+                                                       const float* __restrict__ du,
+                                                       float* __restrict__ dx, int lddx,
+                                                       float* __restrict__ part) {
+  const int b = blockIdx.x;
+  const int e = blockIdx.y * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  const int base = offs[b], len = offs[b + 1] - base;
+  float wk[K], xw[K], fut[K], dw[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    wk[k] = w[e * K + k];
+    fut[k] = 0.f;
+    dw[k] = 0.f;
+  }
+  // xw[k] = x_{t-K+1+k} for the current t (zero before the program start)
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int tt = len - K + k;
+    xw[k] = tt >= 0 ? ld_act(x + (int64_t)(base + tt) * ldx + e) : 0.f;
+  }
+  const float be = bias[e];
+  float db = 0.f;
+  for (int t = len - 1; t >= 0; --t) {
+    float xc = be;
+#pragma unroll
+    for (int k = 0; k < K; ++k) xc = fmaf(wk[k], xw[k], xc);
+    const float dxc = du[(int64_t)(base + t) * E + e] * silu_grad(xc);
+    // future window: fut[j] = dxc_{t+j}
+#pragma unroll
+    for (int j = K - 1; j > 0; --j) fut[j] = fut[j - 1];
+    fut[0] = dxc;
+    float dxv = 0.f;
+#pragma unroll
+    for (int k = 0; k < K; ++k) dxv = fmaf(wk[k], fut[K - 1 - k], dxv);
+    dx[(int64_t)(base + t) * lddx + e] = dxv;
+#pragma unroll
+    for (int k = 0; k < K; ++k) dw[k] = fmaf(dxc, xw[k], dw[k]);
+    db += dxc;
+    // slide the x window one token back
+#pragma unroll
+    for (int k = K - 1; k > 0; --k) xw[k] = xw[k - 1];
+    const int tn = t - K;
+    xw[0] = tn >= 0 ? ld_act(x + (int64_t)(base + tn) * ldx + e) : 0.f;
+  }
+  float* o = part + (int64_t)b * (K + 1) * E + e;
+#pragma unroll
+  for (int k = 0; k < K; ++k) o[(int64_t)k * E] = dw[k];
+  o[(int64_t)K * E] = db;
+}
+
+// ---------------------------------------------------------------- column sums
+// part[s][c] = sum over rows of split s of A[m, c]  (rows < *Mdev).
+__global__ __launch_bounds__(256) void colsum_kernel(const int* __restrict__ Mdev, int Mmax,
+                                                     const float* __restrict__ A, int64_t lda, int C,
+                                                     int rows_per_split, float* __restrict__ part) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  const int M = Mdev ? *Mdev : Mmax;
+  const int r0 = blockIdx.y * rows_per_split;
+  const int r1 = min(r0 + rows_per_split, M);
+  float acc = 0.f;
+  for (int m = r0; m < r1; ++m) acc += A[(int64_t)m * lda + c];
+  part[(int64_t)blockIdx.y * C + c] = acc;
+}
+
+// ---------------------------------------------------------------- reductions
+// blockIdx.y picks the job; its elements are summed over the splits in order.
+__global__ __launch_bounds__(256) void reduce_kernel(const ReduceJob* __restrict__ jobs, int njobs,
+                                                     const float* __restrict__ ws,
+                                                     float* __restrict__ grad,
+                                                     float* __restrict__ loss) {
+  const int j = blockIdx.y;
+  if (j >= njobs) return;
+  const ReduceJob J = jobs[j];
+  float* dst = (J.dst_buf == 0 ? grad : loss) + J.dst;
+  const float* src = ws + J.src;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < J.n; i += (int64_t)gridDim.x * 256) {
+    float acc = 0.f;
+    for (int s = 0; s < J.nsplit; ++s) acc += src[(int64_t)s * J.split_stride + i * J.src_stride];
+    dst[i * J.dst_stride] = acc;
+  }
+}
+
+// ---------------------------------------------------------------- Adam
+__global__ __launch_bounds__(256) void adam_kernel(int64_t n, float* __restrict__ p,
+                                                   float* __restrict__ m, float* __restrict__ v,
+                                                   const float* __restrict__ g, float lr, float b1,
+                                                   float b2, float eps, float bc1, float bc2) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const float gi = g[i];
+    const float mi = fmaf(b1, m[i], (1.0f - b1) * gi);
+    const float vi = fmaf(b2, v[i], (1.0f - b2) * gi * gi);
+    m[i] = mi;
+    v[i] = vi;
+    p[i] -= lr * (mi / bc1) / (sqrtf(vi / bc2) + eps);
+  }
+}
+
+// ---------------------------------------------------------------- weight derivation
+// Every device-side weight layout is derived from the fp32 master blob by a
+// table of jobs (copy, bf16 conversion, transpose, gain fold), in one launch.
+__device__ __forceinline__ float round_to_bf16(float f) { return bf16_to_f32(f32_to_bf16(f)); }
+
+__global__ __launch_bounds__(256) void derive_kernel(const float* __restrict__ master,
+                                                     const DeriveJob* __restrict__ jobs, int njobs,
+                                                     int64_t total, uint8_t* __restrict__ base,
+                                                     int round_bf16) {
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    int lo = 0, hi = njobs;
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (jobs[mid].start <= idx) lo = mid; else hi = mid;
+    }
+    const DeriveJob J = jobs[lo];
+    const int64_t k = idx - J.start;
+    const int r = (int)(k / J.cols), c = (int)(k % J.cols);
+    float v = master[J.src + k];
+    if (round_bf16) v = round_to_bf16(v);
+    if (J.kind == kDeriveFold) {
+      float gv = master[J.src2 + c];
+      if (round_bf16) gv = round_to_bf16(gv);
+      v = v * gv;
+    }
+    const int64_t o = J.transpose ? (int64_t)c * J.ld + r : (int64_t)r * J.ld + c;
+    if (J.kind == kDeriveBF16) reinterpret_cast<uint16_t*>(base + J.dst)[o] = f32_to_bf16(v);
+    else reinterpret_cast<float*>(base + J.dst)[o] = v;
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_rmsnorm_fwd(int d, int Mmax, const int* Mdev, const float* H, const float* g,
+                              float eps, uint16_t* n, float* rstd, hipStream_t s) {
+  dim3 grid((Mmax + 3) / 4);
+  switch (d) {
+    case 64: hipLaunchKernelGGL(rmsnorm_fwd_kernel<64>, grid, dim3(256), 0, s, Mdev, H, g, eps, n, rstd); break;
+    case 128: hipLaunchKernelGGL(rmsnorm_fwd_kernel<128>, grid, dim3(256), 0, s, Mdev, H, g, eps, n, rstd); break;
+    case 256: hipLaunchKernelGGL(rmsnorm_fwd_kernel<256>, grid, dim3(256), 0, s, Mdev, H, g, eps, n, rstd); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int rmsnorm_bwd_blocks(int Mmax) { return (Mmax + 63) / 64; }
+
+hipError_t launch_rmsnorm_bwd(int d, int Mmax, const int* Mdev, const float* dN, const float* H,
+                              const float* rstd, const float* g, float* dH, float* dg_part,
+                              hipStream_t s) {
+  dim3 grid(rmsnorm_bwd_blocks(Mmax));
+  switch (d) {
+    case 64: hipLaunchKernelGGL(rmsnorm_bwd_kernel<64>, grid, dim3(256), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
+    case 128: hipLaunchKernelGGL(rmsnorm_bwd_kernel<128>, grid, dim3(256), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
+    case 256: hipLaunchKernelGGL(rmsnorm_bwd_kernel<256>, grid, dim3(256), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int loss_head_blocks(int B) { return (B + kHB - 1) / kHB; }
+
+hipError_t launch_loss_head_bwd(int B, int d, int h, const float* s, const float* t, const float* y,
+                                const float* a1, const float* W1, const float* W2, float* da1,
+                                float* dpooled, float* part, hipStream_t st) {
+  if (h > 256 || d > 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(loss_head_bwd_kernel, dim3(loss_head_blocks(B)), dim3(256), 0, st, B, d, h, s, t, y,
+                     a1, W1, W2, da1, dpooled, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_normf_pool_bwd(int B, int d, const int* offs, const float* H, const float* g_f,
+                                 int final_norm, float eps, const float* dpooled, float* dH,
+                                 float* dg_part, hipStream_t s) {
+  switch (d) {
+    case 64: hipLaunchKernelGGL(normf_pool_bwd_kernel<64>, dim3(B), dim3(256), 0, s, offs, H, g_f, final_norm, eps, dpooled, dH, dg_part); break;
+    case 128: hipLaunchKernelGGL(normf_pool_bwd_kernel<128>, dim3(B), dim3(256), 0, s, offs, H, g_f, final_norm, eps, dpooled, dH, dg_part); break;
+    case 256: hipLaunchKernelGGL(normf_pool_bwd_kernel<256>, dim3(B), dim3(256), 0, s, offs, H, g_f, final_norm, eps, dpooled, dH, dg_part); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+size_t scan_bwd_ckpt_floats(int B, int E, int L, int N) {
+  return (size_t)B * E * ((L + kTC - 1) / kTC) * N;
+}
+
+hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, const uint16_t* u,
+                           const float* xdbl, const uint16_t* xz, const uint16_t* ysave,
+                           const float* dyg, const float* W_dt, const float* b_dt,
+                           const float* A_log, const float* D, float* ckpt, float* dv, float* du,
+                           float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s) {
+  if (N != 16 || E % 64 || E > 256 || B <= 0) return hipErrorInvalidValue;
+  const size_t shm = ((size_t)L * (R + 2 * N) + 4 * 2 * N) * sizeof(float);
+  if (shm > 64 * 1024) return hipErrorInvalidValue;
+#define TCL_SB(RR)                                                                                    \
+  hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B), dim3(E), shm, s, offs, E, L, u,   \
+                     xdbl, xz, ysave, dyg, W_dt, b_dt, A_log, D, ckpt, dv, du, dxz, dxdbl, dA_part, \
+                     dD_part)
+  switch (R) {
+    case 4: TCL_SB(4); break;
+    case 8: TCL_SB(8); break;
+    case 16: TCL_SB(16); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_SB
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_bwd(int B, int E, int K, const int* offs, const uint16_t* x, int ldx,
+                           const float* w, const float* b, const float* du, float* dx, int lddx,
+                           float* part, hipStream_t s) {
+  dim3 grid(B, (E + 255) / 256);
+  switch (K) {
+    case 1: hipLaunchKernelGGL((conv_bwd_kernel<1, uint16_t>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, du, dx, lddx, part); break;
+    case 2: hipLaunchKernelGGL((conv_bwd_kernel<2, uint16_t>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, du, dx, lddx, part); break;
+    case 3: hipLaunchKernelGGL((conv_bwd_kernel<3, uint16_t>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, du, dx, lddx, part); break;
+    case 4: hipLaunchKernelGGL((conv_bwd_kernel<4, uint16_t>), grid, dim3(256), 0, s, offs, E, x, ldx, w, b, du, dx, lddx, part); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+int colsum_splits(int Mmax) { return min(64, max(1, (Mmax + 255) / 256)); }
+
+hipError_t launch_colsum(const int* Mdev, int Mmax, const float* A, int64_t lda, int C, int splits,
+                         float* part, hipStream_t s) {
+  const int rps = (Mmax + splits - 1) / splits;
+  hipLaunchKernelGGL(colsum_kernel, dim3((C + 255) / 256, splits), dim3(256), 0, s, Mdev, Mmax, A, lda,
+                     C, rps, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, const float* ws,
+                         float* grad, float* loss, hipStream_t s) {
+  if (njobs <= 0) return hipSuccess;
+  const int gx = (int)std::min<int64_t>((max_n + 255) / 256, 256);
+  hipLaunchKernelGGL(reduce_kernel, dim3(gx, njobs), dim3(256), 0, s, d_jobs, njobs, ws, grad, loss);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam(int64_t n, float* p, float* m, float* v, const float* g, float lr, float b1,
+                       float b2, float eps, float bc1, float bc2, hipStream_t s) {
+  const int grid = (int)std::min<int64_t>((n + 255) / 256, 2048);
+  hipLaunchKernelGGL(adam_kernel, dim3(grid), dim3(256), 0, s, n, p, m, v, g, lr, b1, b2, eps, bc1, bc2);
+  return hipGetLastError();
+}
+
+hipError_t launch_derive(const float* master, const DeriveJob* d_jobs, int njobs, int64_t total,
+                         void* base, int round_bf16, hipStream_t s) {
+  if (total <= 0) return hipSuccess;
+  const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(derive_kernel, dim3(grid), dim3(256), 0, s, master, d_jobs, njobs, total,
+                     static_cast<uint8_t*>(base), round_bf16);
+  return hipGetLastError();
+}
+
+}  // namespace tcl

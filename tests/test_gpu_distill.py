@@ -1,0 +1,156 @@
+"""Parity of tcl_distill_step with the fp64 oracle's distillation step on the
+same seeded inputs: the three loss values, every gradient tensor, and the
+student's parameters after Adam.
+
+Tolerances (bf16 compute, fp32 master weights and gradients):
+  loss: relative 2e-2;
+  gradients: per tensor, ||g_gpu - g_oracle|| <= 2e-2 ||g_oracle||;
+  parameters: the update must be Adam applied exactly to the GPU's own
+    gradient, and it must match the oracle's to 2e-2 lr wherever the oracle's
+    gradient is clearly non-zero (|g| > 5e-2 rms of its tensor, > 6 standard
+    deviations of the observed gradient error, and > 1e3 eps, where Adam's
+    first step is lr * sign(g)); near zero a sign flip is allowed, bounding
+    the difference by 2 lr.
+Labels are the oracle teacher's scores plus seeded N(0, 0.05^2) noise.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import model as om
+from paper_2604_12891_amd import binding as tb
+from paper_2604_12891_amd import workload as wl
+from tests.parity import oracle_cfg
+
+pytestmark = pytest.mark.gpu
+LR = 1e-3
+
+
+def _setup(tshape, sshape, B, L, len_lo, seed, perturb=False):
+    rng = np.random.default_rng(seed)
+    tblob = wl.round_to_bf16(wl.init_params(tshape, rng, perturb=perturb))
+    sblob = wl.round_to_bf16(wl.init_params(sshape, rng, perturb=perturb))
+    X, lengths = wl.make_inputs(B, L, tshape.F, len_lo, L, rng)
+    t = om.score(tblob, X, lengths, oracle_cfg(tshape))
+    labels = (t + 0.05 * rng.standard_normal(B)).astype(np.float32)
+    return tblob, sblob, X, lengths, labels, t
+
+
+def _gpu(tshape, sshape, tblob, sblob, X, lengths, labels, steps):
+    teacher = tb.CostModel(tb.config_from_shape(tshape, "bf16"), tblob)
+    student = tb.CostModel(tb.config_from_shape(sshape, "bf16"), sblob)
+    tr = tb.Trainer(teacher, student, lr=LR, max_B=X.shape[0], max_L=X.shape[1])
+    Xd, Ld, Yd = (torch.from_numpy(a).cuda() for a in (X, lengths, labels))
+    out = []
+    for _ in range(steps):
+        loss = tr.step(Xd, Ld, Yd)
+        torch.cuda.synchronize()
+        out.append((loss.cpu().numpy().astype(np.float64), tr.grads().astype(np.float64),
+                    student.get_params().astype(np.float64)))
+    return out
+
+
+def _check(gpu, orc, sshape, what):
+    loss_g, grad_g, params_g = gpu
+    np.testing.assert_allclose(loss_g, np.array(orc["loss"]), rtol=2e-2, err_msg=f"{what}: loss")
+    cfg = oracle_cfg(sshape)
+    G = om.unpack(grad_g, cfg)
+    O = om.unpack(orc["grad"], cfg)
+    for name in O:
+        err = np.linalg.norm(G[name] - O[name])
+        ref = np.linalg.norm(O[name])
+        assert err <= 2e-2 * ref + 1e-12, f"{what}: grad {name} rel err {err / max(ref, 1e-30):.3e}"
+
+
+def _check_params(before, params_g, grad_g, orc, sshape, what):
+    """After one step from zero moments: (1) the GPU applied Adam exactly to its
+    own gradient (m_hat = g, v_hat = g^2 at step 1); (2) its update agrees with
+    the oracle's where the oracle's gradient is clearly non-zero -- |g| above
+    5e-2 rms of its tensor, above 6 standard deviations of the observed
+    per-element gradient error, and far above eps, where the update is
+    lr sign(g); elsewhere a sign flip is allowed (difference <= 2 lr)."""
+    cfg = oracle_cfg(sshape)
+    adam = before - LR * grad_g / (np.abs(grad_g) + 1e-8)
+    np.testing.assert_allclose(params_g, adam, rtol=0, atol=1e-6 * np.abs(before).max() + 1e-9,
+                               err_msg=f"{what}: Adam update")
+    Pg = om.unpack(params_g - before, cfg)
+    Po = om.unpack(orc["params"] - before, cfg)
+    Go = om.unpack(orc["grad"], cfg)
+    Gg = om.unpack(grad_g, cfg)
+    for name in Po:
+        rms = np.sqrt(np.mean(Go[name] ** 2))
+        noise = np.sqrt(np.mean((Gg[name] - Go[name]) ** 2))  # observed per-element gradient error
+        clear = np.abs(Go[name]) > np.maximum(np.maximum(5e-2 * rms, 6 * noise), 1e3 * 1e-8)
+        diff = np.abs(Pg[name] - Po[name])
+        if clear.any():
+            assert np.all(diff[clear] <= 2e-2 * LR), f"{what}: param {name} max diff {diff[clear].max():.3e}"
+        assert np.all(diff <= 2 * LR + 1e-9), f"{what}: param {name} moved too far"
+
+
+@pytest.mark.parametrize("perturb", [False, True])
+def test_distill_small(perturb):
+    """Small teacher and student, ragged lengths including 1 and L."""
+    tshape = wl.ModelShape(d_model=64, d_inner=128, dt_rank=4, n_layers=2, head_hidden=64)
+    sshape = wl.ModelShape(d_model=64, d_inner=128, dt_rank=8, n_layers=2, head_hidden=64)
+    tblob, sblob, X, lengths, labels, t = _setup(tshape, sshape, 40, 19, 1, 31 + perturb, perturb)
+    lengths[0], lengths[1] = 1, 19
+    X[np.arange(19)[None, :] >= lengths[:, None]] = 0
+    t = om.score(tblob, X, lengths, oracle_cfg(tshape))
+    print(f"distill small perturb={perturb}", flush=True)
+    (g,) = _gpu(tshape, sshape, tblob, sblob, X, lengths, labels, 1)
+    orc = om.distill_step(tblob, oracle_cfg(tshape), sblob, oracle_cfg(sshape), X, lengths, labels,
+                          lr=LR, teacher_scores=t)
+    _check(g, orc, sshape, "small")
+    _check_params(sblob.astype(np.float64), g[2], g[1], orc, sshape, "small")
+
+
+def test_distill_full_shapes_two_steps():
+    """The distillation workload's model shapes (teacher d=256 x4, student
+    d=128 x2) at B=128; a second step exercises Adam's moments and step count
+    and the re-derived bf16 weights."""
+    w = wl.WORKLOADS["distill_B1024_L25_t256_s128_bf16"]
+    (tblob, sblob), X, lengths = wl.make_workload(w.name, B=128)
+    t = om.score(tblob, X, lengths, oracle_cfg(w.model))
+    labels = (t + wl.label_noise(128)).astype(np.float32)
+    print("distill full shapes B=128, 2 steps", flush=True)
+    g1, g2 = _gpu(w.model, w.student, tblob, sblob, X, lengths, labels, 2)
+    tc, sc = oracle_cfg(w.model), oracle_cfg(w.student)
+    o1 = om.distill_step(tblob, tc, sblob, sc, X, lengths, labels, lr=LR, teacher_scores=t)
+    _check(g1, o1, w.student, "step 1")
+    _check_params(sblob.astype(np.float64), g1[2], g1[1], o1, w.student, "step 1")
+    # step 2 from the oracle's own state, computing with bf16-rounded master weights
+    p1 = o1["params"]
+    o2 = om.distill_step(tblob, tc, p1, sc, X, lengths, labels, m=o1["m"], v=o1["v"], step=2, lr=LR,
+                         compute_blob=wl.round_to_bf16(p1.astype(np.float32)).astype(np.float64),
+                         teacher_scores=t)
+    _check(g2, o2, w.student, "step 2")
+
+
+def test_distill_full_batch():
+    """B = 1024 programs, L = 25: the workload the benchmark times."""
+    w = wl.WORKLOADS["distill_B1024_L25_t256_s128_bf16"]
+    (tblob, sblob), X, lengths = wl.make_workload(w.name)
+    t = om.score(tblob, X, lengths, oracle_cfg(w.model))
+    labels = (t + wl.label_noise(w.B)).astype(np.float32)
+    print("distill full batch B=1024", flush=True)
+    (g,) = _gpu(w.model, w.student, tblob, sblob, X, lengths, labels, 1)
+    orc = om.distill_step(tblob, oracle_cfg(w.model), sblob, oracle_cfg(w.student), X, lengths, labels,
+                          lr=LR, teacher_scores=t)
+    _check(g, orc, w.student, "B=1024")
+    _check_params(sblob.astype(np.float64), g[2], g[1], orc, w.student, "B=1024")
+
+
+def test_trainer_rejects_bad_arguments():
+    shape = wl.TINY
+    blob = wl.round_to_bf16(wl.init_params(shape, np.random.default_rng(0)))
+    t = tb.CostModel(tb.config_from_shape(shape, "bf16"), blob)
+    s32 = tb.CostModel(tb.config_from_shape(shape, "f32"), blob)
+    with pytest.raises(tb.TclError):
+        tb.Trainer(t, s32)          # the student must be bf16
+    s = tb.CostModel(tb.config_from_shape(shape, "bf16"), blob)
+    tr = tb.Trainer(t, s, max_B=8, max_L=10)
+    assert tr.workspace_bytes(9, 10) == 0 and tr.workspace_bytes(8, 11) == 0
+    X = torch.zeros(9, 10, shape.F, device="cuda")
+    with pytest.raises(tb.TclError):
+        tr.step(X, torch.ones(9, dtype=torch.int32, device="cuda"), torch.zeros(9, device="cuda"),
+                workspace=torch.empty(1 << 20, dtype=torch.uint8, device="cuda"))
