@@ -86,6 +86,128 @@ def cpu_baseline(w, blob, X, lengths, target_s: float) -> dict:
                       f"{dt:.1f} s; host has {os.cpu_count()} CPUs, affinity {len(os.sched_getaffinity(0))}"}
 
 
+def distill_kernel_work(tshape, sshape, M_v: int, B: int) -> dict:
+    """Algorithmic work per step of the distillation step's kernels: the
+    teacher's scoring kernels (bf16, as in kernel_work) and the student's
+    projection backward GEMMs (flops) and scan backward (bytes)."""
+    d, E, N, R, F, h, nl = (sshape.d_model, sshape.d_inner, sshape.d_state, sshape.dt_rank, sshape.F,
+                            sshape.head_hidden, sshape.n_layers)
+    XW = R + 2 * N
+    per_layer = d * E + E * R + XW * E + 2 * E * d  # out_proj, dt_proj, x_proj, in_proj
+    tw = kernel_work(tshape, M_v, B, "bf16")
+    out = {("teacher:" + k): (kind, amount * (tshape.n_layers if k in ("gemm_in_proj", "gemm_x_proj",
+                                                                        "gemm_out_proj", "conv_silu", "scan")
+                                               else 1))
+           for k, (kind, amount) in tw.items()}
+    out.update({
+        "gemm_dX": ("flop", 2 * M_v * per_layer * nl),
+        "gemm_dW": ("flop", 2 * M_v * per_layer * nl + 2 * B * h * d + 2 * M_v * d * F),
+        # reads u, z, y (bf16), dyg, xdbl (fp32); writes dz, du, dv (fp32), dB/dC
+        "scan_bwd": ("byte", nl * M_v * (3 * E * 2 + E * 4 + XW * 4 + 3 * E * 4 + 2 * N * 4)),
+    })
+    return out
+
+
+def bench_distill(args, w):
+    import numpy as np
+    import torch
+
+    from paper_2604_12891_amd import binding as tb
+    from paper_2604_12891_amd import workload as wl
+
+    (tblob, sblob), X, lengths = wl.make_workload(w.name)
+    dev = torch.device("cuda:0")
+    Xd = torch.from_numpy(X).to(dev)
+    Ld = torch.from_numpy(lengths).to(dev)
+    teacher = tb.CostModel(tb.config_from_shape(w.model, w.dtype), tblob)
+    student = tb.CostModel(tb.config_from_shape(w.student, w.dtype), sblob)
+    # labels: the teacher's score plus seeded N(0, 0.05^2) noise (prepared once, untimed)
+    t = teacher.score(Xd, Ld)
+    Yd = (t + torch.from_numpy(wl.label_noise(w.B)).to(dev)).contiguous()
+    tr = tb.Trainer(teacher, student, lr=1e-3, max_B=w.B, max_L=w.L)
+    ws = tr.workspace(w.B, w.L)
+    loss = torch.empty(3, dtype=torch.float32, device=dev)
+    M_v = int(lengths.sum())
+    for _ in range(args.warmup):
+        tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    assert torch.isfinite(loss).all().item(), "non-finite loss"
+
+    tr.timing(True)
+    teacher.timing(True)
+    tr.timing_reset()
+    teacher.timing_reset()
+    for _ in range(args.steps):
+        tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+    torch.cuda.synchronize()
+    rep = {("teacher:" + k): v for k, v in teacher.timing_report().items()}
+    rep.update(tr.timing_report())
+    tr.timing(False)
+    teacher.timing(False)
+    work = distill_kernel_work(w.model, w.student, M_v, w.B)
+    kernels = {}
+    for name, (tot, n) in rep.items():
+        per = tot / n
+        e = {"ms_per_launch": per, "launches_per_step": n // args.steps, "ms_per_step": tot / args.steps}
+        if name in work:
+            kind, amount = work[name]  # per step; the launches of a category share it
+            dtype = "bf16" if name.startswith("teacher:") else "f32"
+            e.update(roofline_entry(kind, amount, tot / args.steps, dtype))
+            e["work_per_step"] = amount
+        kernels[name] = e
+    launches = sum(e["launches_per_step"] for e in kernels.values())
+    dom = max((k for k in kernels if "frac" in kernels[k]), key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    roof = {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 3), "peak": d["peak"],
+            "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None,
+            "ms_per_launch": round(d["ms_per_launch"], 5), "launches_per_step": d["launches_per_step"]}
+    if args.kernels:
+        for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+            print(f"{k:28s} {e['ms_per_step']:9.4f} ms/step  x{e['launches_per_step']:3d}  "
+                  f"{e.get('achieved', float('nan')):10.2f} {e.get('unit', '')}", file=sys.stderr)
+    cpu = None
+    if not args.no_cpu_baseline:
+        from threadpoolctl import threadpool_info
+
+        from oracle import model as om
+
+        def ocfg(m):
+            return dict(F=m.F, d_model=m.d_model, d_inner=m.d_inner, d_state=m.d_state, d_conv=m.d_conv,
+                        dt_rank=m.dt_rank, n_layers=m.n_layers, head_hidden=m.head_hidden,
+                        final_norm=m.final_norm, norm_eps=m.norm_eps)
+        n = 64
+        labels = Yd.cpu().numpy()
+        t0 = time.perf_counter()
+        om.distill_step(tblob, ocfg(w.model), sblob, ocfg(w.student), X[:n], lengths[:n], labels[:n])
+        dt = time.perf_counter() - t0
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        cpu = {"value": 1.0 / (dt * w.B / n), "unit": "steps/s", "cores": max([p.get("num_threads", 1) for p in blas] or [1]),
+               "kind": "oracle",
+               "sample": f"one fp64 numpy step on {n} of the {w.B} programs ({dt:.1f} s), scaled linearly "
+                         f"to the full batch (programs are independent)"}
+    rec = {
+        "metric": "distillation steps/sec (B=1024,L=25)", "value": 1000.0 / ms, "unit": "steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "teacher": "d256 E512 N16 x4",
+                   "student": "d128 E256 N16 x2", "valid_tokens": M_v, "launches_per_step": launches},
+        "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
+                    for k, e in kernels.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,8 +233,8 @@ def main():
 
     w = wl.WORKLOADS[args.workload]
     if w.student is not None:
-        print("distillation benchmark is not built yet", file=sys.stderr)
-        sys.exit(2)
+        bench_distill(args, w)
+        return
     blob, X, lengths = wl.make_workload(w.name)
     dev = torch.device("cuda:0")
     Xd = torch.from_numpy(X).to(dev)

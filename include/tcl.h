@@ -172,7 +172,8 @@ TCL_API tcl_status tcl_timing_reset(tcl_model* model);
 
 /* Create a trainer (allocates the gradient blob and the Adam moments, zeroed;
  * the step count starts at 0). max_B, max_L bound every later step; max_L is
- * also limited by LDS staging in the scan backward (about 300 tokens). */
+ * also limited by the scan backward's LDS staging, (dt_rank + 18 d_state)
+ * * 4 bytes per token within 64 KiB (55 tokens at dt_rank 8). */
 TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, float lr, float beta1,
                                       float beta2, float eps, int32_t max_B, int32_t max_L,
                                       tcl_trainer** out);

@@ -224,9 +224,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
 // for all PB programs (W1 is read once per workgroup, transposed so the
 // reads are coalesced), then the ReLU'd units are dotted with W2 by a
 // block reduction.
-constexpr int kTailPB = 16;
-
-template <int DM>
+template <int DM, int kTailPB>
 __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const int* __restrict__ offs,
                                                    const int* __restrict__ lengths,
                                                    const float* __restrict__ H,
@@ -386,14 +384,20 @@ hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const in
                            float* scores, hipStream_t s, float* pooled_out, float* a1_out) {
   if (B <= 0) return hipSuccess;
   if (h > 256) return hipErrorInvalidValue;
-  dim3 grid((B + kTailPB - 1) / kTailPB);
-#define TCL_TAIL(DD)                                                                          \
-  hipLaunchKernelGGL((tail_kernel<DD>), grid, dim3(256), 0, s, B, L, h, offs, lengths, H, g_f, \
+  // 16 programs per workgroup share each W1 read; small batches use 4 so
+  // that there are enough workgroups to spread over the CUs
+  const int pb = B >= 8192 ? 16 : 4;
+  dim3 grid((B + pb - 1) / pb);
+#define TCL_TAIL(DD, PB)                                                                           \
+  hipLaunchKernelGGL((tail_kernel<DD, PB>), grid, dim3(256), 0, s, B, L, h, offs, lengths, H, g_f, \
                      final_norm, eps, W1T, b1, W2, b2, scores, pooled_out, a1_out)
-  switch (d) {
-    case 64: TCL_TAIL(64); break;
-    case 128: TCL_TAIL(128); break;
-    case 256: TCL_TAIL(256); break;
+  switch (d * 100 + pb) {
+    case 6416: TCL_TAIL(64, 16); break;
+    case 12816: TCL_TAIL(128, 16); break;
+    case 25616: TCL_TAIL(256, 16); break;
+    case 6404: TCL_TAIL(64, 4); break;
+    case 12804: TCL_TAIL(128, 4); break;
+    case 25604: TCL_TAIL(256, 4); break;
     default: return hipErrorInvalidValue;
   }
 #undef TCL_TAIL

@@ -221,24 +221,28 @@ __global__ __launch_bounds__(256) void normf_pool_bwd_kernel(const int* __restri
 }
 
 // ---------------------------------------------------------------- selective-scan backward
-// Block per program, one thread per channel e (E threads). Per channel:
+// Block per program, two lanes per channel e: lane 2e+h owns states
+// n = 8h .. 8h+7 (sums over n are completed with one lane-pair shuffle).
+// Per channel:
 //   forward recompute over the program, storing the state every TC tokens
 //   (checkpoints in a global scratch, one [N] vector per chunk boundary);
 //   reverse sweep chunk by chunk: the chunk's states are recomputed into
 //   registers from its checkpoint, then tokens are walked backwards with the
 //   state adjoint g_t = C_t dy_t + a_{t+1} g_{t+1}, a_t = exp(dt_t A).
 // Per token it writes dz (gate), du (scan part), dv = ddt * softplus'(v);
-// dB_t and dC_t are sums over channels, formed by a butterfly
-// reduce-scatter inside each wavefront plus an LDS sum across wavefronts.
-// dA_log and dD are accumulated per thread and written as per-program partials.
-constexpr int kTC = 8;
+// dB_t and dC_t are sums over channels, formed by a butterfly reduce-scatter
+// over the same-parity lanes of each wavefront, parked in LDS per token and
+// summed across wavefronts once at the end (no barrier inside the sweep).
+// dA_log and dD are accumulated per lane and written as per-program partials.
+constexpr int kTC = 4;
+constexpr int kHalfN = 8;
 
-// Reduce 32 values across the 64 lanes of a wavefront: afterwards lane l
-// holds the wavefront total of value ((l >> 1) & 31).
-__device__ __forceinline__ float butterfly32(float* v, int lane) {
+// Reduce 16 values across the 32 same-parity lanes of a wavefront: lane l
+// ends with the total (over lanes of parity l & 1) of value ((l >> 2) & 15).
+__device__ __forceinline__ float butterfly16(float* v, int lane) {
 #pragma unroll
-  for (int step = 0; step < 5; ++step) {
-    const int half = 16 >> step;      // values kept after this step
+  for (int step = 0; step < 4; ++step) {
+    const int half = 8 >> step;       // values kept after this step
     const int mask = 32 >> step;      // partner lane distance
     const bool up = (lane & mask) != 0;
 #pragma unroll
@@ -248,11 +252,11 @@ __device__ __forceinline__ float butterfly32(float* v, int lane) {
       v[i] = mine + __shfl_xor(other, mask, 64);
     }
   }
-  return v[0] + __shfl_xor(v[0], 1, 64);
+  return v[0] + __shfl_xor(v[0], 2, 64);
 }
 
 template <int N, int R, typename T>
-__global__ __launch_bounds__(256) void scan_bwd_kernel(
+__global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     const int* __restrict__ offs, int E, int L, const T* __restrict__ u,
     const float* __restrict__ xdbl, const T* __restrict__ xz, const T* __restrict__ ysave,
     const float* __restrict__ dyg, const float* __restrict__ W_dt,
@@ -260,30 +264,30 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(
     float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
     float* __restrict__ dxz, float* __restrict__ dxdbl, float* __restrict__ dA_part,
     float* __restrict__ dD_part) {
+  static_assert(N == 2 * kHalfN, "two lanes per channel, eight states each");
   constexpr int XW = R + 2 * N;
+  constexpr int NH = kHalfN;
   extern __shared__ float smem[];
   float* sX = smem;                       // [L][XW] rows of this program
-  float* sRed = smem + L * XW;            // [4 waves][2N]
+  float* sRed = smem + L * XW;            // [L][8 waves][2N] per-wavefront dB_t | dC_t
   const int b = blockIdx.x;
-  const int e = threadIdx.x;              // blockDim == E
-  const int wave = e >> 6, lane = e & 63;
+  const int tid = threadIdx.x;            // blockDim == 2E
+  const int e = tid >> 1, hf = tid & 1, n0 = hf * NH;
+  const int wave = tid >> 6, lane = tid & 63;
   const int base = offs[b], len = offs[b + 1] - base;
   const int nck = (len + kTC - 1) / kTC;
   const int ldz = 2 * E;
 
-  for (int i = threadIdx.x; i < len * XW; i += blockDim.x) sX[i] = xdbl[(int64_t)base * XW + i];
+  for (int i = tid; i < len * XW; i += blockDim.x) sX[i] = xdbl[(int64_t)base * XW + i];
   __syncthreads();
 
-  float a2[N], An[N], wdt[R];
+  float a2[NH], wdt[R];  // a2 = A log2(e); A itself is a2 ln(2) where needed
 #pragma unroll
-  for (int n = 0; n < N; ++n) {
-    An[n] = -expf(A_log[e * N + n]);
-    a2[n] = An[n] * kLog2e;
-  }
+  for (int n = 0; n < NH; ++n) a2[n] = -expf(A_log[e * N + n0 + n]) * kLog2e;
 #pragma unroll
   for (int r = 0; r < R; ++r) wdt[r] = W_dt[e * R + r];
   const float bdt = b_dt[e], Dv = Dp[e];
-  float* ck = ckpt + ((int64_t)b * E + e) * (int64_t)((L + kTC - 1) / kTC) * N;
+  float* ck = ckpt + ((int64_t)b * E + e) * (int64_t)((L + kTC - 1) / kTC) * N + n0;
 
   auto dt_of = [&](int t, float& sig) {
     const float* xr = &sX[t * XW];
@@ -296,27 +300,27 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(
 
   // forward recompute, checkpoint the state at the end of every chunk but the last
   {
-    float s[N];
+    float s[NH];
 #pragma unroll
-    for (int n = 0; n < N; ++n) s[n] = 0.f;
+    for (int n = 0; n < NH; ++n) s[n] = 0.f;
     for (int t = 0; t < len; ++t) {
       float sig;
       const float dt = dt_of(t, sig);
       const float dtu = dt * ld_act(u + (int64_t)(base + t) * E + e);
-      const float* xr = &sX[t * XW];
+      const float* xr = &sX[t * XW] + R + n0;
 #pragma unroll
-      for (int n = 0; n < N; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
+      for (int n = 0; n < NH; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[n]);
       if ((t % kTC) == kTC - 1 && t + 1 < len) {
         float* dst = ck + (t / kTC) * N;
 #pragma unroll
-        for (int n = 0; n < N; ++n) dst[n] = s[n];
+        for (int n = 0; n < NH; ++n) dst[n] = s[n];
       }
     }
   }
 
-  float g[N], anext[N], dA[N];
+  float g[NH], anext[NH], dA[NH];
 #pragma unroll
-  for (int n = 0; n < N; ++n) {
+  for (int n = 0; n < NH; ++n) {
     g[n] = 0.f;
     anext[n] = 0.f;
     dA[n] = 0.f;
@@ -325,27 +329,38 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(
 
   for (int c = nck - 1; c >= 0; --c) {
     const int t0 = c * kTC;
-    float sp[N];  // state before the chunk
+    float sp[NH];  // state before the chunk
 #pragma unroll
-    for (int n = 0; n < N; ++n) sp[n] = c > 0 ? ck[(c - 1) * N + n] : 0.f;
-    float hist[kTC][N];
+    for (int n = 0; n < NH; ++n) sp[n] = c > 0 ? ck[(c - 1) * N + n] : 0.f;
+    // this chunk's per-token inputs, loaded before the dependent arithmetic
+    float uc[kTC], zc[kTC], yc[kTC], gc[kTC];
+#pragma unroll
+    for (int tt = 0; tt < kTC; ++tt) {
+      const int t = min(t0 + tt, len - 1);
+      const int64_t row = base + t;
+      uc[tt] = ld_act(u + row * E + e);
+      zc[tt] = ld_act(xz + row * ldz + E + e);
+      yc[tt] = ld_act(ysave + row * E + e);
+      gc[tt] = dyg[row * E + e];
+    }
+    float hist[kTC][NH];
     {
-      float s[N];
+      float s[NH];
 #pragma unroll
-      for (int n = 0; n < N; ++n) s[n] = sp[n];
+      for (int n = 0; n < NH; ++n) s[n] = sp[n];
 #pragma unroll
       for (int tt = 0; tt < kTC; ++tt) {
         const int t = t0 + tt;
         if (t < len) {
           float sig;
           const float dt = dt_of(t, sig);
-          const float dtu = dt * ld_act(u + (int64_t)(base + t) * E + e);
-          const float* xr = &sX[t * XW];
+          const float dtu = dt * uc[tt];
+          const float* xr = &sX[t * XW] + R + n0;
 #pragma unroll
-          for (int n = 0; n < N; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
+          for (int n = 0; n < NH; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[n]);
         }
 #pragma unroll
-        for (int n = 0; n < N; ++n) hist[tt][n] = s[n];
+        for (int n = 0; n < NH; ++n) hist[tt][n] = s[n];
       }
     }
 #pragma unroll
@@ -353,48 +368,57 @@ __global__ __launch_bounds__(256) void scan_bwd_kernel(
       const int t = t0 + tt;
       if (t < len) {  // uniform across the block: len is per program
         const int64_t row = base + t;
-        const float* xr = &sX[t * XW];
+        const float* xB = &sX[t * XW] + R + n0;
+        const float* xC = &sX[t * XW] + R + N + n0;
         float sig;
         const float dt = dt_of(t, sig);
-        const float uv = ld_act(u + row * E + e);
-        const float zv = ld_act(xz + row * ldz + E + e);
-        const float yv = ld_act(ysave + row * E + e);
-        const float dgo = dyg[row * E + e];
-        const float dy = dgo * silu(zv);
-        dxz[row * ldz + E + e] = dgo * yv * silu_grad(zv);
-        float red[2 * N];
+        const float uv = uc[tt], zv = zc[tt];
+        const float dy = gc[tt] * silu(zv);
+        float red[2 * NH];
         float gB = 0.f, ddt_a = 0.f;
 #pragma unroll
-        for (int n = 0; n < N; ++n) {
+        for (int n = 0; n < NH; ++n) {
           const float a = __builtin_amdgcn_exp2f(dt * a2[n]);
-          g[n] = fmaf(xr[R + N + n], dy, anext[n] * g[n]);
+          g[n] = fmaf(xC[n], dy, anext[n] * g[n]);
           anext[n] = a;
           const float sprev = tt > 0 ? hist[tt - 1][n] : sp[n];
           const float gsa = g[n] * sprev * a;
-          gB = fmaf(g[n], xr[R + n], gB);
-          ddt_a = fmaf(gsa, An[n], ddt_a);
+          gB = fmaf(g[n], xB[n], gB);
+          ddt_a = fmaf(gsa, a2[n], ddt_a);  // scaled by ln 2 below
           dA[n] = fmaf(gsa, dt, dA[n]);
-          red[n] = g[n] * dt * uv;         // dB_t[n] contribution
-          red[N + n] = dy * hist[tt][n];   // dC_t[n] contribution
+          red[n] = g[n] * dt * uv;          // dB_t[n0 + n] contribution
+          red[NH + n] = dy * hist[tt][n];   // dC_t[n0 + n] contribution
         }
-        dD = fmaf(dy, uv, dD);
-        du_out[row * E + e] = fmaf(Dv, dy, dt * gB);
-        dv_out[row * E + e] = (uv * gB + ddt_a) * sig;
-        const float tot = butterfly32(red, lane);
-        if ((lane & 1) == 0) sRed[wave * 2 * N + (lane >> 1)] = tot;
-        __syncthreads();
-        if (threadIdx.x < 2 * N) {
-          float acc = 0.f;
-          for (int w = 0; w < (int)(blockDim.x >> 6); ++w) acc += sRed[w * 2 * N + threadIdx.x];
-          dxdbl[row * XW + R + threadIdx.x] = acc;
+        gB += __shfl_xor(gB, 1, 64);
+        ddt_a += __shfl_xor(ddt_a, 1, 64);
+        if (hf == 0) {
+          dD = fmaf(dy, uv, dD);
+          dxz[row * ldz + E + e] = gc[tt] * yc[tt] * silu_grad(zv);
+          du_out[row * E + e] = fmaf(Dv, dy, dt * gB);
+          dv_out[row * E + e] = fmaf(ddt_a, kLn2, uv * gB) * sig;
         }
-        __syncthreads();
+        const float tot = butterfly16(red, lane);
+        if ((lane & 2) == 0) {
+          const int k = (lane >> 2) & 15;
+          const int j = k < NH ? n0 + k : N + n0 + (k - NH);
+          sRed[(t * 8 + wave) * 2 * N + j] = tot;
+        }
       }
     }
   }
+  // dB_t, dC_t = sums over the block's wavefronts, for every token at once
+  __syncthreads();
+  const int nw = blockDim.x >> 6;
+  for (int i = tid; i < len * 2 * N; i += blockDim.x) {
+    const int t = i / (2 * N), j = i % (2 * N);
+    float acc = 0.f;
+    for (int w = 0; w < nw; ++w) acc += sRed[(t * 8 + w) * 2 * N + j];
+    dxdbl[(int64_t)(base + t) * XW + R + j] = acc;
+  }
 #pragma unroll
-  for (int n = 0; n < N; ++n) dA_part[((int64_t)b * E + e) * N + n] = dA[n] * An[n];  // d/dA_log
-  dD_part[(int64_t)b * E + e] = dD;
+  for (int n = 0; n < NH; ++n)
+    dA_part[((int64_t)b * E + e) * N + n0 + n] = dA[n] * (a2[n] * kLn2);  // d/dA_log
+  if (hf == 0) dD_part[(int64_t)b * E + e] = dD;
 }
 
 // ---------------------------------------------------------------- conv + SiLU backward
@@ -472,20 +496,31 @@ __global__ __launch_bounds__(256) void colsum_kernel(const int* __restrict__ Mde
 }
 
 // ---------------------------------------------------------------- reductions
-// blockIdx.y picks the job; its elements are summed over the splits in order.
+// blockIdx.y picks the job. A block takes 64 consecutive outputs; its four
+// wavefronts each sum a contiguous quarter of the splits, then the quarters
+// are added in order (deterministic for a given split count).
 __global__ __launch_bounds__(256) void reduce_kernel(const ReduceJob* __restrict__ jobs, int njobs,
                                                      const float* __restrict__ ws,
                                                      float* __restrict__ grad,
                                                      float* __restrict__ loss) {
+  __shared__ float sq[4][64];
   const int j = blockIdx.y;
   if (j >= njobs) return;
   const ReduceJob J = jobs[j];
   float* dst = (J.dst_buf == 0 ? grad : loss) + J.dst;
   const float* src = ws + J.src;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < J.n; i += (int64_t)gridDim.x * 256) {
+  const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int per = (J.nsplit + 3) / 4;
+  const int s0 = q * per, s1 = min(s0 + per, J.nsplit);
+  for (int64_t i0 = (int64_t)blockIdx.x * 64; i0 < J.n; i0 += (int64_t)gridDim.x * 64) {
+    const int64_t i = i0 + lane;
     float acc = 0.f;
-    for (int s = 0; s < J.nsplit; ++s) acc += src[(int64_t)s * J.split_stride + i * J.src_stride];
-    dst[i * J.dst_stride] = acc;
+    if (i < J.n)
+      for (int s = s0; s < s1; ++s) acc += src[(int64_t)s * J.split_stride + i * J.src_stride];
+    sq[q][lane] = acc;
+    __syncthreads();
+    if (q == 0 && i < J.n) dst[i * J.dst_stride] = ((sq[0][lane] + sq[1][lane]) + sq[2][lane]) + sq[3][lane];
+    __syncthreads();
   }
 }
 
@@ -599,11 +634,11 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
                            const float* dyg, const float* W_dt, const float* b_dt,
                            const float* A_log, const float* D, float* ckpt, float* dv, float* du,
                            float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s) {
-  if (N != 16 || E % 64 || E > 256 || B <= 0) return hipErrorInvalidValue;
-  const size_t shm = ((size_t)L * (R + 2 * N) + 4 * 2 * N) * sizeof(float);
+  if (N != 16 || E % 32 || E > 256 || B <= 0) return hipErrorInvalidValue;
+  const size_t shm = ((size_t)L * (R + 2 * N) + (size_t)L * 8 * 2 * N) * sizeof(float);
   if (shm > 64 * 1024) return hipErrorInvalidValue;
 #define TCL_SB(RR)                                                                                    \
-  hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B), dim3(E), shm, s, offs, E, L, u,   \
+  hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B), dim3(2 * E), shm, s, offs, E, L, u,   \
                      xdbl, xz, ysave, dyg, W_dt, b_dt, A_log, D, ckpt, dv, du, dxz, dxdbl, dA_part, \
                      dD_part)
   switch (R) {
@@ -630,7 +665,7 @@ hipError_t launch_conv_bwd(int B, int E, int K, const int* offs, const uint16_t*
   return hipGetLastError();
 }
 
-int colsum_splits(int Mmax) { return min(64, max(1, (Mmax + 255) / 256)); }
+int colsum_splits(int Mmax) { return min(1024, max(1, (Mmax + 31) / 32)); }
 
 hipError_t launch_colsum(const int* Mdev, int Mmax, const float* A, int64_t lda, int C, int splits,
                          float* part, hipStream_t s) {
@@ -643,7 +678,7 @@ hipError_t launch_colsum(const int* Mdev, int Mmax, const float* A, int64_t lda,
 hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, const float* ws,
                          float* grad, float* loss, hipStream_t s) {
   if (njobs <= 0) return hipSuccess;
-  const int gx = (int)std::min<int64_t>((max_n + 255) / 256, 256);
+  const int gx = (int)std::min<int64_t>((max_n + 63) / 64, 512);
   hipLaunchKernelGGL(reduce_kernel, dim3(gx, njobs), dim3(256), 0, s, d_jobs, njobs, ws, grad, loss);
   return hipGetLastError();
 }
