@@ -208,6 +208,53 @@ def bench_distill(args, w):
     print(json.dumps(rec), flush=True)
 
 
+def scan_sweep(args):
+    """Time the sequential scan and the chunked two-level scan on their own
+    (kernel-level entry point, HIP events on the launch stream) for programs
+    of length 64..256, batch sizes from the long-sequence workload (8192)
+    down to 16. Prints one JSON line."""
+    import numpy as np
+    import torch
+
+    from paper_2604_12891_amd import binding as tb
+
+    E, N, R, L = 512, 16, 16, 256
+    rng = np.random.default_rng(7)
+    out = []
+    for B in (8192, 1024, 256, 64, 16):
+        lengths = rng.integers(64, L + 1, size=B).astype(np.int32)
+        rows = int(lengths.sum())
+        offs = torch.from_numpy(np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)).cuda()
+        u = torch.randn(rows, E, device="cuda")
+        z = torch.randn(rows, E, device="cuda")
+        xdbl = 0.5 * torch.randn(rows, R + 2 * N, device="cuda")
+        W_dt = 0.25 * torch.rand(E, R, device="cuda") - 0.125
+        b_dt = torch.full((E,), -4.0, device="cuda")
+        A_log = torch.log(torch.arange(1, N + 1, device="cuda", dtype=torch.float32)).repeat(E, 1)
+        D = torch.ones(E, device="cuda")
+        res = torch.empty_like(u)
+        rec = {"B": B, "valid_tokens": rows}
+        for chunks in (0, 2, 4, 8):
+            for _ in range(3):
+                tb.scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, res, chunks=chunks)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = max(3, min(50, int(2e6 // rows)))
+            e0.record()
+            for _ in range(reps):
+                tb.scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, res, chunks=chunks)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            key = "sequential" if chunks == 0 else f"chunked{chunks}"
+            rec[key + "_ms"] = round(ms, 5)
+            rec[key + "_GBps"] = round(rows * (3 * E * 4 + (R + 2 * N) * 4) / (ms * 1e-3) / 1e9, 1)
+        out.append(rec)
+        del u, z, xdbl, res
+        torch.cuda.empty_cache()
+    print(json.dumps({"scan_sweep": out, "L": L, "E": E, "N": N, "dtype": "f32",
+                      "lengths": "uniform 64..256"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,6 +264,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernels", action="store_true", help="print the per-kernel table to stderr")
+    ap.add_argument("--scan-sweep", action="store_true",
+                    help="time the sequential against the chunked scan over batch sizes and exit")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -224,6 +273,10 @@ def main():
               "(batches shard across GPUs by program with no exchange but the scores); run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.scan_sweep:
+        scan_sweep(args)
+        return
 
     import numpy as np
     import torch

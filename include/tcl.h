@@ -239,8 +239,11 @@ TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const
 /* Selective scan with its dt_proj + softplus prologue and gate epilogue,
  * fp32: out = (scan(u, softplus(dt_r W_dt^T + b_dt), -exp(A_log), B, C) +
  * D u) * SiLU(z), with [dt_r|B|C] = d_xdbl rows of R + 2N values and z read
- * from d_z with leading dimension ldz. N must be 16. */
-TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R,
+ * from d_z with leading dimension ldz. N must be 16. chunks = 0 runs the
+ * sequential scan (one thread per program and channel); 1..8 runs the
+ * chunked two-level scan with that many concurrent chunks per program
+ * (tcl_score picks it when the batch is too small to fill the GPU). */
+TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R, int32_t chunks,
                                      const int32_t* d_offs, const float* d_u, const float* d_xdbl,
                                      const float* d_z, int32_t ldz, const float* d_W_dt,
                                      const float* d_b_dt, const float* d_A_log, const float* d_D,

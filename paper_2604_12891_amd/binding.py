@@ -62,7 +62,7 @@ _SIGS = {
     "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
-    "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
+    "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                  _vp, _vp, _vp]),
 }
 
@@ -286,12 +286,13 @@ def conv_silu_f32(offs, x, w, b, E, out, ldx=None, stream=None):
     return out
 
 
-def scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, out, ldz=None, stream=None):
+def scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, out, ldz=None, stream=None, chunks=0):
+    """chunks = 0: sequential scan; 1..8: chunked two-level scan."""
     B = offs.numel() - 1
     E = u.shape[1]
     N = A_log.shape[1]
     R = W_dt.shape[1]
-    check(lib().tcl_test_scan_f32(B, E, N, R, offs.data_ptr(), u.data_ptr(), xdbl.data_ptr(), z.data_ptr(),
+    check(lib().tcl_test_scan_f32(B, E, N, R, chunks, offs.data_ptr(), u.data_ptr(), xdbl.data_ptr(), z.data_ptr(),
                                   z.shape[1] if ldz is None else ldz, W_dt.data_ptr(), b_dt.data_ptr(),
                                   A_log.data_ptr(), D.data_ptr(), out.data_ptr(), _stream(stream)))
     return out

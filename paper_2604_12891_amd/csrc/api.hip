@@ -129,6 +129,7 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
   float* xdbl = reinterpret_cast<float*>(ws + p.xdbl);
   const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
   const int Mmax = B * L;
+  const int chunks = scan_chunks_for(B, E, L);
   Timing& T = m->timing;
 
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
@@ -155,8 +156,13 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
       TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_f32(gx, 0, kNarrow, s));
 
-      TCL_LAUNCH(T, "scan", launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                               W.b_dt, W.A_log, W.D, u, s));
+      if (chunks > 0)
+        TCL_LAUNCH(T, "scan_chunked", launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E,
+                                                                 2 * E, W.W_dt, W.b_dt, W.A_log, W.D,
+                                                                 u, s));
+      else
+        TCL_LAUNCH(T, "scan", launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                                 W.b_dt, W.A_log, W.D, u, s));
       GemmArgs go;
       go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
       go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
@@ -185,8 +191,13 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
       TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32Narrow, s));
 
-      TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                                  W.b_dt, W.A_log, W.D, u, s));
+      if (chunks > 0)
+        TCL_LAUNCH(T, "scan_chunked", launch_scan_chunked<uint16_t>(B, E, N, R, chunks, offs, u, xdbl,
+                                                                    xz + E, 2 * E, W.W_dt, W.b_dt,
+                                                                    W.A_log, W.D, u, s));
+      else
+        TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                                    W.b_dt, W.A_log, W.D, u, s));
       GemmArgsBF16 go;
       go.A = u; go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = H; go.ldc = d;
       go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
@@ -539,17 +550,22 @@ TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const
   return TCL_OK;
 }
 
-TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R,
+TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R, int32_t chunks,
                                      const int32_t* d_offs, const float* d_u, const float* d_xdbl,
                                      const float* d_z, int32_t ldz, const float* d_W_dt,
                                      const float* d_b_dt, const float* d_A_log, const float* d_D,
                                      float* d_out, void* stream) {
   if (B <= 0 || E <= 0 || ldz < E) return fail(TCL_ERR_INVALID_ARG, "bad sizes");
+  if (chunks < 0 || chunks > 8) return fail(TCL_ERR_INVALID_ARG, "chunks must be in [0, 8]");
   if (N != 16) return fail(TCL_ERR_UNSUPPORTED, "d_state must be 16");
   if (R % 4 || R <= 0 || R > 32) return fail(TCL_ERR_UNSUPPORTED, "dt_rank must be 4..32, step 4");
   if (!d_offs || !d_u || !d_xdbl || !d_z || !d_W_dt || !d_b_dt || !d_A_log || !d_D || !d_out)
     return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
-  TCL_HIP(launch_scan<float>(B, E, N, R, d_offs, d_u, d_xdbl, d_z, ldz, d_W_dt, d_b_dt, d_A_log,
-                             d_D, d_out, static_cast<hipStream_t>(stream)));
+  if (chunks > 0)
+    TCL_HIP(launch_scan_chunked<float>(B, E, N, R, chunks, d_offs, d_u, d_xdbl, d_z, ldz, d_W_dt,
+                                       d_b_dt, d_A_log, d_D, d_out, static_cast<hipStream_t>(stream)));
+  else
+    TCL_HIP(launch_scan<float>(B, E, N, R, d_offs, d_u, d_xdbl, d_z, ldz, d_W_dt, d_b_dt, d_A_log,
+                               d_D, d_out, static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }

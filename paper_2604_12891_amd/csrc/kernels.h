@@ -118,6 +118,17 @@ hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, 
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
                        const float* D, T* out, hipStream_t s, T* ysave = nullptr);
 
+// The same scan as a chunked two-level scan: each program's tokens are split
+// into `chunks` (1..8) that are scanned concurrently and stitched through
+// their affine summaries. scan_chunks_for picks the chunk count the batch
+// needs to fill the GPU (0: the sequential kernel already does).
+template <typename T>
+hipError_t launch_scan_chunked(int B, int E, int N, int R, int chunks, const int* offs, const T* u,
+                               const float* xdbl, const T* z, int ldz, const float* W_dt,
+                               const float* b_dt, const float* A_log, const float* D, T* out,
+                               hipStream_t s);
+int scan_chunks_for(int B, int E, int L);
+
 // Final RMSNorm (optional) + masked mean-pool + Linear-ReLU-Linear head.
 // W1T is W1 transposed ([d, h]). Programs with invalid lengths get NaN.
 // pooled_out [B, d] and a1_out [B, h] (optional) keep the pooled vector and

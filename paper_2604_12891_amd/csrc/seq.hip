@@ -217,6 +217,99 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
   }
 }
 
+// ---------------------------------------------------------------- chunked two-level scan
+// For batches too small to fill the GPU with one thread per (program,
+// channel): the sequence is split into W chunks that run concurrently, one
+// wavefront each, for 64 channels of one program (lane = channel, so every
+// load stays coalesced). The recurrence s_t = a_t s_{t-1} + b_t is affine, so
+// a chunk acts on its incoming state as s -> P s + s_loc with
+// P = prod_t a_t = exp(A sum_t dt_t) and s_loc the chunk's end state from a
+// zero start. Level 1: every wavefront scans its chunk from zero and parks
+// (P, s_loc) in LDS. Level 2: after one barrier each wavefront folds the
+// summaries of the chunks before it into its incoming state and re-runs its
+// chunk from there, writing the outputs. This spends twice the exponentials
+// of the sequential scan; it pays only when the extra concurrency is needed.
+template <typename T, int N, int R>
+__global__ __launch_bounds__(512) void scan_chunked_kernel(
+    const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
+    const T* __restrict__ z, int ldz, const float* __restrict__ W_dt,
+    const float* __restrict__ b_dt, const float* __restrict__ A_log,
+    const float* __restrict__ Dp, T* out) {
+  constexpr int XW = R + 2 * N;
+  extern __shared__ float sSum[];  // [W chunks][64 lanes][2N]: P | s_loc
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nw = blockDim.x >> 6;
+  const int e = blockIdx.y * 64 + lane;
+  const bool active = e < E;
+  const int ec = active ? e : 0;
+  const int base = offs[b], len = offs[b + 1] - base;
+  const int tpc = (len + nw - 1) / nw;  // tokens per chunk
+  const int t_begin = min(w * tpc, len), t_end = min(t_begin + tpc, len);
+
+  float a2[N], wdt[R];
+#pragma unroll
+  for (int n = 0; n < N; ++n) a2[n] = -expf(A_log[ec * N + n]) * kLog2e;
+#pragma unroll
+  for (int r = 0; r < R; ++r) wdt[r] = W_dt[ec * R + r];
+  const float bdt = b_dt[ec], Dv = Dp[ec];
+
+  auto dt_at = [&](const float* xr) {
+    float v = bdt;
+#pragma unroll
+    for (int r = 0; r < R; ++r) v = fmaf(wdt[r], xr[r], v);
+    return softplus(v);
+  };
+
+  // level 1: the chunk's summary from a zero incoming state
+  float s[N];
+  float sumdt = 0.f;
+#pragma unroll
+  for (int n = 0; n < N; ++n) s[n] = 0.f;
+  for (int t = t_begin; t < t_end; ++t) {
+    const float* xr = xdbl + (int64_t)(base + t) * XW;  // wavefront-uniform row
+    const float dt = dt_at(xr);
+    sumdt += dt;
+    const float dtu = dt * ld1(u + (int64_t)(base + t) * E + ec);
+#pragma unroll
+    for (int n = 0; n < N; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
+  }
+  float* mine = sSum + ((int64_t)w * 64 + lane) * 2 * N;
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    mine[n] = __builtin_amdgcn_exp2f(a2[n] * sumdt);
+    mine[N + n] = s[n];
+  }
+  __syncthreads();
+
+  // level 2: incoming state = fold of the earlier chunks' summaries, then re-run
+#pragma unroll
+  for (int n = 0; n < N; ++n) s[n] = 0.f;
+  for (int j = 0; j < w; ++j) {
+    const float* sj = sSum + ((int64_t)j * 64 + lane) * 2 * N;
+#pragma unroll
+    for (int n = 0; n < N; ++n) s[n] = fmaf(sj[n], s[n], sj[N + n]);
+  }
+  if (!active) return;
+  for (int t = t_begin; t < t_end; ++t) {
+    const int64_t row = base + t;
+    const float* xr = xdbl + row * XW;
+    const float dt = dt_at(xr);
+    const float uv = ld1(u + row * E + e);
+    const float zv = ld1(z + row * ldz + e);
+    const float dtu = dt * uv;
+    float y = 0.f;
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+      s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
+      y = fmaf(s[n], xr[R + N + n], y);
+    }
+    y = fmaf(Dv, uv, y);
+    st1(out + row * E + e, y * silu(zv));
+  }
+}
+
 // ---------------------------------------------------------------- tail
 // PB programs per workgroup. Phase 1: each wavefront pools whole programs
 // (per token: RMSNorm statistics by a wavefront reduction, then accumulate
@@ -342,6 +435,43 @@ hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, in
 }
 
 template <typename T>
+hipError_t launch_scan_chunked(int B, int E, int N, int R, int chunks, const int* offs, const T* u,
+                               const float* xdbl, const T* z, int ldz, const float* W_dt,
+                               const float* b_dt, const float* A_log, const float* D, T* out,
+                               hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  if (N != 16 || chunks < 1 || chunks > 8) return hipErrorInvalidValue;
+  dim3 grid(B, (E + 63) / 64);
+  const size_t shm = (size_t)chunks * 64 * 2 * N * sizeof(float);
+#define TCL_SCANC(RR)                                                                          \
+  hipLaunchKernelGGL((scan_chunked_kernel<T, 16, RR>), grid, dim3(64 * chunks), shm, s, offs, E, u, \
+                     xdbl, z, ldz, W_dt, b_dt, A_log, D, out)
+  switch (R) {
+    case 4: TCL_SCANC(4); break;
+    case 8: TCL_SCANC(8); break;
+    case 12: TCL_SCANC(12); break;
+    case 16: TCL_SCANC(16); break;
+    case 20: TCL_SCANC(20); break;
+    case 24: TCL_SCANC(24); break;
+    case 28: TCL_SCANC(28); break;
+    case 32: TCL_SCANC(32); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_SCANC
+  return hipGetLastError();
+}
+
+int scan_chunks_for(int B, int E, int L) {
+  // one thread per (program, channel) gives B*E/64 wavefronts; below ~4 per
+  // SIMD of the 256 CUs the chunked scan adds the concurrency that is missing
+  const int64_t waves = (int64_t)B * ((E + 63) / 64);
+  if (L < 64 || waves >= 4096) return 0;
+  int c = 2;
+  while (c < 8 && waves * c < 4096 && L / (2 * c) >= 8) c *= 2;
+  return c;
+}
+
+template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
                        const float* D, T* out, hipStream_t s, T* ysave) {
@@ -370,6 +500,14 @@ template hipError_t launch_conv_silu<float>(int, int, int, const int*, const flo
                                             const float*, float*, hipStream_t);
 template hipError_t launch_conv_silu<uint16_t>(int, int, int, const int*, const uint16_t*, int,
                                                const float*, const float*, uint16_t*, hipStream_t);
+template hipError_t launch_scan_chunked<float>(int, int, int, int, int, const int*, const float*,
+                                               const float*, const float*, int, const float*,
+                                               const float*, const float*, const float*, float*,
+                                               hipStream_t);
+template hipError_t launch_scan_chunked<uint16_t>(int, int, int, int, int, const int*,
+                                                  const uint16_t*, const float*, const uint16_t*, int,
+                                                  const float*, const float*, const float*,
+                                                  const float*, uint16_t*, hipStream_t);
 template hipError_t launch_scan<float>(int, int, int, int, const int*, const float*, const float*,
                                        const float*, int, const float*, const float*, const float*,
                                        const float*, float*, hipStream_t, float*);

@@ -105,15 +105,17 @@ def test_conv_silu_f32(K):
 
 
 @pytest.mark.parametrize("R", [4, 16])
-@pytest.mark.parametrize("L", [1, 25, 70])
-def test_scan_f32(R, L):
+@pytest.mark.parametrize("L", [1, 25, 70, 256])
+@pytest.mark.parametrize("chunks", [0, 1, 3, 8])
+def test_scan_f32(R, L, chunks):
+    """chunks = 0: sequential scan; > 0: the chunked two-level scan."""
     N, E = 16, 320
     rng = np.random.default_rng(R * 100 + L)
     lengths = rng.integers(1, L + 1, size=11).astype(np.int32)
     lengths[0] = L
     lengths[1] = 1
     B = len(lengths)
-    print(f"scan R={R} L={L} B={B} E={E}", flush=True)
+    print(f"scan R={R} L={L} B={B} E={E} chunks={chunks}", flush=True)
     rows = int(lengths.sum())
     u = rng.standard_normal((rows, E)).astype(np.float32)
     z = rng.standard_normal((rows, E)).astype(np.float32)
@@ -124,7 +126,7 @@ def test_scan_f32(R, L):
     D = rng.standard_normal(E).astype(np.float32)
     out = torch.full((rows, E), float("nan"), device="cuda")
     tb.scan_f32(_dev(_offs(lengths), torch.int32), _dev(u), _dev(xdbl), _dev(z), _dev(W_dt), _dev(b_dt),
-                _dev(A_log), _dev(D), out)
+                _dev(A_log), _dev(D), out, chunks=chunks)
     torch.cuda.synchronize()
     f = lambda a: a.astype(np.float64)
     up, zp, xd = (_unpack(f(a), lengths, L) for a in (u, z, xdbl))
@@ -137,7 +139,8 @@ def test_scan_f32(R, L):
     assert np.all(err <= 1e-4 * (np.abs(expect) + scale)), float(np.max(err / (np.abs(expect) + scale)))
 
 
-def test_scan_in_place_matches_out_of_place():
+@pytest.mark.parametrize("chunks", [0, 4])
+def test_scan_in_place_matches_out_of_place(chunks):
     """The model runs the scan with out aliasing u; results must not change."""
     N, E, R = 16, 128, 4
     rng = np.random.default_rng(3)
@@ -153,8 +156,8 @@ def test_scan_in_place_matches_out_of_place():
     d = [_dev(a) for a in args]
     offs = _dev(_offs(lengths), torch.int32)
     out = torch.empty_like(d[0])
-    tb.scan_f32(offs, *d, out)
+    tb.scan_f32(offs, *d, out, chunks=chunks)
     u_copy = d[0].clone()
-    tb.scan_f32(offs, u_copy, *d[1:], u_copy)
+    tb.scan_f32(offs, u_copy, *d[1:], u_copy, chunks=chunks)
     torch.cuda.synchronize()
     assert torch.equal(out, u_copy)

@@ -72,6 +72,21 @@ def test_long_sequences_sampled():
     assert_scores_match(g[idx], oracle_scores(blob, X[idx], lengths[idx], w.model), "f32", w.name)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_long_sequences_small_batch(dtype):
+    """A batch too small to fill the GPU with one thread per (program,
+    channel): tcl_score runs the chunked two-level scan here."""
+    w = wl.WORKLOADS["score_B8192_L256_d256_f32"]
+    blob, X, lengths = wl.make_workload(w.name, B=6, perturb=True)
+    lengths[0], lengths[1] = 256, 64
+    X[np.arange(256)[None, :] >= lengths[:, None]] = 0
+    if dtype == "bf16":
+        blob = wl.round_to_bf16(blob)
+    print(f"tcl_score B=6 L=256 {dtype} (chunked scan)", flush=True)
+    g = _score(_model(w.model, blob, dtype), X, lengths)
+    assert_scores_match(g, oracle_scores(blob, X, lengths, w.model), dtype, "small batch, long sequences")
+
+
 @pytest.mark.parametrize("perturb", [False, True])
 def test_tiny_bf16(perturb):
     """The bf16 path (bf16 weights and activations, fp32 accumulation and scan
