@@ -462,12 +462,14 @@ hipError_t launch_scan_chunked(int B, int E, int N, int R, int chunks, const int
 }
 
 int scan_chunks_for(int B, int E, int L) {
-  // one thread per (program, channel) gives B*E/64 wavefronts; below ~4 per
-  // SIMD of the 256 CUs the chunked scan adds the concurrency that is missing
+  // One thread per (program, channel) gives B*E/64 wavefronts. Measured on
+  // MI355X at L = 256, E = 512: the sequential scan wins from 2048 wavefronts
+  // up (B >= 256), the chunked scan from 512 down (1.7x at B = 64 with 4
+  // chunks, 2.3x at B = 16 with 4-8). Aim for >= 2048 wavefronts in total.
   const int64_t waves = (int64_t)B * ((E + 63) / 64);
-  if (L < 64 || waves >= 4096) return 0;
+  if (L < 64 || waves >= 1024) return 0;
   int c = 2;
-  while (c < 8 && waves * c < 4096 && L / (2 * c) >= 8) c *= 2;
+  while (c < 8 && waves * c < 2048 && L / (2 * c) >= 8) c *= 2;
   return c;
 }
 
