@@ -216,11 +216,17 @@ TCL_API const char* tcl_last_error(void);
  * every [rows, C] activation (row-major, leading dimension C unless given).
  * ------------------------------------------------------------------- */
 
-/* C[M,N] = A[M,K] W[N,K]^T (+ bias[N] if d_bias) in fp32 via the fp32 MFMA
- * GEMM used by the model's projections. K % 4 == 0. */
+/* fp32 MFMA GEMM used by the model's projections, K % 4 == 0:
+ *   epilogue 0: C[M,N] = A W^T (+ bias[N] if d_bias)
+ *   epilogue 1: C += A W^T            (the residual epilogue, C read in place)
+ *   epilogue 2: C = rstd(A) * A W^T  with rstd(A)_m = (mean_k A[m,k]^2 + 1e-5)^-1/2
+ *               (the RMSNorm prologue; the gain is folded into W by the model)
+ * tile selects the workgroup tile (0..7: 128x128, 64x64, 64x128, 128x64,
+ * 128x256, and 128x128 / 64x128 / 128x64 with K staged 64 at a time); -1
+ * picks what the model would use for M rows. */
 TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const float* d_A,
-                                     const float* d_W, const float* d_bias, float* d_C,
-                                     void* stream);
+                                     const float* d_W, const float* d_bias, float* d_C, int32_t tile,
+                                     int32_t epilogue, void* stream);
 
 /* Same with bf16 operands (row-major bf16 bit patterns, K % 8 == 0) on the
  * bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16), fp32 accumulation and output. */

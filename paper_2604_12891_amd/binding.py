@@ -59,7 +59,7 @@ _SIGS = {
     "tcl_trainer_timing_get": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                                       ctypes.POINTER(ctypes.c_int64)]),
     "tcl_trainer_timing_reset": (_i32, [_vp]),
-    "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _i32, _vp]),
     "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
@@ -255,14 +255,15 @@ class Trainer:
         return out
 
 
-def gemm_f32(A, W, bias=None, out=None, stream=None):
+def gemm_f32(A, W, bias=None, out=None, stream=None, tile=-1, epilogue=0):
+    """epilogue 0: A W^T (+ bias); 1: out += A W^T; 2: rstd(A) * A W^T."""
     import torch
     M, K = A.shape
     N = W.shape[0]
     if out is None:
         out = torch.empty(M, N, dtype=torch.float32, device=A.device)
-    check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(),
-                                  _stream(stream)))
+    check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(), tile,
+                                  epilogue, _stream(stream)))
     return out
 
 

@@ -57,15 +57,20 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// bf16 <-> fp32. bf16 is the high half of an fp32; rounding is to nearest,
-// ties to even (NaN inputs are not produced by the model's arithmetic).
+// bf16 <-> fp32. bf16 is the high half of an fp32. Narrowing uses gfx950's
+// v_cvt_pk_bf16_f32 (round to nearest, ties to even).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(((uint32_t)h) << 16);
 }
+// two values -> one 32-bit word, a in the low half
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float a, float b) {
+  const bf16x2_t h = __builtin_convertvector(floatx2_t{a, b}, bf16x2_t);
+  return __builtin_bit_cast(uint32_t, h);
+}
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  return (uint16_t)(f32x2_to_bf16x2(f, 0.0f) & 0xFFFFu);
 }
 
 }  // namespace tcl

@@ -29,9 +29,7 @@ constexpr int BK = 64;          // k per chunk (bf16 elements)
 constexpr int PITCH = BK + 8;   // bf16 per LDS row: 144 bytes, conflict-free 8-lane b128 reads
 constexpr int Q = BK / 8;       // 16-byte units per row chunk
 
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  return (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
-}
+__device__ __forceinline__ uint32_t pack2(float a, float b) { return f32x2_to_bf16x2(a, b); }
 
 template <typename TA, typename TC, int WM, int WN, int TM, int TN, int FL>
 __global__ __launch_bounds__(WM* WN * 64) void gemm_bf16_kernel(GemmArgsBF16 p, int ntm, int ntn) {
@@ -98,6 +96,14 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_bf16_kernel(GemmArgsBF16 p, 
 
   auto gload = [&](int k0) {
     const int k = k0 + q8;
+    // the gain slice is the same for every row this thread stages
+    floatx4 g0 = floatx4{1.f, 1.f, 1.f, 1.f}, g1 = g0;
+    if constexpr (kNorm) {
+      if (k < p.K) {
+        g0 = *reinterpret_cast<const floatx4*>(p.gain + k);
+        g1 = *reinterpret_cast<const floatx4*>(p.gain + k + 4);
+      }
+    }
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       if constexpr (kF32A) {
@@ -109,12 +115,8 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_bf16_kernel(GemmArgsBF16 p, 
         if constexpr (kNorm) {
           ss[i] += lo.x * lo.x + lo.y * lo.y + lo.z * lo.z + lo.w * lo.w +
                    hi.x * hi.x + hi.y * hi.y + hi.z * hi.z + hi.w * hi.w;
-          if (k < p.K) {
-            const floatx4 g0 = *reinterpret_cast<const floatx4*>(p.gain + k);
-            const floatx4 g1 = *reinterpret_cast<const floatx4*>(p.gain + k + 4);
-            lo *= g0;
-            hi *= g1;
-          }
+          lo *= g0;
+          hi *= g1;
         }
         ra[i] = u32x4{pack2(lo.x, lo.y), pack2(lo.z, lo.w), pack2(hi.x, hi.y), pack2(hi.z, hi.w)};
       } else {
@@ -200,7 +202,18 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_bf16_kernel(GemmArgsBF16 p, 
 #pragma unroll
     for (int b = 0; b < TN; ++b) {
       const int col = col0 + wn * TN * 32 + b * 32 + li;
-      if (col >= p.N) continue;
+      const bool cok = col < p.N;
+      // a block's residual loads go before its stores (C may be read in place)
+      float res[16];
+      if constexpr ((FL & kResid) != 0 && sizeof(TC) == 4) {
+        const float* R = p.R ? p.R : reinterpret_cast<const float*>(p.C);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + wm * TM * 32 + a * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+          res[r] = (cok && row < M) ? R[(int64_t)row * p.ldc + col] : 0.f;
+        }
+      }
+      if (!cok) continue;
       const float bias = (FL & kBias) ? p.bias[col] : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -212,8 +225,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_bf16_kernel(GemmArgsBF16 p, 
         v += bias;
         TC* dst = reinterpret_cast<TC*>(p.C) + (int64_t)row * p.ldc + col;
         if constexpr (sizeof(TC) == 4) {
-          if constexpr ((FL & kResid) != 0)
-            v += p.R ? p.R[(int64_t)row * p.ldc + col] : *reinterpret_cast<float*>(dst);
+          if constexpr ((FL & kResid) != 0) v += res[r];
           *reinterpret_cast<float*>(dst) = v;
         } else {
           *reinterpret_cast<uint16_t*>(dst) = f32_to_bf16(v);

@@ -23,12 +23,15 @@
 namespace tcl {
 namespace {
 
-constexpr int BK = 32;
-constexpr int PITCH = BK + 4;  // floats; 144-byte rows keep 8 lanes of b128 reads conflict-free
-constexpr int Q = BK / 4;      // float4 per row chunk
-
-template <int WM, int WN, int TM, int TN, int FL>
-__global__ __launch_bounds__(WM* WN * 64) void gemm_f32_kernel(GemmArgs p, int ntm, int ntn) {
+// Occupancy target: 3 wavefronts per SIMD for K chunks of 32 (the register
+// file then holds three workgroups' tiles), 2 for chunks of 64.
+template <int WM, int WN, int TM, int TN, int BK, int FL>
+__global__ __launch_bounds__(WM* WN * 64, BK == 32 ? 3 : 2) void gemm_f32_kernel(GemmArgs p, int ntm,
+                                                                                 int ntn) {
+  // BK + 4 floats per LDS row: 144- or 272-byte rows keep 8 lanes of b128 reads conflict-free
+  constexpr int PITCH = BK + 4;
+  constexpr int Q = BK / 4;        // float4 per row chunk
+  constexpr int KH = BK / 2;       // k per lane half within a chunk
   constexpr int NT = WM * WN * 64;
   constexpr int BM = WM * TM * 32;
   constexpr int BN = WN * TN * 32;
@@ -140,28 +143,24 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_f32_kernel(GemmArgs p, int n
     __syncthreads();
     if (k0 + BK < p.K) gload(k0 + BK);
 
-    floatx4 a4[TM][4], b4[TN][4];
+    // fragments are read four k at a time, just ahead of the MFMAs that use them
+    const float* srcA = &sA[(wm * TM * 32 + li) * PITCH + lg * KH];
+    const float* srcB = &sB[(wn * TN * 32 + li) * PITCH + lg * KH];
 #pragma unroll
-    for (int a = 0; a < TM; ++a) {
-      const float* src = &sA[(wm * TM * 32 + a * 32 + li) * PITCH + lg * 16];
+    for (int c = 0; c < KH / 4; ++c) {
+      floatx4 a4[TM], b4[TN];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) a4[a][c] = *reinterpret_cast<const floatx4*>(src + 4 * c);
-    }
+      for (int a = 0; a < TM; ++a) a4[a] = *reinterpret_cast<const floatx4*>(srcA + a * 32 * PITCH + 4 * c);
 #pragma unroll
-    for (int b = 0; b < TN; ++b) {
-      const float* src = &sB[(wn * TN * 32 + b * 32 + li) * PITCH + lg * 16];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) b4[b][c] = *reinterpret_cast<const floatx4*>(src + 4 * c);
-    }
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
+      for (int b = 0; b < TN; ++b) b4[b] = *reinterpret_cast<const floatx4*>(srcB + b * 32 * PITCH + 4 * c);
 #pragma unroll
       for (int e = 0; e < 4; ++e)
 #pragma unroll
         for (int a = 0; a < TM; ++a)
 #pragma unroll
           for (int b = 0; b < TN; ++b)
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[a][c][e], b4[b][c][e], acc[a][b], 0, 0, 0);
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(a4[a][e], b4[b][e], acc[a][b], 0, 0, 0);
+    }
   }
 
   if constexpr (kNorm) {
@@ -180,13 +179,25 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_f32_kernel(GemmArgs p, int n
   }
 
   // Accumulator layout of a 32x32 block: lane l holds column l % 32 and rows
-  // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15.
+  // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15. With a residual, a block's 16
+  // residual loads are issued before its 16 stores (C may be read in place, so
+  // loads cannot move past earlier stores).
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) {
       const int col = col0 + wn * TN * 32 + b * 32 + li;
-      if (col >= p.N) continue;
+      const bool cok = col < p.N;
+      float res[16];
+      if constexpr ((FL & kResid) != 0) {
+        const float* R = p.R ? p.R : p.C;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + wm * TM * 32 + a * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+          res[r] = (cok && row < M) ? R[(int64_t)row * p.ldc + col] : 0.f;
+        }
+      }
+      if (!cok) continue;
       const float bias = (FL & kBias) ? p.bias[col] : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -196,43 +207,65 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_f32_kernel(GemmArgs p, int n
         float v = acc[a][b][r];
         if constexpr (kNorm) v *= sR[rl];
         v += bias;
-        float* dst = p.C + (int64_t)row * p.ldc + col;
-        if constexpr ((FL & kResid) != 0) v += p.R ? p.R[(int64_t)row * p.ldc + col] : *dst;
-        *dst = v;
+        if constexpr ((FL & kResid) != 0) v += res[r];
+        p.C[(int64_t)row * p.ldc + col] = v;
       }
     }
   }
 }
 
-template <int WM, int WN, int TM, int TN, int FL>
+template <int WM, int WN, int TM, int TN, int BK, int FL>
 hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
   constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
   const int ntm = (a.Mmax + BM - 1) / BM;
   const int ntn = (a.N + BN - 1) / BN;
   const int grid = 8 * ntn * ((ntm + 7) / 8);
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_f32_kernel<WM, WN, TM, TN, FL>), dim3(grid), dim3(WM * WN * 64), 0, s,
+  hipLaunchKernelGGL((gemm_f32_kernel<WM, WN, TM, TN, BK, FL>), dim3(grid), dim3(WM * WN * 64), 0, s,
                      a, ntm, ntn);
   return hipGetLastError();
 }
 
-template <int WM, int WN, int TM, int TN>
+template <int WM, int WN, int TM, int TN, int BK>
 hipError_t dispatch_flags(const GemmArgs& a, int flags, hipStream_t s) {
   switch (flags) {
-    case 0: return launch_t<WM, WN, TM, TN, 0>(a, s);
-    case kBias: return launch_t<WM, WN, TM, TN, kBias>(a, s);
-    case kResid: return launch_t<WM, WN, TM, TN, kResid>(a, s);
-    case kRowNorm: return launch_t<WM, WN, TM, TN, kRowNorm>(a, s);
-    case kBias | kGather: return launch_t<WM, WN, TM, TN, kBias | kGather>(a, s);
+    case 0: return launch_t<WM, WN, TM, TN, BK, 0>(a, s);
+    case kBias: return launch_t<WM, WN, TM, TN, BK, kBias>(a, s);
+    case kResid: return launch_t<WM, WN, TM, TN, BK, kResid>(a, s);
+    case kRowNorm: return launch_t<WM, WN, TM, TN, BK, kRowNorm>(a, s);
+    case kBias | kGather: return launch_t<WM, WN, TM, TN, BK, kBias | kGather>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 }  // namespace
 
+GemmTile pick_gemm_f32_tile(int Mmax, int N, int K) {
+  // Measured on MI355X with the model's epilogues (fp32 MFMA, TFLOP/s, three
+  // wavefronts per SIMD): at ~62K rows 64x128 tiles win (in_proj with the
+  // RMSNorm prologue 104 vs 98 for 128x128; out_proj with the residual 100 vs
+  // 78), because the last partial round of workgroups is shorter; the
+  // gathered input Linear (K = 164) prefers 128x128 with K chunks of 64
+  // (81 vs 67). At ~1.3M rows 128x128 is best for in_proj (115) and 64x128
+  // for out_proj (113).
+  if (N <= 64) return kNarrow;
+  if (K % 64 != 0) return Mmax >= 500000 ? kWide : kTile128x128K64;
+  if (Mmax >= 500000 && N >= 1024) return kWide;
+  return kTile64x128;
+}
+
 hipError_t launch_gemm_f32(const GemmArgs& a, int flags, GemmTile tile, hipStream_t s) {
-  if (tile == kWide) return dispatch_flags<2, 2, 2, 2>(a, flags, s);
-  return dispatch_flags<2, 2, 1, 1>(a, flags, s);
+  switch (tile) {
+    case kWide: return dispatch_flags<2, 2, 2, 2, 32>(a, flags, s);
+    case kNarrow: return dispatch_flags<2, 2, 1, 1, 32>(a, flags, s);
+    case kTile64x128: return dispatch_flags<2, 2, 1, 2, 32>(a, flags, s);
+    case kTile128x64: return dispatch_flags<2, 2, 2, 1, 32>(a, flags, s);
+    case kTile128x256: return dispatch_flags<2, 4, 2, 2, 32>(a, flags, s);
+    case kTile128x128K64: return dispatch_flags<2, 2, 2, 2, 64>(a, flags, s);
+    case kTile64x128K64: return dispatch_flags<2, 2, 1, 2, 64>(a, flags, s);
+    case kTile128x64K64: return dispatch_flags<2, 2, 2, 1, 64>(a, flags, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace tcl

@@ -34,11 +34,24 @@ struct GemmArgs {
   float eps = 0.f;
 };
 
-// Tile shapes: kWide = 128x128 (2x2 waves of 64x64), kNarrow = 64x64 for
-// small-N projections (x_proj).
-enum GemmTile { kWide = 0, kNarrow = 1 };
+// Tile shapes (rows x columns of C per workgroup, 4 or 8 wavefronts, K staged
+// in chunks of 32 or 64): kWide = 128x128, kNarrow = 64x64 (small-N
+// projections), and the variants below.
+enum GemmTile {
+  kWide = 0,
+  kNarrow = 1,
+  kTile64x128 = 2,
+  kTile128x64 = 3,
+  kTile128x256 = 4,
+  kTile128x128K64 = 5,
+  kTile64x128K64 = 6,
+  kTile128x64K64 = 7,
+  kNumGemmTiles = 8
+};
 
 hipError_t launch_gemm_f32(const GemmArgs& a, int flags, GemmTile tile, hipStream_t s);
+// The tile the scoring and training passes use for a GEMM of up to Mmax rows.
+GemmTile pick_gemm_f32_tile(int Mmax, int N, int K);
 
 // bf16 GEMM: C = A W^T with A fp32 (converted while staged) or bf16, W bf16
 // ([N, ldw] row-major, zero-padded in K to a multiple of 8, ldw % 8 == 0),

@@ -82,8 +82,7 @@ template <> struct Vec<uint16_t> {
   static __device__ __forceinline__ void store(uint16_t* p, const float* v) {
     u32x4 x;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      x[i] = (uint32_t)f32_to_bf16(v[2 * i]) | ((uint32_t)f32_to_bf16(v[2 * i + 1]) << 16);
+    for (int i = 0; i < 4; ++i) x[i] = f32x2_to_bf16x2(v[2 * i], v[2 * i + 1]);
     *reinterpret_cast<u32x4*>(p) = x;
   }
 };

@@ -79,5 +79,5 @@ def test_calls_on_null_handles(lib):
     assert lib.tcl_score(None, 1, 1, None, None, None, None, 0, None) == -1
     assert lib.tcl_score_workspace_bytes(None, 4, 4) == 0
     assert lib.tcl_get_params(None, None, 0) == -1
-    assert lib.tcl_test_gemm_f32(0, 4, 4, None, None, None, None, None) == -1
+    assert lib.tcl_test_gemm_f32(0, 4, 4, None, None, None, None, -1, 0, None) == -1
     assert lib.tcl_test_scan_f32(1, 16, 8, 4, 0, *([None] * 4), 16, *([None] * 6)) in (-1, -2)

@@ -44,19 +44,47 @@ def _unpack(packed, lengths, L):
 @pytest.mark.parametrize("M,N,K", [(1, 64, 4), (31, 48, 512), (129, 256, 164), (1000, 1024, 256),
                                    (257, 256, 512), (77, 100, 36)])
 @pytest.mark.parametrize("bias", [False, True])
-def test_gemm_f32(M, N, K, bias):
-    print(f"gemm M={M} N={N} K={K} bias={bias}", flush=True)
+@pytest.mark.parametrize("tile", [-1, 2, 3, 4, 5, 6, 7])
+def test_gemm_f32(M, N, K, bias, tile):
+    print(f"gemm M={M} N={N} K={K} bias={bias} tile={tile}", flush=True)
     rng = np.random.default_rng(M * 7 + N + K)
     A = rng.standard_normal((M, K)).astype(np.float32)
     W = rng.standard_normal((N, K)).astype(np.float32)
     bv = rng.standard_normal(N).astype(np.float32) if bias else None
-    C = tb.gemm_f32(_dev(A), _dev(W), _dev(bv) if bias else None)
+    C = tb.gemm_f32(_dev(A), _dev(W), _dev(bv) if bias else None, tile=tile)
     torch.cuda.synchronize()
     ref = A.astype(np.float64) @ W.astype(np.float64).T
     bound = (K + 2) * U * (np.abs(A).astype(np.float64) @ np.abs(W).astype(np.float64).T)
     if bias:
         ref += bv
         bound += U * np.abs(ref)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+@pytest.mark.parametrize("M,N,K", [(77, 100, 36), (1000, 1024, 256), (257, 256, 512)])
+@pytest.mark.parametrize("tile", [-1, 0, 3, 5, 7])
+@pytest.mark.parametrize("epilogue", [1, 2])
+def test_gemm_f32_epilogues(M, N, K, tile, epilogue):
+    """The residual (C += A W^T, in place) and RMSNorm row-scale epilogues."""
+    print(f"gemm epilogue={epilogue} M={M} N={N} K={K} tile={tile}", flush=True)
+    rng = np.random.default_rng(M + 3 * N + 7 * K + epilogue)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    C0 = rng.standard_normal((M, N)).astype(np.float32)
+    C = _dev(C0)
+    tb.gemm_f32(_dev(A), _dev(W), out=C, tile=tile, epilogue=epilogue)
+    torch.cuda.synchronize()
+    A64, W64 = A.astype(np.float64), W.astype(np.float64)
+    prod = A64 @ W64.T
+    bound = (K + 2) * U * (np.abs(A64) @ np.abs(W64).T)
+    if epilogue == 1:
+        ref = C0 + prod
+        bound = bound + U * np.abs(ref)
+    else:
+        rstd = 1.0 / np.sqrt(np.mean(A64 * A64, axis=1, keepdims=True) + 1e-5)
+        ref = rstd * prod
+        bound = rstd * bound + (K + 8) * U * np.abs(ref)  # the row statistic's own rounding
     err = np.abs(C.cpu().numpy() - ref)
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
