@@ -228,11 +228,29 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
                                      const float* d_W, const float* d_bias, float* d_C, int32_t tile,
                                      int32_t epilogue, void* stream);
 
-/* Same with bf16 operands (row-major bf16 bit patterns, K % 8 == 0) on the
- * bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16), fp32 accumulation and output. */
-TCL_API tcl_status tcl_test_gemm_bf16(int32_t M, int32_t N, int32_t K, const uint16_t* d_A,
-                                      const uint16_t* d_W, const float* d_bias, float* d_C,
-                                      void* stream);
+/* The bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16, fp32 accumulation) in the
+ * variants the bf16 model runs, selected by kind:
+ *   0: C fp32 [M,N] = A W^T (+ bias[N] if d_bias), A bf16 [M,K]
+ *   1: C bf16 [M,N] = A W^T, A bf16
+ *   2: C bf16 = rstd(A) * (A diag(gain)) W^T, A fp32, rstd as in the fp32
+ *      entry (eps 1e-5): the RMSNorm in front of in_proj, d_gain [K]
+ *   3: C fp32 += A W^T, A bf16 (the residual epilogue, C read in place)
+ *   4: C fp32 = A_g W^T + bias, A fp32 [B, L, K] padded, gathered: packed
+ *      row d_offs[b] + t is A[b, t, :] (d_offs [B+1] int32 prefix sums of
+ *      lengths in 0..L); C holds B*L rows (only the first d_offs[B] are
+ *      written) and M is ignored
+ * Other arguments are ignored (may be NULL / 0) for kinds that do not use
+ * them. bf16 arrays are bit patterns. W is [N, Kw] bf16 with Kw = K rounded
+ * up to a multiple of 8, zero-padded. K % 8 == 0 for bf16 A, K % 4 == 0 for
+ * fp32 A; N % 4 == 0; A, W and C 16-byte aligned.
+ * tile: -1 = what the model uses; 0..6 = 128x128, 64x64, 64x128, 128x64,
+ * 128x256, 256x128, 256x128 on four wavefronts; 7 and 8 = row panels (256 or 128 rows x
+ * all N per workgroup, A held in registers; K <= 256 and 16-byte aligned
+ * rows of C, else TCL_ERR_HIP). */
+TCL_API tcl_status tcl_test_gemm_bf16(int32_t kind, int32_t tile, int32_t M, int32_t N, int32_t K,
+                                      const void* d_A, const int32_t* d_offs, int32_t B, int32_t L,
+                                      const uint16_t* d_W, const float* d_bias, const float* d_gain,
+                                      void* d_C, void* stream);
 
 /* u = SiLU(conv_b + causal depthwise conv(x; conv_w)) per program, fp32.
  * d_x rows have leading dimension ldx >= E (E and ldx multiples of 4, every

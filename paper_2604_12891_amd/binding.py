@@ -60,7 +60,7 @@ _SIGS = {
                                       ctypes.POINTER(ctypes.c_int64)]),
     "tcl_trainer_timing_reset": (_i32, [_vp]),
     "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _i32, _vp]),
-    "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                  _vp, _vp, _vp]),
@@ -267,15 +267,32 @@ def gemm_f32(A, W, bias=None, out=None, stream=None, tile=-1, epilogue=0):
     return out
 
 
-def gemm_bf16(A, W, bias=None, out=None, stream=None):
-    """A [M,K], W [N,K] torch.bfloat16 (cuda) -> fp32 [M,N]."""
+GEMM_BF16_F32, GEMM_BF16_BF16, GEMM_BF16_NORM, GEMM_BF16_RESID, GEMM_BF16_GATHER = range(5)
+
+
+def gemm_bf16(A, W, bias=None, out=None, stream=None, kind=GEMM_BF16_F32, tile=-1, gain=None, offs=None):
+    """The bf16 GEMM variants (see tcl_test_gemm_bf16): W [N, round_up(K, 8)]
+    torch.bfloat16, zero-padded in K.
+    GEMM_BF16_F32: A bf16 [M,K] -> fp32 (+ bias); GEMM_BF16_BF16: -> bf16;
+    GEMM_BF16_NORM: A fp32 -> RMSNorm(gain) -> bf16; GEMM_BF16_RESID: out
+    (fp32, required) += A W^T; GEMM_BF16_GATHER: A fp32 [B, L, K] gathered
+    by offs [B+1] -> fp32 + bias, out [B*L, N]."""
     import torch
-    M, K = A.shape
     N = W.shape[0]
+    if kind == GEMM_BF16_GATHER:
+        Bp, L, K = A.shape
+        M = Bp * L
+    else:
+        (M, K), Bp, L = A.shape, 0, 0
+    if W.shape[1] != (K + 7) // 8 * 8:
+        raise ValueError(f"W must be [N, {(K + 7) // 8 * 8}] (K zero-padded to a multiple of 8)")
     if out is None:
-        out = torch.empty(M, N, dtype=torch.float32, device=A.device)
-    check(lib().tcl_test_gemm_bf16(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(),
-                                   _stream(stream)))
+        if kind == GEMM_BF16_RESID:
+            raise ValueError("GEMM_BF16_RESID accumulates into out")
+        bf16_out = kind in (GEMM_BF16_BF16, GEMM_BF16_NORM)
+        out = torch.empty(M, N, dtype=torch.bfloat16 if bf16_out else torch.float32, device=A.device)
+    check(lib().tcl_test_gemm_bf16(kind, tile, M, N, K, A.data_ptr(), _ptr(offs), Bp, L, W.data_ptr(),
+                                   _ptr(bias), _ptr(gain), out.data_ptr(), _stream(stream)))
     return out
 
 

@@ -175,21 +175,21 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
     g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
     g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
-    TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, s));
+    TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
 
     for (int l = 0; l < c.n_layers; ++l) {
       const auto& W = m->layers[l];
       GemmArgsBF16 gi;
       gi.A = H; gi.lda = d; gi.W = W.W_in_h; gi.ldw = d; gi.gain = W.g; gi.C = xz; gi.ldc = 2 * E;
       gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_bf16(gi, kNormF32toBF16, s));
+      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_bf16(gi, kNormF32toBF16, -1, s));
 
       TCL_LAUNCH(T, "conv_silu", launch_conv_silu<uint16_t>(B, E, c.d_conv, offs, xz, 2 * E,
                                                             W.conv_w, W.conv_b, u, s));
       GemmArgsBF16 gx;
       gx.A = u; gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
       gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32Narrow, s));
+      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32, -1, s));
 
       if (chunks > 0)
         TCL_LAUNCH(T, "scan_chunked", launch_scan_chunked<uint16_t>(B, E, N, R, chunks, offs, u, xdbl,
@@ -201,7 +201,7 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       GemmArgsBF16 go;
       go.A = u; go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = H; go.ldc = d;
       go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, s));
+      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, -1, s));
     }
   }
   TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
@@ -531,17 +531,34 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
   return TCL_OK;
 }
 
-TCL_API tcl_status tcl_test_gemm_bf16(int32_t M, int32_t N, int32_t K, const uint16_t* d_A,
-                                      const uint16_t* d_W, const float* d_bias, float* d_C,
-                                      void* stream) {
-  if (M <= 0 || N <= 0 || K <= 0 || K % 8) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
+TCL_API tcl_status tcl_test_gemm_bf16(int32_t kind, int32_t tile, int32_t M, int32_t N, int32_t K,
+                                      const void* d_A, const int32_t* d_offs, int32_t B, int32_t L,
+                                      const uint16_t* d_W, const float* d_bias, const float* d_gain,
+                                      void* d_C, void* stream) {
+  static const GemmBF16Kind kinds[5] = {kBF16toF32, kBF16toBF16, kNormF32toBF16, kBF16ResidF32,
+                                        kInputF32toF32};
+  if (kind < 0 || kind > 4) return fail(TCL_ERR_INVALID_ARG, "kind must be 0..4 (got %d)", kind);
+  if (tile < -1 || tile >= kNumGemmBF16Tiles) return fail(TCL_ERR_INVALID_ARG, "tile must be -1..%d", kNumGemmBF16Tiles - 1);
+  const bool f32a = kind == 2 || kind == 4;
+  if (kind == 4) {
+    if (B <= 0 || L <= 0 || !d_offs) return fail(TCL_ERR_INVALID_ARG, "gather needs d_offs, B > 0, L > 0");
+    M = B * L;
+  }
+  if (M <= 0 || N <= 0 || K <= 0 || N % 4) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K (N %% 4 == 0 required)");
+  if (K % (f32a ? 4 : 8)) return fail(TCL_ERR_INVALID_ARG, "K must be a multiple of %d", f32a ? 4 : 8);
   if (!d_A || !d_W || !d_C) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
-  if (reinterpret_cast<uintptr_t>(d_A) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
-    return fail(TCL_ERR_INVALID_ARG, "A and W must be 16-byte aligned");
+  if (kind == 2 && !d_gain) return fail(TCL_ERR_INVALID_ARG, "kind 2 needs d_gain");
+  if (kind == 4 && !d_bias) return fail(TCL_ERR_INVALID_ARG, "kind 4 needs d_bias");
+  if (reinterpret_cast<uintptr_t>(d_A) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16 ||
+      reinterpret_cast<uintptr_t>(d_C) % 16 || (d_gain && reinterpret_cast<uintptr_t>(d_gain) % 16))
+    return fail(TCL_ERR_INVALID_ARG, "A, W, C and gain must be 16-byte aligned");
   GemmArgsBF16 g;
-  g.A = d_A; g.lda = K; g.W = d_W; g.ldw = K; g.bias = d_bias; g.C = d_C; g.ldc = N;
-  g.Mmax = M; g.N = N; g.K = K;
-  TCL_HIP(launch_gemm_bf16(g, d_bias ? kBF16toF32Bias : kBF16toF32, static_cast<hipStream_t>(stream)));
+  g.A = d_A; g.lda = K; g.W = d_W; g.ldw = (K + 7) & ~7; g.bias = d_bias; g.gain = d_gain;
+  g.C = d_C; g.ldc = N; g.Mmax = M; g.N = N; g.K = K; g.eps = 1e-5f;
+  if (kind == 4) { g.offs = d_offs; g.B = B; g.L = L; g.Mdev = d_offs + B; }
+  GemmBF16Kind k = kinds[kind];
+  if (k == kBF16toF32 && d_bias) k = kBF16toF32Bias;
+  TCL_HIP(launch_gemm_bf16(g, k, tile, static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }
 

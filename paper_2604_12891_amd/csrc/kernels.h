@@ -56,7 +56,8 @@ GemmTile pick_gemm_f32_tile(int Mmax, int N, int K);
 // bf16 GEMM: C = A W^T with A fp32 (converted while staged) or bf16, W bf16
 // ([N, ldw] row-major, zero-padded in K to a multiple of 8, ldw % 8 == 0),
 // C fp32 or bf16, fp32 accumulation. kRowNorm also scales A by gain[k]
-// before the conversion (the RMSNorm gain) and needs K % 8 == 0.
+// before the conversion (the RMSNorm gain). An fp32 A needs K % 4 == 0, a
+// bf16 A K % 8 == 0.
 struct GemmArgsBF16 {
   const void* A = nullptr;
   int64_t lda = 0;
@@ -78,14 +79,33 @@ struct GemmArgsBF16 {
 enum GemmBF16Kind {
   kInputF32toF32,    // fp32 features (gathered) -> fp32, + bias
   kNormF32toBF16,    // fp32 residual -> RMSNorm (rstd, gain) -> bf16
-  kBF16toF32Narrow,  // bf16 -> fp32, 64x64 tiles
   kBF16ResidF32,     // bf16 -> fp32 C += result
   kBF16toF32,        // bf16 -> fp32
   kBF16toF32Bias,    // bf16 -> fp32, + bias
   kBF16toBF16,       // bf16 -> bf16
 };
 
-hipError_t launch_gemm_bf16(const GemmArgsBF16& a, GemmBF16Kind kind, hipStream_t s);
+// Workgroup tiles (rows x columns of C): 4 wavefronts unless noted.
+enum GemmBF16Tile {
+  kB128x128 = 0,
+  kB64x64 = 1,
+  kB64x128 = 2,
+  kB128x64 = 3,
+  kB128x256 = 4,    // 8 wavefronts
+  kB256x128 = 5,    // 8 wavefronts
+  kB256x128W4 = 6,  // 4 wavefronts of 128x64 each
+  kBPanel = 7,      // row panels: 256 rows x all N per workgroup (K <= 256)
+  kBPanel128 = 8,   // row panels of 128 rows (32 per wavefront)
+  kNumGemmBF16Tiles = 9
+};
+
+// tile < 0: the tile pick_gemm_bf16_tile chooses. N and ldc must be
+// multiples of 4 (hipErrorInvalidValue otherwise).
+hipError_t launch_gemm_bf16(const GemmArgsBF16& a, GemmBF16Kind kind, int tile, hipStream_t s);
+GemmBF16Tile pick_gemm_bf16_tile(GemmBF16Kind kind, int Mmax, int N, int K);
+// the row-panel kernel (kBPanel): K <= 256, C (and R) 16-byte aligned rows
+bool gemm_bf16_panel_fits(const GemmArgsBF16& a, bool bf16_out);
+hipError_t launch_gemm_bf16_panel(const GemmArgsBF16& a, GemmBF16Kind kind, int rows_per_wave, hipStream_t s);
 
 // ---------------------------------------------------------------- weight-gradient GEMM
 // P[s][i][j] = sum over tokens m of split s of A[m, i] * B[m, j]

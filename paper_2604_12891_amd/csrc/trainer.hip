@@ -297,7 +297,7 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
     g.A = d_feats; g.lda = F; g.offs = offs; g.B = B; g.L = L;
     g.W = S->W0_h; g.ldw = S->ldw0_h; g.bias = S->b0; g.C = F32(P.layers[0].Hin); g.ldc = d;
     g.Mdev = Mdev; g.Mmax = Mmax; g.N = d; g.K = F;
-    TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, s));
+    TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
   }
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& W = S->layers[l];
@@ -308,20 +308,20 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
     GemmArgsBF16 gi;
     gi.A = B16(Ly.n); gi.lda = d; gi.W = W.W_in_h; gi.ldw = d; gi.C = B16(Ly.xz); gi.ldc = 2 * E;
     gi.Mdev = Mdev; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d;
-    TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_bf16(gi, kBF16toBF16, s));
+    TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_bf16(gi, kBF16toBF16, -1, s));
     TCL_LAUNCH(T, "conv_silu", launch_conv_silu<uint16_t>(B, E, K, offs, B16(Ly.xz), 2 * E, W.conv_w,
                                                           W.conv_b, B16(Ly.u), s));
     GemmArgsBF16 gx;
     gx.A = B16(Ly.u); gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = F32(Ly.xdbl); gx.ldc = XW;
     gx.Mdev = Mdev; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-    TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32Narrow, s));
+    TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32, -1, s));
     TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, B16(Ly.u), F32(Ly.xdbl),
                                                 B16(Ly.xz) + E, 2 * E, W.W_dt, W.b_dt, W.A_log, W.D,
                                                 B16(Ly.yg), s, B16(Ly.y)));
     GemmArgsBF16 go;
     go.A = B16(Ly.yg); go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = Hout; go.ldc = d;
     go.R = F32(Ly.Hin); go.Mdev = Mdev; go.Mmax = Mmax; go.N = d; go.K = E;
-    TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, s));
+    TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, -1, s));
   }
   TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, h, offs, d_lengths, F32(P.H_last), S->g_f, c.final_norm,
                                         c.norm_eps, S->W1T, S->b1, S->W2, S->b2, F32(P.s_scores), s,

@@ -81,3 +81,24 @@ def test_calls_on_null_handles(lib):
     assert lib.tcl_get_params(None, None, 0) == -1
     assert lib.tcl_test_gemm_f32(0, 4, 4, None, None, None, None, -1, 0, None) == -1
     assert lib.tcl_test_scan_f32(1, 16, 8, 4, 0, *([None] * 4), 16, *([None] * 6)) in (-1, -2)
+
+
+def test_bf16_gemm_entry_rejects_bad_arguments(lib):
+    """Argument checks run on the host, before any device work."""
+    fake = 1 << 20  # never dereferenced: every call below fails its checks first
+    args = dict(kind=0, tile=-1, M=8, N=8, K=8, A=fake, offs=None, B=0, L=0, W=fake, bias=None, gain=None,
+                C=fake, stream=None)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return lib.tcl_test_gemm_bf16(*a.values())
+
+    assert call(kind=5) == -1
+    assert call(tile=9) == -1
+    assert call(N=6) == -1            # N % 4
+    assert call(K=12) == -1           # bf16 A needs K % 8
+    assert call(A=None) == -1
+    assert call(kind=2) == -1         # the RMSNorm variant needs the gain
+    assert call(kind=4) == -1         # the gather needs offsets and B, L
+    assert call(kind=4, offs=fake, B=2, L=3) == -1  # ... and the bias
+    assert call(C=fake + 4) == -1     # alignment

@@ -110,6 +110,98 @@ def test_gemm_bf16(M, N, K, bias):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+def _bf16_w(N, K, rng):
+    """W [N, round_up(K, 8)] bf16-exact, zero-padded in K as the kernels expect."""
+    Kw = (K + 7) // 8 * 8
+    W = np.zeros((N, Kw), np.float32)
+    W[:, :K] = wl.round_to_bf16(rng.standard_normal((N, K)).astype(np.float32))
+    return W
+
+
+@pytest.mark.parametrize("tile", [-1, 0, 1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("kind", ["f32", "bf16", "norm", "resid", "gather"])
+def test_gemm_bf16_variants(kind, tile):
+    """Every bf16 GEMM variant the model runs, on every tile, with ragged M, N
+    and K. Where the kernel rounds an fp32 operand to bf16 (A, or A * gain),
+    the same rounding is applied on the host first (the products of bf16
+    values are then exact), so the bound is that of fp32 accumulation, plus
+    the bf16 unit roundoff 2^-8 where the output is bf16."""
+    print(f"gemm_bf16 kind={kind} tile={tile}", flush=True)
+    rng = np.random.default_rng(["f32", "bf16", "norm", "resid", "gather"].index(kind) * 10 + tile + 1)
+    f32a = kind in ("norm", "gather")
+    # bf16 rows of C must be 16-byte aligned for the row-panel tile
+    M, N, K = 1000, (200 if kind in ("bf16", "norm") else 196), (164 if f32a else 168)
+    W = _bf16_w(N, K, rng)
+    Wk = W[:, :K].astype(np.float64)
+    bv = rng.standard_normal(N).astype(np.float32)
+    gain = (1.0 + 0.5 * rng.standard_normal(K)).astype(np.float32)
+    Wd = _dev(W, torch.bfloat16)
+    if kind == "gather":
+        lengths = rng.integers(0, 26, size=45).astype(np.int32)
+        lengths[3] = 0
+        lengths[7] = 25
+        Bp, L = len(lengths), 25
+        Ap = rng.standard_normal((Bp, L, K)).astype(np.float32)
+        out = torch.full((Bp * L, N), float("nan"), device="cuda")
+        tb.gemm_bf16(_dev(Ap), Wd, bias=_dev(bv), out=out, kind=tb.GEMM_BF16_GATHER, tile=tile,
+                     offs=_dev(_offs(lengths), torch.int32))
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        Mv = int(lengths.sum())
+        assert np.all(np.isnan(got[Mv:])), "rows past the packed tokens were written"
+        got = got[:Mv]
+        Ah = wl.round_to_bf16(_pack(Ap, lengths)).astype(np.float64)
+        ref = Ah @ Wk.T + bv
+        bound = (K + 2) * U * (np.abs(Ah) @ np.abs(Wk).T) + U * np.abs(ref)
+    elif kind == "norm":
+        A = (3.0 * rng.standard_normal((M, K))).astype(np.float32)
+        out = tb.gemm_bf16(_dev(A), Wd, gain=_dev(gain), kind=tb.GEMM_BF16_NORM, tile=tile)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy()
+        Ah = wl.round_to_bf16(A * gain[None, :]).astype(np.float64)  # fp32 product, then RNE
+        rstd = 1.0 / np.sqrt(np.mean(A.astype(np.float64) ** 2, axis=1) + 1e-5)
+        ref = rstd[:, None] * (Ah @ Wk.T)
+        bound = ((K + 4) * U * rstd[:, None] * (np.abs(Ah) @ np.abs(Wk).T)
+                 + (2.0 ** -8 + 8 * U) * np.abs(ref))
+    else:
+        A = wl.round_to_bf16(rng.standard_normal((M, K)).astype(np.float32))
+        Ad = _dev(A, torch.bfloat16)
+        A64 = A.astype(np.float64)
+        prod = A64 @ Wk.T
+        mag = (K + 2) * U * (np.abs(A64) @ np.abs(Wk).T)
+        if kind == "f32":
+            got = tb.gemm_bf16(Ad, Wd, bias=_dev(bv), kind=tb.GEMM_BF16_F32, tile=tile)
+            ref, bound = prod + bv, mag + U * np.abs(prod + bv)
+        elif kind == "bf16":
+            got = tb.gemm_bf16(Ad, Wd, kind=tb.GEMM_BF16_BF16, tile=tile)
+            ref, bound = prod, mag + 2.0 ** -8 * np.abs(prod) * (1 + 1e-3)
+        else:
+            C0 = rng.standard_normal((M, N)).astype(np.float32)
+            got = _dev(C0)
+            tb.gemm_bf16(Ad, Wd, out=got, kind=tb.GEMM_BF16_RESID, tile=tile)
+            ref, bound = C0 + prod, mag + U * np.abs(C0 + prod)
+        torch.cuda.synchronize()
+        got = got.float().cpu().numpy()
+    err = np.abs(got.astype(np.float64) - ref)
+    assert np.all(err <= bound + 1e-30), (kind, tile, float(np.max(err / (bound + 1e-30))))
+
+
+def test_gemm_bf16_panel_rejects_unaligned_rows():
+    """The row-panel tile stores 16-byte row segments: bf16 rows of 196
+    columns (392 bytes) are refused when it is asked for explicitly, and the
+    model's tile choice falls back to the tiled kernel for them."""
+    rng = np.random.default_rng(3)
+    M = 140000  # enough rows for the model's policy to want row panels
+    A = _dev(wl.round_to_bf16(rng.standard_normal((M, 64)).astype(np.float32)), torch.bfloat16)
+    W = _dev(_bf16_w(196, 64, rng), torch.bfloat16)
+    with pytest.raises(tb.TclError):
+        tb.gemm_bf16(A, W, kind=tb.GEMM_BF16_BF16, tile=7)
+    out = tb.gemm_bf16(A, W, kind=tb.GEMM_BF16_BF16, tile=-1)
+    torch.cuda.synchronize()
+    ref = A.float().cpu().numpy().astype(np.float64) @ W.float().cpu().numpy().astype(np.float64).T
+    np.testing.assert_allclose(out.float().cpu().numpy(), ref, rtol=2.0 ** -7, atol=1e-3)
+
+
 @pytest.mark.parametrize("K", [1, 3, 4])
 def test_conv_silu_f32(K):
     rng = np.random.default_rng(K)
