@@ -52,6 +52,8 @@ __global__ __launch_bounds__(1024) void offsets_kernel(const int* __restrict__ l
 // Activations are fp32 or bf16 in memory; every kernel computes in fp32.
 __device__ __forceinline__ float ld1(const float* p) { return *p; }
 __device__ __forceinline__ float ld1(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 __device__ __forceinline__ void st1(float* p, float v) { *p = v; }
 __device__ __forceinline__ void st1(uint16_t* p, float v) { *p = f32_to_bf16(v); }
 
@@ -65,6 +67,10 @@ template <> struct Vec<float> {
     const floatx4 x = *reinterpret_cast<const floatx4*>(p);
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   }
+  static __device__ __forceinline__ void cvt(u32x4 x, float* v) {
+    v[0] = __uint_as_float(x[0]); v[1] = __uint_as_float(x[1]);
+    v[2] = __uint_as_float(x[2]); v[3] = __uint_as_float(x[3]);
+  }
   static __device__ __forceinline__ void store(float* p, const float* v) {
     *reinterpret_cast<floatx4*>(p) = floatx4{v[0], v[1], v[2], v[3]};
   }
@@ -73,6 +79,13 @@ template <> struct Vec<uint16_t> {
   static constexpr int CH = 8;
   static __device__ __forceinline__ void load(const uint16_t* p, float* v) {
     const u32x4 x = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(x[i] << 16);
+      v[2 * i + 1] = __uint_as_float(x[i] & 0xFFFF0000u);
+    }
+  }
+  static __device__ __forceinline__ void cvt(u32x4 x, float* v) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       v[2 * i] = __uint_as_float(x[i] << 16);
@@ -89,8 +102,8 @@ template <> struct Vec<uint16_t> {
 
 // ---------------------------------------------------------------- conv + SiLU
 // One thread per (program, CH adjacent channels): 16-byte loads and stores,
-// x_{t-K+1..t} of its channels in a K-deep register window. The loop is
-// unrolled by 4 tokens with the loads issued ahead of the arithmetic.
+// x_{t-K+1..t} of its channels in a K-deep register window. Tokens go in
+// groups of 4 whose loads are issued one group ahead of the arithmetic.
 template <typename T, int K>
 __global__ __launch_bounds__(256) void conv_silu_kernel(const int* __restrict__ offs, int E,
                                                         const T* __restrict__ x, int ldx,
@@ -130,14 +143,33 @@ __global__ __launch_bounds__(256) void conv_silu_kernel(const int* __restrict__ 
     }
     Vec<T>::store(dst, acc);
   };
+  // groups of U tokens, ping-ponged between two raw register sets: group
+  // t + U is loaded while group t is converted and computed
   constexpr int U = 4;
+  auto load_group = [&](int t0, u32x4* g) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) g[j] = *reinterpret_cast<const u32x4*>(xp + (int64_t)(t0 + j) * ldx);
+  };
+  auto run_group = [&](int t0, const u32x4* g) {
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      float xin[CH];
+      Vec<T>::cvt(g[j], xin);
+      step(xin, up + (int64_t)(t0 + j) * E);
+    }
+  };
+  u32x4 ga[U], gb[U];
   int t = 0;
-  for (; t + U <= len; t += U) {
-    float xin[U][CH];
-#pragma unroll
-    for (int j = 0; j < U; ++j) Vec<T>::load(xp + (int64_t)(t + j) * ldx, xin[j]);
-#pragma unroll
-    for (int j = 0; j < U; ++j) step(xin[j], up + (int64_t)(t + j) * E);
+  if (U <= len) load_group(0, ga);
+  for (;;) {
+    if (t + U > len) break;  // ga holds group t
+    if (t + 2 * U <= len) load_group(t + U, gb);
+    run_group(t, ga);
+    t += U;
+    if (t + U > len) break;  // gb holds group t
+    if (t + 2 * U <= len) load_group(t + U, ga);
+    run_group(t, gb);
+    t += U;
   }
   for (; t < len; ++t) {
     float xin[CH];
@@ -172,7 +204,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
   float a2[N], s[N], wdt[R];
 #pragma unroll
   for (int n = 0; n < N; ++n) {
-    a2[n] = -expf(A_log[ec * N + n]) * kLog2e;
+    a2[n] = -__builtin_amdgcn_exp2f(A_log[ec * N + n] * kLog2e) * kLog2e;
     s[n] = 0.f;
   }
 #pragma unroll
@@ -186,16 +218,18 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
     for (int i = threadIdx.x; i < nt * XW; i += kScanThreads) sX[i] = src[i];
     __syncthreads();
     if (!active) continue;
-    // u and z of the next token are loaded while this token is computed
-    float un = ld1(u + (int64_t)(base + t0) * E + e);
-    float zn = ld1(z + (int64_t)(base + t0) * ldz + e);
+    // u and z of the next token are loaded while this token is computed;
+    // they stay in their storage type until used, so that converting them
+    // does not wait for the load
+    T un = u[(int64_t)(base + t0) * E + e];
+    T zn = z[(int64_t)(base + t0) * ldz + e];
     for (int tt = 0; tt < nt; ++tt) {
       const int64_t row = base + t0 + tt;
       const float* xr = &sX[tt * XW];
-      const float uv = un, zv = zn;
+      const float uv = to_f32(un), zv = to_f32(zn);
       if (tt + 1 < nt) {
-        un = ld1(u + (row + 1) * E + e);
-        zn = ld1(z + (row + 1) * ldz + e);
+        un = u[(row + 1) * E + e];
+        zn = z[(row + 1) * ldz + e];
       }
       float v = bdt;
 #pragma unroll
@@ -249,7 +283,7 @@ __global__ __launch_bounds__(512) void scan_chunked_kernel(
 
   float a2[N], wdt[R];
 #pragma unroll
-  for (int n = 0; n < N; ++n) a2[n] = -expf(A_log[ec * N + n]) * kLog2e;
+  for (int n = 0; n < N; ++n) a2[n] = -__builtin_amdgcn_exp2f(A_log[ec * N + n] * kLog2e) * kLog2e;
 #pragma unroll
   for (int r = 0; r < R; ++r) wdt[r] = W_dt[ec * R + r];
   const float bdt = b_dt[ec], Dv = Dp[ec];
@@ -266,11 +300,15 @@ __global__ __launch_bounds__(512) void scan_chunked_kernel(
   float sumdt = 0.f;
 #pragma unroll
   for (int n = 0; n < N; ++n) s[n] = 0.f;
+  // u (and z) of the next token are loaded while this token is computed
+  T un = t_begin < t_end ? u[(int64_t)(base + t_begin) * E + ec] : T(0);
   for (int t = t_begin; t < t_end; ++t) {
     const float* xr = xdbl + (int64_t)(base + t) * XW;  // wavefront-uniform row
+    const float uv = to_f32(un);
+    if (t + 1 < t_end) un = u[(int64_t)(base + t + 1) * E + ec];
     const float dt = dt_at(xr);
     sumdt += dt;
-    const float dtu = dt * ld1(u + (int64_t)(base + t) * E + ec);
+    const float dtu = dt * uv;
 #pragma unroll
     for (int n = 0; n < N; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[R + n]);
   }
@@ -291,12 +329,17 @@ __global__ __launch_bounds__(512) void scan_chunked_kernel(
     for (int n = 0; n < N; ++n) s[n] = fmaf(sj[n], s[n], sj[N + n]);
   }
   if (!active) return;
+  un = t_begin < t_end ? u[(int64_t)(base + t_begin) * E + e] : T(0);
+  T zn = t_begin < t_end ? z[(int64_t)(base + t_begin) * ldz + e] : T(0);
   for (int t = t_begin; t < t_end; ++t) {
     const int64_t row = base + t;
     const float* xr = xdbl + row * XW;
+    const float uv = to_f32(un), zv = to_f32(zn);
+    if (t + 1 < t_end) {
+      un = u[(row + 1) * E + e];
+      zn = z[(row + 1) * ldz + e];
+    }
     const float dt = dt_at(xr);
-    const float uv = ld1(u + row * E + e);
-    const float zv = ld1(z + row * ldz + e);
     const float dtu = dt * uv;
     float y = 0.f;
 #pragma unroll
