@@ -19,6 +19,8 @@ __device__ __forceinline__ float silu_grad(float x) {
 
 __device__ __forceinline__ float ld_act(const float* p) { return *p; }
 __device__ __forceinline__ float ld_act(const uint16_t* p) { return bf16_to_f32(*p); }
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 
 // ---------------------------------------------------------------- RMSNorm forward
 // One wavefront per token row: n = bf16(h * r * g), r = (mean h^2 + eps)^-1/2.
@@ -283,7 +285,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
 
   float a2[NH], wdt[R];  // a2 = A log2(e); A itself is a2 ln(2) where needed
 #pragma unroll
-  for (int n = 0; n < NH; ++n) a2[n] = -expf(A_log[e * N + n0 + n]) * kLog2e;
+  for (int n = 0; n < NH; ++n) a2[n] = -__builtin_amdgcn_exp2f(A_log[e * N + n0 + n] * kLog2e) * kLog2e;
 #pragma unroll
   for (int r = 0; r < R; ++r) wdt[r] = W_dt[e * R + r];
   const float bdt = b_dt[e], Dv = Dp[e];
@@ -303,10 +305,14 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     float s[NH];
 #pragma unroll
     for (int n = 0; n < NH; ++n) s[n] = 0.f;
+    // u of the next token is loaded (raw) while this token is computed
+    T un = len > 0 ? u[(int64_t)base * E + e] : T(0);  // a program may have no tokens
     for (int t = 0; t < len; ++t) {
       float sig;
       const float dt = dt_of(t, sig);
-      const float dtu = dt * ld_act(u + (int64_t)(base + t) * E + e);
+      const float uv = to_f32(un);
+      if (t + 1 < len) un = u[(int64_t)(base + t + 1) * E + e];
+      const float dtu = dt * uv;
       const float* xr = &sX[t * XW] + R + n0;
 #pragma unroll
       for (int n = 0; n < NH; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[n]);
@@ -327,22 +333,38 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
   }
   float dD = 0.f;
 
+  // a chunk's per-token inputs and starting state are loaded (raw) one chunk
+  // ahead, while the previous chunk is computed
+  T ur[kTC], zr[kTC], yr[kTC];
+  float gr[kTC], spr[NH];
+  auto load_chunk = [&](int c) {
+#pragma unroll
+    for (int tt = 0; tt < kTC; ++tt) {
+      const int t = min(c * kTC + tt, len - 1);
+      const int64_t row = base + t;
+      ur[tt] = u[row * E + e];
+      zr[tt] = xz[row * ldz + E + e];
+      yr[tt] = ysave[row * E + e];
+      gr[tt] = dyg[row * E + e];
+    }
+#pragma unroll
+    for (int n = 0; n < NH; ++n) spr[n] = c > 0 ? ck[(c - 1) * N + n] : 0.f;
+  };
+  if (nck > 0) load_chunk(nck - 1);
   for (int c = nck - 1; c >= 0; --c) {
     const int t0 = c * kTC;
     float sp[NH];  // state before the chunk
-#pragma unroll
-    for (int n = 0; n < NH; ++n) sp[n] = c > 0 ? ck[(c - 1) * N + n] : 0.f;
-    // this chunk's per-token inputs, loaded before the dependent arithmetic
     float uc[kTC], zc[kTC], yc[kTC], gc[kTC];
 #pragma unroll
+    for (int n = 0; n < NH; ++n) sp[n] = spr[n];
+#pragma unroll
     for (int tt = 0; tt < kTC; ++tt) {
-      const int t = min(t0 + tt, len - 1);
-      const int64_t row = base + t;
-      uc[tt] = ld_act(u + row * E + e);
-      zc[tt] = ld_act(xz + row * ldz + E + e);
-      yc[tt] = ld_act(ysave + row * E + e);
-      gc[tt] = dyg[row * E + e];
+      uc[tt] = to_f32(ur[tt]);
+      zc[tt] = to_f32(zr[tt]);
+      yc[tt] = to_f32(yr[tt]);
+      gc[tt] = gr[tt];
     }
+    if (c > 0) load_chunk(c - 1);
     float hist[kTC][NH];
     {
       float s[NH];
