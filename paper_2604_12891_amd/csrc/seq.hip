@@ -189,14 +189,20 @@ constexpr int kScanTC = 32;
 
 template <typename T, int N, int R>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(
-    const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
+    int B, const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
     const T* __restrict__ z, int ldz, const float* __restrict__ W_dt,
     const float* __restrict__ b_dt, const float* __restrict__ A_log,
     const float* __restrict__ Dp, T* out, T* __restrict__ ysave) {
   constexpr int XW = R + 2 * N;
   __shared__ __attribute__((aligned(16))) float sX[kScanTC * XW];
-  const int b = blockIdx.x;
-  const int e = blockIdx.y * kScanThreads + threadIdx.x;
+  // workgroups are handed to the 8 XCDs round-robin: the CG channel groups
+  // of a program take consecutive slots on one XCD, so its xdbl rows are
+  // read from HBM once and then hit that XCD's L2
+  const int CG = (E + kScanThreads - 1) / kScanThreads;
+  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int b = (j / CG) * 8 + xcd;
+  if (b >= B) return;
+  const int e = (j % CG) * kScanThreads + threadIdx.x;
   const bool active = e < E;
   const int ec = active ? e : 0;
   const int base = offs[b], len = offs[b + 1] - base;
@@ -521,10 +527,11 @@ hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, 
                        const float* D, T* out, hipStream_t s, T* ysave) {
   if (B <= 0) return hipSuccess;
   if (N != 16) return hipErrorInvalidValue;
-  dim3 grid(B, (E + kScanThreads - 1) / kScanThreads);
-#define TCL_SCAN(RR)                                                                                 \
-  hipLaunchKernelGGL((scan_kernel<T, 16, RR>), grid, dim3(kScanThreads), 0, s, offs, E, u, xdbl, z, \
-                     ldz, W_dt, b_dt, A_log, D, out, ysave)
+  const int cgroups = (E + kScanThreads - 1) / kScanThreads;
+  const int grid = 8 * cgroups * ((B + 7) / 8);
+#define TCL_SCAN(RR)                                                                                    \
+  hipLaunchKernelGGL((scan_kernel<T, 16, RR>), dim3(grid), dim3(kScanThreads), 0, s, B, offs, E, u, xdbl, \
+                     z, ldz, W_dt, b_dt, A_log, D, out, ysave)
   switch (R) {
     case 4: TCL_SCAN(4); break;
     case 8: TCL_SCAN(8); break;
