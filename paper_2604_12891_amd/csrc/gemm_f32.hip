@@ -92,27 +92,16 @@ __global__ __launch_bounds__(WM* WN * 64, BK == 32 ? 3 : 2) void gemm_f32_kernel
 #pragma unroll
   for (int i = 0; i < NA; ++i) ss[i] = 0.f;
 
+  // Loads go to clamped in-bounds addresses (no branch per load); units
+  // outside A, W or K are zeroed when staged, and the RMSNorm sum of squares
+  // is taken there too, so nothing waits for a load before the MFMAs that
+  // should hide it.
   auto gload = [&](int k0) {
     const bool kin = k0 + q4 < p.K;  // K % 4 == 0: a float4 is all in or all out
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      if (aval[i] && kin) {
-        ra[i] = *reinterpret_cast<const floatx4*>(aptr[i] + k0);
-      } else {
-        ra[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-      }
-      if constexpr (kNorm) {
-        ss[i] += ra[i].x * ra[i].x + ra[i].y * ra[i].y + ra[i].z * ra[i].z + ra[i].w * ra[i].w;
-      }
-    }
+    for (int i = 0; i < NA; ++i) ra[i] = *reinterpret_cast<const floatx4*>(aptr[i] + (kin ? k0 : 0));
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      if (bval[i] && kin) {
-        rb[i] = *reinterpret_cast<const floatx4*>(bptr[i] + k0);
-      } else {
-        rb[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-      }
-    }
+    for (int i = 0; i < NB; ++i) rb[i] = *reinterpret_cast<const floatx4*>(bptr[i] + (kin ? k0 : 0));
   };
 
   const int wave = tid >> 6, lane = tid & 63;
@@ -130,15 +119,19 @@ __global__ __launch_bounds__(WM* WN * 64, BK == 32 ? 3 : 2) void gemm_f32_kernel
   gload(0);
   for (int k0 = 0; k0 < p.K; k0 += BK) {
     __syncthreads();
+    const bool kin = k0 + q4 < p.K;
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       const int r = (tid + i * NT) / Q;
-      *reinterpret_cast<floatx4*>(&sA[r * PITCH + q4]) = ra[i];
+      const floatx4 v = (aval[i] && kin) ? ra[i] : floatx4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (kNorm) ss[i] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      *reinterpret_cast<floatx4*>(&sA[r * PITCH + q4]) = v;
     }
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       const int r = (tid + i * NT) / Q;
-      *reinterpret_cast<floatx4*>(&sB[r * PITCH + q4]) = rb[i];
+      *reinterpret_cast<floatx4*>(&sB[r * PITCH + q4]) =
+          (bval[i] && kin) ? rb[i] : floatx4{0.f, 0.f, 0.f, 0.f};
     }
     __syncthreads();
     if (k0 + BK < p.K) gload(k0 + BK);
