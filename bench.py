@@ -25,6 +25,17 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
 BF16_MFMA_PEAK_TFS = 2516.6    # MI355X dense bf16 matrix, TFLOP/s
+FP32_VALU_PEAK_TFS = 157.3     # MI355X fp32 vector (256 CUs x 4 SIMDs x 32 lanes x 2 flops x 2.4 GHz)
+
+
+def scan_valu_slots(N: int, R: int) -> int:
+    """VALU issue slots per (token, channel) that the selective scan's
+    arithmetic needs, counted from the recurrence (an FMA, multiply or add is
+    one slot; a transcendental four, the quarter rate of gfx9's v_exp/v_log/
+    v_rcp): R FMAs of dt_proj; softplus (exp, log, ~4 ops) 12; dt*u 1; per
+    state dt*a, exp, (dt u)*B, the state FMA and the output FMA = 8; D-skip 1;
+    the SiLU(z) gate (exp, rcp, 3 ops) 11."""
+    return R + 12 + 1 + 8 * N + 1 + 11
 METRIC = "candidate programs scored/sec (B=4096,L=25) + % of HBM / MFMA peak"
 
 
@@ -33,7 +44,8 @@ def kernel_work(shape, M_v: int, B: int, dtype: str) -> dict:
 
     Counts use the valid tokens M_v only (padding is never computed) and each
     kernel's minimal inputs and outputs read or written once.
-    Returns {name: (kind, amount)} with kind "flop" (MFMA-bound) or "byte".
+    Returns {name: (kind, amount)} with kind "flop" (MFMA-bound), "byte"
+    (HBM-bound) or "valu" ((flop-equivalent VALU work, bytes): VALU-bound).
     """
     d, E, N, R, F = shape.d_model, shape.d_inner, shape.d_state, shape.dt_rank, shape.F
     XW = R + 2 * N
@@ -44,13 +56,21 @@ def kernel_work(shape, M_v: int, B: int, dtype: str) -> dict:
         "gemm_x_proj": ("byte", M_v * (E * a + XW * 4)),
         "gemm_out_proj": ("flop", 2 * M_v * E * d),
         "conv_silu": ("byte", M_v * 2 * E * a),
-        "scan": ("byte", M_v * (3 * E * a + XW * 4)),
+        # VALU-bound: 2 flops per issue slot against the fp32 vector peak;
+        # its HBM bytes are reported beside it
+        "scan": ("valu", (2 * M_v * E * scan_valu_slots(N, R), M_v * (3 * E * a + XW * 4))),
         "tail": ("byte", M_v * d * 4 + B * 8),
         "offsets": ("byte", B * 8),
     }
 
 
 def roofline_entry(kind, amount, ms_per_launch, dtype):
+    if kind == "valu":
+        flops, nbytes = amount
+        achieved = flops / (ms_per_launch * 1e-3) / 1e12
+        hbm = nbytes / (ms_per_launch * 1e-3) / 1e9
+        return {"bound": "alu", "achieved": achieved, "peak": FP32_VALU_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": achieved / FP32_VALU_PEAK_TFS, "hbm_gbs": hbm, "hbm_frac": hbm / HBM_PEAK_GBS}
     if kind == "flop":
         achieved = amount / (ms_per_launch * 1e-3) / 1e12
         peak = FP32_MFMA_PEAK_TFS if dtype == "f32" else BF16_MFMA_PEAK_TFS
@@ -370,6 +390,11 @@ def main():
             "unit": d["unit"], "frac": round(d["frac"], 4),
             "traffic": None if traffic is None else int(traffic),
             "ms_per_launch": round(d["ms_per_launch"], 5)}
+    if d["bound"] == "alu":
+        roof["hbm_achieved_gbs"] = round(d["hbm_gbs"], 1)
+        roof["hbm_frac"] = round(d["hbm_frac"], 4)
+        roof["alu_note"] = ("VALU issue slots of the recurrence (transcendentals at quarter rate) x 2 flops, "
+                            "against the fp32 vector peak")
     if traffic is not None:
         roof["traffic_note"] = ("HBM bytes per launch, rocprofv3 FETCH_SIZE + WRITE_SIZE scaled by an "
                                 "elementwise kernel of known size (profiles/)")
@@ -377,8 +402,9 @@ def main():
         print(f"{'kernel':16s} {'ms/step':>9s} {'ms/launch':>10s} {'achieved':>10s} {'unit':8s} {'frac':>6s}",
               file=sys.stderr)
         for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+            extra = f"  (HBM {e['hbm_gbs']:.0f} GB/s = {e['hbm_frac']:.3f})" if "hbm_gbs" in e else ""
             print(f"{k:16s} {e['ms_per_step']:9.4f} {e['ms_per_launch']:10.5f} {e['achieved']:10.2f} "
-                  f"{e['unit']:8s} {e['frac']:6.3f}", file=sys.stderr)
+                  f"{e['unit']:8s} {e['frac']:6.3f}{extra}", file=sys.stderr)
 
     cpu = None
     if not args.no_cpu_baseline:
