@@ -20,13 +20,22 @@ __global__ __launch_bounds__(1024) void offsets_kernel(const int* __restrict__ l
                                                        int* __restrict__ offs) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x;
-  const int per = (B + 1023) / 1024;
+  // each thread owns a contiguous segment of a multiple of 4 programs, read
+  // and written 16 bytes at a time when the arrays allow it
+  const int per = (((B + 1023) / 1024) + 3) & ~3;
   const int s = min(tid * per, B), e = min(s + per, B);
+  const bool vec = reinterpret_cast<uintptr_t>(lengths) % 16 == 0 && reinterpret_cast<uintptr_t>(offs) % 16 == 0;
+  auto valid = [&](int len) { return (len >= 1 && len <= L) ? len : 0; };
   int sum = 0;
-  for (int i = s; i < e; ++i) {
-    const int len = lengths[i];
-    sum += (len >= 1 && len <= L) ? len : 0;
+  int i = s;
+  if (vec) {
+#pragma unroll 4
+    for (; i + 4 <= e; i += 4) {
+      const int4 v = *reinterpret_cast<const int4*>(lengths + i);
+      sum += valid(v.x) + valid(v.y) + valid(v.z) + valid(v.w);
+    }
   }
+  for (; i < e; ++i) sum += valid(lengths[i]);
   // inclusive scan within the wavefront
   const int lane = tid & 63, wave = tid >> 6;
   int inc = sum;
@@ -40,10 +49,22 @@ __global__ __launch_bounds__(1024) void offsets_kernel(const int* __restrict__ l
   int before = 0;
   for (int w = 0; w < wave; ++w) before += wsum[w];
   int run = before + inc - sum;
-  for (int i = s; i < e; ++i) {
+  i = s;
+  if (vec) {
+#pragma unroll 4
+    for (; i + 4 <= e; i += 4) {
+      const int4 v = *reinterpret_cast<const int4*>(lengths + i);
+      int4 o;
+      o.x = run; run += valid(v.x);
+      o.y = run; run += valid(v.y);
+      o.z = run; run += valid(v.z);
+      o.w = run; run += valid(v.w);
+      *reinterpret_cast<int4*>(offs + i) = o;
+    }
+  }
+  for (; i < e; ++i) {
     offs[i] = run;
-    const int len = lengths[i];
-    run += (len >= 1 && len <= L) ? len : 0;
+    run += valid(lengths[i]);
   }
   if (tid == 1023) offs[B] = before + inc;
 }
@@ -392,21 +413,47 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
     if (b < B) {
       const int base = offs[b];
       len = offs[b + 1] - base;
-      for (int t = 0; t < len; ++t) {
-        const float* hr = H + (int64_t)(base + t) * DM + lane * PL;
-        float v[PL];
+      // tokens in groups of U rows, ping-ponged between two register sets:
+      // group t + U is loaded while group t is reduced and accumulated
+      // (loads clamp to the last row; rows past the end are masked at use)
+      constexpr int U = 4;
+      auto load_group = [&](int t0, float (*g)[PL]) {
 #pragma unroll
-        for (int i = 0; i < PL; ++i) v[i] = hr[i];
-        float rs = 1.f;
-        if (final_norm) {
-          float ss = 0.f;
+        for (int j = 0; j < U; ++j) {
+          const float* hr = H + (int64_t)(base + min(t0 + j, len - 1)) * DM + lane * PL;
 #pragma unroll
-          for (int i = 0; i < PL; ++i) ss = fmaf(v[i], v[i], ss);
-          ss = wave_sum(ss);
-          rs = 1.0f / sqrtf(ss / (float)DM + eps);
+          for (int i = 0; i < PL; ++i) g[j][i] = hr[i];
+        }
+      };
+      auto run_group = [&](int t0, float (*g)[PL]) {
+        float rs[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+          rs[j] = t0 + j < len ? 1.f : 0.f;
+          if (final_norm) {
+            float ss = 0.f;
+#pragma unroll
+            for (int i = 0; i < PL; ++i) ss = fmaf(g[j][i], g[j][i], ss);
+            ss = wave_sum(ss);
+            rs[j] *= 1.0f / sqrtf(ss / (float)DM + eps);
+          }
         }
 #pragma unroll
-        for (int i = 0; i < PL; ++i) acc[i] = fmaf(v[i], rs, acc[i]);
+        for (int j = 0; j < U; ++j)
+#pragma unroll
+          for (int i = 0; i < PL; ++i) acc[i] = fmaf(g[j][i], rs[j], acc[i]);
+      };
+      float ga[U][PL], gb[U][PL];
+      if (len > 0) load_group(0, ga);
+      for (int t = 0;;) {
+        if (t >= len) break;  // ga holds group t
+        if (t + U < len) load_group(t + U, gb);
+        run_group(t, ga);
+        t += U;
+        if (t >= len) break;  // gb holds group t
+        if (t + U < len) load_group(t + U, ga);
+        run_group(t, gb);
+        t += U;
       }
     }
     const float inv = len > 0 ? 1.0f / (float)len : 0.f;
