@@ -222,7 +222,9 @@ TCL_API const char* tcl_last_error(void);
  *   epilogue 2: C = rstd(A) * A W^T  with rstd(A)_m = (mean_k A[m,k]^2 + 1e-5)^-1/2
  *               (the RMSNorm prologue; the gain is folded into W by the model)
  * tile selects the workgroup tile (0..7: 128x128, 64x64, 64x128, 128x64,
- * 128x256, and 128x128 / 64x128 / 128x64 with K staged 64 at a time); -1
+ * 128x256, and 128x128 / 64x128 / 128x64 with K staged 64 at a time; 8: row
+ * panels of 128 rows x all N with A held in registers, for K in {64, 128,
+ * 164, 192, 256}, K % 4 == 0, no residual epilogue, else TCL_ERR_HIP); -1
  * picks what the model would use for M rows. */
 TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const float* d_A,
                                      const float* d_W, const float* d_bias, float* d_C, int32_t tile,

@@ -140,14 +140,14 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
     g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
     g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
-    TCL_LAUNCH(T, "gemm_input", launch_gemm_f32(g, kBias | kGather, pick_gemm_f32_tile(Mmax, d, c.F), s));
+    TCL_LAUNCH(T, "gemm_input", launch_gemm_f32(g, kBias | kGather, -1, s));
 
     for (int l = 0; l < c.n_layers; ++l) {
       const auto& W = m->layers[l];
       GemmArgs gi;
       gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
       gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, pick_gemm_f32_tile(Mmax, 2 * E, d), s));
+      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, -1, s));
 
       TCL_LAUNCH(T, "conv_silu", launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w,
                                                          W.conv_b, u, s));
@@ -166,7 +166,7 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       GemmArgs go;
       go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
       go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_f32(go, kResid, pick_gemm_f32_tile(Mmax, d, E), s));
+      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_f32(go, kResid, -1, s));
     }
   } else {
     uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
@@ -524,10 +524,9 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
   g.A = d_A; g.lda = K; g.W = d_W; g.ldw = K; g.bias = d_bias; g.C = d_C; g.ldc = N;
   g.Mmax = M; g.N = N; g.K = K;
   g.eps = 1e-5f;
-  const GemmTile t = tile >= 0 ? static_cast<GemmTile>(tile) : pick_gemm_f32_tile(M, N, K);
   const int flags = epilogue == 1 ? kResid : epilogue == 2 ? kRowNorm : (d_bias ? kBias : 0);
   if (epilogue == 2 && d_bias) return fail(TCL_ERR_INVALID_ARG, "bias and row norm are exclusive");
-  TCL_HIP(launch_gemm_f32(g, flags, t, static_cast<hipStream_t>(stream)));
+  TCL_HIP(launch_gemm_f32(g, flags, tile, static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }
 

@@ -231,23 +231,33 @@ hipError_t dispatch_flags(const GemmArgs& a, int flags, hipStream_t s) {
   }
 }
 
+constexpr int kPanelMinRows = 32768;
+
 }  // namespace
 
-GemmTile pick_gemm_f32_tile(int Mmax, int N, int K) {
+GemmTile pick_gemm_f32_tile(const GemmArgs& a, int flags) {
   // Measured on MI355X with the model's epilogues (fp32 MFMA, TFLOP/s, three
   // wavefronts per SIMD): at ~62K rows 64x128 tiles win (in_proj with the
   // RMSNorm prologue 104 vs 98 for 128x128; out_proj with the residual 100 vs
   // 78), because the last partial round of workgroups is shorter; the
   // gathered input Linear (K = 164) prefers 128x128 with K chunks of 64
   // (81 vs 67). At ~1.3M rows 128x128 is best for in_proj (115) and 64x128
-  // for out_proj (113).
+  // for out_proj (113). Row panels (K <= 256, no residual) replace the tiles
+  // once there are enough rows to give every CU two panels.
+  const int Mmax = a.Mmax, N = a.N, K = a.K;
   if (N <= 64) return kNarrow;
+  if (Mmax >= kPanelMinRows && gemm_f32_panel_fits(a, flags)) return kPanel;
   if (K % 64 != 0) return Mmax >= 500000 ? kWide : kTile128x128K64;
   if (Mmax >= 500000 && N >= 1024) return kWide;
   return kTile64x128;
 }
 
-hipError_t launch_gemm_f32(const GemmArgs& a, int flags, GemmTile tile, hipStream_t s) {
+hipError_t launch_gemm_f32(const GemmArgs& a, int flags, int tile_id, hipStream_t s) {
+  const GemmTile tile = tile_id < 0 ? pick_gemm_f32_tile(a, flags) : static_cast<GemmTile>(tile_id);
+  if (tile == kPanel) {
+    if (!gemm_f32_panel_fits(a, flags)) return hipErrorInvalidValue;
+    return launch_gemm_f32_panel(a, flags, s);
+  }
   switch (tile) {
     case kWide: return dispatch_flags<2, 2, 2, 2, 32>(a, flags, s);
     case kNarrow: return dispatch_flags<2, 2, 1, 1, 32>(a, flags, s);

@@ -46,12 +46,16 @@ enum GemmTile {
   kTile128x128K64 = 5,
   kTile64x128K64 = 6,
   kTile128x64K64 = 7,
-  kNumGemmTiles = 8
+  kPanel = 8,  // row panels: 128 rows x all N per workgroup, A in registers (K <= 256, no residual)
+  kNumGemmTiles = 9
 };
 
-hipError_t launch_gemm_f32(const GemmArgs& a, int flags, GemmTile tile, hipStream_t s);
-// The tile the scoring and training passes use for a GEMM of up to Mmax rows.
-GemmTile pick_gemm_f32_tile(int Mmax, int N, int K);
+// tile < 0: the tile pick_gemm_f32_tile chooses for these arguments.
+hipError_t launch_gemm_f32(const GemmArgs& a, int flags, int tile, hipStream_t s);
+// The tile the scoring and training passes use for this GEMM (up to Mmax rows).
+GemmTile pick_gemm_f32_tile(const GemmArgs& a, int flags);
+bool gemm_f32_panel_fits(const GemmArgs& a, int flags);
+hipError_t launch_gemm_f32_panel(const GemmArgs& a, int flags, hipStream_t s);
 
 // bf16 GEMM: C = A W^T with A fp32 (converted while staged) or bf16, W bf16
 // ([N, ldw] row-major, zero-padded in K to a multiple of 8, ldw % 8 == 0),

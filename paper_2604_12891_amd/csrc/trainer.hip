@@ -349,7 +349,7 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
       GemmArgs g;
       g.A = F32(P.dH); g.lda = d; g.W = W.W_outT; g.ldw = d; g.C = F32(P.dyg); g.ldc = E;
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = E; g.K = d;
-      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, pick_gemm_f32_tile(Mmax, E, d), s));
+      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, -1, s));
     }
     {  // dW_out = dH^T yg
       GemmTNArgs a;
@@ -378,7 +378,7 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
       GemmArgs g;
       g.A = F32(P.dxdbl); g.lda = XW; g.W = W.W_xT; g.ldw = XW; g.C = F32(P.du); g.ldc = E;
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = E; g.K = XW;
-      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, kResid, pick_gemm_f32_tile(Mmax, E, XW), s));
+      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, kResid, -1, s));
     }
     {  // dW_x = dxdbl^T u
       GemmTNArgs a;
@@ -392,7 +392,7 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
       GemmArgs g;
       g.A = F32(P.dxz); g.lda = 2 * E; g.W = W.W_inT; g.ldw = 2 * E; g.C = F32(P.dN); g.ldc = d;
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = d; g.K = 2 * E;
-      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, pick_gemm_f32_tile(Mmax, d, 2 * E), s));
+      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, -1, s));
     }
     {  // dW_in = dxz^T n
       GemmTNArgs a;

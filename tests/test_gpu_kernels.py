@@ -89,6 +89,47 @@ def test_gemm_f32_epilogues(M, N, K, tile, epilogue):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 100, 128), (1000, 256, 164), (777, 1024, 256),
+                                   (129, 36, 256), (40000, 96, 192)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "norm"])
+def test_gemm_f32_row_panels(M, N, K, mode):
+    """Row-panel tile (A held in registers): plain, + bias, RMSNorm row scale;
+    ragged M and N, every supported K."""
+    print(f"gemm panel mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 5 * N + 11 * K + len(mode))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C = tb.gemm_f32(_dev(A), _dev(W), _dev(bv) if bv is not None else None, tile=8,
+                    epilogue=2 if mode == "norm" else 0)
+    torch.cuda.synchronize()
+    A64, W64 = A.astype(np.float64), W.astype(np.float64)
+    ref = A64 @ W64.T
+    bound = (K + 2) * U * (np.abs(A64) @ np.abs(W64).T)
+    if mode == "bias":
+        ref += bv
+        bound += U * np.abs(ref)
+    elif mode == "norm":
+        rstd = 1.0 / np.sqrt(np.mean(A64 * A64, axis=1, keepdims=True) + 1e-5)
+        ref = rstd * ref
+        bound = rstd * bound + (K + 8) * U * np.abs(ref)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+def test_gemm_f32_row_panels_refuse_unsupported():
+    """No residual epilogue and only K in {64, 128, 164, 192, 256} on row panels."""
+    rng = np.random.default_rng(9)
+    A = _dev(rng.standard_normal((64, 256)).astype(np.float32))
+    W = _dev(rng.standard_normal((64, 256)).astype(np.float32))
+    with pytest.raises(tb.TclError):
+        tb.gemm_f32(A, W, out=torch.zeros(64, 64, device="cuda"), tile=8, epilogue=1)
+    A2 = _dev(rng.standard_normal((64, 100)).astype(np.float32))
+    W2 = _dev(rng.standard_normal((64, 100)).astype(np.float32))
+    with pytest.raises(tb.TclError):
+        tb.gemm_f32(A2, W2, tile=8)
+
+
 @pytest.mark.parametrize("M,N,K", [(1, 64, 8), (31, 48, 512), (129, 256, 168), (1000, 1024, 256),
                                    (257, 256, 512), (77, 100, 40)])
 @pytest.mark.parametrize("bias", [False, True])
