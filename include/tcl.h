@@ -224,8 +224,10 @@ TCL_API const char* tcl_last_error(void);
  * tile selects the workgroup tile (0..7: 128x128, 64x64, 64x128, 128x64,
  * 128x256, and 128x128 / 64x128 / 128x64 with K staged 64 at a time; 8: row
  * panels of 128 rows x all N with A held in registers, for K in {64, 128,
- * 164, 192, 256}, K % 4 == 0, no residual epilogue, else TCL_ERR_HIP); -1
- * picks what the model would use for M rows. */
+ * 164, 192, 256}, K % 4 == 0, no residual epilogue; 9: row panels of 64
+ * rows on 16x16 MFMA blocks for K in {256, 384, 512} (up to), K % 4 == 0,
+ * no RMSNorm; an unsupported combination returns TCL_ERR_HIP); -1 picks what
+ * the model would use for M rows. */
 TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const float* d_A,
                                      const float* d_W, const float* d_bias, float* d_C, int32_t tile,
                                      int32_t epilogue, void* stream);

@@ -154,7 +154,7 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       GemmArgs gx;
       gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
       gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_f32(gx, 0, kNarrow, s));
+      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_f32(gx, 0, -1, s));
 
       if (chunks > 0)
         TCL_LAUNCH(T, "scan_chunked", launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E,

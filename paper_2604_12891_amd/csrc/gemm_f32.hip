@@ -242,11 +242,14 @@ GemmTile pick_gemm_f32_tile(const GemmArgs& a, int flags) {
   // 78), because the last partial round of workgroups is shorter; the
   // gathered input Linear (K = 164) prefers 128x128 with K chunks of 64
   // (81 vs 67). At ~1.3M rows 128x128 is best for in_proj (115) and 64x128
-  // for out_proj (113). Row panels (K <= 256, no residual) replace the tiles
-  // once there are enough rows to give every CU two panels.
+  // for out_proj (113). Row panels replace the tiles once there are enough
+  // rows to give every CU two panels: in_proj 117 (B = 4096) and 127
+  // (L = 256) TFLOP/s, the input Linear 97; 16-row panels for out_proj 106
+  // and 114, and for x_proj (N = 48) 72 and 81 against 62 and 65 for 64x64.
   const int Mmax = a.Mmax, N = a.N, K = a.K;
-  if (N <= 64) return kNarrow;
   if (Mmax >= kPanelMinRows && gemm_f32_panel_fits(a, flags)) return kPanel;
+  if (Mmax >= kPanelMinRows && gemm_f32_panel16_fits(a, flags)) return kPanel16;
+  if (N <= 64) return kNarrow;
   if (K % 64 != 0) return Mmax >= 500000 ? kWide : kTile128x128K64;
   if (Mmax >= 500000 && N >= 1024) return kWide;
   return kTile64x128;
@@ -257,6 +260,10 @@ hipError_t launch_gemm_f32(const GemmArgs& a, int flags, int tile_id, hipStream_
   if (tile == kPanel) {
     if (!gemm_f32_panel_fits(a, flags)) return hipErrorInvalidValue;
     return launch_gemm_f32_panel(a, flags, s);
+  }
+  if (tile == kPanel16) {
+    if (!gemm_f32_panel16_fits(a, flags)) return hipErrorInvalidValue;
+    return launch_gemm_f32_panel16(a, flags, s);
   }
   switch (tile) {
     case kWide: return dispatch_flags<2, 2, 2, 2, 32>(a, flags, s);

@@ -46,8 +46,9 @@ enum GemmTile {
   kTile128x128K64 = 5,
   kTile64x128K64 = 6,
   kTile128x64K64 = 7,
-  kPanel = 8,  // row panels: 128 rows x all N per workgroup, A in registers (K <= 256, no residual)
-  kNumGemmTiles = 9
+  kPanel = 8,    // row panels: 128 rows x all N per workgroup, A in registers (K <= 256, no residual)
+  kPanel16 = 9,  // row panels of 64 rows on 16x16 MFMA blocks (K <= 512, no RMSNorm or gather)
+  kNumGemmTiles = 10
 };
 
 // tile < 0: the tile pick_gemm_f32_tile chooses for these arguments.
@@ -56,6 +57,8 @@ hipError_t launch_gemm_f32(const GemmArgs& a, int flags, int tile, hipStream_t s
 GemmTile pick_gemm_f32_tile(const GemmArgs& a, int flags);
 bool gemm_f32_panel_fits(const GemmArgs& a, int flags);
 hipError_t launch_gemm_f32_panel(const GemmArgs& a, int flags, hipStream_t s);
+bool gemm_f32_panel16_fits(const GemmArgs& a, int flags);
+hipError_t launch_gemm_f32_panel16(const GemmArgs& a, int flags, hipStream_t s);
 
 // bf16 GEMM: C = A W^T with A fp32 (converted while staged) or bf16, W bf16
 // ([N, ldw] row-major, zero-padded in K to a multiple of 8, ldw % 8 == 0),

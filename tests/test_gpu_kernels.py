@@ -117,8 +117,38 @@ def test_gemm_f32_row_panels(M, N, K, mode):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+@pytest.mark.parametrize("M,N,K", [(1, 64, 512), (300, 100, 384), (777, 256, 512), (1000, 48, 256),
+                                   (40000, 96, 500)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "resid"])
+def test_gemm_f32_row_panels16(M, N, K, mode):
+    """16-row panels (16x16 MFMA blocks, K up to 512): plain, + bias, and the
+    residual epilogue C += A W^T in place; ragged M, N and K."""
+    print(f"gemm panel16 mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 7 * N + 13 * K + len(mode))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C0 = rng.standard_normal((M, N)).astype(np.float32)
+    C = _dev(C0)
+    tb.gemm_f32(_dev(A), _dev(W), _dev(bv) if bv is not None else None, out=C, tile=9,
+                epilogue=1 if mode == "resid" else 0)
+    torch.cuda.synchronize()
+    A64, W64 = A.astype(np.float64), W.astype(np.float64)
+    ref = A64 @ W64.T
+    bound = (K + 2) * U * (np.abs(A64) @ np.abs(W64).T)
+    if mode == "bias":
+        ref += bv
+    elif mode == "resid":
+        ref += C0
+    if mode != "plain":
+        bound += U * np.abs(ref)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
 def test_gemm_f32_row_panels_refuse_unsupported():
-    """No residual epilogue and only K in {64, 128, 164, 192, 256} on row panels."""
+    """No residual epilogue and only K in {64, 128, 164, 192, 256} on 32-row
+    panels; no RMSNorm on 16-row panels."""
     rng = np.random.default_rng(9)
     A = _dev(rng.standard_normal((64, 256)).astype(np.float32))
     W = _dev(rng.standard_normal((64, 256)).astype(np.float32))
@@ -128,6 +158,8 @@ def test_gemm_f32_row_panels_refuse_unsupported():
     W2 = _dev(rng.standard_normal((64, 100)).astype(np.float32))
     with pytest.raises(tb.TclError):
         tb.gemm_f32(A2, W2, tile=8)
+    with pytest.raises(tb.TclError):
+        tb.gemm_f32(A, W, tile=9, epilogue=2)
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 64, 8), (31, 48, 512), (129, 256, 168), (1000, 1024, 256),
