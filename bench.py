@@ -134,10 +134,13 @@ def distill_kernel_work(tshape, sshape, M_v: int, B: int) -> dict:
     XW = R + 2 * N
     per_layer = d * E + E * R + XW * E + 2 * E * d  # out_proj, dt_proj, x_proj, in_proj
     tw = kernel_work(tshape, M_v, B, "bf16")
-    out = {("teacher:" + k): (kind, amount * (tshape.n_layers if k in ("gemm_in_proj", "gemm_x_proj",
-                                                                        "gemm_out_proj", "conv_silu", "scan")
-                                               else 1))
-           for k, (kind, amount) in tw.items()}
+    per_block = ("gemm_in_proj", "gemm_x_proj", "gemm_out_proj", "conv_silu", "scan")
+    out = {}
+    for k, (kind, amount) in tw.items():
+        reps = tshape.n_layers if k in per_block else 1
+        # the scan's work is a (flops, bytes) pair; scale both
+        amount = tuple(a * reps for a in amount) if isinstance(amount, tuple) else amount * reps
+        out["teacher:" + k] = (kind, amount)
     out.update({
         "gemm_dX": ("flop", 2 * M_v * per_layer * nl),
         "gemm_dW": ("flop", 2 * M_v * per_layer * nl + 2 * B * h * d + 2 * M_v * d * F),
@@ -209,6 +212,9 @@ def bench_distill(args, w):
     roof = {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 3), "peak": d["peak"],
             "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None,
             "ms_per_launch": round(d["ms_per_launch"], 5), "launches_per_step": d["launches_per_step"]}
+    if d["bound"] == "alu":
+        roof["hbm_achieved_gbs"] = round(d["hbm_gbs"], 1)
+        roof["hbm_frac"] = round(d["hbm_frac"], 4)
     if args.kernels:
         for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
             print(f"{k:28s} {e['ms_per_step']:9.4f} ms/step  x{e['launches_per_step']:3d}  "
