@@ -25,6 +25,9 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
 BF16_MFMA_PEAK_TFS = 2516.6    # MI355X dense bf16 matrix, TFLOP/s
+# fp32 GEMMs on the split path run six bf16 MFMA products per fp32 product:
+# their ceiling in fp32 flops is the bf16 peak / 6
+SPLIT_MFMA_PEAK_TFS = BF16_MFMA_PEAK_TFS / 6
 FP32_VALU_PEAK_TFS = 157.3     # MI355X fp32 vector (256 CUs x 4 SIMDs x 32 lanes x 2 flops x 2.4 GHz)
 
 
@@ -64,7 +67,7 @@ def kernel_work(shape, M_v: int, B: int, dtype: str) -> dict:
     }
 
 
-def roofline_entry(kind, amount, ms_per_launch, dtype):
+def roofline_entry(kind, amount, ms_per_launch, dtype, split=False):
     if kind == "valu":
         flops, nbytes = amount
         achieved = flops / (ms_per_launch * 1e-3) / 1e12
@@ -73,8 +76,16 @@ def roofline_entry(kind, amount, ms_per_launch, dtype):
                 "frac": achieved / FP32_VALU_PEAK_TFS, "hbm_gbs": hbm, "hbm_frac": hbm / HBM_PEAK_GBS}
     if kind == "flop":
         achieved = amount / (ms_per_launch * 1e-3) / 1e12
-        peak = FP32_MFMA_PEAK_TFS if dtype == "f32" else BF16_MFMA_PEAK_TFS
-        return {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak}
+        if dtype != "f32":
+            peak = BF16_MFMA_PEAK_TFS
+        else:
+            peak = SPLIT_MFMA_PEAK_TFS if split else FP32_MFMA_PEAK_TFS
+        e = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak}
+        if dtype == "f32" and split:
+            e["peak_note"] = ("fp32 flops on the bf16 matrix cores: operands split exactly into three bf16 "
+                              "parts, six part products per fp32 product, so the peak is the dense bf16 "
+                              "peak / 6 (2.67x the fp32 matrix peak)")
+        return e
     achieved = amount / (ms_per_launch * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS}
@@ -311,6 +322,9 @@ def main():
     ap.add_argument("--kernels", action="store_true", help="print the per-kernel table to stderr")
     ap.add_argument("--scan-sweep", action="store_true",
                     help="time the sequential against the chunked scan over batch sizes and exit")
+    ap.add_argument("--f32-matmul", choices=["split", "native"], default="split",
+                    help="fp32 models: projections on the bf16 matrix cores with split operands (fp32 "
+                         "accuracy), or on the fp32 matrix cores")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run 3 elementwise passes over 256 MiB (known bytes for HBM counters)")
     args = ap.parse_args()
@@ -348,7 +362,9 @@ def main():
         del src, dst
     Xd = torch.from_numpy(X).to(dev)
     Ld = torch.from_numpy(lengths).to(dev)
-    model = tb.CostModel(tb.config_from_shape(w.model, w.dtype), blob)
+    model = tb.CostModel(tb.config_from_shape(w.model, w.dtype, args.f32_matmul), blob)
+    split = w.dtype == "f32" and args.f32_matmul == "split"
+    split_kernels = ("gemm_input", "gemm_in_proj", "gemm_out_proj")
     ws = model.workspace(w.B, w.L)
     out = torch.empty(w.B, dtype=torch.float32, device=dev)
     M_v = int(lengths.sum())
@@ -385,7 +401,7 @@ def main():
         per = tot / n
         kind, amount = work[name]
         # launches of one kernel per step (e.g. one per block) all do the same work
-        e = roofline_entry(kind, amount, per, w.dtype)
+        e = roofline_entry(kind, amount, per, w.dtype, split and name in split_kernels)
         e.update({"ms_per_launch": per, "launches_per_step": n // args.steps,
                   "ms_per_step": tot / args.steps, "work_per_launch": amount, "work_unit": kind})
         kernels[name] = e
@@ -401,6 +417,8 @@ def main():
         roof["hbm_frac"] = round(d["hbm_frac"], 4)
         roof["alu_note"] = ("VALU issue slots of the recurrence (transcendentals at quarter rate) x 2 flops, "
                             "against the fp32 vector peak")
+    if "peak_note" in d:
+        roof["peak_note"] = d["peak_note"]
     if traffic is not None:
         roof["traffic_note"] = ("HBM bytes per launch, rocprofv3 FETCH_SIZE + WRITE_SIZE scaled by an "
                                 "elementwise kernel of known size (profiles/)")
@@ -430,6 +448,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "L": w.L, "F": w.model.F, "d_model": w.model.d_model,
+                   "f32_matmul": args.f32_matmul if w.dtype == "f32" else None,
                    "d_inner": w.model.d_inner, "d_state": w.model.d_state, "n_layers": w.model.n_layers,
                    "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v},
         "wall_ms_per_step": wall * 1e3 / args.steps,

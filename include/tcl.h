@@ -79,6 +79,17 @@ typedef enum tcl_dtype {
                    create; pass bf16-representable values to avoid that.    */
 } tcl_dtype;
 
+/* How an fp32 model runs its dense projections (the input Linear, in_proj
+ * and out_proj; x_proj, which moves more bytes than it computes, stays on
+ * the fp32 path either way). */
+typedef enum tcl_f32_matmul {
+  TCL_F32_MATMUL_SPLIT = 0, /* bf16 matrix cores, fp32 accuracy: both operands
+                               split exactly into three bf16 parts, the six
+                               part products above 2^-23 of the product
+                               accumulated in fp32                         */
+  TCL_F32_MATMUL_NATIVE = 1 /* fp32 matrix cores (v_mfma_f32_*_f32)         */
+} tcl_f32_matmul;
+
 /* Model hyper-parameters (section 5.2; the hyper-parameter study of
  * section 7.2.1 names d_state, d_conv, expand and n_layers).
  * Supported: F % 4 == 0, d_model in {64, 128, 256}, d_inner % 64 == 0 and
@@ -96,6 +107,7 @@ typedef struct tcl_config {
   int32_t final_norm;  /* 1: RMSNorm before the pool (section 5.2)  */
   float norm_eps;      /* RMSNorm epsilon                           */
   int32_t dtype;       /* tcl_dtype                                 */
+  int32_t f32_matmul;  /* tcl_f32_matmul (ignored for bf16 models)  */
 } tcl_config;
 
 typedef struct tcl_model tcl_model;     /* opaque, library-owned */
@@ -231,6 +243,23 @@ TCL_API const char* tcl_last_error(void);
 TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const float* d_A,
                                      const float* d_W, const float* d_bias, float* d_C, int32_t tile,
                                      int32_t epilogue, void* stream);
+
+/* The fp32 GEMM of the split path (TCL_F32_MATMUL_SPLIT): A and W fp32,
+ * each split exactly into three bf16 parts, six part products accumulated
+ * in fp32 on the bf16 matrix cores.
+ *   epilogue 0, 1, 2: as tcl_test_gemm_f32 (A [M,K]; d_offs, B, L ignored)
+ *   epilogue 3: C = A_g W^T + bias, A fp32 [B, L, K] padded, gathered by
+ *               d_offs as in tcl_test_gemm_bf16 kind 4 (M ignored)
+ * variant: 32 (32-row panels, K <= 256, epilogues 0, 2, 3), 16 (16-row
+ * panels, K rounded up to 64 in {64, 128, 256, 512}, epilogues 0, 1), -1
+ * what the model would pick; TCL_ERR_UNSUPPORTED otherwise.
+ * d_Wsplit: caller-owned device scratch of 3 * N * Kw uint16 (Kw = K rounded
+ * up to a multiple of 8, 16-byte aligned) that first receives W's parts.
+ * K % 4 == 0; A 16-byte aligned. */
+TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const float* d_A,
+                                       const int32_t* d_offs, int32_t B, int32_t L, const float* d_W,
+                                       const float* d_bias, float* d_C, int32_t variant,
+                                       int32_t epilogue, uint16_t* d_Wsplit, void* stream);
 
 /* The bf16 MFMA GEMM (v_mfma_f32_32x32x16_bf16, fp32 accumulation) in the
  * variants the bf16 model runs, selected by kind:

@@ -17,6 +17,8 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtcl.so"
 _lib = None
 
 TCL_F32, TCL_BF16 = 0, 1
+TCL_F32_MATMUL_SPLIT, TCL_F32_MATMUL_NATIVE = 0, 1
+F32_MATMUL = {"split": TCL_F32_MATMUL_SPLIT, "native": TCL_F32_MATMUL_NATIVE}
 STATUS = {0: "TCL_OK", -1: "TCL_ERR_INVALID_ARG", -2: "TCL_ERR_UNSUPPORTED", -3: "TCL_ERR_WORKSPACE",
           -4: "TCL_ERR_OOM", -5: "TCL_ERR_HIP"}
 
@@ -30,7 +32,8 @@ class TclError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("F", "d_model", "d_inner", "d_state", "d_conv", "dt_rank", "n_layers", "head_hidden",
-                 "final_norm")] + [("norm_eps", ctypes.c_float), ("dtype", ctypes.c_int32)]
+                 "final_norm")] + [("norm_eps", ctypes.c_float), ("dtype", ctypes.c_int32),
+                                   ("f32_matmul", ctypes.c_int32)]
 
 
 _vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
@@ -60,6 +63,7 @@ _SIGS = {
                                       ctypes.POINTER(ctypes.c_int64)]),
     "tcl_trainer_timing_reset": (_i32, [_vp]),
     "tcl_test_gemm_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _i32, _vp]),
+    "tcl_test_gemm_split": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp]),
     "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
@@ -91,14 +95,16 @@ def check(status: int):
 
 
 def make_config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden,
-                final_norm=1, norm_eps=1e-5, dtype="f32") -> Config:
+                final_norm=1, norm_eps=1e-5, dtype="f32", f32_matmul="split") -> Config:
+    """f32_matmul ("split" or "native") selects how an fp32 model runs its
+    dense projections (tcl_f32_matmul)."""
     return Config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden, final_norm,
-                  norm_eps, TCL_BF16 if dtype == "bf16" else TCL_F32)
+                  norm_eps, TCL_BF16 if dtype == "bf16" else TCL_F32, F32_MATMUL[f32_matmul])
 
 
-def config_from_shape(shape, dtype="f32") -> Config:
+def config_from_shape(shape, dtype="f32", f32_matmul="split") -> Config:
     return make_config(shape.F, shape.d_model, shape.d_inner, shape.d_state, shape.d_conv, shape.dt_rank,
-                       shape.n_layers, shape.head_hidden, shape.final_norm, shape.norm_eps, dtype)
+                       shape.n_layers, shape.head_hidden, shape.final_norm, shape.norm_eps, dtype, f32_matmul)
 
 
 def _ptr(t) -> Optional[int]:
@@ -264,6 +270,28 @@ def gemm_f32(A, W, bias=None, out=None, stream=None, tile=-1, epilogue=0):
         out = torch.empty(M, N, dtype=torch.float32, device=A.device)
     check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(), tile,
                                   epilogue, _stream(stream)))
+    return out
+
+
+def gemm_split(A, W, bias=None, out=None, stream=None, variant=-1, epilogue=0, offs=None):
+    """The split-path fp32 GEMM (tcl_test_gemm_split). epilogue 0: A W^T
+    (+ bias); 1: out += A W^T; 2: rstd(A) * A W^T; 3: A fp32 [B, L, K]
+    gathered by offs [B+1], + bias, out [B*L, N]. variant 32, 16 or -1."""
+    import torch
+    N, K = W.shape
+    if epilogue == 3:
+        Bp, L, _ = A.shape
+        M = Bp * L
+    else:
+        M, Bp, L = A.shape[0], 0, 0
+    if out is None:
+        if epilogue == 1:
+            raise ValueError("epilogue 1 accumulates into out")
+        out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    Kw = (K + 7) // 8 * 8
+    scratch = torch.empty(3 * N * Kw, dtype=torch.int16, device=A.device)
+    check(lib().tcl_test_gemm_split(M, N, K, A.data_ptr(), _ptr(offs), Bp, L, W.data_ptr(), _ptr(bias),
+                                    out.data_ptr(), variant, epilogue, scratch.data_ptr(), _stream(stream)))
     return out
 
 

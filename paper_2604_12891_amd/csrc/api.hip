@@ -140,14 +140,20 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
     g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
     g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
-    TCL_LAUNCH(T, "gemm_input", launch_gemm_f32(g, kBias | kGather, -1, s));
+    // the split path where it has a kernel for the shape, the fp32 MFMA path otherwise
+    auto gemm = [&](const GemmArgs& a, const uint16_t* Ws, int ldws, int flags) {
+      if (m->split && Ws && gemm_split_variant(a, flags) > 0)
+        return launch_gemm_split(a, Ws, ldws, flags, -1, s);
+      return launch_gemm_f32(a, flags, -1, s);
+    };
+    TCL_LAUNCH(T, "gemm_input", gemm(g, m->W0_s, m->ldw0_h, kBias | kGather));
 
     for (int l = 0; l < c.n_layers; ++l) {
       const auto& W = m->layers[l];
       GemmArgs gi;
       gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
       gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-      TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_f32(gi, kRowNorm, -1, s));
+      TCL_LAUNCH(T, "gemm_in_proj", gemm(gi, W.W_in_s, d, kRowNorm));
 
       TCL_LAUNCH(T, "conv_silu", launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w,
                                                          W.conv_b, u, s));
@@ -166,7 +172,7 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       GemmArgs go;
       go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
       go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-      TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_f32(go, kResid, -1, s));
+      TCL_LAUNCH(T, "gemm_out_proj", gemm(go, W.W_out_s, E, kResid));
     }
   } else {
     uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
@@ -217,6 +223,8 @@ tcl_status check_config(const tcl_config* c) {
     return fail(TCL_ERR_INVALID_ARG, "config has a non-positive field");
   if (c->dtype != TCL_F32 && c->dtype != TCL_BF16)
     return fail(TCL_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
+  if (c->f32_matmul != TCL_F32_MATMUL_SPLIT && c->f32_matmul != TCL_F32_MATMUL_NATIVE)
+    return fail(TCL_ERR_INVALID_ARG, "unknown f32_matmul %d", c->f32_matmul);
   if (c->F % 4) return fail(TCL_ERR_UNSUPPORTED, "F must be a multiple of 4 (got %d)", c->F);
   if (c->d_model != 64 && c->d_model != 128 && c->d_model != 256)
     return fail(TCL_ERR_UNSUPPORTED, "d_model must be 64, 128 or 256 (got %d)", c->d_model);
@@ -237,16 +245,18 @@ tcl_status check_config(const tcl_config* c) {
 
 namespace {
 
+bool uses_split(const tcl_config& c) { return c.dtype == TCL_F32 && c.f32_matmul == TCL_F32_MATMUL_SPLIT; }
+
 // Plan of the model's device block: every derived layout, then the master
 // blob, then the job table that derives the former from the latter.
 struct ModelPlan {
   std::vector<DeriveJob> jobs;
   int64_t total = 0;
   size_t bytes = 0, master = 0, jobtab = 0;
-  size_t W0 = 0, b0 = 0, W0_h = 0, g_f = 0, W1 = 0, W1T = 0, b1 = 0, W2 = 0, b2 = 0;
+  size_t W0 = 0, b0 = 0, W0_h = 0, W0_s = 0, g_f = 0, W1 = 0, W1T = 0, b1 = 0, W2 = 0, b2 = 0;
   struct L {
     size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
-    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h;
+    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_out_s;
   };
   std::vector<L> layers;
   int ldw0_h = 0;
@@ -259,11 +269,14 @@ struct ModelPlan {
 //  - transposed fp32 copies of W_out, W_x, W_in, W_dt (backward GEMMs) and W1
 //    (coalesced head reads);
 //  - bf16 copies of the projections for bf16 models, W0 zero-padded in K to
-//    a multiple of 8 (the padding is zeroed once at create).
+//    a multiple of 8 (the padding is zeroed once at create);
+//  - three-way bf16 splits of W0, W_in (gain folded) and W_out for fp32
+//    models on the split path, [3][rows][ld] each.
 ModelPlan plan_model(const tcl_config& c) {
   ModelPlan P;
   const BlobLayout bl = blob_layout(c);
   const bool bf = c.dtype == TCL_BF16;
+  const bool sp = uses_split(c);
   const int d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank, XW = R + 2 * N;
   const int F = c.F, h = c.head_hidden;
   P.ldw0_h = (F + 7) & ~7;
@@ -272,7 +285,8 @@ ModelPlan plan_model(const tcl_config& c) {
                  size_t src2 = 0) {
     const size_t dst = o;
     const int ldd = ld > 0 ? ld : (transpose ? rows : cols);
-    const size_t n_out = transpose ? (size_t)cols * ldd : (size_t)rows * ldd;
+    const int parts = (kind == kDeriveSplit || kind == kDeriveFoldSplit) ? 3 : 1;
+    const size_t n_out = parts * (transpose ? (size_t)cols * ldd : (size_t)rows * ldd);
     o = align256(o + n_out * elem_bytes);
     DeriveJob J{};
     J.start = P.total;
@@ -291,6 +305,7 @@ ModelPlan plan_model(const tcl_config& c) {
   P.W0 = job(bl.W0, d, F, kDeriveF32, 0, 4);
   P.b0 = job(bl.b0, 1, d, kDeriveF32, 0, 4);
   if (bf) P.W0_h = job(bl.W0, d, F, kDeriveBF16, 0, 2, P.ldw0_h);
+  if (sp) P.W0_s = job(bl.W0, d, F, kDeriveSplit, 0, 2, P.ldw0_h);
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& B = bl.layers[l];
     ModelPlan::L L{};
@@ -312,6 +327,10 @@ ModelPlan plan_model(const tcl_config& c) {
       L.W_in_h = job(B.W_in, 2 * E, d, kDeriveBF16, 0, 2);
       L.W_x_h = job(B.W_x, XW, E, kDeriveBF16, 0, 2);
       L.W_out_h = job(B.W_out, d, E, kDeriveBF16, 0, 2);
+    }
+    if (sp) {
+      L.W_in_s = job(B.W_in, 2 * E, d, kDeriveFoldSplit, 0, 2, -1, B.g);
+      L.W_out_s = job(B.W_out, d, E, kDeriveSplit, 0, 2);
     }
     P.layers.push_back(L);
   }
@@ -383,6 +402,8 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
   m->b0 = F32(P.b0);
   m->W0_h = bf ? B16(P.W0_h) : nullptr;
   m->ldw0_h = P.ldw0_h;
+  m->split = uses_split(*cfg);
+  m->W0_s = m->split ? B16(P.W0_s) : nullptr;
   for (const auto& L : P.layers) {
     tcl_model::Layer W{};
     W.W_in_fold = F32(L.W_in_fold);
@@ -403,6 +424,10 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
       W.W_in_h = B16(L.W_in_h);
       W.W_x_h = B16(L.W_x_h);
       W.W_out_h = B16(L.W_out_h);
+    }
+    if (m->split) {
+      W.W_in_s = B16(L.W_in_s);
+      W.W_out_s = B16(L.W_out_s);
     }
     m->layers.push_back(W);
   }
@@ -527,6 +552,46 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
   const int flags = epilogue == 1 ? kResid : epilogue == 2 ? kRowNorm : (d_bias ? kBias : 0);
   if (epilogue == 2 && d_bias) return fail(TCL_ERR_INVALID_ARG, "bias and row norm are exclusive");
   TCL_HIP(launch_gemm_f32(g, flags, tile, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
+TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const float* d_A,
+                                       const int32_t* d_offs, int32_t B, int32_t L, const float* d_W,
+                                       const float* d_bias, float* d_C, int32_t variant,
+                                       int32_t epilogue, uint16_t* d_Wsplit, void* stream) {
+  if (epilogue < 0 || epilogue > 3) return fail(TCL_ERR_INVALID_ARG, "bad epilogue %d", epilogue);
+  if (epilogue == 3) {
+    if (B <= 0 || L <= 0 || !d_offs) return fail(TCL_ERR_INVALID_ARG, "gather needs d_offs, B > 0, L > 0");
+    if (!d_bias) return fail(TCL_ERR_INVALID_ARG, "the gathered input Linear needs d_bias");
+    M = B * L;
+  }
+  if (M <= 0 || N <= 0 || K <= 0 || K % 4) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
+  if (variant != -1 && variant != 16 && variant != 32)
+    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 16 or 32 (got %d)", variant);
+  if ((epilogue == 1 || epilogue == 2) && d_bias)
+    return fail(TCL_ERR_INVALID_ARG, "bias goes with epilogues 0 and 3 only");
+  if (!d_A || !d_W || !d_C || !d_Wsplit) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_A) % 16 || reinterpret_cast<uintptr_t>(d_Wsplit) % 16)
+    return fail(TCL_ERR_INVALID_ARG, "A and the split buffer must be 16-byte aligned");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int Kw = (K + 7) & ~7;
+  GemmArgs g;
+  g.A = d_A; g.lda = K; g.W = d_W; g.ldw = K; g.bias = d_bias; g.C = d_C; g.ldc = N;
+  g.Mmax = M; g.N = N; g.K = K; g.eps = 1e-5f;
+  int flags = epilogue == 1 ? kResid : epilogue == 2 ? kRowNorm : (d_bias ? kBias : 0);
+  if (epilogue == 3) {
+    g.offs = d_offs; g.B = B; g.L = L; g.Mdev = d_offs + B;
+    flags = kBias | kGather;
+  }
+  const int v = gemm_split_variant(g, flags);
+  if (v < 0 || (variant == 32 && (flags & kResid)) || (variant == 16 && (flags & (kRowNorm | kGather))))
+    return fail(TCL_ERR_UNSUPPORTED, "no split kernel for K=%d with epilogue %d (variant %d)", K, epilogue,
+                variant);
+  if (variant == 16 && !((K + 63) / 64 == 1 || (K + 63) / 64 == 2 || (K + 63) / 64 == 4 || (K + 63) / 64 == 8))
+    return fail(TCL_ERR_UNSUPPORTED, "16-row split panels need K rounded up to 64 in {64, 128, 256, 512}");
+  if (variant == 32 && K > 256) return fail(TCL_ERR_UNSUPPORTED, "32-row split panels need K <= 256");
+  TCL_HIP(launch_split_weights(d_W, N, K, Kw, d_Wsplit, s));
+  TCL_HIP(launch_gemm_split(g, d_Wsplit, Kw, flags, variant, s));
   return TCL_OK;
 }
 

@@ -73,4 +73,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)(f32x2_to_bf16x2(f, 0.0f) & 0xFFFFu);
 }
 
+// Exact three-way split of fp32 values into bf16 parts, x = x1 + x2 + x3:
+// x1 = bf16(x), x2 = bf16(x - x1), x3 = x - x1 - x2. Both differences are
+// exact in fp32, |x2| <= 2^-8 |x|, |x3| <= 2^-16 |x|, and x3 has at most 8
+// significant bits, so bf16 holds it exactly (values below ~2^-110, whose
+// parts would be denormal, aside). Two values at a time; each output word
+// holds a's part in its low half and b's in its high half.
+__device__ __forceinline__ void split3_pair(float a, float b, uint32_t& h, uint32_t& m, uint32_t& l) {
+  h = f32x2_to_bf16x2(a, b);
+  const float ra = a - __uint_as_float(h << 16), rb = b - __uint_as_float(h & 0xFFFF0000u);
+  m = f32x2_to_bf16x2(ra, rb);
+  l = f32x2_to_bf16x2(ra - __uint_as_float(m << 16), rb - __uint_as_float(m & 0xFFFF0000u));
+}
+
 }  // namespace tcl

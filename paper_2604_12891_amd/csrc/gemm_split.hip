@@ -1,0 +1,436 @@
+// fp32 GEMMs on the bf16 matrix cores: C = rowscale * (A W^T) + bias (+ R),
+// A and W fp32, with fp32 accuracy.
+//
+// Every fp32 value splits exactly into three bf16 values, x = x1 + x2 + x3
+// (split3 in common.h). Of the nine products x_i y_j of two split values the
+// six with i + j <= 4 are kept; the three dropped ones (x2 y3, x3 y2, x3 y3)
+// are at most 2^-23 |x y| together, two units of fp32 rounding, while the
+// fp32 sum of a K-term dot product is itself only bounded by K units. Each
+// bf16 x bf16 product is exact in fp32 and the MFMA accumulates in fp32. On
+// gfx950 a bf16 MFMA does 16x the work of an fp32 MFMA in the same time, so
+// six of them reach 2.67x the fp32 matrix peak.
+//
+// Row panels, as in the fp32 and bf16 panel kernels: a workgroup of 4
+// wavefronts owns a panel of rows and all N columns.
+//  * prologue: each wavefront loads its rows of A once (gathered rows for
+//    the input Linear), takes the RMSNorm row statistics from them, splits
+//    them and keeps the three parts as MFMA fragments in registers;
+//  * main loop: the three bf16 parts of W (split once when the model's
+//    weights are derived) go through a double-buffered LDS stage a column
+//    block at a time, one barrier per block, the next block's W loaded into
+//    registers while the MFMAs run; per k-step a wavefront reads three W
+//    fragments and issues six MFMAs;
+//  * epilogue per block: row scale, bias and residual on the accumulators,
+//    buffer stores straight from them.
+// split32: v_mfma_f32_32x32x16_bf16, 32 rows per wavefront, K <= 256.
+// split16: v_mfma_f32_16x16x32_bf16, 16 rows per wavefront, K <= 512 (the
+// parts of a 32-row panel would not fit in registers at K = 512).
+//
+// Fragment k-order (A and W alike, which is all the contraction needs):
+// split32 k-step s, lane half g holds k = 16 s + 8 g .. +7; split16 k-step
+// s, lane quarter q holds k = 32 s + 8 q .. +7.
+#include "common.h"
+#include "kernels.h"
+
+namespace tcl {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr uint32_t kBufferFlags = 0x00020000;  // 32-bit data format, raw (stride 0)
+constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every resource used here
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferFlags);
+}
+
+// 8 consecutive fp32 values of a row -> their three bf16 parts, element j
+// of each fragment holding value j
+__device__ __forceinline__ void split8(const floatx4 a, const floatx4 b, bf16x8& p1, bf16x8& p2,
+                                       bf16x8& p3) {
+  const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  u32x4 w1, w2, w3;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t h, m, l;
+    split3_pair(x[2 * i], x[2 * i + 1], h, m, l);
+    w1[i] = h;
+    w2[i] = m;
+    w3[i] = l;
+  }
+  p1 = __builtin_bit_cast(bf16x8, w1);
+  p2 = __builtin_bit_cast(bf16x8, w2);
+  p3 = __builtin_bit_cast(bf16x8, w3);
+}
+
+// Loads 8 fp32 of row `arow` at k (zero past K or for a missing row);
+// K % 4 == 0, so each half is all in or all out.
+__device__ __forceinline__ void load8(const float* arow, bool rok, int k, int K, floatx4& v0,
+                                      floatx4& v1) {
+  const bool ok0 = rok && k < K, ok1 = rok && k + 4 < K;
+  v0 = *reinterpret_cast<const floatx4*>(arow + (ok0 ? k : 0));
+  v1 = *reinterpret_cast<const floatx4*>(arow + (ok1 ? k + 4 : 0));
+  if (!ok0) v0 = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (!ok1) v1 = floatx4{0.f, 0.f, 0.f, 0.f};
+}
+
+// The W stage of one column block: NR rows of each of the three parts, KC
+// chunks of 64 k. Unit u of the block is part u / (NR WU), row (u / WU) % NR,
+// k = 8 (u % WU); rows past N and k past the padded K read zero through the
+// resource (the part stride is N ldw, so a row past N must not be read as
+// the next part's).
+template <int NR, int KC>
+struct WStage {
+  static constexpr int WP = KC * 64 + 8;  // bf16 pitch of a staged row (conflict-free 16-byte reads)
+  static constexpr int WU = KC * 8;       // 16-byte units per row
+  static constexpr int NWU = 3 * NR * WU; // units per block
+  static constexpr int NW = (NWU + kWaves * 64 - 1) / (kWaves * 64);
+  u32x4 r[NW];
+  __device__ __forceinline__ void load(const __amdgpu_buffer_rsrc_t& res, int tid, int n0, int N,
+                                       int ldw, int Kw) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int u = tid + i * kWaves * 64;
+      const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = 8 * (u % WU);
+      const bool ok = (NWU % (kWaves * 64) == 0 || u < NWU) && n < N && k < Kw;
+      const uint32_t off = ok ? (uint32_t)((((int64_t)part * N + n) * ldw + k) * 2) : kOutOfRange;
+      r[i] = __builtin_amdgcn_raw_buffer_load_b128(res, off, 0, 0);
+    }
+  }
+  __device__ __forceinline__ void stage(uint16_t* s, int tid) const {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int u = tid + i * kWaves * 64;
+      if (NWU % (kWaves * 64) == 0 || u < NWU)
+        *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = r[i];
+    }
+  }
+};
+
+// ---------------------------------------------------------------- 32-row panels
+template <int KC, int FL>
+__global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p, const uint16_t* Ws,
+                                                                      int ldws) {
+  constexpr int NS = KC * 4;  // 16-k MFMA steps
+  constexpr int BM = kWaves * 32;
+  using Stage = WStage<32, KC>;
+  constexpr int WP = Stage::WP;
+  constexpr int PART = 32 * WP;  // one part of one buffer
+  constexpr bool kNorm = (FL & kRowNorm) != 0;
+  static_assert((FL & kResid) == 0, "32-row split panels have no residual epilogue");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
+  __shared__ float sR[kWaves][32];
+  __shared__ int sSrc[BM];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 31, lg = lane >> 5;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * BM;
+  if (row0 >= M) return;
+
+  for (int r = tid; r < BM; r += kWaves * 64) {
+    const int grow = row0 + r;
+    int src = grow < M ? grow : -1;
+    if constexpr ((FL & kGather) != 0) {
+      if (src >= 0) {
+        int lo = 0, hi = p.B;
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (p.offs[mid] <= grow) lo = mid; else hi = mid;
+        }
+        src = lo * p.L + (grow - p.offs[lo]);
+      }
+    }
+    sSrc[r] = src;
+  }
+
+  const int Kw = (p.K + 7) & ~7;
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const int nsteps = (p.N + 31) / 32;
+  Stage st;
+  st.load(wres, tid, 0, p.N, ldws, Kw);  // in flight during the prologue
+  __syncthreads();  // sSrc
+
+  // prologue: row li of this wavefront's 32, lane half lg's 8 k of every step
+  bf16x8 a1[NS], a2[NS], a3[NS];
+  {
+    const int src = sSrc[wave * 32 + li];
+    const float* arow = p.A + (src >= 0 ? (int64_t)src * p.lda : 0);
+    float ss = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      floatx4 v0, v1;
+      load8(arow, src >= 0, 16 * s + 8 * lg, p.K, v0, v1);
+      if constexpr (kNorm)
+        ss += v0.x * v0.x + v0.y * v0.y + v0.z * v0.z + v0.w * v0.w + v1.x * v1.x + v1.y * v1.y +
+              v1.z * v1.z + v1.w * v1.w;
+      split8(v0, v1, a1[s], a2[s], a3[s]);
+    }
+    if constexpr (kNorm) {
+      ss += __shfl_xor(ss, 32, 64);  // the other half of the row
+      if (lg == 0) sR[wave][li] = 1.0f / sqrtf(ss / (float)p.K + p.eps);
+    }
+  }
+
+  const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * 4);
+  const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
+
+  for (int s = 0; s < nsteps; ++s) {
+    const int buf = s & 1, n0 = s * 32;
+    st.stage(&sW[buf * 3 * PART], tid);
+    __syncthreads();  // block s visible; every wavefront is past block s-1's reads of this buffer's pair
+    if (s + 1 < nsteps) st.load(wres, tid, n0 + 32, p.N, ldws, Kw);
+
+    // two accumulation chains (the small part products, then the large),
+    // so that consecutive MFMAs do not wait for each other's results
+    floatx16 acc, acc2;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = acc2[r] = 0.f;
+    const uint16_t* wb = &sW[buf * 3 * PART + li * WP + 8 * lg];
+    auto wfrag = [&](int part, int ks) {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+    };
+    // W fragments two k-steps ahead of their MFMAs, in a ring of three
+    bf16x8 q[3][3];
+#pragma unroll
+    for (int ks = 0; ks < 2 && ks < NS; ++ks)
+#pragma unroll
+      for (int j = 0; j < 3; ++j) q[ks][j] = wfrag(j, ks);
+    __builtin_amdgcn_sched_group_barrier(0x0100, NS > 1 ? 6 : 3, 0);
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks) {
+      if (ks + 2 < NS) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) q[(ks + 2) % 3][j] = wfrag(j, ks + 2);
+      }
+      const bf16x8* w = q[ks % 3];
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc, 0, 0, 0);
+      if (ks + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+    }
+
+    // epilogue: lane l holds column l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
+    const int col = n0 + li;
+    const bool cok = col < p.N;
+    const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      float v = acc[r] + acc2[r];
+      if constexpr (kNorm) v *= sR[wave][rl];
+      v += bias;
+      // rows past M fall outside cres
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- 16-row panels
+template <int KC, int FL>
+__global__ __launch_bounds__(kWaves * 64, 1) void gemm_split16_kernel(GemmArgs p, const uint16_t* Ws,
+                                                                      int ldws) {
+  constexpr int NS = KC * 2;  // 32-k MFMA steps
+  constexpr int BM = kWaves * 16;
+  using Stage = WStage<16, KC>;
+  constexpr int WP = Stage::WP;
+  constexpr int PART = 16 * WP;
+  static_assert((FL & (kRowNorm | kGather)) == 0, "16-row split panels serve plain, bias and residual GEMMs");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int lr = lane & 15, lq = lane >> 4;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * BM;
+  if (row0 >= M) return;
+
+  const int Kw = (p.K + 7) & ~7;
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const int nsteps = (p.N + 15) / 16;
+  Stage st;
+  st.load(wres, tid, 0, p.N, ldws, Kw);
+
+  // prologue: row lr of this wavefront's 16, lane quarter lq's 8 k of every step
+  bf16x8 a1[NS], a2[NS], a3[NS];
+  {
+    const int grow = row0 + wave * 16 + lr;
+    const bool rok = grow < M;
+    const float* arow = p.A + (rok ? (int64_t)grow * p.lda : 0);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      floatx4 v0, v1;
+      load8(arow, rok, 32 * s + 8 * lq, p.K, v0, v1);
+      split8(v0, v1, a1[s], a2[s], a3[s]);
+    }
+  }
+
+  const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * 4);
+  const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
+  const __amdgpu_buffer_rsrc_t rres =
+      make_rsrc((p.R ? p.R : p.C) + (int64_t)row0 * p.ldc, (FL & kResid) != 0 ? panel_bytes : 0);
+
+  for (int s = 0; s < nsteps; ++s) {
+    const int buf = s & 1, n0 = s * 16;
+    st.stage(&sW[buf * 3 * PART], tid);
+    __syncthreads();  // block s visible; block s-1's reads of this buffer's pair done
+    if (s + 1 < nsteps) st.load(wres, tid, n0 + 16, p.N, ldws, Kw);
+
+    // the residual of this block's outputs, loaded while the MFMAs run
+    const int col = n0 + lr;
+    const bool cok = col < p.N;
+    float res[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr ((FL & kResid) != 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t off = cok ? (uint32_t)(((wave * 16 + 4 * lq + r) * p.ldc + col) * 4) : kOutOfRange;
+        res[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rres, off, 0, 0));
+      }
+    }
+
+    floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f}, acc2 = acc;  // two chains, as above
+    const uint16_t* wb = &sW[buf * 3 * PART + lr * WP + 8 * lq];
+    auto wfrag = [&](int part, int ks) {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 32 * ks));
+    };
+    bf16x8 q[3][3];
+#pragma unroll
+    for (int ks = 0; ks < 2 && ks < NS; ++ks)
+#pragma unroll
+      for (int j = 0; j < 3; ++j) q[ks][j] = wfrag(j, ks);
+    __builtin_amdgcn_sched_group_barrier(0x0100, NS > 1 ? 6 : 3, 0);
+#pragma unroll
+    for (int ks = 0; ks < NS; ++ks) {
+      if (ks + 2 < NS) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) q[(ks + 2) % 3][j] = wfrag(j, ks + 2);
+      }
+      const bf16x8* w = q[ks % 3];
+      acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3[ks], w[0], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2[ks], w[0], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[ks], w[2], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[ks], w[1], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2[ks], w[1], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[ks], w[0], acc, 0, 0, 0);
+      if (ks + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+    }
+
+    // epilogue: lane l holds column l % 16 and rows 4*(l/16) + r
+    const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v = (acc[r] + acc2[r]) + bias + res[r];
+      const uint32_t off = cok ? (uint32_t)(((wave * 16 + 4 * lq + r) * p.ldc + col) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+    }
+  }
+}
+
+template <int FL>
+hipError_t launch32(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
+  const int grid = (a.Mmax + kWaves * 32 - 1) / (kWaves * 32);
+  if (grid <= 0) return hipSuccess;
+#define TCL_SPLIT32(KC)                                                                            \
+  hipLaunchKernelGGL((gemm_split32_kernel<KC, FL>), dim3(grid), dim3(kWaves * 64), 0, s, a, Ws, ldws); \
+  break
+  switch ((a.K + 63) / 64) {
+    case 1: TCL_SPLIT32(1);
+    case 2: TCL_SPLIT32(2);
+    case 3: TCL_SPLIT32(3);
+    case 4: TCL_SPLIT32(4);
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_SPLIT32
+  return hipGetLastError();
+}
+
+template <int FL>
+hipError_t launch16(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
+  const int grid = (a.Mmax + kWaves * 16 - 1) / (kWaves * 16);
+  if (grid <= 0) return hipSuccess;
+#define TCL_SPLIT16(KC)                                                                            \
+  hipLaunchKernelGGL((gemm_split16_kernel<KC, FL>), dim3(grid), dim3(kWaves * 64), 0, s, a, Ws, ldws); \
+  break
+  switch ((a.K + 63) / 64) {
+    case 1: TCL_SPLIT16(1);
+    case 2: TCL_SPLIT16(2);
+    case 4: TCL_SPLIT16(4);
+    case 8: TCL_SPLIT16(8);
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_SPLIT16
+  return hipGetLastError();
+}
+
+// W -> its three bf16 parts, [3][N][ldw], the padding k >= K zero
+__global__ __launch_bounds__(256) void split_weights_kernel(const float* __restrict__ W, int N, int K,
+                                                            int ldw, uint16_t* __restrict__ out) {
+  const int64_t n_all = (int64_t)N * ldw;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_all; i += (int64_t)gridDim.x * 256) {
+    const int n = (int)(i / ldw), k = (int)(i % ldw);
+    const float v = k < K ? W[(int64_t)n * K + k] : 0.f;
+    uint32_t h, m, l;
+    split3_pair(v, 0.f, h, m, l);
+    out[i] = (uint16_t)h;
+    out[n_all + i] = (uint16_t)m;
+    out[2 * n_all + i] = (uint16_t)l;
+  }
+}
+
+}  // namespace
+
+int gemm_split_variant(const GemmArgs& a, int flags) {
+  const bool al = a.K % 4 == 0 && a.lda % 4 == 0 && reinterpret_cast<uintptr_t>(a.A) % 16 == 0 &&
+                  // byte offsets of the buffer resources stay below 2^31
+                  (int64_t)3 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31) &&
+                  (int64_t)kWaves * 32 * a.ldc * 4 < (1ll << 31);
+  if (!al) return -1;
+  const int kc = (a.K + 63) / 64;
+  if ((flags & kResid) == 0 && kc <= 4) return 32;
+  if ((flags & (kRowNorm | kGather)) == 0 && (kc == 1 || kc == 2 || kc == 4 || kc == 8)) return 16;
+  return -1;
+}
+
+hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, int flags, int variant,
+                             hipStream_t s) {
+  if (variant < 0) variant = gemm_split_variant(a, flags);
+  if (variant == 32) {
+    switch (flags) {
+      case 0: return launch32<0>(a, Ws, ldws, s);
+      case kBias: return launch32<kBias>(a, Ws, ldws, s);
+      case kRowNorm: return launch32<kRowNorm>(a, Ws, ldws, s);
+      case kBias | kGather: return launch32<kBias | kGather>(a, Ws, ldws, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (variant == 16) {
+    switch (flags) {
+      case 0: return launch16<0>(a, Ws, ldws, s);
+      case kBias: return launch16<kBias>(a, Ws, ldws, s);
+      case kResid: return launch16<kResid>(a, Ws, ldws, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s) {
+  if (N <= 0 || K <= 0 || ldw < K) return hipErrorInvalidValue;
+  const int64_t n_all = (int64_t)N * ldw;
+  const int grid = (int)std::min<int64_t>((n_all + 255) / 256, 4096);
+  hipLaunchKernelGGL(split_weights_kernel, dim3(grid), dim3(256), 0, s, W, N, K, ldw, out);
+  return hipGetLastError();
+}
+
+}  // namespace tcl

@@ -60,6 +60,18 @@ hipError_t launch_gemm_f32_panel(const GemmArgs& a, int flags, hipStream_t s);
 bool gemm_f32_panel16_fits(const GemmArgs& a, int flags);
 hipError_t launch_gemm_f32_panel16(const GemmArgs& a, int flags, hipStream_t s);
 
+// fp32 GEMM on the bf16 matrix cores, with fp32 accuracy: A (fp32, from
+// GemmArgs) and W split three ways into bf16 parts, six of the nine part
+// products accumulated in fp32. Ws holds W's parts as [3][N][ldws] bf16
+// (ldws >= K, a multiple of 8, the padding zero; launch_split_weights or the
+// model's derived weights). GemmArgs.W is not read. Variants: 32 (32-row
+// MFMA blocks, K <= 256, no residual) and 16 (16-row blocks, K in 64, 128,
+// 256 or 512 rounded up to 64, no RMSNorm or gather); -1 picks one.
+int gemm_split_variant(const GemmArgs& a, int flags);  // 32, 16, or -1 (unsupported)
+hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, int flags, int variant,
+                             hipStream_t s);
+hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s);
+
 // bf16 GEMM: C = A W^T with A fp32 (converted while staged) or bf16, W bf16
 // ([N, ldw] row-major, zero-padded in K to a multiple of 8, ldw % 8 == 0),
 // C fp32 or bf16, fp32 accumulation. kRowNorm also scales A by gain[k]
@@ -198,8 +210,9 @@ hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, cons
 // all jobs (job j covers [start_j, start_j + rows*cols)); the destination is a
 // byte offset in the model's device block. kDeriveFold multiplies column c by
 // master[src2 + c]. With round_bf16 every master value is first rounded to
-// bf16 (bf16 models compute with the rounded weights).
-enum DeriveKind { kDeriveF32 = 0, kDeriveBF16 = 1, kDeriveFold = 2 };
+// bf16 (bf16 models compute with the rounded weights). The split kinds write
+// the three bf16 parts of the (folded) value to dst as [3][rows][ld].
+enum DeriveKind { kDeriveF32 = 0, kDeriveBF16 = 1, kDeriveFold = 2, kDeriveSplit = 3, kDeriveFoldSplit = 4 };
 struct DeriveJob {
   int64_t start, src, src2, dst;
   int32_t rows, cols, ld, transpose, kind, pad_;

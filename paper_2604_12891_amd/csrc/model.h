@@ -91,11 +91,16 @@ struct tcl_model {
     float *W_outT, *W_xT, *W_inT, *W_dtT;
     // bf16 copies (bf16 models)
     uint16_t *W_in_h, *W_x_h, *W_out_h;
+    // three-way bf16 splits, [3][rows][cols] (fp32 models on the split path):
+    // W_in with the gain folded, W_out
+    uint16_t *W_in_s, *W_out_s;
   };
   float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1 = nullptr, *W1T = nullptr,
         *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;
   uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
   int ldw0_h = 0;
+  uint16_t* W0_s = nullptr;  // three-way bf16 split of W0, [3][d][ldw0_h] (split path)
+  bool split = false;        // fp32 model whose projections run on the split path
   std::vector<Layer> layers;
   tcl::Timing timing;
 };

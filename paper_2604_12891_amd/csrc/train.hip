@@ -582,14 +582,25 @@ __global__ __launch_bounds__(256) void derive_kernel(const float* __restrict__ m
     const int r = (int)(k / J.cols), c = (int)(k % J.cols);
     float v = master[J.src + k];
     if (round_bf16) v = round_to_bf16(v);
-    if (J.kind == kDeriveFold) {
+    if (J.kind == kDeriveFold || J.kind == kDeriveFoldSplit) {
       float gv = master[J.src2 + c];
       if (round_bf16) gv = round_to_bf16(gv);
       v = v * gv;
     }
     const int64_t o = J.transpose ? (int64_t)c * J.ld + r : (int64_t)r * J.ld + c;
-    if (J.kind == kDeriveBF16) reinterpret_cast<uint16_t*>(base + J.dst)[o] = f32_to_bf16(v);
-    else reinterpret_cast<float*>(base + J.dst)[o] = v;
+    if (J.kind == kDeriveSplit || J.kind == kDeriveFoldSplit) {
+      uint32_t h, m, l;
+      split3_pair(v, 0.f, h, m, l);
+      uint16_t* d = reinterpret_cast<uint16_t*>(base + J.dst);
+      const int64_t part = (int64_t)(J.transpose ? J.cols : J.rows) * J.ld;
+      d[o] = (uint16_t)h;
+      d[part + o] = (uint16_t)m;
+      d[2 * part + o] = (uint16_t)l;
+    } else if (J.kind == kDeriveBF16) {
+      reinterpret_cast<uint16_t*>(base + J.dst)[o] = f32_to_bf16(v);
+    } else {
+      reinterpret_cast<float*>(base + J.dst)[o] = v;
+    }
   }
 }
 

@@ -72,6 +72,10 @@ def test_create_rejects_bad_arguments(lib):
     bad.norm_eps = 0.0
     st, _ = _create(lib, bad, blob)
     assert st == -1
+    bad = tb.config_from_shape(wl.TINY)
+    bad.f32_matmul = 2
+    st, _ = _create(lib, bad, blob)
+    assert st == -1 and b"f32_matmul" in lib.tcl_last_error()
 
 
 def test_calls_on_null_handles(lib):
@@ -81,6 +85,28 @@ def test_calls_on_null_handles(lib):
     assert lib.tcl_get_params(None, None, 0) == -1
     assert lib.tcl_test_gemm_f32(0, 4, 4, None, None, None, None, -1, 0, None) == -1
     assert lib.tcl_test_scan_f32(1, 16, 8, 4, 0, *([None] * 4), 16, *([None] * 6)) in (-1, -2)
+
+
+def test_split_gemm_entry_rejects_bad_arguments(lib):
+    """Argument checks of tcl_test_gemm_split run on the host."""
+    fake = 1 << 20
+    args = dict(M=8, N=8, K=8, A=fake, offs=None, B=0, L=0, W=fake, bias=None, C=fake, variant=-1,
+                epilogue=0, Wsplit=fake, stream=None)
+
+    def call(**kw):
+        a = dict(args, **kw)
+        return lib.tcl_test_gemm_split(*a.values())
+
+    assert call(K=6) == -1            # K % 4
+    assert call(variant=8) == -1
+    assert call(epilogue=4) == -1
+    assert call(epilogue=3) == -1     # the gather needs offsets and B, L
+    assert call(epilogue=3, offs=fake, B=2, L=3) == -1  # ... and the bias
+    assert call(epilogue=1, bias=fake) == -1
+    assert call(Wsplit=None) == -1
+    assert call(A=fake + 4) == -1     # alignment
+    assert call(K=320, variant=32) == -2
+    assert call(K=320, variant=16) == -2
 
 
 def test_bf16_gemm_entry_rejects_bad_arguments(lib):

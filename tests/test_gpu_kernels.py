@@ -354,3 +354,121 @@ def test_scan_in_place_matches_out_of_place(chunks):
     tb.scan_f32(offs, u_copy, *d[1:], u_copy, chunks=chunks)
     torch.cuda.synchronize()
     assert torch.equal(out, u_copy)
+
+
+# ---------------------------------------------------------------- split path (fp32 on bf16 MFMA)
+# Both operands split exactly into three bf16 parts; the three dropped part
+# products are at most 2^-23 |a w| = 2U |a w| per product, so the bound is the
+# fp32 dot-product bound with two more units: (K + 4) U sum |a_k w_k|.
+
+def _split_ref(A, W, mode, bv=None, C0=None):
+    A64, W64 = A.astype(np.float64), W.astype(np.float64)
+    K = A.shape[1]
+    ref = A64 @ W64.T
+    bound = (K + 4) * U * (np.abs(A64) @ np.abs(W64).T)
+    if mode == "bias":
+        ref = ref + bv
+        bound = bound + U * np.abs(ref)
+    elif mode == "resid":
+        ref = ref + C0
+        bound = bound + U * np.abs(ref)
+    elif mode == "norm":
+        rstd = 1.0 / np.sqrt(np.mean(A64 * A64, axis=1, keepdims=True) + 1e-5)
+        ref = rstd * ref
+        bound = rstd * bound + (K + 8) * U * np.abs(ref)
+    return ref, bound
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 4), (129, 256, 164), (1000, 1024, 256), (77, 100, 36),
+                                   (300, 48, 64), (40000, 96, 192)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "norm"])
+def test_gemm_split32(M, N, K, mode):
+    """32-row split panels (K <= 256): plain, + bias, RMSNorm row scale; ragged
+    M, N and K (K % 8 == 4 exercises a half-filled last k unit)."""
+    print(f"gemm split32 mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 3 * N + 17 * K + len(mode))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C = tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, variant=32,
+                      epilogue=2 if mode == "norm" else 0)
+    torch.cuda.synchronize()
+    ref, bound = _split_ref(A, W, mode, bv)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 512), (31, 48, 500), (257, 256, 512), (77, 100, 64),
+                                   (200, 256, 128), (65, 40, 256), (40000, 96, 512)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "resid"])
+def test_gemm_split16(M, N, K, mode):
+    """16-row split panels (K up to 512): plain, + bias, and the residual
+    epilogue C += A W^T in place; ragged M, N and K."""
+    print(f"gemm split16 mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 7 * N + 19 * K + len(mode))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C0 = rng.standard_normal((M, N)).astype(np.float32)
+    C = _dev(C0)
+    tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, out=C, variant=16,
+                  epilogue=1 if mode == "resid" else 0)
+    torch.cuda.synchronize()
+    ref, bound = _split_ref(A, W, mode, bv, C0)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+def test_gemm_split_gather():
+    """The input Linear on the split path: rows gathered from padded [B, L, F]
+    features by token offsets, + bias; the padding (NaN here) is never read."""
+    rng = np.random.default_rng(41)
+    B, L, K, N = 37, 25, 164, 256
+    lengths = rng.integers(1, L + 1, B).astype(np.int32)
+    X = rng.standard_normal((B, L, K)).astype(np.float32)
+    for b in range(B):
+        X[b, lengths[b]:] = np.nan
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32)
+    offs = _offs(lengths)
+    C = tb.gemm_split(_dev(X), _dev(W), _dev(bv), variant=32, epilogue=3, offs=_dev(offs, torch.int32))
+    torch.cuda.synchronize()
+    Ap = _pack(X, lengths)
+    ref, bound = _split_ref(Ap, W, "bias", bv)
+    got = C.cpu().numpy()[:offs[-1]]
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got))
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+def test_gemm_split_error_matches_native_fp32():
+    """The split path is as accurate as the fp32 matrix cores: on the model's
+    projection shapes its rms error against fp64 stays within 1.5x of the
+    fp32 MFMA kernel's (and both within the fp32 bound above)."""
+    rng = np.random.default_rng(7)
+    for (M, N, K, variant, tile) in [(4096, 1024, 256, 32, 8), (4096, 256, 512, 16, 9)]:
+        A = rng.standard_normal((M, K)).astype(np.float32)
+        W = (rng.uniform(-1, 1, (N, K)) / np.sqrt(K)).astype(np.float32)
+        ref = A.astype(np.float64) @ W.astype(np.float64).T
+        s = tb.gemm_split(_dev(A), _dev(W), variant=variant).cpu().numpy()
+        n = tb.gemm_f32(_dev(A), _dev(W), tile=tile).cpu().numpy()
+        e_split = float(np.sqrt(np.mean((s - ref) ** 2)))
+        e_nat = float(np.sqrt(np.mean((n - ref) ** 2)))
+        print(f"M={M} N={N} K={K}: rms error split {e_split:.3e}, native fp32 {e_nat:.3e}", flush=True)
+        assert e_split <= 1.5 * e_nat
+
+
+def test_gemm_split_refuses_unsupported():
+    rng = np.random.default_rng(3)
+    A = _dev(rng.standard_normal((64, 320)).astype(np.float32))
+    W = _dev(rng.standard_normal((64, 320)).astype(np.float32))
+    with pytest.raises(tb.TclError):        # 32-row panels stop at K = 256
+        tb.gemm_split(A, W, variant=32)
+    with pytest.raises(tb.TclError):        # K = 320 rounds up to 384: no 16-row kernel
+        tb.gemm_split(A, W, variant=16)
+    A2 = _dev(rng.standard_normal((64, 256)).astype(np.float32))
+    W2 = _dev(rng.standard_normal((64, 256)).astype(np.float32))
+    with pytest.raises(tb.TclError):        # no residual epilogue on 32-row panels
+        tb.gemm_split(A2, W2, out=torch.zeros(64, 64, device="cuda"), variant=32, epilogue=1)
+    with pytest.raises(tb.TclError):        # no RMSNorm on 16-row panels
+        tb.gemm_split(A2, W2, variant=16, epilogue=2)

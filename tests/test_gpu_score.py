@@ -17,8 +17,8 @@ from tests.parity import assert_scores_match, oracle_scores
 pytestmark = pytest.mark.gpu
 
 
-def _model(shape, blob, dtype="f32"):
-    return tb.CostModel(tb.config_from_shape(shape, dtype), blob)
+def _model(shape, blob, dtype="f32", f32_matmul="split"):
+    return tb.CostModel(tb.config_from_shape(shape, dtype, f32_matmul), blob)
 
 
 def _score(model, X, lengths):
@@ -35,38 +35,42 @@ def _sample(lengths, n, seed=0):
     return np.array(sorted(idx))[:max(n, 4)]
 
 
+@pytest.mark.parametrize("f32_matmul", ["split", "native"])
 @pytest.mark.parametrize("perturb", [False, True])
-def test_tiny_full_batch(perturb):
+def test_tiny_full_batch(perturb, f32_matmul):
     w = wl.WORKLOADS["score_B64_L25_d64_f32"]
-    print(f"tcl_score {w.name} perturb={perturb}", flush=True)
+    print(f"tcl_score {w.name} perturb={perturb} {f32_matmul}", flush=True)
     blob, X, lengths = wl.make_workload(w.name, perturb=perturb)
-    g = _score(_model(w.model, blob), X, lengths)
+    g = _score(_model(w.model, blob, f32_matmul=f32_matmul), X, lengths)
     assert_scores_match(g, oracle_scores(blob, X, lengths, w.model), "f32", w.name)
 
 
-def test_headline_full_size_sampled():
+@pytest.mark.parametrize("f32_matmul", ["split", "native"])
+def test_headline_full_size_sampled(f32_matmul):
     w = wl.WORKLOADS["score_B4096_L25_d256_f32"]
-    print(f"tcl_score {w.name} full batch", flush=True)
+    print(f"tcl_score {w.name} full batch {f32_matmul}", flush=True)
     blob, X, lengths = wl.make_workload(w.name)
-    g = _score(_model(w.model, blob), X, lengths)
+    g = _score(_model(w.model, blob, f32_matmul=f32_matmul), X, lengths)
     assert np.all(np.isfinite(g))
     idx = _sample(lengths, 96)
     assert_scores_match(g[idx], oracle_scores(blob, X[idx], lengths[idx], w.model), "f32", w.name)
 
 
-def test_headline_shape_perturbed_weights():
+@pytest.mark.parametrize("f32_matmul", ["split", "native"])
+def test_headline_shape_perturbed_weights(f32_matmul):
     w = wl.WORKLOADS["score_B4096_L25_d256_f32"]
     blob, X, lengths = wl.make_workload(w.name, B=160, perturb=True)
-    print(f"tcl_score {w.name} B=160 perturbed", flush=True)
-    g = _score(_model(w.model, blob), X, lengths)
+    print(f"tcl_score {w.name} B=160 perturbed {f32_matmul}", flush=True)
+    g = _score(_model(w.model, blob, f32_matmul=f32_matmul), X, lengths)
     assert_scores_match(g, oracle_scores(blob, X, lengths, w.model), "f32", w.name + " perturbed")
 
 
-def test_long_sequences_sampled():
+@pytest.mark.parametrize("f32_matmul", ["split", "native"])
+def test_long_sequences_sampled(f32_matmul):
     w = wl.WORKLOADS["score_B8192_L256_d256_f32"]
-    print(f"tcl_score {w.name} full batch", flush=True)
+    print(f"tcl_score {w.name} full batch {f32_matmul}", flush=True)
     blob, X, lengths = wl.make_workload(w.name)
-    g = _score(_model(w.model, blob), X, lengths)
+    g = _score(_model(w.model, blob, f32_matmul=f32_matmul), X, lengths)
     assert np.all(np.isfinite(g))
     idx = _sample(lengths, 12, seed=1)
     assert_scores_match(g[idx], oracle_scores(blob, X[idx], lengths[idx], w.model), "f32", w.name)
