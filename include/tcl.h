@@ -250,9 +250,11 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
  *   epilogue 0, 1, 2: as tcl_test_gemm_f32 (A [M,K]; d_offs, B, L ignored)
  *   epilogue 3: C = A_g W^T + bias, A fp32 [B, L, K] padded, gathered by
  *               d_offs as in tcl_test_gemm_bf16 kind 4 (M ignored)
- * variant: 32 (32-row panels, K <= 256, epilogues 0, 2, 3), 16 (16-row
- * panels, K rounded up to 64 in {64, 128, 256, 512}, epilogues 0, 1), -1
- * what the model would pick; TCL_ERR_UNSUPPORTED otherwise.
+ * variant: 1 (32-row panels, K <= 256, epilogues 0, 2, 3), 2 (16-row
+ * panels, K rounded up to 64 in {64, 128, 256, 512}, epilogues 0, 1), 3
+ * (32-row panels with all N columns accumulated in registers, N <= 256,
+ * K <= 512, epilogues 0, 1), -1 what the model would pick;
+ * TCL_ERR_UNSUPPORTED otherwise.
  * d_Wsplit: caller-owned device scratch of 3 * N * Kw uint16 (Kw = K rounded
  * up to a multiple of 8, 16-byte aligned) that first receives W's parts.
  * K % 4 == 0; A 16-byte aligned. */

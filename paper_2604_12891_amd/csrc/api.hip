@@ -566,8 +566,8 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
     M = B * L;
   }
   if (M <= 0 || N <= 0 || K <= 0 || K % 4) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
-  if (variant != -1 && variant != 16 && variant != 32)
-    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 16 or 32 (got %d)", variant);
+  if (variant < -1 || variant > 3 || variant == 0)
+    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 1, 2 or 3 (got %d)", variant);
   if ((epilogue == 1 || epilogue == 2) && d_bias)
     return fail(TCL_ERR_INVALID_ARG, "bias goes with epilogues 0 and 3 only");
   if (!d_A || !d_W || !d_C || !d_Wsplit) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
@@ -583,15 +583,12 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
     g.offs = d_offs; g.B = B; g.L = L; g.Mdev = d_offs + B;
     flags = kBias | kGather;
   }
-  const int v = gemm_split_variant(g, flags);
-  if (v < 0 || (variant == 32 && (flags & kResid)) || (variant == 16 && (flags & (kRowNorm | kGather))))
-    return fail(TCL_ERR_UNSUPPORTED, "no split kernel for K=%d with epilogue %d (variant %d)", K, epilogue,
-                variant);
-  if (variant == 16 && !((K + 63) / 64 == 1 || (K + 63) / 64 == 2 || (K + 63) / 64 == 4 || (K + 63) / 64 == 8))
-    return fail(TCL_ERR_UNSUPPORTED, "16-row split panels need K rounded up to 64 in {64, 128, 256, 512}");
-  if (variant == 32 && K > 256) return fail(TCL_ERR_UNSUPPORTED, "32-row split panels need K <= 256");
+  const int v = variant < 0 ? gemm_split_variant(g, flags) : variant;
+  if (v < 0 || !gemm_split_supports(g, flags, v))
+    return fail(TCL_ERR_UNSUPPORTED, "no split kernel for N=%d K=%d with epilogue %d (variant %d)", N, K,
+                epilogue, variant);
   TCL_HIP(launch_split_weights(d_W, N, K, Kw, d_Wsplit, s));
-  TCL_HIP(launch_gemm_split(g, d_Wsplit, Kw, flags, variant, s));
+  TCL_HIP(launch_gemm_split(g, d_Wsplit, Kw, flags, v, s));
   return TCL_OK;
 }
 

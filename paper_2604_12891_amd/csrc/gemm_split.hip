@@ -17,14 +17,24 @@
 //    them and keeps the three parts as MFMA fragments in registers;
 //  * main loop: the three bf16 parts of W (split once when the model's
 //    weights are derived) go through a double-buffered LDS stage a column
-//    block at a time, one barrier per block, the next block's W loaded into
-//    registers while the MFMAs run; per k-step a wavefront reads three W
+//    block at a time, one barrier per block; the next block's W is loaded
+//    into registers at the start of a block and written to the other buffer
+//    halfway through its MFMAs (with one wavefront per SIMD nothing else
+//    would cover the staging); per k-step a wavefront reads three W
 //    fragments and issues six MFMAs;
 //  * epilogue per block: row scale, bias and residual on the accumulators,
 //    buffer stores straight from them.
-// split32: v_mfma_f32_32x32x16_bf16, 32 rows per wavefront, K <= 256.
-// split16: v_mfma_f32_16x16x32_bf16, 16 rows per wavefront, K <= 512 (the
-// parts of a 32-row panel would not fit in registers at K = 512).
+// Variants (what limits them is the LDS traffic of the streamed W
+// fragments: one fragment read feeds two MFMAs on average, so a 16-row
+// panel on 16x16 blocks needs twice the LDS bytes per flop of a 32-row one):
+//  1. split32: v_mfma_f32_32x32x16_bf16, 32 rows per wavefront, K <= 256,
+//     any N (in_proj, the input Linear);
+//  2. split16: v_mfma_f32_16x16x32_bf16, 16 rows per wavefront, K <= 512,
+//     any N;
+//  3. split32acc: 32 rows per wavefront and N <= 256, K <= 512: the
+//     accumulators of all N columns stay in registers while K is walked in
+//     chunks (of 128 above K = 256; A's parts for one chunk at a time), so
+//     a 32-row panel fits at K = 512 (out_proj).
 //
 // Fragment k-order (A and W alike, which is all the contraction needs):
 // split32 k-step s, lane half g holds k = 16 s + 8 g .. +7; split16 k-step
@@ -89,11 +99,11 @@ struct WStage {
   static constexpr int NW = (NWU + kWaves * 64 - 1) / (kWaves * 64);
   u32x4 r[NW];
   __device__ __forceinline__ void load(const __amdgpu_buffer_rsrc_t& res, int tid, int n0, int N,
-                                       int ldw, int Kw) {
+                                       int ldw, int Kw, int k0 = 0) {
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
       const int u = tid + i * kWaves * 64;
-      const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = 8 * (u % WU);
+      const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = k0 + 8 * (u % WU);
       const bool ok = (NWU % (kWaves * 64) == 0 || u < NWU) && n < N && k < Kw;
       const uint32_t off = ok ? (uint32_t)((((int64_t)part * N + n) * ldw + k) * 2) : kOutOfRange;
       r[i] = __builtin_amdgcn_raw_buffer_load_b128(res, off, 0, 0);
@@ -179,11 +189,14 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p
   const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * 4);
   const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
 
+  st.stage(&sW[0], tid);
   for (int s = 0; s < nsteps; ++s) {
     const int buf = s & 1, n0 = s * 32;
-    st.stage(&sW[buf * 3 * PART], tid);
-    __syncthreads();  // block s visible; every wavefront is past block s-1's reads of this buffer's pair
-    if (s + 1 < nsteps) st.load(wres, tid, n0 + 32, p.N, ldws, Kw);
+    // block s (staged during block s-1) visible; every wavefront is past
+    // block s-1, so the other buffer is free for block s+1
+    __syncthreads();
+    const bool more = s + 1 < nsteps;
+    if (more) st.load(wres, tid, n0 + 32, p.N, ldws, Kw);
 
     // two accumulation chains (the small part products, then the large),
     // so that consecutive MFMAs do not wait for each other's results
@@ -216,6 +229,11 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc, 0, 0, 0);
       if (ks + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
       __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+      // block s+1 into the other buffer halfway through this block's MFMAs
+      if (ks == NS / 2 && more) {
+        st.stage(&sW[(buf ^ 1) * 3 * PART], tid);
+        __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
+      }
     }
 
     // epilogue: lane l holds column l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
@@ -280,11 +298,12 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split16_kernel(GemmArgs p
   const __amdgpu_buffer_rsrc_t rres =
       make_rsrc((p.R ? p.R : p.C) + (int64_t)row0 * p.ldc, (FL & kResid) != 0 ? panel_bytes : 0);
 
+  st.stage(&sW[0], tid);
   for (int s = 0; s < nsteps; ++s) {
     const int buf = s & 1, n0 = s * 16;
-    st.stage(&sW[buf * 3 * PART], tid);
-    __syncthreads();  // block s visible; block s-1's reads of this buffer's pair done
-    if (s + 1 < nsteps) st.load(wres, tid, n0 + 16, p.N, ldws, Kw);
+    __syncthreads();  // block s visible; the other buffer is free for block s+1
+    const bool more = s + 1 < nsteps;
+    if (more) st.load(wres, tid, n0 + 16, p.N, ldws, Kw);
 
     // the residual of this block's outputs, loaded while the MFMAs run
     const int col = n0 + lr;
@@ -324,6 +343,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split16_kernel(GemmArgs p
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[ks], w[0], acc, 0, 0, 0);
       if (ks + 2 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
       __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+      if (ks == NS / 2 && more) {
+        st.stage(&sW[(buf ^ 1) * 3 * PART], tid);
+        __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
+      }
     }
 
     // epilogue: lane l holds column l % 16 and rows 4*(l/16) + r
@@ -332,6 +355,125 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split16_kernel(GemmArgs p
     for (int r = 0; r < 4; ++r) {
       const float v = (acc[r] + acc2[r]) + bias + res[r];
       const uint32_t off = cok ? (uint32_t)(((wave * 16 + 4 * lq + r) * p.ldc + col) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- 32-row panels, all N in registers
+// KCH chunks of KC * 64 k; NB 32-column blocks (N <= 32 NB).
+template <int KC, int KCH, int NB, int FL>
+__global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArgs p, const uint16_t* Ws,
+                                                                         int ldws) {
+  constexpr int NS = KC * 4;  // 16-k MFMA steps per chunk
+  constexpr int BM = kWaves * 32;
+  using Stage = WStage<32, KC>;
+  constexpr int WP = Stage::WP;
+  constexpr int PART = 32 * WP;
+  static_assert((FL & (kRowNorm | kGather)) == 0, "plain, bias and residual GEMMs only");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 31, lg = lane >> 5;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * BM;
+  if (row0 >= M) return;
+
+  const int Kw = (p.K + 7) & ~7;
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  Stage st;
+  st.load(wres, tid, 0, p.N, ldws, Kw, 0);
+
+  const int grow = row0 + wave * 32 + li;
+  const bool rok = grow < M;
+  const float* arow = p.A + (rok ? (int64_t)grow * p.lda : 0);
+
+  floatx16 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+  st.stage(&sW[0], tid);
+
+#pragma unroll
+  for (int c = 0; c < KCH; ++c) {
+    // keep the next chunk's loads of A below this point: hoisted, they would
+    // hold a second set of A's parts in registers
+    __builtin_amdgcn_sched_barrier(0);
+    // this chunk of the wavefront's 32 rows -> three parts in registers
+    bf16x8 a1[NS], a2[NS], a3[NS];
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) {
+      floatx4 v0, v1;
+      load8(arow, rok, c * KC * 64 + 16 * s2 + 8 * lg, p.K, v0, v1);
+      split8(v0, v1, a1[s2], a2[s2], a3[s2]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int buf = (c * NB + nb) & 1;
+      __syncthreads();  // this block visible; the other buffer is free for the next
+      const bool more = nb + 1 < NB || c + 1 < KCH;
+      if (nb + 1 < NB) st.load(wres, tid, (nb + 1) * 32, p.N, ldws, Kw, c * KC * 64);
+      else if (c + 1 < KCH) st.load(wres, tid, 0, p.N, ldws, Kw, (c + 1) * KC * 64);
+
+      const uint16_t* wb = &sW[buf * 3 * PART + li * WP + 8 * lg];
+      auto wfrag = [&](int part, int ks) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+      };
+      // W fragments one k-step ahead (a ring of two: registers are scarce here)
+      bf16x8 q[2][3];
+#pragma unroll
+      for (int j = 0; j < 3; ++j) q[0][j] = wfrag(j, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks) {
+        if (ks + 1 < NS) {
+#pragma unroll
+          for (int j = 0; j < 3; ++j) q[(ks + 1) & 1][j] = wfrag(j, ks + 1);
+        }
+        const bf16x8* w = q[ks & 1];
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc[nb], 0, 0, 0);
+        if (ks + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+        if (ks == NS / 2 && more) {
+          st.stage(&sW[(buf ^ 1) * 3 * PART], tid);
+          __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
+        }
+      }
+    }
+  }
+
+  // epilogue: lane l holds column nb*32 + l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
+  const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * 4);
+  const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
+  const __amdgpu_buffer_rsrc_t rres =
+      make_rsrc((p.R ? p.R : p.C) + (int64_t)row0 * p.ldc, (FL & kResid) != 0 ? panel_bytes : 0);
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = nb * 32 + li;
+    const bool cok = col < p.N;
+    const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+    float res[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      res[r] = ((FL & kResid) != 0)
+                   ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rres, off, 0, 0))
+                   : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      const float v = acc[nb][r] + bias + res[r];
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
     }
   }
@@ -373,6 +515,36 @@ hipError_t launch16(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t
   return hipGetLastError();
 }
 
+template <int KC, int KCH, int FL>
+hipError_t launch32acc_nb(const GemmArgs& a, const uint16_t* Ws, int ldws, int grid, hipStream_t s) {
+  const int nb = (a.N + 31) / 32;
+#define TCL_SPLIT32ACC(NB) \
+  hipLaunchKernelGGL((gemm_split32acc_kernel<KC, KCH, NB, FL>), dim3(grid), dim3(kWaves * 64), 0, s, a, Ws, ldws)
+  if (nb <= 2) TCL_SPLIT32ACC(2);
+  else if (nb <= 4) TCL_SPLIT32ACC(4);
+  else if (nb <= 8) TCL_SPLIT32ACC(8);
+  else return hipErrorInvalidValue;
+#undef TCL_SPLIT32ACC
+  return hipGetLastError();
+}
+
+template <int FL>
+hipError_t launch32acc(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
+  const int grid = (a.Mmax + kWaves * 32 - 1) / (kWaves * 32);
+  if (grid <= 0) return hipSuccess;
+  switch ((a.K + 63) / 64) {
+    case 1: return launch32acc_nb<1, 1, FL>(a, Ws, ldws, grid, s);
+    case 2: return launch32acc_nb<2, 1, FL>(a, Ws, ldws, grid, s);
+    case 3: return launch32acc_nb<3, 1, FL>(a, Ws, ldws, grid, s);
+    case 4: return launch32acc_nb<4, 1, FL>(a, Ws, ldws, grid, s);
+    // K > 256: chunks of 128 (A's parts of a 256-k chunk, 128 accumulators
+    // and the W stage's registers would not fit together)
+    case 5: case 6: return launch32acc_nb<2, 3, FL>(a, Ws, ldws, grid, s);
+    case 7: case 8: return launch32acc_nb<2, 4, FL>(a, Ws, ldws, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 // W -> its three bf16 parts, [3][N][ldw], the padding k >= K zero
 __global__ __launch_bounds__(256) void split_weights_kernel(const float* __restrict__ W, int N, int K,
                                                             int ldw, uint16_t* __restrict__ out) {
@@ -390,22 +562,44 @@ __global__ __launch_bounds__(256) void split_weights_kernel(const float* __restr
 
 }  // namespace
 
-int gemm_split_variant(const GemmArgs& a, int flags) {
+bool gemm_split_supports(const GemmArgs& a, int flags, int variant) {
   const bool al = a.K % 4 == 0 && a.lda % 4 == 0 && reinterpret_cast<uintptr_t>(a.A) % 16 == 0 &&
                   // byte offsets of the buffer resources stay below 2^31
                   (int64_t)3 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31) &&
                   (int64_t)kWaves * 32 * a.ldc * 4 < (1ll << 31);
-  if (!al) return -1;
+  if (!al || a.K < 1) return false;
   const int kc = (a.K + 63) / 64;
-  if ((flags & kResid) == 0 && kc <= 4) return 32;
-  if ((flags & (kRowNorm | kGather)) == 0 && (kc == 1 || kc == 2 || kc == 4 || kc == 8)) return 16;
+  const bool plain = (flags & (kRowNorm | kGather)) == 0;
+  switch (variant) {
+    case kSplit32: return (flags & kResid) == 0 && kc <= 4;
+    case kSplit16: return plain && (kc == 1 || kc == 2 || kc == 4 || kc == 8);
+    case kSplit32Acc: return plain && kc <= 8 && a.N <= 256;
+    default: return false;
+  }
+}
+
+int gemm_split_variant(const GemmArgs& a, int flags) {
+  // 32-row panels first (half the LDS traffic per flop of 16-row ones);
+  // streaming N blocks when K fits one chunk, else all of N in registers
+  if ((flags & kResid) == 0 && gemm_split_supports(a, flags, kSplit32)) return kSplit32;
+  if (gemm_split_supports(a, flags, kSplit32Acc)) return kSplit32Acc;
+  if (gemm_split_supports(a, flags, kSplit16)) return kSplit16;
   return -1;
 }
 
 hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, int flags, int variant,
                              hipStream_t s) {
   if (variant < 0) variant = gemm_split_variant(a, flags);
-  if (variant == 32) {
+  if (!gemm_split_supports(a, flags, variant)) return hipErrorInvalidValue;
+  if (variant == kSplit32Acc) {
+    switch (flags) {
+      case 0: return launch32acc<0>(a, Ws, ldws, s);
+      case kBias: return launch32acc<kBias>(a, Ws, ldws, s);
+      case kResid: return launch32acc<kResid>(a, Ws, ldws, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (variant == kSplit32) {
     switch (flags) {
       case 0: return launch32<0>(a, Ws, ldws, s);
       case kBias: return launch32<kBias>(a, Ws, ldws, s);
@@ -414,7 +608,7 @@ hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, in
       default: return hipErrorInvalidValue;
     }
   }
-  if (variant == 16) {
+  if (variant == kSplit16) {
     switch (flags) {
       case 0: return launch16<0>(a, Ws, ldws, s);
       case kBias: return launch16<kBias>(a, Ws, ldws, s);

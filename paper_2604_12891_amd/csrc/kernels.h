@@ -64,10 +64,16 @@ hipError_t launch_gemm_f32_panel16(const GemmArgs& a, int flags, hipStream_t s);
 // GemmArgs) and W split three ways into bf16 parts, six of the nine part
 // products accumulated in fp32. Ws holds W's parts as [3][N][ldws] bf16
 // (ldws >= K, a multiple of 8, the padding zero; launch_split_weights or the
-// model's derived weights). GemmArgs.W is not read. Variants: 32 (32-row
-// MFMA blocks, K <= 256, no residual) and 16 (16-row blocks, K in 64, 128,
-// 256 or 512 rounded up to 64, no RMSNorm or gather); -1 picks one.
-int gemm_split_variant(const GemmArgs& a, int flags);  // 32, 16, or -1 (unsupported)
+// model's derived weights). GemmArgs.W is not read. Variants:
+//   kSplit32: 32-row MFMA blocks, K <= 256, no residual;
+//   kSplit16: 16-row blocks, K rounded up to 64 in {64, 128, 256, 512}, no
+//             RMSNorm or gather;
+//   kSplit32Acc: 32-row blocks with all N columns accumulated in registers,
+//             N <= 256, K <= 512, no RMSNorm or gather.
+enum GemmSplitVariant { kSplit32 = 1, kSplit16 = 2, kSplit32Acc = 3 };
+bool gemm_split_supports(const GemmArgs& a, int flags, int variant);
+int gemm_split_variant(const GemmArgs& a, int flags);  // the variant the model uses, or -1 (none)
+// variant < 0: gemm_split_variant's pick; hipErrorInvalidValue if unsupported
 hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, int flags, int variant,
                              hipStream_t s);
 hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s);

@@ -105,8 +105,10 @@ def test_split_gemm_entry_rejects_bad_arguments(lib):
     assert call(epilogue=1, bias=fake) == -1
     assert call(Wsplit=None) == -1
     assert call(A=fake + 4) == -1     # alignment
-    assert call(K=320, variant=32) == -2
-    assert call(K=320, variant=16) == -2
+    assert call(K=320, variant=1) == -2
+    assert call(K=320, variant=2) == -2
+    assert call(N=300, variant=3) == -2
+    assert call(K=600, variant=3) == -2
 
 
 def test_bf16_gemm_entry_rejects_bad_arguments(lib):

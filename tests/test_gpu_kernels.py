@@ -390,7 +390,7 @@ def test_gemm_split32(M, N, K, mode):
     A = rng.standard_normal((M, K)).astype(np.float32)
     W = rng.standard_normal((N, K)).astype(np.float32)
     bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
-    C = tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, variant=32,
+    C = tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, variant=1,
                       epilogue=2 if mode == "norm" else 0)
     torch.cuda.synchronize()
     ref, bound = _split_ref(A, W, mode, bv)
@@ -411,7 +411,7 @@ def test_gemm_split16(M, N, K, mode):
     bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
     C0 = rng.standard_normal((M, N)).astype(np.float32)
     C = _dev(C0)
-    tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, out=C, variant=16,
+    tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, out=C, variant=2,
                   epilogue=1 if mode == "resid" else 0)
     torch.cuda.synchronize()
     ref, bound = _split_ref(A, W, mode, bv, C0)
@@ -431,7 +431,7 @@ def test_gemm_split_gather():
     W = rng.standard_normal((N, K)).astype(np.float32)
     bv = rng.standard_normal(N).astype(np.float32)
     offs = _offs(lengths)
-    C = tb.gemm_split(_dev(X), _dev(W), _dev(bv), variant=32, epilogue=3, offs=_dev(offs, torch.int32))
+    C = tb.gemm_split(_dev(X), _dev(W), _dev(bv), variant=1, epilogue=3, offs=_dev(offs, torch.int32))
     torch.cuda.synchronize()
     Ap = _pack(X, lengths)
     ref, bound = _split_ref(Ap, W, "bias", bv)
@@ -446,7 +446,7 @@ def test_gemm_split_error_matches_native_fp32():
     projection shapes its rms error against fp64 stays within 1.5x of the
     fp32 MFMA kernel's (and both within the fp32 bound above)."""
     rng = np.random.default_rng(7)
-    for (M, N, K, variant, tile) in [(4096, 1024, 256, 32, 8), (4096, 256, 512, 16, 9)]:
+    for (M, N, K, variant, tile) in [(4096, 1024, 256, 1, 8), (4096, 256, 512, 3, 9), (4096, 256, 512, 2, 9)]:
         A = rng.standard_normal((M, K)).astype(np.float32)
         W = (rng.uniform(-1, 1, (N, K)) / np.sqrt(K)).astype(np.float32)
         ref = A.astype(np.float64) @ W.astype(np.float64).T
@@ -463,12 +463,39 @@ def test_gemm_split_refuses_unsupported():
     A = _dev(rng.standard_normal((64, 320)).astype(np.float32))
     W = _dev(rng.standard_normal((64, 320)).astype(np.float32))
     with pytest.raises(tb.TclError):        # 32-row panels stop at K = 256
-        tb.gemm_split(A, W, variant=32)
+        tb.gemm_split(A, W, variant=1)
     with pytest.raises(tb.TclError):        # K = 320 rounds up to 384: no 16-row kernel
-        tb.gemm_split(A, W, variant=16)
+        tb.gemm_split(A, W, variant=2)
     A2 = _dev(rng.standard_normal((64, 256)).astype(np.float32))
     W2 = _dev(rng.standard_normal((64, 256)).astype(np.float32))
-    with pytest.raises(tb.TclError):        # no residual epilogue on 32-row panels
-        tb.gemm_split(A2, W2, out=torch.zeros(64, 64, device="cuda"), variant=32, epilogue=1)
+    with pytest.raises(tb.TclError):        # no residual epilogue on streaming 32-row panels
+        tb.gemm_split(A2, W2, out=torch.zeros(64, 64, device="cuda"), variant=1, epilogue=1)
     with pytest.raises(tb.TclError):        # no RMSNorm on 16-row panels
-        tb.gemm_split(A2, W2, variant=16, epilogue=2)
+        tb.gemm_split(A2, W2, variant=2, epilogue=2)
+    with pytest.raises(tb.TclError):        # no RMSNorm with all of N in registers
+        tb.gemm_split(A2, W2, variant=3, epilogue=2)
+    W3 = _dev(rng.standard_normal((300, 256)).astype(np.float32))
+    with pytest.raises(tb.TclError):        # ... which holds N <= 256
+        tb.gemm_split(A2, W3, variant=3)
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 512), (31, 48, 500), (257, 256, 512), (77, 100, 64),
+                                   (200, 256, 128), (65, 40, 256), (129, 200, 164), (40000, 256, 512),
+                                   (300, 96, 384)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "resid"])
+def test_gemm_split32acc(M, N, K, mode):
+    """32-row split panels with all N columns accumulated in registers (N <=
+    256, K <= 512 in chunks of 256): plain, + bias, residual in place."""
+    print(f"gemm split32acc mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 11 * N + 23 * K + len(mode))
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C0 = rng.standard_normal((M, N)).astype(np.float32)
+    C = _dev(C0)
+    tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, out=C, variant=3,
+                  epilogue=1 if mode == "resid" else 0)
+    torch.cuda.synchronize()
+    ref, bound = _split_ref(A, W, mode, bv, C0)
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
