@@ -241,20 +241,36 @@ constexpr int kHalfN = 8;
 
 // Reduce 16 values across the 32 same-parity lanes of a wavefront: lane l
 // ends with the total (over lanes of parity l & 1) of value ((l >> 2) & 15).
+// A reduce-scatter over lane bits 5, 4, 3, 2, then a plain sum over bit 1.
+// The bit-5 and bit-4 steps use gfx950's half-wave / row swaps, which route
+// both values of a pair at once (no per-lane select); bit 3 is a DPP row
+// rotate by 8 (= xor 8 inside a row of 16), bit 2 a swizzle (xor 4), bit 1 a
+// DPP quad permutation. Every lane of the wavefront must be active.
+__device__ __forceinline__ float dpp_xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
+}
 __device__ __forceinline__ float butterfly16(float* v, int lane) {
+  float w[8], x[4];
 #pragma unroll
-  for (int step = 0; step < 4; ++step) {
-    const int half = 8 >> step;       // values kept after this step
-    const int mask = 32 >> step;      // partner lane distance
-    const bool up = (lane & mask) != 0;
-#pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const float mine = up ? v[half + i] : v[i];
-      const float other = up ? v[i] : v[half + i];
-      v[i] = mine + __shfl_xor(other, mask, 64);
-    }
+  for (int i = 0; i < 8; ++i) {  // lanes 0-31 keep v[i], 32-63 keep v[8 + i]
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[8 + i]), false, false);
+    w[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
   }
-  return v[0] + __shfl_xor(v[0], 2, 64);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {  // rows 0, 2 keep w[i], rows 1, 3 keep w[4 + i]
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(w[i]), __float_as_uint(w[4 + i]), false, false);
+    x[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  const bool b3 = (lane & 8) != 0, b2 = (lane & 4) != 0;
+  float y[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {  // bit 3: row_ror:8
+    const float mine = b3 ? x[2 + i] : x[i], other = b3 ? x[i] : x[2 + i];
+    y[i] = mine + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(other), 0x128, 0xF, 0xF, false));
+  }
+  const float mine = b2 ? y[1] : y[0], other = b2 ? y[0] : y[1];
+  const float z = mine + __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(other), 0x101F));  // xor 4
+  return z + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(z), 0x4E, 0xF, 0xF, false));  // xor 2
 }
 
 template <int N, int R, typename T>
@@ -411,8 +427,8 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
           red[n] = g[n] * dt * uv;          // dB_t[n0 + n] contribution
           red[NH + n] = dy * hist[tt][n];   // dC_t[n0 + n] contribution
         }
-        gB += __shfl_xor(gB, 1, 64);
-        ddt_a += __shfl_xor(ddt_a, 1, 64);
+        gB += dpp_xor1(gB);
+        ddt_a += dpp_xor1(ddt_a);
         if (hf == 0) {
           dD = fmaf(dy, uv, dD);
           dxz[row * ldz + E + e] = gc[tt] * yc[tt] * silu_grad(zv);
