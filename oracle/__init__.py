@@ -4,3 +4,4 @@ Only the tests, the smoke check and the benchmark's CPU-baseline leg use
 this package. It never imports the HIP library's package.
 """
 from . import model  # noqa: F401
+from . import kd  # noqa: F401
