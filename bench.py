@@ -179,16 +179,31 @@ def bench_distill(args, w):
     Yd = (t + torch.from_numpy(wl.label_noise(w.B)).to(dev)).contiguous()
     tr = tb.Trainer(teacher, student, lr=1e-3, max_B=w.B, max_L=w.L)
     ws = tr.workspace(w.B, w.L)
-    loss = torch.empty(3, dtype=torch.float32, device=dev)
+    kd = args.objective == "kd"
+    loss = torch.empty(4 if kd else 3, dtype=torch.float32, device=dev)
     M_v = int(lengths.sum())
+    if kd:
+        # Eq. (9) with the paper's beta = 0.5 and lambda = 1e4; a fixed gate
+        # phi = 0.7 and a seeded Fisher diagonal / previous-task parameters
+        krng = np.random.default_rng(12891)
+        fisher = torch.from_numpy(krng.random(sblob.size).astype(np.float32)).to(dev)
+        theta_prev = torch.from_numpy((sblob + 1e-3 * krng.standard_normal(sblob.size)).astype(np.float32)).to(dev)
+        kd_args = dict(beta=0.5, phi=0.7, sigma=1.0, ewc_lambda=1e4, fisher=fisher, theta_prev=theta_prev)
+
+    def one_step():
+        if kd:
+            tr.step_kd(Xd, Ld, Yd, loss=loss, workspace=ws, **kd_args)
+        else:
+            tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+
     for _ in range(args.warmup):
-        tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+        one_step()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record()
     for _ in range(args.steps):
-        tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+        one_step()
     e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -200,7 +215,7 @@ def bench_distill(args, w):
     tr.timing_reset()
     teacher.timing_reset()
     for _ in range(args.steps):
-        tr.step(Xd, Ld, Yd, loss=loss, workspace=ws)
+        one_step()
     torch.cuda.synchronize()
     rep = {("teacher:" + k): v for k, v in teacher.timing_report().items()}
     rep.update(tr.timing_report())
@@ -243,7 +258,13 @@ def bench_distill(args, w):
         n = 64
         labels = Yd.cpu().numpy()
         t0 = time.perf_counter()
-        om.distill_step(tblob, ocfg(w.model), sblob, ocfg(w.student), X[:n], lengths[:n], labels[:n])
+        if kd:
+            from oracle import kd as okd
+            okd.distill_step_kd(tblob, ocfg(w.model), sblob, ocfg(w.student), X[:n], lengths[:n], labels[:n],
+                                beta=0.5, phi=0.7, lam=1e4, fisher=fisher.cpu().numpy(),
+                                theta_prev=theta_prev.cpu().numpy())
+        else:
+            om.distill_step(tblob, ocfg(w.model), sblob, ocfg(w.student), X[:n], lengths[:n], labels[:n])
         dt = time.perf_counter() - t0
         blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
         cpu = {"value": 1.0 / (dt * w.B / n), "unit": "steps/s", "cores": max([p.get("num_threads", 1) for p in blas] or [1]),
@@ -251,11 +272,14 @@ def bench_distill(args, w):
                "sample": f"one fp64 numpy step on {n} of the {w.B} programs ({dt:.1f} s), scaled linearly "
                          f"to the full batch (programs are independent)"}
     rec = {
-        "metric": "distillation steps/sec (B=1024,L=25)", "value": 1000.0 / ms, "unit": "steps/s",
+        "metric": "distillation steps/sec (B=1024,L=25)" + (", Eq. (9) ranking objective" if kd else ""),
+        "value": 1000.0 / ms, "unit": "steps/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "L": w.L, "teacher": "d256 E512 N16 x4",
-                   "student": "d128 E256 N16 x2", "valid_tokens": M_v, "launches_per_step": launches},
+                   "student": "d128 E256 N16 x2", "valid_tokens": M_v, "launches_per_step": launches,
+                   "objective": ("beta 0.5 LambdaRank(s; labels) + 0.5 phi LambdaRank(s; teacher) + EWC "
+                                 "(lambda 1e4), phi 0.7" if kd else "mse(s, teacher) + mse(s, labels)")},
         "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
                     for k, e in kernels.items()},
@@ -322,6 +346,9 @@ def main():
     ap.add_argument("--kernels", action="store_true", help="print the per-kernel table to stderr")
     ap.add_argument("--scan-sweep", action="store_true",
                     help="time the sequential against the chunked scan over batch sizes and exit")
+    ap.add_argument("--objective", choices=["mse", "kd"], default="mse",
+                    help="distillation workload: the two-MSE loss, or the paper's ranking objective "
+                         "(LambdaRank terms, teacher gate, EWC)")
     ap.add_argument("--f32-matmul", choices=["split", "native"], default="split",
                     help="fp32 models: projections on the bf16 matrix cores with split operands (fp32 "
                          "accuracy), or on the fp32 matrix cores")

@@ -206,6 +206,47 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* trainer, int32_t B, int32_t L, 
                                     const int32_t* d_lengths, const float* d_labels, float* d_loss,
                                     void* d_workspace, size_t ws_bytes, void* stream);
 
+/* The distillation objective of section 6, Eq. (9)-(10), for one batch j:
+ *   L = beta * R(s; y) + (1 - beta) * phi * R(s; t)
+ *       + ewc_lambda / 2 * sum_k F_k (theta_k - theta_prev_k)^2
+ * where s, t are the student's and the teacher's scores, y the labels and
+ * R(scores; labels) the LambdaRank loss of section 5.3, Eq. (6), taken over
+ * the pairs with rel_i > rel_j: |G_i - G_j| |1/D_i - 1/D_j|
+ * log2(1 + exp(-sigma (s_i - s_j))), rel = labels min-max normalised over
+ * the batch, G = (2^rel - 1) / maxDCG, D_i = log2(1 + rank of s_i), maxDCG
+ * the DCG of the ideal order. theta are the student's fp32 master weights. */
+typedef struct tcl_kd_loss {
+  float beta;                /* weight of R(s; y), in [0, 1] (0.5 in the paper)       */
+  float phi;                 /* teacher-loss gate of this batch, Eq. (10), in [0, 1] */
+  float sigma;               /* LambdaRank score scale, > 0 (1)                       */
+  float ewc_lambda;          /* EWC weight, >= 0 (1e4 in the paper); 0: no penalty    */
+  const float* d_fisher;     /* [n_params] diagonal Fisher information, canonical
+                                layout (device); may be NULL when ewc_lambda == 0     */
+  const float* d_theta_prev; /* [n_params] the student's parameters after the
+                                previous platform (device); likewise                  */
+} tcl_kd_loss;
+
+/* One distillation step on the Eq. (9) objective: as tcl_distill_step in
+ * every other respect (same workspace, same backward, Adam, re-derivation).
+ * d_loss [4] fp32 output: total, R(s; t), R(s; y), EWC penalty. The gradient
+ * blob (tcl_trainer_get_grads) includes the EWC gradient. */
+TCL_API tcl_status tcl_distill_step_kd(tcl_trainer* trainer, int32_t B, int32_t L, const float* d_feats,
+                                       const int32_t* d_lengths, const float* d_labels,
+                                       const tcl_kd_loss* kd, float* d_loss, void* d_workspace,
+                                       size_t ws_bytes, void* stream);
+
+/* The LambdaRank loss R(scores; labels) of Eq. (6) on one batch of B <= 65536
+ * items (defined above, under tcl_kd_loss), e.g. the teacher's batch losses
+ * e_T of Eq. (11) that the gate phi is computed from.
+ *   d_scores, d_labels [B] fp32 (device); d_loss [1] fp32 output; d_grad [B]
+ *   fp32 output dR/dscores (may be NULL); d_workspace >=
+ *   tcl_lambdarank_workspace_bytes(B) bytes, 16-byte aligned.
+ * O(B^2) work (ranks are counted pairwise); stream-ordered, deterministic. */
+TCL_API size_t tcl_lambdarank_workspace_bytes(int32_t B);
+TCL_API tcl_status tcl_lambdarank(int32_t B, const float* d_scores, const float* d_labels, float sigma,
+                                  float* d_loss, float* d_grad, void* d_workspace, size_t ws_bytes,
+                                  void* stream);
+
 /* Copy the gradient blob of the last step (canonical layout, fp32) to the
  * host. Synchronous. */
 TCL_API tcl_status tcl_trainer_get_grads(const tcl_trainer* trainer, float* h_out, size_t n_params);

@@ -36,6 +36,12 @@ class Config(ctypes.Structure):
                                    ("f32_matmul", ctypes.c_int32)]
 
 
+class KDLoss(ctypes.Structure):
+    """tcl_kd_loss: the Eq. (9) distillation objective."""
+    _fields_ = [("beta", ctypes.c_float), ("phi", ctypes.c_float), ("sigma", ctypes.c_float),
+                ("ewc_lambda", ctypes.c_float), ("d_fisher", ctypes.c_void_p), ("d_theta_prev", ctypes.c_void_p)]
+
+
 _vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
 _SIGS = {
     "tcl_param_count": (_sz, [ctypes.POINTER(Config)]),
@@ -57,6 +63,9 @@ _SIGS = {
     "tcl_distill_workspace_bytes": (_sz, [_vp, _i32, _i32]),
     "tcl_distill_step": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "tcl_trainer_get_grads": (_i32, [_vp, _vp, _sz]),
+    "tcl_distill_step_kd": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, ctypes.POINTER(KDLoss), _vp, _vp, _sz, _vp]),
+    "tcl_lambdarank_workspace_bytes": (_sz, [_i32]),
+    "tcl_lambdarank": (_i32, [_i32, _vp, _vp, ctypes.c_float, _vp, _vp, _vp, _sz, _vp]),
     "tcl_trainer_timing_enable": (_i32, [_vp, _i32]),
     "tcl_trainer_timing_count": (_i32, [_vp]),
     "tcl_trainer_timing_get": (_i32, [_vp, _i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
@@ -240,6 +249,22 @@ class Trainer:
                                      _stream(stream)))
         return loss
 
+    def step_kd(self, feats, lengths, labels, beta=0.5, phi=1.0, sigma=1.0, ewc_lambda=0.0, fisher=None,
+                theta_prev=None, loss=None, workspace=None, stream=None):
+        """One step on the Eq. (9) objective (tcl_distill_step_kd); fisher and
+        theta_prev are device fp32 tensors of the parameter count. Returns the
+        device tensor [total, rank(s; teacher), rank(s; label), ewc]."""
+        import torch
+        B, L, _ = feats.shape
+        if loss is None:
+            loss = torch.empty(4, dtype=torch.float32, device=feats.device)
+        ws = self.workspace(B, L) if workspace is None else workspace
+        kd = KDLoss(beta, phi, sigma, ewc_lambda, _ptr(fisher), _ptr(theta_prev))
+        check(lib().tcl_distill_step_kd(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), labels.data_ptr(),
+                                        ctypes.byref(kd), loss.data_ptr(), ws.data_ptr(),
+                                        ws.numel() * ws.element_size(), _stream(stream)))
+        return loss
+
     def grads(self) -> np.ndarray:
         out = np.empty(self._n, dtype=np.float32)
         check(lib().tcl_trainer_get_grads(self._h, out.ctypes.data, out.size))
@@ -271,6 +296,20 @@ def gemm_f32(A, W, bias=None, out=None, stream=None, tile=-1, epilogue=0):
     check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(), tile,
                                   epilogue, _stream(stream)))
     return out
+
+
+def lambdarank(scores, labels, sigma=1.0, grad=True, stream=None):
+    """The LambdaRank loss of Eq. (6) (tcl_lambdarank) on device fp32 [B]
+    tensors: returns (loss [1], grad [B] or None) as device tensors."""
+    import torch
+    B = scores.numel()
+    loss = torch.empty(1, dtype=torch.float32, device=scores.device)
+    g = torch.empty(B, dtype=torch.float32, device=scores.device) if grad else None
+    nbytes = lib().tcl_lambdarank_workspace_bytes(B)
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=scores.device)
+    check(lib().tcl_lambdarank(B, scores.data_ptr(), labels.data_ptr(), sigma, loss.data_ptr(), _ptr(g),
+                               ws.data_ptr(), ws.numel(), _stream(stream)))
+    return loss, g
 
 
 def gemm_split(A, W, bias=None, out=None, stream=None, variant=-1, epilogue=0, offs=None):

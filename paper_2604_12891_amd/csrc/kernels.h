@@ -233,10 +233,29 @@ hipError_t launch_rmsnorm_bwd(int d, int Mmax, const int* Mdev, const float* dN,
                               const float* rstd, const float* g, float* dH, float* dg_part,
                               hipStream_t s);
 int loss_head_blocks(int B);
-// part: [blocks][2h + 4] = dW2 (h) | db1 (h) | db2 | mse_t | mse_l | total
+// part: [blocks][2h + 4] = dW2 (h) | db1 (h) | db2 | mse_t | mse_l | total.
+// With ds_in (dL/ds [B]) and loss_in ({total, term_t, term_y}) the score
+// gradient and the loss come from elsewhere (the ranking objective) and the
+// MSE terms are not used.
 hipError_t launch_loss_head_bwd(int B, int d, int h, const float* s, const float* t, const float* y,
                                 const float* a1, const float* W1, const float* W2, float* da1,
-                                float* dpooled, float* part, hipStream_t st);
+                                float* dpooled, float* part, hipStream_t st, const float* ds_in = nullptr,
+                                const float* loss_in = nullptr);
+
+// ---------------------------------------------------------------- ranking objectives
+// LambdaRank (Eq. (6)) of scores s [B] against label set l0 (nsets == 1) or
+// against l0 and l1 weighted w0, w1 (nsets == 2). ds [B] (may be null)
+// receives d/ds of (w0 L(s; l0) + w1 L(s; l1)) (nsets == 1: of L(s; l0));
+// out receives {L} (nsets == 1) or {w0 L0 + w1 L1, L1, L0}. ws: a scratch
+// of rank_workspace_floats(B, nsets) floats.
+size_t rank_workspace_floats(int B, int nsets);
+hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, const float* l1, float sigma,
+                             float w0, float w1, float* ws, float* ds, float* out, hipStream_t st);
+// EWC penalty (Eq. (9)): grad += lam F (theta - prev); loss[3] =
+// lam/2 sum F (theta - prev)^2 and loss[0] += loss[3]. part: ewc_part_floats().
+int ewc_part_floats();
+hipError_t launch_ewc(int64_t n, const float* theta, const float* prev, const float* fisher, float lam,
+                      float* grad, float* part, float* loss, hipStream_t st);
 // dg_part: [B][d]
 hipError_t launch_normf_pool_bwd(int B, int d, const int* offs, const float* H, const float* g_f,
                                  int final_norm, float eps, const float* dpooled, float* dH,

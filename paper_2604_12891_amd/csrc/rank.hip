@@ -1,0 +1,313 @@
+// The ranking objectives: LambdaRank (section 5.3, Eq. (6)) on a batch of
+// scores against one or two label sets, and the EWC penalty of the
+// distillation objective (section 6, Eq. (9)).
+//
+// LambdaRank, per label set:
+//   L = sum over pairs with rel_i > rel_j of
+//       |G_i - G_j| |1/D_i - 1/D_j| log2(1 + exp(-sigma (s_i - s_j)))
+//   rel = labels min-max normalised over the batch, G = (2^rel - 1) / maxDCG,
+//   D_i = log2(1 + r_i) with r_i the 1-based rank of s_i (descending, equal
+//   scores in index order), maxDCG = the DCG of the ordering by rel.
+// The ranks are counted, not sorted: item i's rank is one plus the number of
+// items ahead of it, an O(B^2) pass that is cheap at tuning-round sizes and
+// needs no sort. Three launches:
+//   prep:   per item its score rank, and per set its relevance, gain
+//           2^rel - 1 and ideal-DCG term (gain over log2(1 + ideal rank));
+//   pairs:  a grid of (256 items i) x (256 items j) tiles; each thread
+//           accumulates its item's loss and gradient over one j tile;
+//   finish: sums the j-tile partials in a fixed order (deterministic).
+// All fp32; maxDCG is summed identically by every block.
+#include "common.h"
+#include "kernels.h"
+
+namespace tcl {
+namespace {
+
+constexpr int kRT = 256;    // threads per block = items per i block = items per j tile
+constexpr float kInvLn2 = 1.4426950408889634f;
+
+// Sum over the block; every thread receives the total. The order of the
+// additions depends only on the block size, so every block agrees.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < kRT / 64; ++i) t += red[i];
+  return t;
+}
+
+__device__ __forceinline__ float block_min(float v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fminf(v, __shfl_xor(v, o, 64));
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = red[0];
+#pragma unroll
+  for (int i = 1; i < kRT / 64; ++i) t = fminf(t, red[i]);
+  return t;
+}
+
+__device__ __forceinline__ float block_max(float v, float* red) { return -block_min(-v, red); }
+
+// relevance of a label given the set's min and max (all zero when equal)
+__device__ __forceinline__ float rel_of(float y, float lo, float inv_range) { return (y - lo) * inv_range; }
+
+template <int NS>
+__global__ __launch_bounds__(kRT) void rank_prep_kernel(int B, const float* __restrict__ s,
+                                                        const float* __restrict__ l0,
+                                                        const float* __restrict__ l1,
+                                                        float* __restrict__ rel, float* __restrict__ gain,
+                                                        float* __restrict__ dcg, float* __restrict__ invD) {
+  __shared__ float red[kRT / 64];
+  __shared__ float ts[kRT], tr[NS][kRT];
+  const float* lab[2] = {l0, l1};
+  // every block computes each set's min and max over the whole batch
+  float lo[NS], ir[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    float mn = INFINITY, mx = -INFINITY;
+    for (int j = threadIdx.x; j < B; j += kRT) {
+      mn = fminf(mn, lab[k][j]);
+      mx = fmaxf(mx, lab[k][j]);
+    }
+    lo[k] = block_min(mn, red);
+    const float hi = block_max(mx, red);
+    ir[k] = hi > lo[k] ? 1.0f / (hi - lo[k]) : 0.0f;
+  }
+  const int i = blockIdx.x * kRT + threadIdx.x;
+  const bool ok = i < B;
+  const float si = ok ? s[i] : 0.f;
+  float ri[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) ri[k] = ok ? rel_of(lab[k][i], lo[k], ir[k]) : 0.f;
+  int ahead = 0, iahead[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) iahead[k] = 0;
+  for (int j0 = 0; j0 < B; j0 += kRT) {
+    __syncthreads();
+    const int j = j0 + threadIdx.x;
+    ts[threadIdx.x] = j < B ? s[j] : 0.f;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) tr[k][threadIdx.x] = j < B ? rel_of(lab[k][j], lo[k], ir[k]) : 0.f;
+    __syncthreads();
+    const int n = min(kRT, B - j0);
+    for (int jj = 0; jj < n; ++jj) {
+      const int jg = j0 + jj;
+      const float sj = ts[jj];
+      ahead += (sj > si || (sj == si && jg < i)) ? 1 : 0;
+#pragma unroll
+      for (int k = 0; k < NS; ++k) {
+        const float rj = tr[k][jj];
+        iahead[k] += (rj > ri[k] || (rj == ri[k] && jg < i)) ? 1 : 0;
+      }
+    }
+  }
+  if (!ok) return;
+  invD[i] = 1.0f / __builtin_amdgcn_logf(2.0f + (float)ahead);  // rank = ahead + 1, D = log2(1 + rank)
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    const float g = __builtin_amdgcn_exp2f(ri[k]) - 1.0f;
+    rel[k * B + i] = ri[k];
+    gain[k * B + i] = g;
+    dcg[k * B + i] = g / __builtin_amdgcn_logf(2.0f + (float)iahead[k]);
+  }
+}
+
+// grid (i blocks, j tiles); part_ds [tiles][B], part_loss [tiles][i blocks][NS]
+template <int NS>
+__global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, float w0, float w1,
+                                                        const float* __restrict__ s,
+                                                        const float* __restrict__ rel,
+                                                        const float* __restrict__ gain,
+                                                        const float* __restrict__ dcg,
+                                                        const float* __restrict__ invD,
+                                                        float* __restrict__ part_ds,
+                                                        float* __restrict__ part_loss) {
+  __shared__ float red[kRT / 64];
+  __shared__ float ts[kRT], tD[kRT], tr[NS][kRT], tg[NS][kRT];
+  float imax[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    float acc = 0.f;
+    for (int j = threadIdx.x; j < B; j += kRT) acc += dcg[k * B + j];
+    const float mx = block_sum(acc, red);
+    imax[k] = mx > 0.f ? 1.0f / mx : 0.f;
+  }
+  const int j0 = blockIdx.y * kRT;
+  {
+    const int j = j0 + threadIdx.x;
+    const bool jok = j < B;
+    ts[threadIdx.x] = jok ? s[j] : 0.f;
+    tD[threadIdx.x] = jok ? invD[j] : 0.f;
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      tr[k][threadIdx.x] = jok ? rel[k * B + j] : 0.f;
+      tg[k][threadIdx.x] = jok ? gain[k * B + j] : 0.f;
+    }
+  }
+  __syncthreads();
+  const int i = blockIdx.x * kRT + threadIdx.x;
+  const bool ok = i < B;
+  const float si = ok ? s[i] : 0.f, Di = ok ? invD[i] : 0.f;
+  float ri[NS], gi[NS], loss[NS], grad[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    ri[k] = ok ? rel[k * B + i] : 0.f;
+    gi[k] = ok ? gain[k * B + i] : 0.f;
+    loss[k] = 0.f;
+    grad[k] = 0.f;
+  }
+  const int n = ok ? min(kRT, B - j0) : 0;
+  for (int jj = 0; jj < n; ++jj) {
+    const float x = sigma * (si - ts[jj]);
+    const float dD = fabsf(Di - tD[jj]);
+    // e = exp(-|x|): sigmoid(-x) and softplus(-x) = log(1 + e^-x) from it
+    const float e = exp_fast(-fabsf(x));
+    const float r1 = rcp_fast(1.0f + e);
+    const float sig_neg = x >= 0.f ? e * r1 : r1;   // 1 / (1 + e^x)
+    const float sig_pos = x >= 0.f ? r1 : e * r1;   // 1 / (1 + e^-x)
+    const float lp = log1p_unit(e);
+    const float sp_neg = fmaxf(-x, 0.f) + lp;      // log(1 + e^-x)
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      const float rj = tr[k][jj];
+      const float w = fabsf(gi[k] - tg[k][jj]) * imax[k] * dD;
+      if (ri[k] > rj) {
+        loss[k] = fmaf(w, sp_neg, loss[k]);
+        grad[k] = fmaf(-w, sig_neg, grad[k]);
+      } else if (rj > ri[k]) {
+        grad[k] = fmaf(w, sig_pos, grad[k]);
+      }
+    }
+  }
+  // loss in bits (log2), gradient scaled by sigma / ln 2
+  const float c = sigma * kInvLn2;
+  if (ok) part_ds[(int64_t)blockIdx.y * B + i] = w0 * grad[0] * c + (NS > 1 ? w1 * grad[NS - 1] * c : 0.f);
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    const float t = block_sum(loss[k] * kInvLn2, red);
+    if (threadIdx.x == 0) part_loss[((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * NS + k] = t;
+  }
+}
+
+// ds[i] = sum over j tiles; out: NS == 1: {L}; NS == 2: {w0 L0 + w1 L1, L1, L0}
+template <int NS>
+__global__ __launch_bounds__(kRT) void rank_finish_kernel(int B, int tiles, int iblocks, float w0, float w1,
+                                                          const float* __restrict__ part_ds,
+                                                          const float* __restrict__ part_loss,
+                                                          float* __restrict__ ds, float* __restrict__ out) {
+  const int i = blockIdx.x * kRT + threadIdx.x;
+  if (i < B && ds) {
+    float acc = 0.f;
+    for (int t = 0; t < tiles; ++t) acc += part_ds[(int64_t)t * B + i];
+    ds[i] = acc;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    float L[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) L[k] = 0.f;
+    for (int p = 0; p < tiles * iblocks; ++p)
+#pragma unroll
+      for (int k = 0; k < NS; ++k) L[k] += part_loss[(int64_t)p * NS + k];
+    if (NS == 1) {
+      out[0] = L[0];
+    } else {
+      out[0] = w0 * L[0] + w1 * L[NS - 1];
+      out[1] = L[NS - 1];
+      out[2] = L[0];
+    }
+  }
+}
+
+// EWC: grad += lambda F (theta - theta_prev); part[block] = this block's
+// share of lambda/2 sum F (theta - theta_prev)^2
+constexpr int kEwcBlocks = 256;
+__global__ __launch_bounds__(kRT) void ewc_kernel(int64_t n, const float* __restrict__ theta,
+                                                  const float* __restrict__ prev,
+                                                  const float* __restrict__ fisher, float lam,
+                                                  float* __restrict__ grad, float* __restrict__ part) {
+  __shared__ float red[kRT / 64];
+  float acc = 0.f;
+  for (int64_t k = (int64_t)blockIdx.x * kRT + threadIdx.x; k < n; k += (int64_t)kEwcBlocks * kRT) {
+    const float d = theta[k] - prev[k];
+    const float fd = fisher[k] * d;
+    grad[k] = fmaf(lam, fd, grad[k]);
+    acc = fmaf(fd, d, acc);
+  }
+  const float t = block_sum(acc, red);
+  if (threadIdx.x == 0) part[blockIdx.x] = 0.5f * lam * t;
+}
+
+// loss[3] = the penalty, loss[0] += it
+__global__ __launch_bounds__(64) void ewc_finish_kernel(const float* __restrict__ part, float* __restrict__ loss) {
+  float acc = 0.f;
+  for (int b = threadIdx.x; b < kEwcBlocks; b += 64) acc += part[b];
+  acc = wave_sum(acc);
+  if (threadIdx.x == 0) {
+    loss[3] = acc;
+    loss[0] += acc;
+  }
+}
+
+__global__ void ewc_off_kernel(float* __restrict__ loss) {
+  if (threadIdx.x == 0) loss[3] = 0.f;
+}
+
+}  // namespace
+
+size_t rank_workspace_floats(int B, int nsets) {
+  const size_t tiles = (size_t)(B + kRT - 1) / kRT;
+  // rel, gain, dcg per set; invD; ds; part_ds [tiles][B]; part_loss [tiles][tiles][nsets]
+  return (size_t)3 * nsets * B + B + B + tiles * B + tiles * tiles * nsets;
+}
+
+hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, const float* l1, float sigma,
+                             float w0, float w1, float* ws, float* ds, float* out, hipStream_t st) {
+  if (B <= 0 || (nsets != 1 && nsets != 2) || (nsets == 2 && !l1)) return hipErrorInvalidValue;
+  const int tiles = (B + kRT - 1) / kRT;
+  float* rel = ws;
+  float* gain = rel + (size_t)nsets * B;
+  float* dcg = gain + (size_t)nsets * B;
+  float* invD = dcg + (size_t)nsets * B;
+  float* dsw = invD + B;
+  float* part_ds = dsw + B;
+  float* part_loss = part_ds + (size_t)tiles * B;
+  float* dsout = ds ? ds : dsw;
+  if (nsets == 1) {
+    hipLaunchKernelGGL(rank_prep_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, s, l0, l0, rel, gain, dcg, invD);
+    hipLaunchKernelGGL(rank_pair_kernel<1>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, s, rel, gain,
+                       dcg, invD, part_ds, part_loss);
+    hipLaunchKernelGGL(rank_finish_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, part_ds,
+                       part_loss, dsout, out);
+  } else {
+    hipLaunchKernelGGL(rank_prep_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, s, l0, l1, rel, gain, dcg, invD);
+    hipLaunchKernelGGL(rank_pair_kernel<2>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, s, rel, gain,
+                       dcg, invD, part_ds, part_loss);
+    hipLaunchKernelGGL(rank_finish_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, part_ds,
+                       part_loss, dsout, out);
+  }
+  return hipGetLastError();
+}
+
+int ewc_part_floats() { return kEwcBlocks; }
+
+hipError_t launch_ewc(int64_t n, const float* theta, const float* prev, const float* fisher, float lam,
+                      float* grad, float* part, float* loss, hipStream_t st) {
+  if (n <= 0) return hipErrorInvalidValue;
+  if (lam == 0.f) {  // no penalty: its loss slot reads zero
+    hipLaunchKernelGGL(ewc_off_kernel, dim3(1), dim3(64), 0, st, loss);
+    return hipGetLastError();
+  }
+  if (!theta || !prev || !fisher) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ewc_kernel, dim3(kEwcBlocks), dim3(kRT), 0, st, n, theta, prev, fisher, lam, grad, part);
+  hipLaunchKernelGGL(ewc_finish_kernel, dim3(1), dim3(64), 0, st, part, loss);
+  return hipGetLastError();
+}
+
+}  // namespace tcl

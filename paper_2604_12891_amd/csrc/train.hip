@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void loss_head_bwd_kernel(
     int B, int d, int h, const float* __restrict__ s, const float* __restrict__ t,
     const float* __restrict__ y, const float* __restrict__ a1, const float* __restrict__ W1,
     const float* __restrict__ W2, float* __restrict__ da1, float* __restrict__ dpooled,
-    float* __restrict__ part) {
+    float* __restrict__ part, const float* __restrict__ ds_in, const float* __restrict__ loss_in) {
   __shared__ float sda[kHB][256];
   __shared__ float sds[kHB];
   const int tid = threadIdx.x;
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(256) void loss_head_bwd_kernel(
   const float inv = 2.0f / (float)B;
   if (tid < kHB) {
     const int b = b0 + tid;
-    sds[tid] = b < B ? inv * (2.0f * s[b] - t[b] - y[b]) : 0.f;
+    sds[tid] = b >= B ? 0.f : ds_in ? ds_in[b] : inv * (2.0f * s[b] - t[b] - y[b]);
   }
   __syncthreads();
   float pw2 = 0.f, pb1 = 0.f;
@@ -160,9 +160,18 @@ __global__ __launch_bounds__(256) void loss_head_bwd_kernel(
     }
     const float invB = 1.0f / (float)B;
     out[2 * h] = db2;
-    out[2 * h + 1] = lt * invB;
-    out[2 * h + 2] = ly * invB;
-    out[2 * h + 3] = (lt + ly) * invB;
+    if (ds_in) {
+      // the loss was computed with the gradient: block 0 carries it, the
+      // others add zero, so the reduction reproduces it exactly
+      const bool first = blockIdx.x == 0;
+      out[2 * h + 1] = first ? loss_in[1] : 0.f;
+      out[2 * h + 2] = first ? loss_in[2] : 0.f;
+      out[2 * h + 3] = first ? loss_in[0] : 0.f;
+    } else {
+      out[2 * h + 1] = lt * invB;
+      out[2 * h + 2] = ly * invB;
+      out[2 * h + 3] = (lt + ly) * invB;
+    }
   }
 }
 
@@ -655,10 +664,11 @@ int loss_head_blocks(int B) { return (B + kHB - 1) / kHB; }
 
 hipError_t launch_loss_head_bwd(int B, int d, int h, const float* s, const float* t, const float* y,
                                 const float* a1, const float* W1, const float* W2, float* da1,
-                                float* dpooled, float* part, hipStream_t st) {
-  if (h > 256 || d > 256) return hipErrorInvalidValue;
+                                float* dpooled, float* part, hipStream_t st, const float* ds_in,
+                                const float* loss_in) {
+  if (h > 256 || d > 256 || (ds_in != nullptr) != (loss_in != nullptr)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(loss_head_bwd_kernel, dim3(loss_head_blocks(B)), dim3(256), 0, st, B, d, h, s, t, y,
-                     a1, W1, W2, da1, dpooled, part);
+                     a1, W1, W2, da1, dpooled, part, ds_in, loss_in);
   return hipGetLastError();
 }
 

@@ -48,6 +48,7 @@ struct TrainPlan {
   size_t H_last = 0, pooled = 0, a1 = 0;
   size_t dH = 0, dyg = 0, dxz = 0, du = 0, dv = 0, dxdbl = 0, dN = 0, ckpt = 0, da1 = 0, dpooled = 0;
   size_t p_lh = 0, p_W1 = 0, p_gf = 0, p_W0 = 0, p_b0 = 0;
+  size_t rank_ws = 0, ds = 0, rloss = 0, ewc_part = 0;  // ranking objective (tcl_distill_step_kd)
   int s_W1 = 0, s_W0 = 0, cs = 0, lh_blocks = 0, rn_blocks = 0;
   size_t total = 0;
 };
@@ -116,6 +117,10 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
   P.s_W0 = gemm_tn_splits(Mmax, d, F);
   P.p_W0 = take((size_t)P.s_W0 * d * F * 4);
   P.p_b0 = take((size_t)P.cs * d * 4);
+  P.rank_ws = take(rank_workspace_floats(B, 2) * 4);
+  P.ds = take((size_t)B * 4);
+  P.rloss = take(4 * 4);
+  P.ewc_part = take((size_t)ewc_part_floats() * 4);
   P.total = o;
   return P;
 }
@@ -257,9 +262,13 @@ TCL_API tcl_status tcl_trainer_get_grads(const tcl_trainer* tr, float* h_out, si
   return TCL_OK;
 }
 
-TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats,
-                                    const int32_t* d_lengths, const float* d_labels, float* d_loss,
-                                    void* d_ws, size_t ws_bytes, void* stream) {
+namespace {
+
+// One step on either objective: kd == NULL is the two-MSE loss, else the
+// ranking objective of Eq. (9).
+tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats, const int32_t* d_lengths,
+                        const float* d_labels, const tcl_kd_loss* kd, float* d_loss, void* d_ws,
+                        size_t ws_bytes, void* stream) {
   if (!tr) return fail(TCL_ERR_INVALID_ARG, "trainer is NULL");
   if (B <= 0 || L <= 0 || B > tr->max_B || L > tr->max_L)
     return fail(TCL_ERR_INVALID_ARG, "B=%d L=%d outside [1, max_B=%d] x [1, max_L=%d]", B, L,
@@ -328,9 +337,16 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
                                         F32(P.pooled), F32(P.a1)));
 
   // 3. loss, head, pool and final norm
+  if (kd) {
+    // beta L(s; labels) + (1 - beta) phi L(s; teacher): dL/ds and the loss
+    TCL_LAUNCH(T, "lambdarank", launch_lambdarank(B, 2, F32(P.s_scores), d_labels, F32(P.t_scores), kd->sigma,
+                                                  kd->beta, (1.0f - kd->beta) * kd->phi, F32(P.rank_ws),
+                                                  F32(P.ds), F32(P.rloss), s));
+  }
   TCL_LAUNCH(T, "loss_head_bwd", launch_loss_head_bwd(B, d, h, F32(P.s_scores), F32(P.t_scores), d_labels,
                                                       F32(P.a1), S->W1, S->W2, F32(P.da1),
-                                                      F32(P.dpooled), F32(P.p_lh), s));
+                                                      F32(P.dpooled), F32(P.p_lh), s,
+                                                      kd ? F32(P.ds) : nullptr, kd ? F32(P.rloss) : nullptr));
   {
     GemmTNArgs a;
     a.A = F32(P.da1); a.lda = h; a.Bm = F32(P.pooled); a.ldb = d; a.P = F32(P.p_W1);
@@ -414,12 +430,52 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
   // 5. reduce partials, Adam, refresh the compute layouts
   TCL_LAUNCH(T, "reduce", launch_reduce(tr->d_jobs, tr->njobs, tr->max_n, reinterpret_cast<float*>(ws),
                                         tr->grad, d_loss, s));
+  if (kd)  // EWC on the master weights: gradient and loss[3] (zero when lambda = 0)
+    TCL_LAUNCH(T, "ewc", launch_ewc((int64_t)S->n_params, S->master, kd->d_theta_prev, kd->d_fisher,
+                                    kd->ewc_lambda, tr->grad, F32(P.ewc_part), d_loss, s));
   tr->step += 1;
   const float bc1 = 1.0f - (float)std::pow((double)tr->beta1, (double)tr->step);
   const float bc2 = 1.0f - (float)std::pow((double)tr->beta2, (double)tr->step);
   TCL_LAUNCH(T, "adam", launch_adam((int64_t)S->n_params, S->master, tr->m, tr->v, tr->grad, tr->lr,
                                     tr->beta1, tr->beta2, tr->eps, bc1, bc2, s));
   TCL_LAUNCH(T, "derive", launch_derive(S->master, S->jobs, S->njobs, S->derive_total, S->dev, 1, s));
+  return TCL_OK;
+}
+
+}  // namespace
+
+TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats,
+                                    const int32_t* d_lengths, const float* d_labels, float* d_loss,
+                                    void* d_ws, size_t ws_bytes, void* stream) {
+  return distill_step(tr, B, L, d_feats, d_lengths, d_labels, nullptr, d_loss, d_ws, ws_bytes, stream);
+}
+
+TCL_API tcl_status tcl_distill_step_kd(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats,
+                                       const int32_t* d_lengths, const float* d_labels, const tcl_kd_loss* kd,
+                                       float* d_loss, void* d_ws, size_t ws_bytes, void* stream) {
+  if (!kd) return fail(TCL_ERR_INVALID_ARG, "kd is NULL");
+  if (!(kd->beta >= 0.f && kd->beta <= 1.f) || !(kd->phi >= 0.f && kd->phi <= 1.f) || !(kd->sigma > 0.f) ||
+      !(kd->ewc_lambda >= 0.f))
+    return fail(TCL_ERR_INVALID_ARG, "kd needs beta, phi in [0, 1], sigma > 0, ewc_lambda >= 0");
+  if (kd->ewc_lambda > 0.f && (!kd->d_fisher || !kd->d_theta_prev))
+    return fail(TCL_ERR_INVALID_ARG, "the EWC penalty needs d_fisher and d_theta_prev");
+  return distill_step(tr, B, L, d_feats, d_lengths, d_labels, kd, d_loss, d_ws, ws_bytes, stream);
+}
+
+TCL_API size_t tcl_lambdarank_workspace_bytes(int32_t B) {
+  return B > 0 ? rank_workspace_floats(B, 1) * 4 : 0;
+}
+
+TCL_API tcl_status tcl_lambdarank(int32_t B, const float* d_scores, const float* d_labels, float sigma,
+                                  float* d_loss, float* d_grad, void* d_ws, size_t ws_bytes, void* stream) {
+  if (B <= 0 || B > (1 << 16)) return fail(TCL_ERR_INVALID_ARG, "B=%d outside [1, 65536]", B);
+  if (!(sigma > 0.f)) return fail(TCL_ERR_INVALID_ARG, "sigma must be positive");
+  if (!d_scores || !d_labels || !d_loss || !d_ws) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_ws) % 16) return fail(TCL_ERR_INVALID_ARG, "d_workspace must be 16-byte aligned");
+  if (ws_bytes < rank_workspace_floats(B, 1) * 4)
+    return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, rank_workspace_floats(B, 1) * 4);
+  TCL_HIP(launch_lambdarank(B, 1, d_scores, d_labels, nullptr, sigma, 1.0f, 0.0f, static_cast<float*>(d_ws),
+                            d_grad, d_loss, static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }
 
