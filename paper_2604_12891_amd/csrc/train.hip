@@ -543,30 +543,47 @@ __global__ __launch_bounds__(256) void colsum_kernel(const int* __restrict__ Mde
 }
 
 // ---------------------------------------------------------------- reductions
-// blockIdx.y picks the job. A block takes 64 consecutive outputs; its four
-// wavefronts each sum a contiguous quarter of the splits, then the quarters
-// are added in order (deterministic for a given split count).
-__global__ __launch_bounds__(256) void reduce_kernel(const ReduceJob* __restrict__ jobs, int njobs,
-                                                     const float* __restrict__ ws,
-                                                     float* __restrict__ grad,
-                                                     float* __restrict__ loss) {
-  __shared__ float sq[4][64];
+// blockIdx.y picks the job. A block takes 64 consecutive outputs; its 16
+// wavefronts each sum a contiguous sixteenth of the splits with four
+// independent partial sums (four loads in flight per lane), then the partial
+// sums and the sixteenths are added in a fixed order (deterministic for a
+// given split count).
+constexpr int kRedGroups = 16;
+__global__ __launch_bounds__(64 * kRedGroups) void reduce_kernel(const ReduceJob* __restrict__ jobs, int njobs,
+                                                                const float* __restrict__ ws,
+                                                                float* __restrict__ grad,
+                                                                float* __restrict__ loss) {
+  __shared__ float sq[kRedGroups][64];
   const int j = blockIdx.y;
   if (j >= njobs) return;
   const ReduceJob J = jobs[j];
   float* dst = (J.dst_buf == 0 ? grad : loss) + J.dst;
   const float* src = ws + J.src;
   const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int per = (J.nsplit + 3) / 4;
+  const int per = (J.nsplit + kRedGroups - 1) / kRedGroups;
   const int s0 = q * per, s1 = min(s0 + per, J.nsplit);
   for (int64_t i0 = (int64_t)blockIdx.x * 64; i0 < J.n; i0 += (int64_t)gridDim.x * 64) {
     const int64_t i = i0 + lane;
-    float acc = 0.f;
-    if (i < J.n)
-      for (int s = s0; s < s1; ++s) acc += src[(int64_t)s * J.split_stride + i * J.src_stride];
-    sq[q][lane] = acc;
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    if (i < J.n) {
+      const float* p = src + i * J.src_stride;
+      int s = s0;
+      for (; s + 3 < s1; s += 4) {
+        a0 += p[(int64_t)s * J.split_stride];
+        a1 += p[(int64_t)(s + 1) * J.split_stride];
+        a2 += p[(int64_t)(s + 2) * J.split_stride];
+        a3 += p[(int64_t)(s + 3) * J.split_stride];
+      }
+      for (; s < s1; ++s) a0 += p[(int64_t)s * J.split_stride];
+    }
+    sq[q][lane] = (a0 + a1) + (a2 + a3);
     __syncthreads();
-    if (q == 0 && i < J.n) dst[i * J.dst_stride] = ((sq[0][lane] + sq[1][lane]) + sq[2][lane]) + sq[3][lane];
+    if (q == 0 && i < J.n) {
+      float t = 0.f;
+#pragma unroll
+      for (int g = 0; g < kRedGroups; ++g) t += sq[g][lane];
+      dst[i * J.dst_stride] = t;
+    }
     __syncthreads();
   }
 }
@@ -738,7 +755,7 @@ hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, cons
                          float* grad, float* loss, hipStream_t s) {
   if (njobs <= 0) return hipSuccess;
   const int gx = (int)std::min<int64_t>((max_n + 63) / 64, 512);
-  hipLaunchKernelGGL(reduce_kernel, dim3(gx, njobs), dim3(256), 0, s, d_jobs, njobs, ws, grad, loss);
+  hipLaunchKernelGGL(reduce_kernel, dim3(gx, njobs), dim3(64 * kRedGroups), 0, s, d_jobs, njobs, ws, grad, loss);
   return hipGetLastError();
 }
 
