@@ -247,6 +247,49 @@ TCL_API tcl_status tcl_lambdarank(int32_t B, const float* d_scores, const float*
                                   float* d_loss, float* d_grad, void* d_workspace, size_t ws_bytes,
                                   void* stream);
 
+/* ---------------------------------------------------------------------
+ * What consumes the scores.
+ * ------------------------------------------------------------------- */
+
+/* Top-K per segment (section 3, Fig. 2: the cost model keeps the K best
+ * candidates of a tuning round for measurement). Segment g holds the scores
+ * d_scores[d_seg_offsets[g] .. d_seg_offsets[g+1]-1] (one task's candidates;
+ * offsets nondecreasing). d_out [n_seg * K] int32 receives, per segment, the
+ * global indices of its K highest scores, highest first; equal scores in
+ * index order; NaN scores (unscored programs) after every number; -1 past
+ * the end of a segment with fewer than K candidates. K in [1, 1024].
+ * Stream-ordered; no workspace. */
+TCL_API tcl_status tcl_topk(int32_t n_seg, const int32_t* d_seg_offsets, const float* d_scores, int32_t K,
+                            int32_t* d_out, void* stream);
+
+/* The RDU sampler's selection of programs to label, one step of section 4's
+ * Alg. 1 on a pool of N scored programs:
+ *   f = the predictions d_scores min-max normalised over the pool;
+ *   budget[op] = n_select * (pool items of type op) / N;
+ *   repeat until n_select programs are selected or no candidate is left:
+ *     for each candidate x_i (not labeled), with M labeled programs x_j:
+ *       d_s = min_j |f_i - f_j|                              (Eq. (1))
+ *       u_s = variance of {f_i} and every f_j, i.e. Eq. (2)-(3)
+ *       t_s = f_i * d_s + u_s
+ *     T = argmax t_s (equal t_s: the lower index); T is labeled if its
+ *     operator type is under budget, else dropped from the candidates.
+ *   d_op [N] int32 operator type of each program in [0, n_ops) (programs of
+ *   another type are never selected); n_ops in [1, 4096];
+ *   d_initial [n_initial >= 1] the initial (random) labeled programs,
+ *   distinct indices in [0, N) (entries outside are ignored); they count
+ *   toward neither n_select nor the budgets;
+ *   d_selected [n_select] int32 output, in selection order, -1 past the end;
+ *   d_count [1] int32 output, the number selected;
+ *   d_workspace >= tcl_rdu_workspace_bytes(N, n_ops) bytes, 256-byte aligned.
+ * Scores must be finite (a NaN-scored program is never selected, and must
+ * not be in d_initial). fp64 arithmetic on the device; the host enqueues two
+ * kernels per selection and never waits. */
+TCL_API size_t tcl_rdu_workspace_bytes(int32_t N, int32_t n_ops);
+TCL_API tcl_status tcl_rdu_select(int32_t N, const float* d_scores, const int32_t* d_op, int32_t n_ops,
+                                  const int32_t* d_initial, int32_t n_initial, int32_t n_select,
+                                  int32_t* d_selected, int32_t* d_count, void* d_workspace, size_t ws_bytes,
+                                  void* stream);
+
 /* Copy the gradient blob of the last step (canonical layout, fp32) to the
  * host. Synchronous. */
 TCL_API tcl_status tcl_trainer_get_grads(const tcl_trainer* trainer, float* h_out, size_t n_params);

@@ -65,6 +65,9 @@ _SIGS = {
     "tcl_trainer_get_grads": (_i32, [_vp, _vp, _sz]),
     "tcl_distill_step_kd": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, ctypes.POINTER(KDLoss), _vp, _vp, _sz, _vp]),
     "tcl_lambdarank_workspace_bytes": (_sz, [_i32]),
+    "tcl_topk": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp]),
+    "tcl_rdu_workspace_bytes": (_sz, [_i32, _i32]),
+    "tcl_rdu_select": (_i32, [_i32, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "tcl_lambdarank": (_i32, [_i32, _vp, _vp, ctypes.c_float, _vp, _vp, _vp, _sz, _vp]),
     "tcl_trainer_timing_enable": (_i32, [_vp, _i32]),
     "tcl_trainer_timing_count": (_i32, [_vp]),
@@ -296,6 +299,33 @@ def gemm_f32(A, W, bias=None, out=None, stream=None, tile=-1, epilogue=0):
     check(lib().tcl_test_gemm_f32(M, N, K, A.data_ptr(), W.data_ptr(), _ptr(bias), out.data_ptr(), tile,
                                   epilogue, _stream(stream)))
     return out
+
+
+def topk(scores, seg_offsets, K, stream=None):
+    """Per-segment top-K (tcl_topk): scores fp32 [n], seg_offsets int32
+    [n_seg + 1] (device); returns int32 [n_seg, K] global indices."""
+    import torch
+    n_seg = seg_offsets.numel() - 1
+    out = torch.empty(n_seg, K, dtype=torch.int32, device=scores.device)
+    check(lib().tcl_topk(n_seg, seg_offsets.data_ptr(), scores.data_ptr(), K, out.data_ptr(), _stream(stream)))
+    return out
+
+
+def rdu_select(scores, op, n_ops, initial, n_select, workspace=None, stream=None):
+    """RDU selection (tcl_rdu_select): scores fp32 [N], op int32 [N], initial
+    int32 [M0] (device). Returns (selected int32 [n_select], count int32 [1])."""
+    import torch
+    N = scores.numel()
+    sel = torch.empty(max(n_select, 1), dtype=torch.int32, device=scores.device)
+    cnt = torch.empty(1, dtype=torch.int32, device=scores.device)
+    need = lib().tcl_rdu_workspace_bytes(N, n_ops)
+    ws = workspace
+    if ws is None or ws.numel() * ws.element_size() < need:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=scores.device)
+    check(lib().tcl_rdu_select(N, scores.data_ptr(), op.data_ptr(), n_ops, initial.data_ptr(), initial.numel(),
+                               n_select, sel.data_ptr(), cnt.data_ptr(), ws.data_ptr(),
+                               ws.numel() * ws.element_size(), _stream(stream)))
+    return sel[:n_select], cnt
 
 
 def lambdarank(scores, labels, sigma=1.0, grad=True, stream=None):

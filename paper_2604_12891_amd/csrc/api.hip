@@ -533,6 +533,39 @@ TCL_API tcl_status tcl_timing_reset(tcl_model* m) {
   return TCL_OK;
 }
 
+// ------------------------------------------------------------------ score consumers
+
+TCL_API tcl_status tcl_topk(int32_t n_seg, const int32_t* d_seg_offsets, const float* d_scores, int32_t K,
+                            int32_t* d_out, void* stream) {
+  if (n_seg <= 0) return fail(TCL_ERR_INVALID_ARG, "n_seg must be positive");
+  if (K < 1 || K > 1024) return fail(TCL_ERR_UNSUPPORTED, "K must be in [1, 1024] (got %d)", K);
+  if (!d_seg_offsets || !d_scores || !d_out) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  TCL_HIP(launch_topk(n_seg, d_seg_offsets, d_scores, K, d_out, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
+TCL_API size_t tcl_rdu_workspace_bytes(int32_t N, int32_t n_ops) {
+  if (N <= 0 || n_ops <= 0 || n_ops > 4096) return 0;
+  return rdu_workspace_bytes(N, n_ops);
+}
+
+TCL_API tcl_status tcl_rdu_select(int32_t N, const float* d_scores, const int32_t* d_op, int32_t n_ops,
+                                  const int32_t* d_initial, int32_t n_initial, int32_t n_select,
+                                  int32_t* d_selected, int32_t* d_count, void* d_workspace, size_t ws_bytes,
+                                  void* stream) {
+  if (N <= 0 || n_select < 0 || n_initial < 1)
+    return fail(TCL_ERR_INVALID_ARG, "need N > 0, n_initial > 0 (Eq. (1) needs a labeled set), n_select >= 0");
+  if (n_ops <= 0 || n_ops > 4096) return fail(TCL_ERR_UNSUPPORTED, "n_ops must be in [1, 4096] (got %d)", n_ops);
+  if (!d_scores || !d_op || !d_initial || !d_count || (n_select > 0 && !d_selected) || !d_workspace)
+    return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_workspace) % 256) return fail(TCL_ERR_INVALID_ARG, "d_workspace must be 256-byte aligned");
+  const size_t need = rdu_workspace_bytes(N, n_ops);
+  if (ws_bytes < need) return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  TCL_HIP(launch_rdu_select(N, d_scores, d_op, n_ops, d_initial, n_initial, n_select, d_selected, d_count,
+                            d_workspace, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
 // ------------------------------------------------------------------ kernel-level entry points
 
 TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const float* d_A,

@@ -251,6 +251,19 @@ hipError_t launch_loss_head_bwd(int B, int d, int h, const float* s, const float
 size_t rank_workspace_floats(int B, int nsets);
 hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, const float* l1, float sigma,
                              float w0, float w1, float* ws, float* ds, float* out, hipStream_t st);
+// ---------------------------------------------------------------- score consumers
+// Per-segment top-K: out [n_seg][K] global indices of each segment's K best
+// scores (best first, equal scores in index order, NaN last), -1 past a
+// segment's end. offs [n_seg + 1]. K in [1, 1024].
+hipError_t launch_topk(int n_seg, const int* offs, const float* s, int K, int* out, hipStream_t st);
+// RDU selection (Alg. 1, Eq. (1)-(3)) of up to n_select programs from a pool
+// of N: out [n_select] in selection order (-1 past the end), count [1].
+// op [N] in [0, n_ops) (others are never selected), n_ops <= 4096;
+// init [n_init] the initial labeled programs (distinct, in [0, N)).
+size_t rdu_workspace_bytes(int N, int n_ops);
+hipError_t launch_rdu_select(int N, const float* s, const int* op, int n_ops, const int* init, int n_init,
+                             int n_select, int* out, int* count, void* ws, hipStream_t st);
+
 // EWC penalty (Eq. (9)): grad += lam F (theta - prev); loss[3] =
 // lam/2 sum F (theta - prev)^2 and loss[0] += loss[3]. part: ewc_part_floats().
 int ewc_part_floats();

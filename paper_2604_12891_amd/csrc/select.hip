@@ -1,0 +1,471 @@
+// What consumes the scores: per-segment top-K (the inference phase of
+// section 3 keeps the K best candidates of a tuning round) and the RDU
+// sampler's selection of programs to label (section 4, Alg. 1, Eq. (1)-(3)).
+//
+// Top-K: one workgroup per segment. Scores map to order-preserving 32-bit
+// keys (NaN below everything); a four-pass radix select over 8-bit digits
+// finds the K-th largest key; the items above it and the lowest-index items
+// equal to it are gathered and bitonic-sorted in LDS by (key descending,
+// index ascending).
+//
+// RDU selection: the greedy loop of Alg. 1, one iteration per selected
+// program, on the device (the host only enqueues): a grid pass updates each
+// candidate's distance to the labeled set with the last selected program
+// (Eq. (1) kept as a running minimum), computes t_s = f d_s + u_s with the
+// variance of Eq. (2)-(3) from running sums, and reduces the argmax; a
+// one-workgroup pass labels the winner. A candidate whose operator type has
+// used its budget can never be labeled, so it is masked out as soon as that
+// happens; Alg. 1 drops such candidates one at a time when they come up as
+// the argmax, which leaves the same sequence of labeled programs. fp64
+// throughout (the normalised predictions, distances, sums and t_s).
+#include "common.h"
+#include "kernels.h"
+
+namespace tcl {
+namespace {
+
+constexpr int kST = 256;  // threads per block
+
+// ---------------------------------------------------------------- top-K
+__device__ __forceinline__ uint32_t score_key(float f) {
+  if (f != f) return 0u;  // NaN: below every number
+  uint32_t u = __float_as_uint(f);
+  if ((u << 1) == 0u) u = 0u;  // -0 and +0 are equal scores
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// block-wide exclusive prefix of a 0/1 flag over the 256 threads (in thread
+// order); returns the prefix, *total the block's count
+__device__ __forceinline__ int block_prefix(bool flag, int* wsum, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t m = __ballot(flag);
+  const int in_wave = __popcll(m & ((1ull << lane) - 1ull));
+  __syncthreads();
+  if (lane == 0) wsum[w] = __popcll(m);
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kST / 64; ++i) {
+    before += i < w ? wsum[i] : 0;
+    all += wsum[i];
+  }
+  *total = all;
+  return before + in_wave;
+}
+
+template <int P>  // P: power of two >= K
+__global__ __launch_bounds__(kST) void topk_kernel(const int* __restrict__ offs, const float* __restrict__ s,
+                                                   int K, int* __restrict__ out) {
+  __shared__ int hist[256];
+  __shared__ uint64_t cand[P];
+  __shared__ int wsum[kST / 64];
+  __shared__ int sdig, sabove, cnt_gt;
+  const int g = blockIdx.x;
+  const int lo = offs[g];
+  const int n = max(offs[g + 1] - lo, 0);
+  const int tid = threadIdx.x;
+  const int take = min(n, K);
+
+  for (int i = tid; i < P; i += kST) cand[i] = 0ull;  // padding sorts last
+  if (tid == 0) cnt_gt = 0;
+  uint32_t kth = 0u;
+  int need_eq = take;  // items equal to kth to keep (all, when n <= K)
+  if (n > K) {
+    uint32_t prefix = 0u, pmask = 0u;
+    int krem = K;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      __syncthreads();
+      hist[tid] = 0;
+      __syncthreads();
+      for (int i = tid; i < n; i += kST) {
+        const uint32_t key = score_key(s[lo + i]);
+        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        int above = 0, d = 255;
+        for (; d > 0; --d) {
+          if (above + hist[d] >= krem) break;
+          above += hist[d];
+        }
+        sdig = d;
+        sabove = above;
+      }
+      __syncthreads();
+      krem -= sabove;
+      prefix |= (uint32_t)sdig << shift;
+      pmask |= 0xFFu << shift;
+    }
+    kth = prefix;
+    need_eq = krem;
+  }
+  __syncthreads();
+  // gather: every key above kth, then the first need_eq keys equal to it
+  int eq_base = 0;
+  for (int t0 = 0; t0 < n; t0 += kST) {
+    const int i = t0 + tid;
+    const bool ok = i < n;
+    const uint32_t key = ok ? score_key(s[lo + i]) : 0u;
+    const uint64_t code = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)i);
+    const bool gt = ok && n > K && key > kth;
+    const bool eq = ok && (n <= K || key == kth);
+    if (gt) cand[atomicAdd(&cnt_gt, 1)] = code;
+    int tot;
+    const int r = block_prefix(eq, wsum, &tot);
+    if (eq && eq_base + r < need_eq) cand[(take - need_eq) + eq_base + r] = code;
+    eq_base += tot;
+  }
+  __syncthreads();
+  // bitonic sort, descending
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < P; i += kST) {
+        const int p = i ^ j;
+        if (p > i) {
+          const uint64_t a = cand[i], b = cand[p];
+          const bool desc = (i & k) == 0;
+          if (desc ? (a < b) : (a > b)) {
+            cand[i] = b;
+            cand[p] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int r = tid; r < K; r += kST)
+    out[(int64_t)g * K + r] = r < take ? lo + (int)(0xFFFFFFFFu - (uint32_t)(cand[r] & 0xFFFFFFFFull)) : -1;
+}
+
+// ---------------------------------------------------------------- RDU selection
+struct RduState {
+  double lo, range;  // normalisation of the predictions
+  double S1, S2;     // sums of f and f^2 over the labeled set
+  int M;             // labeled programs
+  int count;         // selected so far
+  int last;          // the last selected program (-1: none yet)
+  int done;
+  int n_select;
+  int pad_[3];
+};
+
+struct Best {
+  double t;
+  int i;
+};
+
+__device__ __forceinline__ bool better(double t, int i, double bt, int bi) {
+  return bi < 0 || t > bt || (t == bt && i < bi);
+}
+
+__device__ __forceinline__ double fhat(const float* s, int i, const RduState& st) {
+  return st.range > 0.0 ? ((double)s[i] - st.lo) / st.range : 0.0;
+}
+
+// block argmax of (t, i), lower index on ties; result in thread 0
+__device__ Best block_best(double t, int i, double* st, int* si) {
+  st[threadIdx.x] = t;
+  si[threadIdx.x] = i;
+  __syncthreads();
+  for (int o = kST / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      const double t2 = st[threadIdx.x + o];
+      const int i2 = si[threadIdx.x + o];
+      if (i2 >= 0 && better(t2, i2, st[threadIdx.x], si[threadIdx.x])) {
+        st[threadIdx.x] = t2;
+        si[threadIdx.x] = i2;
+      }
+    }
+    __syncthreads();
+  }
+  return Best{st[0], si[0]};
+}
+
+// per block: min and max of the scores, and a histogram of operator types
+// (types outside [0, n_ops) are counted in opcount[n_ops])
+constexpr int kMaxOps = 4096;
+__global__ __launch_bounds__(kST) void rdu_stats_kernel(int N, const float* __restrict__ s,
+                                                        const int* __restrict__ op, int n_ops,
+                                                        float* __restrict__ mm, int* __restrict__ opcount) {
+  __shared__ float smin[kST], smax[kST];
+  __shared__ int h[kMaxOps + 1];
+  for (int o = threadIdx.x; o <= n_ops; o += kST) h[o] = 0;
+  __syncthreads();
+  float mn = INFINITY, mx = -INFINITY;
+  for (int i = blockIdx.x * kST + threadIdx.x; i < N; i += gridDim.x * kST) {
+    mn = fminf(mn, s[i]);
+    mx = fmaxf(mx, s[i]);
+    const int o = op[i];
+    atomicAdd(&h[(o >= 0 && o < n_ops) ? o : n_ops], 1);
+  }
+  __syncthreads();
+  for (int o = threadIdx.x; o <= n_ops; o += kST)
+    if (h[o]) atomicAdd(&opcount[o], h[o]);
+  smin[threadIdx.x] = mn;
+  smax[threadIdx.x] = mx;
+  __syncthreads();
+  for (int o = kST / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      smin[threadIdx.x] = fminf(smin[threadIdx.x], smin[threadIdx.x + o]);
+      smax[threadIdx.x] = fmaxf(smax[threadIdx.x], smax[threadIdx.x + o]);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    mm[2 * blockIdx.x] = smin[0];
+    mm[2 * blockIdx.x + 1] = smax[0];
+  }
+}
+
+__global__ __launch_bounds__(kST) void rdu_zero_kernel(int n, int* __restrict__ a) {
+  for (int i = blockIdx.x * kST + threadIdx.x; i < n; i += gridDim.x * kST) a[i] = 0;
+}
+
+// one block: normalisation, budgets, sums over the initial labeled set
+__global__ __launch_bounds__(kST) void rdu_setup_kernel(int N, const float* __restrict__ s, int n_ops,
+                                                        const int* __restrict__ init, int n_init, int n_select,
+                                                        const float* __restrict__ mm, int nmm,
+                                                        const int* __restrict__ opcount,
+                                                        double* __restrict__ budget, int* __restrict__ sel,
+                                                        RduState* __restrict__ state) {
+  __shared__ double r1[kST], r2[kST];
+  __shared__ int rc[kST];
+  __shared__ double slo, srange;
+  if (threadIdx.x == 0) {
+    float mn = mm[0], mx = mm[1];
+    for (int b = 1; b < nmm; ++b) {
+      mn = fminf(mn, mm[2 * b]);
+      mx = fmaxf(mx, mm[2 * b + 1]);
+    }
+    slo = (double)mn;
+    srange = (double)mx - (double)mn;
+  }
+  __syncthreads();
+  RduState st{};
+  st.lo = slo;
+  st.range = srange;
+  for (int o = threadIdx.x; o < n_ops; o += kST) {
+    budget[o] = (double)n_select * (double)opcount[o] / (double)N;
+    sel[o] = 0;
+  }
+  double a1 = 0.0, a2 = 0.0;
+  int c = 0;
+  for (int j = threadIdx.x; j < n_init; j += kST) {
+    const int i = init[j];
+    if (i >= 0 && i < N) {
+      const double f = fhat(s, i, st);
+      a1 += f;
+      a2 += f * f;
+      ++c;
+    }
+  }
+  r1[threadIdx.x] = a1;
+  r2[threadIdx.x] = a2;
+  rc[threadIdx.x] = c;
+  __syncthreads();
+  for (int o = kST / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      r1[threadIdx.x] += r1[threadIdx.x + o];
+      r2[threadIdx.x] += r2[threadIdx.x + o];
+      rc[threadIdx.x] += rc[threadIdx.x + o];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    st.S1 = r1[0];
+    st.S2 = r2[0];
+    st.M = rc[0];
+    st.count = 0;
+    st.last = -1;
+    st.n_select = n_select;
+    st.done = (n_select <= 0 || rc[0] == 0) ? 1 : 0;
+    *state = st;
+  }
+}
+
+// d[i] = min over the initial labeled set of |f_i - f_j|
+__global__ __launch_bounds__(kST) void rdu_dinit_kernel(int N, const float* __restrict__ s,
+                                                        const int* __restrict__ init, int n_init,
+                                                        const RduState* __restrict__ state,
+                                                        double* __restrict__ d) {
+  __shared__ double tf[kST];
+  const RduState st = *state;
+  const int i = blockIdx.x * kST + threadIdx.x;
+  const double fi = i < N ? fhat(s, i, st) : 0.0;
+  double best = INFINITY;
+  for (int j0 = 0; j0 < n_init; j0 += kST) {
+    __syncthreads();
+    const int j = j0 + threadIdx.x;
+    const int idx = j < n_init ? init[j] : -1;
+    tf[threadIdx.x] = (idx >= 0 && idx < N) ? fhat(s, idx, st) : NAN;
+    __syncthreads();
+    const int n = min(kST, n_init - j0);
+    for (int jj = 0; jj < n; ++jj) {
+      const double fj = tf[jj];
+      if (fj == fj) best = fmin(best, fabs(fi - fj));
+    }
+  }
+  if (i < N) d[i] = s[i] == s[i] ? best : -1.0;  // an unscored (NaN) program is no candidate
+}
+
+// the initial labeled programs are not candidates
+__global__ __launch_bounds__(kST) void rdu_mark_kernel(int N, const int* __restrict__ init, int n_init,
+                                                       double* __restrict__ d) {
+  const int j = blockIdx.x * kST + threadIdx.x;
+  if (j < n_init) {
+    const int i = init[j];
+    if (i >= 0 && i < N) d[i] = -1.0;
+  }
+}
+
+// one iteration, grid pass: distances, masks, t_s, block argmax
+__global__ __launch_bounds__(kST) void rdu_score_kernel(int N, const float* __restrict__ s,
+                                                        const int* __restrict__ op, int n_ops,
+                                                        const double* __restrict__ budget,
+                                                        const int* __restrict__ sel,
+                                                        const RduState* __restrict__ state,
+                                                        double* __restrict__ d, Best* __restrict__ part) {
+  __shared__ double bt[kST];
+  __shared__ int bi[kST];
+  const RduState st = *state;
+  if (st.done) return;
+  const double fl = st.last >= 0 ? fhat(s, st.last, st) : 0.0;
+  const double inv = 1.0 / (double)(st.M + 1);
+  double best_t = 0.0;
+  int best_i = -1;
+  for (int i = blockIdx.x * kST + threadIdx.x; i < N; i += gridDim.x * kST) {
+    double di = d[i];
+    if (di < 0.0) continue;  // labeled, or its operator's budget is used up
+    const int o = op[i];
+    if (o < 0 || o >= n_ops || (double)sel[o] >= budget[o]) {
+      d[i] = -1.0;
+      continue;
+    }
+    const double fi = fhat(s, i, st);
+    if (st.last >= 0) {
+      const double dn = fabs(fi - fl);  // Eq. (1) as a running minimum
+      if (dn < di) {
+        di = dn;
+        d[i] = dn;
+      }
+    }
+    const double mu = (fi + st.S1) * inv;                 // Eq. (2)
+    const double u = (fi * fi + st.S2) * inv - mu * mu;   // Eq. (3), from the running sums
+    const double t = fi * di + u;
+    if (better(t, i, best_t, best_i)) {
+      best_t = t;
+      best_i = i;
+    }
+  }
+  const Best b = block_best(best_t, best_i, bt, bi);
+  if (threadIdx.x == 0) part[blockIdx.x] = b;
+}
+
+// one iteration, one block: label the winner
+__global__ __launch_bounds__(kST) void rdu_pick_kernel(int nparts, const float* __restrict__ s,
+                                                       const int* __restrict__ op, const Best* __restrict__ part,
+                                                       int* __restrict__ sel, double* __restrict__ d,
+                                                       RduState* __restrict__ state, int* __restrict__ out) {
+  __shared__ double bt[kST];
+  __shared__ int bi[kST];
+  __shared__ int sdone;
+  if (threadIdx.x == 0) sdone = state->done;
+  __syncthreads();
+  if (sdone) return;
+  double t = 0.0;
+  int i = -1;
+  for (int p = threadIdx.x; p < nparts; p += kST) {
+    const Best b = part[p];
+    if (b.i >= 0 && better(b.t, b.i, t, i)) {
+      t = b.t;
+      i = b.i;
+    }
+  }
+  const Best w = block_best(t, i, bt, bi);
+  if (threadIdx.x == 0) {
+    RduState st = *state;
+    if (w.i < 0) {
+      st.done = 1;
+    } else {
+      const double f = fhat(s, w.i, st);
+      out[st.count] = w.i;
+      st.count += 1;
+      st.M += 1;
+      st.S1 += f;
+      st.S2 += f * f;
+      st.last = w.i;
+      sel[op[w.i]] += 1;
+      d[w.i] = -1.0;
+      if (st.count >= st.n_select) st.done = 1;
+    }
+    *state = st;
+  }
+}
+
+__global__ __launch_bounds__(kST) void rdu_finish_kernel(int n_select, const RduState* __restrict__ state,
+                                                         int* __restrict__ out, int* __restrict__ count) {
+  const int c = state->count;
+  for (int i = threadIdx.x; i < n_select; i += kST)
+    if (i >= c) out[i] = -1;
+  if (threadIdx.x == 0) *count = c;
+}
+
+constexpr int kRduGrid = 1024;  // blocks of the grid passes (grid-stride)
+
+size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace
+
+hipError_t launch_topk(int n_seg, const int* offs, const float* s, int K, int* out, hipStream_t st) {
+  if (n_seg <= 0 || K < 1 || K > 1024) return hipErrorInvalidValue;
+#define TCL_TOPK(PP) hipLaunchKernelGGL((topk_kernel<PP>), dim3(n_seg), dim3(kST), 0, st, offs, s, K, out)
+  if (K <= 64) TCL_TOPK(64);
+  else if (K <= 256) TCL_TOPK(256);
+  else TCL_TOPK(1024);
+#undef TCL_TOPK
+  return hipGetLastError();
+}
+
+size_t rdu_workspace_bytes(int N, int n_ops) {
+  const int grid = std::min((N + kST - 1) / kST, kRduGrid);
+  return al256(sizeof(RduState)) + al256((size_t)N * 8) + al256((size_t)n_ops * 8) +
+         al256((size_t)(n_ops + 1) * 4) * 2 + al256((size_t)grid * 2 * 4) + al256((size_t)grid * sizeof(Best));
+}
+
+hipError_t launch_rdu_select(int N, const float* s, const int* op, int n_ops, const int* init, int n_init,
+                             int n_select, int* out, int* count, void* ws, hipStream_t st) {
+  if (N <= 0 || n_ops <= 0 || n_ops > kMaxOps || n_init < 0 || n_select < 0) return hipErrorInvalidValue;
+  const int grid = std::min((N + kST - 1) / kST, kRduGrid);
+  char* p = static_cast<char*>(ws);
+  RduState* state = reinterpret_cast<RduState*>(p);
+  p += al256(sizeof(RduState));
+  double* d = reinterpret_cast<double*>(p);
+  p += al256((size_t)N * 8);
+  double* budget = reinterpret_cast<double*>(p);
+  p += al256((size_t)n_ops * 8);
+  int* opcount = reinterpret_cast<int*>(p);
+  p += al256((size_t)(n_ops + 1) * 4);
+  int* sel = reinterpret_cast<int*>(p);
+  p += al256((size_t)(n_ops + 1) * 4);
+  float* mm = reinterpret_cast<float*>(p);
+  p += al256((size_t)grid * 2 * 4);
+  Best* part = reinterpret_cast<Best*>(p);
+
+  hipLaunchKernelGGL(rdu_zero_kernel, dim3(std::max(1, std::min((n_ops + kST) / kST, 64))), dim3(kST), 0, st,
+                     n_ops + 1, opcount);
+  hipLaunchKernelGGL(rdu_stats_kernel, dim3(grid), dim3(kST), 0, st, N, s, op, n_ops, mm, opcount);
+  hipLaunchKernelGGL(rdu_setup_kernel, dim3(1), dim3(kST), 0, st, N, s, n_ops, init, n_init, n_select, mm, grid,
+                     opcount, budget, sel, state);
+  hipLaunchKernelGGL(rdu_dinit_kernel, dim3((N + kST - 1) / kST), dim3(kST), 0, st, N, s, init, n_init, state, d);
+  if (n_init > 0)
+    hipLaunchKernelGGL(rdu_mark_kernel, dim3((n_init + kST - 1) / kST), dim3(kST), 0, st, N, init, n_init, d);
+  for (int it = 0; it < n_select; ++it) {
+    hipLaunchKernelGGL(rdu_score_kernel, dim3(grid), dim3(kST), 0, st, N, s, op, n_ops, budget, sel, state, d,
+                       part);
+    hipLaunchKernelGGL(rdu_pick_kernel, dim3(1), dim3(kST), 0, st, grid, s, op, part, sel, d, state, out);
+  }
+  hipLaunchKernelGGL(rdu_finish_kernel, dim3(1), dim3(kST), 0, st, n_select, state, out, count);
+  return hipGetLastError();
+}
+
+}  // namespace tcl
