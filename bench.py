@@ -288,6 +288,81 @@ def bench_distill(args, w):
     print(json.dumps(rec), flush=True)
 
 
+def bench_consumers(args):
+    """What consumes the scores: per-segment top-K over a large round's scores
+    and the RDU selection over a dataset-sized pool, each against HBM."""
+    import numpy as np
+    import torch
+
+    from paper_2604_12891_amd import binding as tb
+
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(12891)
+    res = {}
+
+    def timed(fn, steps):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    # top-K: 65,536 scores (the bf16 pool workload's round) as 16 tasks of 4,096, K = 64
+    B, n_seg, K = 65536, 16, 64
+    s = torch.from_numpy((0.3 * rng.standard_normal(B)).astype(np.float32)).to(dev)
+    offs = torch.arange(0, B + 1, B // n_seg, dtype=torch.int32, device=dev)
+    ms = timed(lambda: tb.topk(s, offs, K), args.steps)
+    nbytes = B * 4 + n_seg * K * 4
+    res["topk"] = {"ms_per_call": ms, "candidates_per_s": B / (ms * 1e-3),
+                   "config": f"{B} scores, {n_seg} segments of {B // n_seg}, K={K}",
+                   "roofline": {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                                "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                "traffic": None, "bytes_per_call": nbytes}}
+    # RDU: a pool the size of one platform's dataset (8.65 M programs), 20
+    # operator types, 1,024 initial labeled programs, 64 selections
+    N, n_ops, n_init, n_sel = 8_650_000, 20, 1024, 64
+    sc = torch.from_numpy((0.3 * rng.standard_normal(N)).astype(np.float32)).to(dev)
+    p = rng.random(n_ops) + 0.1
+    op = torch.from_numpy(rng.choice(n_ops, N, p=p / p.sum()).astype(np.int32)).to(dev)
+    init = torch.from_numpy(rng.choice(N, n_init, replace=False).astype(np.int32)).to(dev)
+    ws = torch.empty(tb.lib().tcl_rdu_workspace_bytes(N, n_ops), dtype=torch.uint8, device=dev)
+    steps = max(2, args.steps // 10)
+    ms = timed(lambda: tb.rdu_select(sc, op, n_ops, init, n_sel, workspace=ws), steps)
+    per_sel = ms / n_sel
+    nbytes = N * 16  # per selection: score, operator type and running distance of every program, read once
+    res["rdu_select"] = {"ms_per_call": ms, "ms_per_selection": per_sel, "selections_per_s": 1e3 / per_sel,
+                         "config": f"pool {N}, {n_ops} operator types, {n_init} initial, {n_sel} selections",
+                         "roofline": {"bound": "hbm", "achieved": nbytes / (per_sel * 1e-3) / 1e9,
+                                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                      "frac": nbytes / (per_sel * 1e-3) / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                                      "bytes_per_selection": nbytes,
+                                      "note": "includes the setup pass (normalisation, budgets, distances "
+                                              "to the initial set) amortised over the selections"}}
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import select as osel
+        n_cpu, sel_cpu = 20000, 4
+        t0 = time.perf_counter()
+        osel.rdu_select(sc[:n_cpu].cpu().numpy().astype(np.float64), op[:n_cpu].cpu().numpy(), n_ops,
+                        np.arange(64), sel_cpu)
+        dt = time.perf_counter() - t0
+        cpu = {"value": sel_cpu / dt * n_cpu / N, "unit": "selections/s (scaled to the 8.65 M pool)", "cores": 1,
+               "kind": "oracle", "sample": f"{sel_cpu} selections from a pool of {n_cpu} with 64 initial "
+                                           f"({dt:.1f} s), scaled linearly in the pool size"}
+    rec = {"metric": "score consumers: top-K candidates/s and RDU selections/s", "value": res["rdu_select"]["selections_per_s"],
+           "unit": "selections/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": res["rdu_select"]["ms_per_selection"], "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f64", "data": "synthetic",
+           "config": {"workload": "rdu_N8650000_topk_B65536"}, "roofline": res["rdu_select"]["roofline"],
+           "consumers": res, "cpu_baseline": cpu}
+    print(json.dumps(rec), flush=True)
+
+
 def scan_sweep(args):
     """Time the sequential scan and the chunked two-level scan on their own
     (kernel-level entry point, HIP events on the launch stream) for programs
@@ -346,6 +421,8 @@ def main():
     ap.add_argument("--kernels", action="store_true", help="print the per-kernel table to stderr")
     ap.add_argument("--scan-sweep", action="store_true",
                     help="time the sequential against the chunked scan over batch sizes and exit")
+    ap.add_argument("--consumers", action="store_true",
+                    help="time the score consumers (top-K, RDU selection) instead of a model workload")
     ap.add_argument("--objective", choices=["mse", "kd"], default="mse",
                     help="distillation workload: the two-MSE loss, or the paper's ranking objective "
                          "(LambdaRank terms, teacher gate, EWC)")
@@ -364,6 +441,9 @@ def main():
 
     if args.scan_sweep:
         scan_sweep(args)
+        return
+    if args.consumers:
+        bench_consumers(args)
         return
 
     import numpy as np

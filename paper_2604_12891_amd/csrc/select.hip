@@ -2,7 +2,7 @@
 // section 3 keeps the K best candidates of a tuning round) and the RDU
 // sampler's selection of programs to label (section 4, Alg. 1, Eq. (1)-(3)).
 //
-// Top-K: one workgroup per segment. Scores map to order-preserving 32-bit
+// Top-K: one workgroup of 1,024 threads per segment. Scores map to order-preserving 32-bit
 // keys (NaN below everything); a four-pass radix select over 8-bit digits
 // finds the K-th largest key; the items above it and the lowest-index items
 // equal to it are gathered and bitonic-sorted in LDS by (key descending,
@@ -34,7 +34,9 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// block-wide exclusive prefix of a 0/1 flag over the 256 threads (in thread
+constexpr int kTK = 1024;  // threads of a top-K workgroup
+
+// block-wide exclusive prefix of a 0/1 flag over the kTK threads (in thread
 // order); returns the prefix, *total the block's count
 __device__ __forceinline__ int block_prefix(bool flag, int* wsum, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -45,7 +47,7 @@ __device__ __forceinline__ int block_prefix(bool flag, int* wsum, int* total) {
   __syncthreads();
   int before = 0, all = 0;
 #pragma unroll
-  for (int i = 0; i < kST / 64; ++i) {
+  for (int i = 0; i < kTK / 64; ++i) {
     before += i < w ? wsum[i] : 0;
     all += wsum[i];
   }
@@ -54,11 +56,12 @@ __device__ __forceinline__ int block_prefix(bool flag, int* wsum, int* total) {
 }
 
 template <int P>  // P: power of two >= K
-__global__ __launch_bounds__(kST) void topk_kernel(const int* __restrict__ offs, const float* __restrict__ s,
+__global__ __launch_bounds__(kTK) void topk_kernel(const int* __restrict__ offs, const float* __restrict__ s,
                                                    int K, int* __restrict__ out) {
-  __shared__ int hist[256];
+  __shared__ int hist[kTK / 64][256];  // one histogram per wavefront (scores crowd a few top digits)
+  __shared__ int tot[4];
   __shared__ uint64_t cand[P];
-  __shared__ int wsum[kST / 64];
+  __shared__ int wsum[kTK / 64];
   __shared__ int sdig, sabove, cnt_gt;
   const int g = blockIdx.x;
   const int lo = offs[g];
@@ -66,30 +69,45 @@ __global__ __launch_bounds__(kST) void topk_kernel(const int* __restrict__ offs,
   const int tid = threadIdx.x;
   const int take = min(n, K);
 
-  for (int i = tid; i < P; i += kST) cand[i] = 0ull;  // padding sorts last
+  for (int i = tid; i < P; i += kTK) cand[i] = 0ull;  // padding sorts last
   if (tid == 0) cnt_gt = 0;
   uint32_t kth = 0u;
   int need_eq = take;  // items equal to kth to keep (all, when n <= K)
   if (n > K) {
     uint32_t prefix = 0u, pmask = 0u;
     int krem = K;
+    const int wave = tid >> 6;
     for (int shift = 24; shift >= 0; shift -= 8) {
       __syncthreads();
-      hist[tid] = 0;
+      for (int b = tid; b < (kTK / 64) * 256; b += kTK) (&hist[0][0])[b] = 0;
       __syncthreads();
-      for (int i = tid; i < n; i += kST) {
+      for (int i = tid; i < n; i += kTK) {
         const uint32_t key = score_key(s[lo + i]);
-        if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255], 1);
+        if ((key & pmask) == prefix) atomicAdd(&hist[wave][(key >> shift) & 255], 1);
       }
       __syncthreads();
-      if (tid == 0) {
-        int above = 0, d = 255;
-        for (; d > 0; --d) {
-          if (above + hist[d] >= krem) break;
-          above += hist[d];
+      // thread t < 256 takes digit 255 - t; an inclusive scan over threads is
+      // then the count of keys at or above that digit, and exactly one digit
+      // has that count reach krem while the digits above it stay below
+      int c = 0, incl = 0;
+      if (tid < 256) {
+#pragma unroll
+        for (int w = 0; w < kTK / 64; ++w) c += hist[w][255 - tid];
+        incl = c;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int v = __shfl_up(incl, o, 64);
+          if ((tid & 63) >= o) incl += v;
         }
-        sdig = d;
-        sabove = above;
+        if ((tid & 63) == 63) tot[tid >> 6] = incl;
+      }
+      __syncthreads();
+      if (tid < 256) {
+        for (int w = 0; w < (tid >> 6); ++w) incl += tot[w];
+        if (incl >= krem && incl - c < krem) {
+          sdig = 255 - tid;
+          sabove = incl - c;
+        }
       }
       __syncthreads();
       krem -= sabove;
@@ -102,7 +120,7 @@ __global__ __launch_bounds__(kST) void topk_kernel(const int* __restrict__ offs,
   __syncthreads();
   // gather: every key above kth, then the first need_eq keys equal to it
   int eq_base = 0;
-  for (int t0 = 0; t0 < n; t0 += kST) {
+  for (int t0 = 0; t0 < n; t0 += kTK) {
     const int i = t0 + tid;
     const bool ok = i < n;
     const uint32_t key = ok ? score_key(s[lo + i]) : 0u;
@@ -119,7 +137,7 @@ __global__ __launch_bounds__(kST) void topk_kernel(const int* __restrict__ offs,
   // bitonic sort, descending
   for (int k = 2; k <= P; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < P; i += kST) {
+      for (int i = tid; i < P; i += kTK) {
         const int p = i ^ j;
         if (p > i) {
           const uint64_t a = cand[i], b = cand[p];
@@ -133,7 +151,7 @@ __global__ __launch_bounds__(kST) void topk_kernel(const int* __restrict__ offs,
       __syncthreads();
     }
   }
-  for (int r = tid; r < K; r += kST)
+  for (int r = tid; r < K; r += kTK)
     out[(int64_t)g * K + r] = r < take ? lo + (int)(0xFFFFFFFFu - (uint32_t)(cand[r] & 0xFFFFFFFFull)) : -1;
 }
 
@@ -283,6 +301,76 @@ __global__ __launch_bounds__(kST) void rdu_setup_kernel(int N, const float* __re
   }
 }
 
+// The initial labeled set's normalised predictions, sorted ascending (at
+// most kSortInit of them; larger sets use rdu_dinit_kernel's direct pass).
+constexpr int kSortInit = 8192;
+__global__ __launch_bounds__(1024) void rdu_sort_init_kernel(int N, const float* __restrict__ s,
+                                                             const int* __restrict__ init, int n_init,
+                                                             const RduState* __restrict__ state,
+                                                             double* __restrict__ sorted, int* __restrict__ n_valid) {
+  __shared__ double v[kSortInit];
+  const RduState st = *state;
+  int P = 1;
+  while (P < n_init) P <<= 1;
+  for (int j = threadIdx.x; j < P; j += 1024) {
+    const int i = j < n_init ? init[j] : -1;
+    v[j] = (i >= 0 && i < N && s[i] == s[i]) ? fhat(s, i, st) : INFINITY;  // invalid entries sort last
+  }
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int jj = k >> 1; jj > 0; jj >>= 1) {
+      for (int i = threadIdx.x; i < P; i += 1024) {
+        const int p = i ^ jj;
+        if (p > i) {
+          const double a = v[i], b = v[p];
+          const bool up = (i & k) == 0;
+          if (up ? (a > b) : (a < b)) {
+            v[i] = b;
+            v[p] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  __shared__ int cnt;
+  if (threadIdx.x == 0) cnt = 0;
+  __syncthreads();
+  for (int j = threadIdx.x; j < n_init; j += 1024) {
+    sorted[j] = v[j];
+    if (v[j] != INFINITY) atomicAdd(&cnt, 1);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) *n_valid = cnt;
+}
+
+// d[i] = min over the initial set of |f_i - f_j|: the nearest value on each
+// side of f_i in the sorted set (a binary search) gives the same minimum
+__global__ __launch_bounds__(kST) void rdu_dinit_sorted_kernel(int N, const float* __restrict__ s,
+                                                               const double* __restrict__ sorted,
+                                                               const int* __restrict__ n_valid,
+                                                               const RduState* __restrict__ state,
+                                                               double* __restrict__ d) {
+  const RduState st = *state;
+  const int m = *n_valid;
+  for (int i = blockIdx.x * kST + threadIdx.x; i < N; i += gridDim.x * kST) {
+    if (s[i] != s[i] || m == 0) {
+      d[i] = s[i] != s[i] ? -1.0 : INFINITY;
+      continue;
+    }
+    const double fi = fhat(s, i, st);
+    int lo = 0, hi = m;  // first index with sorted[idx] >= fi
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (sorted[mid] < fi) lo = mid + 1; else hi = mid;
+    }
+    double best = INFINITY;
+    if (lo < m) best = fmin(best, fabs(fi - sorted[lo]));
+    if (lo > 0) best = fmin(best, fabs(fi - sorted[lo - 1]));
+    d[i] = best;
+  }
+}
+
 // d[i] = min over the initial labeled set of |f_i - f_j|
 __global__ __launch_bounds__(kST) void rdu_dinit_kernel(int N, const float* __restrict__ s,
                                                         const int* __restrict__ init, int n_init,
@@ -418,7 +506,7 @@ size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
 hipError_t launch_topk(int n_seg, const int* offs, const float* s, int K, int* out, hipStream_t st) {
   if (n_seg <= 0 || K < 1 || K > 1024) return hipErrorInvalidValue;
-#define TCL_TOPK(PP) hipLaunchKernelGGL((topk_kernel<PP>), dim3(n_seg), dim3(kST), 0, st, offs, s, K, out)
+#define TCL_TOPK(PP) hipLaunchKernelGGL((topk_kernel<PP>), dim3(n_seg), dim3(kTK), 0, st, offs, s, K, out)
   if (K <= 64) TCL_TOPK(64);
   else if (K <= 256) TCL_TOPK(256);
   else TCL_TOPK(1024);
@@ -429,7 +517,8 @@ hipError_t launch_topk(int n_seg, const int* offs, const float* s, int K, int* o
 size_t rdu_workspace_bytes(int N, int n_ops) {
   const int grid = std::min((N + kST - 1) / kST, kRduGrid);
   return al256(sizeof(RduState)) + al256((size_t)N * 8) + al256((size_t)n_ops * 8) +
-         al256((size_t)(n_ops + 1) * 4) * 2 + al256((size_t)grid * 2 * 4) + al256((size_t)grid * sizeof(Best));
+         al256((size_t)(n_ops + 1) * 4) * 2 + al256((size_t)grid * 2 * 4) + al256((size_t)grid * sizeof(Best)) +
+         al256((size_t)kSortInit * 8) + 256;
 }
 
 hipError_t launch_rdu_select(int N, const float* s, const int* op, int n_ops, const int* init, int n_init,
@@ -450,13 +539,22 @@ hipError_t launch_rdu_select(int N, const float* s, const int* op, int n_ops, co
   float* mm = reinterpret_cast<float*>(p);
   p += al256((size_t)grid * 2 * 4);
   Best* part = reinterpret_cast<Best*>(p);
+  p += al256((size_t)grid * sizeof(Best));
+  double* sorted = reinterpret_cast<double*>(p);
+  p += al256((size_t)kSortInit * 8);
+  int* n_valid = reinterpret_cast<int*>(p);
 
   hipLaunchKernelGGL(rdu_zero_kernel, dim3(std::max(1, std::min((n_ops + kST) / kST, 64))), dim3(kST), 0, st,
                      n_ops + 1, opcount);
   hipLaunchKernelGGL(rdu_stats_kernel, dim3(grid), dim3(kST), 0, st, N, s, op, n_ops, mm, opcount);
   hipLaunchKernelGGL(rdu_setup_kernel, dim3(1), dim3(kST), 0, st, N, s, n_ops, init, n_init, n_select, mm, grid,
                      opcount, budget, sel, state);
-  hipLaunchKernelGGL(rdu_dinit_kernel, dim3((N + kST - 1) / kST), dim3(kST), 0, st, N, s, init, n_init, state, d);
+  if (n_init <= kSortInit) {
+    hipLaunchKernelGGL(rdu_sort_init_kernel, dim3(1), dim3(1024), 0, st, N, s, init, n_init, state, sorted, n_valid);
+    hipLaunchKernelGGL(rdu_dinit_sorted_kernel, dim3(grid), dim3(kST), 0, st, N, s, sorted, n_valid, state, d);
+  } else {
+    hipLaunchKernelGGL(rdu_dinit_kernel, dim3((N + kST - 1) / kST), dim3(kST), 0, st, N, s, init, n_init, state, d);
+  }
   if (n_init > 0)
     hipLaunchKernelGGL(rdu_mark_kernel, dim3((n_init + kST - 1) / kST), dim3(kST), 0, st, N, init, n_init, d);
   for (int it = 0; it < n_select; ++it) {
