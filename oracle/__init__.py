@@ -6,3 +6,4 @@ this package. It never imports the HIP library's package.
 from . import model  # noqa: F401
 from . import kd  # noqa: F401
 from . import select  # noqa: F401
+from . import metric  # noqa: F401

@@ -12,11 +12,18 @@ library primitive); everything else is written out step by step in the
 order the model defines it, with no fusion or reordering.
 
 What the model computes (section 5.2 of the paper, Fig. 5, Eq. (4)-(5)):
-  encoder (one Linear F -> d_model in the configured workloads)
+  encoder: one Linear F -> d_model, or (the paper's form, section 5.2: three
+    Linear layers of widths 64, 128, 128) Linear F -> e_1, ReLU, ...,
+    Linear e_k -> d_model, with cfg["enc_hidden"] = (e_1, ..., e_k)
   -> n_layers x [ h <- h + MambaBlock(RMSNorm(h)) ]
   -> final RMSNorm ("normalized again", section 5.2)
   -> masked mean-pool over the valid tokens of each program
-  -> decoder Linear(d, h) -> ReLU -> Linear(h, 1) = score.
+  -> decoder Linear(d, h) -> ReLU -> Linear(h, 1) = score, or (the paper's
+    three layers of widths 64, 32, 1) Linear(d, h) -> ReLU -> Linear(h, h2)
+    -> ReLU -> Linear(h2, 1) with cfg["dec_hidden2"] = h2.
+The paper names no activation inside its encoder and decoder; a ReLU sits
+between consecutive Linear layers and none after the last one (a stack of
+Linear layers without one would collapse to a single Linear).
 
 Mamba block (the selective SSM that section 5.2 builds on):
   [x | z] = in_proj(n)                       (no bias)
@@ -57,13 +64,24 @@ f64 = np.float64
 # parameter layout
 # --------------------------------------------------------------------------
 
+def encoder_dims(cfg: dict) -> List[int]:
+    """Widths along the encoder: F, the hidden widths, d_model."""
+    return [cfg["F"], *cfg.get("enc_hidden", ()), cfg["d_model"]]
+
+
 def layout(cfg: dict) -> List[Tuple[str, Tuple[int, ...]]]:
-    """Canonical flat-blob order: W0, b0, per block [g, W_in, conv_w, conv_b,
-    W_x, W_dt, b_dt, A_log, D, W_out], then g_f, W1, b1, W2, b2.
-    Matrices are [out, in] row-major."""
-    F, d, E, N = cfg["F"], cfg["d_model"], cfg["d_inner"], cfg["d_state"]
+    """Canonical flat-blob order: the encoder's Linear layers W0, b0 (then
+    W0_1, b0_1, ... for a multi-layer encoder), per block [g, W_in, conv_w,
+    conv_b, W_x, W_dt, b_dt, A_log, D, W_out], then g_f, W1, b1, W2, b2 (and
+    W3, b3 for a three-layer decoder). Matrices are [out, in] row-major."""
+    d, E, N = cfg["d_model"], cfg["d_inner"], cfg["d_state"]
     K, R, h = cfg["d_conv"], cfg["dt_rank"], cfg["head_hidden"]
-    names = [("W0", (d, F)), ("b0", (d,))]
+    h2 = cfg.get("dec_hidden2", 0)
+    dims = encoder_dims(cfg)
+    names = []
+    for i in range(len(dims) - 1):
+        sfx = f"_{i}" if i else ""
+        names += [(f"W0{sfx}", (dims[i + 1], dims[i])), (f"b0{sfx}", (dims[i + 1],))]
     for l in range(cfg["n_layers"]):
         p = f"blk{l}."
         names += [
@@ -72,7 +90,11 @@ def layout(cfg: dict) -> List[Tuple[str, Tuple[int, ...]]]:
             (p + "b_dt", (E,)), (p + "A_log", (E, N)), (p + "D", (E,)),
             (p + "W_out", (d, E)),
         ]
-    names += [("g_f", (d,)), ("W1", (h, d)), ("b1", (h,)), ("W2", (1, h)), ("b2", (1,))]
+    names += [("g_f", (d,)), ("W1", (h, d)), ("b1", (h,))]
+    if h2:
+        names += [("W2", (h2, h)), ("b2", (h2,)), ("W3", (1, h2)), ("b3", (1,))]
+    else:
+        names += [("W2", (1, h)), ("b2", (1,))]
     return names
 
 
@@ -286,6 +308,8 @@ def forward(P, X, lengths, cfg, keep=False):
     lengths = np.asarray(lengths)
     Bn, L, _ = X.shape
     h = X @ P["W0"].T + P["b0"]
+    for i in range(1, len(encoder_dims(cfg)) - 1):
+        h = np.maximum(h, 0.0) @ P[f"W0_{i}"].T + P[f"b0_{i}"]
     caches = []
     for l in range(cfg["n_layers"]):
         h, c = _block_forward(h, P, l, cfg, keep)
@@ -298,9 +322,15 @@ def forward(P, X, lengths, cfg, keep=False):
     pooled = np.sum(hf * mask[:, :, None], axis=1) / lengths[:, None].astype(f64)
     a1 = pooled @ P["W1"].T + P["b1"]
     r1 = np.maximum(a1, 0.0)
-    s = (r1 @ P["W2"].T)[:, 0] + P["b2"][0]
+    if cfg.get("dec_hidden2", 0):
+        r2 = np.maximum(r1 @ P["W2"].T + P["b2"], 0.0)
+        s = (r2 @ P["W3"].T)[:, 0] + P["b3"][0]
+    else:
+        s = (r1 @ P["W2"].T)[:, 0] + P["b2"][0]
     if not keep:
         return s
+    if cfg.get("enc_hidden") or cfg.get("dec_hidden2", 0):
+        raise NotImplementedError("gradients cover the one-Linear encoder and two-layer decoder")
     top = dict(X=X, h_last=h, hf=hf, rf=rf, mask=mask, lengths=lengths,
                pooled=pooled, a1=a1, r1=r1)
     return s, caches, top

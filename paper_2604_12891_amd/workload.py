@@ -54,6 +54,8 @@ class ModelShape:
     head_hidden: int = 256
     final_norm: int = 1
     norm_eps: float = 1e-5
+    enc_hidden: Tuple[int, ...] = ()  # hidden widths of a multi-layer encoder
+    dec_hidden2: int = 0  # second hidden width of a three-layer decoder (0: two layers)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -72,6 +74,14 @@ class Workload:
 TINY = ModelShape(d_model=64, d_inner=128, dt_rank=4, n_layers=2, head_hidden=64)
 D256 = ModelShape()
 STUDENT = ModelShape(d_model=128, d_inner=256, dt_rank=8, n_layers=2, head_hidden=128)
+# The paper's own model (section 5.2 and Table 2's best hyper-parameters): an
+# encoder of three Linear layers F -> 64 -> 128 -> 128, one Mamba block with
+# d_model 128, expand 1, d_state 8, d_conv 4, a decoder 128 -> 64 -> 32 -> 1;
+# dt_rank = ceil(d_model / 16). Features per statement: 22 for the CPU
+# traces, 20 for the GPU ones (section 5.1).
+PAPER_CPU = ModelShape(F=22, d_model=128, d_inner=128, d_state=8, d_conv=4, dt_rank=8, n_layers=1,
+                       head_hidden=64, enc_hidden=(64, 128), dec_hidden2=32)
+PAPER_GPU = dataclasses.replace(PAPER_CPU, F=20)
 
 WORKLOADS: Dict[str, Workload] = {
     w.name: w
@@ -81,6 +91,9 @@ WORKLOADS: Dict[str, Workload] = {
         Workload("score_B65536_L25_d256_bf16", D256, 65536, 25, 5, 25, "bf16", 2),
         Workload("score_B8192_L256_d256_f32", D256, 8192, 256, 64, 256, "f32", 3),
         Workload("distill_B1024_L25_t256_s128_bf16", D256, 1024, 25, 5, 25, "bf16", 4, STUDENT),
+        # the paper's model on its own input shapes: 26 x 22 (CPU) and 41 x 20 (GPU)
+        Workload("paper_B4096_L26_F22_f32", PAPER_CPU, 4096, 26, 5, 26, "f32", 5),
+        Workload("paper_B4096_L41_F20_f32", PAPER_GPU, 4096, 41, 8, 41, "f32", 6),
     ]
 }
 WORKLOAD_ORDER = list(WORKLOADS)
@@ -96,7 +109,11 @@ def _rng(*path: int) -> np.random.Generator:
 def param_layout(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
     """Names and shapes of the parameters, in canonical blob order."""
     d, E, N, K, R, F, h = m.d_model, m.d_inner, m.d_state, m.d_conv, m.dt_rank, m.F, m.head_hidden
-    out: List[Tuple[str, Tuple[int, ...]]] = [("W0", (d, F)), ("b0", (d,))]
+    dims = [F, *m.enc_hidden, d]
+    out: List[Tuple[str, Tuple[int, ...]]] = []
+    for i in range(len(dims) - 1):
+        sfx = f"_{i}" if i else ""
+        out += [(f"W0{sfx}", (dims[i + 1], dims[i])), (f"b0{sfx}", (dims[i + 1],))]
     for l in range(m.n_layers):
         out += [
             (f"blk{l}.g", (d,)),
@@ -110,7 +127,11 @@ def param_layout(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
             (f"blk{l}.D", (E,)),
             (f"blk{l}.W_out", (d, E)),
         ]
-    out += [("g_f", (d,)), ("W1", (h, d)), ("b1", (h,)), ("W2", (1, h)), ("b2", (1,))]
+    out += [("g_f", (d,)), ("W1", (h, d)), ("b1", (h,))]
+    if m.dec_hidden2:
+        out += [("W2", (m.dec_hidden2, h)), ("b2", (m.dec_hidden2,)), ("W3", (1, m.dec_hidden2)), ("b3", (1,))]
+    else:
+        out += [("W2", (1, h)), ("b2", (1,))]
     return out
 
 
@@ -121,14 +142,14 @@ def param_count(m: ModelShape) -> int:
 def init_params(m: ModelShape, rng: np.random.Generator, perturb: bool = False) -> np.ndarray:
     """Flat fp32 parameter blob in canonical order."""
     parts = []
+    fan_in = 0
     for name, shape in param_layout(m):
         base = name.split(".")[-1]
-        if base in ("W0", "W_in", "W_x", "W_dt", "W_out", "W1", "W2"):
+        if base in ("W_in", "W_x", "W_dt", "W_out", "W1", "W2", "W3") or base.startswith("W0"):
             bound = 1.0 / math.sqrt(shape[1])
             a = rng.uniform(-bound, bound, size=shape)
-        elif base in ("b0", "b1", "b2"):
-            fan_in = {"b0": m.F, "b1": m.d_model, "b2": m.head_hidden}[base]
-            bound = 1.0 / math.sqrt(fan_in)
+        elif base in ("b1", "b2", "b3") or base.startswith("b0"):
+            bound = 1.0 / math.sqrt(fan_in)  # fan-in of the weight just before
             a = rng.uniform(-bound, bound, size=shape)
         elif base in ("conv_w", "conv_b"):
             bound = 1.0 / math.sqrt(m.d_conv)
@@ -151,6 +172,8 @@ def init_params(m: ModelShape, rng: np.random.Generator, perturb: bool = False) 
             a = dt0 + np.log(-np.expm1(-dt0))  # inverse of softplus at dt0
         else:  # pragma: no cover - layout and init must list the same names
             raise KeyError(name)
+        if base.startswith("W") and len(shape) == 2:
+            fan_in = shape[1]
         parts.append(np.asarray(a, dtype=np.float32).reshape(-1))
     return np.concatenate(parts)
 

@@ -62,7 +62,8 @@ def assert_scores_match(g, o, dtype: str, what: str = ""):
 def oracle_cfg(shape) -> dict:
     return dict(F=shape.F, d_model=shape.d_model, d_inner=shape.d_inner, d_state=shape.d_state,
                 d_conv=shape.d_conv, dt_rank=shape.dt_rank, n_layers=shape.n_layers,
-                head_hidden=shape.head_hidden, final_norm=shape.final_norm, norm_eps=shape.norm_eps)
+                head_hidden=shape.head_hidden, final_norm=shape.final_norm, norm_eps=shape.norm_eps,
+                enc_hidden=tuple(shape.enc_hidden), dec_hidden2=shape.dec_hidden2)
 
 
 def oracle_scores(blob, X, lengths, shape) -> np.ndarray:

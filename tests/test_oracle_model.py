@@ -20,7 +20,8 @@ TINY_CFG = dict(F=6, d_model=4, d_inner=8, d_state=3, d_conv=4, dt_rank=2, n_lay
 def _cfg(shape: wl.ModelShape) -> dict:
     return dict(F=shape.F, d_model=shape.d_model, d_inner=shape.d_inner, d_state=shape.d_state,
                 d_conv=shape.d_conv, dt_rank=shape.dt_rank, n_layers=shape.n_layers,
-                head_hidden=shape.head_hidden, final_norm=shape.final_norm, norm_eps=shape.norm_eps)
+                head_hidden=shape.head_hidden, final_norm=shape.final_norm, norm_eps=shape.norm_eps,
+                enc_hidden=tuple(shape.enc_hidden), dec_hidden2=shape.dec_hidden2)
 
 
 def _tiny(seed=0, Bn=3, L=7, perturb=True):
@@ -59,7 +60,7 @@ def test_rmsnorm_unit_rms_and_scale_invariance():
 # --------------------------------------------------------------- model-level
 
 def test_layout_matches_workload_generator():
-    for shape in (wl.TINY, wl.D256, wl.STUDENT, wl.ModelShape(**TINY_CFG)):
+    for shape in (wl.TINY, wl.D256, wl.STUDENT, wl.ModelShape(**TINY_CFG), wl.PAPER_CPU, wl.PAPER_GPU):
         cfg = _cfg(shape)
         assert [(n, tuple(s)) for n, s in om.layout(cfg)] == [(n, tuple(s)) for n, s in wl.param_layout(shape)]
 
@@ -121,7 +122,11 @@ def _torch_model_scores(Pt, X, lengths, cfg):
     F = torch.nn.functional
     E, N, R, K = cfg["d_inner"], cfg["d_state"], cfg["dt_rank"], cfg["d_conv"]
     Bn, L, _ = X.shape
-    h = F.linear(X, Pt["W0"], Pt["b0"])
+    # encoder: Linear layers with a ReLU between consecutive ones
+    enc = [F.linear(X, Pt["W0"], Pt["b0"])]
+    for i in range(1, len(cfg.get("enc_hidden", ())) + 1):
+        enc.append(F.linear(F.relu(enc[-1]), Pt[f"W0_{i}"], Pt[f"b0_{i}"]))
+    h = enc[-1]
     causal = torch.tril(torch.ones(L, L, dtype=torch.float64))
     for l in range(cfg["n_layers"]):
         p = f"blk{l}."
@@ -145,7 +150,10 @@ def _torch_model_scores(Pt, X, lengths, cfg):
     hf = F.rms_norm(h, (cfg["d_model"],), Pt["g_f"], eps=cfg["norm_eps"])
     valid = (torch.arange(L)[None, :] < torch.as_tensor(lengths)[:, None]).double()
     pooled = (hf * valid[..., None]).sum(1) / torch.as_tensor(lengths, dtype=torch.float64)[:, None]
-    return F.linear(F.relu(F.linear(pooled, Pt["W1"], Pt["b1"])), Pt["W2"], Pt["b2"])[:, 0]
+    r1 = F.relu(F.linear(pooled, Pt["W1"], Pt["b1"]))
+    if cfg.get("dec_hidden2", 0):
+        return F.linear(F.relu(F.linear(r1, Pt["W2"], Pt["b2"])), Pt["W3"], Pt["b3"])[:, 0]
+    return F.linear(r1, Pt["W2"], Pt["b2"])[:, 0]
 
 
 def test_forward_and_gradients_match_torch_reexpression():
