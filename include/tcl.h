@@ -37,8 +37,14 @@
  *     W_dt[E,R], b_dt[E], A_log[E,N], D[E], W_out[d,E],
  *   g_f[d], W1[h,d], b1[h], W2[1,h], b2[1]
  * with d = d_model, E = d_inner, N = d_state, K = d_conv, R = dt_rank,
- * h = head_hidden. The model it defines:
+ * h = head_hidden. A multi-layer encoder (enc_hidden) replaces W0, b0 by
+ * W0[e1,F], b0[e1], W0_1[e2,e1], b0_1[e2], W0_2[d,e2], b0_2[d] (or W0[e1,F],
+ * b0[e1], W0_1[d,e1], b0_1[d] with one hidden width); a three-layer decoder
+ * (dec_hidden2 = h2) replaces W2, b2 by W2[h2,h], b2[h2], W3[1,h2], b3[1].
+ * The model it defines:
  *   h0   = X W0^T + b0                                   (encoder)
+ *          (multi-layer: ReLU between consecutive Linear layers, none
+ *          after the last)
  *   per block: n = RMSNorm(h; g), [x|z] = n W_in^T,
  *     u = SiLU(conv_b + causal depthwise conv_K(x; conv_w)),
  *     [dt_r|B|C] = u W_x^T, dt = softplus(dt_r W_dt^T + b_dt),
@@ -46,6 +52,7 @@
  *       s_t = exp(dt_t A) s_{t-1} + dt_t u_t B_t,  y_t = C_t.s_t + D u_t,
  *     h = h + (y * SiLU(z)) W_out^T
  *   score = W2 ReLU(W1 pool(RMSNorm(h; g_f)) + b1) + b2
+ *          (three-layer decoder: W3 ReLU(W2 ReLU(W1 p + b1) + b2) + b3)
  * where pool is the mean over each program's valid tokens. RMSNorm uses
  * norm_eps; the conv has K-1 zeros on the left of each program and its last
  * tap multiplies the current token.
@@ -92,9 +99,15 @@ typedef enum tcl_f32_matmul {
 
 /* Model hyper-parameters (section 5.2; the hyper-parameter study of
  * section 7.2.1 names d_state, d_conv, expand and n_layers).
- * Supported: F % 4 == 0, d_model in {64, 128, 256}, d_inner % 64 == 0 and
- * <= 2048, d_state == 16, d_conv in [1, 4], dt_rank % 4 == 0 and <= 32,
- * head_hidden % 64 == 0 and <= 256, n_layers in [1, 16]. */
+ * Supported: F in [1, 1024], d_model in {64, 128, 256}, d_inner % 64 == 0
+ * and <= 2048, d_state 16 (dt_rank % 4 == 0 and <= 32) or 8 (dt_rank 4, 8
+ * or 16), d_conv in [1, 4], head_hidden % 64 == 0 and <= 256, n_layers in
+ * [1, 16]. The paper's own form (section 5.2: encoder widths 64, 128, 128,
+ * decoder widths 64, 32, 1) is enc_hidden = {64, 128}, dec_hidden2 = 32:
+ * enc_hidden entries % 4 == 0 and <= 512 (fp32 models only; {0, 0} is the
+ * one-Linear encoder, {e1, 0} one hidden layer), dec_hidden2 in [0, 256].
+ * A zero-initialised tail of the struct gives the one-Linear encoder and
+ * the two-layer decoder. */
 typedef struct tcl_config {
   int32_t F;           /* features per token                        */
   int32_t d_model;     /* residual width d                          */
@@ -108,6 +121,8 @@ typedef struct tcl_config {
   float norm_eps;      /* RMSNorm epsilon                           */
   int32_t dtype;       /* tcl_dtype                                 */
   int32_t f32_matmul;  /* tcl_f32_matmul (ignored for bf16 models)  */
+  int32_t enc_hidden[2]; /* hidden widths of a multi-layer encoder  */
+  int32_t dec_hidden2;   /* second hidden width of the decoder (0: none) */
 } tcl_config;
 
 typedef struct tcl_model tcl_model;     /* opaque, library-owned */
@@ -261,6 +276,23 @@ TCL_API tcl_status tcl_lambdarank(int32_t B, const float* d_scores, const float*
  * Stream-ordered; no workspace. */
 TCL_API tcl_status tcl_topk(int32_t n_seg, const int32_t* d_seg_offsets, const float* d_scores, int32_t K,
                             int32_t* d_out, void* stream);
+
+/* The Top-k score of Eq. (12) (section 7.1.2), the paper's dataset-level
+ * measure of a cost model: segment g is the candidate set of one subgraph
+ * (of one network), as in tcl_topk; d_latency [N] fp32 holds every
+ * candidate's measured latency, d_weight [n_seg] fp32 each subgraph's
+ * occurrence count in its network, d_scores [N] the model's predictions
+ * (ranked as in tcl_topk: higher first, ties by index, NaN last).
+ *   Top-k = sum_g w_g min_latency_g / sum_g w_g min(latency of g's k best-
+ *   ranked candidates), empty segments adding nothing.
+ * d_out [3] fp64 receives Top-k, the numerator and the denominator (sums
+ * accumulated in fp64 in a fixed order: deterministic). k in [1, 1024].
+ * d_workspace >= tcl_topk_score_workspace_bytes(n_seg, k) bytes, 256-byte
+ * aligned. Stream-ordered. */
+TCL_API size_t tcl_topk_score_workspace_bytes(int32_t n_seg, int32_t k);
+TCL_API tcl_status tcl_topk_score(int32_t n_seg, const int32_t* d_seg_offsets, const float* d_scores,
+                                  const float* d_latency, const float* d_weight, int32_t k, double* d_out,
+                                  void* d_workspace, size_t ws_bytes, void* stream);
 
 /* The RDU sampler's selection of programs to label, one step of section 4's
  * Alg. 1 on a pool of N scored programs:

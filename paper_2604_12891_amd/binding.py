@@ -33,7 +33,8 @@ class Config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("F", "d_model", "d_inner", "d_state", "d_conv", "dt_rank", "n_layers", "head_hidden",
                  "final_norm")] + [("norm_eps", ctypes.c_float), ("dtype", ctypes.c_int32),
-                                   ("f32_matmul", ctypes.c_int32)]
+                                   ("f32_matmul", ctypes.c_int32), ("enc_hidden", ctypes.c_int32 * 2),
+                                   ("dec_hidden2", ctypes.c_int32)]
 
 
 class KDLoss(ctypes.Structure):
@@ -66,6 +67,8 @@ _SIGS = {
     "tcl_distill_step_kd": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, ctypes.POINTER(KDLoss), _vp, _vp, _sz, _vp]),
     "tcl_lambdarank_workspace_bytes": (_sz, [_i32]),
     "tcl_topk": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp]),
+    "tcl_topk_score_workspace_bytes": (_sz, [_i32, _i32]),
+    "tcl_topk_score": (_i32, [_i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "tcl_rdu_workspace_bytes": (_sz, [_i32, _i32]),
     "tcl_rdu_select": (_i32, [_i32, _vp, _vp, _i32, _vp, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "tcl_lambdarank": (_i32, [_i32, _vp, _vp, ctypes.c_float, _vp, _vp, _vp, _sz, _vp]),
@@ -107,16 +110,20 @@ def check(status: int):
 
 
 def make_config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden,
-                final_norm=1, norm_eps=1e-5, dtype="f32", f32_matmul="split") -> Config:
+                final_norm=1, norm_eps=1e-5, dtype="f32", f32_matmul="split", enc_hidden=(), dec_hidden2=0) -> Config:
     """f32_matmul ("split" or "native") selects how an fp32 model runs its
-    dense projections (tcl_f32_matmul)."""
+    dense projections (tcl_f32_matmul); enc_hidden (up to two widths) and
+    dec_hidden2 select the multi-layer encoder and three-layer decoder."""
+    enc = list(enc_hidden) + [0] * (2 - len(enc_hidden))
     return Config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden, final_norm,
-                  norm_eps, TCL_BF16 if dtype == "bf16" else TCL_F32, F32_MATMUL[f32_matmul])
+                  norm_eps, TCL_BF16 if dtype == "bf16" else TCL_F32, F32_MATMUL[f32_matmul],
+                  (ctypes.c_int32 * 2)(*enc), dec_hidden2)
 
 
 def config_from_shape(shape, dtype="f32", f32_matmul="split") -> Config:
     return make_config(shape.F, shape.d_model, shape.d_inner, shape.d_state, shape.d_conv, shape.dt_rank,
-                       shape.n_layers, shape.head_hidden, shape.final_norm, shape.norm_eps, dtype, f32_matmul)
+                       shape.n_layers, shape.head_hidden, shape.final_norm, shape.norm_eps, dtype, f32_matmul,
+                       tuple(getattr(shape, "enc_hidden", ())), getattr(shape, "dec_hidden2", 0))
 
 
 def _ptr(t) -> Optional[int]:
@@ -308,6 +315,20 @@ def topk(scores, seg_offsets, K, stream=None):
     n_seg = seg_offsets.numel() - 1
     out = torch.empty(n_seg, K, dtype=torch.int32, device=scores.device)
     check(lib().tcl_topk(n_seg, seg_offsets.data_ptr(), scores.data_ptr(), K, out.data_ptr(), _stream(stream)))
+    return out
+
+
+def topk_score(scores, latency, weight, seg_offsets, k, stream=None):
+    """The Top-k score of Eq. (12) (tcl_topk_score): scores and latency fp32
+    [n], weight fp32 [n_seg], seg_offsets int32 [n_seg + 1] (device).
+    Returns a device fp64 tensor [3]: Top-k, numerator, denominator."""
+    import torch
+    n_seg = seg_offsets.numel() - 1
+    out = torch.empty(3, dtype=torch.float64, device=scores.device)
+    need = lib().tcl_topk_score_workspace_bytes(n_seg, k)
+    ws = torch.empty(max(need, 256), dtype=torch.uint8, device=scores.device)
+    check(lib().tcl_topk_score(n_seg, seg_offsets.data_ptr(), scores.data_ptr(), latency.data_ptr(),
+                               weight.data_ptr(), k, out.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)))
     return out
 
 

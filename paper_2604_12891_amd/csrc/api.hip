@@ -74,8 +74,16 @@ BlobLayout blob_layout(const tcl_config& c) {
   const size_t d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank;
   const size_t F = c.F, h = c.head_hidden;
   size_t o = 0;
-  bl.W0 = o; o += d * F;
-  bl.b0 = o; o += d;
+  bl.enc_dims[0] = (int)F;
+  bl.n_enc = 1;
+  for (int i = 0; i < 2 && c.enc_hidden[i] > 0; ++i) bl.enc_dims[bl.n_enc++] = c.enc_hidden[i];
+  bl.enc_dims[bl.n_enc] = (int)d;
+  for (int i = 0; i < bl.n_enc; ++i) {
+    bl.We[i] = o; o += (size_t)bl.enc_dims[i + 1] * bl.enc_dims[i];
+    bl.be[i] = o; o += bl.enc_dims[i + 1];
+  }
+  bl.W0 = bl.We[0];
+  bl.b0 = bl.be[0];
   for (int l = 0; l < c.n_layers; ++l) {
     BlobLayout::L L;
     L.g = o; o += d;
@@ -90,11 +98,19 @@ BlobLayout blob_layout(const tcl_config& c) {
     L.W_out = o; o += d * E;
     bl.layers.push_back(L);
   }
+  const size_t h2 = c.dec_hidden2 > 0 ? c.dec_hidden2 : 0;
   bl.g_f = o; o += d;
   bl.W1 = o; o += h * d;
   bl.b1 = o; o += h;
-  bl.W2 = o; o += h;
-  bl.b2 = o; o += 1;
+  if (h2) {
+    bl.W2 = o; o += h2 * h;
+    bl.b2 = o; o += h2;
+    bl.W3 = o; o += h2;
+    bl.b3 = o; o += 1;
+  } else {
+    bl.W2 = o; o += h;
+    bl.b2 = o; o += 1;
+  }
   bl.total = o;
   return bl;
 }
@@ -110,6 +126,10 @@ ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L) {
   p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * act);
   p.u = o; o = align256(o + (size_t)rows * c.d_inner * act);
   p.xdbl = o; o = align256(o + (size_t)rows * XW * 4);
+  // F not a multiple of 4: the features are copied with rows padded to 4
+  p.feats = o; if (c.F % 4) o = align256(o + (size_t)rows * ((c.F + 3) & ~3) * 4);
+  p.enc1 = o; if (c.enc_hidden[0] > 0) o = align256(o + (size_t)rows * c.enc_hidden[0] * 4);
+  p.enc2 = o; if (c.enc_hidden[1] > 0) o = align256(o + (size_t)rows * c.enc_hidden[1] * 4);
   p.total = o;
   return p;
 }
@@ -133,20 +153,46 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
   Timing& T = m->timing;
 
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  // features whose row length is not a multiple of 4 are first copied into
+  // rows padded with zeros (the input Linear reads 16-byte vectors)
+  const float* feats = d_feats;
+  const int ldf = (c.F + 3) & ~3;
+  if (ldf != c.F) {
+    float* fp = reinterpret_cast<float*>(ws + p.feats);
+    TCL_LAUNCH(T, "pad_features", launch_pad_rows(d_feats, (int64_t)B * L, c.F, ldf, fp, s));
+    feats = fp;
+  }
   if (c.dtype == TCL_F32) {
     float* xz = reinterpret_cast<float*>(ws + p.xz);
     float* u = reinterpret_cast<float*>(ws + p.u);
-    GemmArgs g;
-    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
-    g.W = m->W0; g.ldw = c.F; g.bias = m->b0; g.C = H; g.ldc = d;
-    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
     // the split path where it has a kernel for the shape, the fp32 MFMA path otherwise
     auto gemm = [&](const GemmArgs& a, const uint16_t* Ws, int ldws, int flags) {
       if (m->split && Ws && gemm_split_variant(a, flags) > 0)
         return launch_gemm_split(a, Ws, ldws, flags, -1, s);
       return launch_gemm_f32(a, flags, -1, s);
     };
+    // encoder: the gathered input Linear, then (multi-layer encoder) the
+    // hidden Linear layers on the packed rows, a ReLU after every layer but
+    // the last
+    const int e1 = c.enc_hidden[0], e2 = c.enc_hidden[1];
+    const int n_enc = e1 > 0 ? (e2 > 0 ? 3 : 2) : 1;
+    const int dims[4] = {ldf, e1, n_enc == 3 ? e2 : d, d};
+    float* bufs[2] = {reinterpret_cast<float*>(ws + p.enc1), reinterpret_cast<float*>(ws + p.enc2)};
+    GemmArgs g;
+    g.A = feats; g.lda = ldf; g.offs = offs; g.B = B; g.L = L;
+    g.W = m->W0; g.ldw = m->ldw0; g.bias = m->b0; g.C = n_enc > 1 ? bufs[0] : H;
+    g.ldc = n_enc > 1 ? e1 : d; g.Mdev = offs + B; g.Mmax = Mmax; g.N = n_enc > 1 ? e1 : d; g.K = ldf;
+    g.relu = n_enc > 1;
     TCL_LAUNCH(T, "gemm_input", gemm(g, m->W0_s, m->ldw0_h, kBias | kGather));
+    for (int i = 1; i < n_enc; ++i) {
+      const int in = dims[i], out = dims[i + 1];
+      const bool last = i == n_enc - 1;
+      GemmArgs ge;
+      ge.A = bufs[i - 1]; ge.lda = in; ge.W = m->We[i]; ge.ldw = in; ge.bias = m->be[i];
+      ge.C = last ? H : bufs[i]; ge.ldc = out; ge.Mdev = offs + B; ge.Mmax = Mmax; ge.N = out; ge.K = in;
+      ge.relu = !last;
+      TCL_LAUNCH(T, "gemm_encoder", gemm(ge, m->We_s[i], (in + 7) & ~7, kBias));
+    }
 
     for (int l = 0; l < c.n_layers; ++l) {
       const auto& W = m->layers[l];
@@ -178,9 +224,9 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
     uint16_t* u = reinterpret_cast<uint16_t*>(ws + p.u);
     GemmArgsBF16 g;
-    g.A = d_feats; g.lda = c.F; g.offs = offs; g.B = B; g.L = L;
+    g.A = feats; g.lda = ldf; g.offs = offs; g.B = B; g.L = L;
     g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
-    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = c.F;
+    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = ldf;
     TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
 
     for (int l = 0; l < c.n_layers; ++l) {
@@ -210,9 +256,14 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, -1, s));
     }
   }
-  TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
-                                        c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2, m->b2,
-                                        d_scores, s));
+  if (c.dec_hidden2 > 0)
+    TCL_LAUNCH(T, "tail", launch_tail3_f32(B, L, d, c.head_hidden, c.dec_hidden2, offs, d_lengths, H, m->g_f,
+                                           c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2T, m->b2, m->W3,
+                                           m->b3, d_scores, s));
+  else
+    TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
+                                          c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2, m->b2,
+                                          d_scores, s));
   return TCL_OK;
 }
 
@@ -225,15 +276,27 @@ tcl_status check_config(const tcl_config* c) {
     return fail(TCL_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
   if (c->f32_matmul != TCL_F32_MATMUL_SPLIT && c->f32_matmul != TCL_F32_MATMUL_NATIVE)
     return fail(TCL_ERR_INVALID_ARG, "unknown f32_matmul %d", c->f32_matmul);
-  if (c->F % 4) return fail(TCL_ERR_UNSUPPORTED, "F must be a multiple of 4 (got %d)", c->F);
+  if (c->F > 1024) return fail(TCL_ERR_UNSUPPORTED, "F must be <= 1024 (got %d)", c->F);
   if (c->d_model != 64 && c->d_model != 128 && c->d_model != 256)
     return fail(TCL_ERR_UNSUPPORTED, "d_model must be 64, 128 or 256 (got %d)", c->d_model);
   if (c->d_inner % 64 || c->d_inner > 2048)
     return fail(TCL_ERR_UNSUPPORTED, "d_inner must be a multiple of 64, <= 2048 (got %d)", c->d_inner);
-  if (c->d_state != 16) return fail(TCL_ERR_UNSUPPORTED, "d_state must be 16 (got %d)", c->d_state);
+  if (c->d_state != 16 && c->d_state != 8)
+    return fail(TCL_ERR_UNSUPPORTED, "d_state must be 16 or 8 (got %d)", c->d_state);
   if (c->d_conv > 4) return fail(TCL_ERR_UNSUPPORTED, "d_conv must be <= 4 (got %d)", c->d_conv);
-  if (c->dt_rank % 4 || c->dt_rank > 32)
+  if (c->d_state == 16 && (c->dt_rank % 4 || c->dt_rank > 32))
     return fail(TCL_ERR_UNSUPPORTED, "dt_rank must be a multiple of 4, <= 32 (got %d)", c->dt_rank);
+  if (c->d_state == 8 && c->dt_rank != 4 && c->dt_rank != 8 && c->dt_rank != 16)
+    return fail(TCL_ERR_UNSUPPORTED, "with d_state 8, dt_rank must be 4, 8 or 16 (got %d)", c->dt_rank);
+  const int e1 = c->enc_hidden[0], e2 = c->enc_hidden[1];
+  if (e1 < 0 || e2 < 0 || (e1 == 0 && e2 != 0))
+    return fail(TCL_ERR_INVALID_ARG, "enc_hidden must be {0, 0}, {e1, 0} or {e1, e2} with e1, e2 > 0");
+  if (e1 > 0 && c->dtype != TCL_F32)
+    return fail(TCL_ERR_UNSUPPORTED, "a multi-layer encoder needs an fp32 model");
+  if (e1 % 4 || e2 % 4 || e1 > 512 || e2 > 512)
+    return fail(TCL_ERR_UNSUPPORTED, "enc_hidden widths must be multiples of 4, <= 512 (got %d, %d)", e1, e2);
+  if (c->dec_hidden2 < 0 || c->dec_hidden2 > 256)
+    return fail(TCL_ERR_UNSUPPORTED, "dec_hidden2 must be in [0, 256] (got %d)", c->dec_hidden2);
   if (c->head_hidden % 64 || c->head_hidden > 256)
     return fail(TCL_ERR_UNSUPPORTED, "head_hidden must be a multiple of 64, <= 256 (got %d)",
                 c->head_hidden);
@@ -254,6 +317,8 @@ struct ModelPlan {
   int64_t total = 0;
   size_t bytes = 0, master = 0, jobtab = 0;
   size_t W0 = 0, b0 = 0, W0_h = 0, W0_s = 0, g_f = 0, W1 = 0, W1T = 0, b1 = 0, W2 = 0, b2 = 0;
+  size_t We[3] = {0, 0, 0}, be[3] = {0, 0, 0}, We_s[3] = {0, 0, 0}, W2T = 0, W3 = 0, b3 = 0;
+  int ldw0 = 0;
   struct L {
     size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
     size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_out_s;
@@ -280,6 +345,7 @@ ModelPlan plan_model(const tcl_config& c) {
   const int d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank, XW = R + 2 * N;
   const int F = c.F, h = c.head_hidden;
   P.ldw0_h = (F + 7) & ~7;
+  P.ldw0 = (F + 3) & ~3;
   size_t o = 0;
   auto job = [&](size_t src, int rows, int cols, int kind, int transpose, int elem_bytes, int ld = -1,
                  size_t src2 = 0) {
@@ -302,10 +368,19 @@ ModelPlan plan_model(const tcl_config& c) {
     P.total += (int64_t)rows * cols;
     return dst;
   };
-  P.W0 = job(bl.W0, d, F, kDeriveF32, 0, 4);
-  P.b0 = job(bl.b0, 1, d, kDeriveF32, 0, 4);
-  if (bf) P.W0_h = job(bl.W0, d, F, kDeriveBF16, 0, 2, P.ldw0_h);
-  if (sp) P.W0_s = job(bl.W0, d, F, kDeriveSplit, 0, 2, P.ldw0_h);
+  // the encoder's first Linear, K zero-padded; then the hidden layers of a
+  // multi-layer encoder
+  const int e0 = bl.enc_dims[1];
+  P.W0 = job(bl.W0, e0, F, kDeriveF32, 0, 4, P.ldw0);
+  P.b0 = job(bl.b0, 1, e0, kDeriveF32, 0, 4);
+  if (bf) P.W0_h = job(bl.W0, e0, F, kDeriveBF16, 0, 2, P.ldw0_h);
+  if (sp) P.W0_s = job(bl.W0, e0, F, kDeriveSplit, 0, 2, P.ldw0_h);
+  for (int i = 1; i < bl.n_enc; ++i) {
+    const int in = bl.enc_dims[i], out = bl.enc_dims[i + 1];
+    P.We[i] = job(bl.We[i], out, in, kDeriveF32, 0, 4);
+    P.be[i] = job(bl.be[i], 1, out, kDeriveF32, 0, 4);
+    if (sp) P.We_s[i] = job(bl.We[i], out, in, kDeriveSplit, 0, 2, (in + 7) & ~7);
+  }
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& B = bl.layers[l];
     ModelPlan::L L{};
@@ -338,8 +413,16 @@ ModelPlan plan_model(const tcl_config& c) {
   P.W1 = job(bl.W1, h, d, kDeriveF32, 0, 4);
   P.W1T = job(bl.W1, h, d, kDeriveF32, 1, 4);
   P.b1 = job(bl.b1, 1, h, kDeriveF32, 0, 4);
-  P.W2 = job(bl.W2, 1, h, kDeriveF32, 0, 4);
-  P.b2 = job(bl.b2, 1, 1, kDeriveF32, 0, 4);
+  if (c.dec_hidden2 > 0) {
+    const int h2 = c.dec_hidden2;
+    P.W2T = job(bl.W2, h2, h, kDeriveF32, 1, 4);
+    P.b2 = job(bl.b2, 1, h2, kDeriveF32, 0, 4);
+    P.W3 = job(bl.W3, 1, h2, kDeriveF32, 0, 4);
+    P.b3 = job(bl.b3, 1, 1, kDeriveF32, 0, 4);
+  } else {
+    P.W2 = job(bl.W2, 1, h, kDeriveF32, 0, 4);
+    P.b2 = job(bl.b2, 1, 1, kDeriveF32, 0, 4);
+  }
   P.master = o;
   o = align256(o + bl.total * 4);
   P.jobtab = o;
@@ -402,6 +485,7 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
   m->b0 = F32(P.b0);
   m->W0_h = bf ? B16(P.W0_h) : nullptr;
   m->ldw0_h = P.ldw0_h;
+  m->ldw0 = P.ldw0;
   m->split = uses_split(*cfg);
   m->W0_s = m->split ? B16(P.W0_s) : nullptr;
   for (const auto& L : P.layers) {
@@ -435,8 +519,22 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
   m->W1 = F32(P.W1);
   m->W1T = F32(P.W1T);
   m->b1 = F32(P.b1);
-  m->W2 = F32(P.W2);
   m->b2 = F32(P.b2);
+  if (cfg->dec_hidden2 > 0) {
+    m->W2T = F32(P.W2T);
+    m->W3 = F32(P.W3);
+    m->b3 = F32(P.b3);
+  } else {
+    m->W2 = F32(P.W2);
+  }
+  {
+    const BlobLayout bl = blob_layout(*cfg);
+    for (int i = 1; i < bl.n_enc; ++i) {
+      m->We[i] = F32(P.We[i]);
+      m->be[i] = F32(P.be[i]);
+      if (m->split) m->We_s[i] = B16(P.We_s[i]);
+    }
+  }
   auto cleanup = [&](tcl_status s2) {
     (void)hipFree(m->dev);
     delete m;
@@ -541,6 +639,26 @@ TCL_API tcl_status tcl_topk(int32_t n_seg, const int32_t* d_seg_offsets, const f
   if (K < 1 || K > 1024) return fail(TCL_ERR_UNSUPPORTED, "K must be in [1, 1024] (got %d)", K);
   if (!d_seg_offsets || !d_scores || !d_out) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
   TCL_HIP(launch_topk(n_seg, d_seg_offsets, d_scores, K, d_out, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
+TCL_API size_t tcl_topk_score_workspace_bytes(int32_t n_seg, int32_t k) {
+  if (n_seg <= 0 || k < 1 || k > 1024) return 0;
+  return topk_score_workspace_bytes(n_seg, k);
+}
+
+TCL_API tcl_status tcl_topk_score(int32_t n_seg, const int32_t* d_seg_offsets, const float* d_scores,
+                                  const float* d_latency, const float* d_weight, int32_t k, double* d_out,
+                                  void* d_workspace, size_t ws_bytes, void* stream) {
+  if (n_seg <= 0) return fail(TCL_ERR_INVALID_ARG, "n_seg must be positive");
+  if (k < 1 || k > 1024) return fail(TCL_ERR_UNSUPPORTED, "k must be in [1, 1024] (got %d)", k);
+  if (!d_seg_offsets || !d_scores || !d_latency || !d_weight || !d_out || !d_workspace)
+    return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_workspace) % 256) return fail(TCL_ERR_INVALID_ARG, "d_workspace must be 256-byte aligned");
+  const size_t need = topk_score_workspace_bytes(n_seg, k);
+  if (ws_bytes < need) return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  TCL_HIP(launch_topk_score(n_seg, d_seg_offsets, d_scores, d_latency, d_weight, k, d_out, d_workspace,
+                            static_cast<hipStream_t>(stream)));
   return TCL_OK;
 }
 

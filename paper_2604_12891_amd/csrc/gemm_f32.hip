@@ -201,6 +201,7 @@ __global__ __launch_bounds__(WM* WN * 64, BK == 32 ? 3 : 2) void gemm_f32_kernel
         if constexpr (kNorm) v *= sR[rl];
         v += bias;
         if constexpr ((FL & kResid) != 0) v += res[r];
+        if (p.relu) v = fmaxf(v, 0.f);
         p.C[(int64_t)row * p.ldc + col] = v;
       }
     }

@@ -163,6 +163,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_f32_panel_kernel(GemmArgs
       float v = acc[r];
       if constexpr (kNorm) v *= sR[wave][rl];
       v += bias;
+      if (p.relu) v = fmaxf(v, 0.f);
       // rows past M fall outside cres
       const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
@@ -280,7 +281,8 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_f32_panel16_kernel(GemmAr
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float v = acc[r] + bias + res[r];
+      float v = acc[r] + bias + res[r];
+      if (p.relu) v = fmaxf(v, 0.f);
       const uint32_t off = cok ? (uint32_t)(((wave * 16 + 4 * lq + r) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
     }

@@ -246,6 +246,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p
       float v = acc[r] + acc2[r];
       if constexpr (kNorm) v *= sR[wave][rl];
       v += bias;
+      if (p.relu) v = fmaxf(v, 0.f);
       // rows past M fall outside cres
       const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
@@ -353,7 +354,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split16_kernel(GemmArgs p
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float v = (acc[r] + acc2[r]) + bias + res[r];
+      float v = (acc[r] + acc2[r]) + bias + res[r];
+      if (p.relu) v = fmaxf(v, 0.f);
       const uint32_t off = cok ? (uint32_t)(((wave * 16 + 4 * lq + r) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
     }
@@ -472,7 +474,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
-      const float v = acc[nb][r] + bias + res[r];
+      float v = acc[nb][r] + bias + res[r];
+      if (p.relu) v = fmaxf(v, 0.f);
       const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
     }

@@ -32,6 +32,7 @@ struct GemmArgs {
   int Mmax = 0;               // upper bound on the row count (grid size)
   int N = 0, K = 0;
   float eps = 0.f;
+  int relu = 0;               // nonzero: C = max(result, 0) (after bias and residual)
 };
 
 // Tile shapes (rows x columns of C per workgroup, 4 or 8 wavefronts, K staged
@@ -196,6 +197,15 @@ hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const in
                            const float* W1T, const float* b1, const float* W2, const float* b2,
                            float* scores, hipStream_t s, float* pooled_out = nullptr,
                            float* a1_out = nullptr);
+// The same with a three-layer decoder Linear(d,h) ReLU Linear(h,h2) ReLU
+// Linear(h2,1): W2T is the second layer transposed, [h][h2], b2 its bias
+// [h2], W3 [h2] and b3 [1] the output layer. h, h2 <= 256.
+// dst[r][c] = c < F ? src[r][c] : 0 for rows x ld (row-major, src rows of F)
+hipError_t launch_pad_rows(const float* src, int64_t rows, int F, int ld, float* dst, hipStream_t s);
+hipError_t launch_tail3_f32(int B, int L, int d, int h, int h2, const int* offs, const int* lengths,
+                            const float* H, const float* g_f, int final_norm, float eps,
+                            const float* W1T, const float* b1, const float* W2T, const float* b2,
+                            const float* W3, const float* b3, float* scores, hipStream_t s);
 
 // ---------------------------------------------------------------- distillation step
 // Reductions of per-block partials: dst[i * dst_stride] =
@@ -256,6 +266,11 @@ hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, 
 // scores (best first, equal scores in index order, NaN last), -1 past a
 // segment's end. offs [n_seg + 1]. K in [1, 1024].
 hipError_t launch_topk(int n_seg, const int* offs, const float* s, int K, int* out, hipStream_t st);
+// Eq. (12): out[0..2] = Top-k, numerator, denominator (fp64). ws holds
+// topk_score_workspace_bytes(n_seg, k) bytes, 256-byte aligned.
+size_t topk_score_workspace_bytes(int n_seg, int k);
+hipError_t launch_topk_score(int n_seg, const int* offs, const float* s, const float* lat, const float* w,
+                             int k, double* out, void* ws, hipStream_t st);
 // RDU selection (Alg. 1, Eq. (1)-(3)) of up to n_select programs from a pool
 // of N: out [n_select] in selection order (-1 past the end), count [1].
 // op [N] in [0, n_ops) (others are never selected), n_ops <= 4096;

@@ -28,6 +28,12 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // Offsets (in floats) of every tensor of the canonical parameter blob.
 struct BlobLayout {
   size_t W0, b0, g_f, W1, b1, W2, b2, total;
+  // multi-layer encoder: layers 1 and 2 after W0, b0 (n_enc Linear layers in
+  // all); three-layer decoder: W3, b3 after W2 [h2,h], b2 [h2]
+  int n_enc = 1;
+  int enc_dims[4] = {0, 0, 0, 0};  // F, hidden widths, d_model
+  size_t We[3] = {0, 0, 0}, be[3] = {0, 0, 0};
+  size_t W3 = 0, b3 = 0;
   struct L {
     size_t g, W_in, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
   };
@@ -97,6 +103,13 @@ struct tcl_model {
   };
   float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1 = nullptr, *W1T = nullptr,
         *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;
+  int ldw0 = 0;  // leading dimension of the fp32 W0: F rounded up to 4, zero-padded
+  // encoder layers 1.. of a multi-layer encoder (fp32 [out][in], bias, and
+  // the three-way split [3][out][ld] on the split path, ld = in rounded to 8)
+  float *We[3] = {nullptr, nullptr, nullptr}, *be[3] = {nullptr, nullptr, nullptr};
+  uint16_t* We_s[3] = {nullptr, nullptr, nullptr};
+  // three-layer decoder: W2 transposed [h][h2], W3 [h2], b3 [1]
+  float *W2T = nullptr, *W3 = nullptr, *b3 = nullptr;
   uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
   int ldw0_h = 0;
   uint16_t* W0_s = nullptr;  // three-way bf16 split of W0, [3][d][ldw0_h] (split path)
@@ -109,7 +122,7 @@ namespace tcl {
 
 // Workspace plan of one scoring call (byte offsets, 256-aligned).
 struct ScorePlan {
-  size_t offs, H, xz, u, xdbl, total;
+  size_t offs, H, xz, u, xdbl, feats, enc1, enc2, total;
 };
 ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L);
 

@@ -502,7 +502,91 @@ constexpr int kRduGrid = 1024;  // blocks of the grid passes (grid-stride)
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// ---------------------------------------------------------------- Top-k score (Eq. (12))
+// One workgroup per segment: the lowest latency of the segment and the
+// lowest among its k best-ranked candidates (indices from topk_kernel), each
+// times the segment's weight. fp32 latencies and weights multiply exactly in
+// fp64. An empty segment contributes (0, 0).
+__global__ __launch_bounds__(kST) void topk_score_seg_kernel(const int* __restrict__ offs, int k,
+                                                             const int* __restrict__ top,
+                                                             const float* __restrict__ lat,
+                                                             const float* __restrict__ w,
+                                                             double* __restrict__ part) {
+  __shared__ float sA[kST / 64], sB[kST / 64];
+  const int g = blockIdx.x, tid = threadIdx.x;
+  const int lo = offs[g], hi = offs[g + 1];
+  float mAll = __builtin_inff(), mTop = __builtin_inff();
+  for (int i = lo + tid; i < hi; i += kST) mAll = fminf(mAll, lat[i]);
+  for (int j = tid; j < k; j += kST) {
+    const int i = top[(int64_t)g * k + j];
+    if (i >= 0) mTop = fminf(mTop, lat[i]);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    mAll = fminf(mAll, __shfl_xor(mAll, o));
+    mTop = fminf(mTop, __shfl_xor(mTop, o));
+  }
+  if ((tid & 63) == 0) {
+    sA[tid >> 6] = mAll;
+    sB[tid >> 6] = mTop;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float a = sA[0], b = sB[0];
+    for (int v = 1; v < kST / 64; ++v) {
+      a = fminf(a, sA[v]);
+      b = fminf(b, sB[v]);
+    }
+    const bool empty = hi <= lo;
+    part[2 * g] = empty ? 0.0 : (double)w[g] * (double)a;
+    part[2 * g + 1] = empty ? 0.0 : (double)w[g] * (double)b;
+  }
+}
+
+// One workgroup: both sums over the segments in a fixed order (a strided
+// serial pass per thread, then a fixed tree), so the result is deterministic.
+__global__ __launch_bounds__(1024) void topk_score_sum_kernel(int n_seg, const double* __restrict__ part,
+                                                              double* __restrict__ out) {
+  __shared__ double sN[1024], sD[1024];
+  const int tid = threadIdx.x;
+  double n = 0.0, d = 0.0;
+  for (int g = tid; g < n_seg; g += 1024) {
+    n += part[2 * g];
+    d += part[2 * g + 1];
+  }
+  sN[tid] = n;
+  sD[tid] = d;
+  __syncthreads();
+  for (int o = 512; o > 0; o >>= 1) {
+    if (tid < o) {
+      sN[tid] += sN[tid + o];
+      sD[tid] += sD[tid + o];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    out[0] = sN[0] / sD[0];
+    out[1] = sN[0];
+    out[2] = sD[0];
+  }
+}
+
 }  // namespace
+
+size_t topk_score_workspace_bytes(int n_seg, int k) {
+  return al256((size_t)n_seg * k * 4) + al256((size_t)n_seg * 2 * 8);
+}
+
+hipError_t launch_topk_score(int n_seg, const int* offs, const float* s, const float* lat, const float* w,
+                             int k, double* out, void* ws, hipStream_t st) {
+  if (n_seg <= 0 || k < 1 || k > 1024) return hipErrorInvalidValue;
+  int* top = static_cast<int*>(ws);
+  double* part = reinterpret_cast<double*>(static_cast<char*>(ws) + al256((size_t)n_seg * k * 4));
+  hipError_t e = launch_topk(n_seg, offs, s, k, top, st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(topk_score_seg_kernel, dim3(n_seg), dim3(kST), 0, st, offs, k, top, lat, w, part);
+  hipLaunchKernelGGL(topk_score_sum_kernel, dim3(1), dim3(1024), 0, st, n_seg, part, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_topk(int n_seg, const int* offs, const float* s, int K, int* out, hipStream_t st) {
   if (n_seg <= 0 || K < 1 || K > 1024) return hipErrorInvalidValue;

@@ -385,8 +385,11 @@ __global__ __launch_bounds__(512) void scan_chunked_kernel(
 // the normalised row). Phase 2: thread j computes hidden unit j of the head
 // for all PB programs (W1 is read once per workgroup, transposed so the
 // reads are coalesced), then the ReLU'd units are dotted with W2 by a
-// block reduction.
-template <int DM, int kTailPB>
+// block reduction. With DEC3 (a three-layer decoder) the ReLU'd units go
+// through LDS to a second hidden layer of h2 units, thread j computing unit
+// j, and those are dotted with W3 (b2 is then the second layer's bias
+// vector, b3 the output bias).
+template <int DM, int kTailPB, bool DEC3>
 __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const int* __restrict__ offs,
                                                    const int* __restrict__ lengths,
                                                    const float* __restrict__ H,
@@ -397,10 +400,13 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
                                                    const float* __restrict__ b2,
                                                    float* __restrict__ scores,
                                                    float* __restrict__ pooled_out,
-                                                   float* __restrict__ a1_out) {
+                                                   float* __restrict__ a1_out, int h2,
+                                                   const float* __restrict__ W3,
+                                                   const float* __restrict__ b3) {
   constexpr int PL = DM / 64;  // values per lane
   __shared__ float sP[DM][kTailPB];
   __shared__ float sRed[4][kTailPB];
+  __shared__ float sH1[DEC3 ? 256 : 1][kTailPB];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b0 = blockIdx.x * kTailPB;
 
@@ -480,13 +486,36 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
 #pragma unroll
       for (int p = 0; p < kTailPB; ++p) a[p] = fmaf(wv, sP[k][p], a[p]);
     }
-    const float w2 = W2[tid];
+    if constexpr (DEC3) {
 #pragma unroll
-    for (int p = 0; p < kTailPB; ++p) part[p] = w2 * fmaxf(a[p], 0.f);
+      for (int p = 0; p < kTailPB; ++p) sH1[tid][p] = fmaxf(a[p], 0.f);
+    } else {
+      const float w2 = W2[tid];
+#pragma unroll
+      for (int p = 0; p < kTailPB; ++p) part[p] = w2 * fmaxf(a[p], 0.f);
+    }
     if (a1_out) {
 #pragma unroll
       for (int p = 0; p < kTailPB; ++p)
         if (b0 + p < B) a1_out[(int64_t)(b0 + p) * h + tid] = a[p];
+    }
+  }
+  if constexpr (DEC3) {
+    // second hidden layer: W2 is passed transposed, [h][h2]
+    __syncthreads();
+    if (tid < h2) {
+      float a[kTailPB];
+      const float bj = b2[tid];
+#pragma unroll
+      for (int p = 0; p < kTailPB; ++p) a[p] = bj;
+      for (int k = 0; k < h; ++k) {
+        const float wv = W2[k * h2 + tid];
+#pragma unroll
+        for (int p = 0; p < kTailPB; ++p) a[p] = fmaf(wv, sH1[k][p], a[p]);
+      }
+      const float w3 = W3[tid];
+#pragma unroll
+      for (int p = 0; p < kTailPB; ++p) part[p] = w3 * fmaxf(a[p], 0.f);
     }
   }
 #pragma unroll
@@ -498,7 +527,7 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
   if (tid < kTailPB) {
     const int b = b0 + tid;
     if (b < B) {
-      const float sc = sRed[0][tid] + sRed[1][tid] + sRed[2][tid] + sRed[3][tid] + b2[0];
+      const float sc = sRed[0][tid] + sRed[1][tid] + sRed[2][tid] + sRed[3][tid] + (DEC3 ? b3[0] : b2[0]);
       const int len = lengths[b];
       scores[b] = (len >= 1 && len <= L) ? sc : __builtin_nanf("");
     }
@@ -506,6 +535,28 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
 }
 
 }  // namespace
+
+namespace {
+
+__global__ __launch_bounds__(256) void pad_rows_kernel(int64_t n, int F, int ld, const float* __restrict__ src,
+                                                       float* __restrict__ dst) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const int64_t r = i / ld;
+    const int c = (int)(i - r * ld);
+    dst[i] = c < F ? src[r * F + c] : 0.f;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pad_rows(const float* src, int64_t rows, int F, int ld, float* dst, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (F <= 0 || ld < F) return hipErrorInvalidValue;
+  const int64_t n = rows * ld;
+  const int grid = (int)std::min<int64_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(pad_rows_kernel, dim3(grid), dim3(256), 0, s, n, F, ld, src, dst);
+  return hipGetLastError();
+}
 
 hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream_t s) {
   hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(1024), 0, s, lengths, B, L, offs);
@@ -535,21 +586,24 @@ hipError_t launch_scan_chunked(int B, int E, int N, int R, int chunks, const int
                                const float* b_dt, const float* A_log, const float* D, T* out,
                                hipStream_t s) {
   if (B <= 0) return hipSuccess;
-  if (N != 16 || chunks < 1 || chunks > 8) return hipErrorInvalidValue;
+  if ((N != 16 && N != 8) || chunks < 1 || chunks > 8) return hipErrorInvalidValue;
   dim3 grid(B, (E + 63) / 64);
   const size_t shm = (size_t)chunks * 64 * 2 * N * sizeof(float);
-#define TCL_SCANC(RR)                                                                          \
-  hipLaunchKernelGGL((scan_chunked_kernel<T, 16, RR>), grid, dim3(64 * chunks), shm, s, offs, E, u, \
+#define TCL_SCANC(NN, RR)                                                                      \
+  hipLaunchKernelGGL((scan_chunked_kernel<T, NN, RR>), grid, dim3(64 * chunks), shm, s, offs, E, u, \
                      xdbl, z, ldz, W_dt, b_dt, A_log, D, out)
-  switch (R) {
-    case 4: TCL_SCANC(4); break;
-    case 8: TCL_SCANC(8); break;
-    case 12: TCL_SCANC(12); break;
-    case 16: TCL_SCANC(16); break;
-    case 20: TCL_SCANC(20); break;
-    case 24: TCL_SCANC(24); break;
-    case 28: TCL_SCANC(28); break;
-    case 32: TCL_SCANC(32); break;
+  switch (N * 100 + R) {
+    case 1604: TCL_SCANC(16, 4); break;
+    case 1608: TCL_SCANC(16, 8); break;
+    case 1612: TCL_SCANC(16, 12); break;
+    case 1616: TCL_SCANC(16, 16); break;
+    case 1620: TCL_SCANC(16, 20); break;
+    case 1624: TCL_SCANC(16, 24); break;
+    case 1628: TCL_SCANC(16, 28); break;
+    case 1632: TCL_SCANC(16, 32); break;
+    case 804: TCL_SCANC(8, 4); break;
+    case 808: TCL_SCANC(8, 8); break;
+    case 816: TCL_SCANC(8, 16); break;
     default: return hipErrorInvalidValue;
   }
 #undef TCL_SCANC
@@ -573,21 +627,24 @@ hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, 
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
                        const float* D, T* out, hipStream_t s, T* ysave) {
   if (B <= 0) return hipSuccess;
-  if (N != 16) return hipErrorInvalidValue;
+  if (N != 16 && N != 8) return hipErrorInvalidValue;
   const int cgroups = (E + kScanThreads - 1) / kScanThreads;
   const int grid = 8 * cgroups * ((B + 7) / 8);
-#define TCL_SCAN(RR)                                                                                    \
-  hipLaunchKernelGGL((scan_kernel<T, 16, RR>), dim3(grid), dim3(kScanThreads), 0, s, B, offs, E, u, xdbl, \
+#define TCL_SCAN(NN, RR)                                                                                \
+  hipLaunchKernelGGL((scan_kernel<T, NN, RR>), dim3(grid), dim3(kScanThreads), 0, s, B, offs, E, u, xdbl, \
                      z, ldz, W_dt, b_dt, A_log, D, out, ysave)
-  switch (R) {
-    case 4: TCL_SCAN(4); break;
-    case 8: TCL_SCAN(8); break;
-    case 12: TCL_SCAN(12); break;
-    case 16: TCL_SCAN(16); break;
-    case 20: TCL_SCAN(20); break;
-    case 24: TCL_SCAN(24); break;
-    case 28: TCL_SCAN(28); break;
-    case 32: TCL_SCAN(32); break;
+  switch (N * 100 + R) {
+    case 1604: TCL_SCAN(16, 4); break;
+    case 1608: TCL_SCAN(16, 8); break;
+    case 1612: TCL_SCAN(16, 12); break;
+    case 1616: TCL_SCAN(16, 16); break;
+    case 1620: TCL_SCAN(16, 20); break;
+    case 1624: TCL_SCAN(16, 24); break;
+    case 1628: TCL_SCAN(16, 28); break;
+    case 1632: TCL_SCAN(16, 32); break;
+    case 804: TCL_SCAN(8, 4); break;
+    case 808: TCL_SCAN(8, 8); break;
+    case 816: TCL_SCAN(8, 16); break;
     default: return hipErrorInvalidValue;
   }
 #undef TCL_SCAN
@@ -614,19 +671,27 @@ template hipError_t launch_scan<uint16_t>(int, int, int, int, const int*, const 
                                           const float*, const float*, const float*, uint16_t*,
                                           hipStream_t, uint16_t*);
 
-hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const int* lengths,
-                           const float* H, const float* g_f, int final_norm, float eps,
-                           const float* W1T, const float* b1, const float* W2, const float* b2,
-                           float* scores, hipStream_t s, float* pooled_out, float* a1_out) {
+namespace {
+
+hipError_t tail_any(int B, int L, int d, int h, const int* offs, const int* lengths, const float* H,
+                    const float* g_f, int final_norm, float eps, const float* W1T, const float* b1,
+                    const float* W2, const float* b2, float* scores, hipStream_t s, float* pooled_out,
+                    float* a1_out, int h2, const float* W3, const float* b3) {
   if (B <= 0) return hipSuccess;
-  if (h > 256) return hipErrorInvalidValue;
+  if (h <= 0 || h > 256 || h2 < 0 || h2 > 256) return hipErrorInvalidValue;
   // 16 programs per workgroup share each W1 read; small batches use 4 so
   // that there are enough workgroups to spread over the CUs
   const int pb = B >= 8192 ? 16 : 4;
   dim3 grid((B + pb - 1) / pb);
-#define TCL_TAIL(DD, PB)                                                                           \
-  hipLaunchKernelGGL((tail_kernel<DD, PB>), grid, dim3(256), 0, s, B, L, h, offs, lengths, H, g_f, \
-                     final_norm, eps, W1T, b1, W2, b2, scores, pooled_out, a1_out)
+  const bool d3 = h2 > 0;
+#define TCL_TAIL(DD, PB)                                                                                  \
+  if (d3)                                                                                                 \
+    hipLaunchKernelGGL((tail_kernel<DD, PB, true>), grid, dim3(256), 0, s, B, L, h, offs, lengths, H, g_f, \
+                       final_norm, eps, W1T, b1, W2, b2, scores, pooled_out, a1_out, h2, W3, b3);         \
+  else                                                                                                    \
+    hipLaunchKernelGGL((tail_kernel<DD, PB, false>), grid, dim3(256), 0, s, B, L, h, offs, lengths, H,    \
+                       g_f, final_norm, eps, W1T, b1, W2, b2, scores, pooled_out, a1_out, 0, nullptr,     \
+                       nullptr)
   switch (d * 100 + pb) {
     case 6416: TCL_TAIL(64, 16); break;
     case 12816: TCL_TAIL(128, 16); break;
@@ -638,6 +703,25 @@ hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const in
   }
 #undef TCL_TAIL
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const int* lengths,
+                           const float* H, const float* g_f, int final_norm, float eps,
+                           const float* W1T, const float* b1, const float* W2, const float* b2,
+                           float* scores, hipStream_t s, float* pooled_out, float* a1_out) {
+  return tail_any(B, L, d, h, offs, lengths, H, g_f, final_norm, eps, W1T, b1, W2, b2, scores, s,
+                  pooled_out, a1_out, 0, nullptr, nullptr);
+}
+
+hipError_t launch_tail3_f32(int B, int L, int d, int h, int h2, const int* offs, const int* lengths,
+                            const float* H, const float* g_f, int final_norm, float eps,
+                            const float* W1T, const float* b1, const float* W2T, const float* b2,
+                            const float* W3, const float* b3, float* scores, hipStream_t s) {
+  if (h2 <= 0) return hipErrorInvalidValue;
+  return tail_any(B, L, d, h, offs, lengths, H, g_f, final_norm, eps, W1T, b1, W2T, b2, scores, s,
+                  nullptr, nullptr, h2, W3, b3);
 }
 
 }  // namespace tcl

@@ -207,6 +207,9 @@ TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, fl
   if (sc.dtype != TCL_BF16) return fail(TCL_ERR_UNSUPPORTED, "the student must be a bf16 model");
   if (sc.F != tc.F) return fail(TCL_ERR_INVALID_ARG, "teacher and student feature widths differ");
   if (sc.d_inner > 256) return fail(TCL_ERR_UNSUPPORTED, "student d_inner must be <= 256");
+  if (sc.d_state != 16 || sc.F % 4 || sc.enc_hidden[0] != 0 || sc.dec_hidden2 != 0)
+    return fail(TCL_ERR_UNSUPPORTED,
+                "the student must have d_state 16, F %% 4 == 0, a one-Linear encoder and a two-layer decoder");
   if (sc.dt_rank != 4 && sc.dt_rank != 8 && sc.dt_rank != 16)
     return fail(TCL_ERR_UNSUPPORTED, "student dt_rank must be 4, 8 or 16");
   if ((size_t)max_L * (sc.dt_rank + 2 * sc.d_state + 16 * sc.d_state) * 4 > 64 * 1024)

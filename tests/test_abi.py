@@ -35,13 +35,13 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) <= set(tb._SIGS)
 
 
-@pytest.mark.parametrize("shape", [wl.TINY, wl.D256, wl.STUDENT])
+@pytest.mark.parametrize("shape", [wl.TINY, wl.D256, wl.STUDENT, wl.PAPER_CPU, wl.PAPER_GPU])
 def test_param_count_matches_oracle_layout(lib, shape):
     cfg = tb.config_from_shape(shape)
     n = lib.tcl_param_count(ctypes.byref(cfg))
     ocfg = dict(F=shape.F, d_model=shape.d_model, d_inner=shape.d_inner, d_state=shape.d_state,
                 d_conv=shape.d_conv, dt_rank=shape.dt_rank, n_layers=shape.n_layers,
-                head_hidden=shape.head_hidden)
+                head_hidden=shape.head_hidden, enc_hidden=shape.enc_hidden, dec_hidden2=shape.dec_hidden2)
     assert n == sum(int(np.prod(s)) for _, s in om.layout(ocfg)) == wl.param_count(shape)
 
 
@@ -62,12 +62,23 @@ def test_create_rejects_bad_arguments(lib):
     assert st == -1
     st, _ = _create(lib, cfg, blob, n=blob.size - 1)
     assert st == -1 and b"needs" in lib.tcl_last_error()
-    for field, value in [("d_state", 8), ("d_model", 96), ("dt_rank", 6), ("head_hidden", 300), ("F", 163),
-                         ("d_conv", 5)]:
+    for field, value in [("d_state", 4), ("d_model", 96), ("dt_rank", 6), ("head_hidden", 300), ("F", 2000),
+                         ("d_conv", 5), ("dec_hidden2", 300)]:
         bad = tb.config_from_shape(wl.TINY)
         setattr(bad, field, value)
         st, _ = _create(lib, bad, np.zeros(lib.tcl_param_count(ctypes.byref(bad)), np.float32))
         assert st == -2, field
+    # the multi-layer encoder: fp32 only, widths multiples of 4, no e2 without e1
+    for shape, dtype, enc, want in [(wl.TINY, "bf16", (64, 128), -2), (wl.TINY, "f32", (62, 0), -2),
+                                    (wl.TINY, "f32", (0, 64), -1)]:
+        bad = tb.config_from_shape(shape, dtype)
+        bad.enc_hidden[0], bad.enc_hidden[1] = enc
+        st, _ = _create(lib, bad, np.zeros(lib.tcl_param_count(ctypes.byref(bad)), np.float32))
+        assert st == want, (dtype, enc)
+    bad = tb.config_from_shape(wl.PAPER_CPU)
+    bad.dt_rank = 12  # d_state 8 takes dt_rank 4, 8 or 16
+    st, _ = _create(lib, bad, np.zeros(lib.tcl_param_count(ctypes.byref(bad)), np.float32))
+    assert st == -2
     bad = tb.config_from_shape(wl.TINY)
     bad.norm_eps = 0.0
     st, _ = _create(lib, bad, blob)
