@@ -7,3 +7,4 @@ from . import model  # noqa: F401
 from . import kd  # noqa: F401
 from . import select  # noqa: F401
 from . import metric  # noqa: F401
+from . import progressive  # noqa: F401

@@ -69,6 +69,7 @@ class Workload:
     dtype: str  # "f32" or "bf16"
     seed_index: int
     student: ModelShape | None = None  # distillation only
+    adapter: int = 0  # progressive KB + AC forward: the lateral adapters' width
 
 
 TINY = ModelShape(d_model=64, d_inner=128, dt_rank=4, n_layers=2, head_hidden=64)
@@ -94,6 +95,9 @@ WORKLOADS: Dict[str, Workload] = {
         # the paper's model on its own input shapes: 26 x 22 (CPU) and 41 x 20 (GPU)
         Workload("paper_B4096_L26_F22_f32", PAPER_CPU, 4096, 26, 5, 26, "f32", 5),
         Workload("paper_B4096_L41_F20_f32", PAPER_GPU, 4096, 41, 8, 41, "f32", 6),
+        # the CKD framework's continual-learning forward: frozen KB and active
+        # column, both the paper's model, joined by lateral adapters of width 8
+        Workload("progressive_B4096_L41_F20_a8_f32", PAPER_GPU, 4096, 41, 8, 41, "f32", 7, adapter=8),
     ]
 }
 WORKLOAD_ORDER = list(WORKLOADS)
@@ -133,6 +137,39 @@ def param_layout(m: ModelShape) -> List[Tuple[str, Tuple[int, ...]]]:
     else:
         out += [("W2", (1, h)), ("b2", (1,))]
     return out
+
+
+def layer_widths(m: ModelShape) -> List[Tuple[int, int]]:
+    """(n_in, n_out) of every layer in forward order: the encoder's Linear
+    layers, the Mamba blocks, the decoder's Linear layers."""
+    dims = [m.F, *m.enc_hidden, m.d_model]
+    out = [(dims[i], dims[i + 1]) for i in range(len(dims) - 1)]
+    out += [(m.d_model, m.d_model)] * m.n_layers
+    dec = [m.d_model, m.head_hidden] + ([m.dec_hidden2] if m.dec_hidden2 else []) + [1]
+    out += [(dec[i], dec[i + 1]) for i in range(len(dec) - 1)]
+    return out
+
+
+def lateral_layout(m: ModelShape, a: int) -> List[Tuple[str, Tuple[int, ...]]]:
+    """Lateral adapters (KB -> AC, one per layer after the first, forward
+    order): V[a, n_in], c[a], U[n_out, a], alpha[n_out]."""
+    out: List[Tuple[str, Tuple[int, ...]]] = []
+    for j, (n_in, n_out) in enumerate(layer_widths(m)[1:]):
+        out += [(f"lat{j}.V", (a, n_in)), (f"lat{j}.c", (a,)), (f"lat{j}.U", (n_out, a)),
+                (f"lat{j}.alpha", (n_out,))]
+    return out
+
+
+def init_lateral(m: ModelShape, a: int, rng: np.random.Generator) -> np.ndarray:
+    """Flat fp32 lateral blob: V, c ~ U(+-1/sqrt(n_in)), U ~ U(+-1/sqrt(a)),
+    alpha ~ U(0.5, 1.5) (so that every adapter visibly contributes)."""
+    parts = []
+    for (n_in, _), j in zip(layer_widths(m)[1:], range(len(layer_widths(m)) - 1)):
+        bv, bu = 1.0 / math.sqrt(n_in), 1.0 / math.sqrt(a)
+        parts += [rng.uniform(-bv, bv, size=(a, n_in)), rng.uniform(-bv, bv, size=a)]
+        n_out = layer_widths(m)[j + 1][1]
+        parts += [rng.uniform(-bu, bu, size=(n_out, a)), rng.uniform(0.5, 1.5, size=n_out)]
+    return np.concatenate([np.asarray(p, dtype=np.float32).reshape(-1) for p in parts])
 
 
 def param_count(m: ModelShape) -> int:
@@ -212,12 +249,16 @@ def make_workload(name: str, B: int | None = None, perturb: bool = False):
 
     `B` overrides the batch size (a smaller batch is its own draw from the
     same seed path). For the distillation workload `params` is the pair
-    (teacher_blob, student_blob); both are bf16-representable.
+    (teacher_blob, student_blob); both are bf16-representable. For the
+    progressive workload it is (kb_blob, ac_blob, lateral_blob).
     """
     w = WORKLOADS[name]
     Bn = w.B if B is None else B
     prng = _rng(w.seed_index, 0)
-    if w.student is None:
+    if w.adapter:
+        params = (init_params(w.model, prng, perturb), init_params(w.model, _rng(w.seed_index, 1), perturb),
+                  init_lateral(w.model, w.adapter, _rng(w.seed_index, 4)))
+    elif w.student is None:
         params = init_params(w.model, prng, perturb)
         if w.dtype == "bf16":
             params = round_to_bf16(params)

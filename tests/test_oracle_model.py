@@ -116,40 +116,53 @@ def test_token_causality_of_hidden_states():
 
 # ------------------------------------------------- independent torch re-expression
 
+def _torch_block(h, Pt, l, cfg):
+    """One Mamba block with its residual, in torch primitives, the SSM in its
+    explicit (quadratic) convolution form instead of the recurrence."""
+    F = torch.nn.functional
+    E, N, R, K = cfg["d_inner"], cfg["d_state"], cfg["dt_rank"], cfg["d_conv"]
+    L = h.shape[1]
+    causal = torch.tril(torch.ones(L, L, dtype=torch.float64))
+    p = f"blk{l}."
+    n = F.rms_norm(h, (cfg["d_model"],), Pt[p + "g"], eps=cfg["norm_eps"])
+    xz = F.linear(n, Pt[p + "W_in"])
+    xs, z = xz[..., :E], xz[..., E:]
+    xc = F.conv1d(xs.transpose(1, 2), Pt[p + "conv_w"][:, None, :], Pt[p + "conv_b"],
+                  padding=K - 1, groups=E)[..., :L].transpose(1, 2)
+    u = F.silu(xc)
+    xdbl = F.linear(u, Pt[p + "W_x"])
+    dtr, Bm, Cm = xdbl[..., :R], xdbl[..., R:R + N], xdbl[..., R + N:]
+    dt = F.softplus(F.linear(dtr, Pt[p + "W_dt"], Pt[p + "b_dt"]))
+    A = -torch.exp(Pt[p + "A_log"])
+    cum = torch.cumsum(dt[..., None] * A, dim=1)                  # [B,L,E,N]
+    seg = cum[:, :, None] - cum[:, None, :]                        # [B,t,k,E,N]
+    mask = causal[None, :, :, None, None]
+    decay = torch.exp(torch.where(mask > 0, seg, torch.full_like(seg, -1e30))) * mask
+    y = torch.einsum("btn,btken,bkn,bke->bte", Cm, decay, Bm, dt * u)
+    y = y + Pt[p + "D"] * u
+    return h + F.linear(y * F.silu(z), Pt[p + "W_out"])
+
+
+def _torch_pool(h, Pt, lengths, cfg):
+    F = torch.nn.functional
+    L = h.shape[1]
+    hf = F.rms_norm(h, (cfg["d_model"],), Pt["g_f"], eps=cfg["norm_eps"])
+    valid = (torch.arange(L)[None, :] < torch.as_tensor(lengths)[:, None]).double()
+    return (hf * valid[..., None]).sum(1) / torch.as_tensor(lengths, dtype=torch.float64)[:, None]
+
+
 def _torch_model_scores(Pt, X, lengths, cfg):
     """The same model written with torch primitives, and the SSM in its
     explicit (quadratic) convolution form instead of the recurrence."""
     F = torch.nn.functional
-    E, N, R, K = cfg["d_inner"], cfg["d_state"], cfg["dt_rank"], cfg["d_conv"]
-    Bn, L, _ = X.shape
     # encoder: Linear layers with a ReLU between consecutive ones
     enc = [F.linear(X, Pt["W0"], Pt["b0"])]
     for i in range(1, len(cfg.get("enc_hidden", ())) + 1):
         enc.append(F.linear(F.relu(enc[-1]), Pt[f"W0_{i}"], Pt[f"b0_{i}"]))
     h = enc[-1]
-    causal = torch.tril(torch.ones(L, L, dtype=torch.float64))
     for l in range(cfg["n_layers"]):
-        p = f"blk{l}."
-        n = F.rms_norm(h, (cfg["d_model"],), Pt[p + "g"], eps=cfg["norm_eps"])
-        xz = F.linear(n, Pt[p + "W_in"])
-        xs, z = xz[..., :E], xz[..., E:]
-        xc = F.conv1d(xs.transpose(1, 2), Pt[p + "conv_w"][:, None, :], Pt[p + "conv_b"],
-                      padding=K - 1, groups=E)[..., :L].transpose(1, 2)
-        u = F.silu(xc)
-        xdbl = F.linear(u, Pt[p + "W_x"])
-        dtr, Bm, Cm = xdbl[..., :R], xdbl[..., R:R + N], xdbl[..., R + N:]
-        dt = F.softplus(F.linear(dtr, Pt[p + "W_dt"], Pt[p + "b_dt"]))
-        A = -torch.exp(Pt[p + "A_log"])
-        cum = torch.cumsum(dt[..., None] * A, dim=1)                  # [B,L,E,N]
-        seg = cum[:, :, None] - cum[:, None, :]                        # [B,t,k,E,N]
-        mask = causal[None, :, :, None, None]
-        decay = torch.exp(torch.where(mask > 0, seg, torch.full_like(seg, -1e30))) * mask
-        y = torch.einsum("btn,btken,bkn,bke->bte", Cm, decay, Bm, dt * u)
-        y = y + Pt[p + "D"] * u
-        h = h + F.linear(y * F.silu(z), Pt[p + "W_out"])
-    hf = F.rms_norm(h, (cfg["d_model"],), Pt["g_f"], eps=cfg["norm_eps"])
-    valid = (torch.arange(L)[None, :] < torch.as_tensor(lengths)[:, None]).double()
-    pooled = (hf * valid[..., None]).sum(1) / torch.as_tensor(lengths, dtype=torch.float64)[:, None]
+        h = _torch_block(h, Pt, l, cfg)
+    pooled = _torch_pool(h, Pt, lengths, cfg)
     r1 = F.relu(F.linear(pooled, Pt["W1"], Pt["b1"]))
     if cfg.get("dec_hidden2", 0):
         return F.linear(F.relu(F.linear(r1, Pt["W2"], Pt["b2"])), Pt["W3"], Pt["b3"])[:, 0]
