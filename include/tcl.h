@@ -127,6 +127,7 @@ typedef struct tcl_config {
 
 typedef struct tcl_model tcl_model;     /* opaque, library-owned */
 typedef struct tcl_trainer tcl_trainer; /* opaque, library-owned */
+typedef struct tcl_lateral tcl_lateral; /* opaque, library-owned */
 
 /* Number of fp32 values in the canonical parameter blob for `cfg`
  * (0 if cfg is NULL). */
@@ -261,6 +262,47 @@ TCL_API size_t tcl_lambdarank_workspace_bytes(int32_t B);
 TCL_API tcl_status tcl_lambdarank(int32_t B, const float* d_scores, const float* d_labels, float sigma,
                                   float* d_loss, float* d_grad, void* d_workspace, size_t ws_bytes,
                                   void* stream);
+
+/* ---------------------------------------------------------------------
+ * Progressive KB + AC forward (section 6, Fig. 6, Eq. (7)): in the CKD
+ * framework's continual-learning phase the frozen knowledge base (KB) and
+ * the active column (AC), two models of one architecture, run side by side,
+ * and every AC layer after the first reads the KB's input to the same layer
+ * through a lateral adapter:
+ *   h_i = act_i(W_i h_{i-1} + b_i + alpha_i * U_i ReLU(V_i h^KB_{i-1} + c_i))
+ * Layers, in forward order: the encoder's Linear layers, the Mamba blocks
+ * (W_i h_{i-1} + b_i is then the block with its residual), the decoder's
+ * Linear layers (the first one's KB input is the KB's pooled, normalised
+ * vector). act_i is the layer's own activation: ReLU between Linear layers,
+ * none after the encoder's last layer, a block, or the score.
+ * Lateral blob (fp32, per layer i >= 1 in forward order, n_in and n_out the
+ * layer's widths, a the adapter width):
+ *   V[a, n_in], c[a], U[n_out, a], alpha[n_out]
+ * ------------------------------------------------------------------- */
+
+/* Values in the lateral blob of a model with `cfg` and adapter width a (0 on
+ * invalid arguments). */
+TCL_API size_t tcl_lateral_param_count(const tcl_config* cfg, int32_t adapter);
+
+/* Join a KB and an AC (distinct fp32 models with identical configs,
+ * dec_hidden2 % 4 == 0) by adapters of width `adapter` (a multiple of 4 in
+ * [4, 512]) from a host blob of tcl_lateral_param_count values (copied;
+ * alpha is folded into U's rows on upload). Keeps pointers to both models:
+ * they must outlive the handle. Synchronous. */
+TCL_API tcl_status tcl_lateral_create(tcl_model* kb, tcl_model* ac, int32_t adapter, const float* h_params,
+                                      size_t n_params, tcl_lateral** out);
+TCL_API tcl_status tcl_lateral_destroy(tcl_lateral* lateral);
+
+/* Device workspace of one progressive forward with B programs padded to L. */
+TCL_API size_t tcl_progressive_workspace_bytes(const tcl_lateral* lateral, int32_t B, int32_t L);
+
+/* The AC's scores (the CL phase's predictions p_t of Eq. (8)) of B programs,
+ * arguments as for tcl_score. Stream-ordered. With the AC model's timing
+ * enabled (tcl_timing_enable on the AC), launches are timed under the AC's
+ * handle as "kb:*", "ac:*" and "lat:*" entries. */
+TCL_API tcl_status tcl_progressive_score(tcl_lateral* lateral, int32_t B, int32_t L, const float* d_feats,
+                                         const int32_t* d_lengths, float* d_scores, void* d_workspace,
+                                         size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------
  * What consumes the scores.

@@ -67,6 +67,11 @@ _SIGS = {
     "tcl_distill_step_kd": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, ctypes.POINTER(KDLoss), _vp, _vp, _sz, _vp]),
     "tcl_lambdarank_workspace_bytes": (_sz, [_i32]),
     "tcl_topk": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp]),
+    "tcl_lateral_param_count": (_sz, [ctypes.POINTER(Config), _i32]),
+    "tcl_lateral_create": (_i32, [_vp, _vp, _i32, _vp, _sz, ctypes.POINTER(_vp)]),
+    "tcl_lateral_destroy": (_i32, [_vp]),
+    "tcl_progressive_workspace_bytes": (_sz, [_vp, _i32, _i32]),
+    "tcl_progressive_score": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "tcl_topk_score_workspace_bytes": (_sz, [_i32, _i32]),
     "tcl_topk_score": (_i32, [_i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _sz, _vp]),
     "tcl_rdu_workspace_bytes": (_sz, [_i32, _i32]),
@@ -209,6 +214,51 @@ class CostModel:
     def set_params(self, params: np.ndarray):
         blob = np.ascontiguousarray(params, dtype=np.float32)
         check(lib().tcl_set_params(self._h, blob.ctypes.data, blob.size))
+
+
+class Progressive:
+    """A frozen KB and an active column joined by lateral adapters of width
+    `adapter` (tcl_lateral_create / tcl_progressive_score). Keeps both models
+    alive."""
+
+    def __init__(self, kb: CostModel, ac: CostModel, adapter: int, params: np.ndarray):
+        L = lib()
+        self.kb, self.ac, self.adapter = kb, ac, adapter
+        blob = np.ascontiguousarray(params, dtype=np.float32)
+        h = _vp()
+        check(L.tcl_lateral_create(kb.handle, ac.handle, adapter, blob.ctypes.data, blob.size, ctypes.byref(h)))
+        self._h = h
+        self._ws = None
+
+    def close(self):
+        if getattr(self, "_h", None):
+            check(lib().tcl_lateral_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace(self, B: int, L: int):
+        import torch
+        need = lib().tcl_progressive_workspace_bytes(self._h, B, L)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        return self._ws
+
+    def score(self, feats, lengths, out=None, workspace=None, stream=None):
+        """The AC's scores with the KB read through Eq. (7): feats [B,L,F]
+        fp32 cuda, lengths [B] int32 cuda -> [B] fp32 cuda."""
+        import torch
+        B, L, _ = feats.shape
+        if out is None:
+            out = torch.empty(B, dtype=torch.float32, device=feats.device)
+        ws = self.workspace(B, L) if workspace is None else workspace
+        check(lib().tcl_progressive_score(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), out.data_ptr(),
+                                          ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)))
+        return out
 
 
 class Trainer:

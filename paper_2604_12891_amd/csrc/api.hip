@@ -140,6 +140,63 @@ tcl_status derive_weights(tcl_model* m, hipStream_t s) {
   return TCL_OK;
 }
 
+hipError_t model_gemm(const tcl_model* m, const GemmArgs& a, const uint16_t* Ws, int ldws, int flags,
+                      hipStream_t s) {
+  // the split path where it has a kernel for the shape, the fp32 MFMA path otherwise
+  if (m->split && Ws && gemm_split_variant(a, flags) > 0) return launch_gemm_split(a, Ws, ldws, flags, -1, s);
+  return launch_gemm_f32(a, flags, -1, s);
+}
+
+tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string& tag, int i, int B, int L,
+                                     const int* offs, const float* A, float* C, bool act, hipStream_t s) {
+  const tcl_config& c = m->cfg;
+  const BlobLayout bl = blob_layout(c);
+  const int in = i == 0 ? m->ldw0 : bl.enc_dims[i], out = bl.enc_dims[i + 1];
+  GemmArgs g;
+  g.A = A; g.lda = in; g.C = C; g.ldc = out; g.Mdev = offs + B; g.Mmax = B * L; g.N = out; g.K = in;
+  g.relu = act;
+  if (i == 0) {
+    // the gathered input Linear (rows b*L + t of the padded input)
+    g.offs = offs; g.B = B; g.L = L; g.W = m->W0; g.ldw = m->ldw0; g.bias = m->b0;
+    TCL_LAUNCH(T, (tag + "gemm_input").c_str(), model_gemm(m, g, m->W0_s, m->ldw0_h, kBias | kGather, s));
+  } else {
+    g.W = m->We[i]; g.ldw = in; g.bias = m->be[i];
+    TCL_LAUNCH(T, (tag + "gemm_encoder").c_str(), model_gemm(m, g, m->We_s[i], (in + 7) & ~7, kBias, s));
+  }
+  return TCL_OK;
+}
+
+tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, int l, int B, int L,
+                             const int* offs, float* H, float* xz, float* u, float* xdbl, hipStream_t s) {
+  const tcl_config& c = m->cfg;
+  const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
+  const int Mmax = B * L;
+  const int chunks = scan_chunks_for(B, E, L);
+  const auto& W = m->layers[l];
+  GemmArgs gi;
+  gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
+  gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
+  TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), model_gemm(m, gi, W.W_in_s, d, kRowNorm, s));
+  TCL_LAUNCH(T, (tag + "conv_silu").c_str(),
+             launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w, W.conv_b, u, s));
+  GemmArgs gx;
+  gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
+  gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
+  TCL_LAUNCH(T, (tag + "gemm_x_proj").c_str(), launch_gemm_f32(gx, 0, -1, s));
+  if (chunks > 0)
+    TCL_LAUNCH(T, (tag + "scan_chunked").c_str(),
+               launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E, 2 * E, W.W_dt, W.b_dt,
+                                          W.A_log, W.D, u, s));
+  else
+    TCL_LAUNCH(T, (tag + "scan").c_str(), launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+                                                             W.b_dt, W.A_log, W.D, u, s));
+  GemmArgs go;
+  go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
+  go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
+  TCL_LAUNCH(T, (tag + "gemm_out_proj").c_str(), model_gemm(m, go, W.W_out_s, E, kResid, s));
+  return TCL_OK;
+}
+
 tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
                      float* d_scores, char* ws, hipStream_t s) {
   const tcl_config& c = m->cfg;
@@ -165,60 +222,20 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
   if (c.dtype == TCL_F32) {
     float* xz = reinterpret_cast<float*>(ws + p.xz);
     float* u = reinterpret_cast<float*>(ws + p.u);
-    // the split path where it has a kernel for the shape, the fp32 MFMA path otherwise
-    auto gemm = [&](const GemmArgs& a, const uint16_t* Ws, int ldws, int flags) {
-      if (m->split && Ws && gemm_split_variant(a, flags) > 0)
-        return launch_gemm_split(a, Ws, ldws, flags, -1, s);
-      return launch_gemm_f32(a, flags, -1, s);
-    };
     // encoder: the gathered input Linear, then (multi-layer encoder) the
     // hidden Linear layers on the packed rows, a ReLU after every layer but
     // the last
-    const int e1 = c.enc_hidden[0], e2 = c.enc_hidden[1];
-    const int n_enc = e1 > 0 ? (e2 > 0 ? 3 : 2) : 1;
-    const int dims[4] = {ldf, e1, n_enc == 3 ? e2 : d, d};
+    const int n_enc = blob_layout(c).n_enc;
     float* bufs[2] = {reinterpret_cast<float*>(ws + p.enc1), reinterpret_cast<float*>(ws + p.enc2)};
-    GemmArgs g;
-    g.A = feats; g.lda = ldf; g.offs = offs; g.B = B; g.L = L;
-    g.W = m->W0; g.ldw = m->ldw0; g.bias = m->b0; g.C = n_enc > 1 ? bufs[0] : H;
-    g.ldc = n_enc > 1 ? e1 : d; g.Mdev = offs + B; g.Mmax = Mmax; g.N = n_enc > 1 ? e1 : d; g.K = ldf;
-    g.relu = n_enc > 1;
-    TCL_LAUNCH(T, "gemm_input", gemm(g, m->W0_s, m->ldw0_h, kBias | kGather));
-    for (int i = 1; i < n_enc; ++i) {
-      const int in = dims[i], out = dims[i + 1];
+    for (int i = 0; i < n_enc; ++i) {
       const bool last = i == n_enc - 1;
-      GemmArgs ge;
-      ge.A = bufs[i - 1]; ge.lda = in; ge.W = m->We[i]; ge.ldw = in; ge.bias = m->be[i];
-      ge.C = last ? H : bufs[i]; ge.ldc = out; ge.Mdev = offs + B; ge.Mmax = Mmax; ge.N = out; ge.K = in;
-      ge.relu = !last;
-      TCL_LAUNCH(T, "gemm_encoder", gemm(ge, m->We_s[i], (in + 7) & ~7, kBias));
+      tcl_status st = enqueue_encoder_layer_f32(m, T, "", i, B, L, offs, i == 0 ? feats : bufs[i - 1],
+                                                last ? H : bufs[i], !last, s);
+      if (st != TCL_OK) return st;
     }
-
     for (int l = 0; l < c.n_layers; ++l) {
-      const auto& W = m->layers[l];
-      GemmArgs gi;
-      gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
-      gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-      TCL_LAUNCH(T, "gemm_in_proj", gemm(gi, W.W_in_s, d, kRowNorm));
-
-      TCL_LAUNCH(T, "conv_silu", launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w,
-                                                         W.conv_b, u, s));
-      GemmArgs gx;
-      gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
-      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_f32(gx, 0, -1, s));
-
-      if (chunks > 0)
-        TCL_LAUNCH(T, "scan_chunked", launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E,
-                                                                 2 * E, W.W_dt, W.b_dt, W.A_log, W.D,
-                                                                 u, s));
-      else
-        TCL_LAUNCH(T, "scan", launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                                 W.b_dt, W.A_log, W.D, u, s));
-      GemmArgs go;
-      go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
-      go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-      TCL_LAUNCH(T, "gemm_out_proj", gemm(go, W.W_out_s, E, kResid));
+      tcl_status st = enqueue_block_f32(m, T, "", l, B, L, offs, H, xz, u, xdbl, s);
+      if (st != TCL_OK) return st;
     }
   } else {
     uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
@@ -415,6 +432,7 @@ ModelPlan plan_model(const tcl_config& c) {
   P.b1 = job(bl.b1, 1, h, kDeriveF32, 0, 4);
   if (c.dec_hidden2 > 0) {
     const int h2 = c.dec_hidden2;
+    P.W2 = job(bl.W2, h2, h, kDeriveF32, 0, 4);
     P.W2T = job(bl.W2, h2, h, kDeriveF32, 1, 4);
     P.b2 = job(bl.b2, 1, h2, kDeriveF32, 0, 4);
     P.W3 = job(bl.W3, 1, h2, kDeriveF32, 0, 4);
@@ -520,12 +538,11 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
   m->W1T = F32(P.W1T);
   m->b1 = F32(P.b1);
   m->b2 = F32(P.b2);
+  m->W2 = F32(P.W2);
   if (cfg->dec_hidden2 > 0) {
     m->W2T = F32(P.W2T);
     m->W3 = F32(P.W3);
     m->b3 = F32(P.b3);
-  } else {
-    m->W2 = F32(P.W2);
   }
   {
     const BlobLayout bl = blob_layout(*cfg);

@@ -200,6 +200,8 @@ hipError_t launch_tail_f32(int B, int L, int d, int h, const int* offs, const in
 // The same with a three-layer decoder Linear(d,h) ReLU Linear(h,h2) ReLU
 // Linear(h2,1): W2T is the second layer transposed, [h][h2], b2 its bias
 // [h2], W3 [h2] and b3 [1] the output layer. h, h2 <= 256.
+// scores[b] = NaN where lengths[b] is outside [1, L] (an invalid program)
+hipError_t launch_mask_scores(int B, int L, const int* lengths, float* scores, hipStream_t s);
 // dst[r][c] = c < F ? src[r][c] : 0 for rows x ld (row-major, src rows of F)
 hipError_t launch_pad_rows(const float* src, int64_t rows, int F, int ld, float* dst, hipStream_t s);
 hipError_t launch_tail3_f32(int B, int L, int d, int h, int h2, const int* offs, const int* lengths,

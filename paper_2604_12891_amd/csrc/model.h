@@ -108,7 +108,7 @@ struct tcl_model {
   // the three-way split [3][out][ld] on the split path, ld = in rounded to 8)
   float *We[3] = {nullptr, nullptr, nullptr}, *be[3] = {nullptr, nullptr, nullptr};
   uint16_t* We_s[3] = {nullptr, nullptr, nullptr};
-  // three-layer decoder: W2 transposed [h][h2], W3 [h2], b3 [1]
+  // three-layer decoder: W2 [h2][h] and transposed [h][h2], W3 [h2], b3 [1]
   float *W2T = nullptr, *W3 = nullptr, *b3 = nullptr;
   uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
   int ldw0_h = 0;
@@ -125,6 +125,19 @@ struct ScorePlan {
   size_t offs, H, xz, u, xdbl, feats, enc1, enc2, total;
 };
 ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L);
+
+// The model's GEMM: the split path where it has a kernel for the shape,
+// the fp32 MFMA path otherwise.
+hipError_t model_gemm(const tcl_model* m, const GemmArgs& a, const uint16_t* Ws, int ldws, int flags,
+                      hipStream_t s);
+// fp32 models: encoder Linear layer i (0 = the gathered input Linear; A is
+// then the [B, L, ldw0] padded input) from A to C, ReLU when `act`; and
+// Mamba block l in place on the residual stream H [tokens, d]. Launches are
+// timed under tag + kernel name.
+tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string& tag, int i, int B, int L,
+                                     const int* offs, const float* A, float* C, bool act, hipStream_t s);
+tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, int l, int B, int L,
+                             const int* offs, float* H, float* xz, float* u, float* xdbl, hipStream_t s);
 
 // Enqueue the scoring pass (no argument checks).
 tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,

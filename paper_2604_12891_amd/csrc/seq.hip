@@ -547,7 +547,22 @@ __global__ __launch_bounds__(256) void pad_rows_kernel(int64_t n, int F, int ld,
   }
 }
 
+__global__ __launch_bounds__(256) void mask_scores_kernel(int B, int L, const int* __restrict__ lengths,
+                                                          float* __restrict__ scores) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b < B) {
+    const int len = lengths[b];
+    if (len < 1 || len > L) scores[b] = __builtin_nanf("");
+  }
+}
+
 }  // namespace
+
+hipError_t launch_mask_scores(int B, int L, const int* lengths, float* scores, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(mask_scores_kernel, dim3((B + 255) / 256), dim3(256), 0, s, B, L, lengths, scores);
+  return hipGetLastError();
+}
 
 hipError_t launch_pad_rows(const float* src, int64_t rows, int F, int ld, float* dst, hipStream_t s) {
   if (rows <= 0) return hipSuccess;

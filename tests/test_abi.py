@@ -141,3 +141,25 @@ def test_bf16_gemm_entry_rejects_bad_arguments(lib):
     assert call(kind=4) == -1         # the gather needs offsets and B, L
     assert call(kind=4, offs=fake, B=2, L=3) == -1  # ... and the bias
     assert call(C=fake + 4) == -1     # alignment
+
+
+@pytest.mark.parametrize("shape", [wl.TINY, wl.PAPER_CPU])
+def test_lateral_param_count_matches_oracle_layout(lib, shape):
+    from oracle import progressive as op
+    cfg = tb.config_from_shape(shape)
+    ocfg = dict(F=shape.F, d_model=shape.d_model, d_inner=shape.d_inner, d_state=shape.d_state,
+                d_conv=shape.d_conv, dt_rank=shape.dt_rank, n_layers=shape.n_layers,
+                head_hidden=shape.head_hidden, enc_hidden=shape.enc_hidden, dec_hidden2=shape.dec_hidden2)
+    for a in (4, 8, 32):
+        n = lib.tcl_lateral_param_count(ctypes.byref(cfg), a)
+        assert n == sum(int(np.prod(s)) for _, s in op.lateral_layout(ocfg, a))
+        assert n == sum(int(np.prod(s)) for _, s in wl.lateral_layout(shape, a))
+    assert lib.tcl_lateral_param_count(ctypes.byref(cfg), 0) == 0
+
+
+def test_progressive_calls_on_null_handles(lib):
+    h = ctypes.c_void_p()
+    assert lib.tcl_lateral_create(None, None, 8, None, 0, ctypes.byref(h)) == -1 and h.value is None
+    assert lib.tcl_lateral_destroy(None) == 0
+    assert lib.tcl_progressive_workspace_bytes(None, 4, 4) == 0
+    assert lib.tcl_progressive_score(None, 1, 1, None, None, None, None, 0, None) == -1
