@@ -70,8 +70,10 @@ def kernel_work(shape, M_v: int, B: int, dtype: str, L: int = 0) -> dict:
         # VALU-bound: 2 flops per issue slot against the fp32 vector peak;
         # its HBM bytes are reported beside it
         "scan": ("valu", (2 * M_v * E * scan_valu_slots(N, R), M_v * (3 * E * a + XW * 4))),
+        "scan_chunked": ("valu", (2 * M_v * E * scan_valu_slots(N, R), M_v * (3 * E * a + XW * 4))),
         "tail": ("byte", M_v * d * 4 + B * 8 + 4 * (d * h + h + h * h2 + 2 * h2)),
         "offsets": ("byte", B * 8),
+        "mask_scores": ("byte", B * 8),
     }
 
 
@@ -168,6 +170,147 @@ def distill_kernel_work(tshape, sshape, M_v: int, B: int) -> dict:
         "scan_bwd": ("byte", nl * M_v * (3 * E * 2 + E * 4 + XW * 4 + 3 * E * 4 + 2 * N * 4)),
     })
     return out
+
+
+def progressive_work(shape, a: int, M_v: int, B: int, L: int) -> dict:
+    """Algorithmic work per step of each kernel category of the progressive
+    forward ("kb:", "ac:" and "lat:" prefixes): the plain model's per-launch
+    counts for each column's own kernels, and the adapters' GEMMs (2 flops
+    per multiply-add; token rows for the encoder and blocks, pooled rows for
+    the decoder)."""
+    from paper_2604_12891_amd import workload as wl
+
+    per = kernel_work(shape, M_v, B, "f32", L)
+    widths = wl.layer_widths(shape)
+    n_tok = len(shape.enc_hidden) + 1 + shape.n_layers  # layers on token rows
+    # the adapters' GEMMs have K = n_in (V) and K = a (U): with a = 8 they move
+    # more bytes than they compute, so they are counted as HBM work: V reads
+    # the KB's input and writes [rows, a]; U reads [rows, a] and the AC's
+    # output and writes it back
+    V = U = F = 0
+    for i, (n_in, n_out) in enumerate(widths[1:], start=1):
+        rows = M_v if i < n_tok else B
+        V += rows * (n_in + a) * 4
+        U += rows * (a + 2 * n_out) * 4
+        F += rows * (n_in + 2 * n_out) * 4  # the fused adapter: input read, output read and written
+    dec = [2 * B * n_in * n_out for n_in, n_out in widths[n_tok:]]
+    pool = ("byte", M_v * shape.d_model * 4 + B * shape.d_model * 4)
+    totals = {"lat:gemm_V": ("byte", V), "lat:gemm_U": ("byte", U), "lat:adapter": ("byte", F),
+              # the KB's decoder stops before its output layer (no adapter reads it)
+              "ac:gemm_decoder": ("flop", sum(dec)), "kb:gemm_decoder": ("flop", sum(dec[:-1])),
+              "ac:pool": pool, "kb:pool": pool}
+    return per, totals
+
+
+def bench_progressive(args, w):
+    """The CKD framework's continual-learning forward (Eq. (7)): the KB and
+    the AC of the paper's model joined by lateral adapters, one step = one
+    tcl_progressive_score call over the whole batch."""
+    import numpy as np
+    import torch
+
+    from paper_2604_12891_amd import binding as tb
+
+    from paper_2604_12891_amd import workload as wl
+
+    (kb, ac, lat), X, lengths = wl.make_workload(w.name)
+    dev = torch.device("cuda:0")
+    cfg = tb.config_from_shape(w.model, "f32", args.f32_matmul)
+    K, A = tb.CostModel(cfg, kb), tb.CostModel(cfg, ac)
+    prog = tb.Progressive(K, A, w.adapter, lat)
+    Xd, Ld = torch.from_numpy(X).to(dev), torch.from_numpy(lengths).to(dev)
+    ws = prog.workspace(w.B, w.L)
+    out = torch.empty(w.B, dtype=torch.float32, device=dev)
+    M_v = int(lengths.sum())
+    for _ in range(args.warmup):
+        prog.score(Xd, Ld, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        prog.score(Xd, Ld, out=out, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    assert torch.isfinite(out).all().item(), "non-finite scores"
+    A.timing(True)
+    A.timing_reset()
+    for _ in range(args.steps):
+        prog.score(Xd, Ld, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    rep = A.timing_report()
+    A.timing(False)
+
+    per, totals = progressive_work(w.model, w.adapter, M_v, w.B, w.L)
+    split = args.f32_matmul == "split"
+    kernels = {}
+    for name, (tot, n) in rep.items():
+        base = name.split(":", 1)[-1]
+        launches = n // args.steps
+        if name in totals:  # per-step totals: the mean per launch
+            kind, amount = totals[name]
+            amount = amount / launches
+        else:  # each column's own kernels: per-launch counts of the plain model
+            kind, amount = per[base]
+        e = roofline_entry(kind, amount, tot / n, "f32",
+                           split and base in ("gemm_input", "gemm_encoder", "gemm_in_proj", "gemm_out_proj"))
+        e.update({"ms_per_launch": tot / n, "launches_per_step": launches, "ms_per_step": tot / args.steps,
+                  "work_per_launch": amount, "work_unit": kind})
+        kernels[name] = e
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dom]
+    roof = {"kernel": dom, "bound": d["bound"], "achieved": round(d["achieved"], 3), "peak": d["peak"],
+            "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None,
+            "ms_per_launch": round(d["ms_per_launch"], 5)}
+    if d["bound"] == "alu":
+        roof["hbm_achieved_gbs"] = round(d["hbm_gbs"], 1)
+        roof["hbm_frac"] = round(d["hbm_frac"], 4)
+    if "peak_note" in d:
+        roof["peak_note"] = d["peak_note"]
+    if args.kernels:
+        for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+            extra = f"  (HBM {e['hbm_gbs']:.0f} GB/s = {e['hbm_frac']:.3f})" if "hbm_gbs" in e else ""
+            print(f"{k:20s} {e['ms_per_step']:9.4f} ms/step x{e['launches_per_step']:3d} {e['achieved']:10.2f} "
+                  f"{e['unit']:8s} {e['frac']:6.3f}{extra}", file=sys.stderr)
+    cpu = None
+    if not args.no_cpu_baseline:
+        from threadpoolctl import threadpool_info
+
+        from oracle import progressive as op
+        ocfg = dict(F=w.model.F, d_model=w.model.d_model, d_inner=w.model.d_inner, d_state=w.model.d_state,
+                    d_conv=w.model.d_conv, dt_rank=w.model.dt_rank, n_layers=w.model.n_layers,
+                    head_hidden=w.model.head_hidden, final_norm=w.model.final_norm, norm_eps=w.model.norm_eps,
+                    enc_hidden=tuple(w.model.enc_hidden), dec_hidden2=w.model.dec_hidden2)
+        n = 64
+        t = time.perf_counter()
+        op.progressive_scores(kb, ac, lat, w.adapter, X[:n], lengths[:n], ocfg)
+        dt0 = time.perf_counter() - t
+        n = int(min(w.B, max(n, args.cpu_seconds / max(dt0, 1e-6) * n)))
+        idx = np.linspace(0, w.B - 1, n).astype(np.int64)
+        t = time.perf_counter()
+        op.progressive_scores(kb, ac, lat, w.adapter, X[idx], lengths[idx], ocfg)
+        dt = time.perf_counter() - t
+        blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        cpu = {"value": n / dt, "unit": "programs/s", "cores": max([p.get("num_threads", 1) for p in blas] or [1]),
+               "kind": "oracle",
+               "sample": f"{n} of {w.B} programs (evenly strided) of the same batch, numpy fp64, {dt:.1f} s"}
+    rec = {
+        "metric": f"KB+AC progressive forward: programs scored/sec (B={w.B},L={w.L}) + % of HBM / MFMA peak",
+        "value": w.B / (ms * 1e-3), "unit": "programs/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "F": w.model.F, "adapter": w.adapter,
+                   "f32_matmul": args.f32_matmul, "encoder": [w.model.F, *w.model.enc_hidden, w.model.d_model],
+                   "d_state": w.model.d_state, "n_layers": w.model.n_layers,
+                   "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v},
+        "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
+                    for k, e in kernels.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
 
 
 def bench_distill(args, w):
@@ -464,6 +607,9 @@ def main():
     w = wl.WORKLOADS[args.workload]
     if w.student is not None:
         bench_distill(args, w)
+        return
+    if w.adapter:
+        bench_progressive(args, w)
         return
     blob, X, lengths = wl.make_workload(w.name)
     dev = torch.device("cuda:0")

@@ -4,10 +4,10 @@
 // first adds alpha_i * U_i ReLU(V_i h^KB_{i-1} + c_i) of the KB's input to
 // the same layer before its own activation.
 //
-// Per layer: the adapter's inner GEMM (KB input -> [rows, a], bias, ReLU),
-// the AC's own layer, the adapter's outer GEMM accumulated into the AC's
-// output (alpha folded into U's rows at create; ReLU after the sum for
-// hidden Linear layers), then the KB's own layer. The encoder and Mamba
+// Per layer: the AC's own layer, then the adapter on the KB's input to the
+// layer accumulated into the AC's output (alpha folded into U's rows at
+// create; ReLU after the sum for hidden Linear layers; one fused pass per
+// row for narrow adapters, two GEMMs otherwise), then the KB's own layer. The encoder and Mamba
 // blocks run on packed token rows; both columns are pooled and the decoder
 // Linear layers run as GEMMs over the B pooled rows. The KB's last layer is
 // not computed: no AC layer reads its output.
@@ -16,6 +16,7 @@
 #include <algorithm>
 #include <cstring>
 
+#include "common.h"
 #include "model.h"
 
 using namespace tcl;
@@ -113,10 +114,188 @@ GemmArgs plain(const float* A, int lda, const float* W, const float* bias, float
   return g;
 }
 
-// Adapter j: T = ReLU(X_kb V^T + c), then C = act(C + T U'^T).
+// A narrow adapter in one pass over the rows: one wavefront per row (two
+// rows in flight), lane l holding inputs l + 64p and outputs l + 64p; V, c
+// and U' stay in registers. Per row the A inner sums are reduce-scattered
+// across the wavefront (lane bit 5 by a half-wave swap, bit 4 by a row swap,
+// then DPP / swizzle steps; each step halves the values a lane carries until
+// one is left, then plain pair sums), so lane l ends with the total of sum
+// k = l >> (6 - log2 A); the A totals are then read back as wave-uniform
+// values. Every output is C + sum_k U'[j][k] ReLU(t_k + c_k), ReLU'd when
+// `act`. Nothing of size [rows, A] is stored.
+template <int N>
+__device__ __forceinline__ void swap32(float* w) {
+  // bit 5: lanes 0-31 keep w[i], lanes 32-63 keep w[N/2 + i], each summed over the lane pair
+#pragma unroll
+  for (int i = 0; i < N / 2; ++i) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(w[i]), __float_as_uint(w[N / 2 + i]), false, false);
+    w[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+}
+template <int N>
+__device__ __forceinline__ void swap16(float* w) {
+  // bit 4: rows 0, 2 keep w[i], rows 1, 3 keep w[N/2 + i]
+#pragma unroll
+  for (int i = 0; i < N / 2; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(w[i]), __float_as_uint(w[N / 2 + i]), false, false);
+    w[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+}
+__device__ __forceinline__ float ror8(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xF, 0xF, false));  // xor 8 in a row
+}
+__device__ __forceinline__ float xor4(float v) { return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F)); }
+__device__ __forceinline__ float xor2(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+
+// A in {4, 8, 16}: returns lane l's total of value l >> (6 - log2 A).
+template <int A>
+__device__ __forceinline__ float reduce_scatter(float* w, int lane) {
+  swap32<A>(w);
+  swap16<A / 2>(w);
+  float z;
+  if constexpr (A == 4) {
+    z = w[0] + ror8(w[0]);
+    z += xor4(z);
+  } else {
+    const bool b3 = (lane & 8) != 0;
+    float y[A / 8];
+#pragma unroll
+    for (int i = 0; i < A / 8; ++i) {
+      const float mine = b3 ? w[A / 8 + i] : w[i], other = b3 ? w[i] : w[A / 8 + i];
+      y[i] = mine + ror8(other);
+    }
+    if constexpr (A == 8) {
+      z = y[0] + xor4(y[0]);
+    } else {
+      const bool b2 = (lane & 4) != 0;
+      const float mine = b2 ? y[1] : y[0], other = b2 ? y[0] : y[1];
+      z = mine + xor4(other);
+    }
+  }
+  z += xor2(z);
+  return z + xor1(z);
+}
+
+template <int PI, int PO, int A>
+__global__ __launch_bounds__(256) void adapter_kernel(int Mmax, const int* __restrict__ Mdev,
+                                                      const float* __restrict__ X, int n_in,
+                                                      const float* __restrict__ V, const float* __restrict__ cb,
+                                                      const float* __restrict__ U, int n_out, float* __restrict__ C,
+                                                      int ldc, int act) {
+  constexpr int LA = A == 4 ? 2 : A == 8 ? 3 : 4;
+  const int M = Mdev ? *Mdev : Mmax;
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6), nwaves = gridDim.x * 4;
+  float v[A][PI], u[PO][A], c[A];
+#pragma unroll
+  for (int k = 0; k < A; ++k) {
+    c[k] = cb[k];
+#pragma unroll
+    for (int p = 0; p < PI; ++p) {
+      const int i = lane + 64 * p;
+      v[k][p] = i < n_in ? V[k * n_in + i] : 0.f;
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < PO; ++p) {
+    const int j = lane + 64 * p;
+#pragma unroll
+    for (int k = 0; k < A; ++k) u[p][k] = j < n_out ? U[j * A + k] : 0.f;
+  }
+  for (int r0 = 2 * wave; r0 < M; r0 += 2 * nwaves) {
+    // two rows; past the end the second repeats the first and is not stored
+    const int rows[2] = {r0, min(r0 + 1, M - 1)};
+    float x[2][PI], y[2][PO];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const float* xr = X + (int64_t)rows[q] * n_in;
+      const float* cr = C + (int64_t)rows[q] * ldc;
+#pragma unroll
+      for (int p = 0; p < PI; ++p) x[q][p] = xr[min(lane + 64 * p, n_in - 1)];  // V is zero past n_in
+#pragma unroll
+      for (int p = 0; p < PO; ++p) y[q][p] = cr[min(lane + 64 * p, n_out - 1)];
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      float w[A];
+#pragma unroll
+      for (int k = 0; k < A; ++k) {
+        float acc = 0.f;
+#pragma unroll
+        for (int p = 0; p < PI; ++p) acc = fmaf(v[k][p], x[q][p], acc);
+        w[k] = acc;
+      }
+      const float z = reduce_scatter<A>(w, lane);
+      float t[A];
+#pragma unroll
+      for (int k = 0; k < A; ++k)
+        t[k] = fmaxf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(z), k << (6 - LA))) + c[k], 0.f);
+      if (q == 1 && r0 + 1 >= M) break;
+      float* cr = C + (int64_t)rows[q] * ldc;
+#pragma unroll
+      for (int p = 0; p < PO; ++p) {
+        const int j = lane + 64 * p;
+        float o = y[q][p];
+#pragma unroll
+        for (int k = 0; k < A; ++k) o = fmaf(u[p][k], t[k], o);
+        if (act) o = fmaxf(o, 0.f);
+        if (j < n_out) cr[j] = o;
+      }
+    }
+  }
+}
+
+int lanes_per(int n) { return n <= 64 ? 1 : n <= 128 ? 2 : n <= 256 ? 4 : 0; }
+
+// The fused adapter kernel for n_in, n_out <= 256 and a in {4, 8, 16};
+// hipErrorNotSupported otherwise (the caller then uses two GEMMs).
+hipError_t launch_adapter(int Mmax, const int* Mdev, const float* X, int n_in, const float* V, const float* c,
+                          const float* U, int n_out, int a, float* C, int ldc, bool act, hipStream_t s) {
+  const int pi = lanes_per(n_in), po = lanes_per(n_out);
+  if (!pi || !po || (a != 4 && a != 8 && a != 16)) return hipErrorNotSupported;
+  if (Mmax <= 0) return hipSuccess;
+  const int grid = std::min((Mmax + 3) / 4, 4096);
+#define TCL_ADP(PI_, PO_, A_)                                                                                \
+  hipLaunchKernelGGL((adapter_kernel<PI_, PO_, A_>), dim3(grid), dim3(256), 0, s, Mmax, Mdev, X, n_in, V, c, U, \
+                     n_out, C, ldc, act ? 1 : 0)
+#define TCL_ADP_A(PI_, PO_)               \
+  switch (a) {                            \
+    case 4: TCL_ADP(PI_, PO_, 4); break;  \
+    case 8: TCL_ADP(PI_, PO_, 8); break;  \
+    default: TCL_ADP(PI_, PO_, 16); break; \
+  }
+  switch (pi * 10 + po) {
+    case 11: TCL_ADP_A(1, 1); break;
+    case 12: TCL_ADP_A(1, 2); break;
+    case 14: TCL_ADP_A(1, 4); break;
+    case 21: TCL_ADP_A(2, 1); break;
+    case 22: TCL_ADP_A(2, 2); break;
+    case 24: TCL_ADP_A(2, 4); break;
+    case 41: TCL_ADP_A(4, 1); break;
+    case 42: TCL_ADP_A(4, 2); break;
+    default: TCL_ADP_A(4, 4); break;
+  }
+#undef TCL_ADP_A
+#undef TCL_ADP
+  return hipGetLastError();
+}
+
+// Adapter j: C = act(C + U' ReLU(X_kb V^T + c)) -- one fused pass for narrow
+// adapters, else T = ReLU(X_kb V^T + c) by one GEMM and the accumulation by
+// a second (residual epilogue).
 tcl_status lateral(tcl_lateral* lt, Timing& T, int j, const float* X_kb, float* Tbuf, float* C, int ldc,
                    const int* Mdev, int Mmax, bool act, hipStream_t s) {
   const auto& A = lt->lats[j];
+  if (lanes_per(A.n_in) && lanes_per(A.n_out) && (lt->a == 4 || lt->a == 8 || lt->a == 16)) {
+    TCL_LAUNCH(T, "lat:adapter", launch_adapter(Mmax, Mdev, X_kb, A.n_in, A.V, A.c, A.U, A.n_out, lt->a, C, ldc,
+                                                act, s));
+    return TCL_OK;
+  }
   const GemmArgs gv = plain(X_kb, A.n_in, A.V, A.c, Tbuf, lt->a, lt->a, A.n_in, Mdev, Mmax, true);
   TCL_LAUNCH(T, "lat:gemm_V", launch_gemm_f32(gv, kBias, -1, s));
   const GemmArgs gu = plain(Tbuf, lt->a, A.U, nullptr, C, ldc, A.n_out, lt->a, Mdev, Mmax, act);
@@ -178,13 +357,8 @@ tcl_status run_progressive(tcl_lateral* lt, int B, int L, const float* d_feats, 
   float* u = F32(p.u);
   float* xdbl = F32(p.xdbl);
   for (int l = 0; l < c.n_layers; ++l) {
-    const auto& A = lt->lats[j];
-    const GemmArgs gv = plain(Hkb, d, A.V, A.c, Tb, lt->a, lt->a, d, Mdev, Mmax, true);
-    TCL_LAUNCH(T, "lat:gemm_V", launch_gemm_f32(gv, kBias, -1, s));
     TCL_TRY(enqueue_block_f32(ac, T, "ac:", l, B, L, offs, Hac, xz, u, xdbl, s));
-    const GemmArgs gu = plain(Tb, lt->a, A.U, nullptr, Hac, d, d, lt->a, Mdev, Mmax, false);
-    TCL_LAUNCH(T, "lat:gemm_U", launch_gemm_f32(gu, kResid, -1, s));
-    ++j;
+    TCL_TRY(lateral(lt, T, j++, Hkb, Tb, Hac, d, Mdev, Mmax, false, s));
     TCL_TRY(enqueue_block_f32(kb, T, "kb:", l, B, L, offs, Hkb, xz, u, xdbl, s));
   }
   // final norm and pool of both columns (the tail's own head output is not used)

@@ -56,10 +56,11 @@ def test_paper_model_progressive_full_size_sampled():
     assert_scores_match(g[idx], _oracle(w.model, kb, ac, lat, w.adapter, X[idx], lengths[idx]), "f32", NAME)
 
 
-@pytest.mark.parametrize("a", [4, 8, 64])
+@pytest.mark.parametrize("a", [4, 8, 16, 64])
 def test_base_architecture_progressive(a):
     """The one-Linear encoder, two blocks with d_state 16, the two-layer
-    decoder; adapter widths 4 (below one MFMA K step), 8 and 64 (= d)."""
+    decoder; adapter widths 4, 8 and 16 (the fused per-row adapter kernel)
+    and 64 (= d, two GEMMs)."""
     shape = wl.TINY
     rng = np.random.default_rng(60 + a)
     kb = wl.init_params(shape, rng, perturb=True)
