@@ -417,7 +417,8 @@ def gemm_split(A, W, bias=None, out=None, stream=None, variant=-1, epilogue=0, o
     """The split-path fp32 GEMM (tcl_test_gemm_split). epilogue 0: A W^T
     (+ bias); 1: out += A W^T; 2: rstd(A) * A W^T; 3: A fp32 [B, L, K]
     gathered by offs [B+1], + bias, out [B*L, N]. variant 1 (32-row panels),
-    2 (16-row panels), 3 (32-row panels, all N in registers) or -1."""
+    2 (16-row panels), 3 (32-row panels, all N in registers), 4 (32-row
+    panels, K in two halves on two wavefronts per SIMD) or -1."""
     import torch
     N, K = W.shape
     if epilogue == 3:

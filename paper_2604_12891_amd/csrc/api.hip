@@ -734,8 +734,8 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
     M = B * L;
   }
   if (M <= 0 || N <= 0 || K <= 0 || K % 4) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
-  if (variant < -1 || variant > 3 || variant == 0)
-    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 1, 2 or 3 (got %d)", variant);
+  if (variant < -1 || variant > 4 || variant == 0)
+    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 1, 2, 3 or 4 (got %d)", variant);
   if ((epilogue == 1 || epilogue == 2) && d_bias)
     return fail(TCL_ERR_INVALID_ARG, "bias goes with epilogues 0 and 3 only");
   if (!d_A || !d_W || !d_C || !d_Wsplit) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");

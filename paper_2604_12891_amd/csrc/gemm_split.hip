@@ -91,20 +91,20 @@ __device__ __forceinline__ void load8(const float* arow, bool rok, int k, int K,
 // k = 8 (u % WU); rows past N and k past the padded K read zero through the
 // resource (the part stride is N ldw, so a row past N must not be read as
 // the next part's).
-template <int NR, int KC>
+template <int NR, int KC, int NT = kWaves * 64>
 struct WStage {
   static constexpr int WP = KC * 64 + 8;  // bf16 pitch of a staged row (conflict-free 16-byte reads)
   static constexpr int WU = KC * 8;       // 16-byte units per row
   static constexpr int NWU = 3 * NR * WU; // units per block
-  static constexpr int NW = (NWU + kWaves * 64 - 1) / (kWaves * 64);
+  static constexpr int NW = (NWU + NT - 1) / NT;
   u32x4 r[NW];
   __device__ __forceinline__ void load(const __amdgpu_buffer_rsrc_t& res, int tid, int n0, int N,
                                        int ldw, int Kw, int k0 = 0) {
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
-      const int u = tid + i * kWaves * 64;
+      const int u = tid + i * NT;
       const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = k0 + 8 * (u % WU);
-      const bool ok = (NWU % (kWaves * 64) == 0 || u < NWU) && n < N && k < Kw;
+      const bool ok = (NWU % NT == 0 || u < NWU) && n < N && k < Kw;
       const uint32_t off = ok ? (uint32_t)((((int64_t)part * N + n) * ldw + k) * 2) : kOutOfRange;
       r[i] = __builtin_amdgcn_raw_buffer_load_b128(res, off, 0, 0);
     }
@@ -112,9 +112,38 @@ struct WStage {
   __device__ __forceinline__ void stage(uint16_t* s, int tid) const {
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
-      const int u = tid + i * kWaves * 64;
-      if (NWU % (kWaves * 64) == 0 || u < NWU)
+      const int u = tid + i * NT;
+      if (NWU % NT == 0 || u < NWU)
         *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = r[i];
+    }
+  }
+};
+
+// The same units loaded and staged in two halves through NW / 2 + 1
+// registers: [0, H) then [H, NW).
+template <int NR, int KC, int NT>
+struct WStageHalves {
+  using S = WStage<NR, KC, NT>;
+  static constexpr int NW = S::NW, H = (NW + 1) / 2, WP = S::WP, WU = S::WU, NWU = S::NWU;
+  u32x4 r[H];
+  template <int I0, int I1>
+  __device__ __forceinline__ void load(const __amdgpu_buffer_rsrc_t& res, int tid, int n0, int N, int ldw, int Kw) {
+#pragma unroll
+    for (int i = I0; i < I1; ++i) {
+      const int u = tid + i * NT;
+      const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = 8 * (u % WU);
+      const bool ok = (NWU % NT == 0 || u < NWU) && n < N && k < Kw;
+      const uint32_t off = ok ? (uint32_t)((((int64_t)part * N + n) * ldw + k) * 2) : kOutOfRange;
+      r[i - I0] = __builtin_amdgcn_raw_buffer_load_b128(res, off, 0, 0);
+    }
+  }
+  template <int I0, int I1>
+  __device__ __forceinline__ void stage(uint16_t* s, int tid) const {
+#pragma unroll
+    for (int i = I0; i < I1; ++i) {
+      const int u = tid + i * NT;
+      if (NWU % NT == 0 || u < NWU)
+        *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = r[i - I0];
     }
   }
 };
@@ -252,6 +281,191 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
     }
   }
+}
+
+// ---------------------------------------------------------------- 32-row panels, K in two halves
+// The 32-row panel with K split between two wavefronts per SIMD: eight
+// wavefronts per workgroup, wavefront w owning rows 32 (w % 4) .. +31 and
+// the K half w / 4 (KH chunks of 64 each). Each holds only its half of A's
+// parts (half the registers of the one-wavefront panel), so two wavefronts
+// share every SIMD and one issues while the other waits. Per column block
+// the upper-half wavefronts park their partial sums in LDS at the end of the
+// block, and the lower-half wavefronts add them and run the epilogue of that
+// block while the next block's MFMAs go on (the W stage and the partials are
+// both double-buffered, one barrier per block).
+constexpr int kWavesH = 8;
+template <int KH, int FL>
+__global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs p, const uint16_t* Ws,
+                                                                        int ldws) {
+  constexpr int NSH = KH * 4;  // 16-k MFMA steps per half
+  constexpr int KC = 2 * KH;
+  constexpr int BM = 128;
+  constexpr int NT = kWavesH * 64;
+  using Stage = WStageHalves<32, KC, NT>;
+  constexpr int WP = Stage::WP;
+  constexpr int PART = 32 * WP;
+  constexpr int NW = Stage::NW, HW = Stage::H;
+  constexpr bool kNorm = (FL & kRowNorm) != 0;
+  static_assert((FL & kResid) == 0, "no residual epilogue");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
+  __shared__ __attribute__((aligned(16))) float sP[2][4][64][16];  // upper-half partial sums per lane
+  __shared__ float sSS[2][4][32];
+  __shared__ float sR[4][32];
+  __shared__ int sSrc[BM];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int g = wave & 3, h = wave >> 2;
+  const int li = lane & 31, lg = lane >> 5;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * BM;
+  if (row0 >= M) return;
+
+  for (int r = tid; r < BM; r += NT) {
+    const int grow = row0 + r;
+    int src = grow < M ? grow : -1;
+    if constexpr ((FL & kGather) != 0) {
+      if (src >= 0) {
+        int lo = 0, hi = p.B;
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (p.offs[mid] <= grow) lo = mid; else hi = mid;
+        }
+        src = lo * p.L + (grow - p.offs[lo]);
+      }
+    }
+    sSrc[r] = src;
+  }
+
+  const int Kw = (p.K + 7) & ~7;
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const int nsteps = (p.N + 31) / 32;
+  Stage st;
+  __syncthreads();  // sSrc
+
+  // prologue: row li of this wavefront's 32, lane half lg's 8 k of every
+  // step of this wavefront's K half
+  const int kh = h * KH * 64;
+  bf16x8 a1[NSH], a2[NSH], a3[NSH];
+  {
+    const int src = sSrc[g * 32 + li];
+    const float* arow = p.A + (src >= 0 ? (int64_t)src * p.lda : 0);
+    float ss = 0.f;
+#pragma unroll
+    for (int s = 0; s < NSH; ++s) {
+      floatx4 v0, v1;
+      load8(arow, src >= 0, kh + 16 * s + 8 * lg, p.K, v0, v1);
+      if constexpr (kNorm)
+        ss += v0.x * v0.x + v0.y * v0.y + v0.z * v0.z + v0.w * v0.w + v1.x * v1.x + v1.y * v1.y +
+              v1.z * v1.z + v1.w * v1.w;
+      split8(v0, v1, a1[s], a2[s], a3[s]);
+    }
+    if constexpr (kNorm) {
+      ss += __shfl_xor(ss, 32, 64);
+      if (lg == 0) sSS[h][g][li] = ss;
+    }
+  }
+
+  const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * 4);
+  const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
+
+  st.template load<0, HW>(wres, tid, 0, p.N, ldws, Kw);
+  st.template stage<0, HW>(&sW[0], tid);
+  st.template load<HW, NW>(wres, tid, 0, p.N, ldws, Kw);
+  st.template stage<HW, NW>(&sW[0], tid);
+  if constexpr (kNorm) {
+    __syncthreads();  // both halves' sums of squares
+    if (h == 0 && lg == 0) sR[g][li] = 1.0f / sqrtf((sSS[0][g][li] + sSS[1][g][li]) / (float)p.K + p.eps);
+  }
+
+  // the lower-half wavefronts finish block s: its upper-half partials from
+  // LDS, row scale, bias, activation, buffer stores
+  floatx16 res;
+  auto epilogue = [&](int s) {
+    const int col = s * 32 + li;
+    const bool cok = col < p.N;
+    const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+    const floatx4* pp = reinterpret_cast<const floatx4*>(&sP[s & 1][g][lane][0]);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const floatx4 o = pp[q];
+      res[4 * q] += o.x;
+      res[4 * q + 1] += o.y;
+      res[4 * q + 2] += o.z;
+      res[4 * q + 3] += o.w;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      float v = res[r];
+      if constexpr (kNorm) v *= sR[g][rl];
+      v += bias;
+      if (p.relu) v = fmaxf(v, 0.f);
+      const uint32_t off = cok ? (uint32_t)(((g * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+    }
+  };
+
+  for (int s = 0; s < nsteps; ++s) {
+    const int buf = s & 1, n0 = s * 32;
+    // block s staged and block s-1's partials parked; every wavefront is
+    // past block s-1's fragment reads and the partials of block s-2
+    __syncthreads();
+    const bool more = s + 1 < nsteps;
+    // the next block's W in two halves: the first loaded now and staged
+    // halfway through the MFMAs, the second loaded then and staged at the end
+    if (more) st.template load<0, HW>(wres, tid, n0 + 32, p.N, ldws, Kw);
+    if (h == 0 && s > 0) epilogue(s - 1);
+
+    floatx16 acc, acc2;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = acc2[r] = 0.f;
+    const uint16_t* wb = &sW[buf * 3 * PART + li * WP + 8 * lg + kh];
+    auto wfrag = [&](int part, int ks) {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+    };
+    // W fragments one k-step ahead of their MFMAs (the other wavefront on
+    // the SIMD covers the rest of the LDS latency)
+    bf16x8 q[2][3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) q[0][j] = wfrag(j, 0);
+    __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+#pragma unroll
+    for (int ks = 0; ks < NSH; ++ks) {
+      if (ks + 1 < NSH) {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) q[(ks + 1) & 1][j] = wfrag(j, ks + 1);
+      }
+      const bf16x8* w = q[ks & 1];
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], acc, 0, 0, 0);
+      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], acc2, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc, 0, 0, 0);
+      if (ks + 1 < NSH) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+      if (ks == NSH / 2 && more) {
+        st.template stage<0, HW>(&sW[(buf ^ 1) * 3 * PART], tid);
+        st.template load<HW, NW>(wres, tid, n0 + 32, p.N, ldws, Kw);
+        __builtin_amdgcn_sched_group_barrier(0x0200, HW, 0);
+      }
+    }
+    if (more) st.template stage<HW, NW>(&sW[(buf ^ 1) * 3 * PART], tid);
+    if (h == 1) {
+      floatx4* pp = reinterpret_cast<floatx4*>(&sP[buf][g][lane][0]);
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        pp[q4] = floatx4{acc[4 * q4] + acc2[4 * q4], acc[4 * q4 + 1] + acc2[4 * q4 + 1],
+                         acc[4 * q4 + 2] + acc2[4 * q4 + 2], acc[4 * q4 + 3] + acc2[4 * q4 + 3]};
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) res[r] = acc[r] + acc2[r];
+    }
+  }
+  __syncthreads();
+  if (h == 0) epilogue(nsteps - 1);
 }
 
 // ---------------------------------------------------------------- 16-row panels
@@ -501,6 +715,18 @@ hipError_t launch32(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t
 }
 
 template <int FL>
+hipError_t launch32h(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
+  const int grid = (a.Mmax + 127) / 128;
+  if (grid <= 0) return hipSuccess;
+  switch ((a.K + 127) / 128) {
+    case 1: hipLaunchKernelGGL((gemm_split32h_kernel<1, FL>), dim3(grid), dim3(kWavesH * 64), 0, s, a, Ws, ldws); break;
+    case 2: hipLaunchKernelGGL((gemm_split32h_kernel<2, FL>), dim3(grid), dim3(kWavesH * 64), 0, s, a, Ws, ldws); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int FL>
 hipError_t launch16(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
   const int grid = (a.Mmax + kWaves * 16 - 1) / (kWaves * 16);
   if (grid <= 0) return hipSuccess;
@@ -575,6 +801,7 @@ bool gemm_split_supports(const GemmArgs& a, int flags, int variant) {
   const bool plain = (flags & (kRowNorm | kGather)) == 0;
   switch (variant) {
     case kSplit32: return (flags & kResid) == 0 && kc <= 4;
+    case kSplit32H: return (flags & kResid) == 0 && kc <= 4 && (int64_t)128 * a.ldc * 4 < (1ll << 31);
     case kSplit16: return plain && (kc == 1 || kc == 2 || kc == 4 || kc == 8);
     case kSplit32Acc: return plain && kc <= 8 && a.N <= 256;
     default: return false;
@@ -584,6 +811,11 @@ bool gemm_split_supports(const GemmArgs& a, int flags, int variant) {
 int gemm_split_variant(const GemmArgs& a, int flags) {
   // 32-row panels first (half the LDS traffic per flop of 16-row ones);
   // streaming N blocks when K fits one chunk, else all of N in registers
+  // K in (192, 256]: the K halves on two wavefronts per SIMD (measured on
+  // MI355X for in_proj, 61,715 x 1024 x 256 with the RMSNorm: 17% faster than
+  // one wavefront per row group); below that the upper half would be mostly
+  // padding (the input Linear, K = 164: 12% slower)
+  if ((a.K + 63) / 64 == 4 && gemm_split_supports(a, flags, kSplit32H)) return kSplit32H;
   if ((flags & kResid) == 0 && gemm_split_supports(a, flags, kSplit32)) return kSplit32;
   if (gemm_split_supports(a, flags, kSplit32Acc)) return kSplit32Acc;
   if (gemm_split_supports(a, flags, kSplit16)) return kSplit16;
@@ -599,6 +831,15 @@ hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, in
       case 0: return launch32acc<0>(a, Ws, ldws, s);
       case kBias: return launch32acc<kBias>(a, Ws, ldws, s);
       case kResid: return launch32acc<kResid>(a, Ws, ldws, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  if (variant == kSplit32H) {
+    switch (flags) {
+      case 0: return launch32h<0>(a, Ws, ldws, s);
+      case kBias: return launch32h<kBias>(a, Ws, ldws, s);
+      case kRowNorm: return launch32h<kRowNorm>(a, Ws, ldws, s);
+      case kBias | kGather: return launch32h<kBias | kGather>(a, Ws, ldws, s);
       default: return hipErrorInvalidValue;
     }
   }

@@ -70,8 +70,10 @@ hipError_t launch_gemm_f32_panel16(const GemmArgs& a, int flags, hipStream_t s);
 //   kSplit16: 16-row blocks, K rounded up to 64 in {64, 128, 256, 512}, no
 //             RMSNorm or gather;
 //   kSplit32Acc: 32-row blocks with all N columns accumulated in registers,
-//             N <= 256, K <= 512, no RMSNorm or gather.
-enum GemmSplitVariant { kSplit32 = 1, kSplit16 = 2, kSplit32Acc = 3 };
+//             N <= 256, K <= 512, no RMSNorm or gather;
+//   kSplit32H: 32-row blocks with K split between two wavefronts per SIMD
+//             (half the A registers each), K <= 256, no residual.
+enum GemmSplitVariant { kSplit32 = 1, kSplit16 = 2, kSplit32Acc = 3, kSplit32H = 4 };
 bool gemm_split_supports(const GemmArgs& a, int flags, int variant);
 int gemm_split_variant(const GemmArgs& a, int flags);  // the variant the model uses, or -1 (none)
 // variant < 0: gemm_split_variant's pick; hipErrorInvalidValue if unsupported

@@ -382,15 +382,18 @@ def _split_ref(A, W, mode, bv=None, C0=None):
 @pytest.mark.parametrize("M,N,K", [(1, 64, 4), (129, 256, 164), (1000, 1024, 256), (77, 100, 36),
                                    (300, 48, 64), (40000, 96, 192)])
 @pytest.mark.parametrize("mode", ["plain", "bias", "norm"])
-def test_gemm_split32(M, N, K, mode):
-    """32-row split panels (K <= 256): plain, + bias, RMSNorm row scale; ragged
-    M, N and K (K % 8 == 4 exercises a half-filled last k unit)."""
-    print(f"gemm split32 mode={mode} M={M} N={N} K={K}", flush=True)
+@pytest.mark.parametrize("variant", [1, 4])
+def test_gemm_split32(M, N, K, mode, variant):
+    """32-row split panels (K <= 256), one wavefront per panel row group
+    (variant 1) or the K halves on two (variant 4): plain, + bias, RMSNorm
+    row scale; ragged M, N and K (K % 8 == 4 exercises a half-filled last k
+    unit; K <= 128 leaves the upper half empty)."""
+    print(f"gemm split32 variant={variant} mode={mode} M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(M + 3 * N + 17 * K + len(mode))
     A = rng.standard_normal((M, K)).astype(np.float32)
     W = rng.standard_normal((N, K)).astype(np.float32)
     bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
-    C = tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, variant=1,
+    C = tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, variant=variant,
                       epilogue=2 if mode == "norm" else 0)
     torch.cuda.synchronize()
     ref, bound = _split_ref(A, W, mode, bv)
@@ -419,7 +422,8 @@ def test_gemm_split16(M, N, K, mode):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
-def test_gemm_split_gather():
+@pytest.mark.parametrize("variant", [1, 4])
+def test_gemm_split_gather(variant):
     """The input Linear on the split path: rows gathered from padded [B, L, F]
     features by token offsets, + bias; the padding (NaN here) is never read."""
     rng = np.random.default_rng(41)
@@ -431,7 +435,7 @@ def test_gemm_split_gather():
     W = rng.standard_normal((N, K)).astype(np.float32)
     bv = rng.standard_normal(N).astype(np.float32)
     offs = _offs(lengths)
-    C = tb.gemm_split(_dev(X), _dev(W), _dev(bv), variant=1, epilogue=3, offs=_dev(offs, torch.int32))
+    C = tb.gemm_split(_dev(X), _dev(W), _dev(bv), variant=variant, epilogue=3, offs=_dev(offs, torch.int32))
     torch.cuda.synchronize()
     Ap = _pack(X, lengths)
     ref, bound = _split_ref(Ap, W, "bias", bv)
@@ -446,7 +450,8 @@ def test_gemm_split_error_matches_native_fp32():
     projection shapes its rms error against fp64 stays within 1.5x of the
     fp32 MFMA kernel's (and both within the fp32 bound above)."""
     rng = np.random.default_rng(7)
-    for (M, N, K, variant, tile) in [(4096, 1024, 256, 1, 8), (4096, 256, 512, 3, 9), (4096, 256, 512, 2, 9)]:
+    for (M, N, K, variant, tile) in [(4096, 1024, 256, 1, 8), (4096, 1024, 256, 4, 8), (4096, 256, 512, 3, 9),
+                                     (4096, 256, 512, 2, 9)]:
         A = rng.standard_normal((M, K)).astype(np.float32)
         W = (rng.uniform(-1, 1, (N, K)) / np.sqrt(K)).astype(np.float32)
         ref = A.astype(np.float64) @ W.astype(np.float64).T
@@ -464,12 +469,16 @@ def test_gemm_split_refuses_unsupported():
     W = _dev(rng.standard_normal((64, 320)).astype(np.float32))
     with pytest.raises(tb.TclError):        # 32-row panels stop at K = 256
         tb.gemm_split(A, W, variant=1)
+    with pytest.raises(tb.TclError):        # ... also with K in two halves
+        tb.gemm_split(A, W, variant=4)
     with pytest.raises(tb.TclError):        # K = 320 rounds up to 384: no 16-row kernel
         tb.gemm_split(A, W, variant=2)
     A2 = _dev(rng.standard_normal((64, 256)).astype(np.float32))
     W2 = _dev(rng.standard_normal((64, 256)).astype(np.float32))
     with pytest.raises(tb.TclError):        # no residual epilogue on streaming 32-row panels
         tb.gemm_split(A2, W2, out=torch.zeros(64, 64, device="cuda"), variant=1, epilogue=1)
+    with pytest.raises(tb.TclError):
+        tb.gemm_split(A2, W2, out=torch.zeros(64, 64, device="cuda"), variant=4, epilogue=1)
     with pytest.raises(tb.TclError):        # no RMSNorm on 16-row panels
         tb.gemm_split(A2, W2, variant=2, epilogue=2)
     with pytest.raises(tb.TclError):        # no RMSNorm with all of N in registers
