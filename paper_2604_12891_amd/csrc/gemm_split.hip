@@ -309,7 +309,10 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
   static_assert((FL & kResid) == 0, "no residual epilogue");
 
   __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
-  __shared__ __attribute__((aligned(16))) float sP[2][4][64][16];  // upper-half partial sums per lane
+  // upper-half partial sums, [buffer][row group][quarter q][lane][4]: a
+  // lane's four values of quarter q are one 16-byte unit and consecutive
+  // lanes' units are consecutive (conflict-free 16-byte accesses)
+  __shared__ __attribute__((aligned(16))) float sP[2][4][4][64][4];
   __shared__ float sSS[2][4][32];
   __shared__ float sR[4][32];
   __shared__ int sSrc[BM];
@@ -386,10 +389,9 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
     const int col = s * 32 + li;
     const bool cok = col < p.N;
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
-    const floatx4* pp = reinterpret_cast<const floatx4*>(&sP[s & 1][g][lane][0]);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const floatx4 o = pp[q];
+      const floatx4 o = *reinterpret_cast<const floatx4*>(&sP[s & 1][g][q][lane][0]);
       res[4 * q] += o.x;
       res[4 * q + 1] += o.y;
       res[4 * q + 2] += o.z;
@@ -454,11 +456,11 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
     }
     if (more) st.template stage<HW, NW>(&sW[(buf ^ 1) * 3 * PART], tid);
     if (h == 1) {
-      floatx4* pp = reinterpret_cast<floatx4*>(&sP[buf][g][lane][0]);
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4)
-        pp[q4] = floatx4{acc[4 * q4] + acc2[4 * q4], acc[4 * q4 + 1] + acc2[4 * q4 + 1],
-                         acc[4 * q4 + 2] + acc2[4 * q4 + 2], acc[4 * q4 + 3] + acc2[4 * q4 + 3]};
+        *reinterpret_cast<floatx4*>(&sP[buf][g][q4][lane][0]) =
+            floatx4{acc[4 * q4] + acc2[4 * q4], acc[4 * q4 + 1] + acc2[4 * q4 + 1],
+                    acc[4 * q4 + 2] + acc2[4 * q4 + 2], acc[4 * q4 + 3] + acc2[4 * q4 + 3]};
     } else {
 #pragma unroll
       for (int r = 0; r < 16; ++r) res[r] = acc[r] + acc2[r];
