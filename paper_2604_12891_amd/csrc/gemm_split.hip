@@ -39,6 +39,8 @@
 // Fragment k-order (A and W alike, which is all the contraction needs):
 // split32 k-step s, lane half g holds k = 16 s + 8 g .. +7; split16 k-step
 // s, lane quarter q holds k = 32 s + 8 q .. +7.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -409,65 +411,76 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
     }
   };
 
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1, n0 = s * 32;
-    // block s staged and block s-1's partials parked; every wavefront is
-    // past block s-1's fragment reads and the partials of block s-2
-    __syncthreads();
-    const bool more = s + 1 < nsteps;
-    // the next block's W in two halves: the first loaded now and staged
-    // halfway through the MFMAs, the second loaded then and staged at the end
-    if (more) st.template load<0, HW>(wres, tid, n0 + 32, p.N, ldws, Kw);
-    if (h == 0 && s > 0) epilogue(s - 1);
+  // The block loop, compiled once per K half (a wavefront-uniform choice):
+  // the lower half's epilogue stores are then only on its own path, so the
+  // wait for the W stage's loads (issued before them) need not wait for the
+  // stores as well, as it would after a join with the upper half's path.
+  auto blocks = [&](auto lower_tag) {
+    constexpr bool LOWER = decltype(lower_tag)::value;
+    for (int s = 0; s < nsteps; ++s) {
+      const int buf = s & 1, n0 = s * 32;
+      // block s staged and block s-1's partials parked; every wavefront is
+      // past block s-1's fragment reads and the partials of block s-2
+      __syncthreads();
+      const bool more = s + 1 < nsteps;
+      // the next block's W in two halves: the first loaded now and staged
+      // halfway through the MFMAs, the second loaded then and staged at the end
+      if (more) st.template load<0, HW>(wres, tid, n0 + 32, p.N, ldws, Kw);
+      if (LOWER && s > 0) epilogue(s - 1);
 
-    floatx16 acc, acc2;
+      floatx16 acc, acc2;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = acc2[r] = 0.f;
-    const uint16_t* wb = &sW[buf * 3 * PART + li * WP + 8 * lg + kh];
-    auto wfrag = [&](int part, int ks) {
-      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
-    };
-    // W fragments one k-step ahead of their MFMAs (the other wavefront on
-    // the SIMD covers the rest of the LDS latency)
-    bf16x8 q[2][3];
+      for (int r = 0; r < 16; ++r) acc[r] = acc2[r] = 0.f;
+      const uint16_t* wb = &sW[buf * 3 * PART + li * WP + 8 * lg + kh];
+      auto wfrag = [&](int part, int ks) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+      };
+      // W fragments one k-step ahead of their MFMAs (the other wavefront on
+      // the SIMD covers the rest of the LDS latency)
+      bf16x8 q[2][3];
 #pragma unroll
-    for (int j = 0; j < 3; ++j) q[0][j] = wfrag(j, 0);
-    __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+      for (int j = 0; j < 3; ++j) q[0][j] = wfrag(j, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
 #pragma unroll
-    for (int ks = 0; ks < NSH; ++ks) {
-      if (ks + 1 < NSH) {
+      for (int ks = 0; ks < NSH; ++ks) {
+        if (ks + 1 < NSH) {
 #pragma unroll
-        for (int j = 0; j < 3; ++j) q[(ks + 1) & 1][j] = wfrag(j, ks + 1);
+          for (int j = 0; j < 3; ++j) q[(ks + 1) & 1][j] = wfrag(j, ks + 1);
+        }
+        const bf16x8* w = q[ks & 1];
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], acc2, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], acc, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], acc2, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], acc, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], acc2, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc, 0, 0, 0);
+        if (ks + 1 < NSH) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+        if (ks == NSH / 2 && more) {
+          st.template stage<0, HW>(&sW[(buf ^ 1) * 3 * PART], tid);
+          st.template load<HW, NW>(wres, tid, n0 + 32, p.N, ldws, Kw);
+          __builtin_amdgcn_sched_group_barrier(0x0200, HW, 0);
+        }
       }
-      const bf16x8* w = q[ks & 1];
-      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], acc2, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], acc, 0, 0, 0);
-      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], acc2, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], acc, 0, 0, 0);
-      acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], acc2, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc, 0, 0, 0);
-      if (ks + 1 < NSH) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
-      __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
-      if (ks == NSH / 2 && more) {
-        st.template stage<0, HW>(&sW[(buf ^ 1) * 3 * PART], tid);
-        st.template load<HW, NW>(wres, tid, n0 + 32, p.N, ldws, Kw);
-        __builtin_amdgcn_sched_group_barrier(0x0200, HW, 0);
+      if (more) st.template stage<HW, NW>(&sW[(buf ^ 1) * 3 * PART], tid);
+      if constexpr (!LOWER) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          *reinterpret_cast<floatx4*>(&sP[buf][g][q4][lane][0]) =
+              floatx4{acc[4 * q4] + acc2[4 * q4], acc[4 * q4 + 1] + acc2[4 * q4 + 1],
+                      acc[4 * q4 + 2] + acc2[4 * q4 + 2], acc[4 * q4 + 3] + acc2[4 * q4 + 3]};
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) res[r] = acc[r] + acc2[r];
       }
     }
-    if (more) st.template stage<HW, NW>(&sW[(buf ^ 1) * 3 * PART], tid);
-    if (h == 1) {
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-        *reinterpret_cast<floatx4*>(&sP[buf][g][q4][lane][0]) =
-            floatx4{acc[4 * q4] + acc2[4 * q4], acc[4 * q4 + 1] + acc2[4 * q4 + 1],
-                    acc[4 * q4 + 2] + acc2[4 * q4 + 2], acc[4 * q4 + 3] + acc2[4 * q4 + 3]};
-    } else {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) res[r] = acc[r] + acc2[r];
-    }
-  }
-  __syncthreads();
-  if (h == 0) epilogue(nsteps - 1);
+    __syncthreads();
+    if constexpr (LOWER) epilogue(nsteps - 1);
+  };
+  if (__builtin_amdgcn_readfirstlane(h) == 0)
+    blocks(std::true_type{});
+  else
+    blocks(std::false_type{});
 }
 
 // ---------------------------------------------------------------- 16-row panels
