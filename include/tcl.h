@@ -86,9 +86,9 @@ typedef enum tcl_dtype {
                    create; pass bf16-representable values to avoid that.    */
 } tcl_dtype;
 
-/* How an fp32 model runs its dense projections (the input Linear, in_proj
- * and out_proj; x_proj, which moves more bytes than it computes, stays on
- * the fp32 path either way). */
+/* How an fp32 model runs its dense projections (the encoder's Linear
+ * layers, in_proj, x_proj and out_proj; a shape without a split kernel,
+ * such as d_inner > 512 for x_proj and out_proj, runs on the fp32 path). */
 typedef enum tcl_f32_matmul {
   TCL_F32_MATMUL_SPLIT = 0, /* bf16 matrix cores, fp32 accuracy: both operands
                                split exactly into three bf16 parts, the six

@@ -182,7 +182,7 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   GemmArgs gx;
   gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
   gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-  TCL_LAUNCH(T, (tag + "gemm_x_proj").c_str(), launch_gemm_f32(gx, 0, -1, s));
+  TCL_LAUNCH(T, (tag + "gemm_x_proj").c_str(), model_gemm(m, gx, W.W_x_s, E, 0, s));
   if (chunks > 0)
     TCL_LAUNCH(T, (tag + "scan_chunked").c_str(),
                launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E, 2 * E, W.W_dt, W.b_dt,
@@ -338,7 +338,7 @@ struct ModelPlan {
   int ldw0 = 0;
   struct L {
     size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
-    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_out_s;
+    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_x_s, W_out_s;
   };
   std::vector<L> layers;
   int ldw0_h = 0;
@@ -422,6 +422,7 @@ ModelPlan plan_model(const tcl_config& c) {
     }
     if (sp) {
       L.W_in_s = job(B.W_in, 2 * E, d, kDeriveFoldSplit, 0, 2, -1, B.g);
+      L.W_x_s = job(B.W_x, XW, E, kDeriveSplit, 0, 2);
       L.W_out_s = job(B.W_out, d, E, kDeriveSplit, 0, 2);
     }
     P.layers.push_back(L);
@@ -529,6 +530,7 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
     }
     if (m->split) {
       W.W_in_s = B16(L.W_in_s);
+      W.W_x_s = B16(L.W_x_s);
       W.W_out_s = B16(L.W_out_s);
     }
     m->layers.push_back(W);

@@ -98,8 +98,8 @@ struct tcl_model {
     // bf16 copies (bf16 models)
     uint16_t *W_in_h, *W_x_h, *W_out_h;
     // three-way bf16 splits, [3][rows][cols] (fp32 models on the split path):
-    // W_in with the gain folded, W_out
-    uint16_t *W_in_s, *W_out_s;
+    // W_in with the gain folded, W_x, W_out
+    uint16_t *W_in_s, *W_x_s, *W_out_s;
   };
   float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1 = nullptr, *W1T = nullptr,
         *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;
