@@ -164,7 +164,8 @@ struct RduState {
   int last;          // the last selected program (-1: none yet)
   int done;
   int n_select;
-  int pad_[3];
+  unsigned arrived;  // blocks of the current grid pass that have parked their partial
+  int pad_[2];
 };
 
 struct Best {
@@ -406,87 +407,104 @@ __global__ __launch_bounds__(kST) void rdu_mark_kernel(int N, const int* __restr
   }
 }
 
-// one iteration, grid pass: distances, masks, t_s, block argmax
+// one iteration, grid pass: distances, masks, t_s, block argmax; the last
+// block to finish reduces the blocks' partials and labels the winner.
+// Candidates go four per thread per round, their loads issued together.
+constexpr int kRduUnroll = 4;
 __global__ __launch_bounds__(kST) void rdu_score_kernel(int N, const float* __restrict__ s,
                                                         const int* __restrict__ op, int n_ops,
                                                         const double* __restrict__ budget,
-                                                        const int* __restrict__ sel,
-                                                        const RduState* __restrict__ state,
-                                                        double* __restrict__ d, Best* __restrict__ part) {
+                                                        int* __restrict__ sel, RduState* __restrict__ state,
+                                                        double* __restrict__ d, Best* __restrict__ part,
+                                                        int* __restrict__ out) {
   __shared__ double bt[kST];
   __shared__ int bi[kST];
+  __shared__ int am_last;
   const RduState st = *state;
   if (st.done) return;
   const double fl = st.last >= 0 ? fhat(s, st.last, st) : 0.0;
   const double inv = 1.0 / (double)(st.M + 1);
   double best_t = 0.0;
   int best_i = -1;
-  for (int i = blockIdx.x * kST + threadIdx.x; i < N; i += gridDim.x * kST) {
-    double di = d[i];
-    if (di < 0.0) continue;  // labeled, or its operator's budget is used up
-    const int o = op[i];
-    if (o < 0 || o >= n_ops || (double)sel[o] >= budget[o]) {
-      d[i] = -1.0;
-      continue;
+  constexpr int U = kRduUnroll;
+  for (int i0 = blockIdx.x * kST * U + threadIdx.x; i0 < N; i0 += gridDim.x * kST * U) {
+    double dv[U];
+    int ov[U];
+    float sv[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int i = i0 + k * kST;
+      const bool ok = i < N;
+      dv[k] = ok ? d[i] : -1.0;
+      ov[k] = ok ? op[i] : -1;
+      sv[k] = ok ? s[i] : 0.f;
     }
-    const double fi = fhat(s, i, st);
-    if (st.last >= 0) {
-      const double dn = fabs(fi - fl);  // Eq. (1) as a running minimum
-      if (dn < di) {
-        di = dn;
-        d[i] = dn;
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int i = i0 + k * kST;
+      double di = dv[k];
+      if (di < 0.0) continue;  // labeled, past the end, or its operator's budget is used up
+      const int o = ov[k];
+      if (o < 0 || o >= n_ops || (double)sel[o] >= budget[o]) {
+        d[i] = -1.0;
+        continue;
       }
-    }
-    const double mu = (fi + st.S1) * inv;                 // Eq. (2)
-    const double u = (fi * fi + st.S2) * inv - mu * mu;   // Eq. (3), from the running sums
-    const double t = fi * di + u;
-    if (better(t, i, best_t, best_i)) {
-      best_t = t;
-      best_i = i;
+      const double fi = st.range > 0.0 ? ((double)sv[k] - st.lo) / st.range : 0.0;
+      if (st.last >= 0) {
+        const double dn = fabs(fi - fl);  // Eq. (1) as a running minimum
+        if (dn < di) {
+          di = dn;
+          d[i] = dn;
+        }
+      }
+      const double mu = (fi + st.S1) * inv;                 // Eq. (2)
+      const double u = (fi * fi + st.S2) * inv - mu * mu;   // Eq. (3), from the running sums
+      const double t = fi * di + u;
+      if (better(t, i, best_t, best_i)) {
+        best_t = t;
+        best_i = i;
+      }
     }
   }
   const Best b = block_best(best_t, best_i, bt, bi);
-  if (threadIdx.x == 0) part[blockIdx.x] = b;
-}
-
-// one iteration, one block: label the winner
-__global__ __launch_bounds__(kST) void rdu_pick_kernel(int nparts, const float* __restrict__ s,
-                                                       const int* __restrict__ op, const Best* __restrict__ part,
-                                                       int* __restrict__ sel, double* __restrict__ d,
-                                                       RduState* __restrict__ state, int* __restrict__ out) {
-  __shared__ double bt[kST];
-  __shared__ int bi[kST];
-  __shared__ int sdone;
-  if (threadIdx.x == 0) sdone = state->done;
+  if (threadIdx.x == 0) {
+    part[blockIdx.x] = b;
+    __threadfence();  // the partial is visible before the arrival is counted
+    am_last = atomicAdd(&state->arrived, 1u) == gridDim.x - 1;
+  }
   __syncthreads();
-  if (sdone) return;
+  if (!am_last) return;
+
+  // the last block: every partial is in; reduce them and label the winner
+  __threadfence();
   double t = 0.0;
   int i = -1;
-  for (int p = threadIdx.x; p < nparts; p += kST) {
-    const Best b = part[p];
-    if (b.i >= 0 && better(b.t, b.i, t, i)) {
-      t = b.t;
-      i = b.i;
+  for (int q = threadIdx.x; q < (int)gridDim.x; q += kST) {
+    const Best pq = part[q];
+    if (pq.i >= 0 && better(pq.t, pq.i, t, i)) {
+      t = pq.t;
+      i = pq.i;
     }
   }
   const Best w = block_best(t, i, bt, bi);
   if (threadIdx.x == 0) {
-    RduState st = *state;
+    RduState ns = st;
+    ns.arrived = 0;
     if (w.i < 0) {
-      st.done = 1;
+      ns.done = 1;
     } else {
       const double f = fhat(s, w.i, st);
-      out[st.count] = w.i;
-      st.count += 1;
-      st.M += 1;
-      st.S1 += f;
-      st.S2 += f * f;
-      st.last = w.i;
+      out[ns.count] = w.i;
+      ns.count += 1;
+      ns.M += 1;
+      ns.S1 += f;
+      ns.S2 += f * f;
+      ns.last = w.i;
       sel[op[w.i]] += 1;
       d[w.i] = -1.0;
-      if (st.count >= st.n_select) st.done = 1;
+      if (ns.count >= ns.n_select) ns.done = 1;
     }
-    *state = st;
+    *state = ns;
   }
 }
 
@@ -641,11 +659,10 @@ hipError_t launch_rdu_select(int N, const float* s, const int* op, int n_ops, co
   }
   if (n_init > 0)
     hipLaunchKernelGGL(rdu_mark_kernel, dim3((n_init + kST - 1) / kST), dim3(kST), 0, st, N, init, n_init, d);
-  for (int it = 0; it < n_select; ++it) {
-    hipLaunchKernelGGL(rdu_score_kernel, dim3(grid), dim3(kST), 0, st, N, s, op, n_ops, budget, sel, state, d,
-                       part);
-    hipLaunchKernelGGL(rdu_pick_kernel, dim3(1), dim3(kST), 0, st, grid, s, op, part, sel, d, state, out);
-  }
+  const int sgrid = std::min((N + kST * kRduUnroll - 1) / (kST * kRduUnroll), kRduGrid);
+  for (int it = 0; it < n_select; ++it)
+    hipLaunchKernelGGL(rdu_score_kernel, dim3(sgrid), dim3(kST), 0, st, N, s, op, n_ops, budget, sel, state, d,
+                       part, out);
   hipLaunchKernelGGL(rdu_finish_kernel, dim3(1), dim3(kST), 0, st, n_select, state, out, count);
   return hipGetLastError();
 }
