@@ -142,9 +142,11 @@ def cpu_baseline(w, blob, X, lengths, target_s: float) -> dict:
     dt = time.perf_counter() - t
     blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
     threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    libs = sorted({f"{p.get('internal_api', '?')} {p.get('version', '')}".strip() for p in blas})
     return {"value": n / dt, "unit": "programs/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} of {len(lengths)} programs (evenly strided) of the same batch, numpy fp64, "
-                      f"{dt:.1f} s; host has {os.cpu_count()} CPUs, affinity {len(os.sched_getaffinity(0))}"}
+                      f"{dt:.1f} s; host has {os.cpu_count()} CPUs, affinity {len(os.sched_getaffinity(0))}, "
+                      f"BLAS {', '.join(libs) or 'none'} with {threads} threads"}
 
 
 def distill_kernel_work(tshape, sshape, M_v: int, B: int) -> dict:
@@ -648,6 +650,21 @@ def main():
     ms = e0.elapsed_time(e1) / args.steps
     assert torch.isfinite(out).all().item(), "non-finite scores"
 
+    # context only (never the value): the same steps with the features copied
+    # from pinned host memory on the same stream first
+    Xh = torch.from_numpy(X).pin_memory()
+    Lh = torch.from_numpy(lengths).pin_memory()
+    torch.cuda.synchronize()
+    e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e2.record()
+    for _ in range(args.steps):
+        Xd.copy_(Xh, non_blocking=True)
+        Ld.copy_(Lh, non_blocking=True)
+        model.score(Xd, Ld, out=out, workspace=ws)
+    e3.record()
+    torch.cuda.synchronize()
+    ms_h2d = e2.elapsed_time(e3) / args.steps
+
     # the same K steps again with every kernel bracketed by events on its stream
     model.timing(True)
     model.timing_reset()
@@ -720,6 +737,11 @@ def main():
         "roofline": roof,
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
                     for k, e in kernels.items()},
+        "pcie_context": {"ms_per_step_incl_h2d": round(ms_h2d, 5),
+                         "programs_per_s_incl_h2d": w.B / (ms_h2d * 1e-3),
+                         "h2d_bytes": int(X.nbytes + lengths.nbytes),
+                         "note": "features copied from pinned host memory on the scoring stream before every "
+                                 "step; context only, value excludes it"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
