@@ -67,6 +67,9 @@ def kernel_work(shape, M_v: int, B: int, dtype: str, L: int = 0) -> dict:
         "gemm_x_proj": ("byte", M_v * (E * a + XW * 4)),
         "gemm_out_proj": ("flop", 2 * M_v * E * d),
         "conv_silu": ("byte", M_v * 2 * E * a),
+        # the conv fused in front of x_proj: reads x, writes u and [dt_r | B | C]
+        "gemm_x_proj_conv": ("byte", M_v * (2 * E * a + XW * 4)),
+        "token_pos": ("byte", B * 8 + M_v),
         # VALU-bound: 2 flops per issue slot against the fp32 vector peak;
         # its HBM bytes are reported beside it
         "scan": ("valu", (2 * M_v * E * scan_valu_slots(N, R), M_v * (3 * E * a + XW * 4))),

@@ -453,6 +453,23 @@ TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const
                                           const float* d_x, int32_t ldx, const float* d_w,
                                           const float* d_b, float* d_u, void* stream);
 
+/* x_proj with the causal conv + SiLU in front (the split path's fused
+ * kernel, section 5.2's Mamba block: conv, SiLU, then the projection to
+ * [dt_r | B | C]): u = SiLU(conv_b + causal depthwise conv(x; conv_w)) per
+ * program and xdbl = u W^T, fp32 with fp32 accuracy. Kernel size 4;
+ * E a multiple of 64, <= 512; 1 <= N <= 64; ldx >= E a multiple of 4.
+ * d_offs [B+1] int32 prefix sums of the lengths; rows = Mmax >= d_offs[B]
+ * bounds the grid; d_x [rows, ldx]; d_w [E, 4], d_b [E]; d_W [N, E];
+ * d_u [rows, E], d_xdbl [rows, N] (rows past d_offs[B] are not written).
+ * Scratch (caller-owned, device): d_Wsplit 3 N E uint16, d_tpos rows bytes.
+ * Every pointer but d_tpos 16-byte aligned. Unsupported shapes give
+ * TCL_ERR_UNSUPPORTED. */
+TCL_API tcl_status tcl_test_xproj_conv_f32(int32_t B, int32_t rows, int32_t E, int32_t N,
+                                           const int32_t* d_offs, const float* d_x, int32_t ldx,
+                                           const float* d_w, const float* d_b, const float* d_W,
+                                           uint16_t* d_Wsplit, uint8_t* d_tpos, float* d_u,
+                                           float* d_xdbl, void* stream);
+
 /* Selective scan with its dt_proj + softplus prologue and gate epilogue,
  * fp32: out = (scan(u, softplus(dt_r W_dt^T + b_dt), -exp(A_log), B, C) +
  * D u) * SiLU(z), with [dt_r|B|C] = d_xdbl rows of R + 2N values and z read

@@ -86,6 +86,8 @@ _SIGS = {
     "tcl_test_gemm_split": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp]),
     "tcl_test_gemm_bf16": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
+    "tcl_test_xproj_conv_f32": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _vp, _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                  _vp, _vp, _vp]),
 }
@@ -472,6 +474,23 @@ def conv_silu_f32(offs, x, w, b, E, out, ldx=None, stream=None):
                                        x.shape[1] if ldx is None else ldx, w.data_ptr(), b.data_ptr(),
                                        out.data_ptr(), _stream(stream)))
     return out
+
+
+def xproj_conv_f32(offs, x, w, b, W, rows, E, ldx=None, stream=None):
+    """The fused conv + SiLU + x_proj kernel (tcl_test_xproj_conv_f32):
+    returns (u [rows, E], xdbl [rows, N]); rows past offs[B] are NaN."""
+    import torch
+    B = offs.numel() - 1
+    N = W.shape[0]
+    u = torch.full((rows, E), float("nan"), dtype=torch.float32, device=x.device)
+    xdbl = torch.full((rows, N), float("nan"), dtype=torch.float32, device=x.device)
+    wsplit = torch.empty(3 * N * E, dtype=torch.int16, device=x.device)
+    tpos = torch.empty(rows, dtype=torch.uint8, device=x.device)
+    check(lib().tcl_test_xproj_conv_f32(B, rows, E, N, offs.data_ptr(), x.data_ptr(),
+                                        x.shape[1] if ldx is None else ldx, w.data_ptr(), b.data_ptr(),
+                                        W.data_ptr(), wsplit.data_ptr(), tpos.data_ptr(), u.data_ptr(),
+                                        xdbl.data_ptr(), _stream(stream)))
+    return u, xdbl
 
 
 def scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, out, ldz=None, stream=None, chunks=0):

@@ -122,6 +122,7 @@ ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L) {
   const size_t act = c.dtype == TCL_BF16 ? 2 : 4;  // bytes per stored activation
   size_t o = 0;
   p.offs = o; o = align256(o + (size_t)(B + 1) * 4);
+  p.tpos = o; o = align256(o + (size_t)rows);
   p.H = o; o = align256(o + (size_t)rows * c.d_model * 4);
   p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * act);
   p.u = o; o = align256(o + (size_t)rows * c.d_inner * act);
@@ -167,7 +168,8 @@ tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string&
 }
 
 tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, int l, int B, int L,
-                             const int* offs, float* H, float* xz, float* u, float* xdbl, hipStream_t s) {
+                             const int* offs, const uint8_t* tpos, float* H, float* xz, float* u, float* xdbl,
+                             hipStream_t s) {
   const tcl_config& c = m->cfg;
   const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
   const int Mmax = B * L;
@@ -177,12 +179,19 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
   gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
   TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), model_gemm(m, gi, W.W_in_s, d, kRowNorm, s));
-  TCL_LAUNCH(T, (tag + "conv_silu").c_str(),
-             launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w, W.conv_b, u, s));
   GemmArgs gx;
   gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
   gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-  TCL_LAUNCH(T, (tag + "gemm_x_proj").c_str(), model_gemm(m, gx, W.W_x_s, E, 0, s));
+  ConvIn cv;
+  cv.x = xz; cv.ldx = 2 * E; cv.w = W.conv_w; cv.b = W.conv_b; cv.tpos = tpos; cv.u = u;
+  if (m->split && W.W_x_s && gemm_split_conv_supports(gx, cv, c.d_conv)) {
+    // the conv + SiLU computed in front of x_proj, u stored on the way
+    TCL_LAUNCH(T, (tag + "gemm_x_proj_conv").c_str(), launch_gemm_split_conv(gx, cv, W.W_x_s, E, s));
+  } else {
+    TCL_LAUNCH(T, (tag + "conv_silu").c_str(),
+               launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w, W.conv_b, u, s));
+    TCL_LAUNCH(T, (tag + "gemm_x_proj").c_str(), model_gemm(m, gx, W.W_x_s, E, 0, s));
+  }
   if (chunks > 0)
     TCL_LAUNCH(T, (tag + "scan_chunked").c_str(),
                launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E, 2 * E, W.W_dt, W.b_dt,
@@ -210,6 +219,8 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
   Timing& T = m->timing;
 
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  uint8_t* tpos = reinterpret_cast<uint8_t*>(ws + p.tpos);
+  if (c.dtype == TCL_F32 && m->split) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
   // features whose row length is not a multiple of 4 are first copied into
   // rows padded with zeros (the input Linear reads 16-byte vectors)
   const float* feats = d_feats;
@@ -234,7 +245,7 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       if (st != TCL_OK) return st;
     }
     for (int l = 0; l < c.n_layers; ++l) {
-      tcl_status st = enqueue_block_f32(m, T, "", l, B, L, offs, H, xz, u, xdbl, s);
+      tcl_status st = enqueue_block_f32(m, T, "", l, B, L, offs, m->split ? tpos : nullptr, H, xz, u, xdbl, s);
       if (st != TCL_OK) return st;
     }
   } else {
@@ -801,6 +812,28 @@ TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const
   if (!d_offs || !d_x || !d_w || !d_b || !d_u) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
   TCL_HIP(launch_conv_silu<float>(B, E, K, d_offs, d_x, ldx, d_w, d_b, d_u,
                                   static_cast<hipStream_t>(stream)));
+  return TCL_OK;
+}
+
+TCL_API tcl_status tcl_test_xproj_conv_f32(int32_t B, int32_t rows, int32_t E, int32_t N,
+                                           const int32_t* d_offs, const float* d_x, int32_t ldx,
+                                           const float* d_w, const float* d_b, const float* d_W,
+                                           uint16_t* d_Wsplit, uint8_t* d_tpos, float* d_u,
+                                           float* d_xdbl, void* stream) {
+  if (B <= 0 || rows <= 0 || E <= 0 || N <= 0 || ldx < E) return fail(TCL_ERR_INVALID_ARG, "bad sizes");
+  if (!d_offs || !d_x || !d_w || !d_b || !d_W || !d_Wsplit || !d_tpos || !d_u || !d_xdbl)
+    return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  GemmArgs g;
+  g.A = d_u; g.lda = E; g.W = d_W; g.ldw = E; g.C = d_xdbl; g.ldc = N;
+  g.Mdev = d_offs + B; g.Mmax = rows; g.N = N; g.K = E;
+  ConvIn cv;
+  cv.x = d_x; cv.ldx = ldx; cv.w = d_w; cv.b = d_b; cv.tpos = d_tpos; cv.u = d_u;
+  if (!gemm_split_conv_supports(g, cv, 4))
+    return fail(TCL_ERR_UNSUPPORTED, "shape or alignment not supported by the fused conv + x_proj kernel");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  TCL_HIP(launch_split_weights(d_W, N, E, E, d_Wsplit, s));
+  TCL_HIP(launch_token_pos(d_offs, B, d_tpos, s));
+  TCL_HIP(launch_gemm_split_conv(g, cv, d_Wsplit, E, s));
   return TCL_OK;
 }
 

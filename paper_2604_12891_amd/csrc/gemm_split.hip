@@ -49,6 +49,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWaves = 4;
 constexpr uint32_t kBufferFlags = 0x00020000;  // 32-bit data format, raw (stride 0)
@@ -711,6 +712,198 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
   }
 }
 
+// ---------------------------------------------------------------- x_proj with the conv in front
+// The 32-row, all-N-in-registers panel of x_proj, walking K in chunks of 64
+// channels whose A chunk is made in the kernel: each wavefront computes the
+// causal conv + SiLU of its 32 rows (lane = channel; the 35 input rows, 3 of
+// them before the wavefront's first row, are loaded one chunk ahead into
+// registers), stores u, parks the chunk in LDS and reads its MFMA fragments
+// from there. Two workgroups fit a CU. Taps that reach before a program's
+// first token read zero, as in the stand-alone conv kernel, and the taps are
+// summed in the same order, so u is the same bits either way.
+// Copies the compiler cannot see through: values derived from them per
+// chunk (lane masks, per-row offsets) are then built where they are used
+// instead of being kept live across all chunks.
+__device__ __forceinline__ uint32_t opaque_s(uint32_t v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+__device__ __forceinline__ uint32_t opaque_v(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+template <int KCH, int NB>
+__global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmArgs p, ConvIn cv, const uint16_t* Ws,
+                                                                          int ldws) {
+  constexpr int NS = 4;               // 16-k MFMA steps per chunk
+  constexpr int CW = 64;              // channels per chunk
+  constexpr int PA = CW + 4;          // fp32 pitch of a parked row (conflict-free 16-byte reads)
+  constexpr int XR = 32 + 3;          // conv input rows per wavefront
+  constexpr int BM = kWaves * 32;
+  using Stage = WStage<32, 1>;
+  constexpr int WP = Stage::WP;
+  constexpr int PART = 32 * WP;
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
+  __shared__ __attribute__((aligned(16))) float sA[BM * PA];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 31, lg = lane >> 5;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * BM;
+  if (row0 >= M) return;
+  const int E = p.K;
+
+  const int Kw = (p.K + 7) & ~7;
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  Stage st;
+  st.load(wres, tid, 0, p.N, ldws, Kw, 0);
+
+  // rows of this wavefront: wb .. wb + 31. p0 = position of row wb in its
+  // program (clamped to 3); bit r of `starts` (r >= 1): row wb + r is a
+  // program's first row
+  const int wb = row0 + wave * 32;
+  int tp = 3;
+  if (lane < 32 && wb + lane < M) tp = min((int)cv.tpos[wb + lane], 3);
+  const uint32_t p0 = (uint32_t)__builtin_amdgcn_readfirstlane(tp);
+  const uint32_t starts = (uint32_t)__builtin_amdgcn_ballot_w64(lane >= 1 && lane < 32 && tp == 0);
+  // conv input rows max(row0 - 3, 0) .. min(M, row0 + BM) - 1: a row before
+  // the first or past the last reads zero through the resource
+  const int xr0 = max(row0 - 3, 0);
+  const int xrows = min(M, row0 + BM) - xr0;
+  const __amdgpu_buffer_rsrc_t xres = make_rsrc(cv.x + (int64_t)xr0 * cv.ldx, (uint32_t)(xrows * cv.ldx * 4));
+  const __amdgpu_buffer_rsrc_t ures = make_rsrc(cv.u + (int64_t)row0 * E, (uint32_t)(min(BM, M - row0) * E * 4));
+  const __amdgpu_buffer_rsrc_t cwres = make_rsrc(cv.w, (uint32_t)(E * 4 * 4));
+  const __amdgpu_buffer_rsrc_t cbres = make_rsrc(cv.b, (uint32_t)(E * 4));
+
+  const uint32_t ldx4 = (uint32_t)(cv.ldx * 4);
+  uint32_t xw[XR];
+  u32x4 cw;
+  uint32_t cb;
+  auto load_chunk = [&](int c) {
+    const uint32_t e = c * CW + lane;
+    const uint32_t ve = opaque_v(e * 4), ld = opaque_s(ldx4);
+#pragma unroll
+    for (int i = 0; i < XR; ++i) {
+      const int row = wb - 3 + i;
+      const uint32_t off = row >= 0 ? (uint32_t)(row - xr0) * ld + ve : kOutOfRange;
+      xw[i] = __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0);
+    }
+    cw = __builtin_amdgcn_raw_buffer_load_b128(cwres, ve * 4, 0, 0);
+    cb = __builtin_amdgcn_raw_buffer_load_b32(cbres, ve, 0, 0);
+  };
+  load_chunk(0);
+
+  floatx16 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+  st.stage(&sW[0], tid);
+
+  float* myA = &sA[wave * 32 * PA];
+#pragma unroll
+  for (int c = 0; c < KCH; ++c) {
+    __builtin_amdgcn_sched_barrier(0);
+    // conv + SiLU of rows wb .. wb + 31 at channel c CW + lane
+    {
+      const float w0 = __uint_as_float(cw.x), w1 = __uint_as_float(cw.y), w2 = __uint_as_float(cw.z),
+                  w3 = __uint_as_float(cw.w), bias = __uint_as_float(cb);
+      const uint32_t pc = opaque_s(p0), sc = opaque_s(starts);
+      // the rows before the wavefront's first row that lie in an earlier program
+      if (pc < 3) xw[0] = 0u;
+      if (pc < 2) xw[1] = 0u;
+      if (pc < 1) xw[2] = 0u;
+      const uint32_t ue = opaque_v((uint32_t)(wave * 32 * E + c * CW + lane) * 4), ur = opaque_s((uint32_t)E * 4);
+#pragma unroll
+      for (int r = 0; r < 32; ++r) {
+        // row wb + r starts a program: the three rows before it are no
+        // longer anyone's taps
+        if (r > 0 && ((sc >> r) & 1u)) xw[r] = xw[r + 1] = xw[r + 2] = 0u;
+        float a = bias;
+        a = fmaf(w0, __uint_as_float(xw[r]), a);
+        a = fmaf(w1, __uint_as_float(xw[r + 1]), a);
+        a = fmaf(w2, __uint_as_float(xw[r + 2]), a);
+        a = fmaf(w3, __uint_as_float(xw[r + 3]), a);
+        const float o = silu(a);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), ures, ue + r * ur, 0, 0);
+        myA[r * PA + lane] = o;
+      }
+    }
+    // the next chunk's conv inputs load while this chunk's MFMAs run
+    if (c + 1 < KCH) load_chunk(c + 1);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    bf16x8 a1[NS], a2[NS], a3[NS];
+#pragma unroll
+    for (int s2 = 0; s2 < NS; ++s2) {
+      const float* ap = &myA[li * PA + 16 * s2 + 8 * lg];
+      split8(*reinterpret_cast<const floatx4*>(ap), *reinterpret_cast<const floatx4*>(ap + 4), a1[s2], a2[s2],
+             a3[s2]);
+    }
+    // every lane's fragment reads are done before the next chunk's rows are parked
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int buf = (c * NB + nb) & 1;
+      __syncthreads();  // this block visible; the other buffer is free for the next
+      const bool more = nb + 1 < NB || c + 1 < KCH;
+      if (nb + 1 < NB) st.load(wres, tid, (nb + 1) * 32, p.N, ldws, Kw, c * CW);
+      else if (c + 1 < KCH) st.load(wres, tid, 0, p.N, ldws, Kw, (c + 1) * CW);
+
+      const uint16_t* wbp = &sW[buf * 3 * PART + li * WP + 8 * lg];
+      auto wfrag = [&](int part, int ks) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wbp + part * PART + 16 * ks));
+      };
+      bf16x8 q[2][3];
+#pragma unroll
+      for (int j = 0; j < 3; ++j) q[0][j] = wfrag(j, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks) {
+        if (ks + 1 < NS) {
+#pragma unroll
+          for (int j = 0; j < 3; ++j) q[(ks + 1) & 1][j] = wfrag(j, ks + 1);
+        }
+        const bf16x8* w = q[ks & 1];
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], acc[nb], 0, 0, 0);
+        if (ks + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+        if (ks == NS / 2 && more) {
+          st.stage(&sW[(buf ^ 1) * 3 * PART], tid);
+          __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
+        }
+      }
+    }
+  }
+
+  // epilogue: lane l holds column nb*32 + l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
+  const __amdgpu_buffer_rsrc_t cres =
+      make_rsrc(p.C + (int64_t)row0 * p.ldc, (uint32_t)(min(BM, M - row0) * p.ldc * 4));
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = nb * 32 + li;
+    const bool cok = col < p.N;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      // (a bit cast straight from the vector element would read element 0)
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[nb][r]), cres, off, 0, 0);
+    }
+  }
+}
+
 template <int FL>
 hipError_t launch32(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
   const int grid = (a.Mmax + kWaves * 32 - 1) / (kWaves * 32);
@@ -876,6 +1069,36 @@ hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, in
     }
   }
   return hipErrorInvalidValue;
+}
+
+bool gemm_split_conv_supports(const GemmArgs& a, const ConvIn& cv, int d_conv) {
+  const auto a16 = [](const void* q) { return reinterpret_cast<uintptr_t>(q) % 16 == 0; };
+  return d_conv == 4 && !a.relu && a.K % 64 == 0 && a.K >= 64 && a.K <= 512 && a.N >= 1 && a.N <= 64 && cv.x && cv.w &&
+         cv.b && cv.tpos && cv.u && a16(cv.x) && a16(cv.w) && a16(cv.u) && cv.ldx % 4 == 0 && cv.ldx >= a.K &&
+         // byte offsets of the buffer resources stay below 2^31
+         (int64_t)(kWaves * 32 + 3) * cv.ldx * 4 < (1ll << 31) && (int64_t)kWaves * 32 * a.K * 4 < (1ll << 31) && (int64_t)kWaves * 32 * a.ldc * 4 < (1ll << 31) &&
+         (int64_t)3 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31);
+}
+
+hipError_t launch_gemm_split_conv(const GemmArgs& a, const ConvIn& cv, const uint16_t* Ws, int ldws, hipStream_t s) {
+  if (!gemm_split_conv_supports(a, cv, 4)) return hipErrorInvalidValue;
+  const int grid = (a.Mmax + kWaves * 32 - 1) / (kWaves * 32);
+  if (grid <= 0) return hipSuccess;
+#define TCL_SPLITCONV(KCH) \
+  hipLaunchKernelGGL((gemm_split32conv_kernel<KCH, 2>), dim3(grid), dim3(kWaves * 64), 0, s, a, cv, Ws, ldws)
+  switch (a.K / 64) {
+    case 1: TCL_SPLITCONV(1); break;
+    case 2: TCL_SPLITCONV(2); break;
+    case 3: TCL_SPLITCONV(3); break;
+    case 4: TCL_SPLITCONV(4); break;
+    case 5: TCL_SPLITCONV(5); break;
+    case 6: TCL_SPLITCONV(6); break;
+    case 7: TCL_SPLITCONV(7); break;
+    case 8: TCL_SPLITCONV(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_SPLITCONV
+  return hipGetLastError();
 }
 
 hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s) {

@@ -81,6 +81,24 @@ hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, in
                              hipStream_t s);
 hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s);
 
+// x_proj with the causal depthwise conv + SiLU in front (split path, 32-row
+// blocks, all N in registers): u = SiLU(b + sum_k w[e,k] x[t-3+k, e]) within
+// each program is computed per 128-channel chunk, stored to u [rows, K] and
+// contracted with W (Ws as above) into C = u W^T. GemmArgs.A is not read;
+// a.K = d_inner. tpos[r] is the position of packed row r in its program
+// (clamped to 255). Kernel size 4, K a multiple of 64 and <= 512, N <= 64.
+struct ConvIn {
+  const float* x = nullptr;   // conv input [rows, ldx] (the x half of in_proj's output)
+  int64_t ldx = 0;
+  const float* w = nullptr;   // [K, 4]
+  const float* b = nullptr;   // [K]
+  const uint8_t* tpos = nullptr;
+  float* u = nullptr;         // [rows, K]
+};
+bool gemm_split_conv_supports(const GemmArgs& a, const ConvIn& cv, int d_conv);
+hipError_t launch_gemm_split_conv(const GemmArgs& a, const ConvIn& cv, const uint16_t* Ws, int ldws,
+                                  hipStream_t s);
+
 // bf16 GEMM: C = A W^T with A fp32 (converted while staged) or bf16, W bf16
 // ([N, ldw] row-major, zero-padded in K to a multiple of 8, ldw % 8 == 0),
 // C fp32 or bf16, fp32 accumulation. kRowNorm also scales A by gain[k]
@@ -160,6 +178,9 @@ hipError_t launch_gemm_tn(const GemmTNArgs& a, TNKind kind, int splits, hipStrea
 // offs[b] = sum of valid lengths before b; offs[B] = total packed rows.
 // Lengths outside [1, L] count as 0 tokens.
 hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream_t s);
+// tpos[r] = position of packed row r in its program, clamped to 255 (rows
+// past offs[B] are not written).
+hipError_t launch_token_pos(const int* offs, int B, uint8_t* tpos, hipStream_t s);
 
 // Activations are stored as fp32 (T = float) or bf16 (T = uint16_t); the
 // arithmetic is fp32 either way.

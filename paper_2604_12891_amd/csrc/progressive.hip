@@ -69,7 +69,7 @@ bool same_architecture(const tcl_config& x, const tcl_config& y) {
 }
 
 struct ProgPlan {
-  size_t offs, feats, Hkb, Hac, xz, u, xdbl, T, ekb[2], eac[2], Pkb, Pac, rkb[2], rac[2], scr, total;
+  size_t offs, tpos, feats, Hkb, Hac, xz, u, xdbl, T, ekb[2], eac[2], Pkb, Pac, rkb[2], rac[2], scr, total;
 };
 
 ProgPlan prog_plan(const tcl_config& c, int a, int64_t B, int64_t L) {
@@ -84,6 +84,7 @@ ProgPlan prog_plan(const tcl_config& c, int a, int64_t B, int64_t L) {
     return at;
   };
   p.offs = take((size_t)(B + 1) * 4);
+  p.tpos = take((size_t)rows);
   p.feats = take(c.F % 4 ? (size_t)rows * ((c.F + 3) & ~3) * 4 : 0);
   p.Hkb = take((size_t)rows * c.d_model * 4);
   p.Hac = take((size_t)rows * c.d_model * 4);
@@ -324,6 +325,9 @@ tcl_status run_progressive(tcl_lateral* lt, int B, int L, const float* d_feats, 
   const int n_enc = bl.n_enc, d = c.d_model, h = c.head_hidden, h2 = c.dec_hidden2;
 
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  uint8_t* tpos = reinterpret_cast<uint8_t*>(ws + p.tpos);
+  const bool fuse = kb->split && ac->split;
+  if (fuse) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
   const float* feats = d_feats;
   const int ldf = (c.F + 3) & ~3;
   if (ldf != c.F) {
@@ -357,9 +361,9 @@ tcl_status run_progressive(tcl_lateral* lt, int B, int L, const float* d_feats, 
   float* u = F32(p.u);
   float* xdbl = F32(p.xdbl);
   for (int l = 0; l < c.n_layers; ++l) {
-    TCL_TRY(enqueue_block_f32(ac, T, "ac:", l, B, L, offs, Hac, xz, u, xdbl, s));
+    TCL_TRY(enqueue_block_f32(ac, T, "ac:", l, B, L, offs, fuse ? tpos : nullptr, Hac, xz, u, xdbl, s));
     TCL_TRY(lateral(lt, T, j++, Hkb, Tb, Hac, d, Mdev, Mmax, false, s));
-    TCL_TRY(enqueue_block_f32(kb, T, "kb:", l, B, L, offs, Hkb, xz, u, xdbl, s));
+    TCL_TRY(enqueue_block_f32(kb, T, "kb:", l, B, L, offs, fuse ? tpos : nullptr, Hkb, xz, u, xdbl, s));
   }
   // final norm and pool of both columns (the tail's own head output is not used)
   float* Pkb = F32(p.Pkb);

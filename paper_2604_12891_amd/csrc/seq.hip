@@ -578,6 +578,23 @@ hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream
   return hipGetLastError();
 }
 
+namespace {
+// One thread per program writes the positions of its tokens.
+__global__ __launch_bounds__(256) void token_pos_kernel(const int* __restrict__ offs, int B,
+                                                        uint8_t* __restrict__ tpos) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  const int base = offs[b], len = offs[b + 1] - base;
+  for (int t = 0; t < len; ++t) tpos[base + t] = (uint8_t)min(t, 255);
+}
+}  // namespace
+
+hipError_t launch_token_pos(const int* offs, int B, uint8_t* tpos, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(token_pos_kernel, dim3((B + 255) / 256), dim3(256), 0, s, offs, B, tpos);
+  return hipGetLastError();
+}
+
 template <typename T>
 hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, int ldx,
                             const float* w, const float* b, T* u, hipStream_t s) {

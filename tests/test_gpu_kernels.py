@@ -297,6 +297,54 @@ def test_conv_silu_f32(K):
     np.testing.assert_array_less(np.abs(out.cpu().numpy() - expect), 1e-5 * scale + 1e-7)
 
 
+@pytest.mark.parametrize("E,N", [(512, 48), (128, 20), (64, 64), (320, 33)])
+def test_xproj_conv_f32(E, N):
+    """The fused conv + SiLU + x_proj kernel: u is the same bits as the
+    stand-alone conv kernel's, both within the conv bound of the oracle's
+    conv, and xdbl = u W^T within the split GEMM's fp32 bound. Programs of
+    length 1..4 around wavefront and panel edges, an empty program, a
+    ragged last panel, and a row count bound above the packed rows."""
+    rng = np.random.default_rng(E + N)
+    L = 40
+    lengths = np.concatenate([[1, 2, 3, 4, 0, 40, 31, 33, 1, 1, 1, 29, 3], rng.integers(1, L + 1, 60)])
+    lengths = lengths.astype(np.int32)
+    B = len(lengths)
+    M = int(lengths.sum())
+    rows = M + 77
+    ldx = 2 * E
+    print(f"xproj_conv E={E} N={N} B={B} M={M}", flush=True)
+    x = rng.standard_normal((B, L, E))
+    w = rng.uniform(-0.5, 0.5, (E, 4)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, E).astype(np.float32)
+    W = (rng.uniform(-1, 1, (N, E)) / np.sqrt(E)).astype(np.float32)
+    xp = rng.standard_normal((rows, ldx)).astype(np.float32)  # rows past M and the z half: noise
+    xp[:M, :E] = _pack(x, lengths)
+    offs = _dev(_offs(lengths), torch.int32)
+    u, xdbl = tb.xproj_conv_f32(offs, _dev(xp), _dev(w), _dev(b), _dev(W), rows, E, ldx=ldx)
+    ref_u = torch.full((M, E), float("nan"), device="cuda")
+    tb.conv_silu_f32(offs, _dev(xp), _dev(w), _dev(b), E, ref_u, ldx=ldx)
+    torch.cuda.synchronize()
+    u, xdbl, ref_u = u.cpu().numpy(), xdbl.cpu().numpy(), ref_u.cpu().numpy()
+    assert np.all(np.isnan(u[M:])) and np.all(np.isnan(xdbl[M:]))
+    np.testing.assert_array_equal(u[:M].view(np.uint32), ref_u.view(np.uint32))
+    xr = _unpack(xp[:M, :E].astype(np.float64), lengths, L)
+    wf, bf = w.astype(np.float64), b.astype(np.float64)
+    expect = _pack(om.silu(om.causal_conv1d(xr, wf, bf)), lengths)
+    scale = np.abs(bf) + _pack(om.causal_conv1d(np.abs(xr), np.abs(wf), 0 * bf), lengths)
+    np.testing.assert_array_less(np.abs(u[:M] - expect), 1e-5 * scale + 1e-7)
+    ref, bound = _split_ref(u[:M], W, "plain")
+    err = np.abs(xdbl[:M] - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+def test_xproj_conv_rejects_unsupported():
+    offs = _dev(_offs(np.array([3, 2], np.int32)), torch.int32)
+    for E, N in [(96, 48), (576, 48), (128, 65)]:
+        with pytest.raises(tb.TclError):
+            tb.xproj_conv_f32(offs, torch.zeros(5, 2 * E, device="cuda"), torch.zeros(E, 4, device="cuda"),
+                              torch.zeros(E, device="cuda"), torch.zeros(N, E, device="cuda"), 5, E)
+
+
 @pytest.mark.parametrize("R", [4, 16])
 @pytest.mark.parametrize("L", [1, 25, 70, 256])
 @pytest.mark.parametrize("chunks", [0, 1, 3, 8])
