@@ -108,7 +108,11 @@ struct WStage {
       const int u = tid + i * NT;
       const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = k0 + 8 * (u % WU);
       const bool ok = (NWU % NT == 0 || u < NWU) && n < N && k < Kw;
-      const uint32_t off = ok ? (uint32_t)((((int64_t)part * N + n) * ldw + k) * 2) : kOutOfRange;
+      // 32-bit offsets (the resource is below 2^31 bytes), moved out of range
+      // by setting bit 31: arithmetic, not a branch around the load (which
+      // makes the compiler wait for every outstanding memory operation
+      // before the other side reuses the registers)
+      const uint32_t off = (uint32_t)(((part * N + n) * ldw + k) * 2) | ((uint32_t)!ok << 31);
       r[i] = __builtin_amdgcn_raw_buffer_load_b128(res, off, 0, 0);
     }
   }
@@ -136,7 +140,7 @@ struct WStageHalves {
       const int u = tid + i * NT;
       const int part = u / (NR * WU), n = n0 + (u / WU) % NR, k = 8 * (u % WU);
       const bool ok = (NWU % NT == 0 || u < NWU) && n < N && k < Kw;
-      const uint32_t off = ok ? (uint32_t)((((int64_t)part * N + n) * ldw + k) * 2) : kOutOfRange;
+      const uint32_t off = (uint32_t)(((part * N + n) * ldw + k) * 2) | ((uint32_t)!ok << 31);
       r[i - I0] = __builtin_amdgcn_raw_buffer_load_b128(res, off, 0, 0);
     }
   }
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p
   }
 
   const int Kw = (p.K + 7) & ~7;
-  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
   const int nsteps = (p.N + 31) / 32;
   Stage st;
   st.load(wres, tid, 0, p.N, ldws, Kw);  // in flight during the prologue
@@ -345,7 +349,7 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
   }
 
   const int Kw = (p.K + 7) & ~7;
-  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
   const int nsteps = (p.N + 31) / 32;
   Stage st;
   __syncthreads();  // sSrc
@@ -505,7 +509,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split16_kernel(GemmArgs p
   if (row0 >= M) return;
 
   const int Kw = (p.K + 7) & ~7;
-  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
   const int nsteps = (p.N + 15) / 16;
   Stage st;
   st.load(wres, tid, 0, p.N, ldws, Kw);
@@ -614,7 +618,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
   if (row0 >= M) return;
 
   const int Kw = (p.K + 7) & ~7;
-  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
   Stage st;
   st.load(wres, tid, 0, p.N, ldws, Kw, 0);
 
@@ -733,7 +737,7 @@ __device__ __forceinline__ uint32_t opaque_v(uint32_t v) {
   return v;
 }
 
-template <int KCH, int NB>
+template <int KCH>
 __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmArgs p, ConvIn cv, const uint16_t* Ws,
                                                                           int ldws) {
   constexpr int NS = 4;               // 16-k MFMA steps per chunk
@@ -756,10 +760,13 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
   if (row0 >= M) return;
   const int E = p.K;
 
+  // W goes through LDS in two 32-column blocks per chunk; a block's loads
+  // are issued a block or more ahead (before the conv inputs of the next
+  // chunk, so that waiting for them never waits for those)
   const int Kw = (p.K + 7) & ~7;
-  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)(3 * p.N * ldws * 2));
-  Stage st;
-  st.load(wres, tid, 0, p.N, ldws, Kw, 0);
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
+  Stage st0, st1;
+  st0.load(wres, tid, 0, p.N, ldws, Kw, 0);
 
   // rows of this wavefront: wb .. wb + 31. p0 = position of row wb in its
   // program (clamped to 3); bit r of `starts` (r >= 1): row wb + r is a
@@ -796,18 +803,21 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
   };
   load_chunk(0);
 
-  floatx16 acc[NB];
+  floatx16 acc[2];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
+  for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
-  st.stage(&sW[0], tid);
+  st0.stage(&sW[0], tid);
 
   float* myA = &sA[wave * 32 * PA];
 #pragma unroll
   for (int c = 0; c < KCH; ++c) {
     __builtin_amdgcn_sched_barrier(0);
-    // conv + SiLU of rows wb .. wb + 31 at channel c CW + lane
+    // W of this chunk's second block and of the next chunk's first
+    st1.load(wres, tid, 32, p.N, ldws, Kw, c * CW);
+    if (c + 1 < KCH) st0.load(wres, tid, 0, p.N, ldws, Kw, (c + 1) * CW);
+    // conv + SiLU of rows wb .. wb + 31 at channel c CW + lane, parked in LDS
     {
       const float w0 = __uint_as_float(cw.x), w1 = __uint_as_float(cw.y), w2 = __uint_as_float(cw.z),
                   w3 = __uint_as_float(cw.w), bias = __uint_as_float(cb);
@@ -816,7 +826,6 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
       if (pc < 3) xw[0] = 0u;
       if (pc < 2) xw[1] = 0u;
       if (pc < 1) xw[2] = 0u;
-      const uint32_t ue = opaque_v((uint32_t)(wave * 32 * E + c * CW + lane) * 4), ur = opaque_s((uint32_t)E * 4);
 #pragma unroll
       for (int r = 0; r < 32; ++r) {
         // row wb + r starts a program: the three rows before it are no
@@ -827,9 +836,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
         a = fmaf(w1, __uint_as_float(xw[r + 1]), a);
         a = fmaf(w2, __uint_as_float(xw[r + 2]), a);
         a = fmaf(w3, __uint_as_float(xw[r + 3]), a);
-        const float o = silu(a);
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), ures, ue + r * ur, 0, 0);
-        myA[r * PA + lane] = o;
+        myA[r * PA + lane] = silu(a);
       }
     }
     // the next chunk's conv inputs load while this chunk's MFMAs run
@@ -837,6 +844,16 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // u: the parked rows stored 16 bytes per lane (four rows per instruction)
+    {
+      const uint32_t uo = opaque_v((uint32_t)((wave * 32 + (lane >> 4)) * E + c * CW + 4 * (lane & 15)) * 4);
+      const uint32_t ur = opaque_s((uint32_t)E * 16);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(&myA[(4 * i + (lane >> 4)) * PA + 4 * (lane & 15)]);
+        __builtin_amdgcn_raw_buffer_store_b128(v, ures, uo + i * ur, 0, 0);
+      }
+    }
     bf16x8 a1[NS], a2[NS], a3[NS];
 #pragma unroll
     for (int s2 = 0; s2 < NS; ++s2) {
@@ -844,18 +861,15 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
       split8(*reinterpret_cast<const floatx4*>(ap), *reinterpret_cast<const floatx4*>(ap + 4), a1[s2], a2[s2],
              a3[s2]);
     }
-    // every lane's fragment reads are done before the next chunk's rows are parked
+    // every lane's reads of the parked rows are done before the next chunk's rows are parked
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int buf = (c * NB + nb) & 1;
+    for (int nb = 0; nb < 2; ++nb) {
+      const int buf = (c * 2 + nb) & 1;
       __syncthreads();  // this block visible; the other buffer is free for the next
-      const bool more = nb + 1 < NB || c + 1 < KCH;
-      if (nb + 1 < NB) st.load(wres, tid, (nb + 1) * 32, p.N, ldws, Kw, c * CW);
-      else if (c + 1 < KCH) st.load(wres, tid, 0, p.N, ldws, Kw, (c + 1) * CW);
-
+      const bool more = nb == 0 || c + 1 < KCH;
       const uint16_t* wbp = &sW[buf * 3 * PART + li * WP + 8 * lg];
       auto wfrag = [&](int part, int ks) {
         return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wbp + part * PART + 16 * ks));
@@ -880,7 +894,8 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
         if (ks + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 3, 0);
         __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
         if (ks == NS / 2 && more) {
-          st.stage(&sW[(buf ^ 1) * 3 * PART], tid);
+          if (nb == 0) st1.stage(&sW[(buf ^ 1) * 3 * PART], tid);
+          else st0.stage(&sW[(buf ^ 1) * 3 * PART], tid);
           __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
         }
       }
@@ -891,7 +906,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
   const __amdgpu_buffer_rsrc_t cres =
       make_rsrc(p.C + (int64_t)row0 * p.ldc, (uint32_t)(min(BM, M - row0) * p.ldc * 4));
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
+  for (int nb = 0; nb < 2; ++nb) {
     const int col = nb * 32 + li;
     const bool cok = col < p.N;
 #pragma unroll
@@ -1085,7 +1100,7 @@ hipError_t launch_gemm_split_conv(const GemmArgs& a, const ConvIn& cv, const uin
   const int grid = (a.Mmax + kWaves * 32 - 1) / (kWaves * 32);
   if (grid <= 0) return hipSuccess;
 #define TCL_SPLITCONV(KCH) \
-  hipLaunchKernelGGL((gemm_split32conv_kernel<KCH, 2>), dim3(grid), dim3(kWaves * 64), 0, s, a, cv, Ws, ldws)
+  hipLaunchKernelGGL((gemm_split32conv_kernel<KCH>), dim3(grid), dim3(kWaves * 64), 0, s, a, cv, Ws, ldws)
   switch (a.K / 64) {
     case 1: TCL_SPLITCONV(1); break;
     case 2: TCL_SPLITCONV(2); break;

@@ -194,11 +194,16 @@ hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, in
 // Selective scan with dt_proj+softplus prologue, D skip and SiLU(z) gate.
 // xdbl rows ([dt_r | B | C], R + 2N values) are fp32. out may alias u (each
 // element is read then written by the same thread).
-// ysave (optional): the pre-gate output y, for the backward pass.
+// ysave (optional) keeps y before the gate, for the backward pass; ckpt (optional, N = 16, with the
+// padded length L) keeps the state after every kScanCkptTokens-th token of a
+// program but its last chunk, [B][E][ceil(L / kScanCkptTokens)][N], which is
+// where the backward scan restarts its recomputation.
+constexpr int kScanCkptTokens = 4;
 template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
-                       const float* D, T* out, hipStream_t s, T* ysave = nullptr);
+                       const float* D, T* out, hipStream_t s, T* ysave = nullptr, float* ckpt = nullptr,
+                       int L = 0);
 
 // The same scan as a chunked two-level scan: each program's tokens are split
 // into `chunks` (1..8) that are scanned concurrently and stitched through
@@ -314,11 +319,12 @@ hipError_t launch_normf_pool_bwd(int B, int d, const int* offs, const float* H, 
                                  int final_norm, float eps, const float* dpooled, float* dH,
                                  float* dg_part, hipStream_t s);
 size_t scan_bwd_ckpt_floats(int B, int E, int L, int N);
+// ckpt: the forward scan's checkpoints of this layer (launch_scan's ckpt).
 // dA_part: [B][E][N] (already d/dA_log), dD_part: [B][E]
 hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, const uint16_t* u,
                            const float* xdbl, const uint16_t* xz, const uint16_t* ysave,
                            const float* dyg, const float* W_dt, const float* b_dt,
-                           const float* A_log, const float* D, float* ckpt, float* dv, float* du,
+                           const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
                            float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s);
 // part: [B][K+1][E] = dw (K rows) | db
 hipError_t launch_conv_bwd(int B, int E, int K, const int* offs, const uint16_t* x, int ldx,

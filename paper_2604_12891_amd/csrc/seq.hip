@@ -213,7 +213,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
     int B, const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
     const T* __restrict__ z, int ldz, const float* __restrict__ W_dt,
     const float* __restrict__ b_dt, const float* __restrict__ A_log,
-    const float* __restrict__ Dp, T* out, T* __restrict__ ysave) {
+    const float* __restrict__ Dp, T* out, T* __restrict__ ysave, float* __restrict__ ckpt, int nck) {
   constexpr int XW = R + 2 * N;
   __shared__ __attribute__((aligned(16))) float sX[kScanTC * XW];
   // workgroups are handed to the 8 XCDs round-robin: the CG channel groups
@@ -273,6 +273,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
       y = fmaf(Dv, uv, y);
       if (ysave) st1(ysave + row * E + e, y);
       st1(out + row * E + e, y * silu(zv));
+      const int t = t0 + tt;
+      if (ckpt && t % kScanCkptTokens == kScanCkptTokens - 1 && t + 1 < len) {
+        floatx4* dst = reinterpret_cast<floatx4*>(ckpt + (((int64_t)b * E + e) * nck + t / kScanCkptTokens) * N);
+#pragma unroll
+        for (int n = 0; n < N; n += 4) dst[n / 4] = floatx4{s[n], s[n + 1], s[n + 2], s[n + 3]};
+      }
     }
   }
 }
@@ -657,14 +663,16 @@ int scan_chunks_for(int B, int E, int L) {
 template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
-                       const float* D, T* out, hipStream_t s, T* ysave) {
+                       const float* D, T* out, hipStream_t s, T* ysave, float* ckpt, int L) {
   if (B <= 0) return hipSuccess;
   if (N != 16 && N != 8) return hipErrorInvalidValue;
+  if (ckpt && (L <= 0 || reinterpret_cast<uintptr_t>(ckpt) % 16)) return hipErrorInvalidValue;
+  const int nck = (L + kScanCkptTokens - 1) / kScanCkptTokens;
   const int cgroups = (E + kScanThreads - 1) / kScanThreads;
   const int grid = 8 * cgroups * ((B + 7) / 8);
 #define TCL_SCAN(NN, RR)                                                                                \
   hipLaunchKernelGGL((scan_kernel<T, NN, RR>), dim3(grid), dim3(kScanThreads), 0, s, B, offs, E, u, xdbl, \
-                     z, ldz, W_dt, b_dt, A_log, D, out, ysave)
+                     z, ldz, W_dt, b_dt, A_log, D, out, ysave, ckpt, nck)
   switch (N * 100 + R) {
     case 1604: TCL_SCAN(16, 4); break;
     case 1608: TCL_SCAN(16, 8); break;
@@ -697,11 +705,11 @@ template hipError_t launch_scan_chunked<uint16_t>(int, int, int, int, int, const
                                                   const float*, uint16_t*, hipStream_t);
 template hipError_t launch_scan<float>(int, int, int, int, const int*, const float*, const float*,
                                        const float*, int, const float*, const float*, const float*,
-                                       const float*, float*, hipStream_t, float*);
+                                       const float*, float*, hipStream_t, float*, float*, int);
 template hipError_t launch_scan<uint16_t>(int, int, int, int, const int*, const uint16_t*,
                                           const float*, const uint16_t*, int, const float*,
                                           const float*, const float*, const float*, uint16_t*,
-                                          hipStream_t, uint16_t*);
+                                          hipStream_t, uint16_t*, float*, int);
 
 namespace {
 

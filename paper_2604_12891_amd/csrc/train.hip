@@ -235,8 +235,10 @@ __global__ __launch_bounds__(256) void normf_pool_bwd_kernel(const int* __restri
 // Block per program, two lanes per channel e: lane 2e+h owns states
 // n = 8h .. 8h+7 (sums over n are completed with one lane-pair shuffle).
 // Per channel:
-//   forward recompute over the program, storing the state every TC tokens
-//   (checkpoints in a global scratch, one [N] vector per chunk boundary);
+//   the state every TC tokens comes from the forward scan, which stored it
+//   (launch_scan's checkpoints, one [N] vector per chunk boundary; the
+//   recurrence below is the forward kernel's, operation for operation, so
+//   the recomputed states are the same bits);
 //   reverse sweep chunk by chunk: the chunk's states are recomputed into
 //   registers from its checkpoint, then tokens are walked backwards with the
 //   state adjoint g_t = C_t dy_t + a_{t+1} g_{t+1}, a_t = exp(dt_t A).
@@ -245,7 +247,7 @@ __global__ __launch_bounds__(256) void normf_pool_bwd_kernel(const int* __restri
 // over the same-parity lanes of each wavefront, parked in LDS per token and
 // summed across wavefronts once at the end (no barrier inside the sweep).
 // dA_log and dD are accumulated per lane and written as per-program partials.
-constexpr int kTC = 4;
+constexpr int kTC = kScanCkptTokens;
 constexpr int kHalfN = 8;
 
 // Reduce 16 values across the 32 same-parity lanes of a wavefront: lane l
@@ -288,7 +290,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     const float* __restrict__ xdbl, const T* __restrict__ xz, const T* __restrict__ ysave,
     const float* __restrict__ dyg, const float* __restrict__ W_dt,
     const float* __restrict__ b_dt, const float* __restrict__ A_log, const float* __restrict__ Dp,
-    float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
+    const float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
     float* __restrict__ dxz, float* __restrict__ dxdbl, float* __restrict__ dA_part,
     float* __restrict__ dD_part) {
   static_assert(N == 2 * kHalfN, "two lanes per channel, eight states each");
@@ -314,7 +316,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
 #pragma unroll
   for (int r = 0; r < R; ++r) wdt[r] = W_dt[e * R + r];
   const float bdt = b_dt[e], Dv = Dp[e];
-  float* ck = ckpt + ((int64_t)b * E + e) * (int64_t)((L + kTC - 1) / kTC) * N + n0;
+  const float* ck = ckpt + ((int64_t)b * E + e) * (int64_t)((L + kTC - 1) / kTC) * N + n0;
 
   auto dt_of = [&](int t, float& sig) {
     const float* xr = &sX[t * XW];
@@ -324,30 +326,6 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     sig = sigmoid_fast(v);
     return softplus(v);
   };
-
-  // forward recompute, checkpoint the state at the end of every chunk but the last
-  {
-    float s[NH];
-#pragma unroll
-    for (int n = 0; n < NH; ++n) s[n] = 0.f;
-    // u of the next token is loaded (raw) while this token is computed
-    T un = len > 0 ? u[(int64_t)base * E + e] : T(0);  // a program may have no tokens
-    for (int t = 0; t < len; ++t) {
-      float sig;
-      const float dt = dt_of(t, sig);
-      const float uv = to_f32(un);
-      if (t + 1 < len) un = u[(int64_t)(base + t + 1) * E + e];
-      const float dtu = dt * uv;
-      const float* xr = &sX[t * XW] + R + n0;
-#pragma unroll
-      for (int n = 0; n < NH; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[n]);
-      if ((t % kTC) == kTC - 1 && t + 1 < len) {
-        float* dst = ck + (t / kTC) * N;
-#pragma unroll
-        for (int n = 0; n < NH; ++n) dst[n] = s[n];
-      }
-    }
-  }
 
   float g[NH], anext[NH], dA[NH];
 #pragma unroll
@@ -708,7 +686,7 @@ size_t scan_bwd_ckpt_floats(int B, int E, int L, int N) {
 hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, const uint16_t* u,
                            const float* xdbl, const uint16_t* xz, const uint16_t* ysave,
                            const float* dyg, const float* W_dt, const float* b_dt,
-                           const float* A_log, const float* D, float* ckpt, float* dv, float* du,
+                           const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
                            float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s) {
   if (N != 16 || E % 32 || E > 256 || B <= 0) return hipErrorInvalidValue;
   const size_t shm = ((size_t)L * (R + 2 * N) + (size_t)L * 8 * 2 * N) * sizeof(float);

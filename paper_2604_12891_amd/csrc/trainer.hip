@@ -40,13 +40,13 @@ namespace {
 struct TrainPlan {
   size_t teacher_ws = 0, t_scores = 0, s_scores = 0, offs = 0;
   struct Layer {
-    size_t Hin, n, rstd, xz, u, xdbl, y, yg;
+    size_t Hin, n, rstd, xz, u, xdbl, y, yg, ckpt;
     size_t p_Wout, p_Wdt, p_bdt, p_A, p_D, p_Wx, p_conv, p_Win, p_g;
     int s_Wout, s_Wdt, s_Wx, s_Win;
   };
   std::vector<Layer> layers;
   size_t H_last = 0, pooled = 0, a1 = 0;
-  size_t dH = 0, dyg = 0, dxz = 0, du = 0, dv = 0, dxdbl = 0, dN = 0, ckpt = 0, da1 = 0, dpooled = 0;
+  size_t dH = 0, dyg = 0, dxz = 0, du = 0, dv = 0, dxdbl = 0, dN = 0, da1 = 0, dpooled = 0;
   size_t p_lh = 0, p_W1 = 0, p_gf = 0, p_W0 = 0, p_b0 = 0;
   size_t rank_ws = 0, ds = 0, rloss = 0, ewc_part = 0;  // ranking objective (tcl_distill_step_kd)
   int s_W1 = 0, s_W0 = 0, cs = 0, lh_blocks = 0, rn_blocks = 0;
@@ -82,6 +82,7 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
     Ly.xdbl = take(rows * XW * 4);
     Ly.y = take(rows * E * 2);
     Ly.yg = take(rows * E * 2);
+    Ly.ckpt = take(scan_bwd_ckpt_floats(B, E, L, N) * 4);
     Ly.s_Wout = gemm_tn_splits(Mmax, d, E);
     Ly.s_Wdt = gemm_tn_splits(Mmax, E, R);
     Ly.s_Wx = gemm_tn_splits(Mmax, XW, E);
@@ -107,7 +108,6 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
   P.dv = take(rows * E * 4);
   P.dxdbl = take(rows * XW * 4);
   P.dN = take(rows * d * 4);
-  P.ckpt = take(scan_bwd_ckpt_floats(B, E, L, N) * 4);
   P.da1 = take((size_t)B * h * 4);
   P.dpooled = take((size_t)B * d * 4);
   P.p_lh = take((size_t)P.lh_blocks * (2 * h + 4) * 4);
@@ -329,7 +329,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32, -1, s));
     TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, B16(Ly.u), F32(Ly.xdbl),
                                                 B16(Ly.xz) + E, 2 * E, W.W_dt, W.b_dt, W.A_log, W.D,
-                                                B16(Ly.yg), s, B16(Ly.y)));
+                                                B16(Ly.yg), s, B16(Ly.y), F32(Ly.ckpt), L));
     GemmArgsBF16 go;
     go.A = B16(Ly.yg); go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = Hout; go.ldc = d;
     go.R = F32(Ly.Hin); go.Mdev = Mdev; go.Mmax = Mmax; go.N = d; go.K = E;
@@ -378,7 +378,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     }
     TCL_LAUNCH(T, "scan_bwd", launch_scan_bwd(B, E, L, N, R, offs, B16(Ly.u), F32(Ly.xdbl), B16(Ly.xz),
                                               B16(Ly.y), F32(P.dyg), W.W_dt, W.b_dt, W.A_log, W.D,
-                                              F32(P.ckpt), F32(P.dv), F32(P.du), F32(P.dxz),
+                                              F32(Ly.ckpt), F32(P.dv), F32(P.du), F32(P.dxz),
                                               F32(P.dxdbl), F32(Ly.p_A), F32(Ly.p_D), s));
     {  // d dt_r = dv W_dt  -> columns [0, R) of dxdbl
       GemmArgs g;
