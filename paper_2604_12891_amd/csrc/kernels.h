@@ -325,7 +325,10 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
                            const float* xdbl, const uint16_t* xz, const uint16_t* ysave,
                            const float* dyg, const float* W_dt, const float* b_dt,
                            const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
-                           float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s);
+                           float* dxz, float* dxdbl, float* dA_part, float* dD_part, float* dbc_part,
+                           hipStream_t s);
+// dbc_part (scratch for launch_scan_bwd; null: one block per program)
+size_t scan_bwd_part_floats(int B, int L, int N);
 // part: [B][K+1][E] = dw (K rows) | db
 hipError_t launch_conv_bwd(int B, int E, int K, const int* offs, const uint16_t* x, int ldx,
                            const float* w, const float* b, const float* du, float* dx, int lddx,

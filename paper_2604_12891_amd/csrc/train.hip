@@ -292,7 +292,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     const float* __restrict__ b_dt, const float* __restrict__ A_log, const float* __restrict__ Dp,
     const float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
     float* __restrict__ dxz, float* __restrict__ dxdbl, float* __restrict__ dA_part,
-    float* __restrict__ dD_part) {
+    float* __restrict__ dD_part, float* __restrict__ dbc_part, int Mmax) {
   static_assert(N == 2 * kHalfN, "two lanes per channel, eight states each");
   constexpr int XW = R + 2 * N;
   constexpr int NH = kHalfN;
@@ -300,8 +300,8 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
   float* sX = smem;                       // [L][XW] rows of this program
   float* sRed = smem + L * XW;            // [L][8 waves][2N] per-wavefront dB_t | dC_t
   const int b = blockIdx.x;
-  const int tid = threadIdx.x;            // blockDim == 2E
-  const int e = tid >> 1, hf = tid & 1, n0 = hf * NH;
+  const int tid = threadIdx.x;            // blockDim == 2E / gridDim.y: the program's channels in groups
+  const int e = blockIdx.y * (blockDim.x >> 1) + (tid >> 1), hf = tid & 1, n0 = hf * NH;
   const int wave = tid >> 6, lane = tid & 63;
   const int base = offs[b], len = offs[b + 1] - base;
   const int nck = (len + kTC - 1) / kTC;
@@ -438,7 +438,8 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     const int t = i / (2 * N), j = i % (2 * N);
     float acc = 0.f;
     for (int w = 0; w < nw; ++w) acc += sRed[(t * 8 + w) * 2 * N + j];
-    dxdbl[(int64_t)(base + t) * XW + R + j] = acc;
+    if (gridDim.y == 1) dxdbl[(int64_t)(base + t) * XW + R + j] = acc;
+    else dbc_part[((int64_t)blockIdx.y * Mmax + base + t) * 2 * N + j] = acc;
   }
 #pragma unroll
   for (int n = 0; n < NH; ++n)
@@ -683,18 +684,38 @@ size_t scan_bwd_ckpt_floats(int B, int E, int L, int N) {
   return (size_t)B * E * ((L + kTC - 1) / kTC) * N;
 }
 
+namespace {
+// dB_t | dC_t of every token = the two channel groups' partial sums, in that order.
+__global__ __launch_bounds__(256) void sum_dbc_kernel(const int* __restrict__ Mdev, int Mmax, int XW, int R,
+                                                      int N2, const float* __restrict__ part,
+                                                      float* __restrict__ dxdbl) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = i / N2;
+  if (row >= *Mdev) return;
+  dxdbl[row * XW + R + i % N2] = part[i] + part[(int64_t)Mmax * N2 + i];
+}
+}  // namespace
+
+size_t scan_bwd_part_floats(int B, int L, int N) { return (size_t)2 * B * L * 2 * N; }
+
 hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, const uint16_t* u,
                            const float* xdbl, const uint16_t* xz, const uint16_t* ysave,
                            const float* dyg, const float* W_dt, const float* b_dt,
                            const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
-                           float* dxz, float* dxdbl, float* dA_part, float* dD_part, hipStream_t s) {
+                           float* dxz, float* dxdbl, float* dA_part, float* dD_part, float* dbc_part,
+                           hipStream_t s) {
   if (N != 16 || E % 32 || E > 256 || B <= 0) return hipErrorInvalidValue;
   const size_t shm = ((size_t)L * (R + 2 * N) + (size_t)L * 8 * 2 * N) * sizeof(float);
   if (shm > 64 * 1024) return hipErrorInvalidValue;
-#define TCL_SB(RR)                                                                                    \
-  hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B), dim3(2 * E), shm, s, offs, E, L, u,   \
-                     xdbl, xz, ysave, dyg, W_dt, b_dt, A_log, D, ckpt, dv, du, dxz, dxdbl, dA_part, \
-                     dD_part)
+  // the channels of a program in two blocks of E threads where E allows
+  // (three such blocks fit a CU at this kernel's register count, against one
+  // block of 2E threads); their dB/dC partial sums are added afterwards
+  const int groups = (E % 64 == 0 && dbc_part) ? 2 : 1;
+  const int Mmax = B * L;
+#define TCL_SB(RR)                                                                                       \
+  hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B, groups), dim3(2 * E / groups), shm, s, \
+                     offs, E, L, u, xdbl, xz, ysave, dyg, W_dt, b_dt, A_log, D, ckpt, dv, du, dxz, dxdbl,   \
+                     dA_part, dD_part, dbc_part, Mmax)
   switch (R) {
     case 4: TCL_SB(4); break;
     case 8: TCL_SB(8); break;
@@ -702,6 +723,11 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
     default: return hipErrorInvalidValue;
   }
 #undef TCL_SB
+  if (groups == 2) {
+    const int64_t n = (int64_t)Mmax * 2 * N;
+    hipLaunchKernelGGL(sum_dbc_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, offs + B, Mmax,
+                       R + 2 * N, R, 2 * N, dbc_part, dxdbl);
+  }
   return hipGetLastError();
 }
 

@@ -46,7 +46,7 @@ struct TrainPlan {
   };
   std::vector<Layer> layers;
   size_t H_last = 0, pooled = 0, a1 = 0;
-  size_t dH = 0, dyg = 0, dxz = 0, du = 0, dv = 0, dxdbl = 0, dN = 0, da1 = 0, dpooled = 0;
+  size_t dH = 0, dyg = 0, dxz = 0, du = 0, dv = 0, dxdbl = 0, dbc_part = 0, dN = 0, da1 = 0, dpooled = 0;
   size_t p_lh = 0, p_W1 = 0, p_gf = 0, p_W0 = 0, p_b0 = 0;
   size_t rank_ws = 0, ds = 0, rloss = 0, ewc_part = 0;  // ranking objective (tcl_distill_step_kd)
   int s_W1 = 0, s_W0 = 0, cs = 0, lh_blocks = 0, rn_blocks = 0;
@@ -107,6 +107,7 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
   P.du = take(rows * E * 4);
   P.dv = take(rows * E * 4);
   P.dxdbl = take(rows * XW * 4);
+  P.dbc_part = take(scan_bwd_part_floats(B, L, N) * 4);
   P.dN = take(rows * d * 4);
   P.da1 = take((size_t)B * h * 4);
   P.dpooled = take((size_t)B * d * 4);
@@ -379,7 +380,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     TCL_LAUNCH(T, "scan_bwd", launch_scan_bwd(B, E, L, N, R, offs, B16(Ly.u), F32(Ly.xdbl), B16(Ly.xz),
                                               B16(Ly.y), F32(P.dyg), W.W_dt, W.b_dt, W.A_log, W.D,
                                               F32(Ly.ckpt), F32(P.dv), F32(P.du), F32(P.dxz),
-                                              F32(P.dxdbl), F32(Ly.p_A), F32(Ly.p_D), s));
+                                              F32(P.dxdbl), F32(Ly.p_A), F32(Ly.p_D), F32(P.dbc_part), s));
     {  // d dt_r = dv W_dt  -> columns [0, R) of dxdbl
       GemmArgs g;
       g.A = F32(P.dv); g.lda = E; g.W = W.W_dtT; g.ldw = E; g.C = F32(P.dxdbl); g.ldc = XW;
