@@ -607,8 +607,13 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
   constexpr int WP = Stage::WP;
   constexpr int PART = 32 * WP;
   static_assert((FL & (kRowNorm | kGather)) == 0, "plain, bias and residual GEMMs only");
+  // PAIR: column blocks in pairs whose MFMAs alternate between the two
+  // accumulators (no MFMA waits for the one before it), one barrier per
+  // pair, W staged through a ring of four one-block LDS buffers
+  constexpr bool PAIR = NB >= 4 && KC <= 2;
+  constexpr int NBUF = PAIR ? 4 : 2;
 
-  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 3 * PART];
+  __shared__ __attribute__((aligned(16))) uint16_t sW[NBUF * 3 * PART];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -632,6 +637,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
   st.stage(&sW[0], tid);
+  if constexpr (PAIR) {
+    st.load(wres, tid, 32, p.N, ldws, Kw, 0);
+    st.stage(&sW[3 * PART], tid);
+  }
 
 #pragma unroll
   for (int c = 0; c < KCH; ++c) {
@@ -646,6 +655,68 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
       load8(arow, rok, c * KC * 64 + 16 * s2 + 8 * lg, p.K, v0, v1);
       split8(v0, v1, a1[s2], a2[s2], a3[s2]);
     }
+    if constexpr (PAIR) {
+#pragma unroll
+      for (int pp = 0; pp < NB / 2; ++pp) {
+        const int g = c * NB + 2 * pp;  // global index of the pair's first block
+        __syncthreads();  // this pair visible; the previous pair's buffers are free
+        const bool more = pp + 1 < NB / 2 || c + 1 < KCH;
+        const int ncol = pp + 1 < NB / 2 ? (2 * pp + 2) * 32 : 0;
+        const int nk = pp + 1 < NB / 2 ? c * KC * 64 : (c + 1) * KC * 64;
+        if (more) st.load(wres, tid, ncol, p.N, ldws, Kw, nk);
+
+        const uint16_t* wb0 = &sW[(g & 3) * 3 * PART + li * WP + 8 * lg];
+        const uint16_t* wb1 = &sW[((g + 1) & 3) * 3 * PART + li * WP + 8 * lg];
+        auto wfrag = [&](const uint16_t* wb, int part, int ks) {
+          return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+        };
+        bf16x8 q[2][6];
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+          q[0][j] = wfrag(wb0, j, 0);
+          q[0][3 + j] = wfrag(wb1, j, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x0100, 6, 0);
+        floatx16& x0 = acc[2 * pp];
+        floatx16& x1 = acc[2 * pp + 1];
+#pragma unroll
+        for (int ks = 0; ks < NS; ++ks) {
+          if (ks + 1 < NS) {
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+              q[(ks + 1) & 1][j] = wfrag(wb0, j, ks + 1);
+              q[(ks + 1) & 1][3 + j] = wfrag(wb1, j, ks + 1);
+            }
+          }
+          const bf16x8* w = q[ks & 1];
+          x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[0], x0, 0, 0, 0);
+          x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a3[ks], w[3], x1, 0, 0, 0);
+          x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[1], x0, 0, 0, 0);
+          x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[4], x1, 0, 0, 0);
+          x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[2], x0, 0, 0, 0);
+          x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[5], x1, 0, 0, 0);
+          x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[0], x0, 0, 0, 0);
+          x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2[ks], w[3], x1, 0, 0, 0);
+          x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[1], x0, 0, 0, 0);
+          x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[4], x1, 0, 0, 0);
+          x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[0], x0, 0, 0, 0);
+          x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks], w[3], x1, 0, 0, 0);
+          if (ks + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 6, 0);
+          __builtin_amdgcn_sched_group_barrier(0x0008, 12, 0);
+          // the next pair's two blocks: the first staged a quarter of the
+          // way through, the second loaded then and staged at three quarters
+          if (ks == NS / 4 && more) {
+            st.stage(&sW[((g + 2) & 3) * 3 * PART], tid);
+            __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
+            st.load(wres, tid, ncol + 32, p.N, ldws, Kw, nk);
+          }
+          if (ks == 3 * NS / 4 && more) {
+            st.stage(&sW[((g + 3) & 3) * 3 * PART], tid);
+            __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
+          }
+        }
+      }
+    } else {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int buf = (c * NB + nb) & 1;
@@ -683,6 +754,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
           __builtin_amdgcn_sched_group_barrier(0x0200, Stage::NW, 0);
         }
       }
+    }
     }
   }
 
