@@ -156,7 +156,12 @@ TCL_API size_t tcl_score_workspace_bytes(const tcl_model* model, int32_t B, int3
  *   d_workspace, ws_bytes: >= tcl_score_workspace_bytes(model, B, L) bytes,
  *   256-byte aligned; its contents on entry are ignored.
  * Only the valid tokens are computed: tokens are packed program by program
- * on the device and every kernel works on the packed rows. */
+ * on the device and every kernel works on the packed rows.
+ * Work is ordered on `stream` (NULL: the default stream). Batches of 2048
+ * programs or more run as two halves on two streams the model owns, forked
+ * from `stream` and joined back into it by events, so the call is still
+ * ordered on `stream` as a whole (and can be captured into a graph);
+ * calls on one model must not be issued from several host threads at once. */
 TCL_API tcl_status tcl_score(tcl_model* model, int32_t B, int32_t L, const float* d_feats,
                              const int32_t* d_lengths, float* d_scores, void* d_workspace,
                              size_t ws_bytes, void* stream);
@@ -167,9 +172,16 @@ TCL_API tcl_status tcl_get_params(const tcl_model* model, float* h_out, size_t n
 /* Replace the parameters from a host blob (synchronous, like create). */
 TCL_API tcl_status tcl_set_params(tcl_model* model, const float* h_params, size_t n_params);
 
+/* How tcl_score runs a batch of >= 2048 programs: n = 2 (the default) as two
+ * concurrent halves on the model's two streams, n = 1 as one pass on the
+ * caller's stream (the same scores, bit for bit; one pass gives each
+ * kernel's own time without the other half's kernels beside it). Other
+ * values: TCL_ERR_INVALID_ARG. A workspace sized for n = 2 also serves n = 1. */
+TCL_API tcl_status tcl_set_score_streams(tcl_model* model, int32_t n);
+
 /* Per-kernel timing, for measurement. While enabled, every kernel launch of
- * tcl_score is bracketed by a pair of hipEvents recorded on the caller's
- * stream (the stream the kernel runs on), grouped by kernel name.
+ * tcl_score is bracketed by a pair of hipEvents recorded on the stream the
+ * kernel runs on (the caller's, or a half batch's), grouped by kernel name.
  * tcl_timing_get waits for the recorded events and returns, for entry
  * `idx` in [0, tcl_timing_count(model)), the kernel name (library-owned
  * string), the summed duration in milliseconds and the number of launches.

@@ -49,6 +49,7 @@ _SIGS = {
     "tcl_cost_model_create": (_i32, [ctypes.POINTER(Config), _vp, _sz, ctypes.POINTER(_vp)]),
     "tcl_cost_model_destroy": (_i32, [_vp]),
     "tcl_score_workspace_bytes": (_sz, [_vp, _i32, _i32]),
+    "tcl_set_score_streams": (_i32, [_vp, _i32]),
     "tcl_score": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "tcl_get_params": (_i32, [_vp, _vp, _sz]),
     "tcl_set_params": (_i32, [_vp, _vp, _sz]),
@@ -191,6 +192,11 @@ class CostModel:
         check(lib().tcl_score(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), out.data_ptr(),
                               ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)))
         return out
+
+    def set_score_streams(self, n: int):
+        """1: one pass per batch; 2 (default): batches of >= 2048 programs as
+        two concurrent halves (tcl_set_score_streams)."""
+        check(lib().tcl_set_score_streams(self._h, n))
 
     def timing(self, enable: bool):
         check(lib().tcl_timing_enable(self._h, int(enable)))

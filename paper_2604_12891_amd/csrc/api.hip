@@ -480,6 +480,31 @@ TCL_API size_t tcl_param_count(const tcl_config* cfg) {
 
 TCL_API const char* tcl_last_error(void) { return last_error(); }
 
+namespace {
+// Batches of at least this many programs are scored as two concurrent halves
+// (measured at B = 4096, L = 25: 3% faster than one pass; four quarters were
+// slower than one pass).
+constexpr int kScoreSplitMinB = 2048;
+
+bool score_split(const tcl_model* m, int B, int L) {
+  return m->score_streams == 2 && m->aux[0] && m->aux[1] && B >= kScoreSplitMinB &&
+         ((int64_t)(B / 2) * L * m->cfg.F * 4) % 16 == 0;  // the second half's features stay 16-byte aligned
+}
+
+size_t score_ws_bytes(const tcl_model* m, int B, int L) {
+  if (!score_split(m, B, L)) return score_plan(m->cfg, B, L).total;
+  const int h = B / 2;
+  return align256(score_plan(m->cfg, h, L).total) + score_plan(m->cfg, B - h, L).total;
+}
+
+void release_streams(tcl_model* m) {
+  for (auto& e : m->ev)
+    if (e) (void)hipEventDestroy(e), e = nullptr;
+  for (auto& q : m->aux)
+    if (q) (void)hipStreamDestroy(q), q = nullptr;
+}
+}  // namespace
+
 TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_params,
                                          size_t n_params, tcl_model** out) {
   if (!out) return fail(TCL_ERR_INVALID_ARG, "out is NULL");
@@ -577,12 +602,21 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
     return cleanup(fail(TCL_ERR_HIP, "upload of the derivation table failed"));
   st = load_params(m, h_params);
   if (st != TCL_OK) return cleanup(st);
+  // default-priority streams for tcl_score's half batches
+  bool ok = true;
+  for (int i = 0; i < 2 && ok; ++i) ok = hipStreamCreateWithFlags(&m->aux[i], hipStreamNonBlocking) == hipSuccess;
+  for (int i = 0; i < 3 && ok; ++i) ok = hipEventCreateWithFlags(&m->ev[i], hipEventDisableTiming) == hipSuccess;
+  if (!ok) {
+    release_streams(m);
+    (void)hipGetLastError();
+  }
   *out = m;
   return TCL_OK;
 }
 
 TCL_API tcl_status tcl_cost_model_destroy(tcl_model* m) {
   if (!m) return TCL_OK;
+  release_streams(m);
   m->timing.release();
   if (m->dev) (void)hipFree(m->dev);
   delete m;
@@ -608,7 +642,7 @@ TCL_API tcl_status tcl_set_params(tcl_model* m, const float* h_params, size_t n)
 
 TCL_API size_t tcl_score_workspace_bytes(const tcl_model* m, int32_t B, int32_t L) {
   if (!m || B <= 0 || L <= 0) return 0;
-  return score_plan(m->cfg, B, L).total;
+  return score_ws_bytes(m, B, L);
 }
 
 TCL_API tcl_status tcl_score(tcl_model* m, int32_t B, int32_t L, const float* d_feats,
@@ -622,14 +656,39 @@ TCL_API tcl_status tcl_score(tcl_model* m, int32_t B, int32_t L, const float* d_
     return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
   if (reinterpret_cast<uintptr_t>(d_feats) % 16 || reinterpret_cast<uintptr_t>(d_ws) % 256)
     return fail(TCL_ERR_INVALID_ARG, "d_feats must be 16-byte and d_workspace 256-byte aligned");
-  const ScorePlan p = score_plan(m->cfg, B, L);
-  if (ws_bytes < p.total)
-    return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, p.total);
-  return run_score(m, B, L, d_feats, d_lengths, d_scores, static_cast<char*>(d_ws),
-                   static_cast<hipStream_t>(stream));
+  const size_t need = score_ws_bytes(m, B, L);
+  if (ws_bytes < need) return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(d_ws);
+  if (!score_split(m, B, L)) return run_score(m, B, L, d_feats, d_lengths, d_scores, ws, s);
+  // two half batches on the model's two streams, forked from and joined
+  // back into the caller's stream: each half's kernels fill the CUs the
+  // other's leave idle (launch gaps, the last round of a grid)
+  const int h = B / 2;
+  const size_t off2 = align256(score_plan(m->cfg, h, L).total);
+  TCL_HIP(hipEventRecord(m->ev[0], s));
+  TCL_HIP(hipStreamWaitEvent(m->aux[0], m->ev[0], 0));
+  TCL_HIP(hipStreamWaitEvent(m->aux[1], m->ev[0], 0));
+  tcl_status st = run_score(m, h, L, d_feats, d_lengths, d_scores, ws, m->aux[0]);
+  if (st != TCL_OK) return st;
+  st = run_score(m, B - h, L, d_feats + (int64_t)h * L * m->cfg.F, d_lengths + h, d_scores + h, ws + off2,
+                 m->aux[1]);
+  if (st != TCL_OK) return st;
+  TCL_HIP(hipEventRecord(m->ev[1], m->aux[0]));
+  TCL_HIP(hipEventRecord(m->ev[2], m->aux[1]));
+  TCL_HIP(hipStreamWaitEvent(s, m->ev[1], 0));
+  TCL_HIP(hipStreamWaitEvent(s, m->ev[2], 0));
+  return TCL_OK;
 }
 
 // ------------------------------------------------------------------ timing
+
+TCL_API tcl_status tcl_set_score_streams(tcl_model* m, int32_t n) {
+  if (!m) return fail(TCL_ERR_INVALID_ARG, "model is NULL");
+  if (n != 1 && n != 2) return fail(TCL_ERR_INVALID_ARG, "n must be 1 or 2 (got %d)", n);
+  m->score_streams = n;
+  return TCL_OK;
+}
 
 TCL_API tcl_status tcl_timing_enable(tcl_model* m, int32_t enable) {
   if (!m) return fail(TCL_ERR_INVALID_ARG, "model is NULL");

@@ -83,6 +83,11 @@ struct Timing {
 struct tcl_model {
   tcl_config cfg{};
   int device = 0;
+  // tcl_score's two half-batch streams and their fork/join events (null
+  // when they could not be created: the batch then runs as one)
+  hipStream_t aux[2] = {nullptr, nullptr};
+  hipEvent_t ev[3] = {nullptr, nullptr, nullptr};
+  int score_streams = 2;  // tcl_set_score_streams
   size_t n_params = 0;
   void* dev = nullptr;
   size_t dev_bytes = 0;

@@ -197,3 +197,35 @@ def test_workspace_too_small_is_rejected():
     with pytest.raises(tb.TclError) as e:
         m.score(X, lens, workspace=ws)
     assert e.value.status == -3
+
+
+def test_two_concurrent_halves_match_separate_calls():
+    """A batch of >= 2048 programs runs as two halves on the model's two
+    streams; its scores are the same bits as scoring the programs in
+    smaller single-stream batches (every kernel treats rows and programs
+    independently and in a fixed order), and the workspace query covers
+    both halves."""
+    w = wl.WORKLOADS["score_B4096_L25_d256_f32"]
+    blob, X, lengths = wl.make_workload(w.name)
+    m = _model(w.model, blob)
+    B, L = X.shape[:2]
+    assert m.workspace_bytes(B, L) >= 2 * m.workspace_bytes(1000, L)
+    print("tcl_score two halves vs batches of 1000", flush=True)
+    g = _score(m, X, lengths)
+    parts = [_score(m, X[i:i + 1000], lengths[i:i + 1000]) for i in range(0, B, 1000)]
+    np.testing.assert_array_equal(g, np.concatenate(parts))
+    # one pass over the whole batch: the same bits
+    m.set_score_streams(1)
+    np.testing.assert_array_equal(_score(m, X, lengths), g)
+    m.set_score_streams(2)
+    for bad in (0, 3, -1):
+        with pytest.raises(tb.TclError):
+            m.set_score_streams(bad)
+    # and on a non-default stream, twice in a row
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        out = torch.empty(B, device="cuda")
+        for _ in range(2):
+            m.score(torch.from_numpy(X).cuda(), torch.from_numpy(lengths).cuda(), out=out, stream=s)
+    s.synchronize()
+    np.testing.assert_array_equal(out.cpu().numpy(), g)
