@@ -229,3 +229,35 @@ def test_two_concurrent_halves_match_separate_calls():
             m.score(torch.from_numpy(X).cuda(), torch.from_numpy(lengths).cuda(), out=out, stream=s)
     s.synchronize()
     np.testing.assert_array_equal(out.cpu().numpy(), g)
+
+
+@pytest.mark.parametrize("B", [2048, 2049, 2051])
+def test_two_halves_edges(B):
+    """The split at B = 2048 (halves of 1024), odd B (the second half one
+    program longer), invalid and empty programs on both sides of the split
+    point: scores match the one-pass run bit for bit, invalid ones are NaN,
+    and a workspace one byte short is refused."""
+    w = wl.WORKLOADS["score_B4096_L25_d256_f32"]
+    blob, X, lengths = wl.make_workload(w.name, B=B, perturb=True)
+    h = B // 2
+    lengths = lengths.copy()
+    lengths[[h - 1, h, h + 1, 0, B - 1]] = [0, 26, 1, -3, 25]
+    X = X.copy()
+    X[h + 1, 1:] = 0.0
+    m = _model(w.model, blob)
+    print(f"tcl_score two halves B={B}", flush=True)
+    g2 = _score(m, X, lengths)
+    m.set_score_streams(1)
+    g1 = _score(m, X, lengths)
+    m.set_score_streams(2)
+    np.testing.assert_array_equal(g2, g1)
+    bad = np.zeros(B, bool)
+    bad[[h - 1, h, 0]] = True
+    assert np.all(np.isnan(g2[bad])) and np.all(np.isfinite(g2[~bad]))
+    idx = np.array([1, h + 1, h + 2, B - 1])
+    assert_scores_match(g2[idx], oracle_scores(blob, X[idx], lengths[idx], w.model), "f32", "split edges")
+    L = X.shape[1]
+    need = m.workspace_bytes(B, L)
+    ws = torch.empty(need - 1, dtype=torch.uint8, device="cuda")
+    with pytest.raises(tb.TclError):
+        m.score(torch.from_numpy(X).cuda(), torch.from_numpy(lengths).cuda(), workspace=ws)
