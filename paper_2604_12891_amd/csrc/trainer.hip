@@ -299,9 +299,18 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   const int* Mdev = offs + B;
   Timing& T = tr->timing;
 
-  // 1. frozen teacher
-  st = run_score(tr->teacher, B, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws, s);
+  // 1. frozen teacher, on the teacher model's first stream where it has one:
+  // it shares nothing with the student's forward but the inputs, so the two
+  // forwards run side by side until the loss needs the teacher's scores
+  tcl_model* Tm = tr->teacher;
+  const bool fork = Tm->aux[0] && Tm->ev[0] && Tm->ev[1];
+  if (fork) {
+    TCL_HIP(hipEventRecord(Tm->ev[0], s));
+    TCL_HIP(hipStreamWaitEvent(Tm->aux[0], Tm->ev[0], 0));
+  }
+  st = run_score(Tm, B, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws, fork ? Tm->aux[0] : s);
   if (st != TCL_OK) return st;
+  if (fork) TCL_HIP(hipEventRecord(Tm->ev[1], Tm->aux[0]));
 
   // 2. student forward, keeping activations
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
@@ -340,7 +349,8 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
                                         c.norm_eps, S->W1T, S->b1, S->W2, S->b2, F32(P.s_scores), s,
                                         F32(P.pooled), F32(P.a1)));
 
-  // 3. loss, head, pool and final norm
+  // 3. loss, head, pool and final norm (the teacher's scores are needed from here)
+  if (fork) TCL_HIP(hipStreamWaitEvent(s, Tm->ev[1], 0));
   if (kd) {
     // beta L(s; labels) + (1 - beta) phi L(s; teacher): dL/ds and the loss
     TCL_LAUNCH(T, "lambdarank", launch_lambdarank(B, 2, F32(P.s_scores), d_labels, F32(P.t_scores), kd->sigma,
