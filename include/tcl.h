@@ -229,7 +229,11 @@ TCL_API size_t tcl_distill_workspace_bytes(const tcl_trainer* trainer, int32_t B
  *   d_workspace >= tcl_distill_workspace_bytes, 256-byte aligned.
  * The first step with a new (B, L) uploads a small reduction table and
  * synchronises the device once. Programs with invalid lengths must not be
- * passed (their NaN scores would poison the loss). */
+ * passed (their NaN scores would poison the loss). The teacher's forward
+ * runs on the teacher model's first stream, forked from `stream` and joined
+ * back before the loss by events, beside the student's forward; the step is
+ * ordered on `stream` as a whole, and calls that use the teacher model must
+ * not be issued from several host threads at once. */
 TCL_API tcl_status tcl_distill_step(tcl_trainer* trainer, int32_t B, int32_t L, const float* d_feats,
                                     const int32_t* d_lengths, const float* d_labels, float* d_loss,
                                     void* d_workspace, size_t ws_bytes, void* stream);
