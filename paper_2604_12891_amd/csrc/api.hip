@@ -149,7 +149,9 @@ hipError_t model_gemm(const tcl_model* m, const GemmArgs& a, const uint16_t* Ws,
 }
 
 tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string& tag, int i, int B, int L,
-                                     const int* offs, const float* A, float* C, bool act, hipStream_t s) {
+                                     const int* offs, const float* A, float* C, bool act, hipStream_t s,
+                                     uint8_t* tpos_out, bool* tpos_written) {
+  if (tpos_written) *tpos_written = false;
   const tcl_config& c = m->cfg;
   const BlobLayout bl = blob_layout(c);
   const int in = i == 0 ? m->ldw0 : bl.enc_dims[i], out = bl.enc_dims[i + 1];
@@ -159,6 +161,12 @@ tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string&
   if (i == 0) {
     // the gathered input Linear (rows b*L + t of the padded input)
     g.offs = offs; g.B = B; g.L = L; g.W = m->W0; g.ldw = m->ldw0; g.bias = m->b0;
+    // on the split path the row lookup of the gather also yields the token positions
+    const bool on_split = m->split && m->W0_s && gemm_split_variant(g, kBias | kGather) > 0;
+    if (on_split && tpos_out) {
+      g.tpos = tpos_out;
+      if (tpos_written) *tpos_written = true;
+    }
     TCL_LAUNCH(T, (tag + "gemm_input").c_str(), model_gemm(m, g, m->W0_s, m->ldw0_h, kBias | kGather, s));
   } else {
     g.W = m->We[i]; g.ldw = in; g.bias = m->be[i];
@@ -220,7 +228,6 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
 
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
   uint8_t* tpos = reinterpret_cast<uint8_t*>(ws + p.tpos);
-  if (c.dtype == TCL_F32 && m->split) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
   // features whose row length is not a multiple of 4 are first copied into
   // rows padded with zeros (the input Linear reads 16-byte vectors)
   const float* feats = d_feats;
@@ -238,12 +245,16 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     // the last
     const int n_enc = blob_layout(c).n_enc;
     float* bufs[2] = {reinterpret_cast<float*>(ws + p.enc1), reinterpret_cast<float*>(ws + p.enc2)};
+    bool tpos_done = false;
     for (int i = 0; i < n_enc; ++i) {
       const bool last = i == n_enc - 1;
       tcl_status st = enqueue_encoder_layer_f32(m, T, "", i, B, L, offs, i == 0 ? feats : bufs[i - 1],
-                                                last ? H : bufs[i], !last, s);
+                                                last ? H : bufs[i], !last, s, m->split ? tpos : nullptr,
+                                                i == 0 ? &tpos_done : nullptr);
       if (st != TCL_OK) return st;
     }
+    // the token positions for the conv fused into x_proj, unless the input Linear wrote them
+    if (m->split && !tpos_done) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
     for (int l = 0; l < c.n_layers; ++l) {
       tcl_status st = enqueue_block_f32(m, T, "", l, B, L, offs, m->split ? tpos : nullptr, H, xz, u, xdbl, s);
       if (st != TCL_OK) return st;

@@ -189,6 +189,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32_kernel(GemmArgs p
           if (p.offs[mid] <= grow) lo = mid; else hi = mid;
         }
         src = lo * p.L + (grow - p.offs[lo]);
+        if (p.tpos) p.tpos[grow] = (uint8_t)min(grow - p.offs[lo], 255);
       }
     }
     sSrc[r] = src;
@@ -343,6 +344,7 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
           if (p.offs[mid] <= grow) lo = mid; else hi = mid;
         }
         src = lo * p.L + (grow - p.offs[lo]);
+        if (p.tpos) p.tpos[grow] = (uint8_t)min(grow - p.offs[lo], 255);
       }
     }
     sSrc[r] = src;

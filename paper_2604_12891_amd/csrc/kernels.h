@@ -33,6 +33,8 @@ struct GemmArgs {
   int N = 0, K = 0;
   float eps = 0.f;
   int relu = 0;               // nonzero: C = max(result, 0) (after bias and residual)
+  uint8_t* tpos = nullptr;    // gather on the split path: also write each packed row's position
+                              // in its program, clamped to 255 (launch_token_pos's array)
 };
 
 // Tile shapes (rows x columns of C per workgroup, 4 or 8 wavefronts, K staged

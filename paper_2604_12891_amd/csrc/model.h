@@ -139,8 +139,11 @@ hipError_t model_gemm(const tcl_model* m, const GemmArgs& a, const uint16_t* Ws,
 // then the [B, L, ldw0] padded input) from A to C, ReLU when `act`; and
 // Mamba block l in place on the residual stream H [tokens, d]. Launches are
 // timed under tag + kernel name.
+// tpos_out (layer 0 only, optional): where the split path's gathered input
+// Linear also writes the token positions; *tpos_written tells whether it did.
 tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string& tag, int i, int B, int L,
-                                     const int* offs, const float* A, float* C, bool act, hipStream_t s);
+                                     const int* offs, const float* A, float* C, bool act, hipStream_t s,
+                                     uint8_t* tpos_out = nullptr, bool* tpos_written = nullptr);
 // tpos (per packed row, its position in its program; launch_token_pos) lets
 // the split path fuse the conv into x_proj; null: the conv runs on its own.
 tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, int l, int B, int L,
