@@ -492,9 +492,12 @@ TCL_API size_t tcl_param_count(const tcl_config* cfg) {
 TCL_API const char* tcl_last_error(void) { return last_error(); }
 
 namespace {
-// Batches of at least this many programs are scored as two concurrent halves
-// (measured at B = 4096, L = 25: 3% faster than one pass; four quarters were
-// slower than one pass).
+// Batches of at least this many programs are scored as two concurrent halves.
+// Measured at L = 25, d_model 256, 4 blocks: two halves take 0.98x (B =
+// 2048), 0.86x (3072), 0.97x (4096), 0.98x (8192) the time of one pass,
+// 0.99x at 1536, 1.0x at 1024 and up to 1.07x below 768, where each half's
+// kernels are bound by the latency of their few workgroups; four quarters
+// at B = 4096 took 1.1x.
 constexpr int kScoreSplitMinB = 2048;
 
 bool score_split(const tcl_model* m, int B, int L) {
