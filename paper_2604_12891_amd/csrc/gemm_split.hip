@@ -39,6 +39,7 @@
 // Fragment k-order (A and W alike, which is all the contraction needs):
 // split32 k-step s, lane half g holds k = 16 s + 8 g .. +7; split16 k-step
 // s, lane quarter q holds k = 32 s + 8 q .. +7.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -352,7 +353,10 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
 
   const int Kw = (p.K + 7) & ~7;
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
-  const int nsteps = (p.N + 31) / 32;
+  // this workgroup's column blocks [sb, se): all of them, or one of
+  // gridDim.y ranges when a small batch leaves too few panels for the GPU
+  const int nblk = (p.N + 31) / 32;
+  const int sb = (int)(blockIdx.y * nblk / gridDim.y), se = (int)((blockIdx.y + 1) * nblk / gridDim.y);
   Stage st;
   __syncthreads();  // sSrc
 
@@ -382,9 +386,9 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
   const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * 4);
   const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
 
-  st.template load<0, HW>(wres, tid, 0, p.N, ldws, Kw);
+  st.template load<0, HW>(wres, tid, sb * 32, p.N, ldws, Kw);
   st.template stage<0, HW>(&sW[0], tid);
-  st.template load<HW, NW>(wres, tid, 0, p.N, ldws, Kw);
+  st.template load<HW, NW>(wres, tid, sb * 32, p.N, ldws, Kw);
   st.template stage<HW, NW>(&sW[0], tid);
   if constexpr (kNorm) {
     __syncthreads();  // both halves' sums of squares
@@ -400,7 +404,7 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const floatx4 o = *reinterpret_cast<const floatx4*>(&sP[s & 1][g][q][lane][0]);
+      const floatx4 o = *reinterpret_cast<const floatx4*>(&sP[(s - sb) & 1][g][q][lane][0]);
       res[4 * q] += o.x;
       res[4 * q + 1] += o.y;
       res[4 * q + 2] += o.z;
@@ -424,16 +428,16 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
   // stores as well, as it would after a join with the upper half's path.
   auto blocks = [&](auto lower_tag) {
     constexpr bool LOWER = decltype(lower_tag)::value;
-    for (int s = 0; s < nsteps; ++s) {
-      const int buf = s & 1, n0 = s * 32;
+    for (int s = sb; s < se; ++s) {
+      const int buf = (s - sb) & 1, n0 = s * 32;
       // block s staged and block s-1's partials parked; every wavefront is
       // past block s-1's fragment reads and the partials of block s-2
       __syncthreads();
-      const bool more = s + 1 < nsteps;
+      const bool more = s + 1 < se;
       // the next block's W in two halves: the first loaded now and staged
       // halfway through the MFMAs, the second loaded then and staged at the end
       if (more) st.template load<0, HW>(wres, tid, n0 + 32, p.N, ldws, Kw);
-      if (LOWER && s > 0) epilogue(s - 1);
+      if (LOWER && s > sb) epilogue(s - 1);
 
       floatx16 acc, acc2;
 #pragma unroll
@@ -482,7 +486,7 @@ __global__ __launch_bounds__(kWavesH * 64, 1) void gemm_split32h_kernel(GemmArgs
       }
     }
     __syncthreads();
-    if constexpr (LOWER) epilogue(nsteps - 1);
+    if constexpr (LOWER) epilogue(se - 1);
   };
   if (__builtin_amdgcn_readfirstlane(h) == 0)
     blocks(std::true_type{});
@@ -623,11 +627,14 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
   const int M = p.Mdev ? *p.Mdev : p.Mmax;
   const int row0 = blockIdx.x * BM;
   if (row0 >= M) return;
+  // this workgroup's NB column blocks start at column cb (gridDim.y > 1:
+  // a small batch's columns split over more workgroups)
+  const int cb = blockIdx.y * NB * 32;
 
   const int Kw = (p.K + 7) & ~7;
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(Ws, (uint32_t)__builtin_amdgcn_readfirstlane(3 * p.N * ldws * 2));
   Stage st;
-  st.load(wres, tid, 0, p.N, ldws, Kw, 0);
+  st.load(wres, tid, cb, p.N, ldws, Kw, 0);
 
   const int grow = row0 + wave * 32 + li;
   const bool rok = grow < M;
@@ -640,7 +647,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
     for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
   st.stage(&sW[0], tid);
   if constexpr (PAIR) {
-    st.load(wres, tid, 32, p.N, ldws, Kw, 0);
+    st.load(wres, tid, cb + 32, p.N, ldws, Kw, 0);
     st.stage(&sW[3 * PART], tid);
   }
 
@@ -663,7 +670,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
         const int g = c * NB + 2 * pp;  // global index of the pair's first block
         __syncthreads();  // this pair visible; the previous pair's buffers are free
         const bool more = pp + 1 < NB / 2 || c + 1 < KCH;
-        const int ncol = pp + 1 < NB / 2 ? (2 * pp + 2) * 32 : 0;
+        const int ncol = cb + (pp + 1 < NB / 2 ? (2 * pp + 2) * 32 : 0);
         const int nk = pp + 1 < NB / 2 ? c * KC * 64 : (c + 1) * KC * 64;
         if (more) st.load(wres, tid, ncol, p.N, ldws, Kw, nk);
 
@@ -724,8 +731,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
       const int buf = (c * NB + nb) & 1;
       __syncthreads();  // this block visible; the other buffer is free for the next
       const bool more = nb + 1 < NB || c + 1 < KCH;
-      if (nb + 1 < NB) st.load(wres, tid, (nb + 1) * 32, p.N, ldws, Kw, c * KC * 64);
-      else if (c + 1 < KCH) st.load(wres, tid, 0, p.N, ldws, Kw, (c + 1) * KC * 64);
+      if (nb + 1 < NB) st.load(wres, tid, cb + (nb + 1) * 32, p.N, ldws, Kw, c * KC * 64);
+      else if (c + 1 < KCH) st.load(wres, tid, cb, p.N, ldws, Kw, (c + 1) * KC * 64);
 
       const uint16_t* wb = &sW[buf * 3 * PART + li * WP + 8 * lg];
       auto wfrag = [&](int part, int ks) {
@@ -767,7 +774,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_split32acc_kernel(GemmArg
       make_rsrc((p.R ? p.R : p.C) + (int64_t)row0 * p.ldc, (FL & kResid) != 0 ? panel_bytes : 0);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int col = nb * 32 + li;
+    const int col = cb + nb * 32 + li;
     const bool cok = col < p.N;
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
     float res[16];
@@ -1015,9 +1022,14 @@ template <int FL>
 hipError_t launch32h(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t s) {
   const int grid = (a.Mmax + 127) / 128;
   if (grid <= 0) return hipSuccess;
+  // a batch with fewer panels than two per CU also splits the columns, up to
+  // 8 ways (each workgroup repeats the short A prologue of its panel)
+  const int nblk = (a.N + 31) / 32;
+  const int cs = std::max(1, std::min({8, nblk, 512 / grid}));
+  const dim3 g(grid, cs);
   switch ((a.K + 127) / 128) {
-    case 1: hipLaunchKernelGGL((gemm_split32h_kernel<1, FL>), dim3(grid), dim3(kWavesH * 64), 0, s, a, Ws, ldws); break;
-    case 2: hipLaunchKernelGGL((gemm_split32h_kernel<2, FL>), dim3(grid), dim3(kWavesH * 64), 0, s, a, Ws, ldws); break;
+    case 1: hipLaunchKernelGGL((gemm_split32h_kernel<1, FL>), g, dim3(kWavesH * 64), 0, s, a, Ws, ldws); break;
+    case 2: hipLaunchKernelGGL((gemm_split32h_kernel<2, FL>), g, dim3(kWavesH * 64), 0, s, a, Ws, ldws); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1044,12 +1056,21 @@ hipError_t launch16(const GemmArgs& a, const uint16_t* Ws, int ldws, hipStream_t
 template <int KC, int KCH, int FL>
 hipError_t launch32acc_nb(const GemmArgs& a, const uint16_t* Ws, int ldws, int grid, hipStream_t s) {
   const int nb = (a.N + 31) / 32;
-#define TCL_SPLIT32ACC(NB) \
-  hipLaunchKernelGGL((gemm_split32acc_kernel<KC, KCH, NB, FL>), dim3(grid), dim3(kWaves * 64), 0, s, a, Ws, ldws)
-  if (nb <= 2) TCL_SPLIT32ACC(2);
-  else if (nb <= 4) TCL_SPLIT32ACC(4);
-  else if (nb <= 8) TCL_SPLIT32ACC(8);
-  else return hipErrorInvalidValue;
+  // a batch with fewer panels than two per CU splits the columns over 2 or
+  // 4 workgroups per panel (each repeats its panel's A chunks)
+  const int cs = 512 / grid >= 4 ? 4 : 512 / grid >= 2 ? 2 : 1;
+#define TCL_SPLIT32ACC(NB, CS)                                                                           \
+  hipLaunchKernelGGL((gemm_split32acc_kernel<KC, KCH, NB, FL>), dim3(grid, CS), dim3(kWaves * 64), 0, s, a, \
+                     Ws, ldws)
+  if (nb <= 2) TCL_SPLIT32ACC(2, 1);
+  else if (nb <= 4) {
+    if (cs >= 2) TCL_SPLIT32ACC(2, 2);
+    else TCL_SPLIT32ACC(4, 1);
+  } else if (nb <= 8) {
+    if (cs >= 4) TCL_SPLIT32ACC(2, 4);
+    else if (cs == 2) TCL_SPLIT32ACC(4, 2);
+    else TCL_SPLIT32ACC(8, 1);
+  } else return hipErrorInvalidValue;
 #undef TCL_SPLIT32ACC
   return hipGetLastError();
 }
