@@ -171,7 +171,7 @@ def distill_kernel_work(tshape, sshape, M_v: int, B: int) -> dict:
     XW = R + 2 * N
     per_layer = d * E + E * R + XW * E + 2 * E * d  # out_proj, dt_proj, x_proj, in_proj
     tw = kernel_work(tshape, M_v, B, "bf16")
-    per_block = ("gemm_in_proj", "gemm_x_proj", "gemm_out_proj", "conv_silu", "scan")
+    per_block = ("gemm_in_proj", "gemm_x_proj", "gemm_x_proj_conv", "gemm_out_proj", "conv_silu", "scan")
     out = {}
     for k, (kind, amount) in tw.items():
         reps = tshape.n_layers if k in per_block else 1

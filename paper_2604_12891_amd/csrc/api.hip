@@ -268,6 +268,17 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = ldf;
     TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
 
+    // the conv + SiLU fused in front of x_proj where the shape allows
+    auto conv_args = [&](int l) {
+      const auto& W = m->layers[l];
+      ConvArgsBF16 a;
+      a.x = xz; a.ldx = 2 * E; a.w = W.conv_w; a.b = W.conv_b; a.tpos = tpos; a.u = u;
+      a.W = W.W_x_h; a.ldw = E; a.C = xdbl; a.ldc = XW; a.Mdev = offs + B; a.Mmax = Mmax; a.N = XW; a.E = E;
+      return a;
+    };
+    const bool fuse = gemm_bf16_conv_supports(conv_args(0), c.d_conv);
+    if (fuse) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
+
     for (int l = 0; l < c.n_layers; ++l) {
       const auto& W = m->layers[l];
       GemmArgsBF16 gi;
@@ -275,12 +286,16 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
       TCL_LAUNCH(T, "gemm_in_proj", launch_gemm_bf16(gi, kNormF32toBF16, -1, s));
 
-      TCL_LAUNCH(T, "conv_silu", launch_conv_silu<uint16_t>(B, E, c.d_conv, offs, xz, 2 * E,
-                                                            W.conv_w, W.conv_b, u, s));
-      GemmArgsBF16 gx;
-      gx.A = u; gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
-      gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
-      TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32, -1, s));
+      if (fuse) {
+        TCL_LAUNCH(T, "gemm_x_proj_conv", launch_gemm_bf16_conv(conv_args(l), s));
+      } else {
+        TCL_LAUNCH(T, "conv_silu", launch_conv_silu<uint16_t>(B, E, c.d_conv, offs, xz, 2 * E,
+                                                              W.conv_w, W.conv_b, u, s));
+        GemmArgsBF16 gx;
+        gx.A = u; gx.lda = E; gx.W = W.W_x_h; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
+        gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
+        TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32, -1, s));
+      }
 
       if (chunks > 0)
         TCL_LAUNCH(T, "scan_chunked", launch_scan_chunked<uint16_t>(B, E, N, R, chunks, offs, u, xdbl,

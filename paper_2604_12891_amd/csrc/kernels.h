@@ -98,6 +98,26 @@ struct ConvIn {
   float* u = nullptr;         // [rows, K]
 };
 bool gemm_split_conv_supports(const GemmArgs& a, const ConvIn& cv, int d_conv);
+
+// The same fusion for bf16 models: x and u bf16, W bf16 [N][ldw] (the
+// model's bf16 x_proj weights), C fp32 [rows, ldc]. Kernel size 4, E a
+// multiple of 128 and <= 512, N <= 64.
+struct ConvArgsBF16 {
+  const uint16_t* x = nullptr;  // conv input [rows, ldx] (the x half of in_proj's output)
+  int64_t ldx = 0;
+  const float* w = nullptr;     // [E, 4]
+  const float* b = nullptr;     // [E]
+  const uint8_t* tpos = nullptr;
+  uint16_t* u = nullptr;        // [rows, E]
+  const uint16_t* W = nullptr;
+  int64_t ldw = 0;
+  float* C = nullptr;
+  int64_t ldc = 0;
+  const int* Mdev = nullptr;
+  int Mmax = 0, N = 0, E = 0;
+};
+bool gemm_bf16_conv_supports(const ConvArgsBF16& a, int d_conv);
+hipError_t launch_gemm_bf16_conv(const ConvArgsBF16& a, hipStream_t s);
 hipError_t launch_gemm_split_conv(const GemmArgs& a, const ConvIn& cv, const uint16_t* Ws, int ldws,
                                   hipStream_t s);
 
