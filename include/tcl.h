@@ -486,6 +486,15 @@ TCL_API tcl_status tcl_test_xproj_conv_f32(int32_t B, int32_t rows, int32_t E, i
                                            uint16_t* d_Wsplit, uint8_t* d_tpos, float* d_u,
                                            float* d_xdbl, void* stream);
 
+/* The same for bf16 activations (the bf16 models' fused kernel): d_x [rows,
+ * ldx] and d_u [rows, E] bf16, d_W [N, E] bf16 (E a multiple of 128, <= 512;
+ * 1 <= N <= 64; ldx a multiple of 8), d_xdbl fp32; bf16 MFMA products
+ * accumulated in fp32. d_tpos: caller-owned scratch of rows bytes. */
+TCL_API tcl_status tcl_test_xproj_conv_bf16(int32_t B, int32_t rows, int32_t E, int32_t N,
+                                            const int32_t* d_offs, const uint16_t* d_x, int32_t ldx,
+                                            const float* d_w, const float* d_b, const uint16_t* d_W,
+                                            uint8_t* d_tpos, uint16_t* d_u, float* d_xdbl, void* stream);
+
 /* Selective scan with its dt_proj + softplus prologue and gate epilogue,
  * fp32: out = (scan(u, softplus(dt_r W_dt^T + b_dt), -exp(A_log), B, C) +
  * D u) * SiLU(z), with [dt_r|B|C] = d_xdbl rows of R + 2N values and z read

@@ -89,6 +89,8 @@ _SIGS = {
     "tcl_test_conv_silu_f32": (_i32, [_i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp]),
     "tcl_test_xproj_conv_f32": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _vp, _vp]),
+    "tcl_test_xproj_conv_bf16": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                        _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                  _vp, _vp, _vp]),
 }
@@ -496,6 +498,24 @@ def xproj_conv_f32(offs, x, w, b, W, rows, E, ldx=None, stream=None):
                                         x.shape[1] if ldx is None else ldx, w.data_ptr(), b.data_ptr(),
                                         W.data_ptr(), wsplit.data_ptr(), tpos.data_ptr(), u.data_ptr(),
                                         xdbl.data_ptr(), _stream(stream)))
+    return u, xdbl
+
+
+def xproj_conv_bf16(offs, x, w, b, W, rows, E, ldx=None, stream=None):
+    """The bf16 fused conv + SiLU + x_proj kernel (tcl_test_xproj_conv_bf16):
+    x torch.bfloat16 [rows, ldx], W torch.bfloat16 [N, E]; returns (u bf16
+    [rows, E], xdbl fp32 [rows, N]); rows past offs[B] are left as they were
+    (u zero, xdbl NaN)."""
+    import torch
+    B = offs.numel() - 1
+    N = W.shape[0]
+    u = torch.zeros((rows, E), dtype=torch.bfloat16, device=x.device)
+    xdbl = torch.full((rows, N), float("nan"), dtype=torch.float32, device=x.device)
+    tpos = torch.empty(rows, dtype=torch.uint8, device=x.device)
+    check(lib().tcl_test_xproj_conv_bf16(B, rows, E, N, offs.data_ptr(), x.data_ptr(),
+                                         x.shape[1] if ldx is None else ldx, w.data_ptr(), b.data_ptr(),
+                                         W.data_ptr(), tpos.data_ptr(), u.data_ptr(), xdbl.data_ptr(),
+                                         _stream(stream)))
     return u, xdbl
 
 

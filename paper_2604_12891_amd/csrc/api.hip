@@ -925,6 +925,24 @@ TCL_API tcl_status tcl_test_xproj_conv_f32(int32_t B, int32_t rows, int32_t E, i
   return TCL_OK;
 }
 
+TCL_API tcl_status tcl_test_xproj_conv_bf16(int32_t B, int32_t rows, int32_t E, int32_t N,
+                                            const int32_t* d_offs, const uint16_t* d_x, int32_t ldx,
+                                            const float* d_w, const float* d_b, const uint16_t* d_W,
+                                            uint8_t* d_tpos, uint16_t* d_u, float* d_xdbl, void* stream) {
+  if (B <= 0 || rows <= 0 || E <= 0 || N <= 0 || ldx < E) return fail(TCL_ERR_INVALID_ARG, "bad sizes");
+  if (!d_offs || !d_x || !d_w || !d_b || !d_W || !d_tpos || !d_u || !d_xdbl)
+    return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  ConvArgsBF16 a;
+  a.x = d_x; a.ldx = ldx; a.w = d_w; a.b = d_b; a.tpos = d_tpos; a.u = d_u; a.W = d_W; a.ldw = E;
+  a.C = d_xdbl; a.ldc = N; a.Mdev = d_offs + B; a.Mmax = rows; a.N = N; a.E = E;
+  if (!gemm_bf16_conv_supports(a, 4))
+    return fail(TCL_ERR_UNSUPPORTED, "shape or alignment not supported by the fused bf16 conv + x_proj kernel");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  TCL_HIP(launch_token_pos(d_offs, B, d_tpos, s));
+  TCL_HIP(launch_gemm_bf16_conv(a, s));
+  return TCL_OK;
+}
+
 TCL_API tcl_status tcl_test_scan_f32(int32_t B, int32_t E, int32_t N, int32_t R, int32_t chunks,
                                      const int32_t* d_offs, const float* d_u, const float* d_xdbl,
                                      const float* d_z, int32_t ldz, const float* d_W_dt,

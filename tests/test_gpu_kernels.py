@@ -337,6 +337,45 @@ def test_xproj_conv_f32(E, N):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+@pytest.mark.parametrize("E,N", [(512, 48), (128, 20), (256, 64)])
+def test_xproj_conv_bf16(E, N):
+    """The bf16 fused kernel: u (bf16) within the conv bound of the oracle's
+    conv plus one bf16 rounding, and xdbl = u W^T from the kernel's own bf16
+    u within the fp32 accumulation bound (bf16 products are exact); program
+    edges around wavefront and panel boundaries, an empty program, a ragged
+    last panel."""
+    rng = np.random.default_rng(E + 3 * N)
+    L = 40
+    lengths = np.concatenate([[1, 2, 3, 4, 0, 40, 31, 33, 1, 1, 1, 29, 3], rng.integers(1, L + 1, 60)])
+    lengths = lengths.astype(np.int32)
+    B = len(lengths)
+    M = int(lengths.sum())
+    rows = M + 77
+    ldx = 2 * E
+    print(f"xproj_conv_bf16 E={E} N={N} B={B} M={M}", flush=True)
+    xp = torch.from_numpy(rng.standard_normal((rows, ldx)).astype(np.float32)).to(torch.bfloat16)
+    w = rng.uniform(-0.5, 0.5, (E, 4)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, E).astype(np.float32)
+    W = torch.from_numpy((rng.uniform(-1, 1, (N, E)) / np.sqrt(E)).astype(np.float32)).to(torch.bfloat16)
+    offs = _dev(_offs(lengths), torch.int32)
+    u, xdbl = tb.xproj_conv_bf16(offs, xp.cuda(), _dev(w), _dev(b), W.cuda(), rows, E, ldx=ldx)
+    torch.cuda.synchronize()
+    u = u.float().cpu().numpy().astype(np.float64)
+    xdbl = xdbl.cpu().numpy()
+    assert np.all(np.isnan(xdbl[M:])) and np.all(u[M:] == 0)
+    xf = xp.float().numpy().astype(np.float64)[:M, :E]
+    xr = _unpack(xf, lengths, L)
+    wf, bf = w.astype(np.float64), b.astype(np.float64)
+    expect = _pack(om.silu(om.causal_conv1d(xr, wf, bf)), lengths)
+    scale = np.abs(bf) + _pack(om.causal_conv1d(np.abs(xr), np.abs(wf), 0 * bf), lengths)
+    np.testing.assert_array_less(np.abs(u[:M] - expect), 1e-5 * scale + 2.0 ** -8 * np.abs(expect) + 1e-7)
+    W64 = W.float().numpy().astype(np.float64)
+    ref = u[:M] @ W64.T
+    bound = (E + 2) * U * (np.abs(u[:M]) @ np.abs(W64).T)
+    err = np.abs(xdbl[:M] - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
 def test_xproj_conv_rejects_unsupported():
     offs = _dev(_offs(np.array([3, 2], np.int32)), torch.int32)
     for E, N in [(96, 48), (576, 48), (128, 65)]:
