@@ -68,3 +68,19 @@ def oracle_cfg(shape) -> dict:
 
 def oracle_scores(blob, X, lengths, shape) -> np.ndarray:
     return om.score(blob, X, lengths, oracle_cfg(shape))
+
+
+def golden_scores(name: str, blob, X, lengths) -> np.ndarray:
+    """The fp64 oracle's scores of every program of a named workload, as
+    written by tests/golden/make_golden.py; fails if the stored digest does
+    not match the inputs being scored."""
+    import os
+
+    from tests.golden import make_golden as mg
+
+    path = mg.path(name)
+    assert os.path.exists(path), f"missing golden scores {path}: run python -m tests.golden.make_golden {name}"
+    with np.load(path, allow_pickle=False) as z:
+        scores, sha = z["scores"], str(z["sha256"])
+    assert sha == mg.digest(blob, X, lengths), f"{name}: inputs differ from those the golden scores were made from"
+    return scores

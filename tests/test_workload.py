@@ -2,6 +2,7 @@
 import math
 
 import numpy as np
+import pytest
 import scipy.stats
 
 from paper_2604_12891_amd import workload as wl
@@ -51,3 +52,21 @@ def test_distill_workload_pair():
     (t, s), X, lengths = wl.make_workload("distill_B1024_L25_t256_s128_bf16", B=8)
     assert t.size == wl.param_count(wl.D256) and s.size == wl.param_count(wl.STUDENT)
     assert np.all((s.view(np.uint32) & 0xFFFF) == 0)
+
+
+@pytest.mark.parametrize("name", ["score_B4096_L25_d256_f32", "score_B65536_L25_d256_bf16",
+                                  "score_B8192_L256_d256_f32"])
+def test_golden_scores_are_the_oracles(name):
+    """The stored full-batch scores were written from today's generator
+    (digest) and are the oracle's: a seeded sample of programs, including
+    the first and the last, rescored by the oracle here agrees to rounding."""
+    from oracle import model as om
+    from tests.parity import golden_scores, oracle_cfg
+
+    w = wl.WORKLOADS[name]
+    blob, X, lengths = wl.make_workload(name)
+    g = golden_scores(name, blob, X, lengths)
+    assert g.shape == (w.B,) and np.all(np.isfinite(g))
+    idx = np.unique(np.concatenate([[0, w.B - 1], np.random.default_rng(7).choice(w.B, 6, replace=False)]))
+    o = om.score(blob, X[idx], lengths[idx], oracle_cfg(w.model))
+    np.testing.assert_allclose(g[idx], o, rtol=1e-12, atol=1e-14)
