@@ -106,3 +106,47 @@ def rdu_select(scores, op, n_ops, initial, n_select):
         else:
             dropped.add(T)
     return out
+
+
+def rdu_select_pool(scores, op, n_ops, initial, n_select, elems=1 << 22):
+    """rdu_select for dataset-sized pools: the same selection loop, with
+    Eq. (1)-(3) evaluated for a block of candidates at a time against the
+    whole labeled set (the same per-candidate formulas as rdu_scores, as
+    numpy array expressions over [candidates, labeled] blocks of about
+    `elems` entries instead of a Python loop over candidates). Equal t_s
+    keep the lower index, across blocks too."""
+    f = normalise(scores)
+    op = np.asarray(op)
+    N = len(f)
+    budget = budgets(op, n_ops, n_select)
+    is_cand = np.ones(N, dtype=bool)
+    labeled = set(int(i) for i in initial)
+    is_cand[np.asarray(sorted(labeled), dtype=np.int64)] = False
+    selected = np.zeros(n_ops, dtype=np.int64)
+    out = []
+    while len(out) < n_select:
+        cand = np.nonzero(is_cand)[0]
+        if cand.size == 0:
+            break
+        fl = f[np.asarray(sorted(labeled), dtype=np.int64)]
+        M = len(fl)
+        step = max(1, elems // max(M, 1))
+        best_t, T = -np.inf, -1
+        for c0 in range(0, cand.size, step):
+            ci = cand[c0:c0 + step]
+            fi = f[ci]
+            d = np.min(np.abs(fi[:, None] - fl[None, :]), axis=1)             # Eq. (1)
+            mu = (fi + np.sum(fl)) / (M + 1)                                    # Eq. (2)
+            u = ((fi - mu) ** 2 + np.sum((fl[None, :] - mu[:, None]) ** 2, axis=1)) / (M + 1)  # Eq. (3)
+            t = fi * d + u
+            k = int(np.argmax(t))
+            if t[k] > best_t:
+                best_t, T = t[k], int(ci[k])
+        if selected[op[T]] < budget[op[T]]:
+            labeled.add(T)
+            is_cand[T] = False
+            selected[op[T]] += 1
+            out.append(T)
+        else:
+            is_cand[T] = False
+    return out

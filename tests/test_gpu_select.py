@@ -101,3 +101,34 @@ def test_rdu_select_budgets_bind_and_pool_runs_out():
     _check_rdu(s, op, 4, init, 50)
     small_s, small_op = s[:20].copy(), np.zeros(20, np.int32)
     _check_rdu(small_s, small_op, 1, np.array([3, 7], np.int32), 30)
+
+
+def _check_rdu_pool(s, op, n_ops, init, n_select):
+    sel, cnt = _tb().rdu_select(_dev(s, torch.float32), _dev(op, torch.int32), n_ops, _dev(init, torch.int32),
+                                n_select)
+    torch.cuda.synchronize()
+    got = sel.cpu().numpy().tolist()
+    c = int(cnt.cpu().numpy()[0])
+    ref = osel.rdu_select_pool(s.astype(np.float64), op, n_ops, init, n_select)
+    assert c == len(ref) and got[:c] == ref, (got[:c], ref)
+
+
+def test_rdu_select_grid_stride_pool():
+    """A pool of 1.2 M programs: more candidates than one pass of the
+    selection grid covers (1024 blocks x 256 threads x 4), so every kernel's
+    grid-stride loop runs more than once; 20 operator types, 64 initial
+    programs, 6 selections, against the oracle's blocked form."""
+    N, n_ops, n_init, n_sel = 1_200_000, 20, 64, 6
+    assert N > 1024 * 256 * 4
+    print(f"rdu pool N={N} init={n_init} select={n_sel}", flush=True)
+    s, op, init = _rdu_case(N, n_ops, n_init, 77)
+    _check_rdu_pool(s, op, n_ops, init, n_sel)
+
+
+def test_rdu_select_large_initial_set():
+    """More initial labeled programs (8,500) than the sorted-set path holds
+    (8,192): the distances to the initial set come from the direct pass."""
+    N, n_ops, n_init, n_sel = 60_000, 8, 8_500, 3
+    print(f"rdu N={N} init={n_init} select={n_sel}", flush=True)
+    s, op, init = _rdu_case(N, n_ops, n_init, 78)
+    _check_rdu_pool(s, op, n_ops, init, n_sel)

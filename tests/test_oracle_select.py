@@ -103,3 +103,30 @@ def test_rdu_select_invariants():
         cand = [i for i in range(N) if i not in lab]
         assert k == cand[int(np.argmax(osel.rdu_scores(f, lab, cand)))]
         lab.add(k)
+
+
+@pytest.mark.parametrize("N,n_ops,n_init,n_select,seed", [(300, 4, 10, 40, 1), (120, 3, 60, 30, 2),
+                                                          (500, 1, 1, 20, 3), (400, 6, 5, 60, 4)])
+def test_rdu_select_pool_equals_rdu_select(N, n_ops, n_init, n_select, seed):
+    """The blocked form for large pools selects exactly what the per-candidate
+    loop selects, with small blocks so that the argmax crosses blocks (and
+    budgets bind on the skewed pools)."""
+    rng = np.random.default_rng(seed)
+    s = 0.3 * rng.standard_normal(N)
+    p = rng.random(n_ops) + 0.05
+    op = rng.choice(n_ops, N, p=p / p.sum())
+    init = rng.choice(N, n_init, replace=False)
+    ref = osel.rdu_select(s, op, n_ops, init, n_select)
+    for elems in (1 << 22, 7 * max(n_init, 1), 1):
+        assert osel.rdu_select_pool(s, op, n_ops, init, n_select, elems=elems) == ref
+
+
+def test_rdu_select_pool_ties_take_the_lower_index():
+    """Candidates with identical scores tie in t_s: the lower index wins,
+    also when the tie spans two blocks."""
+    s = np.array([0.0, 1.0, 0.5, 1.0, 1.0, 0.2])
+    op = np.zeros(6, dtype=np.int64)
+    for elems in (1 << 22, 1, 2):
+        sel = osel.rdu_select_pool(s, op, 1, [0], 3, elems=elems)
+        assert sel == osel.rdu_select(s, op, 1, [0], 3)
+        assert sel[0] == 1
