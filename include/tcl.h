@@ -256,6 +256,9 @@ typedef struct tcl_kd_loss {
                                 layout (device); may be NULL when ewc_lambda == 0     */
   const float* d_theta_prev; /* [n_params] the student's parameters after the
                                 previous platform (device); likewise                  */
+  const float* d_phi;        /* optional device pointer to this batch's gate (e.g. an
+                                entry of tcl_teacher_gate's output); when non-NULL it
+                                replaces `phi` (read on the device, no host sync)     */
 } tcl_kd_loss;
 
 /* One distillation step on the Eq. (9) objective: as tcl_distill_step in
@@ -278,6 +281,34 @@ TCL_API size_t tcl_lambdarank_workspace_bytes(int32_t B);
 TCL_API tcl_status tcl_lambdarank(int32_t B, const float* d_scores, const float* d_labels, float sigma,
                                   float* d_loss, float* d_grad, void* d_workspace, size_t ws_bytes,
                                   void* stream);
+
+/* The teacher-loss gate of section 6, Eq. (10)-(11): the teacher's
+ * LambdaRank loss e_j of every batch j (Eq. (11), e.g. tcl_lambdarank of the
+ * teacher's scores against the ground truth, one call per batch writing
+ * d_e + j) turned into per-batch weights
+ *   phi_j = 1 - (e_j - min_k e_k) / (max_k e_k - min_k e_k),
+ * so the batch the teacher ranks best gets 1 and the worst 0; all ones when
+ * every e_j is equal.
+ *   d_e [n] fp32 (device, finite), d_phi [n] fp32 output (device; may not
+ *   alias d_e). The normalisation runs in fp64 (each phi_j is the fp32
+ *   rounding of the value from the fp32 inputs). One workgroup;
+ *   stream-ordered; no workspace. */
+TCL_API tcl_status tcl_teacher_gate(int32_t n, const float* d_e, float* d_phi, void* stream);
+
+/* Test entry: tcl_distill_step_kd with two additions for parity tests of
+ * the ranking objective. d_rank_keys [B] (device, may be NULL): the values
+ * the positions D_i of Eq. (6) are counted from (descending, equal keys in
+ * index order) in place of the student's own scores, so that a test can
+ * give the library and a reference the same ranking where the student's
+ * scores are within rounding of each other (each ordering of such scores
+ * is a correct result); with NULL it is the product step. d_scores_out [2B]
+ * (device, may be NULL) receives the step's student scores, then the
+ * teacher's. Everything else as tcl_distill_step_kd. */
+TCL_API tcl_status tcl_test_distill_step_kd_ranked(tcl_trainer* trainer, int32_t B, int32_t L,
+                                                   const float* d_feats, const int32_t* d_lengths,
+                                                   const float* d_labels, const tcl_kd_loss* kd,
+                                                   const float* d_rank_keys, float* d_scores_out, float* d_loss,
+                                                   void* d_workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------
  * Progressive KB + AC forward (section 6, Fig. 6, Eq. (7)): in the CKD

@@ -40,7 +40,8 @@ class Config(ctypes.Structure):
 class KDLoss(ctypes.Structure):
     """tcl_kd_loss: the Eq. (9) distillation objective."""
     _fields_ = [("beta", ctypes.c_float), ("phi", ctypes.c_float), ("sigma", ctypes.c_float),
-                ("ewc_lambda", ctypes.c_float), ("d_fisher", ctypes.c_void_p), ("d_theta_prev", ctypes.c_void_p)]
+                ("ewc_lambda", ctypes.c_float), ("d_fisher", ctypes.c_void_p), ("d_theta_prev", ctypes.c_void_p),
+                ("d_phi", ctypes.c_void_p)]
 
 
 _vp, _i32, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
@@ -67,6 +68,9 @@ _SIGS = {
     "tcl_trainer_get_grads": (_i32, [_vp, _vp, _sz]),
     "tcl_distill_step_kd": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, ctypes.POINTER(KDLoss), _vp, _vp, _sz, _vp]),
     "tcl_lambdarank_workspace_bytes": (_sz, [_i32]),
+    "tcl_teacher_gate": (_i32, [_i32, _vp, _vp, _vp]),
+    "tcl_test_distill_step_kd_ranked": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, ctypes.POINTER(KDLoss), _vp, _vp,
+                                               _vp, _vp, _sz, _vp]),
     "tcl_topk": (_i32, [_i32, _vp, _vp, _i32, _vp, _vp]),
     "tcl_lateral_param_count": (_sz, [ctypes.POINTER(Config), _i32]),
     "tcl_lateral_create": (_i32, [_vp, _vp, _i32, _vp, _sz, ctypes.POINTER(_vp)]),
@@ -320,19 +324,29 @@ class Trainer:
         return loss
 
     def step_kd(self, feats, lengths, labels, beta=0.5, phi=1.0, sigma=1.0, ewc_lambda=0.0, fisher=None,
-                theta_prev=None, loss=None, workspace=None, stream=None):
+                theta_prev=None, loss=None, workspace=None, stream=None, phi_dev=None, rank_keys=None,
+                scores_out=None):
         """One step on the Eq. (9) objective (tcl_distill_step_kd); fisher and
-        theta_prev are device fp32 tensors of the parameter count. Returns the
-        device tensor [total, rank(s; teacher), rank(s; label), ewc]."""
+        theta_prev are device fp32 tensors of the parameter count; phi_dev
+        (a device fp32 tensor of one element, optional) replaces phi. Returns
+        the device tensor [total, rank(s; teacher), rank(s; label), ewc].
+        rank_keys / scores_out (device fp32 [B] / [2B]) go through the test
+        entry tcl_test_distill_step_kd_ranked."""
         import torch
         B, L, _ = feats.shape
         if loss is None:
             loss = torch.empty(4, dtype=torch.float32, device=feats.device)
         ws = self.workspace(B, L) if workspace is None else workspace
-        kd = KDLoss(beta, phi, sigma, ewc_lambda, _ptr(fisher), _ptr(theta_prev))
-        check(lib().tcl_distill_step_kd(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), labels.data_ptr(),
-                                        ctypes.byref(kd), loss.data_ptr(), ws.data_ptr(),
-                                        ws.numel() * ws.element_size(), _stream(stream)))
+        kd = KDLoss(beta, phi, sigma, ewc_lambda, _ptr(fisher), _ptr(theta_prev), _ptr(phi_dev))
+        if rank_keys is None and scores_out is None:
+            check(lib().tcl_distill_step_kd(self._h, B, L, feats.data_ptr(), lengths.data_ptr(),
+                                            labels.data_ptr(), ctypes.byref(kd), loss.data_ptr(), ws.data_ptr(),
+                                            ws.numel() * ws.element_size(), _stream(stream)))
+        else:
+            check(lib().tcl_test_distill_step_kd_ranked(
+                self._h, B, L, feats.data_ptr(), lengths.data_ptr(), labels.data_ptr(), ctypes.byref(kd),
+                _ptr(rank_keys), _ptr(scores_out), loss.data_ptr(), ws.data_ptr(), ws.numel() * ws.element_size(),
+                _stream(stream)))
         return loss
 
     def grads(self) -> np.ndarray:
@@ -421,6 +435,16 @@ def lambdarank(scores, labels, sigma=1.0, grad=True, stream=None):
     check(lib().tcl_lambdarank(B, scores.data_ptr(), labels.data_ptr(), sigma, loss.data_ptr(), _ptr(g),
                                ws.data_ptr(), ws.numel(), _stream(stream)))
     return loss, g
+
+
+def teacher_gate(e, out=None, stream=None):
+    """The teacher-loss gate of Eq. (10)-(11) (tcl_teacher_gate) over device
+    fp32 batch losses e [n]; returns phi [n] (device)."""
+    import torch
+    if out is None:
+        out = torch.empty_like(e)
+    check(lib().tcl_teacher_gate(e.numel(), e.data_ptr(), out.data_ptr(), _stream(stream)))
+    return out
 
 
 def gemm_split(A, W, bias=None, out=None, stream=None, variant=-1, epilogue=0, offs=None):

@@ -1,6 +1,6 @@
 """Build libtcl.so (the HIP kernels + C ABI) for gfx950 with hipcc, in-tree.
 
-    python -m paper_2604_12891_amd.build
+    python -m paper_2604_12891_amd.build [--incremental] [-v]
 
 Objects go to paper_2604_12891_amd/_build/, the library to
 paper_2604_12891_amd/libtcl.so. Always recompiles.
@@ -33,13 +33,25 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
+def _stale(src: str, obj: str) -> bool:
+    """An object is stale if it is missing or older than its source or any
+    header it may include."""
+    if not os.path.exists(obj):
+        return True
+    deps = [src] + glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(ROOT, "include", "*.h"))
+    return max(os.path.getmtime(d) for d in deps) > os.path.getmtime(obj)
+
+
+def build(verbose: bool = False, incremental: bool = False) -> str:
+    """Compile every source (incremental=True: only stale objects) and link."""
     os.makedirs(BUILD, exist_ok=True)
     procs = []
     objs = []
     for src in sources():
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
         objs.append(obj)
+        if incremental and not _stale(src, obj):
+            continue
         cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
@@ -64,4 +76,4 @@ def build(verbose: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, incremental="--incremental" in sys.argv))

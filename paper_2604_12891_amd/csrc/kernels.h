@@ -309,10 +309,17 @@ hipError_t launch_loss_head_bwd(int B, int d, int h, const float* s, const float
 // against l0 and l1 weighted w0, w1 (nsets == 2). ds [B] (may be null)
 // receives d/ds of (w0 L(s; l0) + w1 L(s; l1)) (nsets == 1: of L(s; l0));
 // out receives {L} (nsets == 1) or {w0 L0 + w1 L1, L1, L0}. ws: a scratch
-// of rank_workspace_floats(B, nsets) floats.
+// of rank_workspace_floats(B, nsets) floats. key [B] (may be null: s) holds
+// the values the score ranks D_i are counted from (descending, equal keys
+// in index order); w1_scale (may be null: 1) is a device value that
+// multiplies w1 (the teacher gate of the batch).
 size_t rank_workspace_floats(int B, int nsets);
 hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, const float* l1, float sigma,
-                             float w0, float w1, float* ws, float* ds, float* out, hipStream_t st);
+                             float w0, float w1, float* ws, float* ds, float* out, hipStream_t st,
+                             const float* key = nullptr, const float* w1_scale = nullptr);
+// The teacher-loss gate of Eq. (10)-(11): phi[j] = 1 - (e[j] - min e) /
+// (max e - min e) over n batch losses (all ones when they are equal).
+hipError_t launch_teacher_gate(int n, const float* e, float* phi, hipStream_t st);
 // ---------------------------------------------------------------- score consumers
 // Per-segment top-K: out [n_seg][K] global indices of each segment's K best
 // scores (best first, equal scores in index order, NaN last), -1 past a

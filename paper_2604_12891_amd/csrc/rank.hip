@@ -1,6 +1,7 @@
 // The ranking objectives: LambdaRank (section 5.3, Eq. (6)) on a batch of
-// scores against one or two label sets, and the EWC penalty of the
-// distillation objective (section 6, Eq. (9)).
+// scores against one or two label sets, the teacher-loss gate (Eq. (10)-
+// (11)) and the EWC penalty of the distillation objective (section 6,
+// Eq. (9)).
 //
 // LambdaRank, per label set:
 //   L = sum over pairs with rel_i > rel_j of
@@ -122,6 +123,7 @@ __global__ __launch_bounds__(kRT) void rank_prep_kernel(int B, const float* __re
 // grid (i blocks, j tiles); part_ds [tiles][B], part_loss [tiles][i blocks][NS]
 template <int NS>
 __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, float w0, float w1,
+                                                        const float* __restrict__ w1_scale,
                                                         const float* __restrict__ s,
                                                         const float* __restrict__ rel,
                                                         const float* __restrict__ gain,
@@ -188,6 +190,7 @@ __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, floa
   }
   // loss in bits (log2), gradient scaled by sigma / ln 2
   const float c = sigma * kInvLn2;
+  if (w1_scale) w1 *= w1_scale[0];
   if (ok) part_ds[(int64_t)blockIdx.y * B + i] = w0 * grad[0] * c + (NS > 1 ? w1 * grad[NS - 1] * c : 0.f);
 #pragma unroll
   for (int k = 0; k < NS; ++k) {
@@ -199,6 +202,7 @@ __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, floa
 // ds[i] = sum over j tiles; out: NS == 1: {L}; NS == 2: {w0 L0 + w1 L1, L1, L0}
 template <int NS>
 __global__ __launch_bounds__(kRT) void rank_finish_kernel(int B, int tiles, int iblocks, float w0, float w1,
+                                                          const float* __restrict__ w1_scale,
                                                           const float* __restrict__ part_ds,
                                                           const float* __restrict__ part_loss,
                                                           float* __restrict__ ds, float* __restrict__ out) {
@@ -218,6 +222,7 @@ __global__ __launch_bounds__(kRT) void rank_finish_kernel(int B, int tiles, int 
     if (NS == 1) {
       out[0] = L[0];
     } else {
+      if (w1_scale) w1 *= w1_scale[0];
       out[0] = w0 * L[0] + w1 * L[NS - 1];
       out[1] = L[NS - 1];
       out[2] = L[0];
@@ -259,6 +264,26 @@ __global__ void ewc_off_kernel(float* __restrict__ loss) {
   if (threadIdx.x == 0) loss[3] = 0.f;
 }
 
+// The teacher-loss gate (Eq. (10)-(11)): phi_j = 1 - (e_j - min e) /
+// (max e - min e) over every batch j, one workgroup striding over the n
+// losses (a few thousand batches per dataset: latency-bound either way).
+// The normalisation runs in fp64 so that each phi_j is the fp32 rounding of
+// the exact value; equal losses (max = min) give phi = 1 everywhere.
+__global__ __launch_bounds__(kRT) void teacher_gate_kernel(int n, const float* __restrict__ e,
+                                                           float* __restrict__ phi) {
+  __shared__ float red[kRT / 64];
+  float mn = INFINITY, mx = -INFINITY;
+  for (int j = threadIdx.x; j < n; j += kRT) {
+    mn = fminf(mn, e[j]);
+    mx = fmaxf(mx, e[j]);
+  }
+  const float lo = block_min(mn, red);
+  const float hi = block_max(mx, red);
+  const double range = (double)hi - (double)lo;
+  for (int j = threadIdx.x; j < n; j += kRT)
+    phi[j] = range > 0.0 ? (float)(1.0 - ((double)e[j] - (double)lo) / range) : 1.0f;
+}
+
 }  // namespace
 
 size_t rank_workspace_floats(int B, int nsets) {
@@ -268,7 +293,8 @@ size_t rank_workspace_floats(int B, int nsets) {
 }
 
 hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, const float* l1, float sigma,
-                             float w0, float w1, float* ws, float* ds, float* out, hipStream_t st) {
+                             float w0, float w1, float* ws, float* ds, float* out, hipStream_t st,
+                             const float* key, const float* w1_scale) {
   if (B <= 0 || (nsets != 1 && nsets != 2) || (nsets == 2 && !l1)) return hipErrorInvalidValue;
   const int tiles = (B + kRT - 1) / kRT;
   float* rel = ws;
@@ -279,19 +305,26 @@ hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, 
   float* part_ds = dsw + B;
   float* part_loss = part_ds + (size_t)tiles * B;
   float* dsout = ds ? ds : dsw;
+  const float* rk = key ? key : s;  // what the score ranks D_i are counted from
   if (nsets == 1) {
-    hipLaunchKernelGGL(rank_prep_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, s, l0, l0, rel, gain, dcg, invD);
-    hipLaunchKernelGGL(rank_pair_kernel<1>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, s, rel, gain,
-                       dcg, invD, part_ds, part_loss);
-    hipLaunchKernelGGL(rank_finish_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, part_ds,
-                       part_loss, dsout, out);
+    hipLaunchKernelGGL(rank_prep_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, rk, l0, l0, rel, gain, dcg, invD);
+    hipLaunchKernelGGL(rank_pair_kernel<1>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, w1_scale, s,
+                       rel, gain, dcg, invD, part_ds, part_loss);
+    hipLaunchKernelGGL(rank_finish_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, w1_scale,
+                       part_ds, part_loss, dsout, out);
   } else {
-    hipLaunchKernelGGL(rank_prep_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, s, l0, l1, rel, gain, dcg, invD);
-    hipLaunchKernelGGL(rank_pair_kernel<2>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, s, rel, gain,
-                       dcg, invD, part_ds, part_loss);
-    hipLaunchKernelGGL(rank_finish_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, part_ds,
-                       part_loss, dsout, out);
+    hipLaunchKernelGGL(rank_prep_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, rk, l0, l1, rel, gain, dcg, invD);
+    hipLaunchKernelGGL(rank_pair_kernel<2>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, w1_scale, s,
+                       rel, gain, dcg, invD, part_ds, part_loss);
+    hipLaunchKernelGGL(rank_finish_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, w1_scale,
+                       part_ds, part_loss, dsout, out);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_teacher_gate(int n, const float* e, float* phi, hipStream_t st) {
+  if (n <= 0 || !e || !phi) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(teacher_gate_kernel, dim3(1), dim3(kRT), 0, st, n, e, phi);
   return hipGetLastError();
 }
 

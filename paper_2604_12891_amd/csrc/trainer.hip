@@ -270,9 +270,13 @@ namespace {
 
 // One step on either objective: kd == NULL is the two-MSE loss, else the
 // ranking objective of Eq. (9).
+// rank_keys (may be null): what the student's score ranks are counted from
+// instead of its own scores; scores_out (may be null): [2B] receives the
+// student's then the teacher's scores of the step.
 tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats, const int32_t* d_lengths,
                         const float* d_labels, const tcl_kd_loss* kd, float* d_loss, void* d_ws,
-                        size_t ws_bytes, void* stream) {
+                        size_t ws_bytes, void* stream, const float* rank_keys = nullptr,
+                        float* scores_out = nullptr) {
   if (!tr) return fail(TCL_ERR_INVALID_ARG, "trainer is NULL");
   if (B <= 0 || L <= 0 || B > tr->max_B || L > tr->max_L)
     return fail(TCL_ERR_INVALID_ARG, "B=%d L=%d outside [1, max_B=%d] x [1, max_L=%d]", B, L,
@@ -353,9 +357,12 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   if (fork) TCL_HIP(hipStreamWaitEvent(s, Tm->ev[1], 0));
   if (kd) {
     // beta L(s; labels) + (1 - beta) phi L(s; teacher): dL/ds and the loss
+    // the gate phi is a host value, or a device value (e.g. an entry of
+    // tcl_teacher_gate's output) that scales (1 - beta) inside the kernels
+    const float w1 = kd->d_phi ? 1.0f - kd->beta : (1.0f - kd->beta) * kd->phi;
     TCL_LAUNCH(T, "lambdarank", launch_lambdarank(B, 2, F32(P.s_scores), d_labels, F32(P.t_scores), kd->sigma,
-                                                  kd->beta, (1.0f - kd->beta) * kd->phi, F32(P.rank_ws),
-                                                  F32(P.ds), F32(P.rloss), s));
+                                                  kd->beta, w1, F32(P.rank_ws), F32(P.ds), F32(P.rloss), s,
+                                                  rank_keys, kd->d_phi));
   }
   TCL_LAUNCH(T, "loss_head_bwd", launch_loss_head_bwd(B, d, h, F32(P.s_scores), F32(P.t_scores), d_labels,
                                                       F32(P.a1), S->W1, S->W2, F32(P.da1),
@@ -441,6 +448,11 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   }
   TCL_LAUNCH(T, "colsum", launch_colsum(Mdev, Mmax, F32(P.dH), d, d, P.cs, F32(P.p_b0), s));
 
+  if (scores_out) {
+    TCL_HIP(hipMemcpyAsync(scores_out, F32(P.s_scores), (size_t)B * 4, hipMemcpyDeviceToDevice, s));
+    TCL_HIP(hipMemcpyAsync(scores_out + B, F32(P.t_scores), (size_t)B * 4, hipMemcpyDeviceToDevice, s));
+  }
+
   // 5. reduce partials, Adam, refresh the compute layouts
   TCL_LAUNCH(T, "reduce", launch_reduce(tr->d_jobs, tr->njobs, tr->max_n, reinterpret_cast<float*>(ws),
                                         tr->grad, d_loss, s));
@@ -464,16 +476,44 @@ TCL_API tcl_status tcl_distill_step(tcl_trainer* tr, int32_t B, int32_t L, const
   return distill_step(tr, B, L, d_feats, d_lengths, d_labels, nullptr, d_loss, d_ws, ws_bytes, stream);
 }
 
-TCL_API tcl_status tcl_distill_step_kd(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats,
-                                       const int32_t* d_lengths, const float* d_labels, const tcl_kd_loss* kd,
-                                       float* d_loss, void* d_ws, size_t ws_bytes, void* stream) {
+namespace {
+
+tcl_status check_kd(const tcl_kd_loss* kd) {
   if (!kd) return fail(TCL_ERR_INVALID_ARG, "kd is NULL");
   if (!(kd->beta >= 0.f && kd->beta <= 1.f) || !(kd->phi >= 0.f && kd->phi <= 1.f) || !(kd->sigma > 0.f) ||
       !(kd->ewc_lambda >= 0.f))
     return fail(TCL_ERR_INVALID_ARG, "kd needs beta, phi in [0, 1], sigma > 0, ewc_lambda >= 0");
   if (kd->ewc_lambda > 0.f && (!kd->d_fisher || !kd->d_theta_prev))
     return fail(TCL_ERR_INVALID_ARG, "the EWC penalty needs d_fisher and d_theta_prev");
+  return TCL_OK;
+}
+
+}  // namespace
+
+TCL_API tcl_status tcl_distill_step_kd(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats,
+                                       const int32_t* d_lengths, const float* d_labels, const tcl_kd_loss* kd,
+                                       float* d_loss, void* d_ws, size_t ws_bytes, void* stream) {
+  const tcl_status st = check_kd(kd);
+  if (st != TCL_OK) return st;
   return distill_step(tr, B, L, d_feats, d_lengths, d_labels, kd, d_loss, d_ws, ws_bytes, stream);
+}
+
+TCL_API tcl_status tcl_test_distill_step_kd_ranked(tcl_trainer* tr, int32_t B, int32_t L, const float* d_feats,
+                                                   const int32_t* d_lengths, const float* d_labels,
+                                                   const tcl_kd_loss* kd, const float* d_rank_keys,
+                                                   float* d_scores_out, float* d_loss, void* d_ws,
+                                                   size_t ws_bytes, void* stream) {
+  const tcl_status st = check_kd(kd);
+  if (st != TCL_OK) return st;
+  return distill_step(tr, B, L, d_feats, d_lengths, d_labels, kd, d_loss, d_ws, ws_bytes, stream, d_rank_keys,
+                      d_scores_out);
+}
+
+TCL_API tcl_status tcl_teacher_gate(int32_t n, const float* d_e, float* d_phi, void* stream) {
+  if (n <= 0) return fail(TCL_ERR_INVALID_ARG, "n=%d must be positive", n);
+  if (!d_e || !d_phi) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  TCL_HIP(launch_teacher_gate(n, d_e, d_phi, static_cast<hipStream_t>(stream)));
+  return TCL_OK;
 }
 
 TCL_API size_t tcl_lambdarank_workspace_bytes(int32_t B) {

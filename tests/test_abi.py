@@ -96,6 +96,9 @@ def test_calls_on_null_handles(lib):
     assert lib.tcl_get_params(None, None, 0) == -1
     assert lib.tcl_test_gemm_f32(0, 4, 4, None, None, None, None, -1, 0, None) == -1
     assert lib.tcl_test_scan_f32(1, 16, 8, 4, 0, *([None] * 4), 16, *([None] * 6)) in (-1, -2)
+    assert lib.tcl_teacher_gate(0, None, None, None) == -1
+    assert lib.tcl_teacher_gate(4, None, None, None) == -1
+    assert lib.tcl_test_distill_step_kd_ranked(None, 1, 1, *([None] * 8), 0, None) == -1
 
 
 def test_split_gemm_entry_rejects_bad_arguments(lib):

@@ -419,6 +419,50 @@ def test_scan_f32(R, L, chunks):
     assert np.all(err <= 1e-4 * (np.abs(expect) + scale)), float(np.max(err / (np.abs(expect) + scale)))
 
 
+def test_scan_chunked_at_long_sequence_shape():
+    """The long-sequence workload's scan shape (B = 8192 programs of 64..256
+    tokens, E = 512, N = 16, R = 16) through the chunked two-level scan
+    forced to 8 chunks per program (tcl_score picks the sequential scan at
+    this batch size): every element against the sequential scan (the same
+    recurrence, its chunks stitched through per-chunk affine summaries, so
+    equal to rounding: 1e-4 of |y| plus the output's rms), and a sample of
+    programs, the first and last among them, against the oracle."""
+    N, E, R, L, B = 16, 512, 16, 256, 8192
+    rng = np.random.default_rng(8192)
+    lengths = rng.integers(64, L + 1, size=B).astype(np.int32)
+    rows = int(lengths.sum())
+    u = rng.standard_normal((rows, E), dtype=np.float32)
+    z = rng.standard_normal((rows, E), dtype=np.float32)
+    xdbl = 0.5 * rng.standard_normal((rows, R + 2 * N), dtype=np.float32)
+    W_dt = rng.uniform(-0.25, 0.25, (E, R)).astype(np.float32)
+    b_dt = np.log(np.expm1(np.exp(rng.uniform(np.log(1e-3), np.log(1e-1), E)))).astype(np.float32)
+    A_log = (np.log(np.arange(1, N + 1))[None, :] + 0.3 * rng.standard_normal((E, N))).astype(np.float32)
+    D = rng.standard_normal(E).astype(np.float32)
+    print(f"scan B={B} rows={rows} E={E}: chunked (8) vs sequential", flush=True)
+    offs = _offs(lengths)
+    d = [_dev(a) for a in (u, xdbl, z, W_dt, b_dt, A_log, D)]
+    od = _dev(offs, torch.int32)
+    seq = torch.full((rows, E), float("nan"), device="cuda")
+    chk = torch.full((rows, E), float("nan"), device="cuda")
+    tb.scan_f32(od, *d, seq, chunks=0)
+    tb.scan_f32(od, *d, chk, chunks=8)
+    torch.cuda.synchronize()
+    scale = float(torch.sqrt(torch.mean(seq.double() ** 2)))
+    bad = (chk - seq).abs() > 1e-4 * (seq.abs() + scale)
+    assert not torch.isnan(chk).any() and int(bad.sum()) == 0, int(bad.sum())
+    idx = np.unique(np.concatenate([[0, B - 1], rng.choice(B, 4, replace=False)]))
+    f = lambda a: a.astype(np.float64)
+    got = chk.cpu().numpy()
+    for b in idx:
+        r0, r1 = int(offs[b]), int(offs[b + 1])
+        dt = om.softplus(f(xdbl[r0:r1, :R]) @ f(W_dt).T + f(b_dt))
+        y = om.selective_scan(f(u[r0:r1])[None], dt[None], -np.exp(f(A_log)), f(xdbl[r0:r1, R:R + N])[None],
+                              f(xdbl[r0:r1, R + N:])[None], f(D))[0]
+        expect = y * om.silu(f(z[r0:r1]))
+        err = np.abs(got[r0:r1] - expect)
+        assert np.all(err <= 1e-4 * (np.abs(expect) + scale)), (int(b), float(np.max(err)))
+
+
 @pytest.mark.parametrize("chunks", [0, 4])
 def test_scan_in_place_matches_out_of_place(chunks):
     """The model runs the scan with out aliasing u; results must not change."""
