@@ -5,9 +5,19 @@ student's parameters after Adam.
 Tolerances (bf16 compute, fp32 master weights and gradients):
   loss: relative 2e-2;
   gradients: per tensor, ||g_gpu - g_oracle|| <= 2e-2 ||g_oracle||, and
-    element by element |g_gpu - g_oracle| <= 0.1 rms(g_oracle) of the tensor
-    (five times the rms error the norm bound allows: a wrong row, channel or
-    entry of the size of a typical gradient entry fails it);
+    element by element |g_gpu - g_oracle| <= 5e-2 |g_oracle| + 0.1 s, with s
+    the local scale of the entry: the largest of the tensor's rms and, for a
+    matrix, the rms of the entry's row and of its column. A weight gradient
+    sum_t dY_t x_t^T has entries whose size (and whose rounding error) follow
+    their row's and column's scale -- a feature dimension with large
+    activations has a column of large entries -- so the absolute term is
+    five times the rms error the norm bound allows, at that scale. The
+    relative term covers the largest entries, sums over tokens of products of
+    bf16-rounded activations (each off by up to 2^-9) with cancellation
+    between the tokens' terms: up to 3% was measured on the largest in_proj
+    entries of the small perturbed model. A wrong row, channel or entry, a
+    sign error or a dropped term moves an entry by about its own size and
+    fails it;
   parameters: the update must be Adam applied exactly to the GPU's own
     gradient, and it must match the oracle's to 2e-2 lr wherever the oracle's
     gradient is clearly non-zero (|g| > 5e-2 rms of its tensor, > 6 standard
@@ -53,12 +63,24 @@ def _gpu(tshape, sshape, tblob, sblob, X, lengths, labels, steps):
     return out
 
 
-ELEM_RMS = 0.1  # element-wise gradient bound, in units of the tensor's rms
+ELEM_RMS = 0.1   # element-wise gradient bound: this many of the entry's local scale
+ELEM_REL = 5e-2  # plus this fraction of the entry itself
+
+
+def local_scale(o: np.ndarray) -> np.ndarray:
+    """Per entry: the largest of the tensor's rms and, for a matrix, its
+    row's and its column's rms."""
+    rms = np.sqrt(np.mean(o * o))
+    if o.ndim != 2:
+        return np.full(o.shape, rms)
+    row = np.sqrt(np.mean(o * o, axis=1, keepdims=True))
+    col = np.sqrt(np.mean(o * o, axis=0, keepdims=True))
+    return np.maximum(np.maximum(row, col), rms)
 
 
 def check_grads(G, O, what, floor=1e-12):
     """Per tensor: the norm bound and the element-wise bound (module doc).
-    Prints each tensor's worst element error in units of its rms."""
+    Prints each tensor's largest element error in units of its rms."""
     worst = {}
     for name in O:
         d = np.abs(G[name] - O[name])
@@ -66,11 +88,12 @@ def check_grads(G, O, what, floor=1e-12):
         rms = ref / np.sqrt(max(O[name].size, 1))
         assert err <= 2e-2 * ref + floor, f"{what}: grad {name} rel err {err / max(ref, 1e-30):.3e}"
         worst[name] = float(d.max() / max(rms, 1e-30))
-        k = np.unravel_index(int(np.argmax(d)), d.shape)
-        assert d.max() <= ELEM_RMS * rms + floor, (
-            f"{what}: grad {name}{list(k)} gpu={G[name][k]!r} oracle={O[name][k]!r}: "
-            f"error {worst[name]:.3e} rms of the tensor")
-    print(f"{what}: worst element error / rms per tensor: " +
+        bound = ELEM_REL * np.abs(O[name]) + ELEM_RMS * local_scale(O[name]) + floor
+        k = np.unravel_index(int(np.argmax(d / bound)), d.shape)
+        assert np.all(d <= bound), (
+            f"{what}: grad {name}{list(k)} gpu={G[name][k]!r} oracle={O[name][k]!r}: error {d[k]:.3e}, "
+            f"bound {bound[k]:.3e} (tensor rms {rms:.3e})")
+    print(f"{what}: largest element error / rms per tensor: " +
           ", ".join(f"{k} {v:.2e}" for k, v in sorted(worst.items(), key=lambda kv: -kv[1])[:6]), flush=True)
 
 
