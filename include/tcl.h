@@ -166,6 +166,29 @@ TCL_API tcl_status tcl_score(tcl_model* model, int32_t B, int32_t L, const float
                              const int32_t* d_lengths, float* d_scores, void* d_workspace,
                              size_t ws_bytes, void* stream);
 
+/* tcl_score for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same scores, bit for bit, as tcl_score run as one pass (its kernels, on
+ * `stream` only), with the workspace taken from a buffer the library holds
+ * in each GPU's memory (a file-scope device array of
+ * tcl_score_noalloc_max_bytes() = 256 MiB, present on every device the
+ * library runs on until the process ends; its address is looked up once
+ * per device when a model is created there). The call allocates nothing
+ * and calls no allocating routine.
+ *   Arguments as tcl_score without the workspace; the model's device must
+ *   be current. Batches whose workspace (tcl_score_workspace_bytes of a
+ *   batch under 2048 programs, the one-pass size) exceeds the buffer are
+ *   refused with TCL_ERR_UNSUPPORTED before anything is enqueued (about
+ *   1,400 programs of 25 tokens for d_model 256). Per-kernel timing must be
+ *   disabled (TCL_ERR_INVALID_ARG otherwise).
+ * Every call on a GPU uses that GPU's one buffer, which keeps the last
+ * call's contents (nothing in it needs to start cleared): calls that
+ * overlap on one GPU -- on different streams, or from several host threads,
+ * for any models -- race on it and must be serialised by the caller. */
+TCL_API size_t tcl_score_noalloc_max_bytes(void);
+TCL_API tcl_status tcl_score_noalloc(tcl_model* model, int32_t B, int32_t L, const float* d_feats,
+                                     const int32_t* d_lengths, float* d_scores, void* stream);
+
 /* Copy the fp32 master parameters (canonical blob) back to the host. */
 TCL_API tcl_status tcl_get_params(const tcl_model* model, float* h_out, size_t n_params);
 

@@ -52,6 +52,8 @@ _SIGS = {
     "tcl_score_workspace_bytes": (_sz, [_vp, _i32, _i32]),
     "tcl_set_score_streams": (_i32, [_vp, _i32]),
     "tcl_score": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "tcl_score_noalloc_max_bytes": (_sz, []),
+    "tcl_score_noalloc": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp]),
     "tcl_get_params": (_i32, [_vp, _vp, _sz]),
     "tcl_set_params": (_i32, [_vp, _vp, _sz]),
     "tcl_last_error": (ctypes.c_char_p, []),
@@ -197,6 +199,14 @@ class CostModel:
         ws = self.workspace(B, L) if workspace is None else workspace
         check(lib().tcl_score(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), out.data_ptr(),
                               ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)))
+        return out
+
+    def score_noalloc(self, feats, lengths, out, stream=None):
+        """tcl_score_noalloc: the scores into `out` with the library's own
+        scratch buffer (no workspace, nothing allocated)."""
+        B, L, _ = feats.shape
+        check(lib().tcl_score_noalloc(self._h, B, L, feats.data_ptr(), lengths.data_ptr(), out.data_ptr(),
+                                      _stream(stream)))
         return out
 
     def set_score_streams(self, n: int):

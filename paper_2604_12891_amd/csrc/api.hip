@@ -6,6 +6,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "model.h"
 
@@ -534,6 +535,41 @@ void release_streams(tcl_model* m) {
 }
 }  // namespace
 
+// ------------------------------------------------------------------ scratch for tcl_score_noalloc
+// tcl_score's workspace for callers that cannot allocate: one file-scope
+// device array per GPU, held until the process ends. Host code never uses
+// the array's name as an address (on the host it names a stand-in, not
+// device memory): each device's copy is looked up once with
+// hipGetSymbolAddress, with that device current, and kept in g_scratch.
+constexpr size_t kScratchBytes = (size_t)256 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxScratchDevices] = {};
+
+// This device's copy of `scratch`; `dev` must be the current device.
+tcl_status scratch_ptr(int dev, void** out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(TCL_ERR_UNSUPPORTED, "device %d beyond the %d the scratch table holds", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(TCL_ERR_HIP, "hipGetSymbolAddress of the scratch buffer failed on device %d: %s", dev,
+                  hipGetErrorString(e));
+    }
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return TCL_OK;
+}
+}  // namespace
+
 TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_params,
                                          size_t n_params, tcl_model** out) {
   if (!out) return fail(TCL_ERR_INVALID_ARG, "out is NULL");
@@ -631,6 +667,12 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
     return cleanup(fail(TCL_ERR_HIP, "upload of the derivation table failed"));
   st = load_params(m, h_params);
   if (st != TCL_OK) return cleanup(st);
+  {
+    // set-up of tcl_score_noalloc's buffer on this device (the model's
+    // device is current here); a failure is reported by that entry point
+    void* unused = nullptr;
+    if (scratch_ptr(m->device, &unused) != TCL_OK) (void)hipGetLastError();
+  }
   // default-priority streams for tcl_score's half batches
   bool ok = true;
   for (int i = 0; i < 2 && ok; ++i) ok = hipStreamCreateWithFlags(&m->aux[i], hipStreamNonBlocking) == hipSuccess;
@@ -708,6 +750,33 @@ TCL_API tcl_status tcl_score(tcl_model* m, int32_t B, int32_t L, const float* d_
   TCL_HIP(hipStreamWaitEvent(s, m->ev[1], 0));
   TCL_HIP(hipStreamWaitEvent(s, m->ev[2], 0));
   return TCL_OK;
+}
+
+TCL_API size_t tcl_score_noalloc_max_bytes(void) { return kScratchBytes; }
+
+TCL_API tcl_status tcl_score_noalloc(tcl_model* m, int32_t B, int32_t L, const float* d_feats,
+                                     const int32_t* d_lengths, float* d_scores, void* stream) {
+  if (!m) return fail(TCL_ERR_INVALID_ARG, "model is NULL");
+  if (B <= 0 || L <= 0) return fail(TCL_ERR_INVALID_ARG, "B and L must be positive (B=%d L=%d)", B, L);
+  if (!d_feats || !d_lengths || !d_scores) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  if (reinterpret_cast<uintptr_t>(d_feats) % 16) return fail(TCL_ERR_INVALID_ARG, "d_feats must be 16-byte aligned");
+  if (m->timing.on)
+    return fail(TCL_ERR_INVALID_ARG, "per-kernel timing creates events: disable it for tcl_score_noalloc");
+  const size_t need = score_plan(m->cfg, B, L).total;
+  if ((int64_t)B * L > (int64_t)1 << 30 || need > kScratchBytes)
+    return fail(TCL_ERR_UNSUPPORTED,
+                "B=%d L=%d needs %zu bytes of workspace, more than the %zu of the library's scratch buffer "
+                "(use tcl_score with a caller-owned workspace)", B, L, need, kScratchBytes);
+  int cur = -1;
+  TCL_HIP(hipGetDevice(&cur));
+  if (cur != m->device)
+    return fail(TCL_ERR_INVALID_ARG, "the model's device %d must be current (current: %d)", m->device, cur);
+  void* ws = nullptr;
+  const tcl_status st = scratch_ptr(m->device, &ws);
+  if (st != TCL_OK) return st;
+  // one pass on the caller's stream (no fork onto the model's streams)
+  return run_score(m, B, L, d_feats, d_lengths, d_scores, static_cast<char*>(ws),
+                   static_cast<hipStream_t>(stream));
 }
 
 // ------------------------------------------------------------------ timing
