@@ -25,10 +25,28 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
 BF16_MFMA_PEAK_TFS = 2516.6    # MI355X dense bf16 matrix, TFLOP/s
-# fp32 GEMMs on the split path run six bf16 MFMA products per fp32 product:
-# they are reported against the fp32 matrix peak (the arithmetic they
-# deliver) and, beside it, as the bf16 matrix-core work they issue
-SPLIT_PRODUCTS = 6
+# fp32 GEMMs on the split path deliver fp32 results from the 16-bit matrix
+# cores: in_proj and the encoder's Linear layers with two-part fp16 operands
+# (three part products per fp32 product), the others with three-part bf16
+# operands (six). They are reported against the fp32 matrix peak (the
+# arithmetic they deliver) and, beside it, as the 16-bit matrix-core work they
+# issue against the dense fp16 / bf16 peak (the same 2.5 PFLOP/s).
+F16_SPLIT_KERNELS = ("gemm_input", "gemm_encoder", "gemm_in_proj")
+BF16_SPLIT_KERNELS = ("gemm_out_proj",)
+
+
+def split_form(name: str, f32_matmul: str):
+    """(products per fp32 product, matrix dtype) of a split-path GEMM, or None."""
+    if f32_matmul == "split":
+        if name in F16_SPLIT_KERNELS:
+            return 3, "fp16"
+        if name in BF16_SPLIT_KERNELS:
+            return 6, "bf16"
+    if f32_matmul == "split_bf16" and name in F16_SPLIT_KERNELS + BF16_SPLIT_KERNELS:
+        return 6, "bf16"
+    return None
+
+
 # the paper's end-to-end results (tuning time to reach Tenset-MLP's latency
 # after 2000 trials, section 7.3, Fig. 10): context only, not this metric
 PAPER_CONTEXT = {
@@ -91,19 +109,21 @@ def expected_launches(name: str, shape) -> int:
     return 1
 
 
-def roofline_entry(kind, amount, ms_per_launch, dtype, split=False):
+def roofline_entry(kind, amount, ms_per_launch, dtype, split=None):
+    """split: (products, matrix dtype) of a split-path fp32 GEMM, else None."""
     if kind == "flop":
         achieved = amount / (ms_per_launch * 1e-3) / 1e12
         peak = BF16_MFMA_PEAK_TFS if dtype != "f32" else FP32_MFMA_PEAK_TFS
         e = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak}
         if dtype == "f32" and split:
-            issued = SPLIT_PRODUCTS * achieved
-            e["bf16_mfma"] = {"achieved": issued, "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s",
-                              "frac": issued / BF16_MFMA_PEAK_TFS}
-            e["peak_note"] = ("fp32 results at fp32 accuracy, against the fp32 matrix peak; computed on the bf16 "
-                              "matrix cores with both operands split exactly into three bf16 parts and six part "
-                              "products per fp32 product, so bf16_mfma is 6x the fp32 rate against the dense "
-                              "bf16 peak")
+            products, mdt = split
+            issued = products * achieved
+            e["matrix_core"] = {"dtype": mdt, "products": products, "achieved": issued,
+                                "peak": BF16_MFMA_PEAK_TFS, "unit": "TFLOP/s", "frac": issued / BF16_MFMA_PEAK_TFS}
+            e["peak_note"] = ("fp32 results against the fp32 matrix peak; computed on the 16-bit matrix cores "
+                              "with both operands in exact parts (two fp16 parts, three part products, or three "
+                              "bf16 parts, six products): matrix_core is that issued work against the dense "
+                              "fp16/bf16 peak")
         return e
     achieved = amount / (ms_per_launch * 1e-3) / 1e9
     return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -115,8 +135,8 @@ def _roof(name: str, d: dict) -> dict:
     roof = {"kernel": name, "bound": d["bound"], "achieved": round(d["achieved"], 3), "peak": d["peak"],
             "unit": d["unit"], "frac": round(d["frac"], 4), "traffic": None,
             "ms_per_launch": round(d["ms_per_launch"], 5)}
-    if "bf16_mfma" in d:
-        roof["bf16_mfma"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in d["bf16_mfma"].items()}
+    if "matrix_core" in d:
+        roof["matrix_core"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in d["matrix_core"].items()}
     if "peak_note" in d:
         roof["peak_note"] = d["peak_note"]
     return roof
@@ -277,8 +297,7 @@ def bench_progressive(args, w):
             amount = amount / launches
         else:  # each column's own kernels: per-launch counts of the plain model
             kind, amount = per[base]
-        e = roofline_entry(kind, amount, tot / n, "f32",
-                           split and base in ("gemm_input", "gemm_encoder", "gemm_in_proj", "gemm_out_proj"))
+        e = roofline_entry(kind, amount, tot / n, "f32", split_form(base, args.f32_matmul))
         e.update({"ms_per_launch": tot / n, "launches_per_step": launches, "ms_per_step": tot / args.steps,
                   "work_per_launch": amount, "work_unit": kind})
         kernels[name] = e
@@ -592,9 +611,10 @@ def main():
     ap.add_argument("--no-single-stream", action="store_true",
                     help="skip the second per-kernel timing pass with the batch in one pass (so that a "
                          "profiler's per-dispatch averages cover the timed configuration only)")
-    ap.add_argument("--f32-matmul", choices=["split", "native"], default="split",
-                    help="fp32 models: projections on the bf16 matrix cores with split operands (fp32 "
-                         "accuracy), or on the fp32 matrix cores")
+    ap.add_argument("--f32-matmul", choices=["split", "split_bf16", "native"], default="split",
+                    help="fp32 models: projections on the 16-bit matrix cores with split operands (two-part "
+                         "fp16 where the shape allows, else three-part bf16; split_bf16: three-part bf16 "
+                         "everywhere), or on the fp32 matrix cores")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run 3 elementwise passes over 256 MiB (known bytes for HBM counters)")
     args = ap.parse_args()
@@ -639,8 +659,7 @@ def main():
     Xd = torch.from_numpy(X).to(dev)
     Ld = torch.from_numpy(lengths).to(dev)
     model = tb.CostModel(tb.config_from_shape(w.model, w.dtype, args.f32_matmul), blob)
-    split = w.dtype == "f32" and args.f32_matmul == "split"
-    split_kernels = ("gemm_input", "gemm_encoder", "gemm_in_proj", "gemm_out_proj")
+    split = w.dtype == "f32" and args.f32_matmul in ("split", "split_bf16")
     ws = model.workspace(w.B, w.L)
     out = torch.empty(w.B, dtype=torch.float32, device=dev)
     M_v = int(lengths.sum())
@@ -700,7 +719,7 @@ def main():
             # kernel once per half, each with (about) half the work
             parts = max(1, round(n / args.steps / expected_launches(name, w.model)))
             amount = tuple(a / parts for a in amount) if isinstance(amount, tuple) else amount / parts
-            e = roofline_entry(kind, amount, per, w.dtype, split and name in split_kernels)
+            e = roofline_entry(kind, amount, per, w.dtype, split_form(name, args.f32_matmul) if split else None)
             e.update({"ms_per_launch": per, "launches_per_step": n // args.steps,
                       "ms_per_step": tot / args.steps, "work_per_launch": amount, "work_unit": kind})
             kernels[name] = e
@@ -712,7 +731,8 @@ def main():
             print(f"{'kernel':16s} {'ms/step':>9s} {'ms/launch':>10s} {'achieved':>10s} {'unit':8s} "
                   f"{'frac':>6s}", file=sys.stderr)
             for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
-                extra = f"  (bf16 MFMA {e['bf16_mfma']['frac']:.3f})" if "bf16_mfma" in e else ""
+                extra = (f"  ({e['matrix_core']['dtype']} matrix cores {e['matrix_core']['frac']:.3f})"
+                         if "matrix_core" in e else "")
                 print(f"{k:16s} {e['ms_per_step']:9.4f} {e['ms_per_launch']:10.5f} {e['achieved']:10.2f} "
                       f"{e['unit']:8s} {e['frac']:6.3f}{extra}", file=sys.stderr)
         return kernels, roof

@@ -17,8 +17,9 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtcl.so"
 _lib = None
 
 TCL_F32, TCL_BF16 = 0, 1
-TCL_F32_MATMUL_SPLIT, TCL_F32_MATMUL_NATIVE = 0, 1
-F32_MATMUL = {"split": TCL_F32_MATMUL_SPLIT, "native": TCL_F32_MATMUL_NATIVE}
+TCL_F32_MATMUL_SPLIT, TCL_F32_MATMUL_NATIVE, TCL_F32_MATMUL_SPLIT_BF16 = 0, 1, 2
+F32_MATMUL = {"split": TCL_F32_MATMUL_SPLIT, "native": TCL_F32_MATMUL_NATIVE,
+              "split_bf16": TCL_F32_MATMUL_SPLIT_BF16}
 STATUS = {0: "TCL_OK", -1: "TCL_ERR_INVALID_ARG", -2: "TCL_ERR_UNSUPPORTED", -3: "TCL_ERR_WORKSPACE",
           -4: "TCL_ERR_OOM", -5: "TCL_ERR_HIP"}
 
@@ -127,7 +128,7 @@ def check(status: int):
 
 def make_config(F, d_model, d_inner, d_state, d_conv, dt_rank, n_layers, head_hidden,
                 final_norm=1, norm_eps=1e-5, dtype="f32", f32_matmul="split", enc_hidden=(), dec_hidden2=0) -> Config:
-    """f32_matmul ("split" or "native") selects how an fp32 model runs its
+    """f32_matmul ("split", "split_bf16" or "native") selects how an fp32 model runs its
     dense projections (tcl_f32_matmul); enc_hidden (up to two widths) and
     dec_hidden2 select the multi-layer encoder and three-layer decoder."""
     enc = list(enc_hidden) + [0] * (2 - len(enc_hidden))

@@ -163,15 +163,22 @@ tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string&
     // the gathered input Linear (rows b*L + t of the padded input)
     g.offs = offs; g.B = B; g.L = L; g.W = m->W0; g.ldw = m->ldw0; g.bias = m->b0;
     // on the split path the row lookup of the gather also yields the token positions
-    const bool on_split = m->split && m->W0_s && gemm_split_variant(g, kBias | kGather) > 0;
+    const bool on_h2 = m->W0_h2 && m->W0_h2_ok && gemm_f16s_supports(g, kBias | kGather);
+    const bool on_split = on_h2 || (m->split && m->W0_s && gemm_split_variant(g, kBias | kGather) > 0);
     if (on_split && tpos_out) {
       g.tpos = tpos_out;
       if (tpos_written) *tpos_written = true;
     }
-    TCL_LAUNCH(T, (tag + "gemm_input").c_str(), model_gemm(m, g, m->W0_s, m->ldw0_h, kBias | kGather, s));
+    if (on_h2)
+      TCL_LAUNCH(T, (tag + "gemm_input").c_str(), launch_gemm_f16s(g, m->W0_h2, m->ldw0_h, kBias | kGather, s));
+    else
+      TCL_LAUNCH(T, (tag + "gemm_input").c_str(), model_gemm(m, g, m->W0_s, m->ldw0_h, kBias | kGather, s));
   } else {
     g.W = m->We[i]; g.ldw = in; g.bias = m->be[i];
-    TCL_LAUNCH(T, (tag + "gemm_encoder").c_str(), model_gemm(m, g, m->We_s[i], (in + 7) & ~7, kBias, s));
+    if (m->We_h2[i] && m->We_h2_ok[i] && gemm_f16s_supports(g, kBias))
+      TCL_LAUNCH(T, (tag + "gemm_encoder").c_str(), launch_gemm_f16s(g, m->We_h2[i], (in + 7) & ~7, kBias, s));
+    else
+      TCL_LAUNCH(T, (tag + "gemm_encoder").c_str(), model_gemm(m, g, m->We_s[i], (in + 7) & ~7, kBias, s));
   }
   return TCL_OK;
 }
@@ -187,7 +194,10 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   GemmArgs gi;
   gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
   gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-  TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), model_gemm(m, gi, W.W_in_s, d, kRowNorm, s));
+  if (W.W_in_h2 && W.in_h2_ok && gemm_f16s_supports(gi, kRowNorm))
+    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), launch_gemm_f16s(gi, W.W_in_h2, (d + 7) & ~7, kRowNorm, s));
+  else
+    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), model_gemm(m, gi, W.W_in_s, d, kRowNorm, s));
   GemmArgs gx;
   gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
   gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
@@ -329,7 +339,8 @@ tcl_status check_config(const tcl_config* c) {
     return fail(TCL_ERR_INVALID_ARG, "config has a non-positive field");
   if (c->dtype != TCL_F32 && c->dtype != TCL_BF16)
     return fail(TCL_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
-  if (c->f32_matmul != TCL_F32_MATMUL_SPLIT && c->f32_matmul != TCL_F32_MATMUL_NATIVE)
+  if (c->f32_matmul != TCL_F32_MATMUL_SPLIT && c->f32_matmul != TCL_F32_MATMUL_NATIVE &&
+      c->f32_matmul != TCL_F32_MATMUL_SPLIT_BF16)
     return fail(TCL_ERR_INVALID_ARG, "unknown f32_matmul %d", c->f32_matmul);
   if (c->F > 1024) return fail(TCL_ERR_UNSUPPORTED, "F must be <= 1024 (got %d)", c->F);
   if (c->d_model != 64 && c->d_model != 128 && c->d_model != 256)
@@ -363,7 +374,11 @@ tcl_status check_config(const tcl_config* c) {
 
 namespace {
 
-bool uses_split(const tcl_config& c) { return c.dtype == TCL_F32 && c.f32_matmul == TCL_F32_MATMUL_SPLIT; }
+bool uses_split(const tcl_config& c) {
+  return c.dtype == TCL_F32 && (c.f32_matmul == TCL_F32_MATMUL_SPLIT || c.f32_matmul == TCL_F32_MATMUL_SPLIT_BF16);
+}
+// the two-part fp16 GEMMs where their shapes allow (in_proj, the encoder)
+bool uses_f16_split(const tcl_config& c) { return c.dtype == TCL_F32 && c.f32_matmul == TCL_F32_MATMUL_SPLIT; }
 
 // Plan of the model's device block: every derived layout, then the master
 // blob, then the job table that derives the former from the latter.
@@ -371,12 +386,13 @@ struct ModelPlan {
   std::vector<DeriveJob> jobs;
   int64_t total = 0;
   size_t bytes = 0, master = 0, jobtab = 0;
-  size_t W0 = 0, b0 = 0, W0_h = 0, W0_s = 0, g_f = 0, W1 = 0, W1T = 0, b1 = 0, W2 = 0, b2 = 0;
-  size_t We[3] = {0, 0, 0}, be[3] = {0, 0, 0}, We_s[3] = {0, 0, 0}, W2T = 0, W3 = 0, b3 = 0;
+  size_t W0 = 0, b0 = 0, W0_h = 0, W0_s = 0, W0_h2 = 0, g_f = 0, W1 = 0, W1T = 0, b1 = 0, W2 = 0, b2 = 0;
+  size_t We[3] = {0, 0, 0}, be[3] = {0, 0, 0}, We_s[3] = {0, 0, 0}, We_h2[3] = {0, 0, 0};
+  size_t W2T = 0, W3 = 0, b3 = 0;
   int ldw0 = 0;
   struct L {
     size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
-    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_x_s, W_out_s;
+    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_x_s, W_out_s, W_in_h2;
   };
   std::vector<L> layers;
   int ldw0_h = 0;
@@ -391,12 +407,14 @@ struct ModelPlan {
 //  - bf16 copies of the projections for bf16 models, W0 zero-padded in K to
 //    a multiple of 8 (the padding is zeroed once at create);
 //  - three-way bf16 splits of W0, W_in (gain folded) and W_out for fp32
-//    models on the split path, [3][rows][ld] each.
+//    models on the split path, [3][rows][ld] each, and two-part fp16 splits
+//    of W0, the hidden encoder layers and W_in (gain folded), [2][rows][ld].
 ModelPlan plan_model(const tcl_config& c) {
   ModelPlan P;
   const BlobLayout bl = blob_layout(c);
   const bool bf = c.dtype == TCL_BF16;
   const bool sp = uses_split(c);
+  const bool h2 = uses_f16_split(c);
   const int d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank, XW = R + 2 * N;
   const int F = c.F, h = c.head_hidden;
   P.ldw0_h = (F + 7) & ~7;
@@ -406,7 +424,9 @@ ModelPlan plan_model(const tcl_config& c) {
                  size_t src2 = 0) {
     const size_t dst = o;
     const int ldd = ld > 0 ? ld : (transpose ? rows : cols);
-    const int parts = (kind == kDeriveSplit || kind == kDeriveFoldSplit) ? 3 : 1;
+    const int parts = (kind == kDeriveSplit || kind == kDeriveFoldSplit)        ? 3
+                      : (kind == kDeriveSplitF16 || kind == kDeriveFoldSplitF16) ? 2
+                                                                                 : 1;
     const size_t n_out = parts * (transpose ? (size_t)cols * ldd : (size_t)rows * ldd);
     o = align256(o + n_out * elem_bytes);
     DeriveJob J{};
@@ -430,11 +450,13 @@ ModelPlan plan_model(const tcl_config& c) {
   P.b0 = job(bl.b0, 1, e0, kDeriveF32, 0, 4);
   if (bf) P.W0_h = job(bl.W0, e0, F, kDeriveBF16, 0, 2, P.ldw0_h);
   if (sp) P.W0_s = job(bl.W0, e0, F, kDeriveSplit, 0, 2, P.ldw0_h);
+  if (h2) P.W0_h2 = job(bl.W0, e0, F, kDeriveSplitF16, 0, 2, P.ldw0_h);
   for (int i = 1; i < bl.n_enc; ++i) {
     const int in = bl.enc_dims[i], out = bl.enc_dims[i + 1];
     P.We[i] = job(bl.We[i], out, in, kDeriveF32, 0, 4);
     P.be[i] = job(bl.be[i], 1, out, kDeriveF32, 0, 4);
     if (sp) P.We_s[i] = job(bl.We[i], out, in, kDeriveSplit, 0, 2, (in + 7) & ~7);
+    if (h2) P.We_h2[i] = job(bl.We[i], out, in, kDeriveSplitF16, 0, 2, (in + 7) & ~7);
   }
   for (int l = 0; l < c.n_layers; ++l) {
     const auto& B = bl.layers[l];
@@ -463,6 +485,7 @@ ModelPlan plan_model(const tcl_config& c) {
       L.W_x_s = job(B.W_x, XW, E, kDeriveSplit, 0, 2);
       L.W_out_s = job(B.W_out, d, E, kDeriveSplit, 0, 2);
     }
+    if (h2) L.W_in_h2 = job(B.W_in, 2 * E, d, kDeriveFoldSplitF16, 0, 2, (d + 7) & ~7, B.g);
     P.layers.push_back(L);
   }
   P.g_f = job(bl.g_f, 1, d, kDeriveF32, 0, 4);
@@ -490,7 +513,29 @@ ModelPlan plan_model(const tcl_config& c) {
 
 // Upload a host blob into the model's master and derive every layout.
 // Synchronous.
+// Which matrices the two-part fp16 GEMMs may take: every (gain-folded)
+// weight below 32 in magnitude, so that its 2^10 scale stays in fp16's range
+// (the others keep the three-part bf16 split).
+void check_f16_ranges(tcl_model* m, const float* hp) {
+  const tcl_config& c = m->cfg;
+  if (!uses_f16_split(c)) return;
+  const BlobLayout bl = blob_layout(c);
+  auto fits = [&](size_t off, int rows, int cols, const float* g) {
+    for (int r = 0; r < rows; ++r)
+      for (int k = 0; k < cols; ++k) {
+        const float v = hp[off + (size_t)r * cols + k] * (g ? g[k] : 1.0f);
+        if (!(fabsf(v) < 32.0f)) return false;
+      }
+    return true;
+  };
+  m->W0_h2_ok = fits(bl.W0, bl.enc_dims[1], c.F, nullptr);
+  for (int i = 1; i < bl.n_enc; ++i) m->We_h2_ok[i] = fits(bl.We[i], bl.enc_dims[i + 1], bl.enc_dims[i], nullptr);
+  for (int l = 0; l < c.n_layers; ++l)
+    m->layers[l].in_h2_ok = fits(bl.layers[l].W_in, 2 * c.d_inner, c.d_model, hp + bl.layers[l].g);
+}
+
 tcl_status load_params(tcl_model* m, const float* h_params) {
+  check_f16_ranges(m, h_params);
   TCL_HIP(hipMemcpy(m->master, h_params, m->n_params * 4, hipMemcpyHostToDevice));
   tcl_status st = derive_weights(m, nullptr);
   if (st != TCL_OK) return st;
@@ -608,6 +653,7 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
   m->ldw0 = P.ldw0;
   m->split = uses_split(*cfg);
   m->W0_s = m->split ? B16(P.W0_s) : nullptr;
+  m->W0_h2 = uses_f16_split(*cfg) ? B16(P.W0_h2) : nullptr;
   for (const auto& L : P.layers) {
     tcl_model::Layer W{};
     W.W_in_fold = F32(L.W_in_fold);
@@ -634,6 +680,7 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
       W.W_x_s = B16(L.W_x_s);
       W.W_out_s = B16(L.W_out_s);
     }
+    W.W_in_h2 = uses_f16_split(*cfg) ? B16(L.W_in_h2) : nullptr;
     m->layers.push_back(W);
   }
   m->g_f = F32(P.g_f);
@@ -653,6 +700,7 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
       m->We[i] = F32(P.We[i]);
       m->be[i] = F32(P.be[i]);
       if (m->split) m->We_s[i] = B16(P.We_s[i]);
+      if (uses_f16_split(*cfg)) m->We_h2[i] = B16(P.We_h2[i]);
     }
   }
   auto cleanup = [&](tcl_status s2) {
@@ -904,8 +952,8 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
     M = B * L;
   }
   if (M <= 0 || N <= 0 || K <= 0 || K % 4) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
-  if (variant < -1 || variant > 4 || variant == 0)
-    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 1, 2, 3 or 4 (got %d)", variant);
+  if (variant < -1 || variant > 5 || variant == 0)
+    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 1, 2, 3, 4 or 5 (got %d)", variant);
   if ((epilogue == 1 || epilogue == 2) && d_bias)
     return fail(TCL_ERR_INVALID_ARG, "bias goes with epilogues 0 and 3 only");
   if (!d_A || !d_W || !d_C || !d_Wsplit) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
@@ -920,6 +968,13 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
   if (epilogue == 3) {
     g.offs = d_offs; g.B = B; g.L = L; g.Mdev = d_offs + B;
     flags = kBias | kGather;
+  }
+  if (variant == 5) {  // the two-part fp16 panels
+    if (!gemm_f16s_supports(g, flags))
+      return fail(TCL_ERR_UNSUPPORTED, "no fp16 split kernel for N=%d K=%d with epilogue %d", N, K, epilogue);
+    TCL_HIP(launch_split_weights_f16(d_W, N, K, Kw, d_Wsplit, s));
+    TCL_HIP(launch_gemm_f16s(g, d_Wsplit, Kw, flags, s));
+    return TCL_OK;
   }
   const int v = variant < 0 ? gemm_split_variant(g, flags) : variant;
   if (v < 0 || !gemm_split_supports(g, flags, v))

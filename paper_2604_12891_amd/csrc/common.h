@@ -86,4 +86,17 @@ __device__ __forceinline__ void split3_pair(float a, float b, uint32_t& h, uint3
   l = f32x2_to_bf16x2(ra - __uint_as_float(m << 16), rb - __uint_as_float(m & 0xFFFF0000u));
 }
 
+// Two-part fp16 form of fp32 values (the fp16 split GEMMs): x = h + 2^-11 l
+// + r, h = fp16(x), l = fp16(2^11 (x - h)), |r| <= 2^-22 |x| while x is in
+// fp16's normal range. Weights are scaled by 2^kF16WeightExp first.
+constexpr int kF16WeightExp = 10;
+constexpr float kF16LowScale = 2048.0f;  // 2^11
+__device__ __forceinline__ void split2_f16_scaled(float v, uint16_t& h, uint16_t& l) {
+  const float x = v * (float)(1 << kF16WeightExp);
+  const _Float16 hh = (_Float16)x;
+  const _Float16 ll = (_Float16)((x - (float)hh) * kF16LowScale);
+  h = __builtin_bit_cast(uint16_t, hh);
+  l = __builtin_bit_cast(uint16_t, ll);
+}
+
 }  // namespace tcl

@@ -1,0 +1,331 @@
+// fp32 GEMMs on the fp16 matrix cores with two-part operands: C = rowscale *
+// (A W^T) + bias, A and W fp32, with fp32-level accuracy. The fp32 model's
+// in_proj (with the RMSNorm prologue) and its gathered input Linear run here.
+//
+// Two-part fp16 operands. After an exact power-of-two scale that puts it in
+// fp16's range, each fp32 value x is held as x = h + 2^-11 l + r with
+// h = fp16(x) and l = fp16(2^11 (x - h)): x - h is exact in fp32 and at most
+// 2^-11 |x|, and rounding it to l's 11 bits leaves |r| <= 2^-22 |x| (for
+// |x| >= 2^-3; smaller scaled values lose bits of l in fp16's subnormal range,
+// an absolute error below 2^-36). Of the four products of two such values
+// three are kept, h_a h_w + 2^-11 (h_a l_w + l_a h_w), in two accumulators
+// (the large products, and the two small ones together):
+// fp16 x fp16 products are exact in fp32 and the MFMA accumulates in fp32.
+// The dropped 2^-22 l_a l_w and the two operands' r add at most 3 * 2^-22 |a w|
+// to each product, 12 units of fp32 rounding (2^-24), against the K units that
+// bound an fp32 dot product itself. An fp16 MFMA runs at the bf16 rate, so the
+// three products cost half the six of the three-part bf16 split, with the
+// operands in two parts instead of three (two thirds of the registers, LDS
+// bytes and fragment reads).
+//
+// Scales: each row of A by 2^eA, taken from the row's RMS (RMSNorm prologue:
+// scaled values below 2 * 16 * 2^8 for K <= 256) or from its largest value
+// (below 2^15); W by 2^10 when its parts are derived (the model routes a
+// matrix here only if every |w| < 32, so the scaled W stays below 2^15). The
+// epilogue multiplies by 2^-(eA + 10) (exact) and by the RMSNorm factor.
+//
+// Row panels of 128 rows, 4 wavefronts of 32 rows, each holding its rows'
+// two parts over the whole K (up to 256) as MFMA fragments in registers; W's
+// two parts stream through a double-buffered LDS stage 32 columns at a time
+// (one barrier per block; the next block loaded in two halves and staged
+// halfway through and at the end of the current block's MFMAs). A workgroup
+// takes 68 KB of LDS and at most 256 registers per lane, so two share a CU:
+// up to 512 panels run at once (61,715 token rows are 483 panels, one round),
+// and on each SIMD one workgroup's wavefront issues while the other's waits.
+// Fragment k-order (A and W alike): k-step s, lane half g holds k = 16 s +
+// 8 g .. +7.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace tcl {
+namespace {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kNT = kWaves * 64;
+constexpr int kBM = kWaves * 32;
+constexpr uint32_t kBufferFlags = 0x00020000;  // 32-bit data format, raw (stride 0)
+constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every resource used here
+constexpr float kLowInv = 1.0f / kF16LowScale;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferFlags);
+}
+
+// 2^e as a float, e in [-126, 127]
+__device__ __forceinline__ float pow2f(int e) { return __uint_as_float((uint32_t)(e + 127) << 23); }
+
+// floor(log2(x)) for a positive normal float (the exponent field); -127 for 0
+__device__ __forceinline__ int exponent_of(float x) { return (int)((__float_as_uint(x) >> 23) & 0xFF) - 127; }
+
+// 8 scaled fp32 values -> their two fp16 parts
+__device__ __forceinline__ void split8_f16(const float* x, f16x8& h, f16x8& l) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const _Float16 hj = (_Float16)x[j];
+    h[j] = hj;
+    l[j] = (_Float16)((x[j] - (float)hj) * kF16LowScale);
+  }
+}
+
+template <int KS, int FL>
+__global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uint16_t* Wh, int ldwh) {
+  constexpr int KP = KS * 16;       // K rounded up to the MFMA k-steps
+  // halves per staged W row: K rounded up to 64, plus 8 (conflict-free 16-byte reads)
+  constexpr int WP = (KP + 63) / 64 * 64 + 8;
+  constexpr int PART = 32 * WP;     // one part of one buffer
+  constexpr int WU = KP / 8;        // 16-byte units per staged row
+  constexpr int NWU = 2 * 32 * WU;  // units per column block (two parts)
+  constexpr int NW = (NWU + kNT - 1) / kNT;
+  constexpr int H = (NW + 1) / 2;   // the block's units, loaded and staged in two halves
+  constexpr bool kNorm = (FL & kRowNorm) != 0;
+  static_assert((FL & kResid) == 0, "no residual epilogue");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 2 * PART];
+  __shared__ float sF[kWaves][32];
+  __shared__ int sSrc[kBM];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 31, lg = lane >> 5;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * kBM;
+  if (row0 >= M) return;
+
+  for (int r = tid; r < kBM; r += kNT) {
+    const int grow = row0 + r;
+    int src = grow < M ? grow : -1;
+    if constexpr ((FL & kGather) != 0) {
+      if (src >= 0) {
+        int lo = 0, hi = p.B;
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (p.offs[mid] <= grow) lo = mid; else hi = mid;
+        }
+        src = lo * p.L + (grow - p.offs[lo]);
+        if (p.tpos) p.tpos[grow] = (uint8_t)min(grow - p.offs[lo], 255);
+      }
+    }
+    sSrc[r] = src;
+  }
+
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Wh, (uint32_t)__builtin_amdgcn_readfirstlane(2 * p.N * ldwh * 2));
+  // this workgroup's column blocks [sb, se): all of them, or one of
+  // gridDim.y ranges when a small batch leaves too few panels for the GPU
+  const int nblk = (p.N + 31) / 32;
+  const int sb = (int)(blockIdx.y * nblk / gridDim.y), se = (int)((blockIdx.y + 1) * nblk / gridDim.y);
+
+  // W stage: unit u of a block is part u / (32 WU), row (u / WU) % 32,
+  // k = 8 (u % WU); rows past N and k past ldwh read zero (the offset is moved
+  // out of range by bit 31: arithmetic, not a branch around the load)
+  u32x4 wr[H];
+  auto wload = [&](int half, int n0) {
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+      const int u = tid + (half * H + i) * kNT;
+      const int part = u / (32 * WU), n = n0 + (u / WU) % 32, k = 8 * (u % WU);
+      const bool ok = u < NWU && half * H + i < NW && n < p.N && k < ldwh;
+      const uint32_t off = (uint32_t)(((part * p.N + n) * ldwh + k) * 2) | ((uint32_t)!ok << 31);
+      wr[i] = __builtin_amdgcn_raw_buffer_load_b128(wres, off, 0, 0);
+    }
+  };
+  auto wstage = [&](int half, uint16_t* s) {
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+      const int u = tid + (half * H + i) * kNT;
+      if (u < NWU && half * H + i < NW) *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = wr[i];
+    }
+  };
+  wload(0, sb * 32);  // in flight during the prologue
+  __syncthreads();    // sSrc
+
+  // prologue: row li of this wavefront's 32, lane half lg's 8 k of every
+  // k-step, scaled by a power of two and split into its two fp16 parts
+  f16x8 ah[KS], al[KS];
+  {
+    const int src = sSrc[wave * 32 + li];
+    const float* arow = p.A + (src >= 0 ? (int64_t)src * p.lda : 0);
+    float x[KS][8];
+    float ss = 0.f, mx = 0.f;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int k = 16 * s + 8 * lg;
+      const bool ok0 = src >= 0 && k < p.K, ok1 = src >= 0 && k + 4 < p.K;
+      floatx4 v0 = *reinterpret_cast<const floatx4*>(arow + (ok0 ? k : 0));
+      floatx4 v1 = *reinterpret_cast<const floatx4*>(arow + (ok1 ? k + 4 : 0));
+      if (!ok0) v0 = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (!ok1) v1 = floatx4{0.f, 0.f, 0.f, 0.f};
+      x[s][0] = v0.x; x[s][1] = v0.y; x[s][2] = v0.z; x[s][3] = v0.w;
+      x[s][4] = v1.x; x[s][5] = v1.y; x[s][6] = v1.z; x[s][7] = v1.w;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if constexpr (kNorm) ss = fmaf(x[s][j], x[s][j], ss);
+        else mx = fmaxf(mx, fabsf(x[s][j]));
+      }
+    }
+    int eA;
+    float f;
+    if constexpr (kNorm) {
+      ss += __shfl_xor(ss, 32, 64);  // the other half of the row
+      const float ms = ss / (float)p.K;
+      // the scaled row's RMS in [2^8, 2^9): every value below 2^8 * 2 sqrt(K)
+      eA = ms > 0.f ? 8 - exponent_of(sqrtf(ms)) : 0;
+      eA = min(max(eA, -100), 100);
+      f = pow2f(-(eA + kF16WeightExp)) * (1.0f / sqrtf(ms + p.eps));
+    } else {
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      // the scaled row's largest value in [2^14, 2^15)
+      eA = mx > 0.f ? 14 - exponent_of(mx) : 0;
+      eA = min(max(eA, -100), 100);
+      f = pow2f(-(eA + kF16WeightExp));
+    }
+    const float sc = pow2f(eA);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[s][j] *= sc;
+      split8_f16(x[s], ah[s], al[s]);
+    }
+    if (lg == 0) sF[wave][li] = f;
+  }
+
+  const uint32_t panel_bytes = (uint32_t)(min(kBM, M - row0) * p.ldc * 4);
+  const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
+
+  wstage(0, &sW[0]);
+  wload(1, sb * 32);
+  wstage(1, &sW[0]);
+
+  for (int s = sb; s < se; ++s) {
+    const int buf = (s - sb) & 1, n0 = s * 32;
+    // block s (staged during block s-1) and sF visible; every wavefront is
+    // past block s-1, so the other buffer is free for block s+1
+    __syncthreads();
+    const bool more = s + 1 < se;
+    if (more) wload(0, n0 + 32);
+
+    floatx16 am, ax;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) am[r] = ax[r] = 0.f;
+    const uint16_t* wb = &sW[buf * 2 * PART + li * WP + 8 * lg];
+    auto wfrag = [&](int part, int ks) {
+      return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+    };
+    // W fragments one k-step ahead of their MFMAs (the other workgroup's
+    // wavefront on the SIMD covers the rest of the LDS latency)
+    f16x8 q[2][2];
+    q[0][0] = wfrag(0, 0);
+    q[0][1] = wfrag(1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) {
+        q[(ks + 1) & 1][0] = wfrag(0, ks + 1);
+        q[(ks + 1) & 1][1] = wfrag(1, ks + 1);
+      }
+      const f16x8* w = q[ks & 1];
+      // the small products' chain between the two MFMAs of the large one's
+      ax = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[1], ax, 0, 0, 0);
+      am = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[0], am, 0, 0, 0);
+      ax = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[ks], w[0], ax, 0, 0, 0);
+      if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0008, 3, 0);
+      // the next block's first half into the other buffer halfway through
+      // this block's MFMAs, then its second half loaded
+      if (ks == KS / 2 && more) {
+        wstage(0, &sW[(buf ^ 1) * 2 * PART]);
+        wload(1, n0 + 32);
+        __builtin_amdgcn_sched_group_barrier(0x0200, H, 0);
+      }
+    }
+    if (more) wstage(1, &sW[(buf ^ 1) * 2 * PART]);
+
+    // epilogue: lane l holds column l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
+    const int col = n0 + li;
+    const bool cok = col < p.N;
+    const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      float v = fmaf(ax[r], kLowInv, am[r]) * sF[wave][rl] + bias;
+      if (p.relu) v = fmaxf(v, 0.f);
+      // rows past M fall outside cres
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+    }
+  }
+}
+
+template <int FL>
+hipError_t launch_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, hipStream_t s) {
+  const int grid = (a.Mmax + kBM - 1) / kBM;
+  if (grid <= 0) return hipSuccess;
+  // two workgroups per CU: with fewer than two panels per CU the columns are
+  // also split, up to 8 ways (each workgroup repeats its panel's prologue)
+  const int nblk = (a.N + 31) / 32;
+  const int cs = std::max(1, std::min({8, nblk, 512 / grid}));
+  const dim3 g(grid, cs);
+#define TCL_F16S(KS)                                                                        \
+  hipLaunchKernelGGL((gemm_f16s_kernel<KS, FL>), g, dim3(kNT), 0, s, a, Wh, ldwh); \
+  break
+  switch ((a.K + 15) / 16) {
+    case 4: TCL_F16S(4);
+    case 8: TCL_F16S(8);
+    case 11: TCL_F16S(11);
+    case 12: TCL_F16S(12);
+    case 16: TCL_F16S(16);
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_F16S
+  return hipGetLastError();
+}
+
+// W -> its two fp16 parts after the 2^10 scale, [2][N][ldw], the padding k >= K zero
+__global__ __launch_bounds__(256) void split_weights_f16_kernel(const float* __restrict__ W, int N, int K,
+                                                                int ldw, uint16_t* __restrict__ out) {
+  const int64_t n_all = (int64_t)N * ldw;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_all; i += (int64_t)gridDim.x * 256) {
+    const int n = (int)(i / ldw), k = (int)(i % ldw);
+    const float v = k < K ? W[(int64_t)n * K + k] : 0.f;
+    uint16_t h, l;
+    split2_f16_scaled(v, h, l);
+    out[i] = h;
+    out[n_all + i] = l;
+  }
+}
+
+}  // namespace
+
+bool gemm_f16s_supports(const GemmArgs& a, int flags) {
+  const int ks = (a.K + 15) / 16;
+  const bool kfit = ks == 4 || ks == 8 || ks == 11 || ks == 12 || ks == 16;
+  const bool fl = flags == kRowNorm || flags == (kBias | kGather) || flags == kBias || flags == 0;
+  return kfit && fl && a.K % 4 == 0 && a.lda % 4 == 0 && reinterpret_cast<uintptr_t>(a.A) % 16 == 0 &&
+         // byte offsets of the buffer resources stay below 2^31
+         (int64_t)2 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31) && (int64_t)kBM * a.ldc * 4 < (1ll << 31);
+}
+
+hipError_t launch_gemm_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, int flags, hipStream_t s) {
+  if (!gemm_f16s_supports(a, flags) || ldwh < a.K || ldwh % 8) return hipErrorInvalidValue;
+  switch (flags) {
+    case 0: return launch_f16s<0>(a, Wh, ldwh, s);
+    case kBias: return launch_f16s<kBias>(a, Wh, ldwh, s);
+    case kRowNorm: return launch_f16s<kRowNorm>(a, Wh, ldwh, s);
+    case kBias | kGather: return launch_f16s<kBias | kGather>(a, Wh, ldwh, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_split_weights_f16(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s) {
+  if (N <= 0 || K <= 0 || ldw < K) return hipErrorInvalidValue;
+  const int64_t n_all = (int64_t)N * ldw;
+  const int grid = (int)std::min<int64_t>((n_all + 255) / 256, 4096);
+  hipLaunchKernelGGL(split_weights_f16_kernel, dim3(grid), dim3(256), 0, s, W, N, K, ldw, out);
+  return hipGetLastError();
+}
+
+}  // namespace tcl

@@ -83,6 +83,18 @@ hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, in
                              hipStream_t s);
 hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s);
 
+// fp32 GEMM on the fp16 matrix cores with two-part operands, fp32-level
+// accuracy (each operand in two fp16 parts after an exact power-of-two
+// scale, three of the four part products accumulated in fp32; per product
+// at most 12 units of fp32 rounding beyond the exact value). Wh holds W's
+// parts as [2][N][ldwh] fp16 (launch_split_weights_f16 or the model's
+// derived weights: W scaled by 2^kF16WeightExp, so |W| < 32). 32-row panels
+// of 128 rows per workgroup, two workgroups per CU; ceil(K / 16) in {4, 8,
+// 11, 12, 16}; flags 0, kBias, kRowNorm or kBias | kGather.
+bool gemm_f16s_supports(const GemmArgs& a, int flags);
+hipError_t launch_gemm_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, int flags, hipStream_t s);
+hipError_t launch_split_weights_f16(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s);
+
 // x_proj with the causal depthwise conv + SiLU in front (split path, 32-row
 // blocks, all N in registers): u = SiLU(b + sum_k w[e,k] x[t-3+k, e]) within
 // each program is computed per 128-channel chunk, stored to u [rows, K] and
@@ -280,7 +292,15 @@ hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, cons
 // master[src2 + c]. With round_bf16 every master value is first rounded to
 // bf16 (bf16 models compute with the rounded weights). The split kinds write
 // the three bf16 parts of the (folded) value to dst as [3][rows][ld].
-enum DeriveKind { kDeriveF32 = 0, kDeriveBF16 = 1, kDeriveFold = 2, kDeriveSplit = 3, kDeriveFoldSplit = 4 };
+enum DeriveKind {
+  kDeriveF32 = 0,
+  kDeriveBF16 = 1,
+  kDeriveFold = 2,
+  kDeriveSplit = 3,        // three bf16 parts
+  kDeriveFoldSplit = 4,
+  kDeriveSplitF16 = 5,     // two fp16 parts of 2^kF16WeightExp W (split2_f16_scaled)
+  kDeriveFoldSplitF16 = 6
+};
 struct DeriveJob {
   int64_t start, src, src2, dst;
   int32_t rows, cols, ld, transpose, kind, pad_;

@@ -105,6 +105,10 @@ struct tcl_model {
     // three-way bf16 splits, [3][rows][cols] (fp32 models on the split path):
     // W_in with the gain folded, W_x, W_out
     uint16_t *W_in_s, *W_x_s, *W_out_s;
+    // two-part fp16 split of W_in with the gain folded, [2][rows][cols]
+    // (fp32 models on the split path), and whether its range allows it
+    uint16_t* W_in_h2;
+    bool in_h2_ok;
   };
   float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1 = nullptr, *W1T = nullptr,
         *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;
@@ -113,11 +117,15 @@ struct tcl_model {
   // the three-way split [3][out][ld] on the split path, ld = in rounded to 8)
   float *We[3] = {nullptr, nullptr, nullptr}, *be[3] = {nullptr, nullptr, nullptr};
   uint16_t* We_s[3] = {nullptr, nullptr, nullptr};
+  uint16_t* We_h2[3] = {nullptr, nullptr, nullptr};  // two-part fp16 splits, [2][out][ld]
+  bool We_h2_ok[3] = {false, false, false};
   // three-layer decoder: W2 [h2][h] and transposed [h][h2], W3 [h2], b3 [1]
   float *W2T = nullptr, *W3 = nullptr, *b3 = nullptr;
   uint16_t* W0_h = nullptr;  // bf16 [d, ldw0_h], K zero-padded to a multiple of 8
   int ldw0_h = 0;
   uint16_t* W0_s = nullptr;  // three-way bf16 split of W0, [3][d][ldw0_h] (split path)
+  uint16_t* W0_h2 = nullptr;  // two-part fp16 split of W0, [2][d][ldw0_h] (split path)
+  bool W0_h2_ok = false;
   bool split = false;        // fp32 model whose projections run on the split path
   std::vector<Layer> layers;
   tcl::Timing timing;

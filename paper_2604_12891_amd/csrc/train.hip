@@ -603,7 +603,7 @@ __global__ __launch_bounds__(256) void derive_kernel(const float* __restrict__ m
     const int r = (int)(k / J.cols), c = (int)(k % J.cols);
     float v = master[J.src + k];
     if (round_bf16) v = round_to_bf16(v);
-    if (J.kind == kDeriveFold || J.kind == kDeriveFoldSplit) {
+    if (J.kind == kDeriveFold || J.kind == kDeriveFoldSplit || J.kind == kDeriveFoldSplitF16) {
       float gv = master[J.src2 + c];
       if (round_bf16) gv = round_to_bf16(gv);
       v = v * gv;
@@ -617,6 +617,13 @@ __global__ __launch_bounds__(256) void derive_kernel(const float* __restrict__ m
       d[o] = (uint16_t)h;
       d[part + o] = (uint16_t)m;
       d[2 * part + o] = (uint16_t)l;
+    } else if (J.kind == kDeriveSplitF16 || J.kind == kDeriveFoldSplitF16) {
+      uint16_t h, l;
+      split2_f16_scaled(v, h, l);
+      uint16_t* d = reinterpret_cast<uint16_t*>(base + J.dst);
+      const int64_t part = (int64_t)(J.transpose ? J.cols : J.rows) * J.ld;
+      d[o] = h;
+      d[part + o] = l;
     } else if (J.kind == kDeriveBF16) {
       reinterpret_cast<uint16_t*>(base + J.dst)[o] = f32_to_bf16(v);
     } else {

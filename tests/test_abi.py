@@ -84,7 +84,7 @@ def test_create_rejects_bad_arguments(lib):
     st, _ = _create(lib, bad, blob)
     assert st == -1
     bad = tb.config_from_shape(wl.TINY)
-    bad.f32_matmul = 2
+    bad.f32_matmul = 3
     st, _ = _create(lib, bad, blob)
     assert st == -1 and b"f32_matmul" in lib.tcl_last_error()
 

@@ -576,6 +576,95 @@ def test_gemm_split_gather(variant):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+# ---------------------------------------------------------------- two-part fp16 split (TCL_F32_MATMUL_SPLIT)
+# Each operand (after an exact power-of-two scale) is h + 2^-11 l + r with
+# |r| <= 2^-22 |x|; three of the four part products are kept. Per product the
+# two r and the dropped 2^-22 l_a l_w add at most 3 * 2^-22 = 12 U of |a w|,
+# so the element bound is the fp32 dot-product bound with 16 more units.
+
+def _f16_ref(A, W, mode, bv=None):
+    A64, W64 = A.astype(np.float64), W.astype(np.float64)
+    K = A.shape[1]
+    ref = A64 @ W64.T
+    bound = (K + 16) * U * (np.abs(A64) @ np.abs(W64).T)
+    if mode == "bias":
+        ref = ref + bv
+        bound = bound + U * np.abs(ref)
+    elif mode == "norm":
+        rstd = 1.0 / np.sqrt(np.mean(A64 * A64, axis=1, keepdims=True) + 1e-5)
+        ref = rstd * ref
+        bound = rstd * bound + (K + 8) * U * np.abs(ref)
+    return ref, bound
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (129, 256, 164), (1000, 1024, 256), (77, 100, 60),
+                                   (300, 48, 128), (40000, 96, 192), (33, 1024, 252)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "norm"])
+def test_gemm_f16split(M, N, K, mode):
+    """The two-part fp16 panels (variant 5): plain, + bias, RMSNorm row scale;
+    ragged M, N and K; rows spanning 10^-30 .. 10^30 in magnitude (10^-15 ..
+    10^15 with the RMSNorm, whose fp32 sum of squares bounds the range as in
+    every fp32 kernel; the per-row power-of-two scale keeps every row inside
+    fp16's range) and one all-zero row."""
+    print(f"gemm f16split mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 3 * N + 17 * K + len(mode) + 5)
+    A = rng.standard_normal((M, K))
+    span = 15 if mode == "norm" else 30
+    A *= 10.0 ** rng.integers(-span, span + 1, size=(M, 1))
+    A[M // 2] = 0.0
+    A = A.astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C = tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, variant=5,
+                      epilogue=2 if mode == "norm" else 0)
+    torch.cuda.synchronize()
+    ref, bound = _f16_ref(A, W, mode, bv)
+    got = C.cpu().numpy()
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got))
+    assert np.all(err <= bound + 1e-300), float(np.max(err / (bound + 1e-300)))
+
+
+def test_gemm_f16split_gather():
+    """The input Linear on the fp16 split path: rows gathered from padded
+    [B, L, F] features by token offsets, + bias; NaN padding never read."""
+    rng = np.random.default_rng(43)
+    B, L, K, N = 37, 25, 164, 256
+    lengths = rng.integers(1, L + 1, B).astype(np.int32)
+    X = np.log1p(rng.lognormal(0.0, 1.0, (B, L, K))).astype(np.float32)
+    for b in range(B):
+        X[b, lengths[b]:] = np.nan
+    W = rng.uniform(-1, 1, (N, K)).astype(np.float32) / np.float32(np.sqrt(K))
+    bv = rng.standard_normal(N).astype(np.float32)
+    offs = _offs(lengths)
+    C = tb.gemm_split(_dev(X), _dev(W), _dev(bv), variant=5, epilogue=3, offs=_dev(offs, torch.int32))
+    torch.cuda.synchronize()
+    ref, bound = _f16_ref(_pack(X, lengths), W, "bias", bv)
+    got = C.cpu().numpy()[:offs[-1]]
+    assert np.all(np.isfinite(got))
+    err = np.abs(got - ref)
+    assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
+
+
+def test_gemm_f16split_error_against_native_fp32():
+    """On the model's in_proj shape (K = 256, unit-scale rows, weights
+    U(+-1/sqrt K)) the two-part fp16 path's rms error against fp64 is within
+    4x of the fp32 matrix cores' (each operand carries 22 of fp32's 24 bits,
+    so a product is off by up to 12 units of fp32 rounding against the fp32
+    kernel's one); both within the element bounds above."""
+    rng = np.random.default_rng(8)
+    M, N, K = 4096, 1024, 256
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.uniform(-1, 1, (N, K)) / np.sqrt(K)).astype(np.float32)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    h = tb.gemm_split(_dev(A), _dev(W), variant=5).cpu().numpy()
+    n = tb.gemm_f32(_dev(A), _dev(W), tile=8).cpu().numpy()
+    e_h = float(np.sqrt(np.mean((h - ref) ** 2)))
+    e_n = float(np.sqrt(np.mean((n - ref) ** 2)))
+    print(f"M={M} N={N} K={K}: rms error fp16 split {e_h:.3e}, native fp32 {e_n:.3e}", flush=True)
+    assert e_h <= 4.0 * e_n
+
+
 def test_gemm_split_error_matches_native_fp32():
     """The split path is as accurate as the fp32 matrix cores: on the model's
     projection shapes its rms error against fp64 stays within 1.5x of the

@@ -38,7 +38,7 @@ def _sample(lengths, n, seed=0):
     return np.array(sorted(idx))
 
 
-@pytest.mark.parametrize("f32_matmul", ["split", "native"])
+@pytest.mark.parametrize("f32_matmul", ["split", "split_bf16", "native"])
 @pytest.mark.parametrize("perturb", [False, True])
 def test_tiny_full_batch(perturb, f32_matmul):
     w = wl.WORKLOADS["score_B64_L25_d64_f32"]
@@ -48,7 +48,7 @@ def test_tiny_full_batch(perturb, f32_matmul):
     assert_scores_match(g, oracle_scores(blob, X, lengths, w.model), "f32", w.name)
 
 
-@pytest.mark.parametrize("f32_matmul", ["split", "native"])
+@pytest.mark.parametrize("f32_matmul", ["split", "split_bf16", "native"])
 def test_headline_full_batch(f32_matmul):
     """The headline round (B = 4096, L = 25), scored whole in the launch
     configuration the benchmark times: every program against the oracle's
@@ -61,7 +61,7 @@ def test_headline_full_batch(f32_matmul):
     assert_scores_match(g, o, "f32", w.name)
 
 
-@pytest.mark.parametrize("f32_matmul", ["split", "native"])
+@pytest.mark.parametrize("f32_matmul", ["split", "split_bf16", "native"])
 def test_headline_shape_perturbed_weights(f32_matmul):
     w = wl.WORKLOADS["score_B4096_L25_d256_f32"]
     blob, X, lengths = wl.make_workload(w.name, B=160, perturb=True)
