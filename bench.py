@@ -26,13 +26,13 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix, TFLOP/s
 BF16_MFMA_PEAK_TFS = 2516.6    # MI355X dense bf16 matrix, TFLOP/s
 # fp32 GEMMs on the split path deliver fp32 results from the 16-bit matrix
-# cores: in_proj and the encoder's Linear layers with two-part fp16 operands
-# (three part products per fp32 product), the others with three-part bf16
-# operands (six). They are reported against the fp32 matrix peak (the
+# cores: in_proj, out_proj and the encoder's Linear layers with two-part fp16
+# operands (three part products per fp32 product); split_bf16 runs them with
+# three-part bf16 operands (six). They are reported against the fp32 matrix peak (the
 # arithmetic they deliver) and, beside it, as the 16-bit matrix-core work they
 # issue against the dense fp16 / bf16 peak (the same 2.5 PFLOP/s).
-F16_SPLIT_KERNELS = ("gemm_input", "gemm_encoder", "gemm_in_proj")
-BF16_SPLIT_KERNELS = ("gemm_out_proj",)
+F16_SPLIT_KERNELS = ("gemm_input", "gemm_encoder", "gemm_in_proj", "gemm_out_proj")
+BF16_SPLIT_KERNELS = ()
 
 
 def split_form(name: str, f32_matmul: str):

@@ -91,14 +91,15 @@ typedef enum tcl_dtype {
  * such as d_inner > 512 for x_proj and out_proj, runs on the fp32 path). */
 typedef enum tcl_f32_matmul {
   TCL_F32_MATMUL_SPLIT = 0,     /* bf16/fp16 matrix cores, fp32-level accuracy:
-                                   in_proj and the encoder's Linear layers take
-                                   both operands in two fp16 parts (after exact
-                                   power-of-two scales; three part products,
-                                   at most 12 units of fp32 rounding each) when
-                                   every weight is below 32 in magnitude; the
-                                   other projections split both operands
-                                   exactly into three bf16 parts (six part
-                                   products, at most 2 units)               */
+                                   in_proj, out_proj and the encoder's Linear
+                                   layers take both operands in two fp16 parts
+                                   (after exact power-of-two scales; three part
+                                   products, at most 12 units of fp32 rounding
+                                   each) when every weight of the matrix is
+                                   below 32 in magnitude; x_proj (and any other
+                                   matrix) splits both operands exactly into
+                                   three bf16 parts (six part products, at most
+                                   2 units)                                 */
   TCL_F32_MATMUL_NATIVE = 1,    /* fp32 matrix cores (v_mfma_f32_*_f32)     */
   TCL_F32_MATMUL_SPLIT_BF16 = 2 /* the three-part bf16 split everywhere      */
 } tcl_f32_matmul;
@@ -490,8 +491,10 @@ TCL_API tcl_status tcl_test_gemm_f32(int32_t M, int32_t N, int32_t K, const floa
  * K <= 512, epilogues 0, 1), 4 (32-row panels with K in two halves on two
  * wavefronts per SIMD, K <= 256, epilogues 0, 2, 3), 5 (the two-part fp16
  * form of TCL_F32_MATMUL_SPLIT: 32-row panels, two workgroups per CU,
- * ceil(K / 16) in {4, 8, 11, 12, 16}, epilogues 0, 2, 3; |W| < 32), -1 what
- * the model would pick among 1-4; TCL_ERR_UNSUPPORTED otherwise.
+ * ceil(K / 16) in {4, 8, 11, 12, 16}, epilogues 0, 2, 3; |W| < 32), 6 (the
+ * same operands with all N <= 256 columns in registers, K <= 512 in chunks of
+ * 128 under a running power-of-two row scale, epilogues 0, 1; |W| < 32), -1
+ * what the model would pick among 1-4; TCL_ERR_UNSUPPORTED otherwise.
  * d_Wsplit: caller-owned device scratch of 3 * N * Kw uint16 (Kw = K rounded
  * up to a multiple of 8, 16-byte aligned) that first receives W's parts
  * (three bf16 parts; variant 5: two fp16 parts of 2^10 W).

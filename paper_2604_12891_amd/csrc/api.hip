@@ -221,7 +221,10 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   GemmArgs go;
   go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
   go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
-  TCL_LAUNCH(T, (tag + "gemm_out_proj").c_str(), model_gemm(m, go, W.W_out_s, E, kResid, s));
+  if (W.W_out_h2 && W.out_h2_ok && gemm_f16acc_supports(go, kResid))
+    TCL_LAUNCH(T, (tag + "gemm_out_proj").c_str(), launch_gemm_f16acc(go, W.W_out_h2, (E + 7) & ~7, kResid, s));
+  else
+    TCL_LAUNCH(T, (tag + "gemm_out_proj").c_str(), model_gemm(m, go, W.W_out_s, E, kResid, s));
   return TCL_OK;
 }
 
@@ -392,7 +395,7 @@ struct ModelPlan {
   int ldw0 = 0;
   struct L {
     size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
-    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_x_s, W_out_s, W_in_h2;
+    size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_x_s, W_out_s, W_in_h2, W_out_h2;
   };
   std::vector<L> layers;
   int ldw0_h = 0;
@@ -424,9 +427,10 @@ ModelPlan plan_model(const tcl_config& c) {
                  size_t src2 = 0) {
     const size_t dst = o;
     const int ldd = ld > 0 ? ld : (transpose ? rows : cols);
-    const int parts = (kind == kDeriveSplit || kind == kDeriveFoldSplit)        ? 3
-                      : (kind == kDeriveSplitF16 || kind == kDeriveFoldSplitF16) ? 2
-                                                                                 : 1;
+    const int parts = (kind == kDeriveSplit || kind == kDeriveFoldSplit) ? 3
+                      : (kind == kDeriveSplitF16 || kind == kDeriveFoldSplitF16 || kind == kDeriveSplitF16Flat)
+                          ? 2
+                          : 1;
     const size_t n_out = parts * (transpose ? (size_t)cols * ldd : (size_t)rows * ldd);
     o = align256(o + n_out * elem_bytes);
     DeriveJob J{};
@@ -485,7 +489,10 @@ ModelPlan plan_model(const tcl_config& c) {
       L.W_x_s = job(B.W_x, XW, E, kDeriveSplit, 0, 2);
       L.W_out_s = job(B.W_out, d, E, kDeriveSplit, 0, 2);
     }
-    if (h2) L.W_in_h2 = job(B.W_in, 2 * E, d, kDeriveFoldSplitF16, 0, 2, (d + 7) & ~7, B.g);
+    if (h2) {
+      L.W_in_h2 = job(B.W_in, 2 * E, d, kDeriveFoldSplitF16, 0, 2, (d + 7) & ~7, B.g);
+      L.W_out_h2 = job(B.W_out, d, E, kDeriveSplitF16Flat, 0, 2, (E + 7) & ~7);
+    }
     P.layers.push_back(L);
   }
   P.g_f = job(bl.g_f, 1, d, kDeriveF32, 0, 4);
@@ -530,8 +537,10 @@ void check_f16_ranges(tcl_model* m, const float* hp) {
   };
   m->W0_h2_ok = fits(bl.W0, bl.enc_dims[1], c.F, nullptr);
   for (int i = 1; i < bl.n_enc; ++i) m->We_h2_ok[i] = fits(bl.We[i], bl.enc_dims[i + 1], bl.enc_dims[i], nullptr);
-  for (int l = 0; l < c.n_layers; ++l)
+  for (int l = 0; l < c.n_layers; ++l) {
     m->layers[l].in_h2_ok = fits(bl.layers[l].W_in, 2 * c.d_inner, c.d_model, hp + bl.layers[l].g);
+    m->layers[l].out_h2_ok = fits(bl.layers[l].W_out, c.d_model, c.d_inner, nullptr);
+  }
 }
 
 tcl_status load_params(tcl_model* m, const float* h_params) {
@@ -681,6 +690,7 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
       W.W_out_s = B16(L.W_out_s);
     }
     W.W_in_h2 = uses_f16_split(*cfg) ? B16(L.W_in_h2) : nullptr;
+    W.W_out_h2 = uses_f16_split(*cfg) ? B16(L.W_out_h2) : nullptr;
     m->layers.push_back(W);
   }
   m->g_f = F32(P.g_f);
@@ -952,8 +962,8 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
     M = B * L;
   }
   if (M <= 0 || N <= 0 || K <= 0 || K % 4) return fail(TCL_ERR_INVALID_ARG, "bad M/N/K");
-  if (variant < -1 || variant > 5 || variant == 0)
-    return fail(TCL_ERR_INVALID_ARG, "variant must be -1, 1, 2, 3, 4 or 5 (got %d)", variant);
+  if (variant < -1 || variant > 6 || variant == 0)
+    return fail(TCL_ERR_INVALID_ARG, "variant must be -1 or 1..6 (got %d)", variant);
   if ((epilogue == 1 || epilogue == 2) && d_bias)
     return fail(TCL_ERR_INVALID_ARG, "bias goes with epilogues 0 and 3 only");
   if (!d_A || !d_W || !d_C || !d_Wsplit) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
@@ -968,6 +978,13 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
   if (epilogue == 3) {
     g.offs = d_offs; g.B = B; g.L = L; g.Mdev = d_offs + B;
     flags = kBias | kGather;
+  }
+  if (variant == 6) {  // the two-part fp16 panels with all N in registers
+    if (!gemm_f16acc_supports(g, flags))
+      return fail(TCL_ERR_UNSUPPORTED, "no fp16 all-N kernel for N=%d K=%d with epilogue %d", N, K, epilogue);
+    TCL_HIP(launch_split_weights_f16(d_W, N, K, Kw, d_Wsplit, s, true));
+    TCL_HIP(launch_gemm_f16acc(g, d_Wsplit, Kw, flags, s));
+    return TCL_OK;
   }
   if (variant == 5) {  // the two-part fp16 panels
     if (!gemm_f16s_supports(g, flags))

@@ -98,5 +98,15 @@ __device__ __forceinline__ void split2_f16_scaled(float v, uint16_t& h, uint16_t
   h = __builtin_bit_cast(uint16_t, hh);
   l = __builtin_bit_cast(uint16_t, ll);
 }
+// The same with the low part unscaled, l = fp16(x - h), for kernels that sum
+// all part products into one accumulator; |r| <= 2^-22 |x| while x - h is
+// in fp16's normal range (|x| >= 2^-3 after the 2^10 scale).
+__device__ __forceinline__ void split2_f16_flat(float v, uint16_t& h, uint16_t& l) {
+  const float x = v * (float)(1 << kF16WeightExp);
+  const _Float16 hh = (_Float16)x;
+  const _Float16 ll = (_Float16)(x - (float)hh);
+  h = __builtin_bit_cast(uint16_t, hh);
+  l = __builtin_bit_cast(uint16_t, ll);
+}
 
 }  // namespace tcl

@@ -62,13 +62,14 @@ __device__ __forceinline__ float pow2f(int e) { return __uint_as_float((uint32_t
 // floor(log2(x)) for a positive normal float (the exponent field); -127 for 0
 __device__ __forceinline__ int exponent_of(float x) { return (int)((__float_as_uint(x) >> 23) & 0xFF) - 127; }
 
-// 8 scaled fp32 values -> their two fp16 parts
+// 8 scaled fp32 values -> their two fp16 parts (FLAT: the low part unscaled)
+template <bool FLAT = false>
 __device__ __forceinline__ void split8_f16(const float* x, f16x8& h, f16x8& l) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const _Float16 hj = (_Float16)x[j];
     h[j] = hj;
-    l[j] = (_Float16)((x[j] - (float)hj) * kF16LowScale);
+    l[j] = FLAT ? (_Float16)(x[j] - (float)hj) : (_Float16)((x[j] - (float)hj) * kF16LowScale);
   }
 }
 
@@ -173,14 +174,12 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
       ss += __shfl_xor(ss, 32, 64);  // the other half of the row
       const float ms = ss / (float)p.K;
       // the scaled row's RMS in [2^8, 2^9): every value below 2^8 * 2 sqrt(K)
-      eA = ms > 0.f ? 8 - exponent_of(sqrtf(ms)) : 0;
-      eA = min(max(eA, -100), 100);
+      eA = ms > 0.f ? min(8 - exponent_of(sqrtf(ms)), 100) : 0;
       f = pow2f(-(eA + kF16WeightExp)) * (1.0f / sqrtf(ms + p.eps));
     } else {
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       // the scaled row's largest value in [2^14, 2^15)
-      eA = mx > 0.f ? 14 - exponent_of(mx) : 0;
-      eA = min(max(eA, -100), 100);
+      eA = mx > 0.f ? min(14 - exponent_of(mx), 100) : 0;
       f = pow2f(-(eA + kF16WeightExp));
     }
     const float sc = pow2f(eA);
@@ -260,6 +259,219 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
   }
 }
 
+// ---------------------------------------------------------------- all N in registers (out_proj)
+// 32-row panels whose accumulators for all N <= 256 columns stay in
+// registers while K (up to 512) is walked in chunks of 128: out_proj with its
+// residual epilogue. With eight blocks of accumulators there is no room for a
+// second set, so the low parts are unscaled (l = fp16(x - h), for A and for W:
+// split2_f16_flat) and all three part products go into one accumulator;
+// x - h stays in fp16's normal range for every value above 2^-17 of the
+// chunk's largest (after its scale), and W's scale puts every weight above
+// 2^-13 there. A row's values are not all known when its first chunk
+// is split, so the row scale runs: chunk c is scaled by 2^e with e the
+// smallest of (14 - the exponent of each chunk's largest value so far), and
+// when e drops the accumulators already holding earlier chunks are
+// multiplied by the power of two between the old and the new scale (exact).
+// Column blocks go in pairs whose MFMAs alternate between the two blocks'
+// accumulators (no MFMA waits for the one before it), one barrier per pair,
+// W staged through a ring of four one-block LDS buffers: the next pair's
+// first block staged a quarter of the way through the pair's k-steps, its
+// second at three quarters.
+template <int KCH, int NB, int FL>
+__global__ __launch_bounds__(kNT, 1) void gemm_f16acc_kernel(GemmArgs p, const uint16_t* Wh, int ldwh) {
+  constexpr int NS = 8;              // 16-k MFMA steps per chunk of 128
+  constexpr int WP = 128 + 8;        // halves per staged W row
+  constexpr int PART = 32 * WP;      // one part of one block buffer
+  constexpr int WU = 16;             // 16-byte units per staged row
+  constexpr int NWU = 2 * 32 * WU;   // units per block (two parts)
+  constexpr int NW = NWU / kNT;      // 4
+  static_assert(NB % 2 == 0 && NB >= 2, "column blocks go in pairs");
+  static_assert((FL & (kRowNorm | kGather)) == 0, "plain, bias and residual GEMMs only");
+
+  __shared__ __attribute__((aligned(16))) uint16_t sW[4 * 2 * PART];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 31, lg = lane >> 5;
+  const int M = p.Mdev ? *p.Mdev : p.Mmax;
+  const int row0 = blockIdx.x * kBM;
+  if (row0 >= M) return;
+  // this workgroup's NB column blocks start at column cb (gridDim.y > 1:
+  // a small batch's columns split over more workgroups)
+  const int cb = blockIdx.y * NB * 32;
+
+  const __amdgpu_buffer_rsrc_t wres = make_rsrc(Wh, (uint32_t)__builtin_amdgcn_readfirstlane(2 * p.N * ldwh * 2));
+  u32x4 wr[NW];
+  auto wload = [&](int n0, int k0) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int u = tid + i * kNT;
+      const int part = u / (32 * WU), n = n0 + (u / WU) % 32, k = k0 + 8 * (u % WU);
+      const bool ok = n < p.N && k < ldwh;
+      const uint32_t off = (uint32_t)(((part * p.N + n) * ldwh + k) * 2) | ((uint32_t)!ok << 31);
+      wr[i] = __builtin_amdgcn_raw_buffer_load_b128(wres, off, 0, 0);
+    }
+  };
+  auto wstage = [&](uint16_t* s) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const int u = tid + i * kNT;
+      *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = wr[i];
+    }
+  };
+  wload(cb, 0);
+  wstage(&sW[0]);
+  wload(cb + 32, 0);
+  wstage(&sW[2 * PART]);
+
+  const int grow = row0 + wave * 32 + li;
+  const bool rok = grow < M;
+  const float* arow = p.A + (rok ? (int64_t)grow * p.lda : 0);
+
+  floatx16 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+  int erun = 100;  // this lane's row's running scale exponent
+
+#pragma unroll
+  for (int c = 0; c < KCH; ++c) {
+    // keep the next chunk's loads of A below this point: hoisted, they would
+    // hold a second chunk in registers
+    __builtin_amdgcn_sched_barrier(0);
+    f16x8 ah[NS], al[NS];
+    {
+      float x[NS][8];
+      float mx = 0.f;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const int k = c * 128 + 16 * s + 8 * lg;
+        const bool ok0 = rok && k < p.K, ok1 = rok && k + 4 < p.K;
+        floatx4 v0 = *reinterpret_cast<const floatx4*>(arow + (ok0 ? k : 0));
+        floatx4 v1 = *reinterpret_cast<const floatx4*>(arow + (ok1 ? k + 4 : 0));
+        if (!ok0) v0 = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (!ok1) v1 = floatx4{0.f, 0.f, 0.f, 0.f};
+        x[s][0] = v0.x; x[s][1] = v0.y; x[s][2] = v0.z; x[s][3] = v0.w;
+        x[s][4] = v1.x; x[s][5] = v1.y; x[s][6] = v1.z; x[s][7] = v1.w;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) mx = fmaxf(mx, fabsf(x[s][j]));
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      // 14 - exponent puts the chunk's largest value in [2^14, 2^15) (at least
+      // -113 for finite values); rows of values below 2^-86 are scaled by 2^100
+      const int ec = mx > 0.f ? min(14 - exponent_of(mx), 100) : 100;
+      const int enew = min(erun, ec);
+      if (c > 0) {
+        // accumulator entry r of this lane is row 8 (r / 4) + 4 lg + r % 4,
+        // whose scale exponents are held by lane (that row) of the wavefront
+        const int dlt = enew - erun;  // <= 0
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+          const float f = pow2f(max(__shfl(dlt, rl, 64), -126));
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) acc[nb][r] *= f;
+        }
+      }
+      erun = enew;
+      const float sc = pow2f(erun);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[s][j] *= sc;
+        split8_f16<true>(x[s], ah[s], al[s]);
+      }
+    }
+#pragma unroll
+    for (int pp = 0; pp < NB / 2; ++pp) {
+      const int g = c * NB + 2 * pp;  // global index of the pair's first block
+      __syncthreads();  // this pair visible; the previous pair's buffers are free
+      const bool more = pp + 1 < NB / 2 || c + 1 < KCH;
+      const int ncol = cb + (pp + 1 < NB / 2 ? (2 * pp + 2) * 32 : 0);
+      const int nk = pp + 1 < NB / 2 ? c * 128 : (c + 1) * 128;
+      if (more) wload(ncol, nk);
+
+      const uint16_t* wb0 = &sW[(g & 3) * 2 * PART + li * WP + 8 * lg];
+      const uint16_t* wb1 = &sW[((g + 1) & 3) * 2 * PART + li * WP + 8 * lg];
+      auto wfrag = [&](const uint16_t* wb, int part, int ks) {
+        return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+      };
+      f16x8 q[2][4];
+      q[0][0] = wfrag(wb0, 0, 0);
+      q[0][1] = wfrag(wb0, 1, 0);
+      q[0][2] = wfrag(wb1, 0, 0);
+      q[0][3] = wfrag(wb1, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x0100, 4, 0);
+      floatx16& x0 = acc[2 * pp];
+      floatx16& x1 = acc[2 * pp + 1];
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks) {
+        if (ks + 1 < NS) {
+          q[(ks + 1) & 1][0] = wfrag(wb0, 0, ks + 1);
+          q[(ks + 1) & 1][1] = wfrag(wb0, 1, ks + 1);
+          q[(ks + 1) & 1][2] = wfrag(wb1, 0, ks + 1);
+          q[(ks + 1) & 1][3] = wfrag(wb1, 1, ks + 1);
+        }
+        const f16x8* w = q[ks & 1];
+        // the small part products first, the large last
+        x0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[ks], w[0], x0, 0, 0, 0);
+        x1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[ks], w[2], x1, 0, 0, 0);
+        x0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[1], x0, 0, 0, 0);
+        x1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[3], x1, 0, 0, 0);
+        x0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[0], x0, 0, 0, 0);
+        x1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[2], x1, 0, 0, 0);
+        if (ks + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
+        if (ks == NS / 4 && more) {
+          wstage(&sW[((g + 2) & 3) * 2 * PART]);
+          __builtin_amdgcn_sched_group_barrier(0x0200, NW, 0);
+          wload(ncol + 32, nk);
+        }
+        if (ks == 3 * NS / 4 && more) {
+          wstage(&sW[((g + 3) & 3) * 2 * PART]);
+          __builtin_amdgcn_sched_group_barrier(0x0200, NW, 0);
+        }
+      }
+    }
+  }
+
+  // epilogue: lane l holds column nb*32 + l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
+  const uint32_t panel_bytes = (uint32_t)(min(kBM, M - row0) * p.ldc * 4);
+  const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
+  const __amdgpu_buffer_rsrc_t rres =
+      make_rsrc((p.R ? p.R : p.C) + (int64_t)row0 * p.ldc, (FL & kResid) != 0 ? panel_bytes : 0);
+  float fr[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+    fr[r] = pow2f(-(__shfl(erun, rl, 64) + kF16WeightExp));
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = cb + nb * 32 + li;
+    const bool cok = col < p.N;
+    const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+    float res[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      res[r] = ((FL & kResid) != 0)
+                   ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rres, off, 0, 0))
+                   : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      float v = fmaf(acc[nb][r], fr[r], bias + res[r]);
+      if (p.relu) v = fmaxf(v, 0.f);
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+    }
+  }
+}
+
 template <int FL>
 hipError_t launch_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, hipStream_t s) {
   const int grid = (a.Mmax + kBM - 1) / kBM;
@@ -286,19 +498,54 @@ hipError_t launch_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, hipStrea
 
 // W -> its two fp16 parts after the 2^10 scale, [2][N][ldw], the padding k >= K zero
 __global__ __launch_bounds__(256) void split_weights_f16_kernel(const float* __restrict__ W, int N, int K,
-                                                                int ldw, uint16_t* __restrict__ out) {
+                                                                int ldw, uint16_t* __restrict__ out, int flat) {
   const int64_t n_all = (int64_t)N * ldw;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n_all; i += (int64_t)gridDim.x * 256) {
     const int n = (int)(i / ldw), k = (int)(i % ldw);
     const float v = k < K ? W[(int64_t)n * K + k] : 0.f;
     uint16_t h, l;
-    split2_f16_scaled(v, h, l);
+    if (flat)
+      split2_f16_flat(v, h, l);
+    else
+      split2_f16_scaled(v, h, l);
     out[i] = h;
     out[n_all + i] = l;
   }
 }
 
 }  // namespace
+
+template <int FL>
+hipError_t launch_f16acc(const GemmArgs& a, const uint16_t* Wh, int ldwh, hipStream_t s) {
+  const int grid = (a.Mmax + kBM - 1) / kBM;
+  if (grid <= 0) return hipSuccess;
+  const int nb = (a.N + 31) / 32;
+  // a batch with fewer panels than two per CU splits the columns over 2 or
+  // 4 workgroups per panel (each repeats its panel's A chunks)
+  const int cs = 512 / grid >= 4 ? 4 : 512 / grid >= 2 ? 2 : 1;
+#define TCL_F16ACC(KCH, NB, CS) \
+  hipLaunchKernelGGL((gemm_f16acc_kernel<KCH, NB, FL>), dim3(grid, CS), dim3(kNT), 0, s, a, Wh, ldwh)
+#define TCL_F16ACC_K(KCH)                                  \
+  if (nb <= 2) TCL_F16ACC(KCH, 2, 1);                      \
+  else if (nb <= 4) {                                      \
+    if (cs >= 2) TCL_F16ACC(KCH, 2, 2);                    \
+    else TCL_F16ACC(KCH, 4, 1);                            \
+  } else {                                                 \
+    if (cs >= 4) TCL_F16ACC(KCH, 2, 4);                    \
+    else if (cs == 2) TCL_F16ACC(KCH, 4, 2);               \
+    else TCL_F16ACC(KCH, 8, 1);                            \
+  }
+  switch ((a.K + 127) / 128) {
+    case 1: TCL_F16ACC_K(1); break;
+    case 2: TCL_F16ACC_K(2); break;
+    case 3: TCL_F16ACC_K(3); break;
+    case 4: TCL_F16ACC_K(4); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef TCL_F16ACC_K
+#undef TCL_F16ACC
+  return hipGetLastError();
+}
 
 bool gemm_f16s_supports(const GemmArgs& a, int flags) {
   const int ks = (a.K + 15) / 16;
@@ -320,11 +567,29 @@ hipError_t launch_gemm_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, int
   }
 }
 
-hipError_t launch_split_weights_f16(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s) {
+bool gemm_f16acc_supports(const GemmArgs& a, int flags) {
+  const bool fl = flags == 0 || flags == kBias || flags == kResid;
+  return fl && a.K % 4 == 0 && a.K <= 512 && a.N >= 1 && a.N <= 256 && a.lda % 4 == 0 &&
+         reinterpret_cast<uintptr_t>(a.A) % 16 == 0 && (int64_t)2 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31) &&
+         (int64_t)kBM * a.ldc * 4 < (1ll << 31);
+}
+
+hipError_t launch_gemm_f16acc(const GemmArgs& a, const uint16_t* Wh, int ldwh, int flags, hipStream_t s) {
+  if (!gemm_f16acc_supports(a, flags) || ldwh < a.K || ldwh % 8) return hipErrorInvalidValue;
+  switch (flags) {
+    case 0: return launch_f16acc<0>(a, Wh, ldwh, s);
+    case kBias: return launch_f16acc<kBias>(a, Wh, ldwh, s);
+    case kResid: return launch_f16acc<kResid>(a, Wh, ldwh, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_split_weights_f16(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s,
+                                    bool flat) {
   if (N <= 0 || K <= 0 || ldw < K) return hipErrorInvalidValue;
   const int64_t n_all = (int64_t)N * ldw;
   const int grid = (int)std::min<int64_t>((n_all + 255) / 256, 4096);
-  hipLaunchKernelGGL(split_weights_f16_kernel, dim3(grid), dim3(256), 0, s, W, N, K, ldw, out);
+  hipLaunchKernelGGL(split_weights_f16_kernel, dim3(grid), dim3(256), 0, s, W, N, K, ldw, out, (int)flat);
   return hipGetLastError();
 }
 

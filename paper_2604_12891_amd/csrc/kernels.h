@@ -93,7 +93,15 @@ hipError_t launch_split_weights(const float* W, int N, int K, int ldw, uint16_t*
 // 11, 12, 16}; flags 0, kBias, kRowNorm or kBias | kGather.
 bool gemm_f16s_supports(const GemmArgs& a, int flags);
 hipError_t launch_gemm_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, int flags, hipStream_t s);
-hipError_t launch_split_weights_f16(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s);
+// The same operands with the low parts unscaled (all three part products in
+// one accumulator), all N <= 256 columns' accumulators in registers and
+// K <= 512 walked in chunks of 128 under a running power-of-two row scale: flags
+// 0, kBias or kResid (out_proj). Wh: launch_split_weights_f16(flat = true).
+bool gemm_f16acc_supports(const GemmArgs& a, int flags);
+hipError_t launch_gemm_f16acc(const GemmArgs& a, const uint16_t* Wh, int ldwh, int flags, hipStream_t s);
+// flat: the low parts unscaled (gemm_f16acc's operand form), else scaled by 2^11
+hipError_t launch_split_weights_f16(const float* W, int N, int K, int ldw, uint16_t* out, hipStream_t s,
+                                    bool flat = false);
 
 // x_proj with the causal depthwise conv + SiLU in front (split path, 32-row
 // blocks, all N in registers): u = SiLU(b + sum_k w[e,k] x[t-3+k, e]) within
@@ -299,7 +307,8 @@ enum DeriveKind {
   kDeriveSplit = 3,        // three bf16 parts
   kDeriveFoldSplit = 4,
   kDeriveSplitF16 = 5,     // two fp16 parts of 2^kF16WeightExp W (split2_f16_scaled)
-  kDeriveFoldSplitF16 = 6
+  kDeriveFoldSplitF16 = 6,
+  kDeriveSplitF16Flat = 7  // the same, low part unscaled (split2_f16_flat)
 };
 struct DeriveJob {
   int64_t start, src, src2, dst;

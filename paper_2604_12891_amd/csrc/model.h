@@ -105,10 +105,10 @@ struct tcl_model {
     // three-way bf16 splits, [3][rows][cols] (fp32 models on the split path):
     // W_in with the gain folded, W_x, W_out
     uint16_t *W_in_s, *W_x_s, *W_out_s;
-    // two-part fp16 split of W_in with the gain folded, [2][rows][cols]
-    // (fp32 models on the split path), and whether its range allows it
-    uint16_t* W_in_h2;
-    bool in_h2_ok;
+    // two-part fp16 splits of W_in (gain folded) and W_out, [2][rows][cols]
+    // (fp32 models on the split path), and whether their ranges allow them
+    uint16_t *W_in_h2, *W_out_h2;
+    bool in_h2_ok, out_h2_ok;
   };
   float *W0 = nullptr, *b0 = nullptr, *g_f = nullptr, *W1 = nullptr, *W1T = nullptr,
         *b1 = nullptr, *W2 = nullptr, *b2 = nullptr;

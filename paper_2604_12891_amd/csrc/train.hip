@@ -617,9 +617,12 @@ __global__ __launch_bounds__(256) void derive_kernel(const float* __restrict__ m
       d[o] = (uint16_t)h;
       d[part + o] = (uint16_t)m;
       d[2 * part + o] = (uint16_t)l;
-    } else if (J.kind == kDeriveSplitF16 || J.kind == kDeriveFoldSplitF16) {
+    } else if (J.kind == kDeriveSplitF16 || J.kind == kDeriveFoldSplitF16 || J.kind == kDeriveSplitF16Flat) {
       uint16_t h, l;
-      split2_f16_scaled(v, h, l);
+      if (J.kind == kDeriveSplitF16Flat)
+        split2_f16_flat(v, h, l);
+      else
+        split2_f16_scaled(v, h, l);
       uint16_t* d = reinterpret_cast<uint16_t*>(base + J.dst);
       const int64_t part = (int64_t)(J.transpose ? J.cols : J.rows) * J.ld;
       d[o] = h;

@@ -647,8 +647,8 @@ def test_gemm_f16split_gather():
 
 
 def test_gemm_f16split_error_against_native_fp32():
-    """On the model's in_proj shape (K = 256, unit-scale rows, weights
-    U(+-1/sqrt K)) the two-part fp16 path's rms error against fp64 is within
+    """On the model's in_proj and out_proj shapes (unit-scale rows, weights
+    U(+-1/sqrt K)) the two-part fp16 paths' rms error against fp64 is within
     4x of the fp32 matrix cores' (each operand carries 22 of fp32's 24 bits,
     so a product is off by up to 12 units of fp32 rounding against the fp32
     kernel's one); both within the element bounds above."""
@@ -663,6 +663,50 @@ def test_gemm_f16split_error_against_native_fp32():
     e_n = float(np.sqrt(np.mean((n - ref) ** 2)))
     print(f"M={M} N={N} K={K}: rms error fp16 split {e_h:.3e}, native fp32 {e_n:.3e}", flush=True)
     assert e_h <= 4.0 * e_n
+    # out_proj's shape on the all-N kernel
+    M, N, K = 4096, 256, 512
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (rng.uniform(-1, 1, (N, K)) / np.sqrt(K)).astype(np.float32)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    h = tb.gemm_split(_dev(A), _dev(W), variant=6).cpu().numpy()
+    n = tb.gemm_f32(_dev(A), _dev(W), tile=9).cpu().numpy()
+    e_h = float(np.sqrt(np.mean((h - ref) ** 2)))
+    e_n = float(np.sqrt(np.mean((n - ref) ** 2)))
+    print(f"M={M} N={N} K={K}: rms error fp16 split {e_h:.3e}, native fp32 {e_n:.3e}", flush=True)
+    assert e_h <= 4.0 * e_n
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 64, 512), (31, 48, 500), (257, 256, 512), (77, 100, 64),
+                                   (200, 256, 128), (65, 40, 256), (40000, 96, 512), (129, 256, 384)])
+@pytest.mark.parametrize("mode", ["plain", "bias", "resid"])
+def test_gemm_f16acc(M, N, K, mode):
+    """The two-part fp16 panels with all N in registers (variant 6: out_proj's
+    kernel): plain, + bias, and the residual epilogue C += A W^T in place;
+    ragged M, N and K; each row's 128-wide K chunks scaled by independent
+    powers of ten between 10^-20 and 10^20, so the running row scale drops
+    (and the accumulators are rescaled) at every kind of chunk boundary."""
+    print(f"gemm f16acc mode={mode} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M + 5 * N + 23 * K + len(mode))
+    A = rng.standard_normal((M, K))
+    nch = (K + 127) // 128
+    A *= np.repeat(10.0 ** rng.integers(-20, 21, size=(M, nch)), 128, axis=1)[:, :K]
+    A[M // 2] = 0.0
+    A = A.astype(np.float32)
+    W = rng.standard_normal((N, K)).astype(np.float32)
+    bv = rng.standard_normal(N).astype(np.float32) if mode == "bias" else None
+    C0 = rng.standard_normal((M, N)).astype(np.float32)
+    C = _dev(C0)
+    tb.gemm_split(_dev(A), _dev(W), _dev(bv) if bv is not None else None, out=C, variant=6,
+                  epilogue=1 if mode == "resid" else 0)
+    torch.cuda.synchronize()
+    ref, bound = _f16_ref(A, W, "bias" if mode == "bias" else "plain", bv)
+    if mode == "resid":
+        ref = ref + C0
+        bound = bound + U * np.abs(ref)
+    got = C.cpu().numpy()
+    assert np.all(np.isfinite(got))
+    err = np.abs(got - ref)
+    assert np.all(err <= bound + 1e-300), float(np.max(err / (bound + 1e-300)))
 
 
 def test_gemm_split_error_matches_native_fp32():
