@@ -47,6 +47,11 @@ def split_form(name: str, f32_matmul: str):
     return None
 
 
+# VALU issue: 256 CUs x 4 SIMDs x 2.4 GHz, one wave64 VALU instruction per 4
+# cycles per SIMD (16 lanes a cycle: the non-packed half of the 157.3 TFLOP/s
+# fp32 vector peak); a transcendental takes two such slots (fitted to the
+# scan's VALU busy cycles, profiles/*_counters.md)
+VALU_SLOT_PEAK_G = 256 * 4 * 2.4 / 4  # 614.4 G wave64 VALU slots/s
 # the paper's end-to-end results (tuning time to reach Tenset-MLP's latency
 # after 2000 trials, section 7.3, Fig. 10): context only, not this metric
 PAPER_CONTEXT = {
@@ -137,6 +142,9 @@ def _roof(name: str, d: dict) -> dict:
             "ms_per_launch": round(d["ms_per_launch"], 5)}
     if "matrix_core" in d:
         roof["matrix_core"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in d["matrix_core"].items()}
+    if "hbm" in d:
+        roof["hbm"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in d["hbm"].items()}
+        roof["alu_note"] = d["alu_note"]
     if "peak_note" in d:
         roof["peak_note"] = d["peak_note"]
     return roof
@@ -159,6 +167,38 @@ def measured_traffic(workload: str) -> dict:
             if os.path.exists(f) and hashlib.sha256(open(f, "rb").read()).hexdigest()[:16] == digest:
                 out[cat] = nbytes
     return out
+
+
+def measured_valu_slots(workload: str) -> dict:
+    """VALU issue slots per valid token of a kernel (SQ_INSTS_VALU plus one more
+    per transcendental), from the committed counter summary of this workload,
+    while the kernel's source file still has the hash recorded with them."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{workload}_counters.md")
+    out = {}
+    if not os.path.exists(path):
+        return out
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 5 and parts[0] == "valu_slots_per_token:":
+            cat, slots, src, digest = parts[1], float(parts[2]), parts[3], parts[4]
+            f = os.path.join(ROOT, "paper_2604_12891_amd", "csrc", src)
+            if os.path.exists(f) and hashlib.sha256(open(f, "rb").read()).hexdigest()[:16] == digest:
+                out[cat] = slots
+    return out
+
+
+def alu_entry(hbm_entry: dict, slots: float, ms_per_launch: float) -> dict:
+    """A VALU-issue-bound kernel: its counted issue slots per launch over its
+    duration against the issue peak, with its HBM rate beside it."""
+    achieved = slots / (ms_per_launch * 1e-3) / 1e9
+    return {"bound": "alu", "achieved": achieved, "peak": VALU_SLOT_PEAK_G, "unit": "G VALU slots/s",
+            "frac": achieved / VALU_SLOT_PEAK_G,
+            "hbm": {"achieved": hbm_entry["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": hbm_entry["frac"]},
+            "alu_note": "wave64 VALU instructions per launch (rocprofv3 SQ_INSTS_VALU, transcendentals "
+                        "counted twice) over the launch's duration, against 256 CUs x 4 SIMDs x 2.4 GHz / 4 "
+                        "cycles per instruction"}
 
 
 def cpu_baseline(w, blob, X, lengths, target_s: float) -> dict:
@@ -592,6 +632,77 @@ def scan_sweep(args):
                       "lengths": "uniform 64..256"}), flush=True)
 
 
+def other_workloads(args) -> dict:
+    """The other configurations, timed the same way on the same GPU in the
+    same run (warmup, then events around K steps on the current stream):
+    programs/s of the small, the large bf16 and the long-sequence scoring
+    workloads, and steps/s of the distillation step on both objectives.
+    Parity of each is in the GPU tests; these are their rates."""
+    import numpy as np
+    import torch
+
+    from paper_2604_12891_amd import binding as tb
+    from paper_2604_12891_amd import workload as wl
+
+    dev = torch.device("cuda:0")
+    steps, warmup = max(5, args.steps // 4), max(2, args.warmup // 2)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    out = {}
+    for name in ("score_B64_L25_d64_f32", "score_B65536_L25_d256_bf16", "score_B8192_L256_d256_f32"):
+        w = wl.WORKLOADS[name]
+        blob, X, lengths = wl.make_workload(name)
+        model = tb.CostModel(tb.config_from_shape(w.model, w.dtype, args.f32_matmul), blob)
+        Xd, Ld = torch.from_numpy(X).to(dev), torch.from_numpy(lengths).to(dev)
+        del X
+        ws = model.workspace(w.B, w.L)
+        o = torch.empty(w.B, dtype=torch.float32, device=dev)
+        ms = timed(lambda: model.score(Xd, Ld, out=o, workspace=ws))
+        assert torch.isfinite(o).all().item()
+        out[name] = {"value": w.B / (ms * 1e-3), "unit": "programs/s", "ms_per_step": ms, "dtype": w.dtype,
+                     "B": w.B, "L": w.L, "valid_tokens": int(lengths.sum()), "steps": steps}
+        del model, Xd, Ld, ws, o
+        torch.cuda.empty_cache()
+    w = wl.WORKLOADS["distill_B1024_L25_t256_s128_bf16"]
+    (tblob, sblob), X, lengths = wl.make_workload(w.name)
+    Xd, Ld = torch.from_numpy(X).to(dev), torch.from_numpy(lengths).to(dev)
+    teacher = tb.CostModel(tb.config_from_shape(w.model, w.dtype), tblob)
+    Yd = (teacher.score(Xd, Ld) + torch.from_numpy(wl.label_noise(w.B)).to(dev)).contiguous()
+    krng = np.random.default_rng(12891)
+    fisher = torch.from_numpy(krng.random(sblob.size).astype(np.float32)).to(dev)
+    theta_prev = torch.from_numpy((sblob + 1e-3 * krng.standard_normal(sblob.size)).astype(np.float32)).to(dev)
+    for objective in ("mse", "kd"):
+        student = tb.CostModel(tb.config_from_shape(w.student, w.dtype), sblob)
+        tr = tb.Trainer(teacher, student, lr=1e-3, max_B=w.B, max_L=w.L)
+        ws = tr.workspace(w.B, w.L)
+        loss = torch.empty(4, dtype=torch.float32, device=dev)
+        if objective == "kd":
+            fn = lambda: tr.step_kd(Xd, Ld, Yd, beta=0.5, phi=0.7, sigma=1.0, ewc_lambda=1e4, fisher=fisher,
+                                    theta_prev=theta_prev, loss=loss, workspace=ws)
+        else:
+            fn = lambda: tr.step(Xd, Ld, Yd, loss=loss[:3], workspace=ws)
+        ms = timed(fn)
+        assert torch.isfinite(loss[:3]).all().item()
+        out[f"{w.name}:{objective}"] = {"value": 1e3 / ms, "unit": "steps/s", "ms_per_step": ms, "dtype": w.dtype,
+                                        "B": w.B, "L": w.L, "steps": steps,
+                                        "objective": "mse(s, teacher) + mse(s, labels)" if objective == "mse" else
+                                        "Eq. (9): beta 0.5, phi 0.7, LambdaRank terms, EWC lambda 1e4"}
+        tr.close()
+        del student, tr, ws
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -615,6 +726,8 @@ def main():
                     help="fp32 models: projections on the 16-bit matrix cores with split operands (two-part "
                          "fp16 where the shape allows, else three-part bf16; split_bf16: three-part bf16 "
                          "everywhere), or on the fp32 matrix cores")
+    ap.add_argument("--no-others", action="store_true",
+                    help="with the headline workload, skip timing the other configurations")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run 3 elementwise passes over 256 MiB (known bytes for HBM counters)")
     args = ap.parse_args()
@@ -697,6 +810,7 @@ def main():
     ms_h2d = e2.elapsed_time(e3) / args.steps
 
     work = kernel_work(w.model, M_v, w.B, w.dtype, w.L)
+    valu_slots = measured_valu_slots(w.name)
 
     def timed_pass(streams: int):
         """The same K steps with every kernel bracketed by events on its
@@ -720,6 +834,8 @@ def main():
             parts = max(1, round(n / args.steps / expected_launches(name, w.model)))
             amount = tuple(a / parts for a in amount) if isinstance(amount, tuple) else amount / parts
             e = roofline_entry(kind, amount, per, w.dtype, split_form(name, args.f32_matmul) if split else None)
+            if name in valu_slots:
+                e = alu_entry(e, valu_slots[name] * M_v / parts, per)
             e.update({"ms_per_launch": per, "launches_per_step": n // args.steps,
                       "ms_per_step": tot / args.steps, "work_per_launch": amount, "work_unit": kind})
             kernels[name] = e
@@ -732,7 +848,8 @@ def main():
                   f"{'frac':>6s}", file=sys.stderr)
             for k, e in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
                 extra = (f"  ({e['matrix_core']['dtype']} matrix cores {e['matrix_core']['frac']:.3f})"
-                         if "matrix_core" in e else "")
+                         if "matrix_core" in e else
+                         f"  (HBM {e['hbm']['achieved']:.0f} GB/s = {e['hbm']['frac']:.3f})" if "hbm" in e else "")
                 print(f"{k:16s} {e['ms_per_step']:9.4f} {e['ms_per_launch']:10.5f} {e['achieved']:10.2f} "
                       f"{e['unit']:8s} {e['frac']:6.3f}{extra}", file=sys.stderr)
         return kernels, roof
@@ -754,6 +871,10 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, blob, X, lengths, args.cpu_seconds)
+    others = None
+    if w.name == "score_B4096_L25_d256_f32" and not args.no_others:
+        del Xh, Lh
+        others = other_workloads(args)
 
     rec = {
         "metric": METRIC if w.name == "score_B4096_L25_d256_f32" else
@@ -788,6 +909,7 @@ def main():
                          "note": "features copied from pinned host memory on the scoring stream before every "
                                  "step; context only, value excludes it"},
         "cpu_baseline": cpu,
+        "other_workloads": others,
         "paper_context": PAPER_CONTEXT,
     }
     print(json.dumps(rec), flush=True)
