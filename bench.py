@@ -380,6 +380,9 @@ def bench_progressive(args, w):
                    "d_state": w.model.d_state, "n_layers": w.model.n_layers,
                    "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v},
         "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
+        "graph_replay": {"ms_per_step": ms_graph, "steps_per_s": 1000.0 / ms_graph,
+                         "vs_launched": ms / ms_graph,
+                         "note": "the same step captured into one HIP graph (stream capture) and replayed"},
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
                     for k, e in kernels.items()},
         "cpu_baseline": cpu,
@@ -435,6 +438,23 @@ def bench_distill(args, w):
     wall = time.perf_counter() - t0
     ms = e0.elapsed_time(e1) / args.steps
     assert torch.isfinite(loss).all().item(), "non-finite loss"
+
+    # the same step captured once into a HIP graph and replayed K times (each
+    # replay is one more step): what launching ~90 kernels one by one costs
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        one_step()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_graph = e0.elapsed_time(e1) / args.steps
+    assert torch.isfinite(loss).all().item(), "non-finite loss after graph replays"
+    del graph
 
     tr.timing(True)
     teacher.timing(True)
@@ -503,6 +523,9 @@ def bench_distill(args, w):
                    "objective": ("beta 0.5 LambdaRank(s; labels) + 0.5 phi LambdaRank(s; teacher) + EWC "
                                  "(lambda 1e4), phi 0.7" if kd else "mse(s, teacher) + mse(s, labels)")},
         "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
+        "graph_replay": {"ms_per_step": ms_graph, "steps_per_s": 1000.0 / ms_graph,
+                         "vs_launched": ms / ms_graph,
+                         "note": "the same step captured into one HIP graph (stream capture) and replayed"},
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
                     for k, e in kernels.items()},
         "cpu_baseline": cpu,
@@ -709,7 +732,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="score_B4096_L25_d256_f32")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget")
+    ap.add_argument("--cpu-seconds", type=float, default=22.0, help="oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernels", action="store_true", help="print the per-kernel table to stderr")
     ap.add_argument("--scan-sweep", action="store_true",

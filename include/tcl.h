@@ -263,7 +263,12 @@ TCL_API size_t tcl_distill_workspace_bytes(const tcl_trainer* trainer, int32_t B
  * runs on the teacher model's first stream, forked from `stream` and joined
  * back before the loss by events, beside the student's forward; the step is
  * ordered on `stream` as a whole, and calls that use the teacher model must
- * not be issued from several host threads at once. */
+ * not be issued from several host threads at once.
+ * The step may be captured into a HIP graph on `stream` (stream capture)
+ * once a step of the same (B, L) has run uncaptured, with per-kernel timing
+ * off on the trainer and the teacher (else TCL_ERR_INVALID_ARG); each replay
+ * is one more step: Adam's step count is kept on the device. Replays must
+ * not overlap other steps or calls that use the teacher model. */
 TCL_API tcl_status tcl_distill_step(tcl_trainer* trainer, int32_t B, int32_t L, const float* d_feats,
                                     const int32_t* d_lengths, const float* d_labels, float* d_loss,
                                     void* d_workspace, size_t ws_bytes, void* stream);

@@ -314,8 +314,9 @@ struct DeriveJob {
   int64_t start, src, src2, dst;
   int32_t rows, cols, ld, transpose, kind, pad_;
 };
+// step_bump (may be null): a training step's device step count, advanced by one
 hipError_t launch_derive(const float* master, const DeriveJob* d_jobs, int njobs, int64_t total,
-                         void* base, int round_bf16, hipStream_t s);
+                         void* base, int round_bf16, hipStream_t s, int64_t* step_bump = nullptr);
 
 hipError_t launch_rmsnorm_fwd(int d, int Mmax, const int* Mdev, const float* H, const float* g,
                               float eps, uint16_t* n, float* rstd, hipStream_t s);
@@ -394,7 +395,8 @@ hipError_t launch_conv_bwd(int B, int E, int K, const int* offs, const uint16_t*
 int colsum_splits(int Mmax);
 hipError_t launch_colsum(const int* Mdev, int Mmax, const float* A, int64_t lda, int C, int splits,
                          float* part, hipStream_t s);
+// d_step: the steps taken before this one (device), for the bias correction
 hipError_t launch_adam(int64_t n, float* p, float* m, float* v, const float* g, float lr, float b1,
-                       float b2, float eps, float bc1, float bc2, hipStream_t s);
+                       float b2, float eps, const int64_t* d_step, hipStream_t s);
 
 }  // namespace tcl

@@ -568,10 +568,16 @@ __global__ __launch_bounds__(64 * kRedGroups) void reduce_kernel(const ReduceJob
 }
 
 // ---------------------------------------------------------------- Adam
+// Bias correction from the step count on the device (the steps already
+// taken, before this one), so that a captured step replays with the right
+// correction: bc_k = 1 - beta_k^t for t = *d_step + 1.
 __global__ __launch_bounds__(256) void adam_kernel(int64_t n, float* __restrict__ p,
                                                    float* __restrict__ m, float* __restrict__ v,
                                                    const float* __restrict__ g, float lr, float b1,
-                                                   float b2, float eps, float bc1, float bc2) {
+                                                   float b2, float eps, const int64_t* __restrict__ d_step) {
+  const double t = (double)(*d_step + 1);
+  const float bc1 = 1.0f - (float)pow((double)b1, t);
+  const float bc2 = 1.0f - (float)pow((double)b2, t);
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
     const float gi = g[i];
     const float mi = fmaf(b1, m[i], (1.0f - b1) * gi);
@@ -590,7 +596,10 @@ __device__ __forceinline__ float round_to_bf16(float f) { return bf16_to_f32(f32
 __global__ __launch_bounds__(256) void derive_kernel(const float* __restrict__ master,
                                                      const DeriveJob* __restrict__ jobs, int njobs,
                                                      int64_t total, uint8_t* __restrict__ base,
-                                                     int round_bf16) {
+                                                     int round_bf16, int64_t* __restrict__ step_bump) {
+  // after a training step's Adam (the previous kernel on the stream, done
+  // reading the count): advance the step count
+  if (step_bump && blockIdx.x == 0 && threadIdx.x == 0) *step_bump += 1;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
        idx += (int64_t)gridDim.x * 256) {
     int lo = 0, hi = njobs;
@@ -774,18 +783,18 @@ hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, cons
 }
 
 hipError_t launch_adam(int64_t n, float* p, float* m, float* v, const float* g, float lr, float b1,
-                       float b2, float eps, float bc1, float bc2, hipStream_t s) {
+                       float b2, float eps, const int64_t* d_step, hipStream_t s) {
   const int grid = (int)std::min<int64_t>((n + 255) / 256, 2048);
-  hipLaunchKernelGGL(adam_kernel, dim3(grid), dim3(256), 0, s, n, p, m, v, g, lr, b1, b2, eps, bc1, bc2);
+  hipLaunchKernelGGL(adam_kernel, dim3(grid), dim3(256), 0, s, n, p, m, v, g, lr, b1, b2, eps, d_step);
   return hipGetLastError();
 }
 
 hipError_t launch_derive(const float* master, const DeriveJob* d_jobs, int njobs, int64_t total,
-                         void* base, int round_bf16, hipStream_t s) {
+                         void* base, int round_bf16, hipStream_t s, int64_t* step_bump) {
   if (total <= 0) return hipSuccess;
   const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
   hipLaunchKernelGGL(derive_kernel, dim3(grid), dim3(256), 0, s, master, d_jobs, njobs, total,
-                     static_cast<uint8_t*>(base), round_bf16);
+                     static_cast<uint8_t*>(base), round_bf16, step_bump);
   return hipGetLastError();
 }
 

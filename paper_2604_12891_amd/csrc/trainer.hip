@@ -22,7 +22,7 @@ struct tcl_trainer {
   tcl_model* teacher = nullptr;
   tcl_model* student = nullptr;
   float lr = 1e-3f, beta1 = 0.9f, beta2 = 0.999f, eps = 1e-8f;
-  int64_t step = 0;
+  int64_t* d_step = nullptr;  // steps taken (device): Adam's bias correction
   int max_B = 0, max_L = 0;
   void* dev = nullptr;  // gradient blob, Adam moments, reduction table
   float *grad = nullptr, *m = nullptr, *v = nullptr;
@@ -175,8 +175,11 @@ std::vector<ReduceJob> reduce_jobs(const tcl_trainer* tr, const TrainPlan& P, in
   return J;
 }
 
-tcl_status ensure_plan(tcl_trainer* tr, int B, int L, const TrainPlan& P) {
+tcl_status ensure_plan(tcl_trainer* tr, int B, int L, const TrainPlan& P, bool capturing) {
   if (tr->plan_B == B && tr->plan_L == L) return TCL_OK;
+  if (capturing)
+    return fail(TCL_ERR_INVALID_ARG, "a step with a new (B, L) = (%d, %d) cannot be captured: run one "
+                "step of that shape first", B, L);
   const std::vector<ReduceJob> J = reduce_jobs(tr, P, B);
   if ((int)J.size() > tr->max_jobs) return fail(TCL_ERR_UNSUPPORTED, "too many reduction jobs");
   // the table changes only with the batch shape; the copy waits for
@@ -226,7 +229,7 @@ TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, fl
   tr->max_L = max_L;
   tr->max_jobs = 64 + 16 * sc.n_layers;
   const size_t n = student->n_params;
-  const size_t bytes = align256(n * 4) * 3 + align256((size_t)tr->max_jobs * sizeof(ReduceJob));
+  const size_t bytes = align256(n * 4) * 3 + align256((size_t)tr->max_jobs * sizeof(ReduceJob)) + 256;
   if (hipMalloc(&tr->dev, bytes) != hipSuccess) {
     delete tr;
     return fail(TCL_ERR_OOM, "hipMalloc of %zu bytes for the trainer failed", bytes);
@@ -236,6 +239,8 @@ TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, fl
   tr->m = reinterpret_cast<float*>(base + align256(n * 4));
   tr->v = reinterpret_cast<float*>(base + 2 * align256(n * 4));
   tr->d_jobs = reinterpret_cast<ReduceJob*>(base + 3 * align256(n * 4));
+  tr->d_step = reinterpret_cast<int64_t*>(base + 3 * align256(n * 4) +
+                                          align256((size_t)tr->max_jobs * sizeof(ReduceJob)));
   if (hipMemset(tr->dev, 0, bytes) != hipSuccess) {
     (void)hipFree(tr->dev);
     delete tr;
@@ -288,10 +293,16 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   const TrainPlan P = plan_step(tr, B, L);
   if (ws_bytes < P.total)
     return fail(TCL_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, P.total);
-  tcl_status st = ensure_plan(tr, B, L, P);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // a step may be captured into a graph on `stream` once its shape has run
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  TCL_HIP(hipStreamIsCapturing(s, &cap));
+  const bool capturing = cap != hipStreamCaptureStatusNone;
+  if (capturing && (tr->timing.on || tr->teacher->timing.on))
+    return fail(TCL_ERR_INVALID_ARG, "per-kernel timing is on: a timed step cannot be captured");
+  tcl_status st = ensure_plan(tr, B, L, P, capturing);
   if (st != TCL_OK) return st;
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(d_ws);
   auto F32 = [&](size_t off) { return reinterpret_cast<float*>(ws + off); };
   auto B16 = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
@@ -459,12 +470,12 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   if (kd)  // EWC on the master weights: gradient and loss[3] (zero when lambda = 0)
     TCL_LAUNCH(T, "ewc", launch_ewc((int64_t)S->n_params, S->master, kd->d_theta_prev, kd->d_fisher,
                                     kd->ewc_lambda, tr->grad, F32(P.ewc_part), d_loss, s));
-  tr->step += 1;
-  const float bc1 = 1.0f - (float)std::pow((double)tr->beta1, (double)tr->step);
-  const float bc2 = 1.0f - (float)std::pow((double)tr->beta2, (double)tr->step);
+  // the step count lives on the device (Adam reads it, derive advances it),
+  // so that a captured step replays as a fresh one
   TCL_LAUNCH(T, "adam", launch_adam((int64_t)S->n_params, S->master, tr->m, tr->v, tr->grad, tr->lr,
-                                    tr->beta1, tr->beta2, tr->eps, bc1, bc2, s));
-  TCL_LAUNCH(T, "derive", launch_derive(S->master, S->jobs, S->njobs, S->derive_total, S->dev, 1, s));
+                                    tr->beta1, tr->beta2, tr->eps, tr->d_step, s));
+  TCL_LAUNCH(T, "derive", launch_derive(S->master, S->jobs, S->njobs, S->derive_total, S->dev, 1, s,
+                                        tr->d_step));
   return TCL_OK;
 }
 
