@@ -295,12 +295,15 @@ hipError_t dispatch_tile(const GemmArgsBF16& a, GemmBF16Tile tile, hipStream_t s
 GemmBF16Tile pick_gemm_bf16_tile(GemmBF16Kind kind, int Mmax, int N, int K) {
   // Measured on MI355X (microseconds per call, ~983K rows unless noted):
   // in_proj (RMSNorm, N = 1024, K = 256) row panels 923 vs 1489 for the best
-  // tile; gathered input Linear (N = 256, K = 164) 128-row panels 376 vs 391
-  // for 256-row ones and 591 for the best tile; out_proj (K = 512, no panel)
-  // 128x128 629; x_proj (N = 48) 64x64 227. At ~15K rows (distillation)
-  // 128x64 wins for N <= 256 (7.2 vs 9.4 at N = 128, 11.9 vs 13.5 at 256).
+  // tile, and at 492K rows 128-row panels (whole-line bf16 stores) 448 vs
+  // 496 for 256-row ones; gathered input Linear (N = 256, K = 164) 128-row
+  // panels 376 vs 391 for 256-row ones and 591 for the best tile; out_proj
+  // (K = 512, no panel) 128x128 629; x_proj (N = 48) 64x64 227. At ~15K rows
+  // (distillation) 128x64 wins for N <= 256 (7.2 vs 9.4 at N = 128, 11.9 vs
+  // 13.5 at 256).
   if (N <= 64) return kB64x64;
-  if (K <= 256 && Mmax >= 131072) return kind == kInputF32toF32 ? kBPanel128 : kBPanel;
+  if (K <= 256 && Mmax >= 131072)
+    return kind == kInputF32toF32 || kind == kNormF32toBF16 || kind == kBF16toBF16 ? kBPanel128 : kBPanel;
   if (Mmax < 131072 && N <= 256) return kB128x64;
   return kB128x128;
 }

@@ -46,6 +46,7 @@ constexpr int cmax(int a, int b) { return a > b ? a : b; }
 // branches, and the compiler can count outstanding memory operations exactly.
 constexpr uint32_t kBufferFlags = 0x00020000;  // 32-bit data format, raw (stride 0)
 constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every resource used here
+constexpr int kStoreNT = 2;  // cache-policy bits of a buffer store: non-temporal
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferFlags);
@@ -68,7 +69,12 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
   static_assert(!kNorm || kF32A, "RMSNorm prologue needs the fp32 residual stream");
   constexpr int PK = kF32A ? 32 : 64;   // k per prologue piece (128 bytes of an A row)
   constexpr int KPIECES = KC * 64 / PK;
-  constexpr int CP = 36;                // fp32 pitch of the output stage (conflict-free both ways)
+  // bf16 rows of one 32-column step are 64 bytes, half a 128-byte line; with
+  // one row block per wavefront (registers to spare) two steps are stored
+  // together, as whole lines
+  constexpr int SPS = (!kF32C && MB == 1) ? 2 : 1;  // steps per store
+  constexpr int CW = 32 * SPS;          // columns per store
+  constexpr int CP = CW + 4;            // fp32 pitch of the output stage (conflict-free both ways)
   constexpr int APITCH = PK + 8;        // bf16 pitch of the A stage (80 or 144 B: conflict-free fragment reads)
   constexpr int kStageA = 32 * APITCH * 2;
   constexpr int kStageC = RW * CP * 4;
@@ -222,13 +228,13 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
   const __amdgpu_buffer_rsrc_t rres = make_rsrc(
       (p.R ? p.R : reinterpret_cast<const float*>(p.C)) + ((FL & kResid) != 0 ? (int64_t)row0 * p.ldc : 0),
       (FL & kResid) != 0 ? panel_bytes : 0);
+  floatx16 acc[MB], accp[MB];  // this step's accumulators, and the group's previous step's
   for (int s = 0; s < nsteps; ++s) {
     const int buf = s & 1, n0 = s * 32;
     stage_w(buf);
     __syncthreads();  // W step s visible; every wavefront is past step s-1's reads of this buffer's pair
     if (s + 1 < nsteps) gload_w(n0 + 32);
 
-    floatx16 acc[MB];
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -257,18 +263,31 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
       }
     }
 
-    // epilogue: accumulator layout (lane l: column l % 32, rows
-    // 8*(r/4) + 4*(l/32) + (r%4)) -> fp32 row-major stage -> each lane
-    // finishes 8 consecutive columns of 4 rows: row scale, bias, residual,
-    // conversion, 16-byte stores
+    // epilogue, after the last step of each group of SPS: accumulator layout
+    // (lane l: column l % 32, rows 8*(r/4) + 4*(l/32) + (r%4)) -> fp32
+    // row-major stage -> each lane finishes 8 consecutive columns of its
+    // rows: row scale, bias, residual, conversion, 16-byte stores
+    const int g0 = s - s % SPS;  // first step of this group
+    if (s != g0 + SPS - 1 && s + 1 < nsteps) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) accp[mb] = acc[mb];
+      continue;
+    }
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) stC[(mb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3)) * CP + li] = acc[mb][r];
+      for (int r = 0; r < 16; ++r) {
+        const int row = mb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+        if (s > g0) stC[row * CP + li] = accp[mb][r];
+        stC[row * CP + 32 * (s - g0) + li] = acc[mb][r];
+      }
     wave_lds_order();
-    const int u = lane & 3;  // 8-column unit of this lane (the same for all its rows)
-    const int c0 = n0 + 8 * u;
-    const bool ok0 = c0 < p.N, ok1 = c0 + 4 < p.N;  // N % 4 == 0: halves are all in or all out
+    constexpr int LPR = CW / 8;          // lanes per row
+    constexpr int RPI = 64 / LPR;        // rows per store instruction
+    const int u = lane % LPR;  // 8-column unit of this lane (the same for all its rows)
+    const int c0 = g0 * 32 + 8 * u;
+    const bool staged = 8 * u < 32 * (s - g0 + 1);  // a group cut short by the last step
+    const bool ok0 = staged && c0 < p.N, ok1 = staged && c0 + 4 < p.N;  // N % 4 == 0: halves are all in or all out
     floatx4 b0 = floatx4{0.f, 0.f, 0.f, 0.f}, b1 = b0;
     if constexpr ((FL & kBias) != 0) {
       const floatx4 x0 = *reinterpret_cast<const floatx4*>(p.bias + (ok0 ? c0 : 0));
@@ -277,8 +296,8 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
       if (ok1) b1 = x1;
     }
 #pragma unroll
-    for (int i = 0; i < RW / 16; ++i) {
-      const int rl = (lane >> 2) + 16 * i;
+    for (int i = 0; i < RW / RPI; ++i) {
+      const int rl = lane / LPR + RPI * i;
       const int prow = wave * RW + rl;  // row within the panel; rows past M fall outside cres
       floatx4 v0 = *reinterpret_cast<const floatx4*>(&stC[rl * CP + 8 * u]);
       floatx4 v1 = *reinterpret_cast<const floatx4*>(&stC[rl * CP + 8 * u + 4]);
@@ -299,9 +318,10 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v0), cres, o0, 0, 0);
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v1), cres, o1, 0, 0);
       } else {
-        // N % 8 == 0 for bf16 C: a unit is all in or all out
+        // N % 8 == 0 for bf16 C: a unit is all in or all out; stored
+        // non-temporal (a streamed output, re-read only by the next kernel)
         const u32x4 w = u32x4{pack2(v0.x, v0.y), pack2(v0.z, v0.w), pack2(v1.x, v1.y), pack2(v1.z, v1.w)};
-        __builtin_amdgcn_raw_buffer_store_b128(w, cres, ok0 ? off : kOutOfRange, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(w, cres, ok0 ? off : kOutOfRange, 0, kStoreNT);
       }
     }
     wave_lds_order();

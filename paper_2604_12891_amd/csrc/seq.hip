@@ -80,6 +80,26 @@ __device__ __forceinline__ void st1(uint16_t* p, float v) { *p = f32_to_bf16(v);
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// One element per lane of row `row` of a buffer of rows: the lane's byte
+// offset is fixed, the row's is wave-uniform (scalar), so a sequential
+// kernel walking rows spends no vector instruction on addresses.
+__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t lane_bytes, uint32_t row_bytes,
+                                        const float*) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, lane_bytes, row_bytes, 0));
+}
+__device__ __forceinline__ uint16_t buf_ld(__amdgpu_buffer_rsrc_t r, uint32_t lane_bytes, uint32_t row_bytes,
+                                           const uint16_t*) {
+  return __builtin_amdgcn_raw_buffer_load_b16(r, lane_bytes, row_bytes, 0);
+}
+__device__ __forceinline__ void buf_st(float v, __amdgpu_buffer_rsrc_t r, uint32_t lane_bytes,
+                                       uint32_t row_bytes, float*) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, lane_bytes, row_bytes, 0);
+}
+__device__ __forceinline__ void buf_st(float v, __amdgpu_buffer_rsrc_t r, uint32_t lane_bytes,
+                                       uint32_t row_bytes, uint16_t*) {
+  __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(v), r, lane_bytes, row_bytes, 0);
+}
+
 // CH adjacent channels per thread: one 16-byte access (4 fp32 or 8 bf16).
 template <typename T> struct Vec;
 template <> struct Vec<float> {
@@ -245,19 +265,18 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
     for (int i = threadIdx.x; i < nt * XW; i += kScanThreads) sX[i] = src[i];
     __syncthreads();
     if (!active) continue;
-    // u and z of the next token are loaded while this token is computed;
-    // they stay in their storage type until used, so that converting them
-    // does not wait for the load
-    T un = u[(int64_t)(base + t0) * E + e];
-    T zn = z[(int64_t)(base + t0) * ldz + e];
-    for (int tt = 0; tt < nt; ++tt) {
-      const int64_t row = base + t0 + tt;
+    // this chunk's rows of u, z, out and ysave as buffers: row offsets stay
+    // scalar (each resource spans at most kScanTC rows, so 32 bits suffice)
+    const int64_t r0 = base + t0;
+    const __amdgpu_buffer_rsrc_t ub = raw_rsrc(u + r0 * E, (uint32_t)(nt * E * sizeof(T)));
+    const __amdgpu_buffer_rsrc_t zb = raw_rsrc(z + r0 * ldz, (uint32_t)(nt * ldz * sizeof(T)));
+    const __amdgpu_buffer_rsrc_t ob = raw_rsrc(out + r0 * E, (uint32_t)(nt * E * sizeof(T)));
+    const __amdgpu_buffer_rsrc_t yb = raw_rsrc(ysave ? ysave + r0 * E : out, ysave ? (uint32_t)(nt * E * sizeof(T)) : 0u);
+    const uint32_t lane = (uint32_t)(e * sizeof(T)), urow = (uint32_t)(E * sizeof(T)),
+                   zrow = (uint32_t)(ldz * sizeof(T));
+    auto token = [&](int tt, T ut, T zt) {
       const float* xr = &sX[tt * XW];
-      const float uv = to_f32(un), zv = to_f32(zn);
-      if (tt + 1 < nt) {
-        un = u[(row + 1) * E + e];
-        zn = z[(row + 1) * ldz + e];
-      }
+      const float uv = to_f32(ut), zv = to_f32(zt);
       float v = bdt;
 #pragma unroll
       for (int r = 0; r < R; ++r) v = fmaf(wdt[r], xr[r], v);
@@ -271,15 +290,33 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
         y = fmaf(s[n], xr[R + N + n], y);
       }
       y = fmaf(Dv, uv, y);
-      if (ysave) st1(ysave + row * E + e, y);
-      st1(out + row * E + e, y * silu(zv));
+      if (ysave) buf_st(y, yb, lane, tt * urow, ysave);
+      buf_st(y * silu(zv), ob, lane, tt * urow, out);
       const int t = t0 + tt;
       if (ckpt && t % kScanCkptTokens == kScanCkptTokens - 1 && t + 1 < len) {
         floatx4* dst = reinterpret_cast<floatx4*>(ckpt + (((int64_t)b * E + e) * nck + t / kScanCkptTokens) * N);
 #pragma unroll
         for (int n = 0; n < N; n += 4) dst[n / 4] = floatx4{s[n], s[n + 1], s[n + 2], s[n + 3]};
       }
+    };
+    // Two tokens per trip (the state then alternates between two register
+    // sets instead of being copied back after every token). u and z are
+    // loaded a pair ahead of their use; rows past the chunk read as 0 from
+    // the buffer, so the loads need no guard. They stay in their storage
+    // type until used, so that converting them does not wait for the load.
+    T u0 = buf_ld(ub, lane, 0, u), z0 = buf_ld(zb, lane, 0, z);
+    T u1 = buf_ld(ub, lane, urow, u), z1 = buf_ld(zb, lane, zrow, z);
+    int tt = 0;
+    for (; tt + 1 < nt; tt += 2) {
+      const T ua = u0, za = z0, ub1 = u1, zb1 = z1;
+      u0 = buf_ld(ub, lane, (tt + 2) * urow, u);
+      z0 = buf_ld(zb, lane, (tt + 2) * zrow, z);
+      u1 = buf_ld(ub, lane, (tt + 3) * urow, u);
+      z1 = buf_ld(zb, lane, (tt + 3) * zrow, z);
+      token(tt, ua, za);
+      token(tt + 1, ub1, zb1);
     }
+    if (tt < nt) token(tt, u0, z0);
   }
 }
 
