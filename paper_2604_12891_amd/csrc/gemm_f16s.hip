@@ -259,11 +259,15 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
   }
 }
 
-// ---------------------------------------------------------------- all N in registers (out_proj)
-// 32-row panels whose accumulators for all N <= 256 columns stay in
-// registers while K (up to 512) is walked in chunks of 128: out_proj with its
-// residual epilogue. With eight blocks of accumulators there is no room for a
-// second set, so the low parts are unscaled (l = fp16(x - h), for A and for W:
+// ---------------------------------------------------------------- columns in registers (out_proj)
+// 128-row panels (32 rows per wavefront) whose accumulators for up to 128
+// columns stay in registers while K (up to 512) is walked in chunks of 128:
+// out_proj with its residual epilogue. N <= 256 columns are split over two
+// (or, for small batches, four) workgroups per panel, and two workgroups
+// share a CU (one, holding all 256 columns, left the MFMAs idle while its
+// single wavefront per SIMD waited for A: 8-12% slower). With the
+// accumulators taking most registers there is no room for a second set, so
+// the low parts are unscaled (l = fp16(x - h), for A and for W:
 // split2_f16_flat) and all three part products go into one accumulator;
 // x - h stays in fp16's normal range for every value above 2^-17 of the
 // chunk's largest (after its scale), and W's scale puts every weight above
@@ -278,7 +282,7 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
 // first block staged a quarter of the way through the pair's k-steps, its
 // second at three quarters.
 template <int KCH, int NB, int FL>
-__global__ __launch_bounds__(kNT, 1) void gemm_f16acc_kernel(GemmArgs p, const uint16_t* Wh, int ldwh) {
+__global__ __launch_bounds__(kNT, 2) void gemm_f16acc_kernel(GemmArgs p, const uint16_t* Wh, int ldwh) {
   constexpr int NS = 8;              // 16-k MFMA steps per chunk of 128
   constexpr int WP = 128 + 8;        // halves per staged W row
   constexpr int PART = 32 * WP;      // one part of one block buffer
@@ -294,11 +298,15 @@ __global__ __launch_bounds__(kNT, 1) void gemm_f16acc_kernel(GemmArgs p, const u
   const int wave = tid >> 6, lane = tid & 63;
   const int li = lane & 31, lg = lane >> 5;
   const int M = p.Mdev ? *p.Mdev : p.Mmax;
-  const int row0 = blockIdx.x * kBM;
+  // the columns split over CS workgroups per panel (NB blocks of 32 each).
+  // Workgroups go to the 8 XCDs round-robin: the CS workgroups of a panel
+  // take consecutive slots on one XCD, so the panel's A is read from HBM
+  // once and then hits that XCD's L2
+  const int CS = ((p.N + 31) / 32 + NB - 1) / NB;
+  const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const int row0 = ((j / CS) * 8 + xcd) * kBM;
   if (row0 >= M) return;
-  // this workgroup's NB column blocks start at column cb (gridDim.y > 1:
-  // a small batch's columns split over more workgroups)
-  const int cb = blockIdx.y * NB * 32;
+  const int cb = (j % CS) * NB * 32;
 
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(Wh, (uint32_t)__builtin_amdgcn_readfirstlane(2 * p.N * ldwh * 2));
   u32x4 wr[NW];
@@ -520,21 +528,17 @@ hipError_t launch_f16acc(const GemmArgs& a, const uint16_t* Wh, int ldwh, hipStr
   const int grid = (a.Mmax + kBM - 1) / kBM;
   if (grid <= 0) return hipSuccess;
   const int nb = (a.N + 31) / 32;
-  // a batch with fewer panels than two per CU splits the columns over 2 or
-  // 4 workgroups per panel (each repeats its panel's A chunks)
-  const int cs = 512 / grid >= 4 ? 4 : 512 / grid >= 2 ? 2 : 1;
+  // at most 128 columns per workgroup (two workgroups per CU); a batch with
+  // fewer panels than two per CU splits 256 columns over 4 workgroups per
+  // panel instead of 2 (each repeats its panel's A chunks, from L2)
+  const bool small = 512 / grid >= 4;
 #define TCL_F16ACC(KCH, NB, CS) \
-  hipLaunchKernelGGL((gemm_f16acc_kernel<KCH, NB, FL>), dim3(grid, CS), dim3(kNT), 0, s, a, Wh, ldwh)
-#define TCL_F16ACC_K(KCH)                                  \
-  if (nb <= 2) TCL_F16ACC(KCH, 2, 1);                      \
-  else if (nb <= 4) {                                      \
-    if (cs >= 2) TCL_F16ACC(KCH, 2, 2);                    \
-    else TCL_F16ACC(KCH, 4, 1);                            \
-  } else {                                                 \
-    if (cs >= 4) TCL_F16ACC(KCH, 2, 4);                    \
-    else if (cs == 2) TCL_F16ACC(KCH, 4, 2);               \
-    else TCL_F16ACC(KCH, 8, 1);                            \
-  }
+  hipLaunchKernelGGL((gemm_f16acc_kernel<KCH, NB, FL>), dim3(8 * (CS) * ((grid + 7) / 8)), dim3(kNT), 0, s, a, Wh, ldwh)
+#define TCL_F16ACC_K(KCH)                       \
+  if (nb <= 2) TCL_F16ACC(KCH, 2, 1);           \
+  else if (nb <= 4) TCL_F16ACC(KCH, 2, 2);      \
+  else if (small) TCL_F16ACC(KCH, 2, 4);        \
+  else TCL_F16ACC(KCH, 4, 2);
   switch ((a.K + 127) / 128) {
     case 1: TCL_F16ACC_K(1); break;
     case 2: TCL_F16ACC_K(2); break;

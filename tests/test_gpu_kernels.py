@@ -677,7 +677,8 @@ def test_gemm_f16split_error_against_native_fp32():
 
 
 @pytest.mark.parametrize("M,N,K", [(1, 64, 512), (31, 48, 500), (257, 256, 512), (77, 100, 64),
-                                   (200, 256, 128), (65, 40, 256), (40000, 96, 512), (129, 256, 384)])
+                                   (200, 256, 128), (65, 40, 256), (40000, 96, 512), (129, 256, 384),
+                                   (40000, 256, 512)])
 @pytest.mark.parametrize("mode", ["plain", "bias", "resid"])
 def test_gemm_f16acc(M, N, K, mode):
     """The two-part fp16 panels with all N in registers (variant 6: out_proj's
