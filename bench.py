@@ -104,6 +104,19 @@ def kernel_work(shape, M_v: int, B: int, dtype: str, L: int = 0) -> dict:
     }
 
 
+def gemm_bytes(shape, M_v: int, dtype: str) -> dict:
+    """Minimal HBM bytes per pass of the projections (their operands and
+    results read or written once): the byte side of their roofline. The
+    residual stream H is fp32 in both dtypes."""
+    d, E, F = shape.d_model, shape.d_inner, shape.F
+    a = 4 if dtype == "f32" else 2
+    return {
+        "gemm_input": M_v * 4 * (F + d),               # gathered features in, H out
+        "gemm_in_proj": M_v * (4 * d + 2 * E * a),     # H in, xz out
+        "gemm_out_proj": M_v * (E * a + 2 * 4 * d),    # y and H in, H out
+    }
+
+
 def expected_launches(name: str, shape) -> int:
     """Launches of a kernel per pass of the model over one batch."""
     if name in ("gemm_in_proj", "gemm_x_proj", "gemm_x_proj_conv", "conv_silu", "scan", "scan_chunked",
@@ -147,6 +160,8 @@ def _roof(name: str, d: dict) -> dict:
         roof["alu_note"] = d["alu_note"]
     if "peak_note" in d:
         roof["peak_note"] = d["peak_note"]
+    if "memory" in d:
+        roof["memory"] = {k: (round(v, 4) if isinstance(v, float) else v) for k, v in d["memory"].items()}
     return roof
 
 
@@ -834,6 +849,7 @@ def main():
     ms_h2d = e2.elapsed_time(e3) / args.steps
 
     work = kernel_work(w.model, M_v, w.B, w.dtype, w.L)
+    gbytes = gemm_bytes(w.model, M_v, w.dtype)
     valu_slots = measured_valu_slots(w.name)
 
     def timed_pass(streams: int):
@@ -860,6 +876,11 @@ def main():
             e = roofline_entry(kind, amount, per, w.dtype, split_form(name, args.f32_matmul) if split else None)
             if name in valu_slots:
                 e = alu_entry(e, valu_slots[name] * M_v / parts, per)
+            if name in gbytes:
+                # the projections' bytes at their time: how close to HBM they run
+                gb = gbytes[name] / parts / (per * 1e-3) / 1e9
+                e["memory"] = {"bytes": gbytes[name] / parts, "achieved": gb, "peak": HBM_PEAK_GBS,
+                               "unit": "GB/s", "frac": gb / HBM_PEAK_GBS}
             e.update({"ms_per_launch": per, "launches_per_step": n // args.steps,
                       "ms_per_step": tot / args.steps, "work_per_launch": amount, "work_unit": kind})
             kernels[name] = e
@@ -874,6 +895,8 @@ def main():
                 extra = (f"  ({e['matrix_core']['dtype']} matrix cores {e['matrix_core']['frac']:.3f})"
                          if "matrix_core" in e else
                          f"  (HBM {e['hbm']['achieved']:.0f} GB/s = {e['hbm']['frac']:.3f})" if "hbm" in e else "")
+                if "memory" in e:
+                    extra += f"  (bytes at {e['memory']['achieved']:.0f} GB/s = {e['memory']['frac']:.3f} of HBM)"
                 print(f"{k:16s} {e['ms_per_step']:9.4f} {e['ms_per_launch']:10.5f} {e['achieved']:10.2f} "
                       f"{e['unit']:8s} {e['frac']:6.3f}{extra}", file=sys.stderr)
         return kernels, roof
