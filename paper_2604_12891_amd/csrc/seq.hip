@@ -328,9 +328,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
 // a chunk acts on its incoming state as s -> P s + s_loc with
 // P = prod_t a_t = exp(A sum_t dt_t) and s_loc the chunk's end state from a
 // zero start. Level 1: every wavefront scans its chunk from zero and parks
-// (P, s_loc) in LDS. Level 2: after one barrier each wavefront folds the
-// summaries of the chunks before it into its incoming state and re-runs its
-// chunk from there, writing the outputs. This spends twice the exponentials
+// (P, s_loc) in LDS. Carry: the chunks' maps are composed in order by a
+// prefix scan across lanes (DPP row shifts, eight lanes per channel and
+// state), which leaves every chunk's incoming state in LDS. Level 2: each
+// wavefront re-runs its chunk from there, writing the outputs. This spends twice the exponentials
 // of the sequential scan; it pays only when the extra concurrency is needed.
 template <typename T, int N, int R>
 __global__ __launch_bounds__(512) void scan_chunked_kernel(
@@ -390,14 +391,39 @@ __global__ __launch_bounds__(512) void scan_chunked_kernel(
   }
   __syncthreads();
 
-  // level 2: incoming state = fold of the earlier chunks' summaries, then re-run
-#pragma unroll
-  for (int n = 0; n < N; ++n) s[n] = 0.f;
-  for (int j = 0; j < w; ++j) {
-    const float* sj = sSum + ((int64_t)j * 64 + lane) * 2 * N;
-#pragma unroll
-    for (int n = 0; n < N; ++n) s[n] = fmaf(sj[n], s[n], sj[N + n]);
+  // carry: for every (channel, state) the chunks' maps s -> P s + S are
+  // composed in chunk order by a scan across lanes. Eight lanes take one
+  // (channel, state), lane j of the eight holding chunk j (chunks past nw
+  // hold the identity); three DPP row shifts (by 1, 2, 4 lanes, masked at
+  // the group's start) form the inclusive scan, one more shift the
+  // exclusive one: chunk j's incoming state is the composed S of chunks
+  // 0..j-1 applied to a zero state. It replaces P in the summary slot.
+  {
+    const int j = lane & 7;
+    auto shr = [](float v, int ctrl) {
+      return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xF, 0xF, false));
+    };
+    for (int task0 = 0; task0 < N * 64; task0 += 8 * nw) {
+      const int task = task0 + w * 8 + (lane >> 3);
+      const int c = task & 63, n = task >> 6;
+      const bool ok = task < N * 64 && j < nw;
+      float* slot = sSum + ((int64_t)j * 64 + c) * 2 * N + n;
+      float P = ok ? slot[0] : 1.f, S = ok ? slot[N] : 0.f;
+      float Pp = shr(P, 0x111), Sp = shr(S, 0x111);  // row_shr:1
+      if (j >= 1) { S = fmaf(P, Sp, S); P *= Pp; }
+      Pp = shr(P, 0x112); Sp = shr(S, 0x112);        // row_shr:2
+      if (j >= 2) { S = fmaf(P, Sp, S); P *= Pp; }
+      Pp = shr(P, 0x114); Sp = shr(S, 0x114);        // row_shr:4
+      if (j >= 4) { S = fmaf(P, Sp, S); P *= Pp; }
+      Sp = shr(S, 0x111);
+      if (ok) slot[0] = j >= 1 ? Sp : 0.f;
+    }
   }
+  __syncthreads();
+
+  // level 2: each chunk re-run from its incoming state
+#pragma unroll
+  for (int n = 0; n < N; ++n) s[n] = mine[n];
   if (!active) return;
   un = t_begin < t_end ? u[(int64_t)(base + t_begin) * E + e] : T(0);
   T zn = t_begin < t_end ? z[(int64_t)(base + t_begin) * ldz + e] : T(0);

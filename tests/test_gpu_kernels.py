@@ -386,7 +386,7 @@ def test_xproj_conv_rejects_unsupported():
 
 @pytest.mark.parametrize("R", [4, 16])
 @pytest.mark.parametrize("L", [1, 25, 70, 256])
-@pytest.mark.parametrize("chunks", [0, 1, 3, 8])
+@pytest.mark.parametrize("chunks", [0, 1, 2, 3, 5, 8])
 def test_scan_f32(R, L, chunks):
     """chunks = 0: sequential scan; > 0: the chunked two-level scan."""
     N, E = 16, 320
