@@ -241,9 +241,9 @@ TCL_API tcl_status tcl_timing_reset(tcl_model* model);
  * ------------------------------------------------------------------- */
 
 /* Create a trainer (allocates the gradient blob and the Adam moments, zeroed;
- * the step count starts at 0). max_B, max_L bound every later step; max_L is
- * also limited by the scan backward's LDS staging, (dt_rank + 18 d_state)
- * * 4 bytes per token within 64 KiB (55 tokens at dt_rank 8). */
+ * the step count starts at 0). max_B, max_L bound every later step (the
+ * scan backward stages a program's tokens in windows, so L has no limit of
+ * its own beyond the workspace it needs). */
 TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, float lr, float beta1,
                                       float beta2, float eps, int32_t max_B, int32_t max_L,
                                       tcl_trainer** out);

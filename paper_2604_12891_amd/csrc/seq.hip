@@ -320,6 +320,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
   }
 }
 
+// Lane i of each row of 16 lanes takes lane i - D's value (DPP row_shr:D);
+// the first D lanes of a row receive 0.
+template <int D>
+__device__ __forceinline__ float row_shr(float v) {
+  static_assert(D >= 1 && D <= 15, "row_shr:1..15");
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x110 + D, 0xF, 0xF, false));
+}
+
 // ---------------------------------------------------------------- chunked two-level scan
 // For batches too small to fill the GPU with one thread per (program,
 // channel): the sequence is split into W chunks that run concurrently, one
@@ -400,22 +408,19 @@ __global__ __launch_bounds__(512) void scan_chunked_kernel(
   // 0..j-1 applied to a zero state. It replaces P in the summary slot.
   {
     const int j = lane & 7;
-    auto shr = [](float v, int ctrl) {
-      return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xF, 0xF, false));
-    };
     for (int task0 = 0; task0 < N * 64; task0 += 8 * nw) {
       const int task = task0 + w * 8 + (lane >> 3);
       const int c = task & 63, n = task >> 6;
       const bool ok = task < N * 64 && j < nw;
       float* slot = sSum + ((int64_t)j * 64 + c) * 2 * N + n;
       float P = ok ? slot[0] : 1.f, S = ok ? slot[N] : 0.f;
-      float Pp = shr(P, 0x111), Sp = shr(S, 0x111);  // row_shr:1
+      float Pp = row_shr<1>(P), Sp = row_shr<1>(S);
       if (j >= 1) { S = fmaf(P, Sp, S); P *= Pp; }
-      Pp = shr(P, 0x112); Sp = shr(S, 0x112);        // row_shr:2
+      Pp = row_shr<2>(P); Sp = row_shr<2>(S);
       if (j >= 2) { S = fmaf(P, Sp, S); P *= Pp; }
-      Pp = shr(P, 0x114); Sp = shr(S, 0x114);        // row_shr:4
+      Pp = row_shr<4>(P); Sp = row_shr<4>(S);
       if (j >= 4) { S = fmaf(P, Sp, S); P *= Pp; }
-      Sp = shr(S, 0x111);
+      Sp = row_shr<1>(S);
       if (ok) slot[0] = j >= 1 ? Sp : 0.f;
     }
   }

@@ -292,13 +292,14 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     const float* __restrict__ b_dt, const float* __restrict__ A_log, const float* __restrict__ Dp,
     const float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
     float* __restrict__ dxz, float* __restrict__ dxdbl, float* __restrict__ dA_part,
-    float* __restrict__ dD_part, float* __restrict__ dbc_part, int Mmax) {
+    float* __restrict__ dD_part, float* __restrict__ dbc_part, int Mmax, int TW) {
   static_assert(N == 2 * kHalfN, "two lanes per channel, eight states each");
   constexpr int XW = R + 2 * N;
   constexpr int NH = kHalfN;
   extern __shared__ float smem[];
-  float* sX = smem;                       // [L][XW] rows of this program
-  float* sRed = smem + L * XW;            // [L][8 waves][2N] per-wavefront dB_t | dC_t
+  // a window of TW tokens (a multiple of the checkpoint interval) at a time
+  float* sX = smem;                       // [TW][XW] the window's rows
+  float* sRed = smem + TW * XW;           // [TW][8 waves][2N] per-wavefront dB_t | dC_t
   const int b = blockIdx.x;
   const int tid = threadIdx.x;            // blockDim == 2E / gridDim.y: the program's channels in groups
   const int e = blockIdx.y * (blockDim.x >> 1) + (tid >> 1), hf = tid & 1, n0 = hf * NH;
@@ -307,8 +308,26 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
   const int nck = (len + kTC - 1) / kTC;
   const int ldz = 2 * E;
 
-  for (int i = tid; i < len * XW; i += blockDim.x) sX[i] = xdbl[(int64_t)base * XW + i];
-  __syncthreads();
+  int wbase = 0, wend = 0;  // the staged window [wbase, wend)
+  auto stage_window = [&](int w0) {
+    wbase = w0;
+    wend = min(w0 + TW, len);
+    __syncthreads();  // every wavefront is done with the previous window's rows
+    for (int i = tid; i < (wend - wbase) * XW; i += blockDim.x) sX[i] = xdbl[(int64_t)(base + wbase) * XW + i];
+    __syncthreads();
+  };
+  const int nw = blockDim.x >> 6;
+  // dB_t, dC_t of the window's tokens = sums over the block's wavefronts
+  auto flush_window = [&]() {
+    __syncthreads();
+    for (int i = tid; i < (wend - wbase) * 2 * N; i += blockDim.x) {
+      const int tl = i / (2 * N), j = i % (2 * N), t = wbase + tl;
+      float acc = 0.f;
+      for (int w = 0; w < nw; ++w) acc += sRed[(tl * 8 + w) * 2 * N + j];
+      if (gridDim.y == 1) dxdbl[(int64_t)(base + t) * XW + R + j] = acc;
+      else dbc_part[((int64_t)blockIdx.y * Mmax + base + t) * 2 * N + j] = acc;
+    }
+  };
 
   float a2[NH], wdt[R];  // a2 = A log2(e); A itself is a2 ln(2) where needed
 #pragma unroll
@@ -319,7 +338,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
   const float* ck = ckpt + ((int64_t)b * E + e) * (int64_t)((L + kTC - 1) / kTC) * N + n0;
 
   auto dt_of = [&](int t, float& sig) {
-    const float* xr = &sX[t * XW];
+    const float* xr = &sX[(t - wbase) * XW];
     float v = bdt;
 #pragma unroll
     for (int r = 0; r < R; ++r) v = fmaf(wdt[r], xr[r], v);
@@ -356,6 +375,12 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
   if (nck > 0) load_chunk(nck - 1);
   for (int c = nck - 1; c >= 0; --c) {
     const int t0 = c * kTC;
+    // windows begin at multiples of TW (a multiple of kTC): a chunk never
+    // straddles two; entering a new window flushes the one after it
+    if (c == nck - 1 || t0 < wbase) {
+      if (c != nck - 1) flush_window();
+      stage_window(t0 / TW * TW);
+    }
     float sp[NH];  // state before the chunk
     float uc[kTC], zc[kTC], yc[kTC], gc[kTC];
 #pragma unroll
@@ -380,7 +405,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
           float sig;
           const float dt = dt_of(t, sig);
           const float dtu = dt * uc[tt];
-          const float* xr = &sX[t * XW] + R + n0;
+          const float* xr = &sX[(t - wbase) * XW] + R + n0;
 #pragma unroll
           for (int n = 0; n < NH; ++n) s[n] = fmaf(__builtin_amdgcn_exp2f(dt * a2[n]), s[n], dtu * xr[n]);
         }
@@ -393,8 +418,8 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
       const int t = t0 + tt;
       if (t < len) {  // uniform across the block: len is per program
         const int64_t row = base + t;
-        const float* xB = &sX[t * XW] + R + n0;
-        const float* xC = &sX[t * XW] + R + N + n0;
+        const float* xB = &sX[(t - wbase) * XW] + R + n0;
+        const float* xC = &sX[(t - wbase) * XW] + R + N + n0;
         float sig;
         const float dt = dt_of(t, sig);
         const float uv = uc[tt], zv = zc[tt];
@@ -426,21 +451,12 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
         if ((lane & 2) == 0) {
           const int k = (lane >> 2) & 15;
           const int j = k < NH ? n0 + k : N + n0 + (k - NH);
-          sRed[(t * 8 + wave) * 2 * N + j] = tot;
+          sRed[((t - wbase) * 8 + wave) * 2 * N + j] = tot;
         }
       }
     }
   }
-  // dB_t, dC_t = sums over the block's wavefronts, for every token at once
-  __syncthreads();
-  const int nw = blockDim.x >> 6;
-  for (int i = tid; i < len * 2 * N; i += blockDim.x) {
-    const int t = i / (2 * N), j = i % (2 * N);
-    float acc = 0.f;
-    for (int w = 0; w < nw; ++w) acc += sRed[(t * 8 + w) * 2 * N + j];
-    if (gridDim.y == 1) dxdbl[(int64_t)(base + t) * XW + R + j] = acc;
-    else dbc_part[((int64_t)blockIdx.y * Mmax + base + t) * 2 * N + j] = acc;
-  }
+  if (nck > 0) flush_window();
 #pragma unroll
   for (int n = 0; n < NH; ++n)
     dA_part[((int64_t)b * E + e) * N + n0 + n] = dA[n] * (a2[n] * kLn2);  // d/dA_log
@@ -723,9 +739,14 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
                            const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
                            float* dxz, float* dxdbl, float* dA_part, float* dD_part, float* dbc_part,
                            hipStream_t s) {
-  if (N != 16 || E % 32 || E > 256 || B <= 0) return hipErrorInvalidValue;
-  const size_t shm = ((size_t)L * (R + 2 * N) + (size_t)L * 8 * 2 * N) * sizeof(float);
-  if (shm > 64 * 1024) return hipErrorInvalidValue;
+  if (N != 16 || E % 32 || E > 256 || B <= 0 || L <= 0) return hipErrorInvalidValue;
+  // the program's tokens are staged in windows of TW (a multiple of the
+  // checkpoint interval) within 64 KiB of LDS: a window's [dt_r | B | C]
+  // rows and its per-wavefront dB | dC partial sums
+  const size_t per_token = ((size_t)(R + 2 * N) + (size_t)8 * 2 * N) * sizeof(float);
+  const int fit = (int)((64 * 1024) / per_token) / kScanCkptTokens * kScanCkptTokens;
+  const int TW = std::min((L + kScanCkptTokens - 1) / kScanCkptTokens * kScanCkptTokens, fit);
+  const size_t shm = (size_t)TW * per_token;
   // the channels of a program in two blocks of E threads where E allows
   // (three such blocks fit a CU at this kernel's register count, against one
   // block of 2E threads); their dB/dC partial sums are added afterwards
@@ -734,7 +755,7 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
 #define TCL_SB(RR)                                                                                       \
   hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B, groups), dim3(2 * E / groups), shm, s, \
                      offs, E, L, u, xdbl, xz, ysave, dyg, W_dt, b_dt, A_log, D, ckpt, dv, du, dxz, dxdbl,   \
-                     dA_part, dD_part, dbc_part, Mmax)
+                     dA_part, dD_part, dbc_part, Mmax, TW)
   switch (R) {
     case 4: TCL_SB(4); break;
     case 8: TCL_SB(8); break;

@@ -216,8 +216,6 @@ TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, fl
                 "the student must have d_state 16, F %% 4 == 0, a one-Linear encoder and a two-layer decoder");
   if (sc.dt_rank != 4 && sc.dt_rank != 8 && sc.dt_rank != 16)
     return fail(TCL_ERR_UNSUPPORTED, "student dt_rank must be 4, 8 or 16");
-  if ((size_t)max_L * (sc.dt_rank + 2 * sc.d_state + 16 * sc.d_state) * 4 > 64 * 1024)
-    return fail(TCL_ERR_UNSUPPORTED, "max_L too long for the scan backward's LDS staging");
   tcl_trainer* tr = new tcl_trainer();
   tr->teacher = teacher;
   tr->student = student;

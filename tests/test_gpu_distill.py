@@ -146,6 +146,25 @@ def test_distill_small(perturb):
     _check_params(sblob.astype(np.float64), g[2], g[1], orc, sshape, "small")
 
 
+def test_distill_long_sequences():
+    """L = 130: the scan backward stages a program in windows of 52 tokens, so
+    programs of 53..130 tokens cross one or two window boundaries (lengths at
+    and around each boundary, and 1)."""
+    tshape = wl.ModelShape(d_model=64, d_inner=128, dt_rank=4, n_layers=2, head_hidden=64)
+    sshape = wl.ModelShape(d_model=64, d_inner=128, dt_rank=8, n_layers=2, head_hidden=64)
+    L = 130
+    tblob, sblob, X, lengths, labels, t = _setup(tshape, sshape, 12, L, 1, 41)
+    lengths[:10] = [1, 51, 52, 53, 57, 103, 104, 105, 129, 130]
+    X[np.arange(L)[None, :] >= lengths[:, None]] = 0
+    t = om.score(tblob, X, lengths, oracle_cfg(tshape))
+    print(f"distill long sequences L={L}", flush=True)
+    (g,) = _gpu(tshape, sshape, tblob, sblob, X, lengths, labels, 1)
+    orc = om.distill_step(tblob, oracle_cfg(tshape), sblob, oracle_cfg(sshape), X, lengths, labels,
+                          lr=LR, teacher_scores=t)
+    _check(g, orc, sshape, "long")
+    _check_params(sblob.astype(np.float64), g[2], g[1], orc, sshape, "long")
+
+
 def test_distill_full_shapes_two_steps():
     """The distillation workload's model shapes (teacher d=256 x4, student
     d=128 x2) at B=128; a second step exercises Adam's moments and step count
