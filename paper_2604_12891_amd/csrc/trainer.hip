@@ -32,6 +32,10 @@ struct tcl_trainer {
   int64_t max_n = 0;
   int plan_B = -1, plan_L = -1;
   Timing timing;
+  // the backward's weight-gradient GEMMs run on a stream of their own,
+  // forked from and joined back to the step's stream by events
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_dh = nullptr, ev_layer = nullptr, ev_end = nullptr;
 };
 
 namespace {
@@ -196,6 +200,21 @@ tcl_status ensure_plan(tcl_trainer* tr, int B, int L, const TrainPlan& P, bool c
 
 }  // namespace
 
+namespace {
+void release_side(tcl_trainer* tr) {
+  for (hipEvent_t* e : {&tr->ev_fork, &tr->ev_dh, &tr->ev_layer, &tr->ev_end})
+    if (*e) {
+      (void)hipEventDestroy(*e);
+      *e = nullptr;
+    }
+  if (tr->side) {
+    (void)hipStreamSynchronize(tr->side);
+    (void)hipStreamDestroy(tr->side);
+    tr->side = nullptr;
+  }
+}
+}  // namespace
+
 TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, float lr, float beta1,
                                       float beta2, float eps, int32_t max_B, int32_t max_L,
                                       tcl_trainer** out) {
@@ -244,12 +263,21 @@ TCL_API tcl_status tcl_trainer_create(tcl_model* teacher, tcl_model* student, fl
     delete tr;
     return fail(TCL_ERR_HIP, "hipMemset failed");
   }
+  // default priority; without them the backward runs on one stream
+  bool ok = hipStreamCreateWithFlags(&tr->side, hipStreamNonBlocking) == hipSuccess;
+  for (hipEvent_t* e : {&tr->ev_fork, &tr->ev_dh, &tr->ev_layer, &tr->ev_end})
+    ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
+  if (!ok) {
+    release_side(tr);
+    (void)hipGetLastError();
+  }
   *out = tr;
   return TCL_OK;
 }
 
 TCL_API tcl_status tcl_trainer_destroy(tcl_trainer* tr) {
   if (!tr) return TCL_OK;
+  release_side(tr);
   tr->timing.release();
   if (tr->dev) (void)hipFree(tr->dev);
   delete tr;
@@ -387,7 +415,38 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
                                                         c.norm_eps, F32(P.dpooled), F32(P.dH),
                                                         F32(P.p_gf), s));
 
-  // 4. blocks in reverse
+  // 4. blocks in reverse. The data gradients form the chain on `s`; the
+  // weight gradients (which feed only the final reduction) run on the
+  // trainer's side stream beside it, each forked once its inputs are
+  // ready. Joins guard the buffers the chain overwrites while a side GEMM
+  // may still read them: dH (rewritten by this block's RMSNorm backward)
+  // and dv, dxdbl, dxz (rewritten by the next block's scan backward).
+  const hipStream_t sd = tr->side ? tr->side : s;
+  auto fork_side = [&]() -> tcl_status {
+    if (sd != s) {
+      TCL_HIP(hipEventRecord(tr->ev_fork, s));
+      TCL_HIP(hipStreamWaitEvent(sd, tr->ev_fork, 0));
+    }
+    return TCL_OK;
+  };
+  auto mark = [&](hipEvent_t e) -> tcl_status {
+    if (sd != s) TCL_HIP(hipEventRecord(e, sd));
+    return TCL_OK;
+  };
+  auto join = [&](hipEvent_t e) -> tcl_status {
+    if (sd != s) TCL_HIP(hipStreamWaitEvent(s, e, 0));
+    return TCL_OK;
+  };
+#define TCL_SIDE(NAME, CALL)            \
+  do {                                  \
+    const hipStream_t s = sd;           \
+    TCL_LAUNCH(T, NAME, CALL);          \
+  } while (0)
+#define TCL_TRY(X)                        \
+  do {                                    \
+    const tcl_status st_ = (X);           \
+    if (st_ != TCL_OK) return st_;        \
+  } while (0)
   for (int l = c.n_layers - 1; l >= 0; --l) {
     const auto& W = S->layers[l];
     const auto& Ly = P.layers[l];
@@ -397,12 +456,16 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = E; g.K = d;
       TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, -1, s));
     }
+    TCL_TRY(fork_side());
     {  // dW_out = dH^T yg
       GemmTNArgs a;
       a.A = F32(P.dH); a.lda = d; a.Bm = B16(Ly.yg); a.ldb = E; a.P = F32(Ly.p_Wout);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = d; a.NJ = E;
-      TCL_LAUNCH(T, "gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Wout, s));
+      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Wout, s));
     }
+    TCL_TRY(mark(tr->ev_dh));
+    // the block above's side GEMMs are done with dv, dxdbl and dxz
+    if (l + 1 < c.n_layers) TCL_TRY(join(tr->ev_layer));
     TCL_LAUNCH(T, "scan_bwd", launch_scan_bwd(B, E, L, N, R, offs, B16(Ly.u), F32(Ly.xdbl), B16(Ly.xz),
                                               B16(Ly.y), F32(P.dyg), W.W_dt, W.b_dt, W.A_log, W.D,
                                               F32(Ly.ckpt), F32(P.dv), F32(P.du), F32(P.dxz),
@@ -413,24 +476,26 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = R; g.K = E;
       TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, kNarrow, s));
     }
+    TCL_TRY(fork_side());
     {  // dW_dt = dv^T dt_r
       GemmTNArgs a;
       a.A = F32(P.dv); a.lda = E; a.Bm = F32(Ly.xdbl); a.ldb = XW; a.P = F32(Ly.p_Wdt);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = E; a.NJ = R;
-      TCL_LAUNCH(T, "gemm_dW", launch_gemm_tn(a, kTN_F32_F32, Ly.s_Wdt, s));
+      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_F32, Ly.s_Wdt, s));
     }
-    TCL_LAUNCH(T, "colsum", launch_colsum(Mdev, Mmax, F32(P.dv), E, E, P.cs, F32(Ly.p_bdt), s));
+    TCL_SIDE("colsum", launch_colsum(Mdev, Mmax, F32(P.dv), E, E, P.cs, F32(Ly.p_bdt), s));
     {  // du += dxdbl W_x
       GemmArgs g;
       g.A = F32(P.dxdbl); g.lda = XW; g.W = W.W_xT; g.ldw = XW; g.C = F32(P.du); g.ldc = E;
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = E; g.K = XW;
       TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, kResid, -1, s));
     }
+    TCL_TRY(fork_side());
     {  // dW_x = dxdbl^T u
       GemmTNArgs a;
       a.A = F32(P.dxdbl); a.lda = XW; a.Bm = B16(Ly.u); a.ldb = E; a.P = F32(Ly.p_Wx);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = XW; a.NJ = E;
-      TCL_LAUNCH(T, "gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Wx, s));
+      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Wx, s));
     }
     TCL_LAUNCH(T, "conv_bwd", launch_conv_bwd(B, E, K, offs, B16(Ly.xz), 2 * E, W.conv_w, W.conv_b,
                                               F32(P.du), F32(P.dxz), 2 * E, F32(Ly.p_conv), s));
@@ -440,22 +505,30 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       g.Mdev = Mdev; g.Mmax = Mmax; g.N = d; g.K = 2 * E;
       TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, -1, s));
     }
+    TCL_TRY(fork_side());
     {  // dW_in = dxz^T n
       GemmTNArgs a;
       a.A = F32(P.dxz); a.lda = 2 * E; a.Bm = B16(Ly.n); a.ldb = d; a.P = F32(Ly.p_Win);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = 2 * E; a.NJ = d;
-      TCL_LAUNCH(T, "gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Win, s));
+      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Win, s));
     }
+    TCL_TRY(mark(tr->ev_layer));
+    TCL_TRY(join(tr->ev_dh));  // dW_out is done with dH
     TCL_LAUNCH(T, "rmsnorm_bwd", launch_rmsnorm_bwd(d, Mmax, Mdev, F32(P.dN), F32(Ly.Hin), F32(Ly.rstd),
                                                     W.g, F32(P.dH), F32(Ly.p_g), s));
   }
+  TCL_TRY(fork_side());
   {  // dW0 = dH^T X (gathered), db0 = column sums of dH
     GemmTNArgs a;
     a.A = F32(P.dH); a.lda = d; a.Bm = d_feats; a.ldb = F; a.offs = offs; a.B = B; a.L = L;
     a.P = F32(P.p_W0); a.Mdev = Mdev; a.Mmax = Mmax; a.NI = d; a.NJ = F;
-    TCL_LAUNCH(T, "gemm_dW", launch_gemm_tn(a, kTN_F32_GatherF32, P.s_W0, s));
+    TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_GatherF32, P.s_W0, s));
   }
-  TCL_LAUNCH(T, "colsum", launch_colsum(Mdev, Mmax, F32(P.dH), d, d, P.cs, F32(P.p_b0), s));
+  TCL_SIDE("colsum", launch_colsum(Mdev, Mmax, F32(P.dH), d, d, P.cs, F32(P.p_b0), s));
+  TCL_TRY(mark(tr->ev_end));
+  TCL_TRY(join(tr->ev_end));  // every partial sum is written
+#undef TCL_TRY
+#undef TCL_SIDE
 
   if (scores_out) {
     TCL_HIP(hipMemcpyAsync(scores_out, F32(P.s_scores), (size_t)B * 4, hipMemcpyDeviceToDevice, s));
