@@ -394,7 +394,10 @@ def bench_progressive(args, w):
         "config": {"workload": w.name, "B": w.B, "L": w.L, "F": w.model.F, "adapter": w.adapter,
                    "f32_matmul": args.f32_matmul, "encoder": [w.model.F, *w.model.enc_hidden, w.model.d_model],
                    "d_state": w.model.d_state, "n_layers": w.model.n_layers,
-                   "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v},
+                   "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v,
+                   # the library picks the sequential scan when the batch alone fills the GPU
+                   # (B * d_inner / 64 >= 1024 wavefronts) and the chunked two-level scan below
+                   "scan": "chunked two-level" if "scan_chunked" in kernels else "sequential"},
         "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
         "graph_replay": {"ms_per_step": ms_graph, "steps_per_s": 1000.0 / ms_graph,
                          "vs_launched": ms / ms_graph,
@@ -709,8 +712,13 @@ def other_workloads(args) -> dict:
         o = torch.empty(w.B, dtype=torch.float32, device=dev)
         ms = timed(lambda: model.score(Xd, Ld, out=o, workspace=ws))
         assert torch.isfinite(o).all().item()
+        waves = w.B * ((w.model.d_inner + 63) // 64)
         out[name] = {"value": w.B / (ms * 1e-3), "unit": "programs/s", "ms_per_step": ms, "dtype": w.dtype,
-                     "B": w.B, "L": w.L, "valid_tokens": int(lengths.sum()), "steps": steps}
+                     "B": w.B, "L": w.L, "valid_tokens": int(lengths.sum()), "steps": steps,
+                     # the library's rule: the chunked two-level scan only for L >= 64 with
+                     # fewer than 1024 wavefronts of (program, 64 channels)
+                     "scan": ("chunked two-level" if w.L >= 64 and waves < 1024 else "sequential")
+                             + f" ({waves} wavefronts)"}
         del model, Xd, Ld, ws, o
         torch.cuda.empty_cache()
     w = wl.WORKLOADS["distill_B1024_L25_t256_s128_bf16"]
@@ -942,7 +950,10 @@ def main():
                    "d_inner": w.model.d_inner, "d_state": w.model.d_state, "n_layers": w.model.n_layers,
                    "encoder": [w.model.F, *w.model.enc_hidden, w.model.d_model],
                    "decoder": [w.model.d_model, w.model.head_hidden, *([w.model.dec_hidden2] if w.model.dec_hidden2 else []), 1],
-                   "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v},
+                   "lengths": f"uniform {w.len_lo}..{w.len_hi}", "valid_tokens": M_v,
+                   # the library picks the sequential scan when the batch alone fills the GPU
+                   # (B * d_inner / 64 >= 1024 wavefronts) and the chunked two-level scan below
+                   "scan": "chunked two-level" if "scan_chunked" in kernels else "sequential"},
         "wall_ms_per_step": wall * 1e3 / args.steps,
         "roofline": roof,
         "roofline_single_stream": roof1,
