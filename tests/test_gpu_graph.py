@@ -112,3 +112,49 @@ def test_capture_of_an_unseen_shape_is_refused():
     torch.cuda.synchronize()
     assert torch.isfinite(loss).all().item()
     tr.close()
+
+
+@pytest.mark.parametrize("name,B,entry", [("score_B4096_L25_d256_f32", 4096, "score"),
+                                          ("score_B4096_L25_d256_f32", 300, "score"),
+                                          ("score_B65536_L25_d256_bf16", 2048, "score"),
+                                          ("score_B4096_L25_d256_f32", 1000, "noalloc")])
+def test_score_graph_replays_equal_uncaptured(name, B, entry):
+    """tcl_score (one pass below 2048 programs, two halves on the model's two
+    streams from 2048 up) and tcl_score_noalloc captured into a HIP graph:
+    every replay, with new features copied into the captured input buffer
+    and uncaptured scoring on the same model between replays, equals the
+    uncaptured scores of the same inputs bit for bit."""
+    w = wl.WORKLOADS[name]
+    blob, X, lengths = wl.make_workload(name, B=B)
+    model = tb.CostModel(tb.config_from_shape(w.model, w.dtype), blob)
+    Xd, Ld = torch.from_numpy(X).cuda(), torch.from_numpy(lengths).cuda()
+    out = torch.empty(B, device="cuda")
+    ws = model.workspace(B, w.L) if entry == "score" else None
+    print(f"score graph {name} B={B} entry={entry}", flush=True)
+
+    def run(o):
+        if entry == "score":
+            model.score(Xd, Ld, out=o, workspace=ws)
+        else:
+            model.score_noalloc(Xd, Ld, o)
+
+    run(out)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run(out)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    for k in range(3):
+        # new inputs in the captured buffers (the same shapes and lengths)
+        Xn = X * (1.0 + 0.1 * k) + (0.01 * rng.standard_normal(X.shape)).astype(np.float32) * (X != 0)
+        Xd.copy_(torch.from_numpy(Xn.astype(np.float32)))
+        ref = torch.empty(B, device="cuda")
+        run(ref)  # uncaptured, same model and buffers
+        torch.cuda.synchronize()
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        print(f"replay {k}: max |diff| {np.abs(got - ref.cpu().numpy()).max():.3e}", flush=True)
+        np.testing.assert_array_equal(got, ref.cpu().numpy())
