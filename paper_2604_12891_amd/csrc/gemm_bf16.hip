@@ -240,8 +240,23 @@ __global__ __launch_bounds__(WM* WN * 64, occupancy_for(TM, TN, sizeof(TA) == 4)
       for (int r = 0; r < 16; ++r)
         stg[(8 * (r >> 2) + 4 * lg + (r & 3)) * SP + b * 32 + li] = acc[a][b][r];
     __syncthreads();
+    constexpr int NI = 32 * C4 / 64;
+    // the slice's residuals are loaded before its first store: read in
+    // place (R = C), they would otherwise each wait for the stores before
+    floatx4 rv[(FL & kResid) != 0 ? NI : 1];
+    if constexpr ((FL & kResid) != 0) {
 #pragma unroll
-    for (int i = 0; i < 32 * C4 / 64; ++i) {
+      for (int i = 0; i < NI; ++i) {
+        const int idx = lane + 64 * i;
+        const int rr = idx / C4, c4 = idx % C4;
+        const int row = row0 + wm * TM * 32 + a * 32 + rr;
+        const int col = col0 + wn * TN * 32 + c4 * 4;
+        rv[i] = (row < M && col < p.N) ? *reinterpret_cast<const floatx4*>(R + (int64_t)row * p.ldc + col)
+                                       : floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
       const int idx = lane + 64 * i;
       const int rr = idx / C4, c4 = idx % C4;
       const int rl = wm * TM * 32 + a * 32 + rr;
@@ -254,7 +269,7 @@ __global__ __launch_bounds__(WM* WN * 64, occupancy_for(TM, TN, sizeof(TA) == 4)
         v += floatx4{p.bias[col], p.bias[col + 1], p.bias[col + 2], p.bias[col + 3]};
       const int64_t off = (int64_t)row * p.ldc + col;
       if constexpr (sizeof(TC) == 4) {
-        if constexpr ((FL & kResid) != 0) v += *reinterpret_cast<const floatx4*>(R + off);
+        if constexpr ((FL & kResid) != 0) v += rv[i];
         *reinterpret_cast<floatx4*>(reinterpret_cast<float*>(p.C) + off) = v;
       } else {
         *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(p.C) + off) =

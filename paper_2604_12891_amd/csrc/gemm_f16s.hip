@@ -455,24 +455,33 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16acc_kernel(GemmArgs p, const u
     const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
     fr[r] = pow2f(-(__shfl(erun, rl, 64) + kF16WeightExp));
   }
+  // every column block's residuals are loaded before the first store: the
+  // residual is read in place (R = C), so the compiler keeps loads after
+  // earlier stores, and each block's loads would otherwise wait for the
+  // previous block's stores to complete
+  float res[NB][16];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int col = cb + nb * 32 + li;
+    const bool cok = col < p.N;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
+      res[nb][r] = ((FL & kResid) != 0)
+                       ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rres, off, 0, 0))
+                       : 0.f;
+    }
+  }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int col = cb + nb * 32 + li;
     const bool cok = col < p.N;
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
-    float res[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
-      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
-      res[r] = ((FL & kResid) != 0)
-                   ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rres, off, 0, 0))
-                   : 0.f;
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
-      float v = fmaf(acc[nb][r], fr[r], bias + res[r]);
+      float v = fmaf(acc[nb][r], fr[r], bias + res[nb][r]);
       if (p.relu) v = fmaxf(v, 0.f);
       const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);

@@ -172,24 +172,31 @@ __global__ __launch_bounds__(WM* WN * 64, BK == 32 ? 3 : 2) void gemm_f32_kernel
   }
 
   // Accumulator layout of a 32x32 block: lane l holds column l % 32 and rows
-  // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15. With a residual, a block's 16
-  // residual loads are issued before its 16 stores (C may be read in place, so
-  // loads cannot move past earlier stores).
+  // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15. With a residual, every block's
+  // residuals are loaded before the first store (C may be read in place, so
+  // loads cannot move past earlier stores, and each would wait for them).
+  float res[(FL & kResid) != 0 ? TM : 1][(FL & kResid) != 0 ? TN : 1][16];
+  if constexpr ((FL & kResid) != 0) {
+    const float* R = p.R ? p.R : p.C;
+#pragma unroll
+    for (int a = 0; a < TM; ++a)
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int col = col0 + wn * TN * 32 + b * 32 + li;
+        const bool cok = col < p.N;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + wm * TM * 32 + a * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+          res[a][b][r] = (cok && row < M) ? R[(int64_t)row * p.ldc + col] : 0.f;
+        }
+      }
+  }
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) {
       const int col = col0 + wn * TN * 32 + b * 32 + li;
       const bool cok = col < p.N;
-      float res[16];
-      if constexpr ((FL & kResid) != 0) {
-        const float* R = p.R ? p.R : p.C;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = row0 + wm * TM * 32 + a * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-          res[r] = (cok && row < M) ? R[(int64_t)row * p.ldc + col] : 0.f;
-        }
-      }
       if (!cok) continue;
       const float bias = (FL & kBias) ? p.bias[col] : 0.f;
 #pragma unroll
@@ -200,7 +207,7 @@ __global__ __launch_bounds__(WM* WN * 64, BK == 32 ? 3 : 2) void gemm_f32_kernel
         float v = acc[a][b][r];
         if constexpr (kNorm) v *= sR[rl];
         v += bias;
-        if constexpr ((FL & kResid) != 0) v += res[r];
+        if constexpr ((FL & kResid) != 0) v += res[a][b][r];
         if (p.relu) v = fmaxf(v, 0.f);
         p.C[(int64_t)row * p.ldc + col] = v;
       }
