@@ -35,6 +35,7 @@
 // Fragment k-order (A and W alike): k-step s, lane half g holds k = 16 s +
 // 8 g .. +7.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -75,18 +76,22 @@ __device__ __forceinline__ void split8_f16(const float* x, f16x8& h, f16x8& l) {
 
 template <int KS, int FL>
 __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uint16_t* Wh, int ldwh) {
-  constexpr int KP = KS * 16;       // K rounded up to the MFMA k-steps
-  // halves per staged W row: K rounded up to 64, plus 8 (conflict-free 16-byte reads)
-  constexpr int WP = (KP + 63) / 64 * 64 + 8;
-  constexpr int PART = 32 * WP;     // one part of one buffer
-  constexpr int WU = KP / 8;        // 16-byte units per staged row
-  constexpr int NWU = 2 * 32 * WU;  // units per column block (two parts)
-  constexpr int NW = (NWU + kNT - 1) / kNT;
-  constexpr int H = (NW + 1) / 2;   // the block's units, loaded and staged in two halves
+  constexpr int RU = 2 * KS;                             // 16-byte units (8 k) of a W row
+  constexpr int RUP = RU <= 8 ? 8 : RU <= 16 ? 16 : 32;  // a staged row: a power of two
+  constexpr int SWZ = (RUP < 16 ? RUP : 16) - 1;         // unit swizzle of a staged row
+  constexpr int PARTU = 32 * RUP;                        // units of one part of one buffer
+  constexpr int BUFU = 2 * PARTU;                        // units of one buffer (a column block)
+  constexpr int NI = BUFU / kNT;                         // loads per lane per block
   constexpr bool kNorm = (FL & kRowNorm) != 0;
+  // vector memory operations a block issues after its successor's W loads:
+  // at least the epilogue's 16 stores (vector memory operations complete in
+  // order, so waiting until at most that many are outstanding waits for the
+  // loads; a bias load among them only makes the wait stricter)
+  constexpr int kAfterLoads = 16;
   static_assert((FL & kResid) == 0, "no residual epilogue");
+  static_assert(RU <= 32 && NI * kNT == BUFU, "K up to 256");
 
-  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * 2 * PART];
+  __shared__ __attribute__((aligned(16))) uint16_t sW[2 * BUFU * 8];
   __shared__ float sF[kWaves][32];
   __shared__ int sSrc[kBM];
 
@@ -120,29 +125,34 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
   const int nblk = (p.N + 31) / 32;
   const int sb = (int)(blockIdx.y * nblk / gridDim.y), se = (int)((blockIdx.y + 1) * nblk / gridDim.y);
 
-  // W stage: unit u of a block is part u / (32 WU), row (u / WU) % 32,
-  // k = 8 (u % WU); rows past N and k past ldwh read zero (the offset is moved
-  // out of range by bit 31: arithmetic, not a branch around the load)
-  u32x4 wr[H];
-  auto wload = [&](int half, int n0) {
+  // W goes from memory straight into LDS (buffer_load ... lds: lane l of a
+  // load writes the 16 bytes at the load's base + 16 l, whatever unit it
+  // reads). Staged layout: [part][row 32][RUP units], unit u of row r at
+  // position u ^ (r & SWZ), so that a fragment read (32 rows, one unit each,
+  // per half-wavefront) touches every bank once. A unit with no data (k past
+  // ldwh: A is zero there; rows past N: columns never stored) loads W's
+  // first unit instead.
+  using lds_ptr = __attribute__((address_space(3))) void*;
+  auto wdma = [&](int n0, int buf) {
 #pragma unroll
-    for (int i = 0; i < H; ++i) {
-      const int u = tid + (half * H + i) * kNT;
-      const int part = u / (32 * WU), n = n0 + (u / WU) % 32, k = 8 * (u % WU);
-      const bool ok = u < NWU && half * H + i < NW && n < p.N && k < ldwh;
-      const uint32_t off = (uint32_t)(((part * p.N + n) * ldwh + k) * 2) | ((uint32_t)!ok << 31);
-      wr[i] = __builtin_amdgcn_raw_buffer_load_b128(wres, off, 0, 0);
+    for (int i = 0; i < NI; ++i) {
+      const int f = (wave * NI + i) * 64 + lane;  // staged position this lane writes
+      const int part = f / PARTU, row = (f / RUP) % 32, u = (f % RUP) ^ (row & SWZ);
+      const int n = n0 + row, k = 8 * u;
+      const bool ok = u < RU && n < p.N && k < ldwh;
+      const uint32_t off = ok ? (uint32_t)(((part * p.N + n) * ldwh + k) * 2) : 0u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr)&sW[(buf * BUFU + (wave * NI + i) * 64) * 8], 16,
+                                               off, 0, 0, 0);
     }
   };
-  auto wstage = [&](int half, uint16_t* s) {
-#pragma unroll
-    for (int i = 0; i < H; ++i) {
-      const int u = tid + (half * H + i) * kNT;
-      if (u < NWU && half * H + i < NW) *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = wr[i];
-    }
+  // a wavefront's wait for its own W loads: at most `after` vector memory
+  // operations (issued after them) still outstanding
+  auto wait_vm = [](auto after) {
+    constexpr int n = decltype(after)::value;
+    __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
   };
-  wload(0, sb * 32);  // in flight during the prologue
-  __syncthreads();    // sSrc
+  __syncthreads();   // sSrc
+  wdma(sb * 32, 0);  // in flight during the prologue (after the barrier, which would wait for it)
 
   // prologue: row li of this wavefront's 32, lane half lg's 8 k of every
   // k-step, scaled by a power of two and split into its two fp16 parts
@@ -195,24 +205,26 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
   const uint32_t panel_bytes = (uint32_t)(min(kBM, M - row0) * p.ldc * 4);
   const __amdgpu_buffer_rsrc_t cres = make_rsrc(p.C + (int64_t)row0 * p.ldc, panel_bytes);
 
-  wstage(0, &sW[0]);
-  wload(1, sb * 32);
-  wstage(1, &sW[0]);
-
   for (int s = sb; s < se; ++s) {
     const int buf = (s - sb) & 1, n0 = s * 32;
-    // block s (staged during block s-1) and sF visible; every wavefront is
-    // past block s-1, so the other buffer is free for block s+1
-    __syncthreads();
-    const bool more = s + 1 < se;
-    if (more) wload(0, n0 + 32);
+    // block s in LDS: this wavefront's loads of it are done (only the
+    // previous block's stores and bias load came after them), then every
+    // wavefront's; every wavefront is past block s-1, so the other buffer
+    // is free for block s+1
+    if (s == sb) wait_vm(std::integral_constant<int, 0>{});
+    else wait_vm(std::integral_constant<int, kAfterLoads>{});
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if (s + 1 < se) wdma(n0 + 32, buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
 
     floatx16 am, ax;
 #pragma unroll
     for (int r = 0; r < 16; ++r) am[r] = ax[r] = 0.f;
-    const uint16_t* wb = &sW[buf * 2 * PART + li * WP + 8 * lg];
+    const uint16_t* wb = &sW[(buf * BUFU + li * RUP) * 8];
+    const int wsw = lg ^ (li & SWZ);  // unit 2 ks + lg of row li sits at 2 ks ^ wsw
     auto wfrag = [&](int part, int ks) {
-      return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+      return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(wb + (part * PARTU + ((2 * ks) ^ wsw)) * 8));
     };
     // W fragments one k-step ahead of their MFMAs (the other workgroup's
     // wavefront on the SIMD covers the rest of the LDS latency)
@@ -233,15 +245,7 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
       ax = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[ks], w[0], ax, 0, 0, 0);
       if (ks + 1 < KS) __builtin_amdgcn_sched_group_barrier(0x0100, 2, 0);
       __builtin_amdgcn_sched_group_barrier(0x0008, 3, 0);
-      // the next block's first half into the other buffer halfway through
-      // this block's MFMAs, then its second half loaded
-      if (ks == KS / 2 && more) {
-        wstage(0, &sW[(buf ^ 1) * 2 * PART]);
-        wload(1, n0 + 32);
-        __builtin_amdgcn_sched_group_barrier(0x0200, H, 0);
-      }
     }
-    if (more) wstage(1, &sW[(buf ^ 1) * 2 * PART]);
 
     // epilogue: lane l holds column l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4)
     const int col = n0 + li;
