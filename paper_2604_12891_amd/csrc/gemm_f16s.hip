@@ -288,15 +288,15 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
 template <int KCH, int NB, int FL>
 __global__ __launch_bounds__(kNT, 2) void gemm_f16acc_kernel(GemmArgs p, const uint16_t* Wh, int ldwh) {
   constexpr int NS = 8;              // 16-k MFMA steps per chunk of 128
-  constexpr int WP = 128 + 8;        // halves per staged W row
-  constexpr int PART = 32 * WP;      // one part of one block buffer
-  constexpr int WU = 16;             // 16-byte units per staged row
-  constexpr int NWU = 2 * 32 * WU;   // units per block (two parts)
-  constexpr int NW = NWU / kNT;      // 4
+  constexpr int RU = 16;             // 16-byte units (8 k) of a W row of a chunk
+  constexpr int RP = RU + 1;         // staged row pitch in units (conflict-free fragment reads)
+  constexpr int PARTU = 32 * RP;     // units of one part of one block buffer
+  constexpr int BUFU = 2 * PARTU;    // units of one block buffer
+  constexpr int NQ = BUFU / 64;      // 64-unit loads per block (17), spread over the wavefronts
   static_assert(NB % 2 == 0 && NB >= 2, "column blocks go in pairs");
   static_assert((FL & (kRowNorm | kGather)) == 0, "plain, bias and residual GEMMs only");
 
-  __shared__ __attribute__((aligned(16))) uint16_t sW[4 * 2 * PART];
+  __shared__ __attribute__((aligned(16))) uint16_t sW[4 * BUFU * 8];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -313,28 +313,29 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16acc_kernel(GemmArgs p, const u
   const int cb = (j % CS) * NB * 32;
 
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(Wh, (uint32_t)__builtin_amdgcn_readfirstlane(2 * p.N * ldwh * 2));
-  u32x4 wr[NW];
-  auto wload = [&](int n0, int k0) {
+  // W's blocks go from memory straight into a ring of four LDS buffers
+  // (buffer_load ... lds: lane l of a load writes the 16 bytes at the load's
+  // base + 16 l), rows at a pitch of 17 units so that a fragment read
+  // touches every bank once; the pad unit and a unit with no data (k past
+  // ldwh: A is zero there; rows past N: columns never stored) load W's first
+  // unit instead.
+  using lds_ptr = __attribute__((address_space(3))) void*;
+  auto wdma = [&](int n0, int k0, int buf) {
 #pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int u = tid + i * kNT;
-      const int part = u / (32 * WU), n = n0 + (u / WU) % 32, k = k0 + 8 * (u % WU);
-      const bool ok = n < p.N && k < ldwh;
-      const uint32_t off = (uint32_t)(((part * p.N + n) * ldwh + k) * 2) | ((uint32_t)!ok << 31);
-      wr[i] = __builtin_amdgcn_raw_buffer_load_b128(wres, off, 0, 0);
+    for (int i = 0; i < (NQ + kWaves - 1) / kWaves; ++i) {
+      const int q = i * kWaves + wave;  // this wavefront's i-th load of the block (uniform)
+      if (q < NQ) {
+        const int f = q * 64 + lane;
+        const int part = f / PARTU, row = (f / RP) % 32, u = f % RP;
+        const int n = n0 + row, k = k0 + 8 * u;
+        const bool ok = u < RU && n < p.N && k < ldwh;
+        const uint32_t off = ok ? (uint32_t)(((part * p.N + n) * ldwh + k) * 2) : 0u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(wres, (lds_ptr)&sW[(buf * BUFU + q * 64) * 8], 16, off, 0, 0, 0);
+      }
     }
   };
-  auto wstage = [&](uint16_t* s) {
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const int u = tid + i * kNT;
-      *reinterpret_cast<u32x4*>(&s[(u / WU) * WP + 8 * (u % WU)]) = wr[i];
-    }
-  };
-  wload(cb, 0);
-  wstage(&sW[0]);
-  wload(cb + 32, 0);
-  wstage(&sW[2 * PART]);
+  wdma(cb, 0, 0);
+  wdma(cb + 32, 0, 1);
 
   const int grow = row0 + wave * 32 + li;
   const bool rok = grow < M;
@@ -398,16 +399,24 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16acc_kernel(GemmArgs p, const u
 #pragma unroll
     for (int pp = 0; pp < NB / 2; ++pp) {
       const int g = c * NB + 2 * pp;  // global index of the pair's first block
-      __syncthreads();  // this pair visible; the previous pair's buffers are free
+      // this pair in LDS: this wavefront's loads of it are done (no vector
+      // memory operation is outstanding here but them: the chunk's A loads
+      // were waited for), then every wavefront's; every wavefront is past the
+      // previous pair, whose buffers take the next pair
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+      __builtin_amdgcn_s_barrier();
       const bool more = pp + 1 < NB / 2 || c + 1 < KCH;
       const int ncol = cb + (pp + 1 < NB / 2 ? (2 * pp + 2) * 32 : 0);
       const int nk = pp + 1 < NB / 2 ? c * 128 : (c + 1) * 128;
-      if (more) wload(ncol, nk);
+      if (more) {
+        wdma(ncol, nk, (g + 2) & 3);
+        wdma(ncol + 32, nk, (g + 3) & 3);
+      }
 
-      const uint16_t* wb0 = &sW[(g & 3) * 2 * PART + li * WP + 8 * lg];
-      const uint16_t* wb1 = &sW[((g + 1) & 3) * 2 * PART + li * WP + 8 * lg];
+      const uint16_t* wb0 = &sW[((g & 3) * BUFU + li * RP + lg) * 8];
+      const uint16_t* wb1 = &sW[(((g + 1) & 3) * BUFU + li * RP + lg) * 8];
       auto wfrag = [&](const uint16_t* wb, int part, int ks) {
-        return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(wb + part * PART + 16 * ks));
+        return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(wb + (part * PARTU + 2 * ks) * 8));
       };
       f16x8 q[2][4];
       q[0][0] = wfrag(wb0, 0, 0);
@@ -435,15 +444,6 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16acc_kernel(GemmArgs p, const u
         x1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[ks], w[2], x1, 0, 0, 0);
         if (ks + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x0100, 4, 0);
         __builtin_amdgcn_sched_group_barrier(0x0008, 6, 0);
-        if (ks == NS / 4 && more) {
-          wstage(&sW[((g + 2) & 3) * 2 * PART]);
-          __builtin_amdgcn_sched_group_barrier(0x0200, NW, 0);
-          wload(ncol + 32, nk);
-        }
-        if (ks == 3 * NS / 4 && more) {
-          wstage(&sW[((g + 3) & 3) * 2 * PART]);
-          __builtin_amdgcn_sched_group_barrier(0x0200, NW, 0);
-        }
       }
     }
   }
