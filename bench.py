@@ -399,9 +399,6 @@ def bench_progressive(args, w):
                    # (B * d_inner / 64 >= 1024 wavefronts) and the chunked two-level scan below
                    "scan": "chunked two-level" if "scan_chunked" in kernels else "sequential"},
         "wall_ms_per_step": wall * 1e3 / args.steps, "roofline": roof,
-        "graph_replay": {"ms_per_step": ms_graph, "steps_per_s": 1000.0 / ms_graph,
-                         "vs_launched": ms / ms_graph,
-                         "note": "the same step captured into one HIP graph (stream capture) and replayed"},
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv) for kk, vv in e.items()}
                     for k, e in kernels.items()},
         "cpu_baseline": cpu,
