@@ -14,11 +14,14 @@
 //    stage shared by the 4 wavefronts (one barrier per step; the next
 //    step's W is loaded into registers while the MFMAs run); the W
 //    fragments are read from LDS two k-steps ahead of their MFMAs;
-//  * epilogue per step: the fp32 accumulators go through a per-wavefront
-//    LDS stage; read back along rows, they get the row scale, bias and
-//    residual and are stored (and residuals loaded) as 16-byte row segments.
+//  * epilogue per group of steps: the accumulators go through a
+//    per-wavefront LDS stage and are stored (and residuals loaded) along
+//    rows as 16-byte segments. An fp32 C is staged as fp32 and gets its row
+//    scale, bias and residual on the way out; a bf16 C is scaled and
+//    rounded in the accumulator layout and staged as bf16, which halves the
+//    stage so that three 128-row workgroups fit in a CU's LDS.
 //
-// A is read from memory exactly once and W once per 256 rows. K-order of
+// A is read from memory exactly once and W once per panel. K-order of
 // the fragments: k-step s covers k = 16s .. 16s+15, lane half g supplying
 // 16s + 8g .. +7, for A and W alike.
 #include "common.h"
@@ -74,15 +77,18 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
   // together, as whole lines
   constexpr int SPS = (!kF32C && MB == 1) ? 2 : 1;  // steps per store
   constexpr int CW = 32 * SPS;          // columns per store
-  constexpr int CP = CW + 4;            // fp32 pitch of the output stage (conflict-free both ways)
+  // the output stage holds fp32 values for an fp32 C and the finished bf16
+  // values for a bf16 C (half the LDS: three workgroups then fit on a CU)
+  constexpr int CP = kF32C ? CW + 4 : CW + 8;  // pitch in elements (conflict-free both ways)
   constexpr int APITCH = PK + 8;        // bf16 pitch of the A stage (80 or 144 B: conflict-free fragment reads)
   constexpr int kStageA = 32 * APITCH * 2;
-  constexpr int kStageC = RW * CP * 4;
+  constexpr int kStageC = RW * CP * (kF32C ? 4 : 2);
+  constexpr bool kGath = (FL & kGather) != 0;
 
   __shared__ __attribute__((aligned(16))) uint16_t sW[2][32 * WP];
   __shared__ __attribute__((aligned(16))) unsigned char sX[kWaves][cmax(kStageA, kStageC)];
-  __shared__ float sR[kWaves][RW];
-  __shared__ int sSrc[BM];
+  __shared__ __attribute__((aligned(16))) float sR[kWaves][RW];
+  __shared__ int sSrc[kGath ? BM : 1];
   __shared__ __attribute__((aligned(16))) float sG[kNorm ? KC * 64 : 4];
 
   const int tid = threadIdx.x;
@@ -93,12 +99,13 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
   if (row0 >= M) return;
   const int Kw = (p.K + 7) & ~7;  // W is zero-padded to here
 
-  // source row of each panel row (packed-token gather, or the row itself)
-  for (int r = tid; r < BM; r += kWaves * 64) {
-    const int grow = row0 + r;
-    int src = grow < M ? grow : -1;
-    if constexpr ((FL & kGather) != 0) {
-      if (src >= 0) {
+  // source row of each panel row: the packed-token gather, else the row
+  // itself (-1 past M)
+  if constexpr (kGath) {
+    for (int r = tid; r < BM; r += kWaves * 64) {
+      const int grow = row0 + r;
+      int src = -1;
+      if (grow < M) {
         int lo = 0, hi = p.B;
         while (hi - lo > 1) {
           const int mid = (lo + hi) >> 1;
@@ -106,16 +113,16 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
         }
         src = lo * p.L + (grow - p.offs[lo]);
       }
+      sSrc[r] = src;
     }
-    sSrc[r] = src;
   }
   if constexpr (kNorm) {
     for (int k = tid; k < KC * 64; k += kWaves * 64) sG[k] = k < p.K ? p.gain[k] : 0.f;
   }
 
   // W stage loads: unit i of this thread is row n = u / WU, k = 8 (u % WU);
-  // rows n >= N read zero through the resource, units past Kw are zeroed
-  // when staged (so nothing here waits for the load)
+  // rows n >= N and units past Kw read zero through the resource (an
+  // out-of-range offset), so staging is a plain copy of the loaded units
   const __amdgpu_buffer_rsrc_t wres = make_rsrc(p.W, (uint32_t)(p.N * p.ldw * 2));
   u32x4 rw[NW];
   const int nsteps = (p.N + 31) / 32;
@@ -124,15 +131,15 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
     for (int i = 0; i < NW; ++i) {
       const int u = tid + i * kWaves * 64;
       const int n = n0 + u / WU, k = 8 * (u % WU);
-      rw[i] = __builtin_amdgcn_raw_buffer_load_b128(wres, (uint32_t)((n * p.ldw + k) * 2), 0, 0);
+      rw[i] = __builtin_amdgcn_raw_buffer_load_b128(wres, k < Kw ? (uint32_t)((n * p.ldw + k) * 2) : kOutOfRange,
+                                                    0, 0);
     }
   };
   auto stage_w = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
       const int u = tid + i * kWaves * 64;
-      const int k = 8 * (u % WU);
-      *reinterpret_cast<u32x4*>(&sW[buf][(u / WU) * WP + k]) = k < Kw ? rw[i] : u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(&sW[buf][(u / WU) * WP + 8 * (u % WU)]) = rw[i];
     }
   };
   gload_w(0);  // in flight during the prologue
@@ -150,7 +157,10 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) srcs[mb][j] = sSrc[wave * RW + mb * 32 + (lane + 64 * j) / 8];
+    for (int j = 0; j < 4; ++j) {
+      const int r = wave * RW + mb * 32 + (lane + 64 * j) / 8;
+      srcs[mb][j] = kGath ? sSrc[r] : (row0 + r < M ? row0 + r : -1);
+    }
   u32x4 va[4], vn[4];  // raw 16-byte units (fp32 x4 or bf16 x8)
   auto gload_a = [&](int piece, u32x4* v) {
     const int mb = piece / KPIECES;
@@ -221,6 +231,7 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
 
   // ---- main loop over 32-column steps
   float* stC = reinterpret_cast<float*>(sX[wave]);
+  uint16_t* stB = reinterpret_cast<uint16_t*>(sX[wave]);
   // this panel's rows of C (and of the residual source R, same pitch)
   const uint32_t panel_bytes = (uint32_t)(min(BM, M - row0) * p.ldc * (int)sizeof(TC));
   const __amdgpu_buffer_rsrc_t cres =
@@ -228,66 +239,93 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
   const __amdgpu_buffer_rsrc_t rres = make_rsrc(
       (p.R ? p.R : reinterpret_cast<const float*>(p.C)) + ((FL & kResid) != 0 ? (int64_t)row0 * p.ldc : 0),
       (FL & kResid) != 0 ? panel_bytes : 0);
-  floatx16 acc[MB], accp[MB];  // this step's accumulators, and the group's previous step's
-  for (int s = 0; s < nsteps; ++s) {
-    const int buf = s & 1, n0 = s * 32;
-    stage_w(buf);
-    __syncthreads();  // W step s visible; every wavefront is past step s-1's reads of this buffer's pair
-    if (s + 1 < nsteps) gload_w(n0 + 32);
+  // Steps run in groups of SPS with one epilogue per group, and the next
+  // step's W is loaded on every step but the very last: every path from a
+  // W load to its staging then holds the same memory operations, so the
+  // compiler's wait for it is exact. (With a conditional epilogue the
+  // counts of the two paths merge to the smaller one, and a wavefront would
+  // wait for its own just-issued C stores before staging W.) When nsteps is
+  // odd the last group's extra step stages rows >= N, which read as zero.
+  const int ngroups = (nsteps + SPS - 1) / SPS;
+  for (int grp = 0; grp < ngroups; ++grp) {
+    floatx16 acc[SPS][MB];
+#pragma unroll
+    for (int h = 0; h < SPS; ++h) {
+      const int s = grp * SPS + h, buf = s & 1;
+      stage_w(buf);
+      __syncthreads();  // W step s visible; every wavefront is past step s-1's reads of this buffer's pair
+      if (s + 1 < ngroups * SPS) gload_w((s + 1) * 32);
 
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
-    // W fragments in a ring of 4, read three k-steps ahead so that LDS
-    // latency overlaps the MFMAs in between; the scheduling groups pin the
-    // order (three reads, then per k-step: two MFMAs, one read)
-    auto wfrag = [&](int ks) {
-      return __builtin_bit_cast(bf16x8,
-                                *reinterpret_cast<const u32x4*>(&sW[buf][li * WP + 16 * ks + 8 * lg]));
-    };
-    constexpr int AHEAD = NS < 3 ? NS : 3;
-    bf16x8 bq[4];
-#pragma unroll
-    for (int ks = 0; ks < AHEAD; ++ks) bq[ks] = wfrag(ks);
-    __builtin_amdgcn_sched_group_barrier(0x0100, AHEAD, 0);
-#pragma unroll
-    for (int ks = 0; ks < NS; ++ks) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb][ks], bq[ks & 3], acc[mb], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(0x0008, 2, 0);
-      if (ks + AHEAD < NS) {
-        bq[(ks + AHEAD) & 3] = wfrag(ks + AHEAD);
-        __builtin_amdgcn_sched_group_barrier(0x0100, 1, 0);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[h][mb][r] = 0.f;
+      // W fragments in a ring of 4, read three k-steps ahead so that LDS
+      // latency overlaps the MFMAs in between; the scheduling groups pin the
+      // order (three reads, then per k-step: its MB MFMAs, one read)
+      auto wfrag = [&](int ks) {
+        return __builtin_bit_cast(bf16x8,
+                                  *reinterpret_cast<const u32x4*>(&sW[buf][li * WP + 16 * ks + 8 * lg]));
+      };
+      constexpr int AHEAD = NS < 3 ? NS : 3;
+      bf16x8 bq[4];
+#pragma unroll
+      for (int ks = 0; ks < AHEAD; ++ks) bq[ks] = wfrag(ks);
+      __builtin_amdgcn_sched_group_barrier(0x0100, AHEAD, 0);
+#pragma unroll
+      for (int ks = 0; ks < NS; ++ks) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+          acc[h][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb][ks], bq[ks & 3], acc[h][mb], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x0008, MB, 0);
+        if (ks + AHEAD < NS) {
+          bq[(ks + AHEAD) & 3] = wfrag(ks + AHEAD);
+          __builtin_amdgcn_sched_group_barrier(0x0100, 1, 0);
+        }
       }
     }
 
-    // epilogue, after the last step of each group of SPS: accumulator layout
-    // (lane l: column l % 32, rows 8*(r/4) + 4*(l/32) + (r%4)) -> fp32
-    // row-major stage -> each lane finishes 8 consecutive columns of its
-    // rows: row scale, bias, residual, conversion, 16-byte stores
-    const int g0 = s - s % SPS;  // first step of this group
-    if (s != g0 + SPS - 1 && s + 1 < nsteps) {
+    // epilogue of the group: accumulator layout (lane l: column l % 32,
+    // rows 8*(r/4) + 4*(l/32) + (r%4)) -> row-major stage -> each lane
+    // finishes 8 consecutive columns of its rows with 16-byte stores. fp32
+    // C: staged as fp32, then row scale, bias, residual; bf16 C (no bias,
+    // no residual): row scale and rounding in the accumulator layout,
+    // staged as bf16
+    if constexpr (kF32C) {
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) accp[mb] = acc[mb];
-      continue;
+      for (int h = 0; h < SPS; ++h)
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = mb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+            stC[row * CP + 32 * h + li] = acc[h][mb][r];
+          }
+    } else {
+      static_assert(kF32C || (FL & (kBias | kResid)) == 0, "bf16 C takes neither bias nor residual");
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = mb * 32 + 8 * q + 4 * lg;  // rows row .. row + 3 of this lane
+          floatx4 sc = floatx4{1.f, 1.f, 1.f, 1.f};
+          if constexpr (kNorm) sc = *reinterpret_cast<const floatx4*>(&sR[wave][row]);
+#pragma unroll
+          for (int h = 0; h < SPS; ++h)
+#pragma unroll
+            for (int i = 0; i < 4; i += 2) {
+              const uint32_t w = pack2(acc[h][mb][4 * q + i] * sc[i], acc[h][mb][4 * q + i + 1] * sc[i + 1]);
+              stB[(row + i) * CP + 32 * h + li] = (uint16_t)(w & 0xFFFFu);
+              stB[(row + i + 1) * CP + 32 * h + li] = (uint16_t)(w >> 16);
+            }
+        }
     }
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = mb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-        if (s > g0) stC[row * CP + li] = accp[mb][r];
-        stC[row * CP + 32 * (s - g0) + li] = acc[mb][r];
-      }
     wave_lds_order();
     constexpr int LPR = CW / 8;          // lanes per row
     constexpr int RPI = 64 / LPR;        // rows per store instruction
     const int u = lane % LPR;  // 8-column unit of this lane (the same for all its rows)
-    const int c0 = g0 * 32 + 8 * u;
-    const bool staged = 8 * u < 32 * (s - g0 + 1);  // a group cut short by the last step
-    const bool ok0 = staged && c0 < p.N, ok1 = staged && c0 + 4 < p.N;  // N % 4 == 0: halves are all in or all out
+    const int c0 = grp * CW + 8 * u;
+    const bool ok0 = c0 < p.N, ok1 = c0 + 4 < p.N;  // N % 4 == 0: halves are all in or all out
     floatx4 b0 = floatx4{0.f, 0.f, 0.f, 0.f}, b1 = b0;
     if constexpr ((FL & kBias) != 0) {
       const floatx4 x0 = *reinterpret_cast<const floatx4*>(p.bias + (ok0 ? c0 : 0));
@@ -299,6 +337,14 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
     for (int i = 0; i < RW / RPI; ++i) {
       const int rl = lane / LPR + RPI * i;
       const int prow = wave * RW + rl;  // row within the panel; rows past M fall outside cres
+      const uint32_t off = (uint32_t)(prow * p.ldc + c0) * (uint32_t)sizeof(TC);
+      if constexpr (!kF32C) {
+        // N % 8 == 0 for bf16 C: a unit is all in or all out; stored
+        // non-temporal (a streamed output, re-read only by the next kernel)
+        const u32x4 w = *reinterpret_cast<const u32x4*>(&stB[rl * CP + 8 * u]);
+        __builtin_amdgcn_raw_buffer_store_b128(w, cres, ok0 ? off : kOutOfRange, 0, kStoreNT);
+        continue;
+      }
       floatx4 v0 = *reinterpret_cast<const floatx4*>(&stC[rl * CP + 8 * u]);
       floatx4 v1 = *reinterpret_cast<const floatx4*>(&stC[rl * CP + 8 * u + 4]);
       if constexpr (kNorm) {
@@ -308,8 +354,7 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
       }
       v0 += b0;
       v1 += b1;
-      const uint32_t off = (uint32_t)(prow * p.ldc + c0) * (uint32_t)sizeof(TC);
-      if constexpr (kF32C) {
+      {
         const uint32_t o0 = ok0 ? off : kOutOfRange, o1 = ok1 ? off + 16 : kOutOfRange;
         if constexpr ((FL & kResid) != 0) {
           v0 += __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(rres, o0, 0, 0));
@@ -317,11 +362,6 @@ __global__ __launch_bounds__(kWaves * 64, MB == 1 ? 3 : 2) void gemm_bf16_panel_
         }
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v0), cres, o0, 0, 0);
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v1), cres, o1, 0, 0);
-      } else {
-        // N % 8 == 0 for bf16 C: a unit is all in or all out; stored
-        // non-temporal (a streamed output, re-read only by the next kernel)
-        const u32x4 w = u32x4{pack2(v0.x, v0.y), pack2(v0.z, v0.w), pack2(v1.x, v1.y), pack2(v1.z, v1.w)};
-        __builtin_amdgcn_raw_buffer_store_b128(w, cres, ok0 ? off : kOutOfRange, 0, kStoreNT);
       }
     }
     wave_lds_order();
@@ -358,7 +398,7 @@ bool gemm_bf16_panel_fits(const GemmArgsBF16& a, bool bf16_out) {
   return a.K >= 1 && a.K <= 256 && pitch_bytes % 16 == 0 && al16(a.C) && (a.R == nullptr || al16(a.R)) &&
          (a.bias == nullptr || al16(a.bias)) && (!bf16_out || a.N % 8 == 0) &&
          // byte offsets of the buffer resources stay below 2^31
-         (int64_t)kWaves * 64 * pitch_bytes < (1ll << 31) && (int64_t)a.N * a.ldw * 2 < (1ll << 31);
+         (int64_t)kWaves * 64 * pitch_bytes < (1ll << 31) && (int64_t)(a.N + 64) * a.ldw * 2 < (1ll << 31);
 }
 
 hipError_t launch_gemm_bf16_panel(const GemmArgsBF16& a, GemmBF16Kind kind, int rows_per_wave, hipStream_t s) {
