@@ -19,6 +19,11 @@ __device__ __forceinline__ float silu_grad(float x) {
 
 __device__ __forceinline__ float ld_act(const float* p) { return *p; }
 __device__ __forceinline__ float ld_act(const uint16_t* p) { return bf16_to_f32(*p); }
+// an activation held as loaded (bf16 in the low half of a 32-bit register)
+// and widened to fp32 at use
+template <typename T> using act_raw_t = std::conditional_t<sizeof(T) == 2, uint32_t, float>;
+__device__ __forceinline__ float act_f32(float v) { return v; }
+__device__ __forceinline__ float act_f32(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
 
@@ -69,22 +74,50 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict_
   for (int i = 0; i < PL; ++i) dg[i] = 0.f;
   const int r0 = blockIdx.x * rows_per_block;
   const int r1 = min(r0 + rows_per_block, M);
-  for (int row = r0 + wave; row < r1; row += 4) {
-    const int64_t o = (int64_t)row * DM + lane * PL;
-    const float r = rstd[row];
-    float h[PL], gd[PL], dot = 0.f;
+  // rows of this wavefront in groups of U: the group's loads are issued
+  // together (one memory latency per group instead of one per row); a row
+  // past the block's range re-reads row r0 and is skipped at use
+  constexpr int U = 4;
+  float gl[PL];
 #pragma unroll
-    for (int i = 0; i < PL; ++i) {
-      h[i] = H[o + i];
-      const float dn = dN[o + i];
-      gd[i] = dn * g[lane * PL + i];
-      dot = fmaf(gd[i], h[i], dot);
-      dg[i] = fmaf(dn, h[i] * r, dg[i]);
+  for (int i = 0; i < PL; ++i) gl[i] = g[lane * PL + i];
+  for (int rw = r0 + wave; rw < r1; rw += 4 * U) {
+    float h[U][PL], dn[U][PL], dh[U][PL], r[U];
+#pragma unroll
+    for (int j = 0; j < U; ++j) {
+      const int row = rw + 4 * j < r1 ? rw + 4 * j : r0;
+      const int64_t o = (int64_t)row * DM + lane * PL;
+      r[j] = rstd[row];
+#pragma unroll
+      for (int i = 0; i < PL; ++i) {
+        h[j][i] = H[o + i];
+        dn[j][i] = dN[o + i];
+        dh[j][i] = dH[o + i];
+      }
     }
-    dot = wave_sum(dot);
-    const float c = r * r * r / (float)DM * dot;
+    // every row of the group is computed (so the loads above stay where
+    // they are: a per-row branch would let the compiler sink each row's
+    // loads to its use); rows past the range are neither stored nor summed
 #pragma unroll
-    for (int i = 0; i < PL; ++i) dH[o + i] += r * gd[i] - c * h[i];
+    for (int j = 0; j < U; ++j) {
+      const int row = rw + 4 * j;
+      const bool ok = row < r1;  // wave-uniform
+      const int64_t o = (int64_t)row * DM + lane * PL;
+      float gd[PL], dot = 0.f;
+#pragma unroll
+      for (int i = 0; i < PL; ++i) {
+        gd[i] = dn[j][i] * gl[i];
+        dot = fmaf(gd[i], h[j][i], dot);
+        const float dgi = fmaf(dn[j][i], h[j][i] * r[j], dg[i]);
+        dg[i] = ok ? dgi : dg[i];
+      }
+      dot = wave_sum(dot);
+      const float c = r[j] * r[j] * r[j] / (float)DM * dot;
+      if (ok) {
+#pragma unroll
+        for (int i = 0; i < PL; ++i) dH[o + i] = dh[j][i] + (r[j] * gd[i] - c * h[j][i]);
+      }
+    }
   }
 #pragma unroll
   for (int i = 0; i < PL; ++i) sdg[wave][lane * PL + i] = dg[i];
@@ -116,11 +149,15 @@ __global__ __launch_bounds__(256) void loss_head_bwd_kernel(
   float pw2 = 0.f, pb1 = 0.f;
   if (tid < h) {
     const float w2 = W2[tid];
+    float av[kHB];  // every program's activation loaded up front (one latency)
+#pragma unroll
+    for (int p = 0; p < kHB; ++p) av[p] = b0 + p < B ? a1[(int64_t)(b0 + p) * h + tid] : 0.f;
+#pragma unroll
     for (int p = 0; p < kHB; ++p) {
       const int b = b0 + p;
       float g = 0.f;
       if (b < B) {
-        const float a = a1[(int64_t)b * h + tid];
+        const float a = av[p];
         g = a > 0.f ? sds[p] * w2 : 0.f;
         pw2 = fmaf(sds[p], fmaxf(a, 0.f), pw2);
         da1[(int64_t)b * h + tid] = g;
@@ -134,6 +171,8 @@ __global__ __launch_bounds__(256) void loss_head_bwd_kernel(
     float acc[kHB];
 #pragma unroll
     for (int p = 0; p < kHB; ++p) acc[p] = 0.f;
+    // unrolled so that several rows of W1 are in flight at once
+#pragma unroll 8
     for (int j = 0; j < h; ++j) {
       const float w = W1[(int64_t)j * d + tid];
 #pragma unroll
@@ -200,28 +239,50 @@ __global__ __launch_bounds__(256) void normf_pool_bwd_kernel(const int* __restri
     gg[i] = final_norm ? g_f[lane * PL + i] : 1.f;
     dg[i] = 0.f;
   }
-  for (int t = wave; t < len; t += 4) {
-    const int64_t o = (int64_t)(base + t) * DM + lane * PL;
-    if (!final_norm) {
+  if (!final_norm) {
+    for (int t = wave; t < len; t += 4) {
+      const int64_t o = (int64_t)(base + t) * DM + lane * PL;
 #pragma unroll
       for (int i = 0; i < PL; ++i) dH[o + i] = dhf[i];
-      continue;
     }
-    float hv[PL], ss = 0.f, dot = 0.f;
+  } else {
+    // this wavefront's tokens in groups of U whose rows are loaded together
+    // (a token past the end re-reads the first row and is skipped)
+    constexpr int U = 4;
+    for (int t0 = wave; t0 < len; t0 += 4 * U) {
+      float hv[U][PL];
 #pragma unroll
-    for (int i = 0; i < PL; ++i) {
-      hv[i] = H[o + i];
-      ss = fmaf(hv[i], hv[i], ss);
-      dot = fmaf(gg[i] * dhf[i], hv[i], dot);
-    }
-    ss = wave_sum(ss);
-    dot = wave_sum(dot);
-    const float r = 1.0f / sqrtf(ss / (float)DM + eps);
-    const float c = r * r * r / (float)DM * dot;
+      for (int j = 0; j < U; ++j) {
+        const int t = t0 + 4 * j < len ? t0 + 4 * j : 0;
+        const int64_t o = (int64_t)(base + t) * DM + lane * PL;
 #pragma unroll
-    for (int i = 0; i < PL; ++i) {
-      dH[o + i] = r * gg[i] * dhf[i] - c * hv[i];
-      dg[i] = fmaf(dhf[i], hv[i] * r, dg[i]);
+        for (int i = 0; i < PL; ++i) hv[j][i] = H[o + i];
+      }
+      // every token of the group is computed (a per-token branch would let
+      // the compiler sink each token's loads to its use); tokens past the
+      // end are neither stored nor summed
+#pragma unroll
+      for (int j = 0; j < U; ++j) {
+        const int t = t0 + 4 * j;
+        const bool ok = t < len;  // wave-uniform
+        const int64_t o = (int64_t)(base + t) * DM + lane * PL;
+        float ss = 0.f, dot = 0.f;
+#pragma unroll
+        for (int i = 0; i < PL; ++i) {
+          ss = fmaf(hv[j][i], hv[j][i], ss);
+          dot = fmaf(gg[i] * dhf[i], hv[j][i], dot);
+        }
+        ss = wave_sum(ss);
+        dot = wave_sum(dot);
+        const float r = 1.0f / sqrtf(ss / (float)DM + eps);
+        const float c = r * r * r / (float)DM * dot;
+#pragma unroll
+        for (int i = 0; i < PL; ++i) {
+          if (ok) dH[o + i] = r * gg[i] * dhf[i] - c * hv[j][i];
+          const float dgi = fmaf(dhf[i], hv[j][i] * r, dg[i]);
+          dg[i] = ok ? dgi : dg[i];
+        }
+      }
     }
   }
 #pragma unroll
@@ -487,34 +548,70 @@ __global__ __launch_bounds__(256) void conv_bwd_kernel(const int* __restrict__ o
     dw[k] = 0.f;
   }
   // xw[k] = x_{t-K+1+k} for the current t (zero before the program start)
+  act_raw_t<T> xr[K];  // (an empty program reads row 0 and uses none of it)
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int tt = len - K + k;
-    xw[k] = tt >= 0 ? ld_act(x + (int64_t)(base + tt) * ldx + e) : 0.f;
-  }
+  for (int k = 0; k < K; ++k) xr[k] = x[(int64_t)(len > 0 ? base + max(len - K + k, 0) : 0) * ldx + e];
+#pragma unroll
+  for (int k = 0; k < K; ++k) xw[k] = len - K + k >= 0 ? act_f32(xr[k]) : 0.f;
   const float be = bias[e];
   float db = 0.f;
-  for (int t = len - 1; t >= 0; --t) {
-    float xc = be;
+  // tokens in groups of U, walked backwards; the next group's du and x
+  // values are loaded while the current group is processed (ping-pong
+  // between two register sets), so a group costs one memory latency
+  constexpr int U = 4;
+  // Loads are unconditional, from clamped rows (the program has a token
+  // when a group is loaded), and kept raw: values outside the program are
+  // zeroed, and bf16 widened, only at use, so nothing waits between loads.
+  using Raw = act_raw_t<T>;
+  auto load_group = [&](int t0, float* dv, Raw* xv) {  // tokens t0, t0 - 1, ..., t0 - U + 1
 #pragma unroll
-    for (int k = 0; k < K; ++k) xc = fmaf(wk[k], xw[k], xc);
-    const float dxc = du[(int64_t)(base + t) * E + e] * silu_grad(xc);
-    // future window: fut[j] = dxc_{t+j}
+    for (int j = 0; j < U; ++j) {
+      const int tt = t0 - j, tn = tt - K;
+      dv[j] = du[(int64_t)(base + max(tt, 0)) * E + e];
+      xv[j] = x[(int64_t)(base + max(tn, 0)) * ldx + e];
+    }
+  };
+  auto run_group = [&](int t0, const float* dv, const Raw* xv) {
 #pragma unroll
-    for (int j = K - 1; j > 0; --j) fut[j] = fut[j - 1];
-    fut[0] = dxc;
-    float dxv = 0.f;
+    for (int j = 0; j < U; ++j) {
+      const int t = t0 - j;
+      if (t < 0) break;  // block-uniform
+      float xc = be;
 #pragma unroll
-    for (int k = 0; k < K; ++k) dxv = fmaf(wk[k], fut[K - 1 - k], dxv);
-    dx[(int64_t)(base + t) * lddx + e] = dxv;
+      for (int k = 0; k < K; ++k) xc = fmaf(wk[k], xw[k], xc);
+      const float dxc = dv[j] * silu_grad(xc);  // t >= 0 here: dv[j] is token t's
+      // future window: fut[i] = dxc_{t+i}
 #pragma unroll
-    for (int k = 0; k < K; ++k) dw[k] = fmaf(dxc, xw[k], dw[k]);
-    db += dxc;
-    // slide the x window one token back
+      for (int i = K - 1; i > 0; --i) fut[i] = fut[i - 1];
+      fut[0] = dxc;
+      float dxv = 0.f;
 #pragma unroll
-    for (int k = K - 1; k > 0; --k) xw[k] = xw[k - 1];
-    const int tn = t - K;
-    xw[0] = tn >= 0 ? ld_act(x + (int64_t)(base + tn) * ldx + e) : 0.f;
+      for (int k = 0; k < K; ++k) dxv = fmaf(wk[k], fut[K - 1 - k], dxv);
+      dx[(int64_t)(base + t) * lddx + e] = dxv;
+#pragma unroll
+      for (int k = 0; k < K; ++k) dw[k] = fmaf(dxc, xw[k], dw[k]);
+      db += dxc;
+      // slide the x window one token back: xw[0] = x_{t-K}
+#pragma unroll
+      for (int k = K - 1; k > 0; --k) xw[k] = xw[k - 1];
+      xw[0] = t - K >= 0 ? act_f32(xv[j]) : 0.f;
+    }
+  };
+  // (the next group is loaded even when the program has none left: its rows
+  // clamp to the program's first token, so no load is conditional)
+  float da[U], dbv[U];
+  Raw xa[U], xb[U];
+  int t = len - 1;
+  if (t >= 0) load_group(t, da, xa);
+  for (;;) {
+    if (t < 0) break;  // da, xa hold the group at t
+    load_group(t - U, dbv, xb);
+    run_group(t, da, xa);
+    t -= U;
+    if (t < 0) break;  // dbv, xb hold the group at t
+    load_group(t - U, da, xa);
+    run_group(t, dbv, xb);
+    t -= U;
   }
   float* o = part + (int64_t)b * (K + 1) * E + e;
 #pragma unroll
@@ -533,14 +630,16 @@ __global__ __launch_bounds__(256) void colsum_kernel(const int* __restrict__ Mde
   const int r0 = blockIdx.y * rows_per_split;
   const int r1 = min(r0 + rows_per_split, M);
   float acc = 0.f;
+  // unrolled so that several rows' loads are in flight (the sum stays sequential)
+#pragma unroll 8
   for (int m = r0; m < r1; ++m) acc += A[(int64_t)m * lda + c];
   part[(int64_t)blockIdx.y * C + c] = acc;
 }
 
 // ---------------------------------------------------------------- reductions
 // blockIdx.y picks the job. A block takes 64 consecutive outputs; its 16
-// wavefronts each sum a contiguous sixteenth of the splits with four
-// independent partial sums (four loads in flight per lane), then the partial
+// wavefronts each sum a contiguous sixteenth of the splits with eight
+// independent partial sums (eight loads in flight per lane), then the partial
 // sums and the sixteenths are added in a fixed order (deterministic for a
 // given split count).
 constexpr int kRedGroups = 16;
@@ -559,19 +658,17 @@ __global__ __launch_bounds__(64 * kRedGroups) void reduce_kernel(const ReduceJob
   const int s0 = q * per, s1 = min(s0 + per, J.nsplit);
   for (int64_t i0 = (int64_t)blockIdx.x * 64; i0 < J.n; i0 += (int64_t)gridDim.x * 64) {
     const int64_t i = i0 + lane;
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (i < J.n) {
       const float* p = src + i * J.src_stride;
       int s = s0;
-      for (; s + 3 < s1; s += 4) {
-        a0 += p[(int64_t)s * J.split_stride];
-        a1 += p[(int64_t)(s + 1) * J.split_stride];
-        a2 += p[(int64_t)(s + 2) * J.split_stride];
-        a3 += p[(int64_t)(s + 3) * J.split_stride];
+      for (; s + 7 < s1; s += 8) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) a[k] += p[(int64_t)(s + k) * J.split_stride];
       }
-      for (; s < s1; ++s) a0 += p[(int64_t)s * J.split_stride];
+      for (; s < s1; ++s) a[0] += p[(int64_t)s * J.split_stride];
     }
-    sq[q][lane] = (a0 + a1) + (a2 + a3);
+    sq[q][lane] = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
     __syncthreads();
     if (q == 0 && i < J.n) {
       float t = 0.f;
