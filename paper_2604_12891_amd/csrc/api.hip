@@ -228,9 +228,11 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   return TCL_OK;
 }
 
-tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
-                     float* d_scores, char* ws, hipStream_t s) {
+tcl_status run_score_part(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
+                          float* d_scores, char* ws, hipStream_t s, int part) {
   const tcl_config& c = m->cfg;
+  const bool front = part == 0, tail = part == c.n_layers + 1;
+  const int layer = part - 1;  // the block this part runs, when neither front nor tail
   const ScorePlan p = score_plan(c, B, L);
   int* offs = reinterpret_cast<int*>(ws + p.offs);
   float* H = reinterpret_cast<float*>(ws + p.H);
@@ -240,16 +242,27 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
   const int chunks = scan_chunks_for(B, E, L);
   Timing& T = m->timing;
 
-  TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  if (front) TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
   uint8_t* tpos = reinterpret_cast<uint8_t*>(ws + p.tpos);
   // features whose row length is not a multiple of 4 are first copied into
   // rows padded with zeros (the input Linear reads 16-byte vectors)
   const float* feats = d_feats;
   const int ldf = (c.F + 3) & ~3;
-  if (ldf != c.F) {
+  if (front && ldf != c.F) {
     float* fp = reinterpret_cast<float*>(ws + p.feats);
     TCL_LAUNCH(T, "pad_features", launch_pad_rows(d_feats, (int64_t)B * L, c.F, ldf, fp, s));
     feats = fp;
+  }
+  if (tail) {
+    if (c.dec_hidden2 > 0)
+      TCL_LAUNCH(T, "tail", launch_tail3_f32(B, L, d, c.head_hidden, c.dec_hidden2, offs, d_lengths, H, m->g_f,
+                                             c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2T, m->b2, m->W3,
+                                             m->b3, d_scores, s));
+    else
+      TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
+                                            c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2, m->b2,
+                                            d_scores, s));
+    return TCL_OK;
   }
   if (c.dtype == TCL_F32) {
     float* xz = reinterpret_cast<float*>(ws + p.xz);
@@ -257,30 +270,32 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
     // encoder: the gathered input Linear, then (multi-layer encoder) the
     // hidden Linear layers on the packed rows, a ReLU after every layer but
     // the last
-    const int n_enc = blob_layout(c).n_enc;
-    float* bufs[2] = {reinterpret_cast<float*>(ws + p.enc1), reinterpret_cast<float*>(ws + p.enc2)};
-    bool tpos_done = false;
-    for (int i = 0; i < n_enc; ++i) {
-      const bool last = i == n_enc - 1;
-      tcl_status st = enqueue_encoder_layer_f32(m, T, "", i, B, L, offs, i == 0 ? feats : bufs[i - 1],
-                                                last ? H : bufs[i], !last, s, m->split ? tpos : nullptr,
-                                                i == 0 ? &tpos_done : nullptr);
-      if (st != TCL_OK) return st;
+    if (front) {
+      const int n_enc = blob_layout(c).n_enc;
+      float* bufs[2] = {reinterpret_cast<float*>(ws + p.enc1), reinterpret_cast<float*>(ws + p.enc2)};
+      bool tpos_done = false;
+      for (int i = 0; i < n_enc; ++i) {
+        const bool last = i == n_enc - 1;
+        tcl_status st = enqueue_encoder_layer_f32(m, T, "", i, B, L, offs, i == 0 ? feats : bufs[i - 1],
+                                                  last ? H : bufs[i], !last, s, m->split ? tpos : nullptr,
+                                                  i == 0 ? &tpos_done : nullptr);
+        if (st != TCL_OK) return st;
+      }
+      // the token positions for the conv fused into x_proj, unless the input Linear wrote them
+      if (m->split && !tpos_done) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
+      return TCL_OK;
     }
-    // the token positions for the conv fused into x_proj, unless the input Linear wrote them
-    if (m->split && !tpos_done) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
-    for (int l = 0; l < c.n_layers; ++l) {
-      tcl_status st = enqueue_block_f32(m, T, "", l, B, L, offs, m->split ? tpos : nullptr, H, xz, u, xdbl, s);
-      if (st != TCL_OK) return st;
-    }
+    return enqueue_block_f32(m, T, "", layer, B, L, offs, m->split ? tpos : nullptr, H, xz, u, xdbl, s);
   } else {
     uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
     uint16_t* u = reinterpret_cast<uint16_t*>(ws + p.u);
-    GemmArgsBF16 g;
-    g.A = feats; g.lda = ldf; g.offs = offs; g.B = B; g.L = L;
-    g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
-    g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = ldf;
-    TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
+    if (front) {
+      GemmArgsBF16 g;
+      g.A = feats; g.lda = ldf; g.offs = offs; g.B = B; g.L = L;
+      g.W = m->W0_h; g.ldw = m->ldw0_h; g.bias = m->b0; g.C = H; g.ldc = d;
+      g.Mdev = offs + B; g.Mmax = Mmax; g.N = d; g.K = ldf;
+      TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
+    }
 
     // the conv + SiLU fused in front of x_proj where the shape allows
     auto conv_args = [&](int l) {
@@ -291,9 +306,12 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       return a;
     };
     const bool fuse = gemm_bf16_conv_supports(conv_args(0), c.d_conv);
-    if (fuse) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
-
-    for (int l = 0; l < c.n_layers; ++l) {
+    if (front) {
+      if (fuse) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
+      return TCL_OK;
+    }
+    {
+      const int l = layer;
       const auto& W = m->layers[l];
       GemmArgsBF16 gi;
       gi.A = H; gi.lda = d; gi.W = W.W_in_h; gi.ldw = d; gi.gain = W.g; gi.C = xz; gi.ldc = 2 * E;
@@ -324,14 +342,15 @@ tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int
       TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, -1, s));
     }
   }
-  if (c.dec_hidden2 > 0)
-    TCL_LAUNCH(T, "tail", launch_tail3_f32(B, L, d, c.head_hidden, c.dec_hidden2, offs, d_lengths, H, m->g_f,
-                                           c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2T, m->b2, m->W3,
-                                           m->b3, d_scores, s));
-  else
-    TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, c.head_hidden, offs, d_lengths, H, m->g_f,
-                                          c.final_norm, c.norm_eps, m->W1T, m->b1, m->W2, m->b2,
-                                          d_scores, s));
+  return TCL_OK;
+}
+
+tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
+                     float* d_scores, char* ws, hipStream_t s) {
+  for (int part = 0; part <= m->cfg.n_layers + 1; ++part) {
+    const tcl_status st = run_score_part(m, B, L, d_feats, d_lengths, d_scores, ws, s, part);
+    if (st != TCL_OK) return st;
+  }
   return TCL_OK;
 }
 
@@ -798,11 +817,16 @@ TCL_API tcl_status tcl_score(tcl_model* m, int32_t B, int32_t L, const float* d_
   TCL_HIP(hipEventRecord(m->ev[0], s));
   TCL_HIP(hipStreamWaitEvent(m->aux[0], m->ev[0], 0));
   TCL_HIP(hipStreamWaitEvent(m->aux[1], m->ev[0], 0));
-  tcl_status st = run_score(m, h, L, d_feats, d_lengths, d_scores, ws, m->aux[0]);
-  if (st != TCL_OK) return st;
-  st = run_score(m, B - h, L, d_feats + (int64_t)h * L * m->cfg.F, d_lengths + h, d_scores + h, ws + off2,
-                 m->aux[1]);
-  if (st != TCL_OK) return st;
+  // the halves' launches alternate part by part (the front, each block, the
+  // tail), so that the second half starts after the first half's first part
+  // is enqueued rather than after all of it
+  for (int part = 0; part <= m->cfg.n_layers + 1; ++part) {
+    tcl_status st = run_score_part(m, h, L, d_feats, d_lengths, d_scores, ws, m->aux[0], part);
+    if (st != TCL_OK) return st;
+    st = run_score_part(m, B - h, L, d_feats + (int64_t)h * L * m->cfg.F, d_lengths + h, d_scores + h,
+                        ws + off2, m->aux[1], part);
+    if (st != TCL_OK) return st;
+  }
   TCL_HIP(hipEventRecord(m->ev[1], m->aux[0]));
   TCL_HIP(hipEventRecord(m->ev[2], m->aux[1]));
   TCL_HIP(hipStreamWaitEvent(s, m->ev[1], 0));

@@ -158,9 +158,14 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
                              const int* offs, const uint8_t* tpos, float* H, float* xz, float* u, float* xdbl,
                              hipStream_t s);
 
-// Enqueue the scoring pass (no argument checks).
+// Enqueue the scoring pass (no argument checks): its parts in order.
 tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
                      float* d_scores, char* ws, hipStream_t s);
+// One part of the scoring pass: 0 the front (token offsets, the encoder),
+// 1 .. n_layers the Mamba block part - 1, n_layers + 1 the tail (pool and
+// head). The parts of one batch run in order on one stream.
+tcl_status run_score_part(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,
+                          float* d_scores, char* ws, hipStream_t s, int part);
 
 // Re-derive every weight layout from the device master blob (stream-ordered).
 tcl_status derive_weights(tcl_model* m, hipStream_t s);
