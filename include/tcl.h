@@ -520,6 +520,9 @@ TCL_API tcl_status tcl_test_gemm_split(int32_t M, int32_t N, int32_t K, const fl
  *      row d_offs[b] + t is A[b, t, :] (d_offs [B+1] int32 prefix sums of
  *      lengths in 0..L); C holds B*L rows (only the first d_offs[B] are
  *      written) and M is ignored
+ *   5: C fp32 = bf16(A) W^T, A fp32 rounded to bf16 (nearest even) as it is
+ *      staged (the distillation backward's data gradients; tiles only)
+ *   6: C fp32 += bf16(A) W^T, A fp32 as in 5 (C read in place; tiles only)
  * Other arguments are ignored (may be NULL / 0) for kinds that do not use
  * them. bf16 arrays are bit patterns. W is [N, Kw] bf16 with Kw = K rounded
  * up to a multiple of 8, zero-padded. K % 8 == 0 for bf16 A, K % 4 == 0 for

@@ -482,7 +482,8 @@ def gemm_split(A, W, bias=None, out=None, stream=None, variant=-1, epilogue=0, o
     return out
 
 
-GEMM_BF16_F32, GEMM_BF16_BF16, GEMM_BF16_NORM, GEMM_BF16_RESID, GEMM_BF16_GATHER = range(5)
+(GEMM_BF16_F32, GEMM_BF16_BF16, GEMM_BF16_NORM, GEMM_BF16_RESID, GEMM_BF16_GATHER, GEMM_BF16_F32A,
+ GEMM_BF16_F32A_RESID) = range(7)
 
 
 def gemm_bf16(A, W, bias=None, out=None, stream=None, kind=GEMM_BF16_F32, tile=-1, gain=None, offs=None):
@@ -491,7 +492,9 @@ def gemm_bf16(A, W, bias=None, out=None, stream=None, kind=GEMM_BF16_F32, tile=-
     GEMM_BF16_F32: A bf16 [M,K] -> fp32 (+ bias); GEMM_BF16_BF16: -> bf16;
     GEMM_BF16_NORM: A fp32 -> RMSNorm(gain) -> bf16; GEMM_BF16_RESID: out
     (fp32, required) += A W^T; GEMM_BF16_GATHER: A fp32 [B, L, K] gathered
-    by offs [B+1] -> fp32 + bias, out [B*L, N]."""
+    by offs [B+1] -> fp32 + bias, out [B*L, N]; GEMM_BF16_F32A: A fp32
+    (rounded to bf16) -> fp32; GEMM_BF16_F32A_RESID: out (fp32, required)
+    += bf16(A) W^T."""
     import torch
     N = W.shape[0]
     if kind == GEMM_BF16_GATHER:
@@ -502,8 +505,8 @@ def gemm_bf16(A, W, bias=None, out=None, stream=None, kind=GEMM_BF16_F32, tile=-
     if W.shape[1] != (K + 7) // 8 * 8:
         raise ValueError(f"W must be [N, {(K + 7) // 8 * 8}] (K zero-padded to a multiple of 8)")
     if out is None:
-        if kind == GEMM_BF16_RESID:
-            raise ValueError("GEMM_BF16_RESID accumulates into out")
+        if kind in (GEMM_BF16_RESID, GEMM_BF16_F32A_RESID):
+            raise ValueError("the residual kinds accumulate into out")
         bf16_out = kind in (GEMM_BF16_BF16, GEMM_BF16_NORM)
         out = torch.empty(M, N, dtype=torch.bfloat16 if bf16_out else torch.float32, device=A.device)
     check(lib().tcl_test_gemm_bf16(kind, tile, M, N, K, A.data_ptr(), _ptr(offs), Bp, L, W.data_ptr(),

@@ -415,6 +415,7 @@ struct ModelPlan {
   struct L {
     size_t W_in_fold, g, conv_w, conv_b, W_x, W_dt, b_dt, A_log, D, W_out;
     size_t W_outT, W_xT, W_inT, W_dtT, W_in_h, W_x_h, W_out_h, W_in_s, W_x_s, W_out_s, W_in_h2, W_out_h2;
+    size_t W_outT_h, W_xT_h, W_inT_h;
   };
   std::vector<L> layers;
   int ldw0_h = 0;
@@ -502,6 +503,9 @@ ModelPlan plan_model(const tcl_config& c) {
       L.W_in_h = job(B.W_in, 2 * E, d, kDeriveBF16, 0, 2);
       L.W_x_h = job(B.W_x, XW, E, kDeriveBF16, 0, 2);
       L.W_out_h = job(B.W_out, d, E, kDeriveBF16, 0, 2);
+      L.W_outT_h = job(B.W_out, d, E, kDeriveBF16, 1, 2);
+      L.W_xT_h = job(B.W_x, XW, E, kDeriveBF16, 1, 2);
+      L.W_inT_h = job(B.W_in, 2 * E, d, kDeriveBF16, 1, 2);
     }
     if (sp) {
       L.W_in_s = job(B.W_in, 2 * E, d, kDeriveFoldSplit, 0, 2, -1, B.g);
@@ -702,6 +706,9 @@ TCL_API tcl_status tcl_cost_model_create(const tcl_config* cfg, const float* h_p
       W.W_in_h = B16(L.W_in_h);
       W.W_x_h = B16(L.W_x_h);
       W.W_out_h = B16(L.W_out_h);
+      W.W_outT_h = B16(L.W_outT_h);
+      W.W_xT_h = B16(L.W_xT_h);
+      W.W_inT_h = B16(L.W_inT_h);
     }
     if (m->split) {
       W.W_in_s = B16(L.W_in_s);
@@ -1030,11 +1037,11 @@ TCL_API tcl_status tcl_test_gemm_bf16(int32_t kind, int32_t tile, int32_t M, int
                                       const void* d_A, const int32_t* d_offs, int32_t B, int32_t L,
                                       const uint16_t* d_W, const float* d_bias, const float* d_gain,
                                       void* d_C, void* stream) {
-  static const GemmBF16Kind kinds[5] = {kBF16toF32, kBF16toBF16, kNormF32toBF16, kBF16ResidF32,
-                                        kInputF32toF32};
-  if (kind < 0 || kind > 4) return fail(TCL_ERR_INVALID_ARG, "kind must be 0..4 (got %d)", kind);
+  static const GemmBF16Kind kinds[7] = {kBF16toF32, kBF16toBF16, kNormF32toBF16, kBF16ResidF32,
+                                        kInputF32toF32, kF32toF32, kF32ResidF32};
+  if (kind < 0 || kind > 6) return fail(TCL_ERR_INVALID_ARG, "kind must be 0..6 (got %d)", kind);
   if (tile < -1 || tile >= kNumGemmBF16Tiles) return fail(TCL_ERR_INVALID_ARG, "tile must be -1..%d", kNumGemmBF16Tiles - 1);
-  const bool f32a = kind == 2 || kind == 4;
+  const bool f32a = kind == 2 || kind == 4 || kind == 5 || kind == 6;
   if (kind == 4) {
     if (B <= 0 || L <= 0 || !d_offs) return fail(TCL_ERR_INVALID_ARG, "gather needs d_offs, B > 0, L > 0");
     M = B * L;

@@ -317,7 +317,7 @@ GemmBF16Tile pick_gemm_bf16_tile(GemmBF16Kind kind, int Mmax, int N, int K) {
   // (distillation) 128x64 wins for N <= 256 (7.2 vs 9.4 at N = 128, 11.9 vs
   // 13.5 at 256).
   if (N <= 64) return kB64x64;
-  if (K <= 256 && Mmax >= 131072)
+  if (K <= 256 && Mmax >= 131072 && kind != kF32toF32 && kind != kF32ResidF32)
     return kind == kInputF32toF32 || kind == kNormF32toBF16 || kind == kBF16toBF16 ? kBPanel128 : kBPanel;
   if (Mmax < 131072 && N <= 256) return kB128x64;
   return kB128x128;
@@ -346,6 +346,10 @@ hipError_t launch_gemm_bf16(const GemmArgsBF16& a, GemmBF16Kind kind, int tile, 
       return dispatch_tile<uint16_t, float, kBias>(a, t, s);
     case kBF16toBF16:
       return dispatch_tile<uint16_t, uint16_t, 0>(a, t, s);
+    case kF32toF32:  // fp32 gradients -> fp32 (the backward's data gradients)
+      return dispatch_tile<float, float, 0>(a, t, s);
+    case kF32ResidF32:
+      return dispatch_tile<float, float, kResid>(a, t, s);
   }
   return hipErrorInvalidValue;
 }

@@ -410,6 +410,8 @@ hipError_t launch_gemm_bf16_panel(const GemmArgsBF16& a, GemmBF16Kind kind, int 
     case kBF16toF32: return launch_mb<uint16_t, float, 0>(a, rows_per_wave, s);
     case kBF16toF32Bias: return launch_mb<uint16_t, float, kBias>(a, rows_per_wave, s);
     case kBF16toBF16: return launch_mb<uint16_t, uint16_t, 0>(a, rows_per_wave, s);
+    case kF32toF32:
+    case kF32ResidF32: return hipErrorInvalidValue;  // tiles only
   }
   return hipErrorInvalidValue;
 }

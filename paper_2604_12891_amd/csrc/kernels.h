@@ -171,6 +171,8 @@ enum GemmBF16Kind {
   kBF16toF32,        // bf16 -> fp32
   kBF16toF32Bias,    // bf16 -> fp32, + bias
   kBF16toBF16,       // bf16 -> bf16
+  kF32toF32,         // fp32 (rounded to bf16 as staged) -> fp32
+  kF32ResidF32,      // fp32 (rounded to bf16 as staged) -> fp32 C += result
 };
 
 // Workgroup tiles (rows x columns of C): 4 wavefronts unless noted.

@@ -102,6 +102,8 @@ struct tcl_model {
     float *W_outT, *W_xT, *W_inT, *W_dtT;
     // bf16 copies (bf16 models)
     uint16_t *W_in_h, *W_x_h, *W_out_h;
+    // transposed bf16 copies for the backward pass's data gradients (bf16 models)
+    uint16_t *W_outT_h, *W_xT_h, *W_inT_h;
     // three-way bf16 splits, [3][rows][cols] (fp32 models on the split path):
     // W_in with the gain folded, W_x, W_out
     uint16_t *W_in_s, *W_x_s, *W_out_s;

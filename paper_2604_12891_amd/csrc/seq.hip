@@ -555,10 +555,29 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
     const float bj = b1[tid];
 #pragma unroll
     for (int p = 0; p < kTailPB; ++p) a[p] = bj;
-    for (int k = 0; k < DM; ++k) {
-      const float wv = W1T[k * h + tid];
+    // W1 in batches of KB rows, the next batch loaded while the current one
+    // is used (L2 latency, not the FMAs, bounds this loop); fully unrolled,
+    // so the batches are fixed registers and no load is conditional
+    constexpr int KB = kTailPB > 4 ? 8 : 16;  // (more programs: more FMAs per row, fewer rows needed in flight)
+    static_assert(DM % (2 * KB) == 0, "whole pairs of W1 batches");
+    float wa[KB], wb[KB];
+    auto load_w = [&](int k0, float* w) {
 #pragma unroll
-      for (int p = 0; p < kTailPB; ++p) a[p] = fmaf(wv, sP[k][p], a[p]);
+      for (int j = 0; j < KB; ++j) w[j] = W1T[(k0 + j) * h + tid];
+    };
+    auto use_w = [&](int k0, const float* w) {
+#pragma unroll
+      for (int j = 0; j < KB; ++j)
+#pragma unroll
+        for (int p = 0; p < kTailPB; ++p) a[p] = fmaf(w[j], sP[k0 + j][p], a[p]);
+    };
+    load_w(0, wa);
+#pragma unroll
+    for (int k0 = 0; k0 < DM; k0 += 2 * KB) {
+      load_w(k0 + KB, wb);
+      use_w(k0, wa);
+      if (k0 + 2 * KB < DM) load_w(k0 + 2 * KB, wa);
+      use_w(k0 + KB, wb);
     }
     if constexpr (DEC3) {
 #pragma unroll
@@ -582,6 +601,7 @@ __global__ __launch_bounds__(256) void tail_kernel(int B, int L, int h, const in
       const float bj = b2[tid];
 #pragma unroll
       for (int p = 0; p < kTailPB; ++p) a[p] = bj;
+#pragma unroll 32
       for (int k = 0; k < h; ++k) {
         const float wv = W2[k * h2 + tid];
 #pragma unroll

@@ -447,15 +447,28 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     const tcl_status st_ = (X);           \
     if (st_ != TCL_OK) return st_;        \
   } while (0)
+  // Data-gradient GEMMs C (+)= A W with A an fp32 gradient: for a bf16
+  // student on the bf16 matrix cores (A rounded to bf16 as it is staged, W
+  // the transposed bf16 copy, fp32 accumulation), else on the fp32 ones.
+  const bool bf16_dx = c.dtype == TCL_BF16;
+  auto gemm_dx = [&](const float* A, int lda, const float* Wt32, const uint16_t* Wt16, int ldw, float* C,
+                     int ldc, int N_, int K_, bool accumulate) -> hipError_t {
+    if (bf16_dx) {
+      GemmArgsBF16 g;
+      g.A = A; g.lda = lda; g.W = Wt16; g.ldw = ldw; g.C = C; g.ldc = ldc;
+      g.Mdev = Mdev; g.Mmax = Mmax; g.N = N_; g.K = K_;
+      return launch_gemm_bf16(g, accumulate ? kF32ResidF32 : kF32toF32, -1, s);
+    }
+    GemmArgs g;
+    g.A = A; g.lda = lda; g.W = Wt32; g.ldw = ldw; g.C = C; g.ldc = ldc;
+    g.Mdev = Mdev; g.Mmax = Mmax; g.N = N_; g.K = K_;
+    return launch_gemm_f32(g, accumulate ? kResid : 0, -1, s);
+  };
   for (int l = c.n_layers - 1; l >= 0; --l) {
     const auto& W = S->layers[l];
     const auto& Ly = P.layers[l];
-    {  // dyg = dH W_out
-      GemmArgs g;
-      g.A = F32(P.dH); g.lda = d; g.W = W.W_outT; g.ldw = d; g.C = F32(P.dyg); g.ldc = E;
-      g.Mdev = Mdev; g.Mmax = Mmax; g.N = E; g.K = d;
-      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, -1, s));
-    }
+    // dyg = dH W_out
+    TCL_LAUNCH(T, "gemm_dX", gemm_dx(F32(P.dH), d, W.W_outT, W.W_outT_h, d, F32(P.dyg), E, E, d, false));
     TCL_TRY(fork_side());
     {  // dW_out = dH^T yg
       GemmTNArgs a;
@@ -484,12 +497,8 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_F32, Ly.s_Wdt, s));
     }
     TCL_SIDE("colsum", launch_colsum(Mdev, Mmax, F32(P.dv), E, E, P.cs, F32(Ly.p_bdt), s));
-    {  // du += dxdbl W_x
-      GemmArgs g;
-      g.A = F32(P.dxdbl); g.lda = XW; g.W = W.W_xT; g.ldw = XW; g.C = F32(P.du); g.ldc = E;
-      g.Mdev = Mdev; g.Mmax = Mmax; g.N = E; g.K = XW;
-      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, kResid, -1, s));
-    }
+    // du += dxdbl W_x
+    TCL_LAUNCH(T, "gemm_dX", gemm_dx(F32(P.dxdbl), XW, W.W_xT, W.W_xT_h, XW, F32(P.du), E, E, XW, true));
     TCL_TRY(fork_side());
     {  // dW_x = dxdbl^T u
       GemmTNArgs a;
@@ -499,12 +508,8 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     }
     TCL_LAUNCH(T, "conv_bwd", launch_conv_bwd(B, E, K, offs, B16(Ly.xz), 2 * E, W.conv_w, W.conv_b,
                                               F32(P.du), F32(P.dxz), 2 * E, F32(Ly.p_conv), s));
-    {  // dN = dxz W_in
-      GemmArgs g;
-      g.A = F32(P.dxz); g.lda = 2 * E; g.W = W.W_inT; g.ldw = 2 * E; g.C = F32(P.dN); g.ldc = d;
-      g.Mdev = Mdev; g.Mmax = Mmax; g.N = d; g.K = 2 * E;
-      TCL_LAUNCH(T, "gemm_dX", launch_gemm_f32(g, 0, -1, s));
-    }
+    // dN = dxz W_in
+    TCL_LAUNCH(T, "gemm_dX", gemm_dx(F32(P.dxz), 2 * E, W.W_inT, W.W_inT_h, 2 * E, F32(P.dN), d, d, 2 * E, false));
     TCL_TRY(fork_side());
     {  // dW_in = dxz^T n
       GemmTNArgs a;

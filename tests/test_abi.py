@@ -135,10 +135,12 @@ def test_bf16_gemm_entry_rejects_bad_arguments(lib):
         a = dict(args, **kw)
         return lib.tcl_test_gemm_bf16(*a.values())
 
-    assert call(kind=5) == -1
+    assert call(kind=7) == -1
+    assert call(kind=-1) == -1
     assert call(tile=9) == -1
     assert call(N=6) == -1            # N % 4
     assert call(K=12) == -1           # bf16 A needs K % 8
+    assert call(kind=5, K=6) == -1    # fp32 A needs K % 4
     assert call(A=None) == -1
     assert call(kind=2) == -1         # the RMSNorm variant needs the gain
     assert call(kind=4) == -1         # the gather needs offsets and B, L

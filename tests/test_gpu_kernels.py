@@ -191,8 +191,11 @@ def _bf16_w(N, K, rng):
     return W
 
 
+_BF16_KINDS = ["f32", "bf16", "norm", "resid", "gather", "f32a", "f32a_resid"]
+
+
 @pytest.mark.parametrize("tile", [-1, 0, 1, 2, 3, 4, 5, 6, 7, 8])
-@pytest.mark.parametrize("kind", ["f32", "bf16", "norm", "resid", "gather"])
+@pytest.mark.parametrize("kind", _BF16_KINDS)
 def test_gemm_bf16_variants(kind, tile):
     """Every bf16 GEMM variant the model runs, on every tile, with ragged M, N
     and K. Where the kernel rounds an fp32 operand to bf16 (A, or A * gain),
@@ -200,8 +203,18 @@ def test_gemm_bf16_variants(kind, tile):
     values are then exact), so the bound is that of fp32 accumulation, plus
     the bf16 unit roundoff 2^-8 where the output is bf16."""
     print(f"gemm_bf16 kind={kind} tile={tile}", flush=True)
-    rng = np.random.default_rng(["f32", "bf16", "norm", "resid", "gather"].index(kind) * 10 + tile + 1)
-    f32a = kind in ("norm", "gather")
+    rng = np.random.default_rng(_BF16_KINDS.index(kind) * 10 + tile + 1)
+    f32a = kind in ("norm", "gather", "f32a", "f32a_resid")
+    if kind.startswith("f32a") and tile in (7, 8):
+        # the fp32-A kinds (the distillation backward) run on tiles only: an
+        # explicit row-panel tile is refused
+        A = _dev(rng.standard_normal((64, 164)).astype(np.float32))
+        W = _dev(_bf16_w(196, 164, rng), torch.bfloat16)
+        out = torch.zeros(64, 196, device="cuda")
+        k = tb.GEMM_BF16_F32A if kind == "f32a" else tb.GEMM_BF16_F32A_RESID
+        with pytest.raises(tb.TclError):
+            tb.gemm_bf16(A, W, out=out, kind=k, tile=tile)
+        return
     # bf16 rows of C must be 16-byte aligned for the row-panel tile
     M, N, K = 1000, (200 if kind in ("bf16", "norm") else 196), (164 if f32a else 168)
     W = _bf16_w(N, K, rng)
@@ -226,6 +239,21 @@ def test_gemm_bf16_variants(kind, tile):
         Ah = wl.round_to_bf16(_pack(Ap, lengths)).astype(np.float64)
         ref = Ah @ Wk.T + bv
         bound = (K + 2) * U * (np.abs(Ah) @ np.abs(Wk).T) + U * np.abs(ref)
+    elif kind in ("f32a", "f32a_resid"):
+        A = (2.0 * rng.standard_normal((M, K))).astype(np.float32)
+        Ah = wl.round_to_bf16(A).astype(np.float64)  # the kernel rounds A to bf16 (RNE) as it stages it
+        prod = Ah @ Wk.T
+        mag = (K + 2) * U * (np.abs(Ah) @ np.abs(Wk).T)
+        if kind == "f32a":
+            got = tb.gemm_bf16(_dev(A), Wd, kind=tb.GEMM_BF16_F32A, tile=tile)
+            ref, bound = prod, mag + U * np.abs(prod)
+        else:
+            C0 = rng.standard_normal((M, N)).astype(np.float32)
+            got = _dev(C0)
+            tb.gemm_bf16(_dev(A), Wd, out=got, kind=tb.GEMM_BF16_F32A_RESID, tile=tile)
+            ref, bound = C0 + prod, mag + U * np.abs(C0 + prod)
+        torch.cuda.synchronize()
+        got = got.cpu().numpy()
     elif kind == "norm":
         A = (3.0 * rng.standard_normal((M, K))).astype(np.float32)
         out = tb.gemm_bf16(_dev(A), Wd, gain=_dev(gain), kind=tb.GEMM_BF16_NORM, tile=tile)
