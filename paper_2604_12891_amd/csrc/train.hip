@@ -55,9 +55,11 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd_kernel(const int* __restrict_
 
 // ---------------------------------------------------------------- RMSNorm backward
 // dH[row] += r (g dN) - (r^3 / d) h sum(g dN h); per-block partial of
-// dg = sum over rows of dN h r.
+// dg = sum over rows of dN h r. kRnWaves wavefronts per block, each taking
+// every kRnWaves-th row of the block's range.
+constexpr int kRnWaves = 16;
 template <int DM>
-__global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict__ Mdev,
+__global__ __launch_bounds__(64 * kRnWaves) void rmsnorm_bwd_kernel(const int* __restrict__ Mdev,
                                                           const float* __restrict__ dN,
                                                           const float* __restrict__ H,
                                                           const float* __restrict__ rstd,
@@ -66,7 +68,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict_
                                                           float* __restrict__ dg_part,
                                                           int rows_per_block) {
   constexpr int PL = DM / 64;
-  __shared__ float sdg[4][DM];
+  __shared__ float sdg[kRnWaves][DM];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int M = *Mdev;
   float dg[PL];
@@ -81,11 +83,11 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict_
   float gl[PL];
 #pragma unroll
   for (int i = 0; i < PL; ++i) gl[i] = g[lane * PL + i];
-  for (int rw = r0 + wave; rw < r1; rw += 4 * U) {
+  for (int rw = r0 + wave; rw < r1; rw += kRnWaves * U) {
     float h[U][PL], dn[U][PL], dh[U][PL], r[U];
 #pragma unroll
     for (int j = 0; j < U; ++j) {
-      const int row = rw + 4 * j < r1 ? rw + 4 * j : r0;
+      const int row = rw + kRnWaves * j < r1 ? rw + kRnWaves * j : r0;
       const int64_t o = (int64_t)row * DM + lane * PL;
       r[j] = rstd[row];
 #pragma unroll
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict_
     // loads to its use); rows past the range are neither stored nor summed
 #pragma unroll
     for (int j = 0; j < U; ++j) {
-      const int row = rw + 4 * j;
+      const int row = rw + kRnWaves * j;
       const bool ok = row < r1;  // wave-uniform
       const int64_t o = (int64_t)row * DM + lane * PL;
       float gd[PL], dot = 0.f;
@@ -122,8 +124,12 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_kernel(const int* __restrict_
 #pragma unroll
   for (int i = 0; i < PL; ++i) sdg[wave][lane * PL + i] = dg[i];
   __syncthreads();
-  for (int k = threadIdx.x; k < DM; k += 256)
-    dg_part[(int64_t)blockIdx.x * DM + k] = sdg[0][k] + sdg[1][k] + sdg[2][k] + sdg[3][k];
+  for (int k = threadIdx.x; k < DM; k += 64 * kRnWaves) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < kRnWaves; ++w) t += sdg[w][k];
+    dg_part[(int64_t)blockIdx.x * DM + k] = t;
+  }
 }
 
 // ---------------------------------------------------------------- loss + head backward
@@ -780,9 +786,9 @@ hipError_t launch_rmsnorm_bwd(int d, int Mmax, const int* Mdev, const float* dN,
                               hipStream_t s) {
   dim3 grid(rmsnorm_bwd_blocks(Mmax));
   switch (d) {
-    case 64: hipLaunchKernelGGL(rmsnorm_bwd_kernel<64>, grid, dim3(256), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
-    case 128: hipLaunchKernelGGL(rmsnorm_bwd_kernel<128>, grid, dim3(256), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
-    case 256: hipLaunchKernelGGL(rmsnorm_bwd_kernel<256>, grid, dim3(256), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
+    case 64: hipLaunchKernelGGL(rmsnorm_bwd_kernel<64>, grid, dim3(64 * kRnWaves), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
+    case 128: hipLaunchKernelGGL(rmsnorm_bwd_kernel<128>, grid, dim3(64 * kRnWaves), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
+    case 256: hipLaunchKernelGGL(rmsnorm_bwd_kernel<256>, grid, dim3(64 * kRnWaves), 0, s, Mdev, dN, H, rstd, g, dH, dg_part, 64); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
