@@ -209,6 +209,7 @@ struct GemmTNArgs {
   int64_t ldb = 0;
   const int* offs = nullptr;  // gather: token offsets of B's programs
   int B = 0, L = 0;
+  const int* rows = nullptr;  // gather (optional): B's row of each packed token, else found from offs
   float* P = nullptr;
   const int* Mdev = nullptr;
   int Mmax = 0;
@@ -217,6 +218,11 @@ struct GemmTNArgs {
 enum TNKind { kTN_F32_F32, kTN_F32_BF16, kTN_F32_GatherF32 };
 int gemm_tn_splits(int Mmax, int NI, int NJ);
 hipError_t launch_gemm_tn(const GemmTNArgs& a, TNKind kind, int splits, hipStream_t s);
+// rows[offs[b] + t] = b * L + t for the valid tokens of every program b
+hipError_t launch_packed_rows(const int* offs, int B, int L, int* rows, hipStream_t s);
+// the same on the bf16 matrix cores, both operands rounded to bf16 (nearest
+// even), fp32 accumulation: for models that compute in bf16
+hipError_t launch_gemm_tn_bf16(const GemmTNArgs& a, TNKind kind, int splits, hipStream_t s);
 
 // ---------------------------------------------------------------- per-program kernels
 // offs[b] = sum of valid lengths before b; offs[B] = total packed rows.

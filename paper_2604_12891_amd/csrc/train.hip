@@ -177,12 +177,17 @@ __global__ __launch_bounds__(256) void loss_head_bwd_kernel(
     float acc[kHB];
 #pragma unroll
     for (int p = 0; p < kHB; ++p) acc[p] = 0.f;
-    // unrolled so that several rows of W1 are in flight at once
-#pragma unroll 8
-    for (int j = 0; j < h; ++j) {
-      const float w = W1[(int64_t)j * d + tid];
+    // 32 rows of W1 loaded together per batch (h is a multiple of 64): one
+    // memory latency per batch
+    for (int j0 = 0; j0 < h; j0 += 32) {
+      float w[32];
 #pragma unroll
-      for (int p = 0; p < kHB; ++p) acc[p] = fmaf(sda[p][j], w, acc[p]);
+      for (int jj = 0; jj < 32; ++jj) w[jj] = W1[(int64_t)(j0 + jj) * d + tid];
+      __builtin_amdgcn_sched_barrier(0);  // every load of the batch before its first use
+#pragma unroll
+      for (int jj = 0; jj < 32; ++jj)
+#pragma unroll
+        for (int p = 0; p < kHB; ++p) acc[p] = fmaf(sda[p][j0 + jj], w[jj], acc[p]);
     }
 #pragma unroll
     for (int p = 0; p < kHB; ++p)

@@ -43,6 +43,7 @@ namespace {
 // Workspace layout of one step (byte offsets, 256-aligned).
 struct TrainPlan {
   size_t teacher_ws = 0, t_scores = 0, s_scores = 0, offs = 0;
+  size_t prow = 0;  // per packed token: its row of the padded feature tensor
   struct Layer {
     size_t Hin, n, rstd, xz, u, xdbl, y, yg, ckpt;
     size_t p_Wout, p_Wdt, p_bdt, p_A, p_D, p_Wx, p_conv, p_Win, p_g;
@@ -73,6 +74,7 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
   P.t_scores = take((size_t)B * 4);
   P.s_scores = take((size_t)B * 4);
   P.offs = take((size_t)(B + 1) * 4);
+  P.prow = take((size_t)B * L * 4);
   P.cs = colsum_splits(Mmax);
   P.lh_blocks = loss_head_blocks(B);
   P.rn_blocks = rmsnorm_bwd_blocks(Mmax);
@@ -349,12 +351,25 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     TCL_HIP(hipEventRecord(Tm->ev[0], s));
     TCL_HIP(hipStreamWaitEvent(Tm->aux[0], Tm->ev[0], 0));
   }
-  st = run_score(Tm, B, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws, fork ? Tm->aux[0] : s);
+  // the teacher's parts (front, blocks, tail) are enqueued between the
+  // student's layers, so that neither forward waits for the host to finish
+  // enqueueing the other
+  const int t_parts = Tm->cfg.n_layers + 2;
+  int t_next = 0;
+  auto teacher_parts = [&](int upto) -> tcl_status {
+    for (; t_next < upto && t_next < t_parts; ++t_next) {
+      const tcl_status ts = run_score_part(Tm, B, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws,
+                                           fork ? Tm->aux[0] : s, t_next);
+      if (ts != TCL_OK) return ts;
+    }
+    return TCL_OK;
+  };
+  st = teacher_parts(1);
   if (st != TCL_OK) return st;
-  if (fork) TCL_HIP(hipEventRecord(Tm->ev[1], Tm->aux[0]));
 
   // 2. student forward, keeping activations
   TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  TCL_LAUNCH(T, "packed_rows", launch_packed_rows(offs, B, L, reinterpret_cast<int*>(ws + P.prow), s));
   {
     GemmArgsBF16 g;
     g.A = d_feats; g.lda = F; g.offs = offs; g.B = B; g.L = L;
@@ -363,6 +378,8 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     TCL_LAUNCH(T, "gemm_input", launch_gemm_bf16(g, kInputF32toF32, -1, s));
   }
   for (int l = 0; l < c.n_layers; ++l) {
+    st = teacher_parts(l + 2);
+    if (st != TCL_OK) return st;
     const auto& W = S->layers[l];
     const auto& Ly = P.layers[l];
     float* Hout = l + 1 < c.n_layers ? F32(P.layers[l + 1].Hin) : F32(P.H_last);
@@ -386,6 +403,9 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     go.R = F32(Ly.Hin); go.Mdev = Mdev; go.Mmax = Mmax; go.N = d; go.K = E;
     TCL_LAUNCH(T, "gemm_out_proj", launch_gemm_bf16(go, kBF16ResidF32, -1, s));
   }
+  st = teacher_parts(t_parts);
+  if (st != TCL_OK) return st;
+  if (fork) TCL_HIP(hipEventRecord(Tm->ev[1], Tm->aux[0]));
   TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, h, offs, d_lengths, F32(P.H_last), S->g_f, c.final_norm,
                                         c.norm_eps, S->W1T, S->b1, S->W2, S->b2, F32(P.s_scores), s,
                                         F32(P.pooled), F32(P.a1)));
@@ -447,6 +467,11 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     const tcl_status st_ = (X);           \
     if (st_ != TCL_OK) return st_;        \
   } while (0)
+  // Weight-gradient GEMMs (partial sums per token split): on the bf16
+  // matrix cores for a bf16 student, else on the fp32 ones.
+  auto gemm_tn = [&](const GemmTNArgs& a, TNKind kind, int splits, hipStream_t st) -> hipError_t {
+    return c.dtype == TCL_BF16 ? launch_gemm_tn_bf16(a, kind, splits, st) : launch_gemm_tn(a, kind, splits, st);
+  };
   // Data-gradient GEMMs C (+)= A W with A an fp32 gradient: for a bf16
   // student on the bf16 matrix cores (A rounded to bf16 as it is staged, W
   // the transposed bf16 copy, fp32 accumulation), else on the fp32 ones.
@@ -474,7 +499,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       GemmTNArgs a;
       a.A = F32(P.dH); a.lda = d; a.Bm = B16(Ly.yg); a.ldb = E; a.P = F32(Ly.p_Wout);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = d; a.NJ = E;
-      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Wout, s));
+      TCL_SIDE("gemm_dW", gemm_tn(a, kTN_F32_BF16, Ly.s_Wout, s));
     }
     TCL_TRY(mark(tr->ev_dh));
     // the block above's side GEMMs are done with dv, dxdbl and dxz
@@ -494,7 +519,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       GemmTNArgs a;
       a.A = F32(P.dv); a.lda = E; a.Bm = F32(Ly.xdbl); a.ldb = XW; a.P = F32(Ly.p_Wdt);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = E; a.NJ = R;
-      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_F32, Ly.s_Wdt, s));
+      TCL_SIDE("gemm_dW", gemm_tn(a, kTN_F32_F32, Ly.s_Wdt, s));
     }
     TCL_SIDE("colsum", launch_colsum(Mdev, Mmax, F32(P.dv), E, E, P.cs, F32(Ly.p_bdt), s));
     // du += dxdbl W_x
@@ -504,7 +529,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       GemmTNArgs a;
       a.A = F32(P.dxdbl); a.lda = XW; a.Bm = B16(Ly.u); a.ldb = E; a.P = F32(Ly.p_Wx);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = XW; a.NJ = E;
-      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Wx, s));
+      TCL_SIDE("gemm_dW", gemm_tn(a, kTN_F32_BF16, Ly.s_Wx, s));
     }
     TCL_LAUNCH(T, "conv_bwd", launch_conv_bwd(B, E, K, offs, B16(Ly.xz), 2 * E, W.conv_w, W.conv_b,
                                               F32(P.du), F32(P.dxz), 2 * E, F32(Ly.p_conv), s));
@@ -515,22 +540,24 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       GemmTNArgs a;
       a.A = F32(P.dxz); a.lda = 2 * E; a.Bm = B16(Ly.n); a.ldb = d; a.P = F32(Ly.p_Win);
       a.Mdev = Mdev; a.Mmax = Mmax; a.NI = 2 * E; a.NJ = d;
-      TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_BF16, Ly.s_Win, s));
+      TCL_SIDE("gemm_dW", gemm_tn(a, kTN_F32_BF16, Ly.s_Win, s));
     }
     TCL_TRY(mark(tr->ev_layer));
     TCL_TRY(join(tr->ev_dh));  // dW_out is done with dH
     TCL_LAUNCH(T, "rmsnorm_bwd", launch_rmsnorm_bwd(d, Mmax, Mdev, F32(P.dN), F32(Ly.Hin), F32(Ly.rstd),
                                                     W.g, F32(P.dH), F32(Ly.p_g), s));
   }
-  TCL_TRY(fork_side());
+  // the input layer's gradients on this stream (nothing else is left to
+  // overlap them with), while the side stream finishes the first block's
+  TCL_TRY(mark(tr->ev_end));
   {  // dW0 = dH^T X (gathered), db0 = column sums of dH
     GemmTNArgs a;
     a.A = F32(P.dH); a.lda = d; a.Bm = d_feats; a.ldb = F; a.offs = offs; a.B = B; a.L = L;
+    a.rows = reinterpret_cast<const int*>(ws + P.prow);
     a.P = F32(P.p_W0); a.Mdev = Mdev; a.Mmax = Mmax; a.NI = d; a.NJ = F;
-    TCL_SIDE("gemm_dW", launch_gemm_tn(a, kTN_F32_GatherF32, P.s_W0, s));
+    TCL_LAUNCH(T, "gemm_dW", gemm_tn(a, kTN_F32_GatherF32, P.s_W0, s));
   }
-  TCL_SIDE("colsum", launch_colsum(Mdev, Mmax, F32(P.dH), d, d, P.cs, F32(P.p_b0), s));
-  TCL_TRY(mark(tr->ev_end));
+  TCL_LAUNCH(T, "colsum", launch_colsum(Mdev, Mmax, F32(P.dH), d, d, P.cs, F32(P.p_b0), s));
   TCL_TRY(join(tr->ev_end));  // every partial sum is written
 #undef TCL_TRY
 #undef TCL_SIDE
