@@ -298,9 +298,17 @@ struct ReduceJob {
   int64_t n;
   int32_t nsplit;
   int32_t dst_buf;  // 0: gradient blob, 1: loss vector
+  // the job's blocks in the launch: [block0, block0 + nblocks), numbered
+  // from the first job of the launch (reduce_blocks assigns them)
+  int32_t block0, nblocks;
 };
-hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, const float* ws,
-                         float* grad, float* loss, hipStream_t s);
+// Assign block ranges to jobs[0 .. njobs) for one launch; returns the
+// launch's block count.
+int reduce_blocks(ReduceJob* jobs, int njobs);
+// njobs <= kMaxReduceJobs; nblocks = reduce_blocks' result for the same jobs
+constexpr int kMaxReduceJobs = 1024;
+hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int nblocks, const float* ws, float* grad,
+                         float* loss, hipStream_t s);
 
 // Weight layouts derived from the fp32 master blob: one flat index space over
 // all jobs (job j covers [start_j, start_j + rows*cols)); the destination is a

@@ -648,26 +648,39 @@ __global__ __launch_bounds__(256) void colsum_kernel(const int* __restrict__ Mde
 }
 
 // ---------------------------------------------------------------- reductions
-// blockIdx.y picks the job. A block takes 64 consecutive outputs; its 16
-// wavefronts each sum a contiguous sixteenth of the splits with eight
-// independent partial sums (eight loads in flight per lane), then the partial
-// sums and the sixteenths are added in a fixed order (deterministic for a
-// given split count).
+// One launch covers several jobs; each job has its own range of blocks
+// (about one per 64 outputs), so no block is launched without work. A block
+// finds its job from the ranges (staged in LDS), takes 64 consecutive
+// outputs; its 16 wavefronts each sum a contiguous sixteenth of the splits
+// with eight independent partial sums (eight loads in flight per lane), then
+// the partial sums and the sixteenths are added in a fixed order
+// (deterministic for a given split count).
 constexpr int kRedGroups = 16;
 __global__ __launch_bounds__(64 * kRedGroups) void reduce_kernel(const ReduceJob* __restrict__ jobs, int njobs,
                                                                 const float* __restrict__ ws,
                                                                 float* __restrict__ grad,
                                                                 float* __restrict__ loss) {
   __shared__ float sq[kRedGroups][64];
-  const int j = blockIdx.y;
-  if (j >= njobs) return;
-  const ReduceJob J = jobs[j];
+  __shared__ int sb[kMaxReduceJobs];
+  __shared__ int sj;
+  for (int k = threadIdx.x; k < njobs; k += 64 * kRedGroups) sb[k] = jobs[k].block0;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int lo = 0, hi = njobs;  // the last job whose range starts at or before this block
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (sb[mid] <= (int)blockIdx.x) lo = mid; else hi = mid;
+    }
+    sj = lo;
+  }
+  __syncthreads();
+  const ReduceJob J = jobs[sj];
   float* dst = (J.dst_buf == 0 ? grad : loss) + J.dst;
   const float* src = ws + J.src;
   const int lane = threadIdx.x & 63, q = threadIdx.x >> 6;
   const int per = (J.nsplit + kRedGroups - 1) / kRedGroups;
   const int s0 = q * per, s1 = min(s0 + per, J.nsplit);
-  for (int64_t i0 = (int64_t)blockIdx.x * 64; i0 < J.n; i0 += (int64_t)gridDim.x * 64) {
+  for (int64_t i0 = (int64_t)((int)blockIdx.x - J.block0) * 64; i0 < J.n; i0 += (int64_t)J.nblocks * 64) {
     const int64_t i = i0 + lane;
     float a[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (i < J.n) {
@@ -903,11 +916,21 @@ hipError_t launch_colsum(const int* Mdev, int Mmax, const float* A, int64_t lda,
   return hipGetLastError();
 }
 
-hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int64_t max_n, const float* ws,
-                         float* grad, float* loss, hipStream_t s) {
-  if (njobs <= 0) return hipSuccess;
-  const int gx = (int)std::min<int64_t>((max_n + 63) / 64, 512);
-  hipLaunchKernelGGL(reduce_kernel, dim3(gx, njobs), dim3(64 * kRedGroups), 0, s, d_jobs, njobs, ws, grad, loss);
+int reduce_blocks(ReduceJob* jobs, int njobs) {
+  int total = 0;
+  for (int j = 0; j < njobs; ++j) {
+    jobs[j].block0 = total;
+    jobs[j].nblocks = (int)std::min<int64_t>(std::max<int64_t>((jobs[j].n + 63) / 64, 1), 512);
+    total += jobs[j].nblocks;
+  }
+  return total;
+}
+
+hipError_t launch_reduce(const ReduceJob* d_jobs, int njobs, int nblocks, const float* ws, float* grad,
+                         float* loss, hipStream_t s) {
+  if (njobs <= 0 || nblocks <= 0) return hipSuccess;
+  if (njobs > kMaxReduceJobs) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(reduce_kernel, dim3(nblocks), dim3(64 * kRedGroups), 0, s, d_jobs, njobs, ws, grad, loss);
   return hipGetLastError();
 }
 

@@ -29,7 +29,9 @@ struct tcl_trainer {
   ReduceJob* d_jobs = nullptr;
   int max_jobs = 0;
   int njobs = 0;
-  int64_t max_n = 0;
+  // the jobs in groups, one per block: group l (its first job, count and
+  // largest output) is reduced once block l's partial sums are written
+  std::vector<int> grp_first, grp_count, grp_blocks;
   int plan_B = -1, plan_L = -1;
   Timing timing;
   // the backward's weight-gradient GEMMs run on a stream of their own,
@@ -134,7 +136,12 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
 
 // The reductions that turn the step's partial sums into the gradient blob
 // (canonical layout) and the three loss values.
-std::vector<ReduceJob> reduce_jobs(const tcl_trainer* tr, const TrainPlan& P, int B) {
+// Jobs in the order the backward pass finishes their partial sums: the head,
+// then the blocks from the last to the first, then the input layer. Group l
+// is block l's jobs, with the head's in the last block's group and the input
+// layer's in block 0's; first[l] and count[l] locate it.
+std::vector<ReduceJob> reduce_jobs(const tcl_trainer* tr, const TrainPlan& P, int B, std::vector<int>& first,
+                                   std::vector<int>& count) {
   const tcl_config& c = tr->student->cfg;
   const BlobLayout bl = blob_layout(c);
   const int64_t d = c.d_model, E = c.d_inner, N = c.d_state, K = c.d_conv, R = c.dt_rank;
@@ -162,9 +169,13 @@ std::vector<ReduceJob> reduce_jobs(const tcl_trainer* tr, const TrainPlan& P, in
   add(P.p_lh + (2 * h + 2) * 4, lw, 1, P.lh_blocks, 1, 2, 1, 1);   // mse(s, label)
   add(P.p_W1, h * d, 1, P.s_W1, 0, bl.W1, 1, h * d);               // dW1
   add(P.p_gf, d, 1, B, 0, bl.g_f, 1, d);                           // dg_f
-  for (int l = 0; l < c.n_layers; ++l) {
+  const int nl = c.n_layers;
+  first.assign(nl, 0);
+  count.assign(nl, 0);
+  for (int l = nl - 1; l >= 0; --l) {
     const auto& Ly = P.layers[l];
     const auto& Bl = bl.layers[l];
+    first[l] = l == nl - 1 ? 0 : (int)J.size();
     add(Ly.p_Wout, d * E, 1, Ly.s_Wout, 0, Bl.W_out, 1, d * E);
     add(Ly.p_Wdt, E * R, 1, Ly.s_Wdt, 0, Bl.W_dt, 1, E * R);
     add(Ly.p_bdt, E, 1, P.cs, 0, Bl.b_dt, 1, E);
@@ -175,9 +186,11 @@ std::vector<ReduceJob> reduce_jobs(const tcl_trainer* tr, const TrainPlan& P, in
     add(Ly.p_conv + (size_t)K * E * 4, (K + 1) * E, 1, B, 0, Bl.conv_b, 1, E);
     add(Ly.p_Win, 2 * E * d, 1, Ly.s_Win, 0, Bl.W_in, 1, 2 * E * d);
     add(Ly.p_g, d, 1, P.rn_blocks, 0, Bl.g, 1, d);
+    count[l] = (int)J.size() - first[l];
   }
   add(P.p_W0, d * F, 1, P.s_W0, 0, bl.W0, 1, d * F);
   add(P.p_b0, d, 1, P.cs, 0, bl.b0, 1, d);
+  count[0] = (int)J.size() - first[0];
   return J;
 }
 
@@ -186,15 +199,19 @@ tcl_status ensure_plan(tcl_trainer* tr, int B, int L, const TrainPlan& P, bool c
   if (capturing)
     return fail(TCL_ERR_INVALID_ARG, "a step with a new (B, L) = (%d, %d) cannot be captured: run one "
                 "step of that shape first", B, L);
-  const std::vector<ReduceJob> J = reduce_jobs(tr, P, B);
+  std::vector<int> first, count;
+  std::vector<ReduceJob> J = reduce_jobs(tr, P, B, first, count);
+  std::vector<int> blocks(first.size());
+  for (size_t g = 0; g < first.size(); ++g) blocks[g] = reduce_blocks(J.data() + first[g], count[g]);
   if ((int)J.size() > tr->max_jobs) return fail(TCL_ERR_UNSUPPORTED, "too many reduction jobs");
   // the table changes only with the batch shape; the copy waits for
   // earlier steps that may still read the previous table
   TCL_HIP(hipDeviceSynchronize());
   TCL_HIP(hipMemcpy(tr->d_jobs, J.data(), J.size() * sizeof(ReduceJob), hipMemcpyHostToDevice));
   tr->njobs = (int)J.size();
-  tr->max_n = 0;
-  for (const auto& r : J) tr->max_n = std::max<int64_t>(tr->max_n, r.n);
+  tr->grp_first = first;
+  tr->grp_count = count;
+  tr->grp_blocks = blocks;
   tr->plan_B = B;
   tr->plan_L = L;
   return TCL_OK;
@@ -502,6 +519,12 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
       TCL_SIDE("gemm_dW", gemm_tn(a, kTN_F32_BF16, Ly.s_Wout, s));
     }
     TCL_TRY(mark(tr->ev_dh));
+    // the block after this one has written every partial sum (its side
+    // GEMMs earlier on the side stream, the rest before the fork): reduce
+    // them there, beside this block's backward
+    if (l + 1 < c.n_layers)
+      TCL_SIDE("reduce", launch_reduce(tr->d_jobs + tr->grp_first[l + 1], tr->grp_count[l + 1],
+                                       tr->grp_blocks[l + 1], reinterpret_cast<float*>(ws), tr->grad, d_loss, s));
     // the block above's side GEMMs are done with dv, dxdbl and dxz
     if (l + 1 < c.n_layers) TCL_TRY(join(tr->ev_layer));
     TCL_LAUNCH(T, "scan_bwd", launch_scan_bwd(B, E, L, N, R, offs, B16(Ly.u), F32(Ly.xdbl), B16(Ly.xz),
@@ -568,8 +591,9 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   }
 
   // 5. reduce partials, Adam, refresh the compute layouts
-  TCL_LAUNCH(T, "reduce", launch_reduce(tr->d_jobs, tr->njobs, tr->max_n, reinterpret_cast<float*>(ws),
-                                        tr->grad, d_loss, s));
+  // block 0's group (with the input layer's jobs) after the rest
+  TCL_LAUNCH(T, "reduce", launch_reduce(tr->d_jobs + tr->grp_first[0], tr->grp_count[0], tr->grp_blocks[0],
+                                        reinterpret_cast<float*>(ws), tr->grad, d_loss, s));
   if (kd)  // EWC on the master weights: gradient and loss[3] (zero when lambda = 0)
     TCL_LAUNCH(T, "ewc", launch_ewc((int64_t)S->n_params, S->master, kd->d_theta_prev, kd->d_fisher,
                                     kd->ewc_lambda, tr->grad, F32(P.ewc_part), d_loss, s));
