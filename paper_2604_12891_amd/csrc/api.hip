@@ -123,6 +123,7 @@ ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L) {
   const size_t act = c.dtype == TCL_BF16 ? 2 : 4;  // bytes per stored activation
   size_t o = 0;
   p.offs = o; o = align256(o + (size_t)(B + 1) * 4);
+  p.ord = o; o = align256(o + (size_t)B * 4);
   p.tpos = o; o = align256(o + (size_t)rows);
   p.H = o; o = align256(o + (size_t)rows * c.d_model * 4);
   p.xz = o; o = align256(o + (size_t)rows * 2 * c.d_inner * act);
@@ -185,7 +186,7 @@ tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string&
 
 tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, int l, int B, int L,
                              const int* offs, const uint8_t* tpos, float* H, float* xz, float* u, float* xdbl,
-                             hipStream_t s) {
+                             hipStream_t s, const int* ord) {
   const tcl_config& c = m->cfg;
   const int d = c.d_model, E = c.d_inner, N = c.d_state, R = c.dt_rank, XW = R + 2 * N;
   const int Mmax = B * L;
@@ -217,7 +218,8 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
                                           W.A_log, W.D, u, s));
   else
     TCL_LAUNCH(T, (tag + "scan").c_str(), launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                                             W.b_dt, W.A_log, W.D, u, s));
+                                                             W.b_dt, W.A_log, W.D, u, s, nullptr, nullptr, 0,
+                                                             ord));
   GemmArgs go;
   go.A = u; go.lda = E; go.W = W.W_out; go.ldw = E; go.C = H; go.ldc = d;
   go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;
@@ -242,7 +244,8 @@ tcl_status run_score_part(tcl_model* m, int B, int L, const float* d_feats, cons
   const int chunks = scan_chunks_for(B, E, L);
   Timing& T = m->timing;
 
-  if (front) TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  int* ord = reinterpret_cast<int*>(ws + p.ord);  // the programs longest first
+  if (front) TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s, ord));
   uint8_t* tpos = reinterpret_cast<uint8_t*>(ws + p.tpos);
   // features whose row length is not a multiple of 4 are first copied into
   // rows padded with zeros (the input Linear reads 16-byte vectors)
@@ -285,7 +288,8 @@ tcl_status run_score_part(tcl_model* m, int B, int L, const float* d_feats, cons
       if (m->split && !tpos_done) TCL_LAUNCH(T, "token_pos", launch_token_pos(offs, B, tpos, s));
       return TCL_OK;
     }
-    return enqueue_block_f32(m, T, "", layer, B, L, offs, m->split ? tpos : nullptr, H, xz, u, xdbl, s);
+    return enqueue_block_f32(m, T, "", layer, B, L, offs, m->split ? tpos : nullptr, H, xz, u, xdbl, s,
+                             L <= kOrderMaxL ? ord : nullptr);
   } else {
     uint16_t* xz = reinterpret_cast<uint16_t*>(ws + p.xz);
     uint16_t* u = reinterpret_cast<uint16_t*>(ws + p.u);
@@ -335,7 +339,8 @@ tcl_status run_score_part(tcl_model* m, int B, int L, const float* d_feats, cons
                                                                     W.A_log, W.D, u, s));
       else
         TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
-                                                    W.b_dt, W.A_log, W.D, u, s));
+                                                    W.b_dt, W.A_log, W.D, u, s, nullptr, nullptr, 0,
+                                                    L <= kOrderMaxL ? ord : nullptr));
       GemmArgsBF16 go;
       go.A = u; go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = H; go.ldc = d;
       go.Mdev = offs + B; go.Mmax = Mmax; go.N = d; go.K = E;

@@ -226,8 +226,10 @@ hipError_t launch_gemm_tn_bf16(const GemmTNArgs& a, TNKind kind, int splits, hip
 
 // ---------------------------------------------------------------- per-program kernels
 // offs[b] = sum of valid lengths before b; offs[B] = total packed rows.
-// Lengths outside [1, L] count as 0 tokens.
-hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream_t s);
+// Lengths outside [1, L] count as 0 tokens. ord (optional, B entries, used
+// when L <= 4096): the programs longest first.
+constexpr int kOrderMaxL = 4096;
+hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream_t s, int* ord = nullptr);
 // tpos[r] = position of packed row r in its program, clamped to 255 (rows
 // past offs[B] are not written).
 hipError_t launch_token_pos(const int* offs, int B, uint8_t* tpos, hipStream_t s);
@@ -247,13 +249,14 @@ hipError_t launch_conv_silu(int B, int E, int K, const int* offs, const T* x, in
 // ysave (optional) keeps y before the gate, for the backward pass; ckpt (optional, N = 16, with the
 // padded length L) keeps the state after every kScanCkptTokens-th token of a
 // program but its last chunk, [B][E][ceil(L / kScanCkptTokens)][N], which is
-// where the backward scan restarts its recomputation.
+// where the backward scan restarts its recomputation. ord (optional): the
+// order in which programs are handed to workgroups (launch_offsets' ord).
 constexpr int kScanCkptTokens = 4;
 template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
                        const float* D, T* out, hipStream_t s, T* ysave = nullptr, float* ckpt = nullptr,
-                       int L = 0);
+                       int L = 0, const int* ord = nullptr);
 
 // The same scan as a chunked two-level scan: each program's tokens are split
 // into `chunks` (1..8) that are scanned concurrently and stitched through
@@ -401,7 +404,7 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
                            const float* dyg, const float* W_dt, const float* b_dt,
                            const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
                            float* dxz, float* dxdbl, float* dA_part, float* dD_part, float* dbc_part,
-                           hipStream_t s);
+                           hipStream_t s, const int* ord = nullptr);
 // dbc_part (scratch for launch_scan_bwd; null: one block per program)
 size_t scan_bwd_part_floats(int B, int L, int N);
 // part: [B][K+1][E] = dw (K rows) | db

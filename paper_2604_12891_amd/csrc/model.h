@@ -137,7 +137,7 @@ namespace tcl {
 
 // Workspace plan of one scoring call (byte offsets, 256-aligned).
 struct ScorePlan {
-  size_t offs, tpos, H, xz, u, xdbl, feats, enc1, enc2, total;
+  size_t offs, ord, tpos, H, xz, u, xdbl, feats, enc1, enc2, total;
 };
 ScorePlan score_plan(const tcl_config& c, int64_t B, int64_t L);
 
@@ -158,7 +158,7 @@ tcl_status enqueue_encoder_layer_f32(tcl_model* m, Timing& T, const std::string&
 // the split path fuse the conv into x_proj; null: the conv runs on its own.
 tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, int l, int B, int L,
                              const int* offs, const uint8_t* tpos, float* H, float* xz, float* u, float* xdbl,
-                             hipStream_t s);
+                             hipStream_t s, const int* ord = nullptr);
 
 // Enqueue the scoring pass (no argument checks): its parts in order.
 tcl_status run_score(tcl_model* m, int B, int L, const float* d_feats, const int* d_lengths,

@@ -15,10 +15,29 @@ namespace {
 // ---------------------------------------------------------------- offsets
 // One workgroup of 1024 threads: each thread sums a contiguous slice of the
 // lengths, a block-wide exclusive scan gives the slice's start, and the
-// slice is written out.
+// slice is written out. With `ord`, the programs are also listed longest
+// first (a counting sort over the lengths in LDS; the order of programs of
+// equal length is unspecified), for kernels that walk each program's tokens
+// in sequence: handing out the long programs first shortens the last round.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wsum) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += u;
+  }
+  __syncthreads();  // wsum is free
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  int before = 0;
+  for (int w = 0; w < wave; ++w) before += wsum[w];
+  return before + inc - v;
+}
 __global__ __launch_bounds__(1024) void offsets_kernel(const int* __restrict__ lengths, int B, int L,
-                                                       int* __restrict__ offs) {
+                                                       int* __restrict__ offs, int* __restrict__ ord) {
   __shared__ int wsum[16];
+  __shared__ int cnt[kOrderMaxL + 1];
   const int tid = threadIdx.x;
   // each thread owns a contiguous segment of a multiple of 4 programs, read
   // and written 16 bytes at a time when the arrays allow it
@@ -67,6 +86,26 @@ __global__ __launch_bounds__(1024) void offsets_kernel(const int* __restrict__ l
     run += valid(lengths[i]);
   }
   if (tid == 1023) offs[B] = before + inc;
+  if (ord == nullptr || L > kOrderMaxL) return;  // block-uniform
+
+  // counting sort, longest first: bucket L - len
+  const int nb = L + 1;
+  for (int k = tid; k < nb; k += 1024) cnt[k] = 0;
+  __syncthreads();
+  for (int k = tid; k < B; k += 1024) atomicAdd(&cnt[L - valid(lengths[k])], 1);
+  __syncthreads();
+  const int pb = (nb + 1023) / 1024;
+  const int b0 = min(tid * pb, nb), b1 = min(b0 + pb, nb);
+  int csum = 0;
+  for (int k = b0; k < b1; ++k) csum += cnt[k];
+  int at = block_exclusive_scan(csum, wsum);
+  for (int k = b0; k < b1; ++k) {
+    const int c = cnt[k];
+    cnt[k] = at;
+    at += c;
+  }
+  __syncthreads();
+  for (int k = tid; k < B; k += 1024) ord[atomicAdd(&cnt[L - valid(lengths[k])], 1)] = k;
 }
 
 // ---------------------------------------------------------------- element access
@@ -233,16 +272,19 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(
     int B, const int* __restrict__ offs, int E, const T* u, const float* __restrict__ xdbl,
     const T* __restrict__ z, int ldz, const float* __restrict__ W_dt,
     const float* __restrict__ b_dt, const float* __restrict__ A_log,
-    const float* __restrict__ Dp, T* out, T* __restrict__ ysave, float* __restrict__ ckpt, int nck) {
+    const float* __restrict__ Dp, T* out, T* __restrict__ ysave, float* __restrict__ ckpt, int nck,
+    const int* __restrict__ ord) {
   constexpr int XW = R + 2 * N;
   __shared__ __attribute__((aligned(16))) float sX[kScanTC * XW];
   // workgroups are handed to the 8 XCDs round-robin: the CG channel groups
   // of a program take consecutive slots on one XCD, so its xdbl rows are
-  // read from HBM once and then hit that XCD's L2
+  // read from HBM once and then hit that XCD's L2; slots go to programs in
+  // the order `ord` gives (longest first) when there is one
   const int CG = (E + kScanThreads - 1) / kScanThreads;
   const int xcd = blockIdx.x & 7, j = blockIdx.x >> 3;
-  const int b = (j / CG) * 8 + xcd;
-  if (b >= B) return;
+  const int slot = (j / CG) * 8 + xcd;
+  if (slot >= B) return;
+  const int b = ord ? ord[slot] : slot;
   const int e = (j % CG) * kScanThreads + threadIdx.x;
   const bool active = e < E;
   const int ec = active ? e : 0;
@@ -667,8 +709,8 @@ hipError_t launch_pad_rows(const float* src, int64_t rows, int F, int ld, float*
   return hipGetLastError();
 }
 
-hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream_t s) {
-  hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(1024), 0, s, lengths, B, L, offs);
+hipError_t launch_offsets(const int* lengths, int B, int L, int* offs, hipStream_t s, int* ord) {
+  hipLaunchKernelGGL(offsets_kernel, dim3(1), dim3(1024), 0, s, lengths, B, L, offs, ord);
   return hipGetLastError();
 }
 
@@ -751,7 +793,7 @@ int scan_chunks_for(int B, int E, int L) {
 template <typename T>
 hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, const float* xdbl,
                        const T* z, int ldz, const float* W_dt, const float* b_dt, const float* A_log,
-                       const float* D, T* out, hipStream_t s, T* ysave, float* ckpt, int L) {
+                       const float* D, T* out, hipStream_t s, T* ysave, float* ckpt, int L, const int* ord) {
   if (B <= 0) return hipSuccess;
   if (N != 16 && N != 8) return hipErrorInvalidValue;
   if (ckpt && (L <= 0 || reinterpret_cast<uintptr_t>(ckpt) % 16)) return hipErrorInvalidValue;
@@ -760,7 +802,7 @@ hipError_t launch_scan(int B, int E, int N, int R, const int* offs, const T* u, 
   const int grid = 8 * cgroups * ((B + 7) / 8);
 #define TCL_SCAN(NN, RR)                                                                                \
   hipLaunchKernelGGL((scan_kernel<T, NN, RR>), dim3(grid), dim3(kScanThreads), 0, s, B, offs, E, u, xdbl, \
-                     z, ldz, W_dt, b_dt, A_log, D, out, ysave, ckpt, nck)
+                     z, ldz, W_dt, b_dt, A_log, D, out, ysave, ckpt, nck, ord)
   switch (N * 100 + R) {
     case 1604: TCL_SCAN(16, 4); break;
     case 1608: TCL_SCAN(16, 8); break;
@@ -793,11 +835,11 @@ template hipError_t launch_scan_chunked<uint16_t>(int, int, int, int, int, const
                                                   const float*, uint16_t*, hipStream_t);
 template hipError_t launch_scan<float>(int, int, int, int, const int*, const float*, const float*,
                                        const float*, int, const float*, const float*, const float*,
-                                       const float*, float*, hipStream_t, float*, float*, int);
+                                       const float*, float*, hipStream_t, float*, float*, int, const int*);
 template hipError_t launch_scan<uint16_t>(int, int, int, int, const int*, const uint16_t*,
                                           const float*, const uint16_t*, int, const float*,
                                           const float*, const float*, const float*, uint16_t*,
-                                          hipStream_t, uint16_t*, float*, int);
+                                          hipStream_t, uint16_t*, float*, int, const int*);
 
 namespace {
 

@@ -364,7 +364,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
     const float* __restrict__ b_dt, const float* __restrict__ A_log, const float* __restrict__ Dp,
     const float* __restrict__ ckpt, float* __restrict__ dv_out, float* __restrict__ du_out,
     float* __restrict__ dxz, float* __restrict__ dxdbl, float* __restrict__ dA_part,
-    float* __restrict__ dD_part, float* __restrict__ dbc_part, int Mmax, int TW) {
+    float* __restrict__ dD_part, float* __restrict__ dbc_part, int Mmax, int TW, const int* __restrict__ ord) {
   static_assert(N == 2 * kHalfN, "two lanes per channel, eight states each");
   constexpr int XW = R + 2 * N;
   constexpr int NH = kHalfN;
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(512, 2) void scan_bwd_kernel(
   // a window of TW tokens (a multiple of the checkpoint interval) at a time
   float* sX = smem;                       // [TW][XW] the window's rows
   float* sRed = smem + TW * XW;           // [TW][8 waves][2N] per-wavefront dB_t | dC_t
-  const int b = blockIdx.x;
+  const int b = ord ? ord[blockIdx.x] : (int)blockIdx.x;  // longest programs first when ordered
   const int tid = threadIdx.x;            // blockDim == 2E / gridDim.y: the program's channels in groups
   const int e = blockIdx.y * (blockDim.x >> 1) + (tid >> 1), hf = tid & 1, n0 = hf * NH;
   const int wave = tid >> 6, lane = tid & 63;
@@ -859,7 +859,7 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
                            const float* dyg, const float* W_dt, const float* b_dt,
                            const float* A_log, const float* D, const float* ckpt, float* dv, float* du,
                            float* dxz, float* dxdbl, float* dA_part, float* dD_part, float* dbc_part,
-                           hipStream_t s) {
+                           hipStream_t s, const int* ord) {
   if (N != 16 || E % 32 || E > 256 || B <= 0 || L <= 0) return hipErrorInvalidValue;
   // the program's tokens are staged in windows of TW (a multiple of the
   // checkpoint interval) within 64 KiB of LDS: a window's [dt_r | B | C]
@@ -876,7 +876,7 @@ hipError_t launch_scan_bwd(int B, int E, int L, int N, int R, const int* offs, c
 #define TCL_SB(RR)                                                                                       \
   hipLaunchKernelGGL((scan_bwd_kernel<16, RR, uint16_t>), dim3(B, groups), dim3(2 * E / groups), shm, s, \
                      offs, E, L, u, xdbl, xz, ysave, dyg, W_dt, b_dt, A_log, D, ckpt, dv, du, dxz, dxdbl,   \
-                     dA_part, dD_part, dbc_part, Mmax, TW)
+                     dA_part, dD_part, dbc_part, Mmax, TW, ord)
   switch (R) {
     case 4: TCL_SB(4); break;
     case 8: TCL_SB(8); break;

@@ -46,6 +46,7 @@ namespace {
 struct TrainPlan {
   size_t teacher_ws = 0, t_scores = 0, s_scores = 0, offs = 0;
   size_t prow = 0;  // per packed token: its row of the padded feature tensor
+  size_t ord = 0;   // the programs longest first
   struct Layer {
     size_t Hin, n, rstd, xz, u, xdbl, y, yg, ckpt;
     size_t p_Wout, p_Wdt, p_bdt, p_A, p_D, p_Wx, p_conv, p_Win, p_g;
@@ -76,6 +77,7 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
   P.t_scores = take((size_t)B * 4);
   P.s_scores = take((size_t)B * 4);
   P.offs = take((size_t)(B + 1) * 4);
+  P.ord = take((size_t)B * 4);
   P.prow = take((size_t)B * L * 4);
   P.cs = colsum_splits(Mmax);
   P.lh_blocks = loss_head_blocks(B);
@@ -385,7 +387,8 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   if (st != TCL_OK) return st;
 
   // 2. student forward, keeping activations
-  TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s));
+  const int* ord = L <= kOrderMaxL ? reinterpret_cast<const int*>(ws + P.ord) : nullptr;
+  TCL_LAUNCH(T, "offsets", launch_offsets(d_lengths, B, L, offs, s, reinterpret_cast<int*>(ws + P.ord)));
   TCL_LAUNCH(T, "packed_rows", launch_packed_rows(offs, B, L, reinterpret_cast<int*>(ws + P.prow), s));
   {
     GemmArgsBF16 g;
@@ -414,7 +417,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     TCL_LAUNCH(T, "gemm_x_proj", launch_gemm_bf16(gx, kBF16toF32, -1, s));
     TCL_LAUNCH(T, "scan", launch_scan<uint16_t>(B, E, N, R, offs, B16(Ly.u), F32(Ly.xdbl),
                                                 B16(Ly.xz) + E, 2 * E, W.W_dt, W.b_dt, W.A_log, W.D,
-                                                B16(Ly.yg), s, B16(Ly.y), F32(Ly.ckpt), L));
+                                                B16(Ly.yg), s, B16(Ly.y), F32(Ly.ckpt), L, ord));
     GemmArgsBF16 go;
     go.A = B16(Ly.yg); go.lda = E; go.W = W.W_out_h; go.ldw = E; go.C = Hout; go.ldc = d;
     go.R = F32(Ly.Hin); go.Mdev = Mdev; go.Mmax = Mmax; go.N = d; go.K = E;
@@ -530,7 +533,7 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
     TCL_LAUNCH(T, "scan_bwd", launch_scan_bwd(B, E, L, N, R, offs, B16(Ly.u), F32(Ly.xdbl), B16(Ly.xz),
                                               B16(Ly.y), F32(P.dyg), W.W_dt, W.b_dt, W.A_log, W.D,
                                               F32(Ly.ckpt), F32(P.dv), F32(P.du), F32(P.dxz),
-                                              F32(P.dxdbl), F32(Ly.p_A), F32(Ly.p_D), F32(P.dbc_part), s));
+                                              F32(P.dxdbl), F32(Ly.p_A), F32(Ly.p_D), F32(P.dbc_part), s, ord));
     {  // d dt_r = dv W_dt  -> columns [0, R) of dxdbl
       GemmArgs g;
       g.A = F32(P.dv); g.lda = E; g.W = W.W_dtT; g.ldw = E; g.C = F32(P.dxdbl); g.ldc = XW;
