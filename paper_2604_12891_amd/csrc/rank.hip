@@ -11,12 +11,16 @@
 //   scores in index order), maxDCG = the DCG of the ordering by rel.
 // The ranks are counted, not sorted: item i's rank is one plus the number of
 // items ahead of it, an O(B^2) pass that is cheap at tuning-round sizes and
-// needs no sort. Three launches:
-//   prep:   per item its score rank, and per set its relevance, gain
-//           2^rel - 1 and ideal-DCG term (gain over log2(1 + ideal rank));
-//   pairs:  a grid of (256 items i) x (256 items j) tiles; each thread
-//           accumulates its item's loss and gradient over one j tile;
+// needs no sort. Four launches:
+//   count:  a grid of (256 items i) x (j chunks); per item the chunk's
+//           items ahead of it by score and, per set, by relevance;
+//   prep:   per item its score rank (the chunks' counts summed), and per
+//           set its gain 2^rel - 1 and ideal-DCG term (gain over
+//           log2(1 + ideal rank));
+//   pairs:  a grid of (256 items i) x (j tiles); each thread accumulates
+//           its item's loss and gradient over one j tile;
 //   finish: sums the j-tile partials in a fixed order (deterministic).
+// The chunks and tiles are sized so that a few dozen cover the batch.
 // All fp32; maxDCG is summed identically by every block.
 #include "common.h"
 #include "kernels.h"
@@ -59,17 +63,21 @@ __device__ __forceinline__ float block_max(float v, float* red) { return -block_
 // relevance of a label given the set's min and max (all zero when equal)
 __device__ __forceinline__ float rel_of(float y, float lo, float inv_range) { return (y - lo) * inv_range; }
 
+// The j range is cut into chunks (counting) and tiles (pairs) sized so that
+// a few dozen of them cover the batch: at tuning-round sizes the O(B^2)
+// passes then spread over hundreds of workgroups instead of a handful.
+__host__ __device__ constexpr int rank_count_chunk(int B) {
+  const int c = ((B + 15) / 16 + 63) / 64 * 64;  // <= 16 chunks
+  return c < 64 ? 64 : (c > 4096 ? 4096 : c);
+}
+__host__ __device__ constexpr int rank_pair_tile(int B) {
+  const int t = ((B + 63) / 64 + 31) / 32 * 32;  // <= 64 tiles
+  return t < 32 ? 32 : (t > 2048 ? 2048 : t);
+}
+
+// every block: each set's min and max over the batch
 template <int NS>
-__global__ __launch_bounds__(kRT) void rank_prep_kernel(int B, const float* __restrict__ s,
-                                                        const float* __restrict__ l0,
-                                                        const float* __restrict__ l1,
-                                                        float* __restrict__ rel, float* __restrict__ gain,
-                                                        float* __restrict__ dcg, float* __restrict__ invD) {
-  __shared__ float red[kRT / 64];
-  __shared__ float ts[kRT], tr[NS][kRT];
-  const float* lab[2] = {l0, l1};
-  // every block computes each set's min and max over the whole batch
-  float lo[NS], ir[NS];
+__device__ __forceinline__ void label_range(int B, const float* const* lab, float* lo, float* ir, float* red) {
 #pragma unroll
   for (int k = 0; k < NS; ++k) {
     float mn = INFINITY, mx = -INFINITY;
@@ -81,48 +89,88 @@ __global__ __launch_bounds__(kRT) void rank_prep_kernel(int B, const float* __re
     const float hi = block_max(mx, red);
     ir[k] = hi > lo[k] ? 1.0f / (hi - lo[k]) : 0.0f;
   }
+}
+
+// grid (i blocks, j chunks of JC): per item i the number of items of the
+// chunk ahead of it by score and, per set, by relevance (partial counts
+// [chunk][1 + NS][B]); the first chunk's blocks also store rel.
+template <int NS>
+__global__ __launch_bounds__(kRT) void rank_count_kernel(int B, int JC, const float* __restrict__ s,
+                                                         const float* __restrict__ l0,
+                                                         const float* __restrict__ l1, float* __restrict__ rel,
+                                                         int* __restrict__ cnt) {
+  __shared__ float red[kRT / 64];
+  extern __shared__ float tj[];  // [1 + NS][JC]: the chunk's scores and relevances
+  const float* lab[2] = {l0, l1};
+  float lo[NS], ir[NS];
+  label_range<NS>(B, lab, lo, ir, red);
   const int i = blockIdx.x * kRT + threadIdx.x;
   const bool ok = i < B;
   const float si = ok ? s[i] : 0.f;
   float ri[NS];
 #pragma unroll
   for (int k = 0; k < NS; ++k) ri[k] = ok ? rel_of(lab[k][i], lo[k], ir[k]) : 0.f;
+  if (blockIdx.y == 0 && ok) {
+#pragma unroll
+    for (int k = 0; k < NS; ++k) rel[k * B + i] = ri[k];
+  }
+  const int j0 = blockIdx.y * JC;
+  const int n = min(JC, B - j0);
+  for (int jj = threadIdx.x; jj < n; jj += kRT) {
+    tj[jj] = s[j0 + jj];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) tj[(1 + k) * JC + jj] = rel_of(lab[k][j0 + jj], lo[k], ir[k]);
+  }
+  __syncthreads();
   int ahead = 0, iahead[NS];
 #pragma unroll
   for (int k = 0; k < NS; ++k) iahead[k] = 0;
-  for (int j0 = 0; j0 < B; j0 += kRT) {
-    __syncthreads();
-    const int j = j0 + threadIdx.x;
-    ts[threadIdx.x] = j < B ? s[j] : 0.f;
+  for (int jj = 0; jj < n; ++jj) {
+    const int jg = j0 + jj;
+    const float sj = tj[jj];
+    ahead += (sj > si || (sj == si && jg < i)) ? 1 : 0;
 #pragma unroll
-    for (int k = 0; k < NS; ++k) tr[k][threadIdx.x] = j < B ? rel_of(lab[k][j], lo[k], ir[k]) : 0.f;
-    __syncthreads();
-    const int n = min(kRT, B - j0);
-    for (int jj = 0; jj < n; ++jj) {
-      const int jg = j0 + jj;
-      const float sj = ts[jj];
-      ahead += (sj > si || (sj == si && jg < i)) ? 1 : 0;
-#pragma unroll
-      for (int k = 0; k < NS; ++k) {
-        const float rj = tr[k][jj];
-        iahead[k] += (rj > ri[k] || (rj == ri[k] && jg < i)) ? 1 : 0;
-      }
+    for (int k = 0; k < NS; ++k) {
+      const float rj = tj[(1 + k) * JC + jj];
+      iahead[k] += (rj > ri[k] || (rj == ri[k] && jg < i)) ? 1 : 0;
     }
   }
   if (!ok) return;
+  int* c = cnt + (int64_t)blockIdx.y * (1 + NS) * B + i;
+  c[0] = ahead;
+#pragma unroll
+  for (int k = 0; k < NS; ++k) c[(int64_t)(1 + k) * B] = iahead[k];
+}
+
+// per item: its score rank and, per set, its gain and ideal-DCG term from
+// the chunks' counts
+template <int NS>
+__global__ __launch_bounds__(kRT) void rank_prep_kernel(int B, int chunks, const int* __restrict__ cnt,
+                                                        const float* __restrict__ rel, float* __restrict__ gain,
+                                                        float* __restrict__ dcg, float* __restrict__ invD) {
+  const int i = blockIdx.x * kRT + threadIdx.x;
+  if (i >= B) return;
+  int ahead = 0, iahead[NS];
+#pragma unroll
+  for (int k = 0; k < NS; ++k) iahead[k] = 0;
+  for (int c = 0; c < chunks; ++c) {
+    const int* p = cnt + (int64_t)c * (1 + NS) * B + i;
+    ahead += p[0];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) iahead[k] += p[(int64_t)(1 + k) * B];
+  }
   invD[i] = 1.0f / __builtin_amdgcn_logf(2.0f + (float)ahead);  // rank = ahead + 1, D = log2(1 + rank)
 #pragma unroll
   for (int k = 0; k < NS; ++k) {
-    const float g = __builtin_amdgcn_exp2f(ri[k]) - 1.0f;
-    rel[k * B + i] = ri[k];
+    const float g = __builtin_amdgcn_exp2f(rel[k * B + i]) - 1.0f;
     gain[k * B + i] = g;
     dcg[k * B + i] = g / __builtin_amdgcn_logf(2.0f + (float)iahead[k]);
   }
 }
 
-// grid (i blocks, j tiles); part_ds [tiles][B], part_loss [tiles][i blocks][NS]
+// grid (i blocks, j tiles of JT); part_ds [tiles][B], part_loss [tiles][i blocks][NS]
 template <int NS>
-__global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, float w0, float w1,
+__global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, int JT, float sigma, float w0, float w1,
                                                         const float* __restrict__ w1_scale,
                                                         const float* __restrict__ s,
                                                         const float* __restrict__ rel,
@@ -132,7 +180,11 @@ __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, floa
                                                         float* __restrict__ part_ds,
                                                         float* __restrict__ part_loss) {
   __shared__ float red[kRT / 64];
-  __shared__ float ts[kRT], tD[kRT], tr[NS][kRT], tg[NS][kRT];
+  extern __shared__ float tj[];  // [2 + 2 NS][JT]: scores, 1/D, relevances, gains
+  float* ts = tj;
+  float* tD = tj + JT;
+  float* tr = tj + 2 * JT;            // [NS][JT]
+  float* tg = tj + (2 + NS) * JT;     // [NS][JT]
   float imax[NS];
 #pragma unroll
   for (int k = 0; k < NS; ++k) {
@@ -141,16 +193,16 @@ __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, floa
     const float mx = block_sum(acc, red);
     imax[k] = mx > 0.f ? 1.0f / mx : 0.f;
   }
-  const int j0 = blockIdx.y * kRT;
-  {
-    const int j = j0 + threadIdx.x;
-    const bool jok = j < B;
-    ts[threadIdx.x] = jok ? s[j] : 0.f;
-    tD[threadIdx.x] = jok ? invD[j] : 0.f;
+  const int j0 = blockIdx.y * JT;
+  const int nj = min(JT, B - j0);
+  for (int jj = threadIdx.x; jj < nj; jj += kRT) {
+    const int j = j0 + jj;
+    ts[jj] = s[j];
+    tD[jj] = invD[j];
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
-      tr[k][threadIdx.x] = jok ? rel[k * B + j] : 0.f;
-      tg[k][threadIdx.x] = jok ? gain[k * B + j] : 0.f;
+      tr[k * JT + jj] = rel[k * B + j];
+      tg[k * JT + jj] = gain[k * B + j];
     }
   }
   __syncthreads();
@@ -165,7 +217,7 @@ __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, floa
     loss[k] = 0.f;
     grad[k] = 0.f;
   }
-  const int n = ok ? min(kRT, B - j0) : 0;
+  const int n = ok ? nj : 0;
   for (int jj = 0; jj < n; ++jj) {
     const float x = sigma * (si - ts[jj]);
     const float dD = fabsf(Di - tD[jj]);
@@ -178,8 +230,8 @@ __global__ __launch_bounds__(kRT) void rank_pair_kernel(int B, float sigma, floa
     const float sp_neg = fmaxf(-x, 0.f) + lp;      // log(1 + e^-x)
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
-      const float rj = tr[k][jj];
-      const float w = fabsf(gi[k] - tg[k][jj]) * imax[k] * dD;
+      const float rj = tr[k * JT + jj];
+      const float w = fabsf(gi[k] - tg[k * JT + jj]) * imax[k] * dD;
       if (ri[k] > rj) {
         loss[k] = fmaf(w, sp_neg, loss[k]);
         grad[k] = fmaf(-w, sig_neg, grad[k]);
@@ -287,16 +339,21 @@ __global__ __launch_bounds__(kRT) void teacher_gate_kernel(int n, const float* _
 }  // namespace
 
 size_t rank_workspace_floats(int B, int nsets) {
-  const size_t tiles = (size_t)(B + kRT - 1) / kRT;
-  // rel, gain, dcg per set; invD; ds; part_ds [tiles][B]; part_loss [tiles][tiles][nsets]
-  return (size_t)3 * nsets * B + B + B + tiles * B + tiles * tiles * nsets;
+  const size_t iblocks = (size_t)(B + kRT - 1) / kRT;
+  const size_t tiles = (size_t)(B + rank_pair_tile(B) - 1) / rank_pair_tile(B);
+  const size_t chunks = (size_t)(B + rank_count_chunk(B) - 1) / rank_count_chunk(B);
+  // rel, gain, dcg per set; invD; ds; part_ds [tiles][B]; part_loss
+  // [tiles][iblocks][nsets]; counts [chunks][1 + nsets][B] (ints)
+  return (size_t)3 * nsets * B + B + B + tiles * B + tiles * iblocks * nsets + chunks * (1 + nsets) * B;
 }
 
 hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, const float* l1, float sigma,
                              float w0, float w1, float* ws, float* ds, float* out, hipStream_t st,
                              const float* key, const float* w1_scale) {
   if (B <= 0 || (nsets != 1 && nsets != 2) || (nsets == 2 && !l1)) return hipErrorInvalidValue;
-  const int tiles = (B + kRT - 1) / kRT;
+  const int iblocks = (B + kRT - 1) / kRT;
+  const int JT = rank_pair_tile(B), JC = rank_count_chunk(B);
+  const int tiles = (B + JT - 1) / JT, chunks = (B + JC - 1) / JC;
   float* rel = ws;
   float* gain = rel + (size_t)nsets * B;
   float* dcg = gain + (size_t)nsets * B;
@@ -304,21 +361,25 @@ hipError_t launch_lambdarank(int B, int nsets, const float* s, const float* l0, 
   float* dsw = invD + B;
   float* part_ds = dsw + B;
   float* part_loss = part_ds + (size_t)tiles * B;
+  int* cnt = reinterpret_cast<int*>(part_loss + (size_t)tiles * iblocks * nsets);
   float* dsout = ds ? ds : dsw;
   const float* rk = key ? key : s;  // what the score ranks D_i are counted from
-  if (nsets == 1) {
-    hipLaunchKernelGGL(rank_prep_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, rk, l0, l0, rel, gain, dcg, invD);
-    hipLaunchKernelGGL(rank_pair_kernel<1>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, w1_scale, s,
-                       rel, gain, dcg, invD, part_ds, part_loss);
-    hipLaunchKernelGGL(rank_finish_kernel<1>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, w1_scale,
-                       part_ds, part_loss, dsout, out);
-  } else {
-    hipLaunchKernelGGL(rank_prep_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, rk, l0, l1, rel, gain, dcg, invD);
-    hipLaunchKernelGGL(rank_pair_kernel<2>, dim3(tiles, tiles), dim3(kRT), 0, st, B, sigma, w0, w1, w1_scale, s,
-                       rel, gain, dcg, invD, part_ds, part_loss);
-    hipLaunchKernelGGL(rank_finish_kernel<2>, dim3(tiles), dim3(kRT), 0, st, B, tiles, tiles, w0, w1, w1_scale,
-                       part_ds, part_loss, dsout, out);
-  }
+  const size_t cnt_lds = (size_t)(1 + nsets) * JC * sizeof(float);
+  const size_t pair_lds = (size_t)(2 + 2 * nsets) * JT * sizeof(float);
+#define TCL_RANK(NS, L1)                                                                                  \
+  do {                                                                                                    \
+    hipLaunchKernelGGL(rank_count_kernel<NS>, dim3(iblocks, chunks), dim3(kRT), cnt_lds, st, B, JC, rk, l0, \
+                       L1, rel, cnt);                                                                     \
+    hipLaunchKernelGGL(rank_prep_kernel<NS>, dim3(iblocks), dim3(kRT), 0, st, B, chunks, cnt, rel, gain,    \
+                       dcg, invD);                                                                        \
+    hipLaunchKernelGGL(rank_pair_kernel<NS>, dim3(iblocks, tiles), dim3(kRT), pair_lds, st, B, JT, sigma,  \
+                       w0, w1, w1_scale, s, rel, gain, dcg, invD, part_ds, part_loss);                    \
+    hipLaunchKernelGGL(rank_finish_kernel<NS>, dim3(iblocks), dim3(kRT), 0, st, B, tiles, iblocks, w0, w1, \
+                       w1_scale, part_ds, part_loss, dsout, out);                                         \
+  } while (0)
+  if (nsets == 1) TCL_RANK(1, l0);
+  else TCL_RANK(2, l1);
+#undef TCL_RANK
   return hipGetLastError();
 }
 
