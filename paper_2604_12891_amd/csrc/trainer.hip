@@ -61,16 +61,6 @@ struct TrainPlan {
   size_t total = 0;
 };
 
-// The frozen teacher's forward runs as two half batches on the teacher
-// model's two streams from this many programs on (its launches are small
-// and latency bound; the halves' kernels fill each other's idle CUs).
-constexpr int kTeacherSplitMinB = 512;
-
-bool teacher_split(const tcl_model* Tm, int B, int L) {
-  return Tm->score_streams == 2 && Tm->aux[0] && Tm->aux[1] && Tm->ev[0] && Tm->ev[1] && Tm->ev[2] &&
-         B >= kTeacherSplitMinB && ((int64_t)(B / 2) * L * Tm->cfg.F * 4) % 16 == 0;
-}
-
 TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
   const tcl_config& c = tr->student->cfg;
   TrainPlan P;
@@ -83,10 +73,7 @@ TrainPlan plan_step(const tcl_trainer* tr, int B, int L) {
     o = align256(o + bytes);
     return at;
   };
-  P.teacher_ws = take(teacher_split(tr->teacher, B, L)
-                          ? align256(score_plan(tr->teacher->cfg, B / 2, L).total) +
-                                score_plan(tr->teacher->cfg, B - B / 2, L).total
-                          : score_plan(tr->teacher->cfg, B, L).total);
+  P.teacher_ws = take(score_plan(tr->teacher->cfg, B, L).total);
   P.t_scores = take((size_t)B * 4);
   P.s_scores = take((size_t)B * 4);
   P.offs = take((size_t)(B + 1) * 4);
@@ -379,32 +366,19 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   // forwards run side by side until the loss needs the teacher's scores
   tcl_model* Tm = tr->teacher;
   const bool fork = Tm->aux[0] && Tm->ev[0] && Tm->ev[1];
-  const bool halves = teacher_split(Tm, B, L);
   if (fork) {
     TCL_HIP(hipEventRecord(Tm->ev[0], s));
     TCL_HIP(hipStreamWaitEvent(Tm->aux[0], Tm->ev[0], 0));
-    if (halves) TCL_HIP(hipStreamWaitEvent(Tm->aux[1], Tm->ev[0], 0));
   }
   // the teacher's parts (front, blocks, tail) are enqueued between the
   // student's layers, so that neither forward waits for the host to finish
-  // enqueueing the other; with two halves, their parts alternate
+  // enqueueing the other
   const int t_parts = Tm->cfg.n_layers + 2;
-  const int th = B / 2;
-  const size_t t_off2 = align256(score_plan(Tm->cfg, th, L).total);
   int t_next = 0;
   auto teacher_parts = [&](int upto) -> tcl_status {
     for (; t_next < upto && t_next < t_parts; ++t_next) {
-      if (!halves) {
-        const tcl_status ts = run_score_part(Tm, B, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws,
-                                             fork ? Tm->aux[0] : s, t_next);
-        if (ts != TCL_OK) return ts;
-        continue;
-      }
-      tcl_status ts = run_score_part(Tm, th, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws,
-                                     Tm->aux[0], t_next);
-      if (ts != TCL_OK) return ts;
-      ts = run_score_part(Tm, B - th, L, d_feats + (int64_t)th * L * Tm->cfg.F, d_lengths + th,
-                          F32(P.t_scores) + th, ws + P.teacher_ws + t_off2, Tm->aux[1], t_next);
+      const tcl_status ts = run_score_part(Tm, B, L, d_feats, d_lengths, F32(P.t_scores), ws + P.teacher_ws,
+                                           fork ? Tm->aux[0] : s, t_next);
       if (ts != TCL_OK) return ts;
     }
     return TCL_OK;
@@ -452,14 +426,12 @@ tcl_status distill_step(tcl_trainer* tr, int32_t B, int32_t L, const float* d_fe
   st = teacher_parts(t_parts);
   if (st != TCL_OK) return st;
   if (fork) TCL_HIP(hipEventRecord(Tm->ev[1], Tm->aux[0]));
-  if (halves) TCL_HIP(hipEventRecord(Tm->ev[2], Tm->aux[1]));
   TCL_LAUNCH(T, "tail", launch_tail_f32(B, L, d, h, offs, d_lengths, F32(P.H_last), S->g_f, c.final_norm,
                                         c.norm_eps, S->W1T, S->b1, S->W2, S->b2, F32(P.s_scores), s,
                                         F32(P.pooled), F32(P.a1)));
 
   // 3. loss, head, pool and final norm (the teacher's scores are needed from here)
   if (fork) TCL_HIP(hipStreamWaitEvent(s, Tm->ev[1], 0));
-  if (halves) TCL_HIP(hipStreamWaitEvent(s, Tm->ev[2], 0));
   if (kd) {
     // beta L(s; labels) + (1 - beta) phi L(s; teacher): dL/ds and the loss
     // the gate phi is a host value, or a device value (e.g. an entry of
