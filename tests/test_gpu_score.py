@@ -163,6 +163,29 @@ def test_edge_shapes(case):
     assert_scores_match(g, oracle_scores(blob, X, lengths, shape), "f32", case)
 
 
+@pytest.mark.parametrize("L", [4096, 4097])
+def test_long_padding_around_the_ordering_limit(L):
+    """The offsets kernel lists programs longest first (a counting sort over
+    L + 1 length buckets) for L up to 4096, and the sequential scan hands
+    them out in that order; above it the scan takes them in index order.
+    Enough programs for the sequential scan (>= 1024 wavefronts of 64
+    channels), padded to L; the oracle scores the same programs padded only
+    to their longest (a program's score reads its own tokens alone)."""
+    shape = wl.ModelShape(F=8, d_model=64, d_inner=512, dt_rank=4, n_layers=2, head_hidden=64)
+    rng = np.random.default_rng(L)
+    blob = wl.init_params(shape, rng, perturb=True)
+    B = 130
+    X, lengths = wl.make_inputs(B, L, shape.F, 1, 20, rng)
+    for b, n in ((5, 300), (129, 299)):
+        lengths[b] = n
+        X[b, :n] = np.log1p(rng.lognormal(0.0, 1.0, size=(n, shape.F))).astype(np.float32)
+    print(f"tcl_score B={B} L={L} (longest program 300 tokens)", flush=True)
+    g = _score(_model(shape, blob), X, lengths)
+    Lmax = int(lengths.max())
+    assert_scores_match(g, oracle_scores(blob, np.ascontiguousarray(X[:, :Lmax]), lengths, shape), "f32",
+                        f"L={L}")
+
+
 def test_padding_never_read_and_invalid_lengths():
     """Rows past each length hold NaN and must not be read; programs with a
     length outside [1, L] score NaN without disturbing the others."""
