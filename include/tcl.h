@@ -468,6 +468,19 @@ TCL_API const char* tcl_last_error(void);
  * every [rows, C] activation (row-major, leading dimension C unless given).
  * ------------------------------------------------------------------- */
 
+/* The packing of a batch's programs into token rows (every scoring and
+ * training call starts with it): d_offs[b] = sum over b' < b of valid(len_b'),
+ * d_offs[B] = the packed token count, where valid(len) = len for
+ * 1 <= len <= L and 0 otherwise (such a program packs no rows). With d_ord
+ * non-NULL and L <= 4096 it also writes d_ord [B]: the programs by
+ * decreasing valid length, a permutation of 0..B-1 (the order among equal
+ * lengths is unspecified); the scans hand programs out in that order. With
+ * L > 4096 d_ord is left as it is. d_lengths [B], d_offs [B+1] and d_ord are
+ * int32 device memory owned by the caller; B <= 0, L <= 0 or a NULL
+ * d_lengths / d_offs return TCL_ERR_INVALID_ARG. */
+TCL_API tcl_status tcl_test_offsets(int32_t B, int32_t L, const int32_t* d_lengths, int32_t* d_offs,
+                                    int32_t* d_ord, void* stream);
+
 /* fp32 MFMA GEMM used by the model's projections, K % 4 == 0:
  *   epilogue 0: C[M,N] = A W^T (+ bias[N] if d_bias)
  *   epilogue 1: C += A W^T            (the residual epilogue, C read in place)

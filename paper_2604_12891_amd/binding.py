@@ -98,6 +98,7 @@ _SIGS = {
                                        _vp, _vp]),
     "tcl_test_xproj_conv_bf16": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                         _vp]),
+    "tcl_test_offsets": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp]),
     "tcl_test_scan_f32": (_i32, [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp,
                                  _vp, _vp, _vp]),
 }
@@ -555,6 +556,16 @@ def xproj_conv_bf16(offs, x, w, b, W, rows, E, ldx=None, stream=None):
                                          W.data_ptr(), tpos.data_ptr(), u.data_ptr(), xdbl.data_ptr(),
                                          _stream(stream)))
     return u, xdbl
+
+
+def offsets(lengths, L, ord=None, stream=None):
+    """tcl_test_offsets: returns the device int32 offsets [B+1]; ord (a
+    device int32 [B] tensor, optional) receives the longest-first order."""
+    import torch
+    B = lengths.numel()
+    offs = torch.empty(B + 1, dtype=torch.int32, device=lengths.device)
+    check(lib().tcl_test_offsets(B, L, lengths.data_ptr(), offs.data_ptr(), _ptr(ord), _stream(stream)))
+    return offs
 
 
 def scan_f32(offs, u, xdbl, z, W_dt, b_dt, A_log, D, out, ldz=None, stream=None, chunks=0):

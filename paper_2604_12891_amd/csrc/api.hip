@@ -1069,6 +1069,14 @@ TCL_API tcl_status tcl_test_gemm_bf16(int32_t kind, int32_t tile, int32_t M, int
   return TCL_OK;
 }
 
+TCL_API tcl_status tcl_test_offsets(int32_t B, int32_t L, const int32_t* d_lengths, int32_t* d_offs,
+                                    int32_t* d_ord, void* stream) {
+  if (B <= 0 || L <= 0) return fail(TCL_ERR_INVALID_ARG, "B and L must be positive (B=%d L=%d)", B, L);
+  if (!d_lengths || !d_offs) return fail(TCL_ERR_INVALID_ARG, "NULL device pointer");
+  TCL_HIP(launch_offsets(d_lengths, B, L, d_offs, static_cast<hipStream_t>(stream), d_ord));
+  return TCL_OK;
+}
+
 TCL_API tcl_status tcl_test_conv_silu_f32(int32_t B, int32_t E, int32_t K, const int32_t* d_offs,
                                           const float* d_x, int32_t ldx, const float* d_w,
                                           const float* d_b, float* d_u, void* stream) {

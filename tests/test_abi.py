@@ -148,6 +148,15 @@ def test_bf16_gemm_entry_rejects_bad_arguments(lib):
     assert call(C=fake + 4) == -1     # alignment
 
 
+def test_offsets_entry_rejects_bad_arguments(lib):
+    """Argument checks run on the host, before any device work."""
+    fake = 1 << 20  # never dereferenced
+    assert lib.tcl_test_offsets(0, 25, fake, fake, None, None) == -1
+    assert lib.tcl_test_offsets(4, 0, fake, fake, None, None) == -1
+    assert lib.tcl_test_offsets(4, 25, None, fake, None, None) == -1
+    assert lib.tcl_test_offsets(4, 25, fake, None, fake, None) == -1
+
+
 @pytest.mark.parametrize("shape", [wl.TINY, wl.PAPER_CPU])
 def test_lateral_param_count_matches_oracle_layout(lib, shape):
     from oracle import progressive as op

@@ -183,6 +183,37 @@ def test_gemm_bf16(M, N, K, bias):
     assert np.all(err <= bound + 1e-30), float(np.max(err / (bound + 1e-30)))
 
 
+@pytest.mark.parametrize("B,L", [(1, 25), (37, 25), (4096, 25), (32768, 25), (40001, 4096), (5000, 4097),
+                                 (1000, 1)])
+def test_offsets_and_longest_first_order(B, L):
+    """Index work, bit-exact: the packed offsets are the prefix sums of the
+    valid lengths (a length outside [1, L] packs nothing); for L <= 4096 the
+    order is a permutation of the programs by non-increasing valid length
+    (equal lengths may come in any order), above that it is not written.
+    Also with the lengths at a 4-byte offset (the kernel's scalar path)."""
+    print(f"offsets B={B} L={L}", flush=True)
+    rng = np.random.default_rng(B + L)
+    lengths = rng.integers(1, L + 1, size=B + 1).astype(np.int32)
+    if B >= 8:
+        bad = rng.choice(B, size=3, replace=False)
+        lengths[bad] = (0, -3, L + 1)
+    for shift in (0, 1):
+        ln = lengths[shift:shift + B]
+        Ld = torch.from_numpy(lengths).cuda()[shift:shift + B]
+        ordd = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+        offs = tb.offsets(Ld, L, ord=ordd)
+        torch.cuda.synchronize()
+        valid = np.where((ln >= 1) & (ln <= L), ln, 0).astype(np.int64)
+        assert np.array_equal(offs.cpu().numpy(), np.concatenate([[0], np.cumsum(valid)])), (B, L, shift)
+        o = ordd.cpu().numpy()
+        if L <= 4096:
+            assert np.array_equal(np.sort(o), np.arange(B)), "not a permutation"
+            v = valid[o]
+            assert np.all(v[:-1] >= v[1:]), "not longest first"
+        else:
+            assert np.all(o == -7), "the order was written above the limit"
+
+
 def _bf16_w(N, K, rng):
     """W [N, round_up(K, 8)] bf16-exact, zero-padded in K as the kernels expect."""
     Kw = (K + 7) // 8 * 8
