@@ -195,18 +195,34 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   GemmArgs gi;
   gi.A = H; gi.lda = d; gi.W = W.W_in_fold; gi.ldw = d; gi.C = xz; gi.ldc = 2 * E;
   gi.Mdev = offs + B; gi.Mmax = Mmax; gi.N = 2 * E; gi.K = d; gi.eps = c.norm_eps;
-  if (W.W_in_h2 && W.in_h2_ok && gemm_f16s_supports(gi, kRowNorm))
-    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), launch_gemm_f16s(gi, W.W_in_h2, (d + 7) & ~7, kRowNorm, s));
-  else
-    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), model_gemm(m, gi, W.W_in_s, d, kRowNorm, s));
   GemmArgs gx;
   gx.A = u; gx.lda = E; gx.W = W.W_x; gx.ldw = E; gx.C = xdbl; gx.ldc = XW;
   gx.Mdev = offs + B; gx.Mmax = Mmax; gx.N = XW; gx.K = E;
   ConvIn cv;
   cv.x = xz; cv.ldx = 2 * E; cv.w = W.conv_w; cv.b = W.conv_b; cv.tpos = tpos; cv.u = u;
-  if (m->split && W.W_x_s && gemm_split_conv_supports(gx, cv, c.d_conv)) {
+  const bool f16_in = W.W_in_h2 && W.in_h2_ok && gemm_f16s_supports(gi, kRowNorm);
+  const bool fused = m->split && W.W_x_s && gemm_split_conv_supports(gx, cv, c.d_conv);
+  // with both on the split path, in_proj writes x channel-blocked ([E / 64]
+  // blocks of [Mmax][64]) and z after it ([Mmax][E]), so that the conv reads
+  // each chunk's rows contiguously
+  GemmArgs gib = gi;
+  gib.xblk_rows = Mmax; gib.xblk_cols = E;
+  ConvIn cvb = cv;
+  cvb.xblk_rows = Mmax;
+  const bool blk = f16_in && fused && gemm_f16s_supports(gib, kRowNorm | kXBlk) &&
+                   gemm_split_conv_supports(gx, cvb, c.d_conv);
+  const float* z = blk ? xz + (int64_t)Mmax * E : xz + E;
+  const int ldz = blk ? E : 2 * E;
+  if (blk)
+    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(),
+               launch_gemm_f16s(gib, W.W_in_h2, (d + 7) & ~7, kRowNorm | kXBlk, s));
+  else if (f16_in)
+    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), launch_gemm_f16s(gi, W.W_in_h2, (d + 7) & ~7, kRowNorm, s));
+  else
+    TCL_LAUNCH(T, (tag + "gemm_in_proj").c_str(), model_gemm(m, gi, W.W_in_s, d, kRowNorm, s));
+  if (fused) {
     // the conv + SiLU computed in front of x_proj, u stored on the way
-    TCL_LAUNCH(T, (tag + "gemm_x_proj_conv").c_str(), launch_gemm_split_conv(gx, cv, W.W_x_s, E, s));
+    TCL_LAUNCH(T, (tag + "gemm_x_proj_conv").c_str(), launch_gemm_split_conv(gx, blk ? cvb : cv, W.W_x_s, E, s));
   } else {
     TCL_LAUNCH(T, (tag + "conv_silu").c_str(),
                launch_conv_silu<float>(B, E, c.d_conv, offs, xz, 2 * E, W.conv_w, W.conv_b, u, s));
@@ -214,10 +230,10 @@ tcl_status enqueue_block_f32(tcl_model* m, Timing& T, const std::string& tag, in
   }
   if (chunks > 0)
     TCL_LAUNCH(T, (tag + "scan_chunked").c_str(),
-               launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, xz + E, 2 * E, W.W_dt, W.b_dt,
+               launch_scan_chunked<float>(B, E, N, R, chunks, offs, u, xdbl, z, ldz, W.W_dt, W.b_dt,
                                           W.A_log, W.D, u, s));
   else
-    TCL_LAUNCH(T, (tag + "scan").c_str(), launch_scan<float>(B, E, N, R, offs, u, xdbl, xz + E, 2 * E, W.W_dt,
+    TCL_LAUNCH(T, (tag + "scan").c_str(), launch_scan<float>(B, E, N, R, offs, u, xdbl, z, ldz, W.W_dt,
                                                              W.b_dt, W.A_log, W.D, u, s, nullptr, nullptr, 0,
                                                              ord));
   GemmArgs go;

@@ -251,14 +251,32 @@ __global__ __launch_bounds__(kNT, 2) void gemm_f16s_kernel(GemmArgs p, const uin
     const int col = n0 + li;
     const bool cok = col < p.N;
     const float bias = ((FL & kBias) != 0) ? p.bias[cok ? col : 0] : 0.f;
+    // the block's rows: row-major with leading dimension ldc, or (kXBlk) in
+    // its channel block (64 floats a row) or in the packed rest
+    __amdgpu_buffer_rsrc_t bres = cres;
+    int64_t bld = p.ldc;
+    int bcol = col;
+    if constexpr ((FL & kXBlk) != 0) {
+      const int rows = min(kBM, M - row0);
+      if (n0 < p.xblk_cols) {
+        bres = make_rsrc(p.C + ((int64_t)(n0 / 64) * p.xblk_rows + row0) * 64, (uint32_t)(rows * 64 * 4));
+        bld = 64;
+        bcol = col % 64;
+      } else {
+        const int nz = p.N - p.xblk_cols;
+        bres = make_rsrc(p.C + (int64_t)p.xblk_cols * p.xblk_rows + (int64_t)row0 * nz, (uint32_t)(rows * nz * 4));
+        bld = nz;
+        bcol = col - p.xblk_cols;
+      }
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int rl = 8 * (r >> 2) + 4 * lg + (r & 3);
       float v = fmaf(ax[r], kLowInv, am[r]) * sF[wave][rl] + bias;
       if (p.relu) v = fmaxf(v, 0.f);
-      // rows past M fall outside cres
-      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * p.ldc + col) * 4) : kOutOfRange;
-      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), cres, off, 0, 0);
+      // rows past M fall outside the resource
+      const uint32_t off = cok ? (uint32_t)(((wave * 32 + rl) * bld + bcol) * 4) : kOutOfRange;
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), bres, off, 0, 0);
     }
   }
 }
@@ -567,7 +585,10 @@ hipError_t launch_f16acc(const GemmArgs& a, const uint16_t* Wh, int ldwh, hipStr
 bool gemm_f16s_supports(const GemmArgs& a, int flags) {
   const int ks = (a.K + 15) / 16;
   const bool kfit = ks == 4 || ks == 8 || ks == 11 || ks == 12 || ks == 16;
-  const bool fl = flags == kRowNorm || flags == (kBias | kGather) || flags == kBias || flags == 0;
+  const bool fl = flags == kRowNorm || flags == (kBias | kGather) || flags == kBias || flags == 0 ||
+                  (flags == (kRowNorm | kXBlk) && a.xblk_cols > 0 && a.xblk_cols % 64 == 0 &&
+                   a.xblk_cols < a.N && a.xblk_rows >= a.Mmax && (int64_t)kBM * 64 * 4 < (1ll << 31) &&
+                   (int64_t)kBM * (a.N - a.xblk_cols) * 4 < (1ll << 31) && reinterpret_cast<uintptr_t>(a.C) % 16 == 0);
   return kfit && fl && a.K % 4 == 0 && a.lda % 4 == 0 && reinterpret_cast<uintptr_t>(a.A) % 16 == 0 &&
          // byte offsets of the buffer resources stay below 2^31
          (int64_t)2 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31) && (int64_t)kBM * a.ldc * 4 < (1ll << 31);
@@ -579,6 +600,7 @@ hipError_t launch_gemm_f16s(const GemmArgs& a, const uint16_t* Wh, int ldwh, int
     case 0: return launch_f16s<0>(a, Wh, ldwh, s);
     case kBias: return launch_f16s<kBias>(a, Wh, ldwh, s);
     case kRowNorm: return launch_f16s<kRowNorm>(a, Wh, ldwh, s);
+    case kRowNorm | kXBlk: return launch_f16s<kRowNorm | kXBlk>(a, Wh, ldwh, s);
     case kBias | kGather: return launch_f16s<kBias | kGather>(a, Wh, ldwh, s);
     default: return hipErrorInvalidValue;
   }

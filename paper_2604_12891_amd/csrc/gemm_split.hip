@@ -818,7 +818,7 @@ __device__ __forceinline__ uint32_t opaque_v(uint32_t v) {
   return v;
 }
 
-template <int KCH>
+template <int KCH, bool XB>
 __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmArgs p, ConvIn cv, const uint16_t* Ws,
                                                                           int ldws) {
   constexpr int NS = 4;               // 16-k MFMA steps per chunk
@@ -861,7 +861,9 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
   // the first or past the last reads zero through the resource
   const int xr0 = max(row0 - 3, 0);
   const int xrows = min(M, row0 + BM) - xr0;
-  const __amdgpu_buffer_rsrc_t xres = make_rsrc(cv.x + (int64_t)xr0 * cv.ldx, (uint32_t)(xrows * cv.ldx * 4));
+  // (XB: x channel-blocked, each chunk's rows contiguous at 256 bytes a row)
+  const __amdgpu_buffer_rsrc_t xres =
+      make_rsrc(cv.x + (int64_t)xr0 * (XB ? 64 : cv.ldx), (uint32_t)(xrows * (XB ? 64 : cv.ldx) * 4));
   const __amdgpu_buffer_rsrc_t ures = make_rsrc(cv.u + (int64_t)row0 * E, (uint32_t)(min(BM, M - row0) * E * 4));
   const __amdgpu_buffer_rsrc_t cwres = make_rsrc(cv.w, (uint32_t)(E * 4 * 4));
   const __amdgpu_buffer_rsrc_t cbres = make_rsrc(cv.b, (uint32_t)(E * 4));
@@ -872,12 +874,15 @@ __global__ __launch_bounds__(kWaves * 64, 2) void gemm_split32conv_kernel(GemmAr
   uint32_t cb;
   auto load_chunk = [&](int c) {
     const uint32_t e = c * CW + lane;
-    const uint32_t ve = opaque_v(e * 4), ld = opaque_s(ldx4);
+    const uint32_t ve = opaque_v(e * 4);
+    const uint32_t ld = opaque_s(XB ? 256u : ldx4), vx = XB ? opaque_v((uint32_t)lane * 4) : ve;
+    const __amdgpu_buffer_rsrc_t xr =
+        XB ? make_rsrc(cv.x + ((int64_t)c * cv.xblk_rows + xr0) * 64, (uint32_t)(xrows * 64 * 4)) : xres;
 #pragma unroll
     for (int i = 0; i < XR; ++i) {
       const int row = wb - 3 + i;
-      const uint32_t off = row >= 0 ? (uint32_t)(row - xr0) * ld + ve : kOutOfRange;
-      xw[i] = __builtin_amdgcn_raw_buffer_load_b32(xres, off, 0, 0);
+      const uint32_t off = row >= 0 ? (uint32_t)(row - xr0) * ld + vx : kOutOfRange;
+      xw[i] = __builtin_amdgcn_raw_buffer_load_b32(xr, off, 0, 0);
     }
     cw = __builtin_amdgcn_raw_buffer_load_b128(cwres, ve * 4, 0, 0);
     cb = __builtin_amdgcn_raw_buffer_load_b32(cbres, ve, 0, 0);
@@ -1183,10 +1188,13 @@ hipError_t launch_gemm_split(const GemmArgs& a, const uint16_t* Ws, int ldws, in
 
 bool gemm_split_conv_supports(const GemmArgs& a, const ConvIn& cv, int d_conv) {
   const auto a16 = [](const void* q) { return reinterpret_cast<uintptr_t>(q) % 16 == 0; };
+  const bool xin = cv.xblk_rows > 0 ? cv.xblk_rows >= a.Mmax
+                                    : cv.ldx % 4 == 0 && cv.ldx >= a.K &&
+                                          (int64_t)(kWaves * 32 + 3) * cv.ldx * 4 < (1ll << 31);
   return d_conv == 4 && !a.relu && a.K % 64 == 0 && a.K >= 64 && a.K <= 512 && a.N >= 1 && a.N <= 64 && cv.x && cv.w &&
-         cv.b && cv.tpos && cv.u && a16(cv.x) && a16(cv.w) && a16(cv.u) && cv.ldx % 4 == 0 && cv.ldx >= a.K &&
+         cv.b && cv.tpos && cv.u && a16(cv.x) && a16(cv.w) && a16(cv.u) && xin &&
          // byte offsets of the buffer resources stay below 2^31
-         (int64_t)(kWaves * 32 + 3) * cv.ldx * 4 < (1ll << 31) && (int64_t)kWaves * 32 * a.K * 4 < (1ll << 31) && (int64_t)kWaves * 32 * a.ldc * 4 < (1ll << 31) &&
+         (int64_t)kWaves * 32 * a.K * 4 < (1ll << 31) && (int64_t)kWaves * 32 * a.ldc * 4 < (1ll << 31) &&
          (int64_t)3 * a.N * ((a.K + 7) & ~7) * 2 < (1ll << 31);
 }
 
@@ -1194,8 +1202,11 @@ hipError_t launch_gemm_split_conv(const GemmArgs& a, const ConvIn& cv, const uin
   if (!gemm_split_conv_supports(a, cv, 4)) return hipErrorInvalidValue;
   const int grid = (a.Mmax + kWaves * 32 - 1) / (kWaves * 32);
   if (grid <= 0) return hipSuccess;
-#define TCL_SPLITCONV(KCH) \
-  hipLaunchKernelGGL((gemm_split32conv_kernel<KCH>), dim3(grid), dim3(kWaves * 64), 0, s, a, cv, Ws, ldws)
+#define TCL_SPLITCONV(KCH)                                                                                    \
+  if (cv.xblk_rows > 0)                                                                                     \
+    hipLaunchKernelGGL((gemm_split32conv_kernel<KCH, true>), dim3(grid), dim3(kWaves * 64), 0, s, a, cv, Ws, ldws); \
+  else                                                                                                      \
+    hipLaunchKernelGGL((gemm_split32conv_kernel<KCH, false>), dim3(grid), dim3(kWaves * 64), 0, s, a, cv, Ws, ldws)
   switch (a.K / 64) {
     case 1: TCL_SPLITCONV(1); break;
     case 2: TCL_SPLITCONV(2); break;

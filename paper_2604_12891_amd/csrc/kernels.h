@@ -15,6 +15,8 @@ enum GemmFlags : int {
   kResid = 2,     // C += result (residual add, C read before write)
   kRowNorm = 4,   // multiply row r by (mean_k A[r,k]^2 + eps)^-1/2 (RMSNorm)
   kGather = 8,    // A row of packed token r is row b*L + t of the padded input
+  kXBlk = 16,     // the first xblk_cols columns of C channel-blocked, the rest
+                  // packed after them (GemmArgs::xblk_rows; in_proj on the split path)
 };
 
 struct GemmArgs {
@@ -35,6 +37,11 @@ struct GemmArgs {
   int relu = 0;               // nonzero: C = max(result, 0) (after bias and residual)
   uint8_t* tpos = nullptr;    // gather on the split path: also write each packed row's position
                               // in its program, clamped to 255 (launch_token_pos's array)
+  // kXBlk: C holds [xblk_cols / 64 blocks][xblk_rows][64] (column c of row r
+  // at ((c / 64) * xblk_rows + r) * 64 + c % 64), then the other N - xblk_cols
+  // columns as [xblk_rows][N - xblk_cols]; ldc is not used
+  int64_t xblk_rows = 0;
+  int xblk_cols = 0;
 };
 
 // Tile shapes (rows x columns of C per workgroup, 4 or 8 wavefronts, K staged
@@ -116,6 +123,9 @@ struct ConvIn {
   const float* b = nullptr;   // [K]
   const uint8_t* tpos = nullptr;
   float* u = nullptr;         // [rows, K]
+  // > 0: x is channel-blocked, [K / 64][xblk_rows][64] (in_proj's kXBlk
+  // output; ldx is not used), so that a chunk's rows are contiguous
+  int64_t xblk_rows = 0;
 };
 bool gemm_split_conv_supports(const GemmArgs& a, const ConvIn& cv, int d_conv);
 
